@@ -1,0 +1,131 @@
+"""Pure-Python loop versions of the paper's definitions, for tiny inputs.
+
+These pin the float64 oracle: each function is written independently of
+``oracle/`` (plain loops over Python floats, the ``math`` module only), so a
+dropped term, wrong sign or transposed operand in either one shows up as a
+mismatch.
+"""
+import math
+
+
+def gelu(x):
+    return 0.5 * x * (1.0 + math.erf(x / math.sqrt(2.0)))
+
+
+def score(K, V, W1, b1, w2, b2):
+    T, d = len(K), len(K[0])
+    out = []
+    for j in range(T):
+        x = list(K[j]) + list(V[j])
+        acc = float(b2)
+        for a in range(len(W1)):
+            pre = float(b1[a])
+            for c in range(2 * d):
+                pre += float(W1[a][c]) * float(x[c])
+            acc += float(w2[a]) * gelu(pre)
+        out.append(acc)
+    return out
+
+
+def pool_rms(I_rows):
+    n, T = len(I_rows), len(I_rows[0])
+    s = [0.0] * T
+    for i in range(n):
+        mx = max(I_rows[i])
+        den = sum(math.exp(v - mx) for v in I_rows[i])
+        for j in range(T):
+            p = math.exp(I_rows[i][j] - mx) / den
+            s[j] += p * p / n
+    return [math.sqrt(v) for v in s]
+
+
+def select(scores, t):
+    def key(j):
+        v = scores[j]
+        if v != v:            # NaN: after every number
+            return (1, 0.0, j)
+        if v == 0.0:
+            v = 0.0
+        return (0, -v, j)
+    order = sorted(range(len(scores)), key=key)
+    return sorted(order[:t])
+
+
+def dot(a, b):
+    return sum(float(x) * float(y) for x, y in zip(a, b))
+
+
+def logits(Q, K, scale):
+    return [[scale * dot(q, k) for k in K] for q in Q]
+
+
+def profiles(Q, K, scale):
+    L = logits(Q, K, scale)
+    n, T = len(Q), len(K)
+    zm = max(max(row) for row in L)
+    E = [[math.exp(L[i][j] - zm) for j in range(T)] for i in range(n)]
+    U = []
+    for j in range(T):
+        col = [E[i][j] for i in range(n)]
+        nrm = math.sqrt(sum(v * v for v in col))
+        U.append([v / nrm if nrm > 0 else 0.0 for v in col])
+    phi = [sum(E[i][j] for i in range(n)) / n for j in range(T)]
+    return U, phi, zm
+
+
+def assign(U, S):
+    T = len(U)
+    pos = {s: r for r, s in enumerate(S)}
+    kappa = []
+    for j in range(T):
+        if j in pos:
+            kappa.append(pos[j])
+            continue
+        best, br = -math.inf, -1
+        for r, s in enumerate(S):
+            v = dot(U[j], U[s])
+            if v > best:
+                best, br = v, r
+        kappa.append(br)
+    return kappa
+
+
+def merge(K, phi, kappa, S, lam):
+    d = len(K[0])
+    out = []
+    for r, s in enumerate(S):
+        num = [0.0] * d
+        den = 0.0
+        for j in range(len(K)):
+            if kappa[j] == r:
+                den += phi[j]
+                for c in range(d):
+                    num[c] += phi[j] * float(K[j][c])
+        mu = [v / den for v in num] if den > 0 else [float(v) for v in K[s]]
+        out.append([(1 - lam) * float(K[s][c]) + lam * mu[c] for c in range(d)])
+    return out
+
+
+def rowstats(Q, K, V, scale):
+    L = logits(Q, K, scale)
+    z, m, Y = [], [], []
+    for i in range(len(Q)):
+        zi = max(L[i])
+        w = [math.exp(v - zi) for v in L[i]]
+        mi = sum(w)
+        y = [sum(w[j] * float(V[j][c]) for j in range(len(K))) / mi for c in range(len(V[0]))]
+        z.append(zi)
+        m.append(mi)
+        Y.append(y)
+    return z, m, Y
+
+
+def compact_attend(Q, C_k, beta, C_v, scale):
+    out = []
+    for q in Q:
+        x = [scale * dot(q, c) + b for c, b in zip(C_k, beta)]
+        mx = max(x)
+        w = [math.exp(v - mx) for v in x]
+        s = sum(w)
+        out.append([sum(w[r] * C_v[r][c] for r in range(len(C_k))) / s for c in range(len(C_v[0]))])
+    return out

@@ -1,0 +1,406 @@
+"""Pins of the float64 oracle against things other than itself.
+
+Each test checks the oracle against a brute-force loop written separately
+(tests/brute.py), a closed form, an identity the paper states, a library
+routine that solves the same problem another way, or a value printed in the
+workload definitions.  No GPU involved.
+"""
+import math
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from tests import brute
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def rng(seed):
+    return np.random.default_rng(seed)
+
+
+def small_pair(seed=0, T=12, n=20, d=6, hidden=5, outlier=True):
+    g = rng(seed)
+    K = g.standard_normal((T, d))
+    if outlier:
+        K[:, 0] *= 3.0
+    V = g.standard_normal((T, d))
+    Q = g.standard_normal((n, d))
+    W1 = g.uniform(-0.5, 0.5, (hidden, 2 * d))
+    b1 = g.uniform(-0.5, 0.5, hidden)
+    w2 = g.uniform(-0.5, 0.5, hidden)
+    b2 = np.array([g.uniform(-0.5, 0.5)])
+    return K, V, Q, W1, b1, w2, b2
+
+
+# ----------------------------------------------------------------- O0 budget
+def test_budget_golden():
+    rows = [l.split() for l in open(os.path.join(GOLDEN, "budgets.txt")) if l.strip() and not l.startswith("#")]
+    assert rows
+    for T, rho, t in rows:
+        assert oracle.budget(int(T), float(rho)) == int(t)
+
+
+def test_budget_edges():
+    assert oracle.budget(10, 0.0) == 1            # clipped up to 1
+    assert oracle.budget(10, 1.0) == 10
+    assert oracle.budget(10, 5.0) == 10           # clipped down to T
+    assert oracle.budget(10, 0.25) == 3           # 2.5 rounds half up
+    assert oracle.budget(10, 0.24) == 2
+    for T, rho in [(16384, 0.2), (16384, 0.1), (16384, 0.05), (16384, 0.02), (8192, 0.1), (32768, 0.1)]:
+        t = oracle.budget(T, rho)
+        assert abs(t - rho * T) <= 0.5
+
+
+# ----------------------------------------------------------------- O1 score
+def test_gelu_values():
+    xs = np.array([-3.0, -1.0, -0.5, 0.0, 0.5, 1.0, 2.5])
+    got = oracle.gelu(xs)
+    for x, g in zip(xs, got):
+        assert g == pytest.approx(0.5 * x * (1 + math.erf(x / math.sqrt(2))), rel=1e-15, abs=1e-300)
+    assert oracle.gelu(np.array([0.0]))[0] == 0.0
+    # GELU(x) - GELU(-x) = x for the erf form
+    y = np.linspace(-6, 6, 101)
+    np.testing.assert_allclose(oracle.gelu(y) - oracle.gelu(-y), y, rtol=0, atol=1e-14)
+
+
+def test_score_bruteforce():
+    K, V, Q, W1, b1, w2, b2 = small_pair(1)
+    got = oracle.score_mlp(K, V, W1, b1, w2, b2)
+    ref = brute.score(K.tolist(), V.tolist(), W1.tolist(), b1.tolist(), w2.tolist(), b2[0])
+    np.testing.assert_allclose(got, ref, rtol=1e-13, atol=1e-13)
+
+
+def test_score_zero_weights_all_tie():
+    K, V, Q, W1, b1, w2, b2 = small_pair(2)
+    I = oracle.score_mlp(K, V, np.zeros_like(W1), b1, w2, b2)
+    assert np.all(I == I[0])
+    assert oracle.select_topt(I, 5).tolist() == [0, 1, 2, 3, 4]
+
+
+def test_pool_rms_bruteforce_and_single_row():
+    g = rng(3)
+    I = g.standard_normal((7, 15)) * 2
+    np.testing.assert_allclose(oracle.pool_rms(I), brute.pool_rms(I.tolist()), rtol=1e-13)
+    # a query-independent scorer: identical rows -> s = softmax(I), same ranking as I
+    row = g.standard_normal(15)
+    s = oracle.pool_rms(np.tile(row, (4, 1)))
+    e = np.exp(row - row.max())
+    np.testing.assert_allclose(s, e / e.sum(), rtol=1e-13)
+    assert oracle.select_topt(s, 6).tolist() == oracle.select_topt(row, 6).tolist()
+
+
+# ----------------------------------------------------------------- O2 select
+@pytest.mark.parametrize("seed", range(6))
+def test_select_matches_exhaustive_sort(seed):
+    g = rng(10 + seed)
+    T = int(g.integers(1, 60))
+    kind = seed % 3
+    if kind == 0:
+        s = g.standard_normal(T)
+    elif kind == 1:
+        s = g.integers(-3, 3, T).astype(np.float64)          # many duplicates
+    else:
+        s = g.choice([0.0, -0.0, 1.0, -1.0, np.inf, -np.inf, np.nan], T)
+    for t in sorted({1, T, max(1, T // 3), max(1, T // 2)}):
+        assert oracle.select_topt(s, t).tolist() == brute.select(s.tolist(), t)
+
+
+def test_select_special_cases():
+    s = np.array([1.0, 3.0, 3.0, -0.0, 0.0, np.nan, -np.inf])
+    assert oracle.select_topt(s, 1).tolist() == [1]            # lowest-index argmax
+    assert oracle.select_topt(s, 2).tolist() == [1, 2]
+    assert oracle.select_topt(s, 4).tolist() == [0, 1, 2, 3]   # -0 ties +0; lower index wins
+    assert oracle.select_topt(s, 6).tolist() == [0, 1, 2, 3, 4, 6]   # NaN below -inf
+    assert oracle.select_topt(s, 7).tolist() == list(range(7))
+    with pytest.raises(ValueError):
+        oracle.select_topt(s, 0)
+
+
+# ----------------------------------------------------------------- O3-O5
+def test_profiles_bruteforce_and_invariants():
+    K, V, Q, *_ = small_pair(4)
+    s = 0.7
+    E, U, zm = oracle.response_profiles(Q, K, s)
+    Ub, phib, zmb = brute.profiles(Q.tolist(), K.tolist(), s)
+    np.testing.assert_allclose(U.T, Ub, rtol=1e-12, atol=1e-15)
+    np.testing.assert_allclose(oracle.mass_weights(E), phib, rtol=1e-12)
+    assert zm == pytest.approx(zmb, rel=1e-14)
+    np.testing.assert_allclose(np.linalg.norm(U, axis=0), 1.0, rtol=1e-13)
+    # profiles do not depend on the global shift
+    _, U2, _ = oracle.response_profiles(Q, K, s, z_merge=zm - 3.0)
+    np.testing.assert_allclose(U2, U, rtol=1e-12)
+
+
+def test_assign_bruteforce_selfassign_and_partition():
+    K, V, Q, *_ = small_pair(5, T=15)
+    S = np.array([1, 4, 9, 13])
+    _, U, _ = oracle.response_profiles(Q, K, 0.5)
+    kap = oracle.assign(U, S)
+    assert kap.tolist() == brute.assign(U.T.tolist(), S.tolist())
+    assert kap[S].tolist() == list(range(len(S)))          # kappa(s_r) = r
+    groups = [np.flatnonzero(kap == r) for r in range(len(S))]
+    assert sum(len(gr) for gr in groups) == len(K)          # a partition of [T]
+    assert all(len(gr) > 0 and S[r] in gr for r, gr in enumerate(groups))
+
+
+def test_assign_ties_lowest_anchor_and_duplicate_keys():
+    K, V, Q, *_ = small_pair(6, T=10)
+    K[7] = K[2]                       # two anchors with identical keys -> identical profiles
+    K[5] = K[3]                       # a duplicated non-anchor key
+    S = np.array([2, 7])
+    _, U, _ = oracle.response_profiles(Q, K, 0.5)
+    kap = oracle.assign(U, S)
+    assert kap[2] == 0 and kap[7] == 1
+    others = [j for j in range(10) if j not in (2, 7)]
+    assert all(kap[j] == 0 for j in others)   # every similarity ties -> lowest r
+    S2 = np.array([0, 4, 8])
+    kap2 = oracle.assign(U, S2)
+    assert kap2[5] == kap2[3]
+
+
+def test_chunked_path_equals_direct():
+    K, V, Q, *_ = small_pair(7, T=40, n=9)
+    S = np.array([0, 5, 17, 30, 39])
+    E, U, zm = oracle.response_profiles(Q, K, 0.4)
+    old = oracle.core._CHUNK_ELEMS
+    try:
+        oracle.core._CHUNK_ELEMS = 9 * 7                # 7 keys per chunk
+        kap, phi, zm2 = oracle.profiles_assign_phi(Q, K, S, 0.4)
+    finally:
+        oracle.core._CHUNK_ELEMS = old
+    assert kap.tolist() == oracle.assign(U, S).tolist()
+    np.testing.assert_allclose(phi, oracle.mass_weights(E), rtol=1e-13)
+    assert zm2 == zm
+
+
+def test_merge_endpoints_and_bruteforce():
+    K, V, Q, *_ = small_pair(8, T=14)
+    S = np.array([0, 3, 6, 11])
+    kap, phi, _ = oracle.profiles_assign_phi(Q, K, S, 0.5)
+    # lambda_m = 0 leaves the anchors unmerged, bit for bit
+    assert np.array_equal(oracle.merge_keys(K, phi, kap, S, 0.0), K[S])
+    for lam in (0.25, 0.5, 1.0):
+        got = oracle.merge_keys(K, phi, kap, S, lam)
+        ref = brute.merge(K.tolist(), phi.tolist(), kap.tolist(), S.tolist(), lam)
+        np.testing.assert_allclose(got, ref, rtol=1e-13, atol=1e-14)
+    # t = 1: one group holding every key
+    S1 = np.array([4])
+    kap1, phi1, _ = oracle.profiles_assign_phi(Q, K, S1, 0.5)
+    assert np.all(kap1 == 0)
+    mu = (phi1[:, None] * K).sum(0) / phi1.sum()
+    np.testing.assert_allclose(oracle.merge_keys(K, phi1, kap1, S1, 0.3)[0], 0.7 * K[4] + 0.3 * mu, rtol=1e-13)
+    # t = T: singleton groups, C_k = K for every lambda
+    SA = np.arange(len(K))
+    kapA, phiA, _ = oracle.profiles_assign_phi(Q, K, SA, 0.5)
+    np.testing.assert_allclose(oracle.merge_keys(K, phiA, kapA, SA, 0.6), K, rtol=1e-14, atol=1e-15)
+
+
+def test_merge_convex_hull():
+    K, V, Q, *_ = small_pair(9, T=30, n=25)
+    S = np.array([2, 8, 15, 21, 27])
+    kap, phi, _ = oracle.profiles_assign_phi(Q, K, S, 0.5)
+    Ck = oracle.merge_keys(K, phi, kap, S, 0.6)
+    probes = rng(99).standard_normal((50, K.shape[1]))
+    for r in range(len(S)):
+        G = K[kap == r]
+        assert np.all(Ck[r] >= G.min(0) - 1e-12) and np.all(Ck[r] <= G.max(0) + 1e-12)
+        lg = probes @ G.T
+        lc = probes @ Ck[r]
+        assert np.all(lc >= lg.min(1) - 1e-12) and np.all(lc <= lg.max(1) + 1e-12)
+
+
+def test_merge_zero_mass_group_keeps_anchor():
+    K = rng(1).standard_normal((4, 3))
+    S = np.array([0, 2])
+    kap = np.array([0, 0, 1, 1])
+    phi = np.array([0.5, 0.5, 0.0, 0.0])
+    Ck = oracle.merge_keys(K, phi, kap, S, 1.0)
+    assert np.array_equal(Ck[1], K[2])
+
+
+# ----------------------------------------------------------------- O6
+def test_rowstats_bruteforce_and_bounds():
+    K, V, Q, *_ = small_pair(10, T=11, n=7)
+    z, m, Y = oracle.rowstats(Q, K, V, 0.6)
+    zb, mb, Yb = brute.rowstats(Q.tolist(), K.tolist(), V.tolist(), 0.6)
+    np.testing.assert_allclose(z, zb, rtol=1e-14)
+    np.testing.assert_allclose(m, mb, rtol=1e-13)
+    np.testing.assert_allclose(Y, Yb, rtol=1e-12, atol=1e-14)
+    assert np.all(m >= 1.0 - 1e-15) and np.all(m <= len(K))
+    assert np.all(Y >= V.min(0) - 1e-12) and np.all(Y <= V.max(0) + 1e-12)
+    # T = 1: the single value comes back, m = 1
+    z1, m1, Y1 = oracle.rowstats(Q, K[:1], V[:1], 0.6)
+    np.testing.assert_allclose(m1, 1.0)
+    np.testing.assert_allclose(Y1, np.tile(V[0], (len(Q), 1)), rtol=1e-15)
+    np.testing.assert_allclose(z1, 0.6 * Q @ K[0], rtol=1e-14)
+
+
+def test_rowstats_matches_library_softmax():
+    from scipy.special import softmax
+    K, V, Q, *_ = small_pair(11, T=50, n=13)
+    _, _, Y = oracle.rowstats(Q, K, V, 0.3)
+    np.testing.assert_allclose(Y, softmax(0.3 * Q @ K.T, axis=1) @ V, rtol=1e-12)
+
+
+# ----------------------------------------------------------------- O7 mass fit
+def test_mass_fit_single_anchor_closed_form():
+    K, V, Q, *_ = small_pair(12, T=9, n=16)
+    s = 0.5
+    z, m, _ = oracle.rowstats(Q, K, V, s)
+    Ck = K[3:4]
+    bf = oracle.fit_bias(Q, Ck, z, m, s, delta=0.0)
+    phi = np.exp(s * Q @ Ck[0] - z)
+    assert bf.w_tilde[0] == pytest.approx(phi @ m / (phi @ phi), rel=1e-12)
+    assert bf.beta[0] == pytest.approx(math.log(phi @ m / (phi @ phi)), rel=1e-12)
+
+
+def test_mass_fit_matches_lstsq_without_ridge():
+    K, V, Q, *_ = small_pair(13, T=25, n=60)
+    s = 0.5
+    z, m, _ = oracle.rowstats(Q, K, V, s)
+    Ck = K[[1, 5, 9, 14, 20]] * 0.9
+    bf = oracle.fit_bias(Q, Ck, z, m, s, delta=0.0)
+    PhiC = np.exp(s * Q @ Ck.T - z[:, None])
+    w_ls = np.linalg.lstsq(PhiC, m, rcond=None)[0]
+    np.testing.assert_allclose(bf.w_tilde, w_ls, rtol=1e-8, atol=1e-10)
+    np.testing.assert_allclose(bf.beta, np.clip(np.log(np.maximum(np.maximum(w_ls, 0), 1e-12)), -30, 30), rtol=1e-7)
+
+
+def brute_nnls(G, h):
+    t = len(h)
+    best, bw = math.inf, None
+    for mask in range(1 << t):
+        P = [i for i in range(t) if mask >> i & 1]
+        w = np.zeros(t)
+        if P:
+            w[P] = np.linalg.solve(G[np.ix_(P, P)], h[P])
+            if np.any(w[P] < 0):
+                continue
+        f = 0.5 * w @ G @ w - h @ w
+        if f < best - 1e-15:
+            best, bw = f, w
+    return bw
+
+
+@pytest.mark.parametrize("seed", range(5))
+def test_nnls_matches_bruteforce(seed):
+    g = rng(40 + seed)
+    t = int(g.integers(2, 9))
+    A = g.standard_normal((3 * t, t))
+    b = g.standard_normal(3 * t)
+    G, h = A.T @ A, A.T @ b
+    np.testing.assert_allclose(oracle.nnls_gram(G, h), brute_nnls(G, h), rtol=1e-9, atol=1e-11)
+
+
+def test_nnls_mode_on_mass_fit():
+    K, V, Q, *_ = small_pair(14, T=20, n=40)
+    s = 0.8
+    z, m, _ = oracle.rowstats(Q, K, V, s)
+    Ck = K[[0, 2, 3, 7, 11, 12, 19]]
+    bf0 = oracle.fit_bias(Q, Ck, z, m, s, delta=1e-8, mode=0)
+    bf1 = oracle.fit_bias(Q, Ck, z, m, s, delta=1e-8, mode=1)
+    t = len(Ck)
+    Greg = bf1.G + 1e-8 * np.trace(bf1.G) / t * np.eye(t)
+    np.testing.assert_allclose(bf1.w_star, brute_nnls(Greg, bf1.h), rtol=1e-7, atol=1e-10)
+    if np.all(bf0.w_tilde >= 0):        # projected LS = NNLS when nothing is clipped
+        np.testing.assert_allclose(bf0.w_star, bf1.w_star, rtol=1e-7)
+
+
+def test_full_retention_mass_fit_is_exact():
+    K, V, Q, *_ = small_pair(15, T=8, n=30)
+    s = 0.5
+    z, m, _ = oracle.rowstats(Q, K, V, s)
+    bf = oracle.fit_bias(Q, K, z, m, s, delta=0.0)
+    np.testing.assert_allclose(bf.w_tilde, 1.0, rtol=1e-9)
+    np.testing.assert_allclose(bf.beta, 0.0, atol=1e-9)
+
+
+def test_ridge_escalation():
+    A = np.array([[1.0, 1.001], [1.001, 1.0]])          # indefinite by 1e-3
+    X, d, attempts = oracle.ridge_cholesky_solve(A, np.ones(2), 1e-5)
+    assert attempts == 4 and d == pytest.approx(1e-2)
+    np.testing.assert_allclose((A + d * np.eye(2)) @ X, np.ones(2), rtol=1e-10)
+    with pytest.raises(oracle.CholeskyFailure):
+        oracle.ridge_cholesky_solve(A, np.ones(2), 1e-5, max_escalations=2)
+    with pytest.raises(oracle.CholeskyFailure):
+        oracle.ridge_cholesky_solve(np.zeros((2, 2)) - np.eye(2), np.ones(2), 0.0)
+
+
+# ----------------------------------------------------------------- O8 value fit
+def test_value_fit_matches_augmented_lstsq():
+    K, V, Q, *_ = small_pair(16, T=30, n=50)
+    s = 0.5
+    z, m, Y = oracle.rowstats(Q, K, V, s)
+    Ck = K[[0, 4, 9, 13, 22, 29]]
+    beta = rng(0).uniform(-1, 1, 6)
+    vf = oracle.fit_values(Q, Ck, beta, Y, s, delta=1e-3)
+    P = oracle.compact_probs(Q, Ck, beta, s)
+    lam = 1e-3 * np.trace(P.T @ P) / 6
+    Aug = np.vstack([P, math.sqrt(lam) * np.eye(6)])
+    rhs = np.vstack([Y, np.zeros((6, Y.shape[1]))])
+    np.testing.assert_allclose(vf.C_v, np.linalg.lstsq(Aug, rhs, rcond=None)[0], rtol=1e-9, atol=1e-11)
+    # normal-equation residual P^T (P C - Y) + lam C = 0
+    res = P.T @ (P @ vf.C_v - Y) + lam * vf.C_v
+    assert np.abs(res).max() < 1e-12 * max(1.0, np.abs(P.T @ Y).max())
+
+
+def test_value_fit_linear_and_translation_equivariant():
+    K, V, Q, *_ = small_pair(17, T=20, n=40)
+    s = 0.5
+    Ck = K[[1, 6, 12, 18]]
+    beta = np.array([0.1, -0.2, 0.3, 0.0])
+    Y1 = rng(1).standard_normal((40, 6))
+    Y2 = rng(2).standard_normal((40, 6))
+    f = lambda Y, dv: oracle.fit_values(Q, Ck, beta, Y, s, delta=dv).C_v
+    np.testing.assert_allclose(f(2 * Y1 - 3 * Y2, 1e-3), 2 * f(Y1, 1e-3) - 3 * f(Y2, 1e-3), rtol=1e-9, atol=1e-12)
+    c = rng(3).standard_normal(6)
+    np.testing.assert_allclose(f(Y1 + c, 0.0), f(Y1, 0.0) + c, rtol=1e-8, atol=1e-10)
+
+
+def test_compact_attention_bruteforce():
+    g = rng(18)
+    Q, Ck, Cv = g.standard_normal((5, 4)), g.standard_normal((3, 4)), g.standard_normal((3, 4))
+    beta = g.standard_normal(3)
+    np.testing.assert_allclose(oracle.attend_compact(Q, Ck, beta, Cv, 0.7),
+                               brute.compact_attend(Q.tolist(), Ck.tolist(), beta.tolist(), Cv.tolist(), 0.7),
+                               rtol=1e-13)
+
+
+# ----------------------------------------------------------------- O9 end to end
+def test_full_retention_reproduces_full_attention():
+    K, V, Q, W1, b1, w2, b2 = small_pair(19, T=8, n=40)
+    res = oracle.compact_pair(K, V, Q, W1, b1, w2, b2, t=8, scale=0.5, lambda_m=0.5,
+                              delta_beta=0.0, delta_v=0.0)
+    assert res.anchors.tolist() == list(range(8))
+    np.testing.assert_allclose(res.C_k, K, rtol=1e-13, atol=1e-14)
+    np.testing.assert_allclose(res.beta, 0.0, atol=1e-8)
+    np.testing.assert_allclose(res.C_v, V, rtol=1e-7, atol=1e-8)
+    Qh = rng(20).standard_normal((15, K.shape[1]))
+    np.testing.assert_allclose(oracle.attend_compact(Qh, res.C_k, res.beta, res.C_v, 0.5),
+                               oracle.attend_full(Qh, K, V, 0.5), rtol=1e-7, atol=1e-8)
+    # the joint objective with an uncompressed block (Appendix A.7) holds exactly too
+    Kf, Vf = rng(21).standard_normal((3, K.shape[1])), rng(22).standard_normal((3, K.shape[1]))
+    full = oracle.attend_full(Qh, np.vstack([K, Kf]), np.vstack([V, Vf]), 0.5)
+    joint = oracle.attend_compact(Qh, np.vstack([res.C_k, Kf]), np.concatenate([res.beta, np.zeros(3)]),
+                                  np.vstack([res.C_v, Vf]), 0.5)
+    np.testing.assert_allclose(joint, full, rtol=1e-7, atol=1e-8)
+
+
+def test_compaction_beats_hard_subset_on_heldout():
+    """Trend check (Table 1 ordering): merged+fitted cache < hard subset error."""
+    g = rng(23)
+    T, n, d = 200, 160, 16
+    K = g.standard_normal((T, d)); K[:, 0] *= 4
+    V = g.standard_normal((T, d))
+    Q = g.standard_normal((n, d))
+    Qh = g.standard_normal((64, d))
+    W1 = g.uniform(-.2, .2, (8, 2 * d)); b1 = g.uniform(-.2, .2, 8); w2 = g.uniform(-.3, .3, 8)
+    res = oracle.compact_pair(K, V, Q, W1, b1, w2, np.zeros(1), rho=0.1, scale=0.25)
+    O = oracle.attend_full(Qh, K, V, 0.25)
+    fitted = oracle.row_rel_err(oracle.attend_compact(Qh, res.C_k, res.beta, res.C_v, 0.25), O).mean()
+    S = res.anchors
+    hard = oracle.row_rel_err(oracle.attend_compact(Qh, K[S], np.zeros(len(S)), V[S], 0.25), O).mean()
+    assert fitted < hard
