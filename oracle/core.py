@@ -34,7 +34,7 @@ import numpy as np
 # Parameter defaults (readings of the paper where it gives no value).
 LAMBDA_M = 0.25          # Section 4.1 uses 0.25 on QuALITY and RULER
 DELTA_BETA = 1e-6        # relative ridge of the mass fit (paper: unregularised LS)
-DELTA_V = 1e-4           # lambda_v = DELTA_V * tr(A) / t (paper: lambda_v >= 0)
+DELTA_V = 1e-3           # lambda_v = DELTA_V * tr(A) / t (paper: lambda_v >= 0, no value)
 EPS_W = 1e-12            # epsilon_w of eq. (mass_fit)
 B_MIN, B_MAX = -30.0, 30.0
 MAX_ESCALATIONS = 3      # ridge x10 retries when a Cholesky pivot fails
