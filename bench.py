@@ -1,0 +1,184 @@
+"""Throughput of ARC-KV per-context compaction on one MI355X.
+
+One step = one arckv_compact call over every layer-KV-head pair of the
+workload (score, select, row statistics, assignment and merge, mass fit,
+value fit), inputs resident in HBM.  Prints ONE JSON line.
+
+  python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import synth  # noqa: E402
+
+HEADLINE = "llama8b_bf16_T32768"
+PEAK_BF16_TFLOPS = 2500.0        # MI355X dense bf16 MFMA
+PEAK_FP32_TFLOPS = 157.3
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def load_inputs(wl, device):
+    """Generate the seeded workload layer by layer and upload it (bf16 / fp32)."""
+    import torch
+    td = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
+    B, T, n, d = wl.pairs, wl.T, wl.n, wl.d
+    K = torch.empty(B, T, d, dtype=td, device=device)
+    V = torch.empty(B, T, d, dtype=td, device=device)
+    Q = torch.empty(B, n, d, dtype=td, device=device)
+    W1 = torch.empty(B, 64, 2 * d, dtype=td, device=device)
+    b1 = torch.empty(B, 64, dtype=torch.float32, device=device)
+    w2 = torch.empty(B, 64, dtype=torch.float32, device=device)
+    b2 = torch.empty(B, dtype=torch.float32, device=device)
+    step = wl.kv_heads
+    threads = min(16, os.cpu_count() or 1)
+    t0 = time.time()
+    for b0 in range(0, B, step):
+        idx = list(range(b0, min(B, b0 + step)))
+        arr = synth.workload_arrays(wl, pairs=idx, threads=threads)
+        sl = slice(idx[0], idx[-1] + 1)
+        K[sl] = torch.from_numpy(arr["K"]).to(device).to(td)
+        V[sl] = torch.from_numpy(arr["V"]).to(device).to(td)
+        Q[sl] = torch.from_numpy(arr["Q"]).to(device).to(td)
+        W1[sl] = torch.from_numpy(arr["W1"]).to(device).to(td)
+        b1[sl] = torch.from_numpy(arr["b1"]).to(device)
+        w2[sl] = torch.from_numpy(arr["w2"]).to(device)
+        b2[sl] = torch.from_numpy(arr["b2"][:, 0]).to(device)
+        if (b0 // step) % 8 == 0:
+            log(f"[inputs] pairs {idx[-1] + 1}/{B} generated ({time.time() - t0:.1f}s)")
+    torch.cuda.synchronize()
+    return K, V, Q, W1, b1, w2, b2
+
+
+def assign_flops(wl, t):
+    """Algorithmic flops of the key-to-anchor assignment, all pairs: 2 n (T - t) t each."""
+    return 2.0 * wl.n * (wl.T - t) * t * wl.pairs
+
+
+def cpu_baseline(wl, t, budget_s=25.0):
+    """The float64 oracle on a bounded sample of the same workload (whole pairs)."""
+    import oracle
+    try:
+        cores = len(os.sched_getaffinity(0))
+    except AttributeError:
+        cores = os.cpu_count() or 1
+    s = 1.0 / math.sqrt(wl.d)
+    done, t_used = 0, 0.0
+    while done < wl.pairs:
+        layer, head = synth.pair_index(wl, done)
+        p = synth.pair_inputs(wl, layer, head)
+        h = {k: v.astype(np.float64) for k, v in p.items()}
+        t0 = time.perf_counter()
+        oracle.compact_pair(h["K"], h["V"], h["Q"], h["W1"], h["b1"], h["w2"], h["b2"][0], t=t, scale=s)
+        t_used += time.perf_counter() - t0
+        done += 1
+        log(f"[cpu_baseline] oracle pair {done}: {t_used:.1f}s cumulative")
+        if t_used >= budget_s * 0.5:
+            break
+    per_pair = t_used / done
+    value = wl.T / (per_pair * wl.pairs)
+    return {"value": value, "unit": "tokens/s", "cores": cores, "kind": "oracle",
+            "sample": f"{done} of {wl.pairs} pairs (layer 0) of the same workload, float64 numpy oracle, "
+                      f"{per_pair:.2f} s/pair, scaled to all {wl.pairs} pairs"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default=HEADLINE, choices=sorted(synth.WORKLOADS))
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--pair-chunk", type=int, default=0)
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one MI355X: the compaction path has no multi-GPU mode "
+              "(pairs shard across GPUs with no communication); run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2609_36835_amd import arckv
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    wl = synth.WORKLOADS[args.workload]
+    dev = torch.device("cuda:0")
+    log(f"[bench] workload {wl.name}: pairs={wl.pairs} T={wl.T} n={wl.n} rho={wl.rho} dtype={wl.dtype}")
+    K, V, Q, W1, b1, w2, b2 = load_inputs(wl, dev)
+    params = arckv.default_params(pair_chunk=args.pair_chunk)
+    comp = arckv.Compactor(wl.pairs, wl.T, wl.n, wl.rho, K.dtype, dev, scale=1.0 / math.sqrt(wl.d), params=params)
+    t = comp.t
+    log(f"[bench] t={t}, workspace {comp.ws_bytes / 2**30:.1f} GiB")
+
+    for i in range(args.warmup):
+        comp(K, V, Q, W1, b1, w2, b2)
+        torch.cuda.synchronize()
+        log(f"[bench] warmup {i + 1}/{args.warmup} done")
+    info = comp.info.cpu()
+    if int(info.abs().sum()) != 0:
+        log(f"[bench] WARNING: nonzero fit status in {int((info != 0).sum())} entries")
+
+    arckv.reset_timing()
+    arckv.set_timing(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        comp(K, V, Q, W1, b1, w2, b2)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    arckv.set_timing(False)
+    stages = arckv.stage_times()
+    ms_per_step = 1e3 * elapsed / args.steps
+    value = wl.T * args.steps / elapsed
+    log(f"[bench] {args.steps} steps in {elapsed:.3f}s: {ms_per_step:.2f} ms/step, {value:.1f} tokens/s")
+    for name, (ms, cnt) in stages.items():
+        if cnt:
+            log(f"    {name:16s} {ms / args.steps:9.3f} ms/step  ({cnt} launches)")
+
+    ms_assign, cnt_assign = stages["assign_gemm"]
+    avg_launch_s = ms_assign / 1e3 / max(cnt_assign, 1)
+    launches_per_step = max(cnt_assign // args.steps, 1)
+    flops_per_launch = assign_flops(wl, t) / launches_per_step
+    achieved = flops_per_launch / avg_launch_s / 1e12
+    roofline = {"bound": "mfma", "kernel": "k_gemm_tn<bf16,1,1,EpiArgmax> (key-to-anchor assignment)",
+                "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                "avg_launch_ms": round(avg_launch_s * 1e3, 3),
+                "algorithmic_flops_per_launch": flops_per_launch}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        del K, V, Q, comp
+        torch.cuda.empty_cache()
+        cpu = cpu_baseline(wl, t)
+
+    out = {
+        "metric": "full-cache tokens compacted/sec per MI355X (Llama-3.1-8B shapes, 10% kept)",
+        "value": round(value, 2), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 3), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": wl.dtype, "data": "synthetic (seeded Gaussian K/V/Q_ref with RoPE and outlier key channels; "
+                                  "random-init scoring MLP)",
+        "config": {"workload": wl.name, "pairs": wl.pairs, "layers": wl.layers, "kv_heads": wl.kv_heads,
+                   "T": wl.T, "n_ref": wl.n, "t": t, "rho": wl.rho, "head_dim": wl.d,
+                   "pair_chunk": args.pair_chunk or wl.pairs},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "stage_ms_per_step": {k: round(v[0] / args.steps, 3) for k, v in stages.items() if v[1]},
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

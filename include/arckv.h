@@ -1,0 +1,200 @@
+/*
+ * arckv.h -- C ABI of the MI355X (gfx950) ARC-KV per-context compaction library.
+ *
+ * ARC-KV (arXiv 2609.36835) replaces a long key/value cache block (K, V, T rows
+ * of head dimension d) of one layer-KV-head pair by t << T compact entries
+ * (C_k, beta, C_v) so that softmax(q C_k^T + beta) C_v approximates full
+ * attention softmax(q K^T) V and the block's attention mass (Section 3.1,
+ * eq. compact_attention and eq. block_attention_mass).  Per context, four
+ * stages run (Section 3.2):
+ *   1. score every cached token and take the top-t tokens as anchors (Section 3.3);
+ *   2. assign every key to the anchor with the most similar normalised
+ *      attention-response profile and merge each group into one compact key
+ *      inside the group's convex hull (Section 3.4);
+ *   3. fit the mass bias beta by projected least squares (Appendix A.9, eq. mass_fit);
+ *   4. fit the compact values C_v by ridge least squares (Appendix A.9, eq. value_lstsq).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - A call processes B independent pairs (flattened [layer][kv_head]).
+ *  - All array arguments are DEVICE pointers owned by the caller, row-major and
+ *    contiguous: K, V [B][T][d]; Q_ref [B][n][d] (each pair's n rows ordered
+ *    [query head][position]); per-pair vectors [B][len].  Inputs are read-only.
+ *  - K, V and Q_ref share one element type (arckv_problem.dtype): float32 or
+ *    bfloat16.  Only d = 128 is supported.  Outputs are float32 (indices int32).
+ *  - The library never allocates device memory.  Entry points that need scratch
+ *    take a caller-owned device workspace (ws, ws_bytes) of at least
+ *    arckv_workspace_size() bytes, 256-byte aligned.  Its contents are
+ *    undefined on entry and exit; it must not be shared by calls that may
+ *    overlap in time.
+ *  - All device work is enqueued on the caller's stream; no entry point
+ *    synchronises the host.  Results are valid once the stream reaches them.
+ *  - Argument errors are returned synchronously BEFORE any HIP call, so they can
+ *    be checked on a machine without a GPU.  A failed kernel launch returns
+ *    ARCKV_ERR_HIP.  Numerical failures are reported asynchronously in the
+ *    per-pair `info` arrays.  No C++ exception crosses this interface.
+ *  - The logit scale s multiplies q.k everywhere (the paper omits 1/sqrt(d) by
+ *    convention, Section 3.1); scale <= 0 selects 1/sqrt(d).
+ */
+#ifndef ARCKV_H
+#define ARCKV_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  ARCKV_OK = 0,
+  ARCKV_ERR_INVALID_ARG = 1,   /* null pointer, bad size, t outside [1, T], ... */
+  ARCKV_ERR_UNSUPPORTED = 2,   /* d != 128, unknown dtype, bias_mode != 0, ... */
+  ARCKV_ERR_WORKSPACE = 3,     /* ws too small or misaligned */
+  ARCKV_ERR_HIP = 4            /* a HIP launch or runtime call failed */
+} arckv_status;
+
+typedef enum { ARCKV_F32 = 0, ARCKV_BF16 = 1 } arckv_dtype;
+
+typedef struct {
+  int32_t B;       /* pairs in the call, >= 1 */
+  int32_t T;       /* cached tokens per pair, >= 1 */
+  int32_t n;       /* reference queries per pair, >= 1 */
+  int32_t d;       /* head dimension; must be 128 */
+  int32_t dtype;   /* arckv_dtype of K, V, Q_ref */
+  float scale;     /* logit scale s; <= 0 selects 1/sqrt(d) */
+} arckv_problem;
+
+/* The token scorer: a 2-layer MLP on concat(k_j, v_j),
+ * I_j = w2 . GELU(W1 [k_j; v_j] + b1) + b2, GELU in its exact erf form.
+ * It is query-independent, so the root-mean-square pooling of eq.
+ * indexer_pooling reduces to softmax(I), and ranking by I ranks by the pooled
+ * score (Section 3.3). */
+typedef struct {
+  int32_t hidden;     /* hidden width; must be 64 */
+  int32_t w1_dtype;   /* arckv_dtype of W1 */
+  const void *W1;     /* [B][hidden][2d], input order [k ; v] */
+  const float *b1;    /* [B][hidden] */
+  const float *w2;    /* [B][hidden] */
+  const float *b2;    /* [B] */
+} arckv_indexer;
+
+/* Fit parameters (Section 3.4 and Appendix A.9).  The paper gives lambda_m;
+ * the remaining values are this library's readings. */
+typedef struct {
+  float lambda_m;        /* key-merge coefficient in [0, 1]; default 0.25 */
+  float delta_beta;      /* relative ridge of the mass fit: G + delta_beta*tr(G)/t*I; default 1e-6 */
+  float delta_v;         /* relative ridge of the value fit: lambda_v = delta_v*tr(A)/t; default 1e-3 */
+  float eps_w;           /* epsilon_w of eq. mass_fit; default 1e-12 */
+  float b_min, b_max;    /* clip range of beta; default [-30, 30] */
+  int32_t bias_mode;     /* 0 = projected least squares (eq. mass_fit); other values unsupported */
+  int32_t max_escalations; /* ridge x10 retries after a failed Cholesky pivot, 0..6; default 3 */
+  int32_t refine_steps;  /* iterative-refinement steps after each Cholesky solve, 0..4; default 1 */
+  int32_t pair_chunk;    /* pairs processed together by arckv_compact (0 = all B); sizes the workspace */
+} arckv_fit_params;
+
+/* Fill *p with the defaults listed above.  Returns ARCKV_ERR_INVALID_ARG on NULL. */
+arckv_status arckv_default_params(arckv_fit_params *p);
+
+/* Budget t = clip_[1,T](floor(rho*T + 1/2)), computed in double (the paper
+ * rounds the budget by ceil in training, floor per head and round per chunk,
+ * Section 3.5 and Appendix A.2-A.3; round-half-up is this library's reading).
+ * Errors: T < 1, rho not finite or rho < 0, t == NULL. */
+arckv_status arckv_budget(int64_t T, double rho, int32_t *t);
+
+/* Bytes of workspace needed by every entry point below for this problem and
+ * budget (the maximum over stages; arckv_compact with p->pair_chunk pairs in
+ * flight).  p may be NULL (defaults). */
+arckv_status arckv_workspace_size(const arckv_problem *prob, int32_t t,
+                                  const arckv_fit_params *p, size_t *bytes);
+
+/* Stage 1a: token scores I [B][T] (float32), Section 3.3 with the MLP scorer.
+ * No workspace. */
+arckv_status arckv_score(const arckv_problem *prob, const void *K, const void *V,
+                         const arckv_indexer *ix, float *scores, hipStream_t stream);
+
+/* Stage 1b: anchors S = TopK(scores, t) per pair (Section 3.3, eq.
+ * persistent_support), written ascending to anchors [B][t].  Order: larger
+ * score first, ties to the lower index, -0 equal to +0, NaN below every number.
+ * Bit-exact by construction.  Needs 1 <= t <= T. */
+arckv_status arckv_select(const arckv_problem *prob, const float *scores, int32_t t,
+                          int32_t *anchors, void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* Full-cache row statistics (Appendix A.9): with l_ij = s q_i.k_j,
+ *   z [B][n]     z_i = max_j l_ij over the whole cache,
+ *   m [B][n]     m_i = sum_j exp(l_ij - z_i)            (the mass targets Phi_K 1),
+ *   Y [B][n][d]  Y_i = sum_j exp(l_ij - z_i) v_j / m_i   (full attention outputs).
+ * No workspace. */
+arckv_status arckv_rowstats(const arckv_problem *prob, const void *K, const void *V,
+                            const void *Q_ref, float *z, float *m, float *Y, hipStream_t stream);
+
+/* Stage 2: response-profile assignment and convex key merge (Section 3.4,
+ * eq. response_profile, anchor_assignment, mass_centroid, key_merge).
+ *   z        [B][n] row maxima from arckv_rowstats; max_i z_i is z_merge.
+ *   anchors  [B][t] ascending anchor positions.
+ *   C_k      [B][t][d] output; row r is the compact key of anchors[r], a convex
+ *            combination of its group's keys with weights >= 0 summing to 1.
+ *   assign   [B][T] output (may be NULL): the group r of every position;
+ *            anchors are assigned to themselves, ties go to the lowest r.
+ *   phi      [B][T] output (may be NULL): query-averaged mass exp(l - z_merge). */
+arckv_status arckv_merge(const arckv_problem *prob, const void *K, const void *Q_ref,
+                         const float *z, const int32_t *anchors, int32_t t, float lambda_m,
+                         float *C_k, int32_t *assign, float *phi,
+                         void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* Stage 3: mass bias (Appendix A.9, eq. mass_fit).  With
+ * Phi_C = exp(s Q C_k^T - z 1^T): w~ solves (G + delta_beta tr(G)/t I) w = h,
+ * G = Phi_C^T Phi_C, h = Phi_C^T m, by Cholesky (float32, refined);
+ * beta = clip(log max(max(w~, 0), eps_w), b_min, b_max).
+ *   beta  [B][t] output.
+ *   info  [B] output: 0 = ok, k > 0 = Cholesky pivot k failed after all ridge
+ *         escalations (beta is then NaN).
+ *   delta_used [B] output (may be NULL): the relative ridge actually used. */
+arckv_status arckv_fit_bias(const arckv_problem *prob, const void *Q_ref, const float *C_k,
+                            int32_t t, const float *z, const float *m,
+                            const arckv_fit_params *p, float *beta, int32_t *info,
+                            float *delta_used, void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* Stage 4: compact values (Appendix A.9, eq. value_lstsq).  With
+ * P_hat = softmax(s Q C_k^T + 1 beta^T): C_v solves
+ * (A + delta_v tr(A)/t I) C_v = P_hat^T Y, A = P_hat^T P_hat.
+ *   Y     [B][n][d] full-attention outputs from arckv_rowstats.
+ *   C_v   [B][t][d] output.
+ *   info / delta_used as for arckv_fit_bias. */
+arckv_status arckv_fit_values(const arckv_problem *prob, const void *Q_ref, const float *C_k,
+                              const float *beta, int32_t t, const float *Y,
+                              const arckv_fit_params *p, float *C_v, int32_t *info,
+                              float *delta_used, void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* The whole per-context path for B pairs: score, select, row statistics,
+ * merge, mass fit, value fit.  t = arckv_budget(T, rho) is written to *t_out
+ * (host pointer) before any device work.  Outputs: anchors [B][t], C_k [B][t][d],
+ * beta [B][t], C_v [B][t][d], info [B][2] (mass-fit, value-fit status as above).
+ * Pairs are processed p->pair_chunk at a time (0 = all at once). */
+arckv_status arckv_compact(const arckv_problem *prob, const void *K, const void *V,
+                           const void *Q_ref, const arckv_indexer *ix, double rho,
+                           const arckv_fit_params *p, int32_t *t_out, int32_t *anchors,
+                           float *C_k, float *beta, float *C_v, int32_t *info,
+                           void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* Human-readable name of a status code (static string). */
+const char *arckv_status_string(arckv_status s);
+
+/* Instrumentation.  When enabled (non-zero), entry points record HIP events
+ * around each internal kernel stage on the call's stream; arckv_stage_times
+ * then synchronises those events and returns per-stage milliseconds of the
+ * most recent call, accumulated over calls since the last reset.
+ *   names   receives up to max_stages static stage names (may be NULL),
+ *   ms      receives the accumulated milliseconds,
+ *   counts  receives how many launches were timed per stage (may be NULL).
+ * Returns the number of stages via *n_stages.  Not thread-safe. */
+arckv_status arckv_set_timing(int32_t enable);
+arckv_status arckv_stage_times(int32_t max_stages, const char **names, double *ms,
+                               int32_t *counts, int32_t *n_stages);
+arckv_status arckv_reset_timing(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* ARCKV_H */

@@ -1,0 +1,288 @@
+"""Python binding of libarckv.so (ctypes): argument marshalling only.
+
+Every function mirrors the C entry point of the same name in include/arckv.h.
+Tensors must be CUDA (HIP) tensors, contiguous, of the documented dtype; the
+work is enqueued on torch's current stream.  Nothing here computes any part
+of the compaction: if the library is missing, loading fails loudly.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+from typing import Optional
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libarckv.so")
+
+OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP = 0, 1, 2, 3, 4
+F32, BF16 = 0, 1
+
+# Every entry point declared in include/arckv.h.
+ENTRY_POINTS = (
+    "arckv_default_params", "arckv_budget", "arckv_workspace_size", "arckv_score", "arckv_select",
+    "arckv_rowstats", "arckv_merge", "arckv_fit_bias", "arckv_fit_values", "arckv_compact",
+    "arckv_status_string", "arckv_set_timing", "arckv_stage_times", "arckv_reset_timing",
+)
+
+
+class ArckvError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        super().__init__(f"{where}: {status_string(status)} (status {status})")
+        self.status = status
+
+
+class Problem(ctypes.Structure):
+    _fields_ = [("B", ctypes.c_int32), ("T", ctypes.c_int32), ("n", ctypes.c_int32), ("d", ctypes.c_int32),
+                ("dtype", ctypes.c_int32), ("scale", ctypes.c_float)]
+
+
+class Indexer(ctypes.Structure):
+    _fields_ = [("hidden", ctypes.c_int32), ("w1_dtype", ctypes.c_int32), ("W1", ctypes.c_void_p),
+                ("b1", ctypes.c_void_p), ("w2", ctypes.c_void_p), ("b2", ctypes.c_void_p)]
+
+
+class FitParams(ctypes.Structure):
+    _fields_ = [("lambda_m", ctypes.c_float), ("delta_beta", ctypes.c_float), ("delta_v", ctypes.c_float),
+                ("eps_w", ctypes.c_float), ("b_min", ctypes.c_float), ("b_max", ctypes.c_float),
+                ("bias_mode", ctypes.c_int32), ("max_escalations", ctypes.c_int32),
+                ("refine_steps", ctypes.c_int32), ("pair_chunk", ctypes.c_int32)]
+
+
+_LIB = None
+
+
+def lib():
+    """Load libarckv.so (built in-tree by paper_2609_36835_amd.build)."""
+    global _LIB
+    if _LIB is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: run `python -m paper_2609_36835_amd.build` first")
+        L = ctypes.CDLL(LIB_PATH)
+        vp, i32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
+        P = ctypes.POINTER
+        L.arckv_default_params.argtypes = [P(FitParams)]
+        L.arckv_budget.argtypes = [ctypes.c_int64, ctypes.c_double, P(i32)]
+        L.arckv_workspace_size.argtypes = [P(Problem), i32, P(FitParams), P(sz)]
+        L.arckv_score.argtypes = [P(Problem), vp, vp, P(Indexer), vp, vp]
+        L.arckv_select.argtypes = [P(Problem), vp, i32, vp, vp, sz, vp]
+        L.arckv_rowstats.argtypes = [P(Problem), vp, vp, vp, vp, vp, vp, vp]
+        L.arckv_merge.argtypes = [P(Problem), vp, vp, vp, vp, i32, ctypes.c_float, vp, vp, vp, vp, sz, vp]
+        L.arckv_fit_bias.argtypes = [P(Problem), vp, vp, i32, vp, vp, P(FitParams), vp, vp, vp, vp, sz, vp]
+        L.arckv_fit_values.argtypes = [P(Problem), vp, vp, vp, i32, vp, P(FitParams), vp, vp, vp, vp, sz, vp]
+        L.arckv_compact.argtypes = [P(Problem), vp, vp, vp, P(Indexer), ctypes.c_double, P(FitParams), P(i32),
+                                    vp, vp, vp, vp, vp, vp, sz, vp]
+        L.arckv_status_string.argtypes = [ctypes.c_int]
+        L.arckv_status_string.restype = ctypes.c_char_p
+        L.arckv_set_timing.argtypes = [i32]
+        L.arckv_stage_times.argtypes = [i32, P(ctypes.c_char_p), P(ctypes.c_double), P(i32), P(i32)]
+        L.arckv_reset_timing.argtypes = []
+        for name in ENTRY_POINTS:
+            getattr(L, name).restype = ctypes.c_int if name != "arckv_status_string" else ctypes.c_char_p
+        _LIB = L
+    return _LIB
+
+
+def status_string(status: int) -> str:
+    return lib().arckv_status_string(int(status)).decode()
+
+
+def _check(status: int, where: str):
+    if status != OK:
+        raise ArckvError(status, where)
+
+
+def default_params(**overrides) -> FitParams:
+    p = FitParams()
+    _check(lib().arckv_default_params(ctypes.byref(p)), "arckv_default_params")
+    for k, v in overrides.items():
+        if not hasattr(p, k):
+            raise KeyError(k)
+        setattr(p, k, v)
+    return p
+
+
+def budget(T: int, rho: float) -> int:
+    t = ctypes.c_int32()
+    _check(lib().arckv_budget(int(T), float(rho), ctypes.byref(t)), "arckv_budget")
+    return t.value
+
+
+def _dtype_code(dt: torch.dtype) -> int:
+    if dt == torch.bfloat16:
+        return BF16
+    if dt == torch.float32:
+        return F32
+    raise TypeError(f"unsupported dtype {dt}")
+
+
+def problem(K: torch.Tensor, Q: torch.Tensor, scale: Optional[float] = None) -> Problem:
+    B, T, d = K.shape
+    n = Q.shape[1]
+    return Problem(B, T, n, d, _dtype_code(K.dtype), float(scale) if scale else 0.0)
+
+
+def problem_from_dims(B: int, T: int, n: int, d: int = 128, dtype: int = BF16, scale: float = 0.0) -> Problem:
+    return Problem(B, T, n, d, dtype, scale)
+
+
+def workspace_size(prob: Problem, t: int, params: Optional[FitParams] = None) -> int:
+    out = ctypes.c_size_t()
+    pp = ctypes.byref(params) if params is not None else None
+    _check(lib().arckv_workspace_size(ctypes.byref(prob), int(t), pp, ctypes.byref(out)), "arckv_workspace_size")
+    return out.value
+
+
+def _ptr(x: Optional[torch.Tensor]):
+    if x is None:
+        return None
+    if not x.is_cuda:
+        raise ValueError("tensors must live on the GPU")
+    if not x.is_contiguous():
+        raise ValueError("tensors must be contiguous")
+    return ctypes.c_void_p(x.data_ptr())
+
+
+def _stream():
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _workspace(nbytes: int, device) -> torch.Tensor:
+    ws = torch.empty(max(nbytes, 256) + 256, dtype=torch.uint8, device=device)
+    off = (-ws.data_ptr()) % 256
+    return ws[off:off + max(nbytes, 256)]
+
+
+def indexer(W1, b1, w2, b2) -> Indexer:
+    return Indexer(W1.shape[1], _dtype_code(W1.dtype), _ptr(W1), _ptr(b1), _ptr(w2), _ptr(b2))
+
+
+def score(K, V, W1, b1, w2, b2, scale=None) -> torch.Tensor:
+    prob = problem(K, K[:, :1], scale)
+    out = torch.empty(K.shape[0], K.shape[1], dtype=torch.float32, device=K.device)
+    ix = indexer(W1, b1, w2, b2)
+    _check(lib().arckv_score(ctypes.byref(prob), _ptr(K), _ptr(V), ctypes.byref(ix), _ptr(out), _stream()),
+           "arckv_score")
+    return out
+
+
+def select(scores: torch.Tensor, t: int) -> torch.Tensor:
+    B, T = scores.shape
+    prob = Problem(B, T, 1, 128, F32, 0.0)
+    out = torch.empty(B, t, dtype=torch.int32, device=scores.device)
+    _check(lib().arckv_select(ctypes.byref(prob), _ptr(scores), int(t), _ptr(out), None, 0, _stream()),
+           "arckv_select")
+    return out
+
+
+def rowstats(K, V, Q, scale=None):
+    prob = problem(K, Q, scale)
+    B, n = Q.shape[0], Q.shape[1]
+    z = torch.empty(B, n, dtype=torch.float32, device=K.device)
+    m = torch.empty_like(z)
+    Y = torch.empty(B, n, K.shape[2], dtype=torch.float32, device=K.device)
+    _check(lib().arckv_rowstats(ctypes.byref(prob), _ptr(K), _ptr(V), _ptr(Q), _ptr(z), _ptr(m), _ptr(Y),
+                                _stream()), "arckv_rowstats")
+    return z, m, Y
+
+
+def merge(K, Q, z, anchors, lambda_m=0.25, scale=None, ws_bytes: Optional[int] = None):
+    prob = problem(K, Q, scale)
+    t = anchors.shape[1]
+    B, T, d = K.shape
+    Ck = torch.empty(B, t, d, dtype=torch.float32, device=K.device)
+    kappa = torch.empty(B, T, dtype=torch.int32, device=K.device)
+    phi = torch.empty(B, T, dtype=torch.float32, device=K.device)
+    nbytes = ws_bytes if ws_bytes is not None else workspace_size(prob, t)
+    ws = _workspace(nbytes, K.device)
+    _check(lib().arckv_merge(ctypes.byref(prob), _ptr(K), _ptr(Q), _ptr(z), _ptr(anchors), int(t), float(lambda_m),
+                             _ptr(Ck), _ptr(kappa), _ptr(phi), _ptr(ws), nbytes, _stream()), "arckv_merge")
+    return Ck, kappa, phi
+
+
+def fit_bias(Q, C_k, z, m, params: Optional[FitParams] = None, scale=None, T: Optional[int] = None):
+    B, n, d = Q.shape
+    t = C_k.shape[1]
+    prob = Problem(B, T or max(t, 1), n, d, _dtype_code(Q.dtype), float(scale) if scale else 0.0)
+    params = params or default_params()
+    beta = torch.empty(B, t, dtype=torch.float32, device=Q.device)
+    info = torch.empty(B, dtype=torch.int32, device=Q.device)
+    dused = torch.empty(B, dtype=torch.float32, device=Q.device)
+    nbytes = workspace_size(prob, t, params)
+    ws = _workspace(nbytes, Q.device)
+    _check(lib().arckv_fit_bias(ctypes.byref(prob), _ptr(Q), _ptr(C_k), int(t), _ptr(z), _ptr(m),
+                                ctypes.byref(params), _ptr(beta), _ptr(info), _ptr(dused), _ptr(ws), nbytes,
+                                _stream()), "arckv_fit_bias")
+    return beta, info, dused
+
+
+def fit_values(Q, C_k, beta, Y, params: Optional[FitParams] = None, scale=None, T: Optional[int] = None):
+    B, n, d = Q.shape
+    t = C_k.shape[1]
+    prob = Problem(B, T or max(t, 1), n, d, _dtype_code(Q.dtype), float(scale) if scale else 0.0)
+    params = params or default_params()
+    Cv = torch.empty(B, t, d, dtype=torch.float32, device=Q.device)
+    info = torch.empty(B, dtype=torch.int32, device=Q.device)
+    dused = torch.empty(B, dtype=torch.float32, device=Q.device)
+    nbytes = workspace_size(prob, t, params)
+    ws = _workspace(nbytes, Q.device)
+    _check(lib().arckv_fit_values(ctypes.byref(prob), _ptr(Q), _ptr(C_k), _ptr(beta), int(t), _ptr(Y),
+                                  ctypes.byref(params), _ptr(Cv), _ptr(info), _ptr(dused), _ptr(ws), nbytes,
+                                  _stream()), "arckv_fit_values")
+    return Cv, info, dused
+
+
+class Compactor:
+    """Holds output buffers and the workspace for repeated arckv_compact calls."""
+
+    def __init__(self, B, T, n, rho, dtype=torch.bfloat16, device="cuda", scale=None,
+                 params: Optional[FitParams] = None):
+        self.prob = Problem(B, T, n, 128, _dtype_code(dtype), float(scale) if scale else 0.0)
+        self.rho = float(rho)
+        self.params = params or default_params()
+        self.t = budget(T, rho)
+        dev = torch.device(device)
+        self.anchors = torch.empty(B, self.t, dtype=torch.int32, device=dev)
+        self.C_k = torch.empty(B, self.t, 128, dtype=torch.float32, device=dev)
+        self.beta = torch.empty(B, self.t, dtype=torch.float32, device=dev)
+        self.C_v = torch.empty(B, self.t, 128, dtype=torch.float32, device=dev)
+        self.info = torch.empty(B, 2, dtype=torch.int32, device=dev)
+        self.ws_bytes = workspace_size(self.prob, self.t, self.params)
+        self.ws = _workspace(self.ws_bytes, dev)
+
+    def __call__(self, K, V, Q, W1, b1, w2, b2):
+        ix = indexer(W1, b1, w2, b2)
+        t_out = ctypes.c_int32()
+        _check(lib().arckv_compact(ctypes.byref(self.prob), _ptr(K), _ptr(V), _ptr(Q), ctypes.byref(ix), self.rho,
+                                   ctypes.byref(self.params), ctypes.byref(t_out), _ptr(self.anchors),
+                                   _ptr(self.C_k), _ptr(self.beta), _ptr(self.C_v), _ptr(self.info),
+                                   _ptr(self.ws), self.ws_bytes, _stream()), "arckv_compact")
+        assert t_out.value == self.t
+        return self.anchors, self.C_k, self.beta, self.C_v, self.info
+
+
+def compact(K, V, Q, W1, b1, w2, b2, rho, scale=None, params: Optional[FitParams] = None):
+    """One-shot arckv_compact: returns (anchors, C_k, beta, C_v, info)."""
+    B, T, _ = K.shape
+    c = Compactor(B, T, Q.shape[1], rho, K.dtype, K.device, scale, params)
+    return c(K, V, Q, W1, b1, w2, b2)
+
+
+def set_timing(enable: bool):
+    _check(lib().arckv_set_timing(1 if enable else 0), "arckv_set_timing")
+
+
+def reset_timing():
+    _check(lib().arckv_reset_timing(), "arckv_reset_timing")
+
+
+def stage_times() -> dict:
+    n = 64
+    names = (ctypes.c_char_p * n)()
+    ms = (ctypes.c_double * n)()
+    cnt = (ctypes.c_int32 * n)()
+    ns = ctypes.c_int32()
+    _check(lib().arckv_stage_times(n, names, ms, cnt, ctypes.byref(ns)), "arckv_stage_times")
+    return {names[i].decode(): (ms[i], cnt[i]) for i in range(ns.value)}

@@ -1,0 +1,683 @@
+// Host side of the ARC-KV library: argument validation (before any HIP call),
+// workspace planning, and stage sequencing on the caller's stream.
+#include <math.h>
+#include <mutex>
+#include <stdint.h>
+#include <string.h>
+#include <vector>
+
+#include <hip/hip_runtime.h>
+
+#include "arckv.h"
+
+namespace arckv {
+constexpr int kHeadDimH = 128;
+constexpr int64_t kPadH = 256;
+inline int64_t rup(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
+
+struct FitState {
+  double *trace;
+  float *lam;
+  float *delta;
+  int32_t *info;
+};
+
+hipError_t launch_score(int dtype, const void *K, const void *V, const void *W1, const float *b1, const float *w2,
+                        const float *b2, float *scores, int B, int T, hipStream_t s);
+hipError_t launch_select(const float *scores, int B, int T, int t, int32_t *anchors, int32_t *anchor_of,
+                         hipStream_t s);
+hipError_t launch_rowstats(int dtype, const void *K, const void *V, const void *Q, float *z, float *m, float *Y,
+                           int B, int T, int n, float scale, hipStream_t s);
+hipError_t launch_profiles(int dtype, const void *Q, const void *K, const float *zmerge, void *Et, float *phi,
+                           int B, int T, int n, int64_t Tp, int64_t np_, float scale, hipStream_t s);
+hipError_t launch_phic(int dtype, const void *Q, const void *Ckp, const float *z, void *PhiT, float *LT, int B, int t,
+                       int n, int64_t tp, int64_t np_, float scale, hipStream_t s);
+hipError_t launch_zmax(const float *z, int B, int n, float *zmax, hipStream_t s);
+hipError_t launch_anchor_of(const int32_t *anchors, int B, int T, int t, int32_t *anchor_of, hipStream_t s);
+hipError_t launch_anchor_profiles(int dtype, const void *Et, const int32_t *anchors, void *U, int B, int t,
+                                  int64_t Tp, int64_t np_, int64_t tp, hipStream_t s);
+hipError_t launch_assign_finalize(const uint64_t *part, int MT, int64_t Np, const int32_t *anchor_of, int B, int T,
+                                  int32_t *kappa, hipStream_t s);
+hipError_t launch_group_merge(int dtype, const void *K, const float *phi, const int32_t *kappa,
+                              const int32_t *anchors, int B, int T, int t, int64_t tp, float lambda,
+                              int32_t *offsets, int32_t *cursor, int32_t *perm, float *Ck, void *Ckp, hipStream_t s);
+hipError_t launch_assign_gemm(int dtype, const void *U, const void *Et, uint64_t *part, int P, int t, int64_t tp,
+                              int64_t Tp, int64_t np_, hipStream_t s);
+hipError_t launch_gram(int dtype, const void *X, float *G, float *Gc, int P, int64_t tp, int64_t np_, hipStream_t s);
+hipError_t launch_rhs_gemm(int dtype, const void *PT, const void *YT, float *Bm, int P, int64_t tp, int64_t np_,
+                           hipStream_t s);
+hipError_t launch_value_residual(const float *Gc, const float *XT, const float *Bm, const float *X,
+                                 const float *lam, float *R, int P, int64_t tp, hipStream_t s);
+hipError_t launch_hvec(const float *LT, const float *z, const float *m, int B, int n, int t, int64_t tp, int64_t np_,
+                       double *h, hipStream_t s);
+hipError_t launch_cholesky(float *Gw, const float *Gc, int B, int t, int64_t ld, float delta0, int max_esc,
+                           FitState st, hipStream_t s);
+hipError_t launch_trsv(const float *Gw, int B, int64_t ld, const double *rhs, double *y, double *x, double *acc,
+                       const int32_t *info, hipStream_t s);
+hipError_t launch_residual_vec(const float *Gc, int B, int64_t ld, int t, const double *rhs, const double *x,
+                               const float *lam, double *res, const int32_t *info, hipStream_t s);
+hipError_t launch_bias_finalize(const double *w, int B, int64_t ld, int t, float eps, float bmin, float bmax,
+                                const int32_t *info, float *beta, float *beta_ws, hipStream_t s);
+hipError_t launch_phat(int dtype, const float *LT, const float *beta_ws, int B, int n, int t, int64_t tp,
+                       int64_t np_, void *out, hipStream_t s);
+hipError_t launch_transpose128(int dtype, const float *in, int B, int rows, int64_t in_pair, int64_t rows_pad,
+                               void *out, int64_t out_pair, hipStream_t s);
+hipError_t launch_trsm(bool fwd, const float *Gw, int B, int64_t ld, const float *R, float *X, const int32_t *info,
+                       hipStream_t s);
+hipError_t launch_add(float *x, const float *dx, int B, int64_t n_per, const int32_t *info, hipStream_t s);
+hipError_t launch_values_out(const float *Xp, int B, int64_t tp, int t, const int32_t *info, float *Cv,
+                             hipStream_t s);
+hipError_t launch_copy_info(const int32_t *a, const int32_t *b, int B, int32_t *info, hipStream_t s);
+hipError_t launch_copy_f32(const float *src, float *dst, int B, hipStream_t s);
+
+// ------------------------------------------------------------------ timing
+enum Stage {
+  ST_SCORE, ST_SELECT, ST_ROWSTATS, ST_ZMAX, ST_PROFILES, ST_ANCHOR_PROF, ST_ASSIGN, ST_FINALIZE, ST_MERGE,
+  ST_PHIC, ST_GRAM_G, ST_HVEC, ST_CHOL_G, ST_SOLVE_W, ST_PHAT, ST_GRAM_A, ST_RHS, ST_CHOL_A, ST_SOLVE_V,
+  ST_COUNT
+};
+static const char *kStageNames[ST_COUNT] = {
+    "score", "select", "rowstats", "zmax", "profiles", "anchor_profiles", "assign_gemm", "assign_finalize",
+    "merge", "phic", "gram_G", "hvec", "chol_G", "solve_beta", "phat", "gram_A", "rhs_B", "chol_A", "solve_values"};
+
+struct TimingState {
+  std::mutex mu;
+  bool enabled = false;
+  struct Rec { int stage; hipEvent_t a, b; };
+  std::vector<Rec> pending;
+  std::vector<hipEvent_t> pool;
+  double ms[ST_COUNT] = {0};
+  int32_t cnt[ST_COUNT] = {0};
+};
+static TimingState g_timing;
+
+static hipEvent_t take_event() {
+  if (!g_timing.pool.empty()) {
+    hipEvent_t e = g_timing.pool.back();
+    g_timing.pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+struct StageScope {
+  int stage;
+  hipStream_t s;
+  hipEvent_t a = nullptr, b = nullptr;
+  StageScope(int st, hipStream_t str) : stage(st), s(str) {
+    if (!g_timing.enabled) return;
+    std::lock_guard<std::mutex> lk(g_timing.mu);
+    a = take_event();
+    b = take_event();
+    if (a) hipEventRecord(a, s);
+  }
+  ~StageScope() {
+    if (!a || !b) return;
+    hipEventRecord(b, s);
+    std::lock_guard<std::mutex> lk(g_timing.mu);
+    g_timing.pending.push_back({stage, a, b});
+  }
+};
+#define STAGE(id, expr)                              \
+  do {                                               \
+    StageScope _sc(id, stream);                      \
+    if ((expr) != hipSuccess) return ARCKV_ERR_HIP;  \
+  } while (0)
+
+// ------------------------------------------------------------------ workspace plan
+struct Dims {
+  int B, T, n, t, dtype;
+  int64_t Tp, np_, tp, MT;
+  int64_t esz;   // bytes per element of E^T / U_S
+};
+
+static Dims make_dims(const arckv_problem *p, int t) {
+  Dims d;
+  d.B = p->B;
+  d.T = p->T;
+  d.n = p->n;
+  d.t = t;
+  d.dtype = p->dtype;
+  d.Tp = rup(p->T, kPadH);
+  d.np_ = rup(p->n, kPadH);
+  d.tp = rup(t, kPadH);
+  d.MT = d.tp / 128;
+  d.esz = p->dtype == ARCKV_BF16 ? 2 : 4;
+  return d;
+}
+
+struct Bump {
+  int64_t off = 0;
+  int64_t take(int64_t bytes) {
+    int64_t o = off;
+    off += rup(bytes, 256);
+    return o;
+  }
+};
+
+// Persistent per-pair arrays ([B]-sized) followed by a chunk region for P pairs.
+struct Plan {
+  // persistent
+  int64_t scores, z, m, Y, zmax, anchor_of, kappa, phi, beta_ws, info_g, info_a, st_g, st_a;
+  int64_t persistent_bytes;
+  // chunk region (offsets relative to chunk base)
+  int64_t Ckp;
+  int64_t Et, U, part, offsets, cursor, perm;            // merge phase
+  int64_t PhiT, LT, Gw, Gc, h, w, y, x, res, YT, Bm, X, R, Y2, XT;  // fit phase
+  int64_t chunk_bytes;
+};
+
+static Plan make_plan(const Dims &d, int64_t P) {
+  Plan pl;
+  Bump a;
+  const int64_t B = d.B;
+  pl.scores = a.take(B * d.T * 4);
+  pl.z = a.take(B * d.n * 4);
+  pl.m = a.take(B * d.n * 4);
+  pl.Y = a.take(B * d.n * kHeadDimH * 4);
+  pl.zmax = a.take(B * 4);
+  pl.anchor_of = a.take(B * d.T * 4);
+  pl.kappa = a.take(B * d.T * 4);
+  pl.phi = a.take(B * d.T * 4);
+  pl.beta_ws = a.take(B * d.tp * 4);
+  pl.info_g = a.take(B * 4);
+  pl.info_a = a.take(B * 4);
+  pl.st_g = a.take(B * 16);    // trace (8) + lam (4) + delta (4)
+  pl.st_a = a.take(B * 16);
+  pl.persistent_bytes = a.off;
+
+  Bump c;
+  pl.Ckp = c.take(P * d.tp * kHeadDimH * 4);
+  const int64_t phase0 = c.off;
+  Bump m = c;
+  pl.Et = m.take(P * d.Tp * d.np_ * d.esz);
+  pl.U = m.take(P * d.tp * d.np_ * d.esz);
+  pl.part = m.take(P * d.MT * d.Tp * 8);
+  pl.offsets = m.take(P * (int64_t)(d.t + 1) * 4);
+  pl.cursor = m.take(P * (int64_t)d.t * 4);
+  pl.perm = m.take(P * (int64_t)d.T * 4);
+  Bump f = c;
+  pl.PhiT = f.take(P * d.tp * d.np_ * 4);   // two bf16 planes or one fp32 plane
+  pl.LT = f.take(P * d.tp * d.np_ * 4);
+  pl.Gw = f.take(P * d.tp * d.tp * 4);
+  pl.Gc = f.take(P * d.tp * d.tp * 4);
+  pl.h = f.take(P * d.tp * 8);
+  pl.w = f.take(P * d.tp * 8);
+  pl.y = f.take(P * d.tp * 8);
+  pl.x = f.take(P * d.tp * 8);
+  pl.res = f.take(P * d.tp * 8);
+  pl.YT = f.take(P * kHeadDimH * d.np_ * 4);
+  pl.Bm = f.take(P * d.tp * kHeadDimH * 4);
+  pl.X = f.take(P * d.tp * kHeadDimH * 4);
+  pl.R = f.take(P * d.tp * kHeadDimH * 4);
+  pl.Y2 = f.take(P * d.tp * kHeadDimH * 4);
+  pl.XT = f.take(P * d.tp * kHeadDimH * 4);
+  (void)phase0;
+  pl.chunk_bytes = m.off > f.off ? m.off : f.off;
+  return pl;
+}
+
+static size_t plan_total(const Dims &d, int64_t P) {
+  Plan pl = make_plan(d, P);
+  return (size_t)(pl.persistent_bytes + pl.chunk_bytes);
+}
+
+// Largest chunk of pairs that fits the workspace (0 if not even one).
+static int64_t chunk_for(const Dims &d, size_t ws_bytes, int64_t want) {
+  const size_t one = plan_total(d, 1);
+  if (ws_bytes < one) return 0;
+  const size_t per = plan_total(d, 2) - one;
+  int64_t P = 1 + (int64_t)((ws_bytes - one) / (per ? per : 1));
+  if (want > 0 && P > want) P = want;
+  if (P > d.B) P = d.B;
+  while (P > 1 && plan_total(d, P) > ws_bytes) --P;
+  return P;
+}
+
+// ------------------------------------------------------------------ validation
+static bool aligned(const void *p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+static arckv_status check_problem(const arckv_problem *p) {
+  if (!p) return ARCKV_ERR_INVALID_ARG;
+  if (p->B < 1 || p->T < 1 || p->n < 1) return ARCKV_ERR_INVALID_ARG;
+  if (p->d != kHeadDimH) return ARCKV_ERR_UNSUPPORTED;
+  if (p->dtype != ARCKV_F32 && p->dtype != ARCKV_BF16) return ARCKV_ERR_UNSUPPORTED;
+  if (!isfinite(p->scale)) return ARCKV_ERR_INVALID_ARG;
+  if ((int64_t)p->T > (1ll << 30) || (int64_t)p->n > (1ll << 30)) return ARCKV_ERR_UNSUPPORTED;
+  return ARCKV_OK;
+}
+
+static arckv_status check_params(const arckv_fit_params *p) {
+  if (!p) return ARCKV_ERR_INVALID_ARG;
+  if (!(p->lambda_m >= 0.0f && p->lambda_m <= 1.0f)) return ARCKV_ERR_INVALID_ARG;
+  if (!(p->delta_beta >= 0.0f) || !isfinite(p->delta_beta)) return ARCKV_ERR_INVALID_ARG;
+  if (!(p->delta_v >= 0.0f) || !isfinite(p->delta_v)) return ARCKV_ERR_INVALID_ARG;
+  if (!(p->eps_w > 0.0f) || !isfinite(p->eps_w)) return ARCKV_ERR_INVALID_ARG;
+  if (!(p->b_min <= p->b_max) || !isfinite(p->b_min) || !isfinite(p->b_max)) return ARCKV_ERR_INVALID_ARG;
+  if (p->bias_mode != 0) return ARCKV_ERR_UNSUPPORTED;
+  if (p->max_escalations < 0 || p->max_escalations > 6) return ARCKV_ERR_INVALID_ARG;
+  if (p->refine_steps < 0 || p->refine_steps > 4) return ARCKV_ERR_INVALID_ARG;
+  if (p->pair_chunk < 0) return ARCKV_ERR_INVALID_ARG;
+  return ARCKV_OK;
+}
+
+static float eff_scale(const arckv_problem *p) {
+  return p->scale > 0.0f ? p->scale : 1.0f / sqrtf((float)p->d);
+}
+
+static arckv_status check_ws(const Dims &d, void *ws, size_t ws_bytes, int64_t want, int64_t *P) {
+  if (!ws || !aligned(ws, 256)) return ARCKV_ERR_WORKSPACE;
+  *P = chunk_for(d, ws_bytes, want);
+  return *P >= 1 ? ARCKV_OK : ARCKV_ERR_WORKSPACE;
+}
+
+#define CHECK(x)                              \
+  do {                                        \
+    arckv_status _s = (x);                    \
+    if (_s != ARCKV_OK) return _s;            \
+  } while (0)
+
+// ------------------------------------------------------------------ stage bodies
+struct Ctx {
+  Dims d;
+  Plan pl;
+  char *ws;
+  float scale;
+  hipStream_t stream;
+  template <typename T> T *pers(int64_t off) const { return reinterpret_cast<T *>(ws + off); }
+  template <typename T> T *chunk(int64_t off) const { return reinterpret_cast<T *>(ws + pl.persistent_bytes + off); }
+  int64_t in_esz() const { return d.dtype == ARCKV_BF16 ? 2 : 4; }
+};
+
+// Merge stage for pairs [b0, b0+P): needs zmax and anchor_of for those pairs.
+static arckv_status run_merge_chunk(const Ctx &c, int b0, int P, const void *K, const void *Q,
+                                    const int32_t *anchors, float lambda_m, float *Ck, int32_t *kappa, float *phi,
+                                    const float *zmax, const int32_t *anchor_of) {
+  const Dims &d = c.d;
+  hipStream_t stream = c.stream;
+  const char *Kc = (const char *)K + (size_t)b0 * d.T * kHeadDimH * c.in_esz();
+  const char *Qc = (const char *)Q + (size_t)b0 * d.n * kHeadDimH * c.in_esz();
+  const int32_t *anc = anchors + (size_t)b0 * d.t;
+  void *Et = c.chunk<char>(c.pl.Et);
+  void *U = c.chunk<char>(c.pl.U);
+  uint64_t *part = c.chunk<uint64_t>(c.pl.part);
+  STAGE(ST_PROFILES, launch_profiles(d.dtype, Qc, Kc, zmax + b0, Et, phi + (size_t)b0 * d.T, P, d.T, d.n, d.Tp,
+                                     d.np_, c.scale, stream));
+  STAGE(ST_ANCHOR_PROF, launch_anchor_profiles(d.dtype, Et, anc, U, P, d.t, d.Tp, d.np_, d.tp, stream));
+  STAGE(ST_ASSIGN, launch_assign_gemm(d.dtype, U, Et, part, P, d.t, d.tp, d.Tp, d.np_, stream));
+  STAGE(ST_FINALIZE, launch_assign_finalize(part, (int)d.MT, d.Tp, anchor_of + (size_t)b0 * d.T, P, d.T,
+                                            kappa + (size_t)b0 * d.T, stream));
+  STAGE(ST_MERGE, launch_group_merge(d.dtype, Kc, phi + (size_t)b0 * d.T, kappa + (size_t)b0 * d.T, anc, P, d.T,
+                                     d.t, d.tp, lambda_m, c.chunk<int32_t>(c.pl.offsets),
+                                     c.chunk<int32_t>(c.pl.cursor), c.chunk<int32_t>(c.pl.perm),
+                                     Ck + (size_t)b0 * d.t * kHeadDimH, c.chunk<char>(c.pl.Ckp), stream));
+  return ARCKV_OK;
+}
+
+// Padded compact-key operand copy for pairs [b0, b0+P) from a user C_k.
+hipError_t launch_pad_ck(int dtype, const float *Ck, int P, int t, int64_t tp, void *Ckp, hipStream_t s);
+
+static FitState fit_state(const Ctx &c, int64_t st_off, int64_t info_off, int b0) {
+  FitState st;
+  char *base = c.pers<char>(st_off);
+  const int B = c.d.B;
+  st.trace = reinterpret_cast<double *>(base) + b0;
+  st.lam = reinterpret_cast<float *>(base + (size_t)B * 8) + b0;
+  st.delta = reinterpret_cast<float *>(base + (size_t)B * 12) + b0;
+  st.info = c.pers<int32_t>(info_off) + b0;
+  return st;
+}
+
+// Mass fit for pairs [b0, b0+P): needs Ckp (chunk), z, m.
+static arckv_status run_fit_bias_chunk(const Ctx &c, int b0, int P, const void *Q, const float *z, const float *m,
+                                       const arckv_fit_params &fp, float *beta, FitState st) {
+  const Dims &d = c.d;
+  hipStream_t stream = c.stream;
+  const char *Qc = (const char *)Q + (size_t)b0 * d.n * kHeadDimH * c.in_esz();
+  const float *zc = z + (size_t)b0 * d.n, *mc = m + (size_t)b0 * d.n;
+  void *PhiT = c.chunk<char>(c.pl.PhiT);
+  float *LT = c.chunk<float>(c.pl.LT), *Gw = c.chunk<float>(c.pl.Gw), *Gc = c.chunk<float>(c.pl.Gc);
+  double *h = c.chunk<double>(c.pl.h), *w = c.chunk<double>(c.pl.w), *y = c.chunk<double>(c.pl.y);
+  double *x = c.chunk<double>(c.pl.x), *res = c.chunk<double>(c.pl.res);
+  STAGE(ST_PHIC, launch_phic(d.dtype, Qc, c.chunk<char>(c.pl.Ckp), zc, PhiT, LT, P, d.t, d.n, d.tp, d.np_, c.scale,
+                             stream));
+  STAGE(ST_GRAM_G, launch_gram(d.dtype, PhiT, Gw, Gc, P, d.tp, d.np_, stream));
+  STAGE(ST_HVEC, launch_hvec(LT, zc, mc, P, d.n, d.t, d.tp, d.np_, h, stream));
+  STAGE(ST_CHOL_G, launch_cholesky(Gw, Gc, P, d.t, d.tp, fp.delta_beta, fp.max_escalations, st, stream));
+  {
+    StageScope _sc(ST_SOLVE_W, stream);
+    if (launch_trsv(Gw, P, d.tp, h, y, w, nullptr, st.info, stream) != hipSuccess) return ARCKV_ERR_HIP;
+    for (int it = 0; it < fp.refine_steps; ++it) {
+      if (launch_residual_vec(Gc, P, d.tp, d.t, h, w, st.lam, res, st.info, stream) != hipSuccess) return ARCKV_ERR_HIP;
+      if (launch_trsv(Gw, P, d.tp, res, y, x, w, st.info, stream) != hipSuccess) return ARCKV_ERR_HIP;
+    }
+    if (launch_bias_finalize(w, P, d.tp, d.t, fp.eps_w, fp.b_min, fp.b_max, st.info, beta + (size_t)b0 * d.t,
+                             c.pers<float>(c.pl.beta_ws) + (size_t)b0 * d.tp, stream) != hipSuccess)
+      return ARCKV_ERR_HIP;
+  }
+  return ARCKV_OK;
+}
+
+hipError_t launch_pad_beta(const float *beta, int P, int t, int64_t tp, float *beta_ws, hipStream_t s);
+
+// Value fit for pairs [b0, b0+P): needs LT (from the mass fit, or recomputed),
+// beta_ws, Y.
+static arckv_status run_fit_values_chunk(const Ctx &c, int b0, int P, const float *Y, const arckv_fit_params &fp,
+                                         float *Cv, FitState st) {
+  const Dims &d = c.d;
+  hipStream_t stream = c.stream;
+  void *PT = c.chunk<char>(c.pl.PhiT);
+  float *LT = c.chunk<float>(c.pl.LT), *Gw = c.chunk<float>(c.pl.Gw), *Gc = c.chunk<float>(c.pl.Gc);
+  void *YT = c.chunk<char>(c.pl.YT);
+  float *Bm = c.chunk<float>(c.pl.Bm), *X = c.chunk<float>(c.pl.X), *R = c.chunk<float>(c.pl.R);
+  float *Y2 = c.chunk<float>(c.pl.Y2), *XT = c.chunk<float>(c.pl.XT);
+  const int64_t yt_pair = (d.dtype == ARCKV_BF16 ? 2 : 1) * (int64_t)kHeadDimH * d.np_;
+  STAGE(ST_PHAT, launch_phat(d.dtype, LT, c.pers<float>(c.pl.beta_ws) + (size_t)b0 * d.tp, P, d.n, d.t, d.tp,
+                             d.np_, PT, stream));
+  STAGE(ST_GRAM_A, launch_gram(d.dtype, PT, Gw, Gc, P, d.tp, d.np_, stream));
+  {
+    StageScope _sc(ST_RHS, stream);
+    if (launch_transpose128(d.dtype, Y + (size_t)b0 * d.n * kHeadDimH, P, d.n, (int64_t)d.n * kHeadDimH, d.np_, YT,
+                            yt_pair, stream) != hipSuccess)
+      return ARCKV_ERR_HIP;
+    if (launch_rhs_gemm(d.dtype, PT, YT, Bm, P, d.tp, d.np_, stream) != hipSuccess) return ARCKV_ERR_HIP;
+  }
+  STAGE(ST_CHOL_A, launch_cholesky(Gw, Gc, P, d.t, d.tp, fp.delta_v, fp.max_escalations, st, stream));
+  {
+    StageScope _sc(ST_SOLVE_V, stream);
+    if (launch_trsm(true, Gw, P, d.tp, Bm, Y2, st.info, stream) != hipSuccess) return ARCKV_ERR_HIP;
+    if (launch_trsm(false, Gw, P, d.tp, Y2, X, st.info, stream) != hipSuccess) return ARCKV_ERR_HIP;
+    for (int it = 0; it < fp.refine_steps; ++it) {
+      if (launch_transpose128(ARCKV_F32, X, P, (int)d.tp, d.tp * kHeadDimH, d.tp, XT, d.tp * kHeadDimH, stream) !=
+          hipSuccess)
+        return ARCKV_ERR_HIP;
+      if (launch_value_residual(Gc, XT, Bm, X, st.lam, R, P, d.tp, stream) != hipSuccess) return ARCKV_ERR_HIP;
+      if (launch_trsm(true, Gw, P, d.tp, R, Y2, st.info, stream) != hipSuccess) return ARCKV_ERR_HIP;
+      if (launch_trsm(false, Gw, P, d.tp, Y2, R, st.info, stream) != hipSuccess) return ARCKV_ERR_HIP;
+      if (launch_add(X, R, P, d.tp * kHeadDimH, st.info, stream) != hipSuccess) return ARCKV_ERR_HIP;
+    }
+    if (launch_values_out(X, P, d.tp, d.t, st.info, Cv + (size_t)b0 * d.t * kHeadDimH, stream) != hipSuccess)
+      return ARCKV_ERR_HIP;
+  }
+  return ARCKV_OK;
+}
+
+}  // namespace arckv
+
+using namespace arckv;
+
+// ====================================================================== C ABI
+extern "C" {
+
+arckv_status arckv_default_params(arckv_fit_params *p) {
+  if (!p) return ARCKV_ERR_INVALID_ARG;
+  p->lambda_m = 0.25f;
+  p->delta_beta = 1e-6f;
+  p->delta_v = 1e-3f;
+  p->eps_w = 1e-12f;
+  p->b_min = -30.0f;
+  p->b_max = 30.0f;
+  p->bias_mode = 0;
+  p->max_escalations = 3;
+  p->refine_steps = 1;
+  p->pair_chunk = 0;
+  return ARCKV_OK;
+}
+
+arckv_status arckv_budget(int64_t T, double rho, int32_t *t) {
+  if (!t || T < 1 || !isfinite(rho) || rho < 0.0) return ARCKV_ERR_INVALID_ARG;
+  if (T > (1ll << 30)) return ARCKV_ERR_UNSUPPORTED;
+  double v = floor(rho * (double)T + 0.5);
+  if (v < 1.0) v = 1.0;
+  if (v > (double)T) v = (double)T;
+  *t = (int32_t)v;
+  return ARCKV_OK;
+}
+
+arckv_status arckv_workspace_size(const arckv_problem *prob, int32_t t, const arckv_fit_params *p, size_t *bytes) {
+  CHECK(check_problem(prob));
+  if (!bytes || t < 1 || t > prob->T) return ARCKV_ERR_INVALID_ARG;
+  arckv_fit_params def;
+  arckv_default_params(&def);
+  if (!p) p = &def;
+  CHECK(check_params(p));
+  Dims d = make_dims(prob, t);
+  int64_t P = p->pair_chunk > 0 && p->pair_chunk < d.B ? p->pair_chunk : d.B;
+  *bytes = plan_total(d, P);
+  return ARCKV_OK;
+}
+
+arckv_status arckv_score(const arckv_problem *prob, const void *K, const void *V, const arckv_indexer *ix,
+                         float *scores, hipStream_t stream) {
+  CHECK(check_problem(prob));
+  if (!K || !V || !ix || !scores || !ix->W1 || !ix->b1 || !ix->w2 || !ix->b2) return ARCKV_ERR_INVALID_ARG;
+  if (ix->hidden != 64) return ARCKV_ERR_UNSUPPORTED;
+  if (ix->w1_dtype != prob->dtype) return ARCKV_ERR_UNSUPPORTED;
+  if (!aligned(K, 16) || !aligned(V, 16) || !aligned(ix->W1, 16)) return ARCKV_ERR_INVALID_ARG;
+  STAGE(ST_SCORE, launch_score(prob->dtype, K, V, ix->W1, ix->b1, ix->w2, ix->b2, scores, prob->B, prob->T, stream));
+  return ARCKV_OK;
+}
+
+arckv_status arckv_select(const arckv_problem *prob, const float *scores, int32_t t, int32_t *anchors, void *ws,
+                          size_t ws_bytes, hipStream_t stream) {
+  CHECK(check_problem(prob));
+  if (!scores || !anchors || t < 1 || t > prob->T) return ARCKV_ERR_INVALID_ARG;
+  (void)ws;
+  (void)ws_bytes;
+  STAGE(ST_SELECT, launch_select(scores, prob->B, prob->T, t, anchors, nullptr, stream));
+  return ARCKV_OK;
+}
+
+arckv_status arckv_rowstats(const arckv_problem *prob, const void *K, const void *V, const void *Q_ref, float *z,
+                            float *m, float *Y, hipStream_t stream) {
+  CHECK(check_problem(prob));
+  if (!K || !V || !Q_ref || !z || !m || !Y) return ARCKV_ERR_INVALID_ARG;
+  if (!aligned(K, 16) || !aligned(V, 16) || !aligned(Q_ref, 16) || !aligned(Y, 16)) return ARCKV_ERR_INVALID_ARG;
+  STAGE(ST_ROWSTATS, launch_rowstats(prob->dtype, K, V, Q_ref, z, m, Y, prob->B, prob->T, prob->n,
+                                     eff_scale(prob), stream));
+  return ARCKV_OK;
+}
+
+arckv_status arckv_merge(const arckv_problem *prob, const void *K, const void *Q_ref, const float *z,
+                         const int32_t *anchors, int32_t t, float lambda_m, float *C_k, int32_t *assign, float *phi,
+                         void *ws, size_t ws_bytes, hipStream_t stream) {
+  CHECK(check_problem(prob));
+  if (!K || !Q_ref || !z || !anchors || !C_k || t < 1 || t > prob->T) return ARCKV_ERR_INVALID_ARG;
+  if (!(lambda_m >= 0.0f && lambda_m <= 1.0f)) return ARCKV_ERR_INVALID_ARG;
+  if (!aligned(K, 16) || !aligned(Q_ref, 16)) return ARCKV_ERR_INVALID_ARG;
+  Ctx c;
+  c.d = make_dims(prob, t);
+  int64_t P = 0;
+  CHECK(check_ws(c.d, ws, ws_bytes, 0, &P));
+  c.pl = make_plan(c.d, P);
+  c.ws = (char *)ws;
+  c.scale = eff_scale(prob);
+  c.stream = stream;
+  float *zmax = c.pers<float>(c.pl.zmax);
+  int32_t *anchor_of = c.pers<int32_t>(c.pl.anchor_of);
+  int32_t *kappa = assign ? assign : c.pers<int32_t>(c.pl.kappa);
+  float *phiw = phi ? phi : c.pers<float>(c.pl.phi);
+  STAGE(ST_ZMAX, launch_zmax(z, c.d.B, c.d.n, zmax, stream));
+  if (launch_anchor_of(anchors, c.d.B, c.d.T, t, anchor_of, stream) != hipSuccess) return ARCKV_ERR_HIP;
+  for (int b0 = 0; b0 < c.d.B; b0 += (int)P) {
+    const int Pc = (int)(c.d.B - b0 < P ? c.d.B - b0 : P);
+    CHECK(run_merge_chunk(c, b0, Pc, K, Q_ref, anchors, lambda_m, C_k, kappa, phiw, zmax, anchor_of));
+  }
+  return ARCKV_OK;
+}
+
+static arckv_status fit_common(const arckv_problem *prob, const float *C_k, int32_t t, const arckv_fit_params *p,
+                               void *ws, size_t ws_bytes, hipStream_t stream, Ctx &c, int64_t &P) {
+  CHECK(check_problem(prob));
+  if (!C_k || t < 1 || t > prob->T) return ARCKV_ERR_INVALID_ARG;
+  CHECK(check_params(p));
+  c.d = make_dims(prob, t);
+  CHECK(check_ws(c.d, ws, ws_bytes, p->pair_chunk, &P));
+  c.pl = make_plan(c.d, P);
+  c.ws = (char *)ws;
+  c.scale = eff_scale(prob);
+  c.stream = stream;
+  return ARCKV_OK;
+}
+
+arckv_status arckv_fit_bias(const arckv_problem *prob, const void *Q_ref, const float *C_k, int32_t t,
+                            const float *z, const float *m, const arckv_fit_params *p, float *beta, int32_t *info,
+                            float *delta_used, void *ws, size_t ws_bytes, hipStream_t stream) {
+  arckv_fit_params def;
+  arckv_default_params(&def);
+  if (!p) p = &def;
+  if (!Q_ref || !z || !m || !beta || !info) return ARCKV_ERR_INVALID_ARG;
+  if (!aligned(Q_ref, 16)) return ARCKV_ERR_INVALID_ARG;
+  Ctx c;
+  int64_t P = 0;
+  CHECK(fit_common(prob, C_k, t, p, ws, ws_bytes, stream, c, P));
+  for (int b0 = 0; b0 < c.d.B; b0 += (int)P) {
+    const int Pc = (int)(c.d.B - b0 < P ? c.d.B - b0 : P);
+    if (launch_pad_ck(c.d.dtype, C_k + (size_t)b0 * t * kHeadDimH, Pc, t, c.d.tp, c.chunk<char>(c.pl.Ckp), stream) !=
+        hipSuccess)
+      return ARCKV_ERR_HIP;
+    FitState st = fit_state(c, c.pl.st_g, c.pl.info_g, b0);
+    CHECK(run_fit_bias_chunk(c, b0, Pc, Q_ref, z, m, *p, beta, st));
+  }
+  if (launch_copy_info(c.pers<int32_t>(c.pl.info_g), nullptr, c.d.B, info, stream) != hipSuccess) return ARCKV_ERR_HIP;
+  if (delta_used && launch_copy_f32(reinterpret_cast<float *>(c.pers<char>(c.pl.st_g) + (size_t)c.d.B * 12),
+                                    delta_used, c.d.B, stream) != hipSuccess)
+    return ARCKV_ERR_HIP;
+  return ARCKV_OK;
+}
+
+arckv_status arckv_fit_values(const arckv_problem *prob, const void *Q_ref, const float *C_k, const float *beta,
+                              int32_t t, const float *Y, const arckv_fit_params *p, float *C_v, int32_t *info,
+                              float *delta_used, void *ws, size_t ws_bytes, hipStream_t stream) {
+  arckv_fit_params def;
+  arckv_default_params(&def);
+  if (!p) p = &def;
+  if (!Q_ref || !beta || !Y || !C_v || !info) return ARCKV_ERR_INVALID_ARG;
+  if (!aligned(Q_ref, 16)) return ARCKV_ERR_INVALID_ARG;
+  Ctx c;
+  int64_t P = 0;
+  CHECK(fit_common(prob, C_k, t, p, ws, ws_bytes, stream, c, P));
+  const Dims &d = c.d;
+  for (int b0 = 0; b0 < d.B; b0 += (int)P) {
+    const int Pc = (int)(d.B - b0 < P ? d.B - b0 : P);
+    if (launch_pad_ck(d.dtype, C_k + (size_t)b0 * t * kHeadDimH, Pc, t, d.tp, c.chunk<char>(c.pl.Ckp), stream) !=
+        hipSuccess)
+      return ARCKV_ERR_HIP;
+    if (launch_pad_beta(beta + (size_t)b0 * t, Pc, t, d.tp, c.pers<float>(c.pl.beta_ws) + (size_t)b0 * d.tp,
+                        stream) != hipSuccess)
+      return ARCKV_ERR_HIP;
+    // logits of the compact keys (the exp-part is unused here; z only shifts it)
+    const char *Qc = (const char *)Q_ref + (size_t)b0 * d.n * kHeadDimH * c.in_esz();
+    STAGE(ST_PHIC, launch_phic(d.dtype, Qc, c.chunk<char>(c.pl.Ckp), nullptr, c.chunk<char>(c.pl.PhiT),
+                               c.chunk<float>(c.pl.LT), Pc, d.t, d.n, d.tp, d.np_, c.scale, stream));
+    FitState st = fit_state(c, c.pl.st_a, c.pl.info_a, b0);
+    CHECK(run_fit_values_chunk(c, b0, Pc, Y, *p, C_v, st));
+  }
+  if (launch_copy_info(c.pers<int32_t>(c.pl.info_a), nullptr, d.B, info, stream) != hipSuccess) return ARCKV_ERR_HIP;
+  if (delta_used && launch_copy_f32(reinterpret_cast<float *>(c.pers<char>(c.pl.st_a) + (size_t)d.B * 12),
+                                    delta_used, d.B, stream) != hipSuccess)
+    return ARCKV_ERR_HIP;
+  return ARCKV_OK;
+}
+
+arckv_status arckv_compact(const arckv_problem *prob, const void *K, const void *V, const void *Q_ref,
+                           const arckv_indexer *ix, double rho, const arckv_fit_params *p, int32_t *t_out,
+                           int32_t *anchors, float *C_k, float *beta, float *C_v, int32_t *info, void *ws,
+                           size_t ws_bytes, hipStream_t stream) {
+  arckv_fit_params def;
+  arckv_default_params(&def);
+  if (!p) p = &def;
+  CHECK(check_problem(prob));
+  CHECK(check_params(p));
+  if (!K || !V || !Q_ref || !ix || !t_out || !anchors || !C_k || !beta || !C_v || !info) return ARCKV_ERR_INVALID_ARG;
+  if (!ix->W1 || !ix->b1 || !ix->w2 || !ix->b2) return ARCKV_ERR_INVALID_ARG;
+  if (ix->hidden != 64 || ix->w1_dtype != prob->dtype) return ARCKV_ERR_UNSUPPORTED;
+  if (!aligned(K, 16) || !aligned(V, 16) || !aligned(Q_ref, 16) || !aligned(ix->W1, 16)) return ARCKV_ERR_INVALID_ARG;
+  int32_t t = 0;
+  CHECK(arckv_budget(prob->T, rho, &t));
+  Ctx c;
+  c.d = make_dims(prob, t);
+  int64_t P = 0;
+  CHECK(check_ws(c.d, ws, ws_bytes, p->pair_chunk, &P));
+  *t_out = t;
+  c.pl = make_plan(c.d, P);
+  c.ws = (char *)ws;
+  c.scale = eff_scale(prob);
+  c.stream = stream;
+  const Dims &d = c.d;
+  float *scores = c.pers<float>(c.pl.scores);
+  float *z = c.pers<float>(c.pl.z), *m = c.pers<float>(c.pl.m), *Y = c.pers<float>(c.pl.Y);
+  float *zmax = c.pers<float>(c.pl.zmax), *phi = c.pers<float>(c.pl.phi);
+  int32_t *anchor_of = c.pers<int32_t>(c.pl.anchor_of), *kappa = c.pers<int32_t>(c.pl.kappa);
+  STAGE(ST_SCORE, launch_score(d.dtype, K, V, ix->W1, ix->b1, ix->w2, ix->b2, scores, d.B, d.T, stream));
+  STAGE(ST_SELECT, launch_select(scores, d.B, d.T, t, anchors, anchor_of, stream));
+  STAGE(ST_ROWSTATS, launch_rowstats(d.dtype, K, V, Q_ref, z, m, Y, d.B, d.T, d.n, c.scale, stream));
+  STAGE(ST_ZMAX, launch_zmax(z, d.B, d.n, zmax, stream));
+  for (int b0 = 0; b0 < d.B; b0 += (int)P) {
+    const int Pc = (int)(d.B - b0 < P ? d.B - b0 : P);
+    CHECK(run_merge_chunk(c, b0, Pc, K, Q_ref, anchors, p->lambda_m, C_k, kappa, phi, zmax, anchor_of));
+    CHECK(run_fit_bias_chunk(c, b0, Pc, Q_ref, z, m, *p, beta, fit_state(c, c.pl.st_g, c.pl.info_g, b0)));
+    CHECK(run_fit_values_chunk(c, b0, Pc, Y, *p, C_v, fit_state(c, c.pl.st_a, c.pl.info_a, b0)));
+  }
+  if (launch_copy_info(c.pers<int32_t>(c.pl.info_g), c.pers<int32_t>(c.pl.info_a), d.B, info, stream) != hipSuccess)
+    return ARCKV_ERR_HIP;
+  return ARCKV_OK;
+}
+
+const char *arckv_status_string(arckv_status s) {
+  switch (s) {
+    case ARCKV_OK: return "ok";
+    case ARCKV_ERR_INVALID_ARG: return "invalid argument";
+    case ARCKV_ERR_UNSUPPORTED: return "unsupported configuration";
+    case ARCKV_ERR_WORKSPACE: return "workspace too small or misaligned";
+    case ARCKV_ERR_HIP: return "HIP runtime error";
+  }
+  return "unknown status";
+}
+
+arckv_status arckv_set_timing(int32_t enable) {
+  std::lock_guard<std::mutex> lk(g_timing.mu);
+  g_timing.enabled = enable != 0;
+  return ARCKV_OK;
+}
+
+arckv_status arckv_reset_timing(void) {
+  std::lock_guard<std::mutex> lk(g_timing.mu);
+  for (auto &r : g_timing.pending) {
+    g_timing.pool.push_back(r.a);
+    g_timing.pool.push_back(r.b);
+  }
+  g_timing.pending.clear();
+  for (int i = 0; i < ST_COUNT; ++i) {
+    g_timing.ms[i] = 0.0;
+    g_timing.cnt[i] = 0;
+  }
+  return ARCKV_OK;
+}
+
+arckv_status arckv_stage_times(int32_t max_stages, const char **names, double *ms, int32_t *counts,
+                               int32_t *n_stages) {
+  if (!n_stages || max_stages < 0 || (max_stages > 0 && !ms)) return ARCKV_ERR_INVALID_ARG;
+  std::lock_guard<std::mutex> lk(g_timing.mu);
+  for (auto &r : g_timing.pending) {
+    if (hipEventSynchronize(r.b) != hipSuccess) return ARCKV_ERR_HIP;
+    float t = 0.0f;
+    if (hipEventElapsedTime(&t, r.a, r.b) != hipSuccess) return ARCKV_ERR_HIP;
+    g_timing.ms[r.stage] += t;
+    g_timing.cnt[r.stage] += 1;
+    g_timing.pool.push_back(r.a);
+    g_timing.pool.push_back(r.b);
+  }
+  g_timing.pending.clear();
+  *n_stages = ST_COUNT;
+  for (int i = 0; i < ST_COUNT && i < max_stages; ++i) {
+    if (names) names[i] = kStageNames[i];
+    ms[i] = g_timing.ms[i];
+    if (counts) counts[i] = g_timing.cnt[i];
+  }
+  return ARCKV_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,143 @@
+// Exponentiated score matrices, written transposed (query index contiguous)
+// so that the later contractions over queries read both operands K-contiguous.
+//
+// MODE_PROFILE (Section 3.4, eq. response_profile / mass_centroid):
+//   E^T[j][i] = exp(s q_i.k_j - z_merge) for every cached key j,
+//   phi_j = (1/n) sum_i E[i][j].
+// MODE_PHIC (Appendix A.9):
+//   L^T[r][i]   = s q_i.c_r            (logits of the compact keys, fp32)
+//   Phi^T[r][i] = exp(L - z_i)         (z_i: full-cache row maxima)
+//
+// A workgroup owns 128 output rows (keys or compact keys) whose fragments stay
+// in registers, and sweeps all query tiles through LDS.  Padding rows/columns
+// of the workspace are written as zeros.
+#include "common.hpp"
+
+namespace arckv {
+
+enum { MODE_PROFILE = 0, MODE_PHIC = 1 };
+
+template <typename T, int MODE>
+__global__ void __launch_bounds__(256) k_expgen(const T *__restrict__ Q, const void *__restrict__ Bsrc,
+                                                int64_t b_pair_stride, int64_t b_plane_stride, int b_rows,
+                                                const float *__restrict__ shift, void *__restrict__ out,
+                                                int64_t out_pair_stride, int64_t out_plane_stride,
+                                                float *__restrict__ aux, int64_t aux_pair_stride, int n,
+                                                int n_pad, float scale) {
+  using M = Mfma<T>;
+  constexpr int KPL = M::KPL, KSTEP = M::KSTEP, NKS = kHeadDim / KSTEP;
+  constexpr bool SPLIT_B = (MODE == MODE_PHIC) && sizeof(T) == 2;   // compact keys kept as bf16 hi + lo
+  constexpr int NB = SPLIT_B ? 2 : 1;
+  constexpr int EPC = 16 / sizeof(T);
+  constexpr int SQ = kHeadDim + EPC;
+  __shared__ __attribute__((aligned(16))) T sQ[64 * SQ];
+
+  const int b = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int h = lane >> 5, col = lane & 31;
+  const int row = blockIdx.x * 128 + wave * 32 + col;   // key j or compact-key r
+  const bool rvalid = row < b_rows;
+  const T *Bp = reinterpret_cast<const T *>(Bsrc) + (size_t)b * b_pair_stride;
+  typename M::frag bf[NB][NKS];
+  for (int p = 0; p < NB; ++p)
+    for (int ks = 0; ks < NKS; ++ks)
+      bf[p][ks] = rvalid ? M::load(Bp + p * b_plane_stride + (size_t)row * kHeadDim + ks * KSTEP + KPL * h)
+                         : M::zero();
+  const T *Qb = Q + (size_t)b * n * kHeadDim;
+  const float c2 = scale * 1.4426950408889634f;
+  const float zshift = (MODE == MODE_PROFILE) ? shift[b] : 0.0f;
+  float rowsum = 0.0f;
+
+  for (int i0 = 0; i0 < n_pad; i0 += 64) {
+    for (int c = tid; c < 64 * (kHeadDim / EPC); c += 256) {
+      int r = c / (kHeadDim / EPC), cc = (c % (kHeadDim / EPC)) * EPC;
+      f32x4 v = {0.f, 0.f, 0.f, 0.f};
+      if (i0 + r < n) v = *reinterpret_cast<const f32x4 *>(Qb + (size_t)(i0 + r) * kHeadDim + cc);
+      *reinterpret_cast<f32x4 *>(&sQ[r * SQ + cc]) = v;
+    }
+    __syncthreads();
+    for (int ms = 0; ms < 2; ++ms) {
+      f32x16 acc = zero16();
+      const T *arow = &sQ[(32 * ms + col) * SQ + KPL * h];
+      for (int ks = 0; ks < NKS; ++ks) {
+        typename M::frag a = M::load(arow + ks * KSTEP);
+        for (int p = 0; p < NB; ++p) acc = M::mma(a, bf[p][ks], acc);
+      }
+      for (int g = 0; g < 4; ++g) {
+        const int ib = i0 + 32 * ms + 8 * g + 4 * h;   // 4 consecutive queries ib..ib+3
+        float val[4], lg[4];
+        for (int r = 0; r < 4; ++r) {
+          const int i = ib + r;
+          const bool ok = rvalid && i < n;
+          if (MODE == MODE_PROFILE) {
+            val[r] = ok ? exp2f(acc[4 * g + r] * c2 - zshift * 1.4426950408889634f) : 0.0f;
+            rowsum += val[r];
+          } else {
+            lg[r] = ok ? acc[4 * g + r] * scale : 0.0f;
+            val[r] = ok ? expf(lg[r] - (shift ? shift[(size_t)b * n + i] : 0.0f)) : 0.0f;
+          }
+        }
+        char *ob = reinterpret_cast<char *>(out);
+        if constexpr (sizeof(T) == 4) {
+          float *o = reinterpret_cast<float *>(ob) + (size_t)b * out_pair_stride + (size_t)row * n_pad + ib;
+          *reinterpret_cast<f32x4 *>(o) = f32x4{val[0], val[1], val[2], val[3]};
+        } else if constexpr (MODE == MODE_PROFILE) {
+          bf16 *o = reinterpret_cast<bf16 *>(ob) + (size_t)b * out_pair_stride + (size_t)row * n_pad + ib;
+          bf16x4 w = {to_bf16(val[0]), to_bf16(val[1]), to_bf16(val[2]), to_bf16(val[3])};
+          *reinterpret_cast<bf16x4 *>(o) = w;
+        } else {
+          bf16 *o = reinterpret_cast<bf16 *>(ob) + (size_t)b * out_pair_stride + (size_t)row * n_pad + ib;
+          bf16x4 hi, lo;
+          for (int r = 0; r < 4; ++r) {
+            bf16 a, c;
+            split_bf16(val[r], a, c);
+            hi[r] = a;
+            lo[r] = c;
+          }
+          *reinterpret_cast<bf16x4 *>(o) = hi;
+          *reinterpret_cast<bf16x4 *>(o + out_plane_stride) = lo;
+        }
+        if (MODE == MODE_PHIC) {
+          float *L = aux + (size_t)b * aux_pair_stride + (size_t)row * n_pad + ib;
+          *reinterpret_cast<f32x4 *>(L) = f32x4{lg[0], lg[1], lg[2], lg[3]};
+        }
+      }
+    }
+    __syncthreads();
+  }
+  if (MODE == MODE_PROFILE) {
+    rowsum += __shfl_xor(rowsum, 32, 64);
+    if (h == 0 && rvalid) aux[(size_t)b * aux_pair_stride + row] = rowsum / (float)n;
+  }
+}
+
+// E^T [B][Tp][np] (T = bf16 or float) and phi [B][T].
+hipError_t launch_profiles(int dtype, const void *Q, const void *K, const float *zmerge, void *Et, float *phi,
+                           int B, int T, int n, int64_t Tp, int64_t np_, float scale, hipStream_t s) {
+  dim3 grid(Tp / 128, B);
+  if (dtype == ARCKV_BF16)
+    hipLaunchKernelGGL((k_expgen<bf16, MODE_PROFILE>), grid, dim3(256), 0, s, (const bf16 *)Q, K,
+                       (int64_t)T * kHeadDim, (int64_t)0, T, zmerge, Et, Tp * np_, (int64_t)0, phi, (int64_t)T, n,
+                       (int)np_, scale);
+  else
+    hipLaunchKernelGGL((k_expgen<float, MODE_PROFILE>), grid, dim3(256), 0, s, (const float *)Q, K,
+                       (int64_t)T * kHeadDim, (int64_t)0, T, zmerge, Et, Tp * np_, (int64_t)0, phi, (int64_t)T,
+                       n, (int)np_, scale);
+  return hipGetLastError();
+}
+
+// Ckp: padded compact keys [B][planes][tp][128]; Phi^T [B][planes][tp][np]; L^T [B][tp][np].
+hipError_t launch_phic(int dtype, const void *Q, const void *Ckp, const float *z, void *PhiT, float *LT, int B, int t,
+                       int n, int64_t tp, int64_t np_, float scale, hipStream_t s) {
+  dim3 grid(tp / 128, B);
+  if (dtype == ARCKV_BF16)
+    hipLaunchKernelGGL((k_expgen<bf16, MODE_PHIC>), grid, dim3(256), 0, s, (const bf16 *)Q, Ckp,
+                       2 * tp * kHeadDim, tp * kHeadDim, t, z, PhiT, 2 * tp * np_, tp * np_, LT, tp * np_, n,
+                       (int)np_, scale);
+  else
+    hipLaunchKernelGGL((k_expgen<float, MODE_PHIC>), grid, dim3(256), 0, s, (const float *)Q, Ckp,
+                       tp * kHeadDim, (int64_t)0, t, z, PhiT, tp * np_, (int64_t)0, LT, tp * np_, n, (int)np_,
+                       scale);
+  return hipGetLastError();
+}
+
+}  // namespace arckv

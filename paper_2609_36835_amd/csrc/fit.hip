@@ -1,0 +1,607 @@
+// Mass-bias and compact-value fits (Appendix A.9, eq. mass_fit, eq. value_lstsq).
+//
+// Both fits solve ridge-regularised normal equations (M + lam I) x = rhs with
+// M a float32 Gram matrix of size tp (padded; the padding is an identity
+// block with zero right-hand side, so padded unknowns solve to 0):
+//   k_ridge_init     lam = delta * tr(M)/t, write M + lam I into the work copy
+//   Cholesky         right-looking, 64-wide blocks, float32:
+//                      k_chol_diag0   factor diagonal block 0
+//                      k_chol_panel   L_ik = A_ik L_kk^-T for row blocks i > k
+//                      k_chol_update  A_ij -= L_ik L_jk^T (fp32 MFMA); the tile
+//                                     (k+1, k+1) is then factored in place
+//                    a failed pivot records info = column + 1 for that pair
+//   k_chol_escalate  for pairs that failed: restore, delta *= 10, refactor in
+//                    one workgroup; at most max_escalations times
+//   solves           TRSV (one rhs, float64 accumulation) / TRSM (128 rhs)
+//   residuals        rhs - (M + lam I) x, float64 (mass fit) or float32 MFMA
+//                    (value fit), for iterative refinement
+#include "common.hpp"
+#include "gemm.hpp"
+
+namespace arckv {
+
+constexpr int kNB = 64;          // Cholesky block
+constexpr int kSD = kNB + 1;     // LDS stride of a 64x64 fp32 tile
+
+struct FitState {
+  double *trace;   // [P]
+  float *lam;      // [P]
+  float *delta;    // [P]
+  int32_t *info;   // [P]
+};
+
+// --------------------------------------------------------------- h = Phi_C^T m
+// h_r = sum_i exp(L^T[r][i] - z_i) m_i in float64, one wave per row.
+__global__ void __launch_bounds__(256) k_hvec(const float *__restrict__ LT, const float *__restrict__ z,
+                                              const float *__restrict__ m, int n, int t, int64_t tp, int64_t np_,
+                                              double *__restrict__ h) {
+  const int b = blockIdx.y, lane = threadIdx.x & 63;
+  const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (r >= tp) return;
+  double acc = 0.0;
+  if (r < t) {
+    const float *row = LT + ((size_t)b * tp + r) * np_;
+    for (int i = lane; i < n; i += 64)
+      acc += (double)expf(row[i] - z[(size_t)b * n + i]) * (double)m[(size_t)b * n + i];
+    acc = wave_sum(acc);
+  }
+  if (lane == 0) h[(size_t)b * tp + r] = acc;
+}
+
+// --------------------------------------------------------------- ridge
+__global__ void __launch_bounds__(256) k_ridge_init(float *__restrict__ Gw, const float *__restrict__ Gc, int t,
+                                                    int64_t ld, float delta0, FitState st) {
+  __shared__ double red[4];
+  const int b = blockIdx.x, tid = threadIdx.x;
+  const size_t base = (size_t)b * ld * ld;
+  double tr = 0.0;
+  for (int r = tid; r < t; r += 256) tr += (double)Gc[base + (size_t)r * ld + r];
+  tr = wave_sum(tr);
+  if ((tid & 63) == 0) red[tid >> 6] = tr;
+  __syncthreads();
+  tr = red[0] + red[1] + red[2] + red[3];
+  const float lam = (float)((double)delta0 * tr / (double)t);
+  for (int64_t r = tid; r < ld; r += 256) Gw[base + (size_t)r * ld + r] = r < t ? Gc[base + (size_t)r * ld + r] + lam : 1.0f;
+  if (tid == 0) {
+    st.trace[b] = tr;
+    st.lam[b] = lam;
+    st.delta[b] = delta0;
+    st.info[b] = 0;
+  }
+}
+
+// --------------------------------------------------------------- 64x64 building blocks
+__device__ inline void load_tile(float *sD, const float *G, int64_t ld) {
+  for (int c = threadIdx.x; c < kNB * kNB / 4; c += 256) {
+    const int r = c / 16, cc = (c % 16) * 4;
+    f32x4 v = *reinterpret_cast<const f32x4 *>(G + (size_t)r * ld + cc);
+    sD[r * kSD + cc] = v[0];
+    sD[r * kSD + cc + 1] = v[1];
+    sD[r * kSD + cc + 2] = v[2];
+    sD[r * kSD + cc + 3] = v[3];
+  }
+}
+__device__ inline void store_tile(const float *sD, float *G, int64_t ld) {
+  for (int c = threadIdx.x; c < kNB * kNB / 4; c += 256) {
+    const int r = c / 16, cc = (c % 16) * 4;
+    f32x4 v = {sD[r * kSD + cc], sD[r * kSD + cc + 1], sD[r * kSD + cc + 2], sD[r * kSD + cc + 3]};
+    *reinterpret_cast<f32x4 *>(G + (size_t)r * ld + cc) = v;
+  }
+}
+
+// In-place Cholesky of the 64x64 tile in LDS (lower triangle).  Returns the
+// first failing column, or -1.  All 256 threads must call it.
+__device__ int factor_tile(float *sD) {
+  for (int c = 0; c < kNB; ++c) {
+    __syncthreads();
+    const float piv = sD[c * kSD + c];
+    if (!(piv > 0.0f) || !isfinite(piv)) return c;
+    const float d = sqrtf(piv);
+    __syncthreads();
+    if (threadIdx.x == 0) sD[c * kSD + c] = d;
+    const float inv = 1.0f / d;
+    for (int r = c + 1 + threadIdx.x; r < kNB; r += 256) sD[r * kSD + c] *= inv;
+    __syncthreads();
+    for (int e = threadIdx.x; e < kNB * kNB; e += 256) {
+      const int r = e / kNB, s = e % kNB;
+      if (s > c && s <= r) sD[r * kSD + s] -= sD[r * kSD + c] * sD[s * kSD + c];
+    }
+  }
+  __syncthreads();
+  return -1;
+}
+
+// X L^T = A for the 64x64 tile sX (in place), L the factored tile sL.
+__device__ void trsm_tile(const float *sL, float *sX) {
+  __syncthreads();
+  if (threadIdx.x < kNB) {
+    const int r = threadIdx.x;
+    for (int c = 0; c < kNB; ++c) {
+      float s = sX[r * kSD + c];
+      for (int q = 0; q < c; ++q) s -= sX[r * kSD + q] * sL[c * kSD + q];
+      sX[r * kSD + c] = s / sL[c * kSD + c];
+    }
+  }
+  __syncthreads();
+}
+
+// C -= A B^T for 64x64 tiles in LDS, fp32 MFMA, result applied to global C.
+__device__ void update_tile(const float *sA, const float *sB, float *C, int64_t ld) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wi = wave >> 1, wj = wave & 1, h = lane >> 5, col = lane & 31;
+  f32x16 acc = zero16();
+  for (int ks = 0; ks < kNB / 2; ++ks)
+    acc = Mfma<float>::mma(sA[(32 * wi + col) * kSD + 2 * ks + h], sB[(32 * wj + col) * kSD + 2 * ks + h], acc);
+  for (int v = 0; v < 16; ++v) {
+    const int r = 32 * wi + acc_row(v, lane), c = 32 * wj + col;
+    C[(size_t)r * ld + c] -= acc[v];
+  }
+}
+
+// sC -= A B^T with every operand in LDS.
+__device__ void update_tile_lds(const float *sA, const float *sB, float *sC) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wi = wave >> 1, wj = wave & 1, h = lane >> 5, col = lane & 31;
+  f32x16 acc = zero16();
+  for (int ks = 0; ks < kNB / 2; ++ks)
+    acc = Mfma<float>::mma(sA[(32 * wi + col) * kSD + 2 * ks + h], sB[(32 * wj + col) * kSD + 2 * ks + h], acc);
+  __syncthreads();
+  for (int v = 0; v < 16; ++v) sC[(32 * wi + acc_row(v, lane)) * kSD + 32 * wj + col] -= acc[v];
+  __syncthreads();
+}
+
+__device__ inline void decode_lower(int idx, int &a, int &bb) {
+  int m = (int)((sqrtf(8.0f * (float)idx + 1.0f) - 1.0f) * 0.5f);
+  while (m * (m + 1) / 2 > idx) --m;
+  while ((m + 1) * (m + 2) / 2 <= idx) ++m;
+  a = m;
+  bb = idx - m * (m + 1) / 2;
+}
+
+__global__ void __launch_bounds__(256) k_chol_diag0(float *__restrict__ Gw, int64_t ld, int32_t *__restrict__ info) {
+  __shared__ float sD[kNB * kSD];
+  const int b = blockIdx.x;
+  if (info[b] != 0) return;
+  float *G = Gw + (size_t)b * ld * ld;
+  load_tile(sD, G, ld);
+  const int fail = factor_tile(sD);
+  if (fail >= 0) {
+    if (threadIdx.x == 0) info[b] = fail + 1;
+    return;
+  }
+  store_tile(sD, G, ld);
+}
+
+__global__ void __launch_bounds__(256) k_chol_panel(float *__restrict__ Gw, int64_t ld, int k,
+                                                    const int32_t *__restrict__ info) {
+  __shared__ float sL[kNB * kSD], sX[kNB * kSD];
+  const int b = blockIdx.y;
+  if (info[b] != 0) return;
+  const int i = k + 1 + blockIdx.x;
+  float *G = Gw + (size_t)b * ld * ld;
+  load_tile(sL, G + (size_t)k * kNB * ld + k * kNB, ld);
+  load_tile(sX, G + (size_t)i * kNB * ld + k * kNB, ld);
+  trsm_tile(sL, sX);
+  store_tile(sX, G + (size_t)i * kNB * ld + k * kNB, ld);
+}
+
+__global__ void __launch_bounds__(256) k_chol_update(float *__restrict__ Gw, int64_t ld, int k,
+                                                     int32_t *__restrict__ info) {
+  __shared__ float sA[kNB * kSD], sB[kNB * kSD];
+  const int b = blockIdx.y;
+  if (info[b] != 0) return;
+  int a, bb;
+  decode_lower(blockIdx.x, a, bb);
+  const int i = k + 1 + a, j = k + 1 + bb;
+  float *G = Gw + (size_t)b * ld * ld;
+  load_tile(sA, G + (size_t)i * kNB * ld + k * kNB, ld);
+  if (i != j) load_tile(sB, G + (size_t)j * kNB * ld + k * kNB, ld);
+  __syncthreads();
+  float *C = G + (size_t)i * kNB * ld + j * kNB;
+  if (i == j && i == k + 1) {
+    // the next diagonal block: update it in LDS and factor it right away
+    load_tile(sB, C, ld);
+    __syncthreads();
+    update_tile_lds(sA, sA, sB);
+    const int fail = factor_tile(sB);
+    if (fail >= 0) {
+      if (threadIdx.x == 0) info[b] = i * kNB + fail + 1;
+      return;
+    }
+    store_tile(sB, C, ld);
+    return;
+  }
+  update_tile(sA, i != j ? sB : sA, C, ld);
+}
+
+// Whole factorisation in one workgroup (escalation path).
+__device__ int factor_matrix_single(float *G, int64_t ld, int nrb, float *sA, float *sB) {
+  for (int k = 0; k < nrb; ++k) {
+    __syncthreads();
+    load_tile(sA, G + (size_t)k * kNB * ld + k * kNB, ld);
+    const int fail = factor_tile(sA);
+    if (fail >= 0) return k * kNB + fail;
+    store_tile(sA, G + (size_t)k * kNB * ld + k * kNB, ld);
+    for (int i = k + 1; i < nrb; ++i) {
+      load_tile(sB, G + (size_t)i * kNB * ld + k * kNB, ld);
+      trsm_tile(sA, sB);
+      store_tile(sB, G + (size_t)i * kNB * ld + k * kNB, ld);
+    }
+    __threadfence_block();
+    __syncthreads();
+    for (int i = k + 1; i < nrb; ++i)
+      for (int j = k + 1; j <= i; ++j) {
+        __syncthreads();
+        load_tile(sA, G + (size_t)i * kNB * ld + k * kNB, ld);
+        load_tile(sB, G + (size_t)j * kNB * ld + k * kNB, ld);
+        __syncthreads();
+        update_tile(sA, sB, G + (size_t)i * kNB * ld + j * kNB, ld);
+        __threadfence_block();
+      }
+    __syncthreads();
+  }
+  return -1;
+}
+
+__global__ void __launch_bounds__(256) k_chol_escalate(float *__restrict__ Gw, const float *__restrict__ Gc, int t,
+                                                       int64_t ld, int max_esc, FitState st) {
+  __shared__ float sA[kNB * kSD], sB[kNB * kSD];
+  const int b = blockIdx.x;
+  if (st.info[b] == 0) return;
+  float *G = Gw + (size_t)b * ld * ld;
+  const float *Gcb = Gc + (size_t)b * ld * ld;
+  const int nrb = (int)(ld / kNB);
+  float delta = st.delta[b];
+  int fail = st.info[b] - 1;
+  for (int e = 0; e < max_esc && fail >= 0; ++e) {
+    delta *= 10.0f;
+    const float lam = (float)((double)delta * st.trace[b] / (double)t);
+    __syncthreads();
+    for (int64_t x = threadIdx.x; x < ld * ld; x += 256) {
+      const int64_t r = x / ld, c = x % ld;
+      G[x] = (r == c) ? (r < t ? Gcb[x] + lam : 1.0f) : Gcb[x];
+    }
+    __threadfence_block();
+    __syncthreads();
+    fail = factor_matrix_single(G, ld, nrb, sA, sB);
+    if (threadIdx.x == 0) {
+      st.delta[b] = delta;
+      st.lam[b] = lam;
+    }
+  }
+  if (threadIdx.x == 0) st.info[b] = fail >= 0 ? fail + 1 : 0;
+}
+
+// --------------------------------------------------------------- one right-hand side
+// Forward L y = rhs, then backward L^T x = y, float64 accumulation; x written
+// to `x` (and added to `acc` if non-null).  One workgroup per pair.
+__global__ void __launch_bounds__(256) k_trsv(const float *__restrict__ Gw, int64_t ld, const double *__restrict__ rhs,
+                                              double *__restrict__ y, double *__restrict__ x,
+                                              double *__restrict__ acc, const int32_t *__restrict__ info) {
+  __shared__ double part[4][kNB];
+  __shared__ double sy[kNB];
+  const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  if (info[b] != 0) return;
+  const float *L = Gw + (size_t)b * ld * ld;
+  const double *rb = rhs + (size_t)b * ld;
+  double *yb = y + (size_t)b * ld, *xb = x + (size_t)b * ld;
+  const int nrb = (int)(ld / kNB);
+  for (int kb = 0; kb < nrb; ++kb) {
+    const int r0 = kb * kNB;
+    for (int rr = wave; rr < kNB; rr += 4) {  // partial sums over earlier blocks
+      const float *row = L + (size_t)(r0 + rr) * ld;
+      double s = 0.0;
+      for (int c = lane; c < r0; c += 64) s += (double)row[c] * yb[c];
+      s = wave_sum(s);
+      if (lane == 0) sy[rr] = rb[r0 + rr] - s;
+    }
+    __syncthreads();
+    if (wave == 0) {
+      double mine = 0.0;
+      for (int rr = 0; rr < kNB; ++rr) {
+        double term = lane < rr ? (double)L[(size_t)(r0 + rr) * ld + r0 + lane] * mine : 0.0;
+        term = wave_sum(term);
+        const double v = (sy[rr] - term) / (double)L[(size_t)(r0 + rr) * ld + r0 + rr];
+        if (lane == rr) mine = v;
+      }
+      yb[r0 + lane] = mine;
+    }
+    __threadfence_block();
+    __syncthreads();
+  }
+  for (int kb = nrb - 1; kb >= 0; --kb) {
+    const int c0 = kb * kNB;
+    const int c = tid & 63, g = tid >> 6;
+    double s = 0.0;
+    for (int64_t i = c0 + kNB + g; i < ld; i += 4) s += (double)L[(size_t)i * ld + c0 + c] * xb[i];
+    part[g][c] = s;
+    __syncthreads();
+    if (wave == 0) {
+      const double base = yb[c0 + lane] - (part[0][lane] + part[1][lane] + part[2][lane] + part[3][lane]);
+      double mine = 0.0;
+      for (int rr = kNB - 1; rr >= 0; --rr) {
+        double term = lane > rr ? (double)L[(size_t)(c0 + lane) * ld + c0 + rr] * mine : 0.0;
+        term = wave_sum(term);
+        const double bse = __shfl(base, rr, 64);
+        const double v = (bse - term) / (double)L[(size_t)(c0 + rr) * ld + c0 + rr];
+        if (lane == rr) mine = v;
+      }
+      xb[c0 + lane] = mine;
+      if (acc) acc[(size_t)b * ld + c0 + lane] += mine;
+    }
+    __threadfence_block();
+    __syncthreads();
+  }
+}
+
+// res = rhs - (Gc + lam I) x over the first t rows (padded rows: 0), float64.
+__global__ void __launch_bounds__(256) k_residual_vec(const float *__restrict__ Gc, int64_t ld, int t,
+                                                      const double *__restrict__ rhs, const double *__restrict__ x,
+                                                      const float *__restrict__ lam, double *__restrict__ res,
+                                                      const int32_t *__restrict__ info) {
+  const int b = blockIdx.y, lane = threadIdx.x & 63;
+  const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (r >= ld || info[b] != 0) return;
+  double s = 0.0;
+  if (r < t) {
+    const float *row = Gc + ((size_t)b * ld + r) * ld;
+    const double *xb = x + (size_t)b * ld;
+    for (int c = lane; c < t; c += 64) s += (double)row[c] * xb[c];
+    s = wave_sum(s);
+    s = rhs[(size_t)b * ld + r] - s - (double)lam[b] * xb[r];
+  }
+  if (lane == 0) res[(size_t)b * ld + r] = s;
+}
+
+// beta = clip(log(max(max(w, 0), eps)), bmin, bmax); NaN for failed pairs.
+__global__ void __launch_bounds__(256) k_bias_finalize(const double *__restrict__ w, int64_t ld, int t, float eps,
+                                                       float bmin, float bmax, const int32_t *__restrict__ info,
+                                                       float *__restrict__ beta, float *__restrict__ beta_ws) {
+  const int b = blockIdx.y;
+  const int r = blockIdx.x * 256 + threadIdx.x;
+  if (r >= ld) return;
+  float v = 0.0f;
+  if (r < t) {
+    if (info[b] != 0) {
+      v = NAN;
+    } else {
+      const double wv = w[(size_t)b * ld + r];
+      const double ws = wv > 0.0 ? wv : 0.0;
+      v = (float)log(ws > (double)eps ? ws : (double)eps);
+      v = fminf(fmaxf(v, bmin), bmax);
+    }
+    beta[(size_t)b * t + r] = v;
+  }
+  if (beta_ws) beta_ws[(size_t)b * ld + r] = v;
+}
+
+// --------------------------------------------------------------- value-fit operands
+// P^T[r][i] = softmax_r(L^T[r][i] + beta_r) for r < t, i < n (own column max);
+// split into bf16 hi/lo planes (or fp32).  One thread per query.
+template <typename T>
+__global__ void __launch_bounds__(256) k_phat(const float *__restrict__ LT, const float *__restrict__ beta, int n,
+                                              int t, int64_t tp, int64_t np_, void *__restrict__ out) {
+  const int b = blockIdx.y;
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i >= np_) return;
+  const float *L = LT + (size_t)b * tp * np_ + i;
+  const float *bb = beta + (size_t)b * tp;
+  float mx = -INFINITY, sum = 0.0f;
+  if (i < n)
+    for (int r = 0; r < t; ++r) {
+      const float x = L[(size_t)r * np_] + bb[r];
+      if (x > mx) {
+        sum = sum * expf(mx - x) + 1.0f;
+        mx = x;
+      } else {
+        sum += expf(x - mx);
+      }
+    }
+  const float inv = (i < n && sum > 0.0f) ? 1.0f / sum : 0.0f;
+  for (int64_t r = 0; r < tp; ++r) {
+    const float p = (i < n && r < t) ? expf(L[(size_t)r * np_] + bb[r] - mx) * inv : 0.0f;
+    if constexpr (sizeof(T) == 2) {
+      bf16 *o = reinterpret_cast<bf16 *>(out) + (size_t)b * 2 * tp * np_ + (size_t)r * np_ + i;
+      split_bf16(p, o[0], o[tp * np_]);
+    } else {
+      reinterpret_cast<float *>(out)[(size_t)b * tp * np_ + (size_t)r * np_ + i] = p;
+    }
+  }
+}
+
+// out[c][i] = in[i][c] for a [rows][128] fp32 matrix, zero-padded to rows_pad
+// columns; bf16 hi/lo planes or fp32.
+template <typename T>
+__global__ void __launch_bounds__(256) k_transpose128(const float *__restrict__ in, int rows, int64_t in_pair,
+                                                      int64_t rows_pad, void *__restrict__ out, int64_t out_pair) {
+  __shared__ float s[64][kHeadDim + 1];
+  const int b = blockIdx.y, tid = threadIdx.x;
+  const int i0 = blockIdx.x * 64;
+  for (int e = tid; e < 64 * kHeadDim; e += 256) {
+    const int r = e / kHeadDim, c = e % kHeadDim;
+    s[r][c] = (i0 + r < rows) ? in[(size_t)b * in_pair + (size_t)(i0 + r) * kHeadDim + c] : 0.0f;
+  }
+  __syncthreads();
+  for (int e = tid; e < 64 * kHeadDim; e += 256) {
+    const int c = e / 64, r = e % 64;
+    const float v = s[r][c];
+    const size_t o = (size_t)b * out_pair + (size_t)c * rows_pad + i0 + r;
+    if constexpr (sizeof(T) == 2) {
+      bf16 *ob = reinterpret_cast<bf16 *>(out);
+      split_bf16(v, ob[o], ob[o + (size_t)kHeadDim * rows_pad]);
+    } else {
+      reinterpret_cast<float *>(out)[o] = v;
+    }
+  }
+}
+
+// --------------------------------------------------------------- 128 right-hand sides
+// Forward (L X = R) or backward (L^T X = R) substitution for 64 of the 128
+// columns per workgroup, float32, 32-row blocks.  X may alias nothing.
+template <bool FWD>
+__global__ void __launch_bounds__(256) k_trsm(const float *__restrict__ Gw, int64_t ld,
+                                              const float *__restrict__ R, float *__restrict__ X,
+                                              const int32_t *__restrict__ info) {
+  constexpr int RB = 32;
+  __shared__ float sL[RB][RB + 1];
+  __shared__ float sY[RB][64 + 1];
+  const int b = blockIdx.y, tid = threadIdx.x;
+  if (info[b] != 0) return;
+  const int c = tid & 63, g = tid >> 6, c0 = blockIdx.x * 64;
+  const float *L = Gw + (size_t)b * ld * ld;
+  const float *Rb = R + (size_t)b * ld * kHeadDim;
+  float *Xb = X + (size_t)b * ld * kHeadDim;
+  const int nb = (int)(ld / RB);
+  for (int step = 0; step < nb; ++step) {
+    const int kb = FWD ? step : nb - 1 - step;
+    const int r0 = kb * RB;
+    float acc[8];
+    for (int e = 0; e < 8; ++e) acc[e] = Rb[(size_t)(r0 + 8 * g + e) * kHeadDim + c0 + c];
+    const int p_beg = FWD ? 0 : r0 + RB, p_end = FWD ? r0 : (int)ld;
+    for (int p0 = p_beg; p0 < p_end; p0 += RB) {
+      __syncthreads();
+      for (int e = tid; e < RB * RB; e += 256) {
+        const int rr = e / RB, pp = e % RB;
+        // FWD: sL[rr][pp] = L[r0+rr][p0+pp];  BWD: sL[rr][pp] = L[p0+pp][r0+rr]
+        sL[rr][pp] = FWD ? L[(size_t)(r0 + rr) * ld + p0 + pp] : L[(size_t)(p0 + pp) * ld + r0 + rr];
+      }
+      for (int e = tid; e < RB * 64; e += 256) {
+        const int pp = e / 64, cc = e % 64;
+        sY[pp][cc] = Xb[(size_t)(p0 + pp) * kHeadDim + c0 + cc];
+      }
+      __syncthreads();
+      for (int pp = 0; pp < RB; ++pp) {
+        const float yv = sY[pp][c];
+        for (int e = 0; e < 8; ++e) acc[e] -= sL[8 * g + e][pp] * yv;
+      }
+    }
+    __syncthreads();
+    for (int e = tid; e < RB * RB; e += 256) {
+      const int rr = e / RB, pp = e % RB;
+      sL[rr][pp] = L[(size_t)(r0 + rr) * ld + r0 + pp];
+    }
+    for (int e = 0; e < 8; ++e) sY[8 * g + e][c] = acc[e];
+    __syncthreads();
+    if (g == 0) {
+      if (FWD) {
+        for (int rr = 0; rr < RB; ++rr) {
+          float v = sY[rr][c];
+          for (int q = 0; q < rr; ++q) v -= sL[rr][q] * sY[q][c];
+          sY[rr][c] = v / sL[rr][rr];
+        }
+      } else {
+        for (int rr = RB - 1; rr >= 0; --rr) {
+          float v = sY[rr][c];
+          for (int q = rr + 1; q < RB; ++q) v -= sL[q][rr] * sY[q][c];
+          sY[rr][c] = v / sL[rr][rr];
+        }
+      }
+    }
+    __syncthreads();
+    for (int e = 0; e < 8; ++e) Xb[(size_t)(r0 + 8 * g + e) * kHeadDim + c0 + c] = sY[8 * g + e][c];
+    __threadfence_block();
+  }
+}
+
+__global__ void __launch_bounds__(256) k_add_copy(float *__restrict__ x, const float *__restrict__ dx, int64_t n_per,
+                                                  const int32_t *__restrict__ info) {
+  const int b = blockIdx.y;
+  const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (e >= n_per || info[b] != 0) return;
+  x[(size_t)b * n_per + e] += dx[(size_t)b * n_per + e];
+}
+
+// Copy the first t rows of the padded [tp][128] solution to the output, NaN
+// for pairs whose factorisation failed.
+__global__ void __launch_bounds__(256) k_values_out(const float *__restrict__ Xp, int64_t tp, int t,
+                                                    const int32_t *__restrict__ info, float *__restrict__ Cv) {
+  const int b = blockIdx.y;
+  const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (e >= (int64_t)t * kHeadDim) return;
+  Cv[(size_t)b * t * kHeadDim + e] = info[b] != 0 ? NAN : Xp[(size_t)b * tp * kHeadDim + e];
+}
+
+// ------------------------------------------------------------------ launchers
+hipError_t launch_hvec(const float *LT, const float *z, const float *m, int B, int n, int t, int64_t tp, int64_t np_,
+                       double *h, hipStream_t s) {
+  hipLaunchKernelGGL(k_hvec, dim3((unsigned)(tp / 4), B), dim3(256), 0, s, LT, z, m, n, t, tp, np_, h);
+  return hipGetLastError();
+}
+
+// Ridge + factorisation (+ escalation) of the work copy Gw of Gc.
+hipError_t launch_cholesky(float *Gw, const float *Gc, int B, int t, int64_t ld, float delta0, int max_esc,
+                           FitState st, hipStream_t s) {
+  hipLaunchKernelGGL(k_ridge_init, dim3(B), dim3(256), 0, s, Gw, Gc, t, ld, delta0, st);
+  hipLaunchKernelGGL(k_chol_diag0, dim3(B), dim3(256), 0, s, Gw, ld, st.info);
+  const int nrb = (int)(ld / kNB);
+  for (int k = 0; k < nrb - 1; ++k) {
+    const int rem = nrb - k - 1;
+    hipLaunchKernelGGL(k_chol_panel, dim3(rem, B), dim3(256), 0, s, Gw, ld, k, st.info);
+    hipLaunchKernelGGL(k_chol_update, dim3(rem * (rem + 1) / 2, B), dim3(256), 0, s, Gw, ld, k, st.info);
+  }
+  if (max_esc > 0) hipLaunchKernelGGL(k_chol_escalate, dim3(B), dim3(256), 0, s, Gw, Gc, t, ld, max_esc, st);
+  return hipGetLastError();
+}
+
+hipError_t launch_trsv(const float *Gw, int B, int64_t ld, const double *rhs, double *y, double *x, double *acc,
+                       const int32_t *info, hipStream_t s) {
+  hipLaunchKernelGGL(k_trsv, dim3(B), dim3(256), 0, s, Gw, ld, rhs, y, x, acc, info);
+  return hipGetLastError();
+}
+
+hipError_t launch_residual_vec(const float *Gc, int B, int64_t ld, int t, const double *rhs, const double *x,
+                               const float *lam, double *res, const int32_t *info, hipStream_t s) {
+  hipLaunchKernelGGL(k_residual_vec, dim3((unsigned)(ld / 4), B), dim3(256), 0, s, Gc, ld, t, rhs, x, lam, res, info);
+  return hipGetLastError();
+}
+
+hipError_t launch_bias_finalize(const double *w, int B, int64_t ld, int t, float eps, float bmin, float bmax,
+                                const int32_t *info, float *beta, float *beta_ws, hipStream_t s) {
+  hipLaunchKernelGGL(k_bias_finalize, dim3((unsigned)((ld + 255) / 256), B), dim3(256), 0, s, w, ld, t, eps, bmin,
+                     bmax, info, beta, beta_ws);
+  return hipGetLastError();
+}
+
+hipError_t launch_phat(int dtype, const float *LT, const float *beta_ws, int B, int n, int t, int64_t tp,
+                       int64_t np_, void *out, hipStream_t s) {
+  dim3 grid((unsigned)((np_ + 255) / 256), B);
+  if (dtype == ARCKV_BF16)
+    hipLaunchKernelGGL(k_phat<bf16>, grid, dim3(256), 0, s, LT, beta_ws, n, t, tp, np_, out);
+  else
+    hipLaunchKernelGGL(k_phat<float>, grid, dim3(256), 0, s, LT, beta_ws, n, t, tp, np_, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_transpose128(int dtype, const float *in, int B, int rows, int64_t in_pair, int64_t rows_pad,
+                               void *out, int64_t out_pair, hipStream_t s) {
+  dim3 grid((unsigned)(rows_pad / 64), B);
+  if (dtype == ARCKV_BF16)
+    hipLaunchKernelGGL(k_transpose128<bf16>, grid, dim3(256), 0, s, in, rows, in_pair, rows_pad, out, out_pair);
+  else
+    hipLaunchKernelGGL(k_transpose128<float>, grid, dim3(256), 0, s, in, rows, in_pair, rows_pad, out, out_pair);
+  return hipGetLastError();
+}
+
+hipError_t launch_trsm(bool fwd, const float *Gw, int B, int64_t ld, const float *R, float *X, const int32_t *info,
+                       hipStream_t s) {
+  dim3 grid(kHeadDim / 64, B);
+  if (fwd)
+    hipLaunchKernelGGL(k_trsm<true>, grid, dim3(256), 0, s, Gw, ld, R, X, info);
+  else
+    hipLaunchKernelGGL(k_trsm<false>, grid, dim3(256), 0, s, Gw, ld, R, X, info);
+  return hipGetLastError();
+}
+
+hipError_t launch_add(float *x, const float *dx, int B, int64_t n_per, const int32_t *info, hipStream_t s) {
+  hipLaunchKernelGGL(k_add_copy, dim3((unsigned)((n_per + 255) / 256), B), dim3(256), 0, s, x, dx, n_per, info);
+  return hipGetLastError();
+}
+
+hipError_t launch_values_out(const float *Xp, int B, int64_t tp, int t, const int32_t *info, float *Cv,
+                             hipStream_t s) {
+  hipLaunchKernelGGL(k_values_out, dim3((unsigned)(((int64_t)t * kHeadDim + 255) / 256), B), dim3(256), 0, s, Xp, tp,
+                     t, info, Cv);
+  return hipGetLastError();
+}
+
+}  // namespace arckv

@@ -1,0 +1,234 @@
+// Anchor assignment finalisation and convex key merge (Section 3.4).
+//
+//  k_zmax            z_merge = max_i z_i (the global logit maximum equals the
+//                    largest full-cache row maximum, eq. response_profile)
+//  k_anchor_of       position -> anchor slot (or -1)
+//  k_anchor_profiles U_S rows: E^T[s_r] / ||E^T[s_r]|| (anchor response profiles)
+//  k_assign_finalize kappa_j from the per-tile packed argmax; anchors map to
+//                    themselves (eq. anchor_assignment)
+//  k_group_sort      stable counting sort of positions by group (deterministic)
+//  k_group_merge     c_r = sum_j alpha_rj k_j with alpha_rj = lambda phi_j / sum_G phi
+//                    + (1 - lambda)[j = s_r], renormalised to sum exactly to 1
+//                    in float (eq. mass_centroid, eq. key_merge)
+#include "common.hpp"
+
+namespace arckv {
+
+__global__ void __launch_bounds__(256) k_zmax(const float *__restrict__ z, int n, float *__restrict__ zmax) {
+  __shared__ float red[4];
+  const int b = blockIdx.x, tid = threadIdx.x;
+  float v = -INFINITY;
+  for (int i = tid; i < n; i += 256) v = fmaxf(v, z[(size_t)b * n + i]);
+  v = wave_max(v);
+  if ((tid & 63) == 0) red[tid >> 6] = v;
+  __syncthreads();
+  if (tid == 0) zmax[b] = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+}
+
+__global__ void __launch_bounds__(256) k_anchor_of(const int32_t *__restrict__ anchors, int T, int t,
+                                                   int32_t *__restrict__ anchor_of) {
+  const int b = blockIdx.y;
+  const int j = blockIdx.x * 256 + threadIdx.x;
+  if (j < T) anchor_of[(size_t)b * T + j] = -1;
+}
+
+__global__ void __launch_bounds__(256) k_anchor_scatter(const int32_t *__restrict__ anchors, int T, int t,
+                                                        int32_t *__restrict__ anchor_of) {
+  const int b = blockIdx.y;
+  const int r = blockIdx.x * 256 + threadIdx.x;
+  if (r < t) anchor_of[(size_t)b * T + anchors[(size_t)b * t + r]] = r;
+}
+
+// One wave per anchor row: U_S[r][i] = E^T[s_r][i] / ||E^T[s_r][:]||; rows r >= t are zero.
+template <typename T>
+__global__ void __launch_bounds__(256) k_anchor_profiles(const T *__restrict__ Et, const int32_t *__restrict__ anchors,
+                                                         T *__restrict__ U, int t, int64_t Tp, int64_t np_,
+                                                         int64_t tp) {
+  const int b = blockIdx.y, lane = threadIdx.x & 63;
+  const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (r >= tp) return;
+  T *urow = U + ((size_t)b * tp + r) * np_;
+  if (r >= t) {
+    for (int64_t i = lane; i < np_; i += 64) urow[i] = (T)0.0f;
+    return;
+  }
+  const T *erow = Et + ((size_t)b * Tp + anchors[(size_t)b * t + r]) * np_;
+  float ss = 0.0f;
+  for (int64_t i = lane; i < np_; i += 64) {
+    float e = to_f(erow[i]);
+    ss = fmaf(e, e, ss);
+  }
+  ss = wave_sum(ss);
+  const float inv = ss > 0.0f ? 1.0f / sqrtf(ss) : 0.0f;
+  for (int64_t i = lane; i < np_; i += 64) urow[i] = (T)(to_f(erow[i]) * inv);
+}
+
+__global__ void __launch_bounds__(256) k_assign_finalize(const uint64_t *__restrict__ part, int MT, int64_t Np,
+                                                         const int32_t *__restrict__ anchor_of, int T,
+                                                         int32_t *__restrict__ kappa) {
+  const int b = blockIdx.y;
+  const int j = blockIdx.x * 256 + threadIdx.x;
+  if (j >= T) return;
+  int32_t a = anchor_of[(size_t)b * T + j];
+  if (a < 0) {
+    uint64_t best = 0;
+    const uint64_t *pp = part + (size_t)b * MT * Np + j;
+    for (int mt = 0; mt < MT; ++mt) {
+      uint64_t v = pp[(size_t)mt * Np];
+      best = v > best ? v : best;
+    }
+    a = (int32_t)(0xFFFFFFFFu - (uint32_t)(best & 0xFFFFFFFFull));
+  }
+  kappa[(size_t)b * T + j] = a;
+}
+
+// One wave per pair.  Produces offsets [t+1] and perm [T] (positions grouped by
+// kappa, ascending position within each group).  cursor [t] is scratch.
+__global__ void __launch_bounds__(64) k_group_sort(const int32_t *__restrict__ kappa, int T, int t,
+                                                   int32_t *__restrict__ offsets, int32_t *__restrict__ cursor,
+                                                   int32_t *__restrict__ perm) {
+  const int b = blockIdx.x, lane = threadIdx.x;
+  const int32_t *kp = kappa + (size_t)b * T;
+  int32_t *off = offsets + (size_t)b * (t + 1);
+  int32_t *cur = cursor + (size_t)b * t;
+  int32_t *pm = perm + (size_t)b * T;
+  // every access to cur[] is an atomic, fenced between phases
+  for (int r = lane; r < t; r += 64) atomicExch(&cur[r], 0);
+  __threadfence();
+  for (int j = lane; j < T; j += 64) atomicAdd(&cur[kp[j]], 1);
+  __threadfence();
+  // exclusive scan of the counts
+  int32_t carry = 0;
+  for (int r0 = 0; r0 < t; r0 += 64) {
+    const int r = r0 + lane;
+    int32_t c = r < t ? atomicAdd(&cur[r], 0) : 0;
+    int32_t x = c;
+    for (int d = 1; d < 64; d <<= 1) {
+      int32_t y = __shfl_up(x, d, 64);
+      if (lane >= d) x += y;
+    }
+    if (r < t) {
+      off[r] = carry + x - c;
+      atomicExch(&cur[r], carry + x - c);
+    }
+    carry += __shfl(x, 63, 64);
+  }
+  if (lane == 0) off[t] = carry;
+  __threadfence();
+  int nbits = 1;
+  while ((1 << nbits) < t) ++nbits;
+  const uint64_t lanemask = lane == 0 ? 0ull : (~0ull >> (64 - lane));
+  for (int j0 = 0; j0 < T; j0 += 64) {
+    const int j = j0 + lane;
+    const bool in = j < T;
+    const int32_t r = in ? kp[j] : 0;
+    uint64_t match = __ballot(in);
+    for (int bit = 0; bit < nbits; ++bit) {
+      uint64_t bal = __ballot(in && ((r >> bit) & 1));
+      match &= ((r >> bit) & 1) ? bal : ~bal;
+    }
+    const int rank = __popcll(match & lanemask);
+    const int leader = __ffsll((long long)match) - 1;
+    int32_t base = 0;
+    if (in && lane == leader) base = atomicAdd(&cur[r], __popcll(match));
+    base = __shfl(base, leader < 0 ? 0 : leader, 64);
+    if (in && base + rank < T) pm[base + rank] = j;
+  }
+}
+
+// One wave per compact key r (rows r >= t of the padded copies are zeroed).
+// Outputs: C_k [B][t][d] fp32 and the padded operand copy used by Phi_C:
+// bf16 hi/lo planes [B][2][tp][d] (bf16 inputs) or fp32 [B][tp][d].
+template <typename E>
+__global__ void __launch_bounds__(256) k_group_merge(const E *__restrict__ K, const float *__restrict__ phi,
+                                                     const int32_t *__restrict__ offsets,
+                                                     const int32_t *__restrict__ perm,
+                                                     const int32_t *__restrict__ anchors, int T, int t,
+                                                     int64_t tp, float lambda, float *__restrict__ Ck,
+                                                     void *__restrict__ Ckp) {
+  const int b = blockIdx.y, lane = threadIdx.x & 63;
+  const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (r >= tp) return;
+  const int d0 = 2 * lane;
+  float c0 = 0.0f, c1 = 0.0f;
+  if (r < t) {
+    const int32_t beg = offsets[(size_t)b * (t + 1) + r], end = offsets[(size_t)b * (t + 1) + r + 1];
+    const int32_t *pm = perm + (size_t)b * T;
+    const float *ph = phi + (size_t)b * T;
+    const int32_t s = anchors[(size_t)b * t + r];
+    float mass = 0.0f;
+    for (int32_t q = beg; q < end; ++q) mass += ph[pm[q]];
+    const E *Kb = K + (size_t)b * T * kHeadDim;
+    float wsum = 0.0f, a0 = 0.0f, a1 = 0.0f;
+    for (int32_t q = beg; q < end; ++q) {
+      const int32_t j = pm[q];
+      float alpha = (mass > 0.0f) ? lambda * (ph[j] / mass) : 0.0f;
+      if (j == s) alpha += (mass > 0.0f) ? (1.0f - lambda) : 1.0f;
+      wsum += alpha;
+      a0 = fmaf(alpha, to_f(Kb[(size_t)j * kHeadDim + d0]), a0);
+      a1 = fmaf(alpha, to_f(Kb[(size_t)j * kHeadDim + d0 + 1]), a1);
+    }
+    c0 = a0 / wsum;
+    c1 = a1 / wsum;
+    Ck[((size_t)b * t + r) * kHeadDim + d0] = c0;
+    Ck[((size_t)b * t + r) * kHeadDim + d0 + 1] = c1;
+  }
+  if constexpr (sizeof(E) == 2) {
+    bf16 *hi = reinterpret_cast<bf16 *>(Ckp) + ((size_t)b * 2 * tp + r) * kHeadDim;
+    bf16 *lo = hi + tp * kHeadDim;
+    split_bf16(c0, hi[d0], lo[d0]);
+    split_bf16(c1, hi[d0 + 1], lo[d0 + 1]);
+  } else {
+    float *o = reinterpret_cast<float *>(Ckp) + ((size_t)b * tp + r) * kHeadDim;
+    o[d0] = c0;
+    o[d0 + 1] = c1;
+  }
+}
+
+// ------------------------------------------------------------------ launchers
+hipError_t launch_zmax(const float *z, int B, int n, float *zmax, hipStream_t s) {
+  hipLaunchKernelGGL(k_zmax, dim3(B), dim3(256), 0, s, z, n, zmax);
+  return hipGetLastError();
+}
+
+hipError_t launch_anchor_of(const int32_t *anchors, int B, int T, int t, int32_t *anchor_of, hipStream_t s) {
+  hipLaunchKernelGGL(k_anchor_of, dim3((T + 255) / 256, B), dim3(256), 0, s, anchors, T, t, anchor_of);
+  hipLaunchKernelGGL(k_anchor_scatter, dim3((t + 255) / 256, B), dim3(256), 0, s, anchors, T, t, anchor_of);
+  return hipGetLastError();
+}
+
+hipError_t launch_anchor_profiles(int dtype, const void *Et, const int32_t *anchors, void *U, int B, int t,
+                                  int64_t Tp, int64_t np_, int64_t tp, hipStream_t s) {
+  dim3 grid((unsigned)(tp / 4), B);
+  if (dtype == ARCKV_BF16)
+    hipLaunchKernelGGL(k_anchor_profiles<bf16>, grid, dim3(256), 0, s, (const bf16 *)Et, anchors, (bf16 *)U, t, Tp,
+                       np_, tp);
+  else
+    hipLaunchKernelGGL(k_anchor_profiles<float>, grid, dim3(256), 0, s, (const float *)Et, anchors, (float *)U, t,
+                       Tp, np_, tp);
+  return hipGetLastError();
+}
+
+hipError_t launch_assign_finalize(const uint64_t *part, int MT, int64_t Np, const int32_t *anchor_of, int B, int T,
+                                  int32_t *kappa, hipStream_t s) {
+  hipLaunchKernelGGL(k_assign_finalize, dim3((T + 255) / 256, B), dim3(256), 0, s, part, MT, Np, anchor_of, T,
+                     kappa);
+  return hipGetLastError();
+}
+
+hipError_t launch_group_merge(int dtype, const void *K, const float *phi, const int32_t *kappa,
+                              const int32_t *anchors, int B, int T, int t, int64_t tp, float lambda,
+                              int32_t *offsets, int32_t *cursor, int32_t *perm, float *Ck, void *Ckp,
+                              hipStream_t s) {
+  hipLaunchKernelGGL(k_group_sort, dim3(B), dim3(64), 0, s, kappa, T, t, offsets, cursor, perm);
+  dim3 grid((unsigned)(tp / 4), B);
+  if (dtype == ARCKV_BF16)
+    hipLaunchKernelGGL(k_group_merge<bf16>, grid, dim3(256), 0, s, (const bf16 *)K, phi, offsets, perm, anchors, T,
+                       t, tp, lambda, Ck, Ckp);
+  else
+    hipLaunchKernelGGL(k_group_merge<float>, grid, dim3(256), 0, s, (const float *)K, phi, offsets, perm, anchors,
+                       T, t, tp, lambda, Ck, Ckp);
+  return hipGetLastError();
+}
+
+}  // namespace arckv

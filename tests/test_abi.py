@@ -1,0 +1,148 @@
+"""The C ABI on a machine without a GPU: the library loads, exports every
+declared entry point, and rejects bad arguments before touching HIP."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2609_36835_amd import arckv as A
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(__file__)), "include", "arckv.h")
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(arckv_[a-z_]+)\s*\(", src)))
+
+
+def test_library_exports_every_declared_symbol():
+    names = declared_functions()
+    assert len(names) >= 14
+    lib = ctypes.CDLL(A.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(names) == set(A.ENTRY_POINTS)
+
+
+def test_budget():
+    assert A.budget(1024, 0.1) == 102
+    assert A.budget(131072, 0.01) == 1311
+    assert A.budget(32768, 0.1) == 3277
+    assert A.budget(16384, 0.02) == 328
+    assert A.budget(10, 0.0) == 1
+    assert A.budget(10, 3.0) == 10
+    for T, rho in [(0, 0.1), (10, -0.1), (10, float("nan")), (10, float("inf"))]:
+        with pytest.raises(A.ArckvError) as e:
+            A.budget(T, rho)
+        assert e.value.status == A.ERR_INVALID_ARG
+
+
+def test_budget_matches_oracle():
+    import oracle
+    for T in (1, 7, 100, 1024, 8191, 32768, 131072):
+        for rho in (0.001, 0.01, 0.02, 0.05, 0.1, 0.2, 0.5, 1.0):
+            assert A.budget(T, rho) == oracle.budget(T, rho)
+
+
+def test_status_strings():
+    for s in range(5):
+        assert A.status_string(s)
+    assert A.status_string(99) == "unknown status"
+
+
+def test_default_params():
+    p = A.default_params()
+    assert p.lambda_m == pytest.approx(0.25) and p.delta_beta == pytest.approx(1e-6)
+    assert p.delta_v == pytest.approx(1e-3) and p.eps_w == pytest.approx(1e-12)
+    assert (p.b_min, p.b_max, p.bias_mode, p.max_escalations, p.refine_steps) == (-30.0, 30.0, 0, 3, 1)
+
+
+def ws(prob, t, params=None):
+    return A.workspace_size(prob, t, params)
+
+
+def test_workspace_validation_and_monotonicity():
+    p = A.problem_from_dims(8, 8192, 4096)
+    full = ws(p, 819)
+    half = ws(p, 819, A.default_params(pair_chunk=4))
+    one = ws(p, 819, A.default_params(pair_chunk=1))
+    assert full > half > one > 0
+    assert ws(A.problem_from_dims(8, 8192, 4096, dtype=A.F32), 819) > full   # fp32 profiles are wider
+    bad = [
+        (A.problem_from_dims(8, 8192, 4096, d=64), 819, A.ERR_UNSUPPORTED),
+        (A.problem_from_dims(8, 8192, 4096, dtype=7), 819, A.ERR_UNSUPPORTED),
+        (A.problem_from_dims(0, 8192, 4096), 819, A.ERR_INVALID_ARG),
+        (A.problem_from_dims(8, 0, 4096), 1, A.ERR_INVALID_ARG),
+        (A.problem_from_dims(8, 8192, 0), 819, A.ERR_INVALID_ARG),
+        (A.problem_from_dims(8, 8192, 4096), 0, A.ERR_INVALID_ARG),
+        (A.problem_from_dims(8, 8192, 4096), 8193, A.ERR_INVALID_ARG),
+    ]
+    for prob, t, code in bad:
+        with pytest.raises(A.ArckvError) as e:
+            ws(prob, t)
+        assert e.value.status == code
+
+
+@pytest.mark.parametrize("field,value,code", [
+    ("lambda_m", 1.5, A.ERR_INVALID_ARG), ("lambda_m", -0.1, A.ERR_INVALID_ARG),
+    ("delta_beta", -1.0, A.ERR_INVALID_ARG), ("delta_v", float("nan"), A.ERR_INVALID_ARG),
+    ("eps_w", 0.0, A.ERR_INVALID_ARG), ("b_min", 40.0, A.ERR_INVALID_ARG),
+    ("bias_mode", 1, A.ERR_UNSUPPORTED), ("max_escalations", 7, A.ERR_INVALID_ARG),
+    ("refine_steps", -1, A.ERR_INVALID_ARG), ("pair_chunk", -2, A.ERR_INVALID_ARG),
+])
+def test_param_validation(field, value, code):
+    p = A.problem_from_dims(2, 1024, 256)
+    with pytest.raises(A.ArckvError) as e:
+        ws(p, 102, A.default_params(**{field: value}))
+    assert e.value.status == code
+
+
+def test_entry_points_reject_bad_arguments_without_gpu():
+    """Every error below is returned before any HIP call (no GPU here)."""
+    import torch
+    if torch.cuda.is_available():
+        pytest.skip("fake-pointer validation test runs only where no GPU is visible")
+    L = A.lib()
+    prob = A.Problem(2, 1024, 256, 128, A.BF16, 0.0)
+    # Fake device pointers: every case below must fail validation, so nothing is
+    # ever launched with them (this test also runs on GPU machines).
+    fake = ctypes.c_void_p(0x1000)
+    odd = ctypes.c_void_p(0x1001)
+    ix = A.Indexer(64, A.BF16, fake, fake, fake, fake)
+    bad_ix = A.Indexer(32, A.BF16, fake, fake, fake, fake)
+    par = A.default_params()
+    t_out = ctypes.c_int32()
+    r = ctypes.byref
+    cases = [
+        (L.arckv_score(None, fake, fake, r(ix), fake, None), A.ERR_INVALID_ARG),
+        (L.arckv_score(r(prob), None, fake, r(ix), fake, None), A.ERR_INVALID_ARG),
+        (L.arckv_score(r(prob), fake, fake, r(bad_ix), fake, None), A.ERR_UNSUPPORTED),
+        (L.arckv_score(r(prob), odd, fake, r(ix), fake, None), A.ERR_INVALID_ARG),
+        (L.arckv_select(r(prob), fake, 0, fake, None, 0, None), A.ERR_INVALID_ARG),
+        (L.arckv_select(r(prob), fake, 1025, fake, None, 0, None), A.ERR_INVALID_ARG),
+        (L.arckv_rowstats(r(prob), fake, fake, None, fake, fake, fake, None), A.ERR_INVALID_ARG),
+        (L.arckv_merge(r(prob), fake, fake, fake, fake, 10, 0.25, fake, None, None, ctypes.c_void_p(0x1010),
+                       1 << 30, None), A.ERR_WORKSPACE),     # misaligned workspace
+        (L.arckv_merge(r(prob), fake, fake, fake, fake, 10, 0.25, fake, None, None, ctypes.c_void_p(0x10000), 16,
+                       None), A.ERR_WORKSPACE),              # workspace too small
+        (L.arckv_merge(r(prob), fake, fake, fake, fake, 10, 1.5, fake, None, None, fake, 0, None), A.ERR_INVALID_ARG),
+        (L.arckv_fit_bias(r(prob), fake, fake, 10, fake, fake, r(A.default_params(bias_mode=1)), fake, fake, None,
+                          fake, 0, None), A.ERR_UNSUPPORTED),
+        (L.arckv_fit_values(r(prob), fake, fake, fake, 10, None, r(par), fake, fake, None, fake, 0, None),
+         A.ERR_INVALID_ARG),
+        (L.arckv_compact(r(prob), fake, fake, fake, r(ix), float("nan"), r(par), r(t_out), fake, fake, fake, fake,
+                         fake, ctypes.c_void_p(0x10000), 1 << 40, None), A.ERR_INVALID_ARG),
+        (L.arckv_compact(r(prob), fake, fake, fake, r(ix), 0.1, r(par), r(t_out), fake, fake, fake, fake, fake,
+                         ctypes.c_void_p(0x10000), 1024, None), A.ERR_WORKSPACE),
+    ]
+    for i, (got, want) in enumerate(cases):
+        assert got == want, (i, got, want)
+
+
+def test_product_path_has_no_oracle_or_fallback():
+    """The binding never imports the oracle and has no CPU path."""
+    src = open(os.path.join(os.path.dirname(A.__file__), "arckv.py")).read()
+    assert "oracle" not in src.replace("oracle/", "")
+    assert "numpy" not in src
