@@ -159,23 +159,53 @@ def mass_weights(E: np.ndarray) -> np.ndarray:
     return E.mean(axis=0)
 
 
-def profiles_assign_phi(Q, K, S, scale: float):
+def round_to(x: np.ndarray, dtype) -> np.ndarray:
+    """Round float64 values to bfloat16 ("bf16", nearest even) or float32 ("f32")."""
+    x = np.asarray(x, np.float64)
+    if dtype is None:
+        return x
+    if dtype == "f32":
+        return x.astype(np.float32).astype(np.float64)
+    if dtype == "bf16":
+        u = x.astype(np.float32).view(np.uint32).astype(np.uint64)
+        lsb = (u >> np.uint64(16)) & np.uint64(1)
+        r = ((u + np.uint64(0x7FFF) + lsb) & np.uint64(0xFFFF0000)).astype(np.uint32)
+        return r.view(np.float32).astype(np.float64)
+    raise ValueError(dtype)
+
+
+def profiles_assign_phi(Q, K, S, scale: float, profile_dtype=None):
     """O3-O5 inputs for a whole pair, chunked over keys to bound memory.
 
     Each chunk holds whole key columns, so every column's profile,
     similarity row and mass weight is computed exactly as in the
     unchunked definition.  Returns (kappa, phi, z_merge).
+
+    profile_dtype: None computes the argmax of eq. (anchor_assignment) in
+    float64.  "bf16" / "f32" take that integer decision in the precision in
+    which a compared implementation stores the profiles: exp(l - z_merge) and
+    the normalised anchor profiles are rounded to that type before the
+    similarities are formed (in float64).  phi is never rounded.
     """
     Q = np.asarray(Q, np.float64)
     K = np.asarray(K, np.float64)
     S = np.asarray(S)
     z_merge = global_logit_max(Q, K, scale)
-    _, US, _ = response_profiles(Q, K[S], scale, z_merge)       # [n, t]
+    if profile_dtype is None:
+        _, US, _ = response_profiles(Q, K[S], scale, z_merge)       # [n, t]
+    else:
+        ES = round_to(np.exp(logits(Q, K[S], scale) - z_merge), profile_dtype)
+        nrm = np.linalg.norm(ES, axis=0)
+        US = round_to(np.divide(ES, nrm[None, :], out=np.zeros_like(ES), where=nrm[None, :] > 0), profile_dtype)
     T = K.shape[0]
     kappa = np.empty(T, np.int64)
     phi = np.empty(T, np.float64)
     for j0, j1 in _key_chunks(T, Q.shape[0]):
         E, U, _ = response_profiles(Q, K[j0:j1], scale, z_merge)
+        if profile_dtype is not None:
+            Er = round_to(E, profile_dtype)
+            nr = np.linalg.norm(Er, axis=0)
+            U = np.divide(Er, nr[None, :], out=np.zeros_like(Er), where=nr[None, :] > 0)
         kappa[j0:j1] = np.argmax(U.T @ US, axis=1)
         phi[j0:j1] = mass_weights(E)
     kappa[S] = np.arange(S.shape[0])
@@ -409,11 +439,12 @@ def compact_pair(K, V, Q, W1, b1, w2, b2, rho: float = None, t: int = None, scal
                  lambda_m: float = LAMBDA_M, delta_beta: float = DELTA_BETA,
                  delta_v: float = DELTA_V, eps_w: float = EPS_W, b_min: float = B_MIN,
                  b_max: float = B_MAX, bias_mode: int = 0, scores=None,
-                 anchors=None) -> PairResult:
+                 anchors=None, kappa=None, profile_dtype=None) -> PairResult:
     """The four stages in order: score, select, merge, fit (Section 3.2).
 
-    ``scores`` / ``anchors`` may be supplied to run the later stages on given
-    upstream values (stage-wise checking).
+    ``scores`` / ``anchors`` / ``kappa`` may be supplied to run the later
+    stages on given upstream values (stage-wise checking); ``profile_dtype``
+    is passed to the assignment (see profiles_assign_phi).
     """
     K = np.asarray(K, np.float64)
     V = np.asarray(V, np.float64)
@@ -428,7 +459,10 @@ def compact_pair(K, V, Q, W1, b1, w2, b2, rho: float = None, t: int = None, scal
     if anchors is None:
         anchors = select_topt(scores, t)
     anchors = np.asarray(anchors, np.int64)
-    kappa, phi, z_merge = profiles_assign_phi(Q, K, anchors, scale)
+    kap, phi, z_merge = profiles_assign_phi(Q, K, anchors, scale, profile_dtype)
+    if kappa is None:
+        kappa = kap
+    kappa = np.asarray(kappa, np.int64)
     C_k = merge_keys(K, phi, kappa, anchors, lambda_m)
     z, m, Y = rowstats(Q, K, V, scale)
     bf = fit_bias(Q, C_k, z, m, scale, delta_beta, eps_w, b_min, b_max, bias_mode)

@@ -129,3 +129,42 @@ def compact_attend(Q, C_k, beta, C_v, scale):
         s = sum(w)
         out.append([sum(w[r] * C_v[r][c] for r in range(len(C_k))) / s for c in range(len(C_v[0]))])
     return out
+
+
+def round_bf16(x):
+    """Nearest-even bfloat16 value of float x (via its float32 bit pattern)."""
+    import struct
+    u = struct.unpack("<I", struct.pack("<f", x))[0]
+    lower = u & 0xFFFF0000
+    rem = u & 0xFFFF
+    if rem > 0x8000 or (rem == 0x8000 and (u >> 16) & 1):
+        lower += 0x10000
+    return struct.unpack("<f", struct.pack("<I", lower & 0xFFFFFFFF))[0]
+
+
+def assign_rounded(Q, K, S, scale, rnd):
+    """eq. anchor_assignment with exp-profiles and anchor profiles rounded by rnd."""
+    L = logits(Q, K, scale)
+    n, T = len(Q), len(K)
+    zm = max(max(row) for row in L)
+    E = [[rnd(math.exp(L[i][j] - zm)) for j in range(T)] for i in range(n)]
+    US = []
+    for s in S:
+        col = [E[i][s] for i in range(n)]
+        nrm = math.sqrt(sum(v * v for v in col))
+        US.append([rnd(v / nrm) for v in col])
+    pos = {s: r for r, s in enumerate(S)}
+    kappa = []
+    for j in range(T):
+        if j in pos:
+            kappa.append(pos[j])
+            continue
+        col = [E[i][j] for i in range(n)]
+        nrm = math.sqrt(sum(v * v for v in col))
+        best, br = -math.inf, -1
+        for r in range(len(S)):
+            v = sum(col[i] / nrm * US[r][i] for i in range(n))
+            if v > best:
+                best, br = v, r
+        kappa.append(br)
+    return kappa

@@ -404,3 +404,24 @@ def test_compaction_beats_hard_subset_on_heldout():
     S = res.anchors
     hard = oracle.row_rel_err(oracle.attend_compact(Qh, K[S], np.zeros(len(S)), V[S], 0.25), O).mean()
     assert fitted < hard
+
+
+# ----------------------------------------------------------------- kernel-precision assignment
+def test_round_to_matches_struct_rounding():
+    g = rng(50)
+    xs = np.concatenate([g.standard_normal(200) * 10.0 ** g.integers(-8, 8, 200),
+                         [1.0, 1.00390625, 1.005859375, 1.0078125, -2.5, 0.0, 1e-40]])
+    got = oracle.round_to(xs, "bf16")
+    assert got.tolist() == [brute.round_bf16(float(x)) for x in xs]
+    assert oracle.round_to(np.array([1.00390625]), "bf16")[0] == 1.0          # tie to even
+    assert oracle.round_to(np.array([1.01171875]), "bf16")[0] == 1.015625      # tie to even (up)
+    np.testing.assert_array_equal(oracle.round_to(xs, "f32"), xs.astype(np.float32).astype(np.float64))
+
+
+@pytest.mark.parametrize("dt", ["bf16", "f32"])
+def test_assignment_in_storage_precision_bruteforce(dt):
+    K, V, Q, *_ = small_pair(60, T=14, n=9)
+    S = np.array([1, 5, 8, 12])
+    rnd = brute.round_bf16 if dt == "bf16" else (lambda v: float(np.float32(v)))
+    kap, _, _ = oracle.profiles_assign_phi(Q, K, S, 0.6, profile_dtype=dt)
+    assert kap.tolist() == brute.assign_rounded(Q.tolist(), K.tolist(), S.tolist(), 0.6, rnd)
