@@ -90,7 +90,10 @@ typedef struct {
   float b_min, b_max;    /* clip range of beta; default [-30, 30] */
   int32_t bias_mode;     /* 0 = projected least squares (eq. mass_fit); other values unsupported */
   int32_t max_escalations; /* ridge x10 retries after a failed Cholesky pivot, 0..6; default 3 */
-  int32_t refine_steps;  /* iterative-refinement steps after each Cholesky solve, 0..4; default 1 */
+  int32_t refine_steps;  /* iterative-refinement steps after each Cholesky solve, 0..4; default 2.
+                          * Each step recomputes the residual from the data (Phi_C, P_hat),
+                          * not from the float32 Gram, so the solves converge to the
+                          * least-squares solutions of the exact normal equations. */
   int32_t pair_chunk;    /* pairs processed together by arckv_compact (0 = all B); sizes the workspace */
 } arckv_fit_params;
 
@@ -145,7 +148,7 @@ arckv_status arckv_merge(const arckv_problem *prob, const void *K, const void *Q
 
 /* Stage 3: mass bias (Appendix A.9, eq. mass_fit).  With
  * Phi_C = exp(s Q C_k^T - z 1^T): w~ solves (G + delta_beta tr(G)/t I) w = h,
- * G = Phi_C^T Phi_C, h = Phi_C^T m, by Cholesky (float32, refined);
+ * G = Phi_C^T Phi_C, h = Phi_C^T m, by Cholesky (float32) plus refinement;
  * beta = clip(log max(max(w~, 0), eps_w), b_min, b_max).
  *   beta  [B][t] output.
  *   info  [B] output: 0 = ok, k > 0 = Cholesky pivot k failed after all ridge

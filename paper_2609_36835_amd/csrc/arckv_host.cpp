@@ -46,8 +46,14 @@ hipError_t launch_assign_gemm(int dtype, const void *U, const void *Et, uint64_t
 hipError_t launch_gram(int dtype, const void *X, float *G, float *Gc, int P, int64_t tp, int64_t np_, hipStream_t s);
 hipError_t launch_rhs_gemm(int dtype, const void *PT, const void *YT, float *Bm, int P, int64_t tp, int64_t np_,
                            hipStream_t s);
-hipError_t launch_value_residual(const float *Gc, const float *XT, const float *Bm, const float *X,
-                                 const float *lam, float *R, int P, int64_t tp, hipStream_t s);
+hipError_t launch_value_residual(int dtype, const void *XT, const void *Pm, const void *PT, const float *Y, void *UT,
+                                 const float *X, const float *lam, float *R, int P, int n, int64_t tp, int64_t np_,
+                                 hipStream_t s);
+hipError_t launch_mass_residual(const float *LT, const float *z, const float *m, const double *w, const float *lam,
+                                int B, int n, int t, int64_t tp, int64_t np_, double *u, double *res,
+                                const int32_t *info, hipStream_t s);
+hipError_t launch_transpose_planes(int dtype, const void *PT, void *P, int B, int64_t rows, int64_t cols,
+                                   hipStream_t s);
 hipError_t launch_hvec(const float *LT, const float *z, const float *m, int B, int n, int t, int64_t tp, int64_t np_,
                        double *h, hipStream_t s);
 hipError_t launch_cholesky(float *Gw, const float *Gc, int B, int t, int64_t ld, float delta0, int max_esc,
@@ -165,7 +171,7 @@ struct Plan {
   // chunk region (offsets relative to chunk base)
   int64_t Ckp;
   int64_t Et, U, part, offsets, cursor, perm;            // merge phase
-  int64_t PhiT, LT, Gw, Gc, h, w, y, x, res, YT, Bm, X, R, Y2, XT;  // fit phase
+  int64_t PhiT, LT, Gw, Gc, h, w, y, x, res, u, YT, Bm, X, R, Y2, XT, Pm, UT;  // fit phase
   int64_t chunk_bytes;
 };
 
@@ -208,12 +214,15 @@ static Plan make_plan(const Dims &d, int64_t P) {
   pl.y = f.take(P * d.tp * 8);
   pl.x = f.take(P * d.tp * 8);
   pl.res = f.take(P * d.tp * 8);
+  pl.u = f.take(P * d.np_ * 8);
   pl.YT = f.take(P * kHeadDimH * d.np_ * 4);
   pl.Bm = f.take(P * d.tp * kHeadDimH * 4);
   pl.X = f.take(P * d.tp * kHeadDimH * 4);
   pl.R = f.take(P * d.tp * kHeadDimH * 4);
   pl.Y2 = f.take(P * d.tp * kHeadDimH * 4);
   pl.XT = f.take(P * d.tp * kHeadDimH * 4);
+  pl.Pm = f.take(P * d.tp * d.np_ * 4);
+  pl.UT = f.take(P * kHeadDimH * d.np_ * 4);
   (void)phase0;
   pl.chunk_bytes = m.off > f.off ? m.off : f.off;
   return pl;
@@ -349,8 +358,11 @@ static arckv_status run_fit_bias_chunk(const Ctx &c, int b0, int P, const void *
   {
     StageScope _sc(ST_SOLVE_W, stream);
     if (launch_trsv(Gw, P, d.tp, h, y, w, nullptr, st.info, stream) != hipSuccess) return ARCKV_ERR_HIP;
+    // refinement against the data: res = Phi_C^T (m - Phi_C w) - lam w
+    double *u = c.chunk<double>(c.pl.u);
     for (int it = 0; it < fp.refine_steps; ++it) {
-      if (launch_residual_vec(Gc, P, d.tp, d.t, h, w, st.lam, res, st.info, stream) != hipSuccess) return ARCKV_ERR_HIP;
+      if (launch_mass_residual(LT, zc, mc, w, st.lam, P, d.n, d.t, d.tp, d.np_, u, res, st.info, stream) != hipSuccess)
+        return ARCKV_ERR_HIP;
       if (launch_trsv(Gw, P, d.tp, res, y, x, w, st.info, stream) != hipSuccess) return ARCKV_ERR_HIP;
     }
     if (launch_bias_finalize(w, P, d.tp, d.t, fp.eps_w, fp.b_min, fp.b_max, st.info, beta + (size_t)b0 * d.t,
@@ -372,7 +384,10 @@ static arckv_status run_fit_values_chunk(const Ctx &c, int b0, int P, const floa
   float *LT = c.chunk<float>(c.pl.LT), *Gw = c.chunk<float>(c.pl.Gw), *Gc = c.chunk<float>(c.pl.Gc);
   void *YT = c.chunk<char>(c.pl.YT);
   float *Bm = c.chunk<float>(c.pl.Bm), *X = c.chunk<float>(c.pl.X), *R = c.chunk<float>(c.pl.R);
-  float *Y2 = c.chunk<float>(c.pl.Y2), *XT = c.chunk<float>(c.pl.XT);
+  float *Y2 = c.chunk<float>(c.pl.Y2);
+  void *XT = c.chunk<char>(c.pl.XT), *Pm = c.chunk<char>(c.pl.Pm), *UT = c.chunk<char>(c.pl.UT);
+  const float *Yc = Y + (size_t)b0 * d.n * kHeadDimH;
+  const int64_t pl = d.dtype == ARCKV_BF16 ? 2 : 1;
   const int64_t yt_pair = (d.dtype == ARCKV_BF16 ? 2 : 1) * (int64_t)kHeadDimH * d.np_;
   STAGE(ST_PHAT, launch_phat(d.dtype, LT, c.pers<float>(c.pl.beta_ws) + (size_t)b0 * d.tp, P, d.n, d.t, d.tp,
                              d.np_, PT, stream));
@@ -389,11 +404,15 @@ static arckv_status run_fit_values_chunk(const Ctx &c, int b0, int P, const floa
     StageScope _sc(ST_SOLVE_V, stream);
     if (launch_trsm(true, Gw, P, d.tp, Bm, Y2, st.info, stream) != hipSuccess) return ARCKV_ERR_HIP;
     if (launch_trsm(false, Gw, P, d.tp, Y2, X, st.info, stream) != hipSuccess) return ARCKV_ERR_HIP;
+    // refinement against the data: R = P^T (Y - P X) - lam X
+    if (fp.refine_steps > 0 && launch_transpose_planes(d.dtype, PT, Pm, P, d.tp, d.np_, stream) != hipSuccess)
+      return ARCKV_ERR_HIP;
     for (int it = 0; it < fp.refine_steps; ++it) {
-      if (launch_transpose128(ARCKV_F32, X, P, (int)d.tp, d.tp * kHeadDimH, d.tp, XT, d.tp * kHeadDimH, stream) !=
+      if (launch_transpose128(d.dtype, X, P, (int)d.tp, d.tp * kHeadDimH, d.tp, XT, pl * d.tp * kHeadDimH, stream) !=
           hipSuccess)
         return ARCKV_ERR_HIP;
-      if (launch_value_residual(Gc, XT, Bm, X, st.lam, R, P, d.tp, stream) != hipSuccess) return ARCKV_ERR_HIP;
+      if (launch_value_residual(d.dtype, XT, Pm, PT, Yc, UT, X, st.lam, R, P, d.n, d.tp, d.np_, stream) != hipSuccess)
+        return ARCKV_ERR_HIP;
       if (launch_trsm(true, Gw, P, d.tp, R, Y2, st.info, stream) != hipSuccess) return ARCKV_ERR_HIP;
       if (launch_trsm(false, Gw, P, d.tp, Y2, R, st.info, stream) != hipSuccess) return ARCKV_ERR_HIP;
       if (launch_add(X, R, P, d.tp * kHeadDimH, st.info, stream) != hipSuccess) return ARCKV_ERR_HIP;
@@ -421,7 +440,7 @@ arckv_status arckv_default_params(arckv_fit_params *p) {
   p->b_max = 30.0f;
   p->bias_mode = 0;
   p->max_escalations = 3;
-  p->refine_steps = 1;
+  p->refine_steps = 2;
   p->pair_chunk = 0;
   return ARCKV_OK;
 }

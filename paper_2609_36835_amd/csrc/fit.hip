@@ -353,6 +353,71 @@ __global__ void __launch_bounds__(256) k_residual_vec(const float *__restrict__ 
   if (lane == 0) res[(size_t)b * ld + r] = s;
 }
 
+// Refinement residual of the mass fit computed from the data, not from the
+// float32 Gram: res = Phi_C^T (m - Phi_C w) - lam w with Phi_C = exp(L^T - z)
+// re-evaluated in fp32 and every sum in float64.
+// Stage 1 (one thread per query i): u_i = m_i - sum_{r<t} Phi[i][r] w_r.
+__global__ void __launch_bounds__(256) k_mass_resid_rows(const float *__restrict__ LT, const float *__restrict__ z,
+                                                         const float *__restrict__ m, const double *__restrict__ w,
+                                                         int n, int t, int64_t tp, int64_t np_,
+                                                         double *__restrict__ u, const int32_t *__restrict__ info) {
+  const int b = blockIdx.y;
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i >= np_ || info[b] != 0) return;
+  double acc = 0.0;
+  if (i < n) {
+    const float *L = LT + (size_t)b * tp * np_ + i;
+    const double *wb = w + (size_t)b * tp;
+    const float zi = z[(size_t)b * n + i];
+    for (int r = 0; r < t; ++r) acc += (double)expf(L[(size_t)r * np_] - zi) * wb[r];
+    acc = (double)m[(size_t)b * n + i] - acc;
+  }
+  u[(size_t)b * np_ + i] = acc;
+}
+
+// Stage 2 (one wave per compact key r): res_r = sum_i Phi[i][r] u_i - lam w_r.
+__global__ void __launch_bounds__(256) k_mass_resid_cols(const float *__restrict__ LT, const float *__restrict__ z,
+                                                         const double *__restrict__ u, const double *__restrict__ w,
+                                                         const float *__restrict__ lam, int n, int t, int64_t tp,
+                                                         int64_t np_, double *__restrict__ res,
+                                                         const int32_t *__restrict__ info) {
+  const int b = blockIdx.y, lane = threadIdx.x & 63;
+  const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (r >= tp || info[b] != 0) return;
+  double acc = 0.0;
+  if (r < t) {
+    const float *row = LT + ((size_t)b * tp + r) * np_;
+    for (int i = lane; i < n; i += 64)
+      acc += (double)expf(row[i] - z[(size_t)b * n + i]) * u[(size_t)b * np_ + i];
+    acc = wave_sum(acc) - (double)lam[b] * w[(size_t)b * tp + r];
+  }
+  if (lane == 0) res[(size_t)b * tp + r] = acc;
+}
+
+// out[c][r] = in[r][c] for [rows][cols] matrices (2- or 4-byte elements, all
+// dims multiples of 64), `planes` consecutive planes per pair.
+template <typename E>
+__global__ void __launch_bounds__(256) k_transpose2d(const E *__restrict__ in, E *__restrict__ out, int64_t rows,
+                                                     int64_t cols, int planes) {
+  __shared__ E s[64][65];
+  const int b = blockIdx.z;
+  const int64_t r0 = (int64_t)blockIdx.y * 64, c0 = (int64_t)blockIdx.x * 64;
+  for (int q = 0; q < planes; ++q) {
+    const E *ip = in + ((size_t)b * planes + q) * rows * cols;
+    E *op = out + ((size_t)b * planes + q) * rows * cols;
+    __syncthreads();
+    for (int e = threadIdx.x; e < 64 * 64; e += 256) {
+      const int rr = e / 64, cc = e % 64;
+      s[rr][cc] = ip[(size_t)(r0 + rr) * cols + c0 + cc];
+    }
+    __syncthreads();
+    for (int e = threadIdx.x; e < 64 * 64; e += 256) {
+      const int cc = e / 64, rr = e % 64;
+      op[(size_t)(c0 + cc) * rows + r0 + rr] = s[rr][cc];
+    }
+  }
+}
+
 // beta = clip(log(max(max(w, 0), eps)), bmin, bmax); NaN for failed pairs.
 __global__ void __launch_bounds__(256) k_bias_finalize(const double *__restrict__ w, int64_t ld, int t, float eps,
                                                        float bmin, float bmax, const int32_t *__restrict__ info,
@@ -552,6 +617,28 @@ hipError_t launch_trsv(const float *Gw, int B, int64_t ld, const double *rhs, do
 hipError_t launch_residual_vec(const float *Gc, int B, int64_t ld, int t, const double *rhs, const double *x,
                                const float *lam, double *res, const int32_t *info, hipStream_t s) {
   hipLaunchKernelGGL(k_residual_vec, dim3((unsigned)(ld / 4), B), dim3(256), 0, s, Gc, ld, t, rhs, x, lam, res, info);
+  return hipGetLastError();
+}
+
+hipError_t launch_mass_residual(const float *LT, const float *z, const float *m, const double *w, const float *lam,
+                                int B, int n, int t, int64_t tp, int64_t np_, double *u, double *res,
+                                const int32_t *info, hipStream_t s) {
+  hipLaunchKernelGGL(k_mass_resid_rows, dim3((unsigned)(np_ / 256), B), dim3(256), 0, s, LT, z, m, w, n, t, tp, np_,
+                     u, info);
+  hipLaunchKernelGGL(k_mass_resid_cols, dim3((unsigned)(tp / 4), B), dim3(256), 0, s, LT, z, u, w, lam, n, t, tp,
+                     np_, res, info);
+  return hipGetLastError();
+}
+
+// P [B][planes][cols][rows] from PT [B][planes][rows][cols].
+hipError_t launch_transpose_planes(int dtype, const void *PT, void *P, int B, int64_t rows, int64_t cols,
+                                   hipStream_t s) {
+  dim3 grid((unsigned)(cols / 64), (unsigned)(rows / 64), B);
+  if (dtype == ARCKV_BF16)
+    hipLaunchKernelGGL(k_transpose2d<uint16_t>, grid, dim3(256), 0, s, (const uint16_t *)PT, (uint16_t *)P, rows,
+                       cols, 2);
+  else
+    hipLaunchKernelGGL(k_transpose2d<float>, grid, dim3(256), 0, s, (const float *)PT, (float *)P, rows, cols, 1);
   return hipGetLastError();
 }
 

@@ -58,7 +58,7 @@ hipError_t launch_rhs_gemm(int dtype, const void *PT, const void *YT, float *Bm,
   g.syrk = false;
   g.group_m = 8;
   g.lda = g.ldb = np_;
-  EpiStore e{Bm, tp * kHeadDim, kHeadDim, nullptr, nullptr, nullptr};
+  EpiStore e{Bm, tp * kHeadDim, kHeadDim, nullptr, nullptr};
   if (dtype == ARCKV_BF16) {
     g.a_pair = 2 * tp * np_;
     g.a_plane = tp * np_;
@@ -73,25 +73,53 @@ hipError_t launch_rhs_gemm(int dtype, const void *PT, const void *YT, float *Bm,
   return launch_gemm<float, 1, 1>(g, (const float *)PT, (const float *)YT, e, s);
 }
 
-// Refinement residual R = Bm - Gc X - lam X for 128 right-hand sides, fp32 MFMA.
-// Gc [P][tp][tp], XT [P][128][tp] (X transposed), X / Bm / R [P][tp][128].
-hipError_t launch_value_residual(const float *Gc, const float *XT, const float *Bm, const float *X,
-                                 const float *lam, float *R, int P, int64_t tp, hipStream_t s) {
-  GemmShape g;
-  g.batch = P;
-  g.M = (int)tp;
-  g.N = kHeadDim;
-  g.K = (int)tp;
-  g.syrk = false;
-  g.group_m = 8;
-  g.a_pair = tp * tp;
-  g.a_plane = 0;
-  g.lda = tp;
-  g.b_pair = (int64_t)kHeadDim * tp;
-  g.b_plane = 0;
-  g.ldb = tp;
-  EpiStore e{R, tp * kHeadDim, kHeadDim, Bm, X, lam};
-  return launch_gemm<float, 1, 1>(g, Gc, XT, e, s);
+// Value-fit refinement residual from the data, in two contractions over the
+// split (or fp32) operands:
+//   U^T = Y^T - X^T P^T      A = X^T [P][pl][128][tp], B = P [P][pl][np][tp], K = tp
+//   R   = P^T U - lam X       A = P^T [P][pl][tp][np],  B = U^T [P][pl][128][np], K = np
+hipError_t launch_value_residual(int dtype, const void *XT, const void *Pm, const void *PT, const float *Y, void *UT,
+                                 const float *X, const float *lam, float *R, int P, int n, int64_t tp, int64_t np_,
+                                 hipStream_t s) {
+  const bool split = dtype == ARCKV_BF16;
+  const int64_t pl = split ? 2 : 1;
+  GemmShape g1;
+  g1.batch = P;
+  g1.M = kHeadDim;
+  g1.N = (int)np_;
+  g1.K = (int)tp;
+  g1.syrk = false;
+  g1.group_m = 8;
+  g1.a_pair = pl * kHeadDim * tp;
+  g1.a_plane = split ? kHeadDim * tp : 0;
+  g1.lda = tp;
+  g1.b_pair = pl * np_ * tp;
+  g1.b_plane = split ? np_ * tp : 0;
+  g1.ldb = tp;
+  hipError_t e;
+  if (split) {
+    EpiValueResid<true> ep{UT, pl * kHeadDim * np_, kHeadDim * np_, (int)np_, n, Y};
+    e = launch_gemm<bf16, 2, 2>(g1, (const bf16 *)XT, (const bf16 *)Pm, ep, s);
+  } else {
+    EpiValueResid<false> ep{UT, kHeadDim * np_, 0, (int)np_, n, Y};
+    e = launch_gemm<float, 1, 1>(g1, (const float *)XT, (const float *)Pm, ep, s);
+  }
+  if (e != hipSuccess) return e;
+  GemmShape g2;
+  g2.batch = P;
+  g2.M = (int)tp;
+  g2.N = kHeadDim;
+  g2.K = (int)np_;
+  g2.syrk = false;
+  g2.group_m = 8;
+  g2.a_pair = pl * tp * np_;
+  g2.a_plane = split ? tp * np_ : 0;
+  g2.lda = np_;
+  g2.b_pair = pl * kHeadDim * np_;
+  g2.b_plane = split ? kHeadDim * np_ : 0;
+  g2.ldb = np_;
+  EpiStore e2{R, tp * kHeadDim, kHeadDim, X, lam};
+  if (split) return launch_gemm<bf16, 2, 2>(g2, (const bf16 *)PT, (const bf16 *)UT, e2, s);
+  return launch_gemm<float, 1, 1>(g2, (const float *)PT, (const float *)UT, e2, s);
 }
 
 }  // namespace arckv

@@ -192,17 +192,17 @@ struct EpiSym {
   }
 };
 
-// out[r][c] = acc (+ optional: rhs[r][c] - acc - lam[p] * X[r][c] for residuals).
+// out[r][c] = acc, or acc - lam[p] * X[r][c] when X is given (the value-fit
+// residual P^T U - lam X).
 struct EpiStore {
   float *out;
   int64_t pair_stride;
   int ld;
-  const float *rhs;      // nullptr: plain store
-  const float *X;
+  const float *X;        // nullptr: plain store
   const float *lam;      // [P]
   __device__ void operator()(f32x16 (&acc)[2][2], int p, int row0, int col0, int, int, int lane, int) const {
-    const int h = lane >> 5, col = lane & 31;
     const size_t base = (size_t)p * pair_stride;
+    const int col = lane & 31;
     for (int i = 0; i < 2; ++i)
       for (int j = 0; j < 2; ++j) {
         const int c = col0 + 32 * j + col;
@@ -210,8 +210,42 @@ struct EpiStore {
           const int r = row0 + 32 * i + acc_row(v, lane);
           const size_t o = base + (size_t)r * ld + c;
           float val = acc[i][j][v];
-          if (rhs) val = rhs[o] - val - lam[p] * X[o];
+          if (X) val -= lam[p] * X[o];
           out[o] = val;
+        }
+      }
+  }
+};
+
+// U^T[c][i] = Y[i][c] - acc[c][i] (rows c < 128, columns queries i; zero for
+// i >= n), stored as bf16 hi/lo planes or fp32 [P][planes][128][ld].
+template <bool SPLIT>
+struct EpiValueResid {
+  void *out;
+  int64_t pair_stride, plane_stride;   // elements
+  int ld, n;
+  const float *Y;                      // [P][n][128]
+  __device__ void operator()(f32x16 (&acc)[2][2], int p, int row0, int col0, int, int, int lane, int) const {
+    const int h = lane >> 5, col = lane & 31;
+    for (int i = 0; i < 2; ++i)
+      for (int j = 0; j < 2; ++j) {
+        const int q = col0 + 32 * j + col;   // query index
+        for (int g = 0; g < 4; ++g) {
+          const int c0 = row0 + 32 * i + 8 * g + 4 * h;
+          f32x4 y = {0.f, 0.f, 0.f, 0.f};
+          if (q < n) y = *reinterpret_cast<const f32x4 *>(Y + ((size_t)p * n + q) * kHeadDim + c0);
+          for (int e = 0; e < 4; ++e) {
+            const float u = q < n ? y[e] - acc[i][j][4 * g + e] : 0.0f;
+            const size_t o = (size_t)p * pair_stride + (size_t)(c0 + e) * ld + q;
+            if constexpr (SPLIT) {
+              bf16 hi, lo;
+              split_bf16(u, hi, lo);
+              reinterpret_cast<bf16 *>(out)[o] = hi;
+              reinterpret_cast<bf16 *>(out)[o + plane_stride] = lo;
+            } else {
+              reinterpret_cast<float *>(out)[o] = u;
+            }
+          }
         }
       }
   }

@@ -41,12 +41,19 @@ def np64(x):
     return x.detach().float().cpu().numpy().astype(np.float64)
 
 
-def assignment_near_tie(Q, K, S, scale, j, rel):
-    """True if key j's best and runner-up anchor similarities are within rel."""
+def profile_dtype(wl):
+    """The precision the GPU stores response profiles in (bf16 or fp32 inputs)."""
+    return "bf16" if wl.dtype == "bf16" else "f32"
+
+
+def assignment_gap(Q, K, S, scale, j, pdt):
+    """Relative gap between key j's best and runner-up anchor similarity,
+    with profiles rounded to the storage precision pdt."""
     import oracle
     zm = oracle.global_logit_max(Q, K, scale)
-    _, US, _ = oracle.response_profiles(Q, K[S], scale, zm)
-    _, uj, _ = oracle.response_profiles(Q, K[j:j + 1], scale, zm)
-    sim = (uj.T @ US)[0]
+    ES = oracle.round_to(np.exp(oracle.logits(Q, K[S], scale) - zm), pdt)
+    US = oracle.round_to(ES / np.linalg.norm(ES, axis=0)[None, :], pdt)
+    ej = oracle.round_to(np.exp(oracle.logits(Q, K[j:j + 1], scale) - zm), pdt)[:, 0]
+    sim = ej @ US
     top = np.sort(sim)[::-1]
-    return len(top) < 2 or (top[0] - top[1]) <= rel * max(abs(top[0]), 1e-300)
+    return 0.0 if len(top) < 2 else (top[0] - top[1]) / max(abs(top[0]), 1e-300)

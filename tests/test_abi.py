@@ -56,7 +56,7 @@ def test_default_params():
     p = A.default_params()
     assert p.lambda_m == pytest.approx(0.25) and p.delta_beta == pytest.approx(1e-6)
     assert p.delta_v == pytest.approx(1e-3) and p.eps_w == pytest.approx(1e-12)
-    assert (p.b_min, p.b_max, p.bias_mode, p.max_escalations, p.refine_steps) == (-30.0, 30.0, 0, 3, 1)
+    assert (p.b_min, p.b_max, p.bias_mode, p.max_escalations, p.refine_steps) == (-30.0, 30.0, 0, 3, 2)
 
 
 def ws(prob, t, params=None):

@@ -15,7 +15,7 @@ import torch
 
 import oracle
 import synth
-from tests.gpu_common import TOL_OUT, assignment_near_tie, make_inputs, np64, scale_of
+from tests.gpu_common import TOL_OUT, assignment_gap, make_inputs, np64, profile_dtype, scale_of
 
 pytestmark = pytest.mark.gpu
 
@@ -51,7 +51,7 @@ def case(request):
     ref = []
     for b in range(wl.pairs):
         ref.append(oracle.compact_pair(host["K"][b], host["V"][b], host["Q"][b], host["W1"][b], host["b1"][b],
-                                       host["w2"][b], host["b2"][b], t=t, scale=s))
+                                       host["w2"][b], host["b2"][b], t=t, scale=s, profile_dtype=profile_dtype(wl)))
     return wl, dev, host, s, t, ref
 
 
@@ -117,20 +117,22 @@ def test_merge_stagewise(case):
     z = torch.from_numpy(np.stack([r.z for r in ref]).astype(np.float32)).cuda()
     Ck, kappa, phi = A().merge(dev["K"], dev["Q"], z, anchors, lambda_m=oracle.LAMBDA_M, scale=s)
     Ck, kappa, phi = np64(Ck), kappa.cpu().numpy(), np64(phi)
-    # Every similarity term e_ij * u_ir is >= 0, so the relative error of the
-    # sum is at most the per-term relative error: two roundings of the stored
-    # operands (bf16: 2^-9 each; fp32: 2^-24) plus fp32 accumulation (n 2^-24).
-    # A flip between two anchors needs a gap below twice that bound.
-    unit = 2.0 ** -9 if wl.dtype == "bf16" else 2.0 ** -24
-    rel_tie = 2.0 * (3 * unit + wl.n * 2.0 ** -24)
+    # The oracle takes the argmax on profiles rounded to the GPU's storage
+    # precision, so both sides decide kappa on the same stored values; what is
+    # left is fp32 accumulation order and rare one-ulp rounding differences of
+    # single profile entries.  A remaining flip must be a near-tie within one
+    # such ulp-sized term (2^-7 relative for bf16, 2^-23 + n 2^-24 for fp32).
+    rel_tie = 2.0 ** -7 if wl.dtype == "bf16" else 2.0 ** -23 + wl.n * 2.0 ** -24
     for b in range(wl.pairs):
         r = ref[b]
         K = host["K"][b]
         np.testing.assert_allclose(phi[b] / phi[b].sum(), r.phi / r.phi.sum(), rtol=1e-4, atol=1e-12)
         flips = np.flatnonzero(kappa[b] != r.kappa)
+        log(f"  pair {b}: {len(flips)} assignment differences out of {len(K)}")
         for j in flips:
-            assert assignment_near_tie(host["Q"][b], K, r.anchors, s, j, rel_tie), (b, j)
-        assert len(flips) <= max(2, len(K) // 200), (b, len(flips))
+            gap = assignment_gap(host["Q"][b], K, r.anchors, s, j, profile_dtype(wl))
+            assert gap <= rel_tie, (b, j, gap)
+        assert len(flips) <= max(1, len(K) // 1000), (b, len(flips))
         assert np.all(kappa[b][r.anchors] == np.arange(t))
         # C_k against the oracle merge on the GPU's assignment
         ck_ref = oracle.merge_keys(K, r.phi, kappa[b].astype(np.int64), r.anchors, oracle.LAMBDA_M)
