@@ -239,9 +239,10 @@ static int64_t chunk_for(const Dims &d, size_t ws_bytes, int64_t want) {
   if (ws_bytes < one) return 0;
   const size_t per = plan_total(d, 2) - one;
   int64_t P = 1 + (int64_t)((ws_bytes - one) / (per ? per : 1));
-  if (want > 0 && P > want) P = want;
-  if (P > d.B) P = d.B;
+  const int64_t cap = (want > 0 && want < d.B) ? want : d.B;
+  if (P > cap) P = cap;
   while (P > 1 && plan_total(d, P) > ws_bytes) --P;
+  while (P < cap && plan_total(d, P + 1) <= ws_bytes) ++P;
   return P;
 }
 

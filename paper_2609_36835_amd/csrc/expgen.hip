@@ -38,7 +38,9 @@ __global__ void __launch_bounds__(256) k_expgen(const T *__restrict__ Q, const v
   const bool rvalid = row < b_rows;
   const T *Bp = reinterpret_cast<const T *>(Bsrc) + (size_t)b * b_pair_stride;
   typename M::frag bf[NB][NKS];
+  #pragma unroll
   for (int p = 0; p < NB; ++p)
+    #pragma unroll
     for (int ks = 0; ks < NKS; ++ks)
       bf[p][ks] = rvalid ? M::load(Bp + p * b_plane_stride + (size_t)row * kHeadDim + ks * KSTEP + KPL * h)
                          : M::zero();
@@ -55,16 +57,21 @@ __global__ void __launch_bounds__(256) k_expgen(const T *__restrict__ Q, const v
       *reinterpret_cast<f32x4 *>(&sQ[r * SQ + cc]) = v;
     }
     __syncthreads();
+    #pragma unroll
     for (int ms = 0; ms < 2; ++ms) {
       f32x16 acc = zero16();
       const T *arow = &sQ[(32 * ms + col) * SQ + KPL * h];
+      #pragma unroll
       for (int ks = 0; ks < NKS; ++ks) {
         typename M::frag a = M::load(arow + ks * KSTEP);
+        #pragma unroll
         for (int p = 0; p < NB; ++p) acc = M::mma(a, bf[p][ks], acc);
       }
+      #pragma unroll
       for (int g = 0; g < 4; ++g) {
         const int ib = i0 + 32 * ms + 8 * g + 4 * h;   // 4 consecutive queries ib..ib+3
         float val[4], lg[4];
+        #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int i = ib + r;
           const bool ok = rvalid && i < n;
@@ -87,6 +94,7 @@ __global__ void __launch_bounds__(256) k_expgen(const T *__restrict__ Q, const v
         } else {
           bf16 *o = reinterpret_cast<bf16 *>(ob) + (size_t)b * out_pair_stride + (size_t)row * n_pad + ib;
           bf16x4 hi, lo;
+          #pragma unroll
           for (int r = 0; r < 4; ++r) {
             bf16 a, c;
             split_bf16(val[r], a, c);

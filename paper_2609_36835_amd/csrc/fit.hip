@@ -130,8 +130,10 @@ __device__ void update_tile(const float *sA, const float *sB, float *C, int64_t 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wi = wave >> 1, wj = wave & 1, h = lane >> 5, col = lane & 31;
   f32x16 acc = zero16();
+  #pragma unroll
   for (int ks = 0; ks < kNB / 2; ++ks)
     acc = Mfma<float>::mma(sA[(32 * wi + col) * kSD + 2 * ks + h], sB[(32 * wj + col) * kSD + 2 * ks + h], acc);
+  #pragma unroll
   for (int v = 0; v < 16; ++v) {
     const int r = 32 * wi + acc_row(v, lane), c = 32 * wj + col;
     C[(size_t)r * ld + c] -= acc[v];
@@ -143,9 +145,11 @@ __device__ void update_tile_lds(const float *sA, const float *sB, float *sC) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wi = wave >> 1, wj = wave & 1, h = lane >> 5, col = lane & 31;
   f32x16 acc = zero16();
+  #pragma unroll
   for (int ks = 0; ks < kNB / 2; ++ks)
     acc = Mfma<float>::mma(sA[(32 * wi + col) * kSD + 2 * ks + h], sB[(32 * wj + col) * kSD + 2 * ks + h], acc);
   __syncthreads();
+  #pragma unroll
   for (int v = 0; v < 16; ++v) sC[(32 * wi + acc_row(v, lane)) * kSD + 32 * wj + col] -= acc[v];
   __syncthreads();
 }
@@ -521,6 +525,7 @@ __global__ void __launch_bounds__(256) k_trsm(const float *__restrict__ Gw, int6
     const int kb = FWD ? step : nb - 1 - step;
     const int r0 = kb * RB;
     float acc[8];
+    #pragma unroll
     for (int e = 0; e < 8; ++e) acc[e] = Rb[(size_t)(r0 + 8 * g + e) * kHeadDim + c0 + c];
     const int p_beg = FWD ? 0 : r0 + RB, p_end = FWD ? r0 : (int)ld;
     for (int p0 = p_beg; p0 < p_end; p0 += RB) {
@@ -537,6 +542,7 @@ __global__ void __launch_bounds__(256) k_trsm(const float *__restrict__ Gw, int6
       __syncthreads();
       for (int pp = 0; pp < RB; ++pp) {
         const float yv = sY[pp][c];
+        #pragma unroll
         for (int e = 0; e < 8; ++e) acc[e] -= sL[8 * g + e][pp] * yv;
       }
     }
@@ -545,6 +551,7 @@ __global__ void __launch_bounds__(256) k_trsm(const float *__restrict__ Gw, int6
       const int rr = e / RB, pp = e % RB;
       sL[rr][pp] = L[(size_t)(r0 + rr) * ld + r0 + pp];
     }
+    #pragma unroll
     for (int e = 0; e < 8; ++e) sY[8 * g + e][c] = acc[e];
     __syncthreads();
     if (g == 0) {
@@ -563,6 +570,7 @@ __global__ void __launch_bounds__(256) k_trsm(const float *__restrict__ Gw, int6
       }
     }
     __syncthreads();
+    #pragma unroll
     for (int e = 0; e < 8; ++e) Xb[(size_t)(r0 + 8 * g + e) * kHeadDim + c0 + c] = sY[8 * g + e][c];
     __threadfence_block();
   }

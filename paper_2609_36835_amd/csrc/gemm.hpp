@@ -85,35 +85,49 @@ __global__ void __launch_bounds__(256) k_gemm_tn(GemmShape g, const T *__restric
 
   f32x4 ra[NA][CH], rb[NB][CH];
   auto prefetch = [&](int k0) {
+    #pragma unroll
     for (int c = 0; c < CH; ++c) {
       const int idx = tid + 256 * c, r = idx / CPR, cc = (idx % CPR) * EPC;
+      #pragma unroll
       for (int q = 0; q < NA; ++q)
         ra[q][c] = *reinterpret_cast<const f32x4 *>(Ab + q * g.a_plane + (size_t)r * g.lda + k0 + cc);
+      #pragma unroll
       for (int q = 0; q < NB; ++q)
         rb[q][c] = *reinterpret_cast<const f32x4 *>(Bb + q * g.b_plane + (size_t)r * g.ldb + k0 + cc);
     }
   };
   f32x16 acc[2][2];
+  #pragma unroll
   for (int i = 0; i < 2; ++i)
+    #pragma unroll
     for (int j = 0; j < 2; ++j) acc[i][j] = zero16();
 
   prefetch(0);
   for (int k0 = 0; k0 < g.K; k0 += kGBK) {
     __syncthreads();
+    #pragma unroll
     for (int c = 0; c < CH; ++c) {
       const int idx = tid + 256 * c, r = idx / CPR, cc = (idx % CPR) * EPC;
+      #pragma unroll
       for (int q = 0; q < NA; ++q) *reinterpret_cast<f32x4 *>(&sA[q][r * SL + cc]) = ra[q][c];
+      #pragma unroll
       for (int q = 0; q < NB; ++q) *reinterpret_cast<f32x4 *>(&sB[q][r * SL + cc]) = rb[q][c];
     }
     __syncthreads();
     if (k0 + kGBK < g.K) prefetch(k0 + kGBK);
+    #pragma unroll
     for (int ks = 0; ks < kGBK / KSTEP; ++ks) {
       typename Mf::frag fa[NA][2], fb[NB][2];
+      #pragma unroll
       for (int i = 0; i < 2; ++i) {
+        #pragma unroll
         for (int q = 0; q < NA; ++q) fa[q][i] = Mf::load(&sA[q][(wm * 64 + 32 * i + col) * SL + ks * KSTEP + KPL * h]);
+        #pragma unroll
         for (int q = 0; q < NB; ++q) fb[q][i] = Mf::load(&sB[q][(wn * 64 + 32 * i + col) * SL + ks * KSTEP + KPL * h]);
       }
+      #pragma unroll
       for (int i = 0; i < 2; ++i)
+        #pragma unroll
         for (int j = 0; j < 2; ++j) {
           acc[i][j] = Mf::mma(fa[0][i], fb[0][j], acc[i][j]);
           if constexpr (NB > 1) acc[i][j] = Mf::mma(fa[0][i], fb[1][j], acc[i][j]);
@@ -132,13 +146,16 @@ struct EpiArgmax {
   uint64_t *part;       // [P][MT][Np]
   int64_t pair_stride;  // MT * Np
   int Np, t;
-  __device__ void operator()(f32x16 (&acc)[2][2], int p, int row0, int col0, int mt, int nt, int lane,
+  __device__ __forceinline__ void operator()(f32x16 (&acc)[2][2], int p, int row0, int col0, int mt, int nt, int lane,
                              int wm) const {
     __shared__ uint64_t red[128];
     const int h = lane >> 5, col = lane & 31;
     uint64_t best[2] = {0ull, 0ull};
+    #pragma unroll
     for (int j = 0; j < 2; ++j)
+      #pragma unroll
       for (int i = 0; i < 2; ++i)
+        #pragma unroll
         for (int v = 0; v < 16; ++v) {
           const int r = row0 + 32 * i + acc_row(v, lane);
           if (r < t) {
@@ -146,15 +163,18 @@ struct EpiArgmax {
             best[j] = key > best[j] ? key : best[j];
           }
         }
+    #pragma unroll
     for (int j = 0; j < 2; ++j) {
       uint64_t o = __shfl_xor(best[j], 32, 64);
       best[j] = o > best[j] ? o : best[j];
     }
     const int cl = col0 - nt * kGBN;   // 0 or 64 within the block
     if (wm == 1 && h == 0)
+      #pragma unroll
       for (int j = 0; j < 2; ++j) red[cl + 32 * j + col] = best[j];
     __syncthreads();
     if (wm == 0 && h == 0)
+      #pragma unroll
       for (int j = 0; j < 2; ++j) {
         uint64_t o = red[cl + 32 * j + col];
         uint64_t bb = o > best[j] ? o : best[j];
@@ -169,15 +189,19 @@ struct EpiSym {
   float *G, *Gc;
   int64_t pair_stride;  // ld * ld
   int ld;
-  __device__ void operator()(f32x16 (&acc)[2][2], int p, int row0, int col0, int mt, int nt, int lane,
+  __device__ __forceinline__ void operator()(f32x16 (&acc)[2][2], int p, int row0, int col0, int mt, int nt, int lane,
                              int) const {
     const int h = lane >> 5, col = lane & 31;
     float *Gp = G + (size_t)p * pair_stride, *Gcp = Gc + (size_t)p * pair_stride;
+    #pragma unroll
     for (int i = 0; i < 2; ++i)
+      #pragma unroll
       for (int j = 0; j < 2; ++j) {
         const int c = col0 + 32 * j + col;
+        #pragma unroll
         for (int g = 0; g < 4; ++g) {
           const int r0 = row0 + 32 * i + 8 * g + 4 * h;
+          #pragma unroll
           for (int e = 0; e < 4; ++e) {
             Gp[(size_t)(r0 + e) * ld + c] = acc[i][j][4 * g + e];
             Gcp[(size_t)(r0 + e) * ld + c] = acc[i][j][4 * g + e];
@@ -200,12 +224,15 @@ struct EpiStore {
   int ld;
   const float *X;        // nullptr: plain store
   const float *lam;      // [P]
-  __device__ void operator()(f32x16 (&acc)[2][2], int p, int row0, int col0, int, int, int lane, int) const {
+  __device__ __forceinline__ void operator()(f32x16 (&acc)[2][2], int p, int row0, int col0, int, int, int lane, int) const {
     const size_t base = (size_t)p * pair_stride;
     const int col = lane & 31;
+    #pragma unroll
     for (int i = 0; i < 2; ++i)
+      #pragma unroll
       for (int j = 0; j < 2; ++j) {
         const int c = col0 + 32 * j + col;
+        #pragma unroll
         for (int v = 0; v < 16; ++v) {
           const int r = row0 + 32 * i + acc_row(v, lane);
           const size_t o = base + (size_t)r * ld + c;
@@ -225,15 +252,19 @@ struct EpiValueResid {
   int64_t pair_stride, plane_stride;   // elements
   int ld, n;
   const float *Y;                      // [P][n][128]
-  __device__ void operator()(f32x16 (&acc)[2][2], int p, int row0, int col0, int, int, int lane, int) const {
+  __device__ __forceinline__ void operator()(f32x16 (&acc)[2][2], int p, int row0, int col0, int, int, int lane, int) const {
     const int h = lane >> 5, col = lane & 31;
+    #pragma unroll
     for (int i = 0; i < 2; ++i)
+      #pragma unroll
       for (int j = 0; j < 2; ++j) {
         const int q = col0 + 32 * j + col;   // query index
+        #pragma unroll
         for (int g = 0; g < 4; ++g) {
           const int c0 = row0 + 32 * i + 8 * g + 4 * h;
           f32x4 y = {0.f, 0.f, 0.f, 0.f};
           if (q < n) y = *reinterpret_cast<const f32x4 *>(Y + ((size_t)p * n + q) * kHeadDim + c0);
+          #pragma unroll
           for (int e = 0; e < 4; ++e) {
             const float u = q < n ? y[e] - acc[i][j][4 * g + e] : 0.0f;
             const size_t o = (size_t)p * pair_stride + (size_t)(c0 + e) * ld + q;

@@ -103,6 +103,7 @@ __global__ void __launch_bounds__(64) k_group_sort(const int32_t *__restrict__ k
     const int r = r0 + lane;
     int32_t c = r < t ? atomicAdd(&cur[r], 0) : 0;
     int32_t x = c;
+    #pragma unroll
     for (int d = 1; d < 64; d <<= 1) {
       int32_t y = __shfl_up(x, d, 64);
       if (lane >= d) x += y;

@@ -41,12 +41,14 @@ __global__ void __launch_bounds__(256) k_rowstats(const T *__restrict__ K, const
   typename M::frag qf[kHeadDim / KSTEP];
   {
     const T *qrow = Q + ((size_t)b * n + (qvalid ? q : 0)) * kHeadDim;
+    #pragma unroll
     for (int ks = 0; ks < kHeadDim / KSTEP; ++ks)
       qf[ks] = qvalid ? M::load(qrow + ks * KSTEP + KPL * h) : M::zero();
   }
   const float c2 = scale * 1.4426950408889634f;   // exp(s x) = exp2(c2 x)
   float run_max = -INFINITY, run_sum = 0.0f;
   f32x16 accY[4];
+  #pragma unroll
   for (int cs = 0; cs < 4; ++cs) accY[cs] = zero16();
 
   for (int k0 = 0; k0 < Tn; k0 += KB) {
@@ -64,17 +66,22 @@ __global__ void __launch_bounds__(256) k_rowstats(const T *__restrict__ K, const
       }
       *reinterpret_cast<f32x4 *>(&sK[r * SK + cc]) = kv;
       const T *ve = reinterpret_cast<const T *>(&vv);
+      #pragma unroll
       for (int e = 0; e < EPC; ++e) sVt[(cc + e) * SV + r] = ve[e];
     }
     __syncthreads();
     f32x16 accS[NSUB];
+    #pragma unroll
     for (int ms = 0; ms < NSUB; ++ms) {
       accS[ms] = zero16();
       const T *arow = &sK[(32 * ms + col) * SK + KPL * h];
+      #pragma unroll
       for (int ks = 0; ks < kHeadDim / KSTEP; ++ks) accS[ms] = M::mma(M::load(arow + ks * KSTEP), qf[ks], accS[ms]);
     }
     float bmax = -INFINITY;
+    #pragma unroll
     for (int ms = 0; ms < NSUB; ++ms)
+      #pragma unroll
       for (int v = 0; v < 16; ++v) {
         if (k0 + 32 * ms + acc_row(v, lane) >= Tn) accS[ms][v] = -INFINITY;
         bmax = fmaxf(bmax, accS[ms][v]);
@@ -84,30 +91,38 @@ __global__ void __launch_bounds__(256) k_rowstats(const T *__restrict__ K, const
     const float alpha = exp2f((run_max - new_max) * c2);
     run_max = new_max;
     float psum = 0.0f;
+    #pragma unroll
     for (int ms = 0; ms < NSUB; ++ms)
+      #pragma unroll
       for (int v = 0; v < 16; ++v) {
         float p = exp2f((accS[ms][v] - new_max) * c2);
         accS[ms][v] = p;
         psum += p;
       }
     run_sum = run_sum * alpha + psum;
+    #pragma unroll
     for (int cs = 0; cs < 4; ++cs)
+      #pragma unroll
       for (int v = 0; v < 16; ++v) accY[cs][v] *= alpha;
     // Y^T += V^T P^T over this tile's keys, k-slots permuted to the accumulator layout
+    #pragma unroll
     for (int kk = 0; kk < KB / KSTEP; ++kk) {
       typename M::frag pf;
       int keys[KPL];
+      #pragma unroll
       for (int e = 0; e < KPL; ++e) {
         int vv = kk * KPL + e, ms = vv >> 4, v = vv & 15;
         keys[e] = 32 * ms + acc_row(v, lane);
         if constexpr (KPL == 1) pf = (T)accS[ms][v];
         else pf[e] = (T)accS[ms][v];
       }
+      #pragma unroll
       for (int cs = 0; cs < 4; ++cs) {
         const T *vrow = &sVt[(32 * cs + col) * SV];
         typename M::frag vf;
         if constexpr (KPL == 1) vf = vrow[keys[0]];
         else
+          #pragma unroll
           for (int e = 0; e < KPL; ++e) vf[e] = vrow[keys[e]];
         accY[cs] = M::mma(vf, pf, accY[cs]);
       }
@@ -118,7 +133,9 @@ __global__ void __launch_bounds__(256) k_rowstats(const T *__restrict__ K, const
   if (!qvalid) return;
   const float inv = 1.0f / run_sum;
   float *yrow = Y + ((size_t)b * n + q) * kHeadDim;
+  #pragma unroll
   for (int cs = 0; cs < 4; ++cs)
+    #pragma unroll
     for (int g = 0; g < 4; ++g) {
       f32x4 o = {accY[cs][4 * g] * inv, accY[cs][4 * g + 1] * inv, accY[cs][4 * g + 2] * inv,
                  accY[cs][4 * g + 3] * inv};

@@ -37,12 +37,14 @@ __global__ void __launch_bounds__(256) k_score_bf16(const bf16 *__restrict__ K, 
   const size_t row_off = ((size_t)b * T + (valid ? tok : 0)) * kHeadDim;
   // B fragments: token `tok`, features 16*ks + 8*h .. +7 (ks < 8 from K, else V)
   bf16x8 xb[16];
+  #pragma unroll
   for (int ks = 0; ks < 16; ++ks) {
     const bf16 *src = (ks < 8 ? K : V) + row_off + (ks & 7) * 16 + 8 * h;
     xb[ks] = valid ? *reinterpret_cast<const bf16x8 *>(src) : Mfma<bf16>::zero();
   }
   __syncthreads();
   f32x16 acc0 = zero16(), acc1 = zero16();
+  #pragma unroll
   for (int ks = 0; ks < 16; ++ks) {
     bf16x8 a0 = *reinterpret_cast<const bf16x8 *>(&sW[col * kW1Stride + ks * 16 + 8 * h]);
     bf16x8 a1 = *reinterpret_cast<const bf16x8 *>(&sW[(32 + col) * kW1Stride + ks * 16 + 8 * h]);
@@ -51,6 +53,7 @@ __global__ void __launch_bounds__(256) k_score_bf16(const bf16 *__restrict__ K, 
   }
   const float *b1b = b1 + b * kHidden, *w2b = w2 + b * kHidden;
   float part = 0.0f;
+  #pragma unroll
   for (int v = 0; v < 16; ++v) {
     int m0 = acc_row(v, lane);
     part += w2b[m0] * gelu_erf(acc0[v] + b1b[m0]);
