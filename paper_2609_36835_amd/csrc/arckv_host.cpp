@@ -317,7 +317,8 @@ static arckv_status run_merge_chunk(const Ctx &c, int b0, int P, const void *K, 
                                      d.np_, c.scale, stream));
   STAGE(ST_ANCHOR_PROF, launch_anchor_profiles(d.dtype, Et, anc, U, P, d.t, d.Tp, d.np_, d.tp, stream));
   STAGE(ST_ASSIGN, launch_assign_gemm(d.dtype, U, Et, part, P, d.t, d.tp, d.Tp, d.np_, stream));
-  STAGE(ST_FINALIZE, launch_assign_finalize(part, (int)d.MT, d.Tp, anchor_of + (size_t)b0 * d.T, P, d.T,
+  const int mt_used = (int)(d.dtype == ARCKV_BF16 ? d.tp / 256 : d.tp / 128);
+  STAGE(ST_FINALIZE, launch_assign_finalize(part, mt_used, d.Tp, anchor_of + (size_t)b0 * d.T, P, d.T,
                                             kappa + (size_t)b0 * d.T, stream));
   STAGE(ST_MERGE, launch_group_merge(d.dtype, Kc, phi + (size_t)b0 * d.T, kappa + (size_t)b0 * d.T, anc, P, d.T,
                                      d.t, d.tp, lambda_m, c.chunk<int32_t>(c.pl.offsets),

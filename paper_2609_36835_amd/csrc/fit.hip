@@ -277,13 +277,24 @@ __global__ void __launch_bounds__(256) k_chol_escalate(float *__restrict__ Gw, c
 }
 
 // --------------------------------------------------------------- one right-hand side
+__device__ inline double readlane_f64(double v, int lane) {
+  const int64_t bits = __double_as_longlong(v);
+  const int lo = __builtin_amdgcn_readlane((int)(bits & 0xFFFFFFFF), lane);
+  const int hi = __builtin_amdgcn_readlane((int)(bits >> 32), lane);
+  return __longlong_as_double(((int64_t)hi << 32) | (uint32_t)lo);
+}
+
 // Forward L y = rhs, then backward L^T x = y, float64 accumulation; x written
-// to `x` (and added to `acc` if non-null).  One workgroup per pair.
+// to `x` (and added to `acc` if non-null).  One workgroup per pair, 64-row
+// blocks.  Off-diagonal products: each lane accumulates 16 rows over a strided
+// set of columns and a single LDS pass reduces them; diagonal blocks: column
+// substitution in one wave with the solved value broadcast by readlane.
 __global__ void __launch_bounds__(256) k_trsv(const float *__restrict__ Gw, int64_t ld, const double *__restrict__ rhs,
                                               double *__restrict__ y, double *__restrict__ x,
                                               double *__restrict__ acc, const int32_t *__restrict__ info) {
-  __shared__ double part[4][kNB];
-  __shared__ double sy[kNB];
+  __shared__ double red[kNB][kNB + 1];
+  __shared__ float sD[kNB * kSD];
+  __shared__ double sb[kNB];
   const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   if (info[b] != 0) return;
   const float *L = Gw + (size_t)b * ld * ld;
@@ -292,23 +303,29 @@ __global__ void __launch_bounds__(256) k_trsv(const float *__restrict__ Gw, int6
   const int nrb = (int)(ld / kNB);
   for (int kb = 0; kb < nrb; ++kb) {
     const int r0 = kb * kNB;
-    for (int rr = wave; rr < kNB; rr += 4) {  // partial sums over earlier blocks
-      const float *row = L + (size_t)(r0 + rr) * ld;
-      double s = 0.0;
-      for (int c = lane; c < r0; c += 64) s += (double)row[c] * yb[c];
-      s = wave_sum(s);
-      if (lane == 0) sy[rr] = rb[r0 + rr] - s;
+    double part[16];
+#pragma unroll
+    for (int q = 0; q < 16; ++q) part[q] = 0.0;
+    for (int c = lane; c < r0; c += 64) {
+      const double yc = yb[c];
+#pragma unroll
+      for (int q = 0; q < 16; ++q) part[q] += (double)L[(size_t)(r0 + 16 * wave + q) * ld + c] * yc;
     }
+#pragma unroll
+    for (int q = 0; q < 16; ++q) red[16 * wave + q][lane] = part[q];
+    for (int e = tid; e < kNB * kNB; e += 256) sD[(e / kNB) * kSD + e % kNB] = L[(size_t)(r0 + e / kNB) * ld + r0 + e % kNB];
     __syncthreads();
     if (wave == 0) {
-      double mine = 0.0;
-      for (int rr = 0; rr < kNB; ++rr) {
-        double term = lane < rr ? (double)L[(size_t)(r0 + rr) * ld + r0 + lane] * mine : 0.0;
-        term = wave_sum(term);
-        const double v = (sy[rr] - term) / (double)L[(size_t)(r0 + rr) * ld + r0 + rr];
-        if (lane == rr) mine = v;
+      double s = 0.0;
+      for (int c = 0; c < 64; ++c) s += red[lane][c];
+      double bv = rb[r0 + lane] - s, yv = 0.0;
+      for (int q = 0; q < kNB; ++q) {
+        const double v = bv / (double)sD[q * kSD + q];
+        const double yq = readlane_f64(v, q);
+        if (lane == q) yv = yq;
+        if (lane > q) bv -= (double)sD[lane * kSD + q] * yq;
       }
-      yb[r0 + lane] = mine;
+      yb[r0 + lane] = yv;
     }
     __threadfence_block();
     __syncthreads();
@@ -318,20 +335,19 @@ __global__ void __launch_bounds__(256) k_trsv(const float *__restrict__ Gw, int6
     const int c = tid & 63, g = tid >> 6;
     double s = 0.0;
     for (int64_t i = c0 + kNB + g; i < ld; i += 4) s += (double)L[(size_t)i * ld + c0 + c] * xb[i];
-    part[g][c] = s;
+    red[g][c] = s;
+    for (int e = tid; e < kNB * kNB; e += 256) sD[(e / kNB) * kSD + e % kNB] = L[(size_t)(c0 + e / kNB) * ld + c0 + e % kNB];
     __syncthreads();
     if (wave == 0) {
-      const double base = yb[c0 + lane] - (part[0][lane] + part[1][lane] + part[2][lane] + part[3][lane]);
-      double mine = 0.0;
-      for (int rr = kNB - 1; rr >= 0; --rr) {
-        double term = lane > rr ? (double)L[(size_t)(c0 + lane) * ld + c0 + rr] * mine : 0.0;
-        term = wave_sum(term);
-        const double bse = __shfl(base, rr, 64);
-        const double v = (bse - term) / (double)L[(size_t)(c0 + rr) * ld + c0 + rr];
-        if (lane == rr) mine = v;
+      double bv = yb[c0 + lane] - (red[0][lane] + red[1][lane] + red[2][lane] + red[3][lane]), xv = 0.0;
+      for (int q = kNB - 1; q >= 0; --q) {
+        const double v = bv / (double)sD[q * kSD + q];
+        const double xq = readlane_f64(v, q);
+        if (lane == q) xv = xq;
+        if (lane < q) bv -= (double)sD[q * kSD + lane] * xq;
       }
-      xb[c0 + lane] = mine;
-      if (acc) acc[(size_t)b * ld + c0 + lane] += mine;
+      xb[c0 + lane] = xv;
+      if (acc) acc[(size_t)b * ld + c0 + lane] += xv;
     }
     __threadfence_block();
     __syncthreads();
@@ -576,6 +592,94 @@ __global__ void __launch_bounds__(256) k_trsm(const float *__restrict__ Gw, int6
   }
 }
 
+// MFMA variant of the 128-rhs substitution: two workgroups per pair, 64
+// columns each; 64-row blocks.  The update  acc = sum_p L_blk,p X_p  (forward)
+// or  sum_p L_p,blk^T X_p  (backward) runs on fp32 MFMA 32x32x2 with the L
+// tile and the X tile staged in LDS (4 waves = 2 row tiles x 2 column tiles);
+// the 64 x 64 diagonal block is then solved column-parallel in LDS.
+template <bool FWD>
+__global__ void __launch_bounds__(256) k_trsm_mfma(const float *__restrict__ Gw, int64_t ld,
+                                                   const float *__restrict__ R, float *__restrict__ X,
+                                                   const int32_t *__restrict__ info) {
+  constexpr int RB = 64, NC = 64, SLD = RB + 1, SXD = NC + 1;
+  __shared__ float sL[RB * SLD];
+  __shared__ float sX[RB * SXD];
+  const int b = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  if (info[b] != 0) return;
+  const int wr = wave >> 1, wc = wave & 1, h = lane >> 5, col = lane & 31;
+  const int c0 = blockIdx.x * NC;
+  const float *L = Gw + (size_t)b * ld * ld;
+  const float *Rb = R + (size_t)b * ld * kHeadDim;
+  float *Xb = X + (size_t)b * ld * kHeadDim;
+  const int nb = (int)(ld / RB);
+  for (int step = 0; step < nb; ++step) {
+    const int kb = FWD ? step : nb - 1 - step;
+    const int r0 = kb * RB;
+    f32x16 acc = zero16();
+    const int pb0 = FWD ? 0 : kb + 1, pb1 = FWD ? kb : nb;
+    for (int pb = pb0; pb < pb1; ++pb) {
+      const int p0 = pb * RB;
+      __syncthreads();
+      for (int e = tid; e < RB * RB / 4; e += 256) {
+        const int i = e / 16, k4 = (e % 16) * 4;
+        if (FWD) {   // sL[i][k] = L[r0 + i][p0 + k]
+          const f32x4 v = *reinterpret_cast<const f32x4 *>(L + (size_t)(r0 + i) * ld + p0 + k4);
+#pragma unroll
+          for (int q = 0; q < 4; ++q) sL[i * SLD + k4 + q] = v[q];
+        } else {     // sL[i][k] = L[p0 + k][r0 + i]  (row k of L read contiguously)
+          const f32x4 v = *reinterpret_cast<const f32x4 *>(L + (size_t)(p0 + i) * ld + r0 + k4);
+#pragma unroll
+          for (int q = 0; q < 4; ++q) sL[(k4 + q) * SLD + i] = v[q];
+        }
+      }
+      for (int e = tid; e < RB * NC / 4; e += 256) {
+        const int k = e / 16, c4 = (e % 16) * 4;
+        const f32x4 v = *reinterpret_cast<const f32x4 *>(Xb + (size_t)(p0 + k) * kHeadDim + c0 + c4);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) sX[k * SXD + c4 + q] = v[q];
+      }
+      __syncthreads();
+#pragma unroll 8
+      for (int ks = 0; ks < RB / 2; ++ks)
+        acc = Mfma<float>::mma(sL[(32 * wr + col) * SLD + 2 * ks + h], sX[(2 * ks + h) * SXD + 32 * wc + col], acc);
+    }
+    __syncthreads();
+    // right-hand side minus update, into sX; diagonal block into sL (transposed for backward)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int r = 32 * wr + acc_row(v, lane), c = 32 * wc + col;
+      sX[r * SXD + c] = Rb[(size_t)(r0 + r) * kHeadDim + c0 + c] - acc[v];
+    }
+    for (int e = tid; e < RB * RB; e += 256) {
+      const int i = e / RB, k = e % RB;
+      sL[i * SLD + k] = FWD ? L[(size_t)(r0 + i) * ld + r0 + k] : L[(size_t)(r0 + k) * ld + r0 + i];
+    }
+    __syncthreads();
+    if (tid < NC) {
+      const int c = tid;
+      if (FWD) {
+        for (int r = 0; r < RB; ++r) {
+          float v = sX[r * SXD + c];
+          for (int q = 0; q < r; ++q) v -= sL[r * SLD + q] * sX[q * SXD + c];
+          sX[r * SXD + c] = v / sL[r * SLD + r];
+        }
+      } else {
+        for (int r = RB - 1; r >= 0; --r) {
+          float v = sX[r * SXD + c];
+          for (int q = r + 1; q < RB; ++q) v -= sL[r * SLD + q] * sX[q * SXD + c];
+          sX[r * SXD + c] = v / sL[r * SLD + r];
+        }
+      }
+    }
+    __syncthreads();
+    for (int e = tid; e < RB * NC; e += 256) {
+      const int r = e / NC, c = e % NC;
+      Xb[(size_t)(r0 + r) * kHeadDim + c0 + c] = sX[r * SXD + c];
+    }
+    __threadfence_block();
+  }
+}
+
 __global__ void __launch_bounds__(256) k_add_copy(float *__restrict__ x, const float *__restrict__ dx, int64_t n_per,
                                                   const int32_t *__restrict__ info) {
   const int b = blockIdx.y;
@@ -681,9 +785,9 @@ hipError_t launch_trsm(bool fwd, const float *Gw, int B, int64_t ld, const float
                        hipStream_t s) {
   dim3 grid(kHeadDim / 64, B);
   if (fwd)
-    hipLaunchKernelGGL(k_trsm<true>, grid, dim3(256), 0, s, Gw, ld, R, X, info);
+    hipLaunchKernelGGL(k_trsm_mfma<true>, grid, dim3(256), 0, s, Gw, ld, R, X, info);
   else
-    hipLaunchKernelGGL(k_trsm<false>, grid, dim3(256), 0, s, Gw, ld, R, X, info);
+    hipLaunchKernelGGL(k_trsm_mfma<false>, grid, dim3(256), 0, s, Gw, ld, R, X, info);
   return hipGetLastError();
 }
 
