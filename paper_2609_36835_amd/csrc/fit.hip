@@ -4,11 +4,13 @@
 // M a float32 Gram matrix of size tp (padded; the padding is an identity
 // block with zero right-hand side, so padded unknowns solve to 0):
 //   k_ridge_init     lam = delta * tr(M)/t, write M + lam I into the work copy
-//   Cholesky         right-looking, 64-wide blocks, float32:
-//                      k_chol_diag0   factor diagonal block 0
+//   Cholesky         right-looking, float32, two-level blocking:
+//                      k_chol_diag    factor a 64 x 64 diagonal block in LDS
 //                      k_chol_panel   L_ik = A_ik L_kk^-T for row blocks i > k
-//                      k_chol_update  A_ij -= L_ik L_jk^T (fp32 MFMA); the tile
-//                                     (k+1, k+1) is then factored in place
+//                      k_chol_upd     A -= L L^T over a panel's columns
+//                                     (fp32 MFMA, 128 x 128 tiles), once per
+//                                     64 columns inside a 256-wide outer panel
+//                                     and once per outer panel for the rest
 //                    a failed pivot records info = column + 1 for that pair
 //   k_chol_escalate  for pairs that failed: restore, delta *= 10, refactor in
 //                    one workgroup; at most max_escalations times
@@ -140,42 +142,6 @@ __device__ void update_tile(const float *sA, const float *sB, float *C, int64_t 
   }
 }
 
-// sC -= A B^T with every operand in LDS.
-__device__ void update_tile_lds(const float *sA, const float *sB, float *sC) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int wi = wave >> 1, wj = wave & 1, h = lane >> 5, col = lane & 31;
-  f32x16 acc = zero16();
-  #pragma unroll
-  for (int ks = 0; ks < kNB / 2; ++ks)
-    acc = Mfma<float>::mma(sA[(32 * wi + col) * kSD + 2 * ks + h], sB[(32 * wj + col) * kSD + 2 * ks + h], acc);
-  __syncthreads();
-  #pragma unroll
-  for (int v = 0; v < 16; ++v) sC[(32 * wi + acc_row(v, lane)) * kSD + 32 * wj + col] -= acc[v];
-  __syncthreads();
-}
-
-__device__ inline void decode_lower(int idx, int &a, int &bb) {
-  int m = (int)((sqrtf(8.0f * (float)idx + 1.0f) - 1.0f) * 0.5f);
-  while (m * (m + 1) / 2 > idx) --m;
-  while ((m + 1) * (m + 2) / 2 <= idx) ++m;
-  a = m;
-  bb = idx - m * (m + 1) / 2;
-}
-
-__global__ void __launch_bounds__(256) k_chol_diag0(float *__restrict__ Gw, int64_t ld, int32_t *__restrict__ info) {
-  __shared__ float sD[kNB * kSD];
-  const int b = blockIdx.x;
-  if (info[b] != 0) return;
-  float *G = Gw + (size_t)b * ld * ld;
-  load_tile(sD, G, ld);
-  const int fail = factor_tile(sD);
-  if (fail >= 0) {
-    if (threadIdx.x == 0) info[b] = fail + 1;
-    return;
-  }
-  store_tile(sD, G, ld);
-}
-
 __global__ void __launch_bounds__(256) k_chol_panel(float *__restrict__ Gw, int64_t ld, int k,
                                                     const int32_t *__restrict__ info) {
   __shared__ float sL[kNB * kSD], sX[kNB * kSD];
@@ -189,33 +155,86 @@ __global__ void __launch_bounds__(256) k_chol_panel(float *__restrict__ Gw, int6
   store_tile(sX, G + (size_t)i * kNB * ld + k * kNB, ld);
 }
 
-__global__ void __launch_bounds__(256) k_chol_update(float *__restrict__ Gw, int64_t ld, int k,
-                                                     int32_t *__restrict__ info) {
-  __shared__ float sA[kNB * kSD], sB[kNB * kSD];
-  const int b = blockIdx.y;
+// Factor the 64 x 64 diagonal block k in place (one workgroup per pair).
+__global__ void __launch_bounds__(256) k_chol_diag(float *__restrict__ Gw, int64_t ld, int k,
+                                                   int32_t *__restrict__ info) {
+  __shared__ float sD[kNB * kSD];
+  const int b = blockIdx.x;
   if (info[b] != 0) return;
-  int a, bb;
-  decode_lower(blockIdx.x, a, bb);
-  const int i = k + 1 + a, j = k + 1 + bb;
-  float *G = Gw + (size_t)b * ld * ld;
-  load_tile(sA, G + (size_t)i * kNB * ld + k * kNB, ld);
-  if (i != j) load_tile(sB, G + (size_t)j * kNB * ld + k * kNB, ld);
-  __syncthreads();
-  float *C = G + (size_t)i * kNB * ld + j * kNB;
-  if (i == j && i == k + 1) {
-    // the next diagonal block: update it in LDS and factor it right away
-    load_tile(sB, C, ld);
-    __syncthreads();
-    update_tile_lds(sA, sA, sB);
-    const int fail = factor_tile(sB);
-    if (fail >= 0) {
-      if (threadIdx.x == 0) info[b] = i * kNB + fail + 1;
-      return;
-    }
-    store_tile(sB, C, ld);
+  float *D = Gw + (size_t)b * ld * ld + (size_t)k * kNB * ld + k * kNB;
+  load_tile(sD, D, ld);
+  const int fail = factor_tile(sD);
+  if (fail >= 0) {
+    if (threadIdx.x == 0) info[b] = k * kNB + fail + 1;
     return;
   }
-  update_tile(sA, i != j ? sB : sA, C, ld);
+  store_tile(sD, D, ld);
+}
+
+// Trailing update of the blocked factorisation on fp32 MFMA:
+//   G[r][c] -= sum_{q in [q0, q0+kw)} L[r][q] L[c][q]
+// for r in [r_lo, ld), c in [c_lo, c_hi), with 128 x 128 output tiles (4
+// waves of 64 x 64) starting at (r_lo, c_lo); tiles entirely above the
+// diagonal exit at once, and rows/columns past the region are masked.  The L
+// operands are the finished panel columns [q0, q0+kw), streamed through LDS
+// in slabs of 32.
+__global__ void __launch_bounds__(256) k_chol_upd(float *__restrict__ Gw, int64_t ld, int r_lo, int c_lo, int c_hi,
+                                                  int q0, int kw, int n_ct, const int32_t *__restrict__ info) {
+  constexpr int TB = 128, BKc = 32, SLc = BKc + 4;
+  __shared__ float sA[TB * SLc], sB[TB * SLc];
+  const int b = blockIdx.y;
+  if (info[b] != 0) return;
+  const int ti = blockIdx.x / n_ct, tj = blockIdx.x % n_ct;
+  const int rb = r_lo + TB * ti, cb = c_lo + TB * tj;
+  if (cb > rb + TB - 1) return;               // entirely above the diagonal
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1, h = lane >> 5, col = lane & 31;
+  float *G = Gw + (size_t)b * ld * ld;
+  f32x16 acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) acc[i][j] = zero16();
+  for (int kq = 0; kq < kw; kq += BKc) {
+    __syncthreads();
+    for (int e = tid; e < TB * BKc / 4; e += 256) {
+      const int r = e / (BKc / 4), c4 = (e % (BKc / 4)) * 4;
+      const int ra = rb + r, rc = cb + r;
+      f32x4 va = {0.f, 0.f, 0.f, 0.f}, vb = va;
+      if (ra < ld) va = *reinterpret_cast<const f32x4 *>(G + (size_t)ra * ld + q0 + kq + c4);
+      if (rc < c_hi) vb = *reinterpret_cast<const f32x4 *>(G + (size_t)rc * ld + q0 + kq + c4);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        sA[r * SLc + c4 + q] = va[q];
+        sB[r * SLc + c4 + q] = vb[q];
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int ks = 0; ks < BKc / 2; ++ks) {
+      float fa[2], fb[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        fa[i] = sA[(wm * 64 + 32 * i + col) * SLc + 2 * ks + h];
+        fb[i] = sB[(wn * 64 + 32 * i + col) * SLc + 2 * ks + h];
+      }
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[i][j] = Mfma<float>::mma(fa[i], fb[j], acc[i][j]);
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int c = cb + wn * 64 + 32 * j + col;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int r = rb + wm * 64 + 32 * i + acc_row(v, lane);
+        if (r < ld && c < c_hi && c <= r + 63) G[(size_t)r * ld + c] -= acc[i][j][v];
+      }
+    }
 }
 
 // Whole factorisation in one workgroup (escalation path).
@@ -709,12 +728,31 @@ hipError_t launch_hvec(const float *LT, const float *z, const float *m, int B, i
 hipError_t launch_cholesky(float *Gw, const float *Gc, int B, int t, int64_t ld, float delta0, int max_esc,
                            FitState st, hipStream_t s) {
   hipLaunchKernelGGL(k_ridge_init, dim3(B), dim3(256), 0, s, Gw, Gc, t, ld, delta0, st);
-  hipLaunchKernelGGL(k_chol_diag0, dim3(B), dim3(256), 0, s, Gw, ld, st.info);
+  // Two-level right-looking blocking: 64-wide diagonal factor + panel solve
+  // steps inside 256-wide outer panels; inside an outer panel only its own
+  // columns are updated, and the trailing matrix is updated once per outer
+  // panel with k = 256 (a quarter of the trailing-matrix traffic of 64-wide
+  // steps).
+  constexpr int kOuter = 256;
   const int nrb = (int)(ld / kNB);
-  for (int k = 0; k < nrb - 1; ++k) {
-    const int rem = nrb - k - 1;
-    hipLaunchKernelGGL(k_chol_panel, dim3(rem, B), dim3(256), 0, s, Gw, ld, k, st.info);
-    hipLaunchKernelGGL(k_chol_update, dim3(rem * (rem + 1) / 2, B), dim3(256), 0, s, Gw, ld, k, st.info);
+  for (int K0 = 0; K0 < ld; K0 += kOuter) {
+    const int K1 = (int)(K0 + kOuter < ld ? K0 + kOuter : ld);
+    for (int c = K0; c < K1; c += kNB) {
+      const int k = c / kNB;
+      hipLaunchKernelGGL(k_chol_diag, dim3(B), dim3(256), 0, s, Gw, ld, k, st.info);
+      const int rem = nrb - k - 1;
+      if (rem > 0) hipLaunchKernelGGL(k_chol_panel, dim3(rem, B), dim3(256), 0, s, Gw, ld, k, st.info);
+      if (c + kNB < K1) {
+        const int r_lo = c + kNB, n_rt = (int)((ld - r_lo + 127) / 128), n_ct = (K1 - r_lo + 127) / 128;
+        hipLaunchKernelGGL(k_chol_upd, dim3(n_rt * n_ct, B), dim3(256), 0, s, Gw, ld, r_lo, r_lo, K1, c, kNB, n_ct,
+                           st.info);
+      }
+    }
+    if (K1 < ld) {
+      const int n_rt = (int)((ld - K1 + 127) / 128), n_ct = n_rt;
+      hipLaunchKernelGGL(k_chol_upd, dim3(n_rt * n_ct, B), dim3(256), 0, s, Gw, ld, K1, K1, (int)ld, K0,
+                         K1 - K0, n_ct, st.info);
+    }
   }
   if (max_esc > 0) hipLaunchKernelGGL(k_chol_escalate, dim3(B), dim3(256), 0, s, Gw, Gc, t, ld, max_esc, st);
   return hipGetLastError();
