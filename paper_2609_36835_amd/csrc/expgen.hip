@@ -49,6 +49,46 @@ __global__ void __launch_bounds__(256) k_expgen(const T *__restrict__ Q, const v
   const float zshift = (MODE == MODE_PROFILE) ? shift[b] : 0.0f;
   float rowsum = 0.0f;
 
+  // Output tiles (this wave's 32 rows x 64 queries) are staged in LDS so that
+  // global stores are whole 128/256-byte row segments.
+  constexpr int SO = 64 + 4;                               // staging row (4-byte words)
+  __shared__ float sOut[4][32 * SO];
+  float *so = sOut[wave];
+  auto flush_f32 = [&](const float (&v)[2][16], float *dst_base) {   // dst_base: row 0 of this wave, col i0
+#pragma unroll
+    for (int ms = 0; ms < 2; ++ms)
+#pragma unroll
+      for (int vv = 0; vv < 16; ++vv) so[col * SO + 32 * ms + acc_row(vv, lane)] = v[ms][vv];
+    __syncthreads();
+#pragma unroll
+    for (int pass = 0; pass < 8; ++pass) {             // 32 rows x 16 chunks of 16 B
+      const int chunk = pass * 64 + lane, r = chunk / 16, c4 = (chunk % 16) * 4;
+      const f32x4 w = {so[r * SO + c4], so[r * SO + c4 + 1], so[r * SO + c4 + 2], so[r * SO + c4 + 3]};
+      *reinterpret_cast<f32x4 *>(dst_base + (size_t)r * n_pad + c4) = w;
+    }
+    __syncthreads();
+  };
+  auto flush_bf16 = [&](const float (&v)[2][16], int part, bf16 *dst_base) {   // part: 0 value, 1 hi, 2 lo
+    bf16 *sb = reinterpret_cast<bf16 *>(so);
+#pragma unroll
+    for (int ms = 0; ms < 2; ++ms)
+#pragma unroll
+      for (int vv = 0; vv < 16; ++vv) {
+        bf16 hi, lo;
+        split_bf16(v[ms][vv], hi, lo);
+        sb[col * (2 * SO) + 32 * ms + acc_row(vv, lane)] = part == 2 ? lo : hi;
+      }
+    __syncthreads();
+#pragma unroll
+    for (int pass = 0; pass < 4; ++pass) {             // 32 rows x 8 chunks of 16 B
+      const int chunk = pass * 64 + lane, r = chunk / 8, c8 = (chunk % 8) * 8;
+      *reinterpret_cast<bf16x8 *>(dst_base + (size_t)r * n_pad + c8) =
+          *reinterpret_cast<const bf16x8 *>(&sb[r * (2 * SO) + c8]);
+    }
+    __syncthreads();
+  };
+  const int row0 = blockIdx.x * 128 + wave * 32;          // first output row of this wave
+
   for (int i0 = 0; i0 < n_pad; i0 += 64) {
     for (int c = tid; c < 64 * (kHeadDim / EPC); c += 256) {
       int r = c / (kHeadDim / EPC), cc = (c % (kHeadDim / EPC)) * EPC;
@@ -57,60 +97,43 @@ __global__ void __launch_bounds__(256) k_expgen(const T *__restrict__ Q, const v
       *reinterpret_cast<f32x4 *>(&sQ[r * SQ + cc]) = v;
     }
     __syncthreads();
-    #pragma unroll
+    float val[2][16], lg[2][16];
+#pragma unroll
     for (int ms = 0; ms < 2; ++ms) {
       f32x16 acc = zero16();
       const T *arow = &sQ[(32 * ms + col) * SQ + KPL * h];
-      #pragma unroll
+#pragma unroll
       for (int ks = 0; ks < NKS; ++ks) {
         typename M::frag a = M::load(arow + ks * KSTEP);
-        #pragma unroll
+#pragma unroll
         for (int p = 0; p < NB; ++p) acc = M::mma(a, bf[p][ks], acc);
       }
-      #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int ib = i0 + 32 * ms + 8 * g + 4 * h;   // 4 consecutive queries ib..ib+3
-        float val[4], lg[4];
-        #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int i = ib + r;
-          const bool ok = rvalid && i < n;
-          if (MODE == MODE_PROFILE) {
-            val[r] = ok ? exp2f(acc[4 * g + r] * c2 - zshift * 1.4426950408889634f) : 0.0f;
-            rowsum += val[r];
-          } else {
-            lg[r] = ok ? acc[4 * g + r] * scale : 0.0f;
-            val[r] = ok ? expf(lg[r] - (shift ? shift[(size_t)b * n + i] : 0.0f)) : 0.0f;
-          }
-        }
-        char *ob = reinterpret_cast<char *>(out);
-        if constexpr (sizeof(T) == 4) {
-          float *o = reinterpret_cast<float *>(ob) + (size_t)b * out_pair_stride + (size_t)row * n_pad + ib;
-          *reinterpret_cast<f32x4 *>(o) = f32x4{val[0], val[1], val[2], val[3]};
-        } else if constexpr (MODE == MODE_PROFILE) {
-          bf16 *o = reinterpret_cast<bf16 *>(ob) + (size_t)b * out_pair_stride + (size_t)row * n_pad + ib;
-          bf16x4 w = {to_bf16(val[0]), to_bf16(val[1]), to_bf16(val[2]), to_bf16(val[3])};
-          *reinterpret_cast<bf16x4 *>(o) = w;
+#pragma unroll
+      for (int vv = 0; vv < 16; ++vv) {
+        const int i = i0 + 32 * ms + acc_row(vv, lane);
+        const bool ok = rvalid && i < n;
+        if (MODE == MODE_PROFILE) {
+          val[ms][vv] = ok ? exp2f(acc[vv] * c2 - zshift * 1.4426950408889634f) : 0.0f;
+          rowsum += val[ms][vv];
+          lg[ms][vv] = 0.0f;
         } else {
-          bf16 *o = reinterpret_cast<bf16 *>(ob) + (size_t)b * out_pair_stride + (size_t)row * n_pad + ib;
-          bf16x4 hi, lo;
-          #pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            bf16 a, c;
-            split_bf16(val[r], a, c);
-            hi[r] = a;
-            lo[r] = c;
-          }
-          *reinterpret_cast<bf16x4 *>(o) = hi;
-          *reinterpret_cast<bf16x4 *>(o + out_plane_stride) = lo;
-        }
-        if (MODE == MODE_PHIC) {
-          float *L = aux + (size_t)b * aux_pair_stride + (size_t)row * n_pad + ib;
-          *reinterpret_cast<f32x4 *>(L) = f32x4{lg[0], lg[1], lg[2], lg[3]};
+          lg[ms][vv] = ok ? acc[vv] * scale : 0.0f;
+          val[ms][vv] = ok ? expf(lg[ms][vv] - (shift ? shift[(size_t)b * n + i] : 0.0f)) : 0.0f;
         }
       }
     }
-    __syncthreads();
+    __syncthreads();   // sQ is refilled at the next i0; sOut is free
+    char *ob = reinterpret_cast<char *>(out);
+    if constexpr (sizeof(T) == 4) {
+      flush_f32(val, reinterpret_cast<float *>(ob) + (size_t)b * out_pair_stride + (size_t)row0 * n_pad + i0);
+    } else if constexpr (MODE == MODE_PROFILE) {
+      flush_bf16(val, 0, reinterpret_cast<bf16 *>(ob) + (size_t)b * out_pair_stride + (size_t)row0 * n_pad + i0);
+    } else {
+      bf16 *o = reinterpret_cast<bf16 *>(ob) + (size_t)b * out_pair_stride + (size_t)row0 * n_pad + i0;
+      flush_bf16(val, 1, o);
+      flush_bf16(val, 2, o + out_plane_stride);
+    }
+    if (MODE == MODE_PHIC) flush_f32(lg, aux + (size_t)b * aux_pair_stride + (size_t)row0 * n_pad + i0);
   }
   if (MODE == MODE_PROFILE) {
     rowsum += __shfl_xor(rowsum, 32, 64);

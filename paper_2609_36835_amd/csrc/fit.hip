@@ -180,8 +180,11 @@ __global__ void __launch_bounds__(256) k_chol_diag(float *__restrict__ Gw, int64
 // in slabs of 32.
 __global__ void __launch_bounds__(256) k_chol_upd(float *__restrict__ Gw, int64_t ld, int r_lo, int c_lo, int c_hi,
                                                   int q0, int kw, int n_ct, const int32_t *__restrict__ info) {
-  constexpr int TB = 128, BKc = 32, SLc = BKc + 4;
-  __shared__ float sA[TB * SLc], sB[TB * SLc];
+  // LDS rows of 33 floats: the 4-byte fragment reads of 32 consecutive rows
+  // then fall in 32 distinct banks.  Two buffers; the next slab is fetched into
+  // registers while the current one is consumed.
+  constexpr int TB = 128, BKc = 32, SLc = BKc + 1, CHc = TB * BKc / 4 / 256;
+  __shared__ float sA[2][TB * SLc], sB[2][TB * SLc];
   const int b = blockIdx.y;
   if (info[b] != 0) return;
   const int ti = blockIdx.x / n_ct, tj = blockIdx.x % n_ct;
@@ -190,39 +193,57 @@ __global__ void __launch_bounds__(256) k_chol_upd(float *__restrict__ Gw, int64_
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1, h = lane >> 5, col = lane & 31;
   float *G = Gw + (size_t)b * ld * ld;
+  f32x4 ra[CHc], rbv[CHc];
+  auto fetch = [&](int kq) {
+#pragma unroll
+    for (int c = 0; c < CHc; ++c) {
+      const int e = tid + 256 * c, r = e / (BKc / 4), c4 = (e % (BKc / 4)) * 4;
+      const int row_a = rb + r, row_b = cb + r;
+      ra[c] = f32x4{0.f, 0.f, 0.f, 0.f};
+      rbv[c] = ra[c];
+      if (row_a < ld) ra[c] = *reinterpret_cast<const f32x4 *>(G + (size_t)row_a * ld + q0 + kq + c4);
+      if (row_b < c_hi) rbv[c] = *reinterpret_cast<const f32x4 *>(G + (size_t)row_b * ld + q0 + kq + c4);
+    }
+  };
+  auto stash = [&](int bf) {
+#pragma unroll
+    for (int c = 0; c < CHc; ++c) {
+      const int e = tid + 256 * c, r = e / (BKc / 4), c4 = (e % (BKc / 4)) * 4;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        sA[bf][r * SLc + c4 + q] = ra[c][q];
+        sB[bf][r * SLc + c4 + q] = rbv[c][q];
+      }
+    }
+  };
   f32x16 acc[2][2];
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
     for (int j = 0; j < 2; ++j) acc[i][j] = zero16();
+  fetch(0);
+  stash(0);
+  __syncthreads();
+  int bf = 0;
   for (int kq = 0; kq < kw; kq += BKc) {
-    __syncthreads();
-    for (int e = tid; e < TB * BKc / 4; e += 256) {
-      const int r = e / (BKc / 4), c4 = (e % (BKc / 4)) * 4;
-      const int ra = rb + r, rc = cb + r;
-      f32x4 va = {0.f, 0.f, 0.f, 0.f}, vb = va;
-      if (ra < ld) va = *reinterpret_cast<const f32x4 *>(G + (size_t)ra * ld + q0 + kq + c4);
-      if (rc < c_hi) vb = *reinterpret_cast<const f32x4 *>(G + (size_t)rc * ld + q0 + kq + c4);
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        sA[r * SLc + c4 + q] = va[q];
-        sB[r * SLc + c4 + q] = vb[q];
-      }
-    }
-    __syncthreads();
+    const bool more = kq + BKc < kw;
+    if (more) fetch(kq + BKc);
 #pragma unroll
     for (int ks = 0; ks < BKc / 2; ++ks) {
       float fa[2], fb[2];
 #pragma unroll
       for (int i = 0; i < 2; ++i) {
-        fa[i] = sA[(wm * 64 + 32 * i + col) * SLc + 2 * ks + h];
-        fb[i] = sB[(wn * 64 + 32 * i + col) * SLc + 2 * ks + h];
+        fa[i] = sA[bf][(wm * 64 + 32 * i + col) * SLc + 2 * ks + h];
+        fb[i] = sB[bf][(wn * 64 + 32 * i + col) * SLc + 2 * ks + h];
       }
 #pragma unroll
       for (int i = 0; i < 2; ++i)
 #pragma unroll
         for (int j = 0; j < 2; ++j) acc[i][j] = Mfma<float>::mma(fa[i], fb[j], acc[i][j]);
     }
+    if (more) stash(bf ^ 1);
+    __syncthreads();
+    bf ^= 1;
   }
 #pragma unroll
   for (int i = 0; i < 2; ++i)
@@ -621,8 +642,8 @@ __global__ void __launch_bounds__(256) k_trsm_mfma(const float *__restrict__ Gw,
                                                    const float *__restrict__ R, float *__restrict__ X,
                                                    const int32_t *__restrict__ info) {
   constexpr int RB = 64, NC = 64, SLD = RB + 1, SXD = NC + 1;
-  __shared__ float sL[RB * SLD];
-  __shared__ float sX[RB * SXD];
+  __shared__ float sL[2][RB * SLD];
+  __shared__ float sX[2][RB * SXD];
   const int b = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   if (info[b] != 0) return;
   const int wr = wave >> 1, wc = wave & 1, h = lane >> 5, col = lane & 31;
@@ -631,69 +652,84 @@ __global__ void __launch_bounds__(256) k_trsm_mfma(const float *__restrict__ Gw,
   const float *Rb = R + (size_t)b * ld * kHeadDim;
   float *Xb = X + (size_t)b * ld * kHeadDim;
   const int nb = (int)(ld / RB);
+  f32x4 rl[4], rx[4];
+  // tile (i, k) of the operand: forward L[r0+i][p0+k], backward L[p0+k][r0+i]
+  auto fetch = [&](int r0, int p0) {
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const int e = tid + 256 * c, i = e / 16, k4 = (e % 16) * 4;
+      rl[c] = FWD ? *reinterpret_cast<const f32x4 *>(L + (size_t)(r0 + i) * ld + p0 + k4)
+                  : *reinterpret_cast<const f32x4 *>(L + (size_t)(p0 + i) * ld + r0 + k4);
+      rx[c] = *reinterpret_cast<const f32x4 *>(Xb + (size_t)(p0 + i) * kHeadDim + c0 + k4);
+    }
+  };
+  auto stash = [&](int bf) {
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const int e = tid + 256 * c, i = e / 16, k4 = (e % 16) * 4;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        if (FWD) sL[bf][i * SLD + k4 + q] = rl[c][q];
+        else sL[bf][(k4 + q) * SLD + i] = rl[c][q];
+        sX[bf][i * SXD + k4 + q] = rx[c][q];
+      }
+    }
+  };
   for (int step = 0; step < nb; ++step) {
     const int kb = FWD ? step : nb - 1 - step;
     const int r0 = kb * RB;
     f32x16 acc = zero16();
     const int pb0 = FWD ? 0 : kb + 1, pb1 = FWD ? kb : nb;
+    int bf = 0;
+    if (pb0 < pb1) {
+      __syncthreads();
+      fetch(r0, pb0 * RB);
+      stash(0);
+      __syncthreads();
+    }
     for (int pb = pb0; pb < pb1; ++pb) {
-      const int p0 = pb * RB;
-      __syncthreads();
-      for (int e = tid; e < RB * RB / 4; e += 256) {
-        const int i = e / 16, k4 = (e % 16) * 4;
-        if (FWD) {   // sL[i][k] = L[r0 + i][p0 + k]
-          const f32x4 v = *reinterpret_cast<const f32x4 *>(L + (size_t)(r0 + i) * ld + p0 + k4);
-#pragma unroll
-          for (int q = 0; q < 4; ++q) sL[i * SLD + k4 + q] = v[q];
-        } else {     // sL[i][k] = L[p0 + k][r0 + i]  (row k of L read contiguously)
-          const f32x4 v = *reinterpret_cast<const f32x4 *>(L + (size_t)(p0 + i) * ld + r0 + k4);
-#pragma unroll
-          for (int q = 0; q < 4; ++q) sL[(k4 + q) * SLD + i] = v[q];
-        }
-      }
-      for (int e = tid; e < RB * NC / 4; e += 256) {
-        const int k = e / 16, c4 = (e % 16) * 4;
-        const f32x4 v = *reinterpret_cast<const f32x4 *>(Xb + (size_t)(p0 + k) * kHeadDim + c0 + c4);
-#pragma unroll
-        for (int q = 0; q < 4; ++q) sX[k * SXD + c4 + q] = v[q];
-      }
-      __syncthreads();
+      const bool more = pb + 1 < pb1;
+      if (more) fetch(r0, (pb + 1) * RB);
 #pragma unroll 8
       for (int ks = 0; ks < RB / 2; ++ks)
-        acc = Mfma<float>::mma(sL[(32 * wr + col) * SLD + 2 * ks + h], sX[(2 * ks + h) * SXD + 32 * wc + col], acc);
+        acc = Mfma<float>::mma(sL[bf][(32 * wr + col) * SLD + 2 * ks + h],
+                               sX[bf][(2 * ks + h) * SXD + 32 * wc + col], acc);
+      if (more) stash(bf ^ 1);
+      __syncthreads();
+      bf ^= 1;
     }
     __syncthreads();
-    // right-hand side minus update, into sX; diagonal block into sL (transposed for backward)
+    // right-hand side minus update, into sX[0]; diagonal block into sL[0] (transposed for backward)
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
       const int r = 32 * wr + acc_row(v, lane), c = 32 * wc + col;
-      sX[r * SXD + c] = Rb[(size_t)(r0 + r) * kHeadDim + c0 + c] - acc[v];
+      sX[0][r * SXD + c] = Rb[(size_t)(r0 + r) * kHeadDim + c0 + c] - acc[v];
     }
     for (int e = tid; e < RB * RB; e += 256) {
       const int i = e / RB, k = e % RB;
-      sL[i * SLD + k] = FWD ? L[(size_t)(r0 + i) * ld + r0 + k] : L[(size_t)(r0 + k) * ld + r0 + i];
+      sL[0][i * SLD + k] = FWD ? L[(size_t)(r0 + i) * ld + r0 + k] : L[(size_t)(r0 + k) * ld + r0 + i];
     }
     __syncthreads();
     if (tid < NC) {
       const int c = tid;
       if (FWD) {
         for (int r = 0; r < RB; ++r) {
-          float v = sX[r * SXD + c];
-          for (int q = 0; q < r; ++q) v -= sL[r * SLD + q] * sX[q * SXD + c];
-          sX[r * SXD + c] = v / sL[r * SLD + r];
+          float v = sX[0][r * SXD + c];
+          for (int q = 0; q < r; ++q) v -= sL[0][r * SLD + q] * sX[0][q * SXD + c];
+          sX[0][r * SXD + c] = v / sL[0][r * SLD + r];
         }
       } else {
         for (int r = RB - 1; r >= 0; --r) {
-          float v = sX[r * SXD + c];
-          for (int q = r + 1; q < RB; ++q) v -= sL[r * SLD + q] * sX[q * SXD + c];
-          sX[r * SXD + c] = v / sL[r * SLD + r];
+          float v = sX[0][r * SXD + c];
+          for (int q = r + 1; q < RB; ++q) v -= sL[0][r * SLD + q] * sX[0][q * SXD + c];
+          sX[0][r * SXD + c] = v / sL[0][r * SLD + r];
         }
       }
     }
     __syncthreads();
     for (int e = tid; e < RB * NC; e += 256) {
       const int r = e / NC, c = e % NC;
-      Xb[(size_t)(r0 + r) * kHeadDim + c0 + c] = sX[r * SXD + c];
+      Xb[(size_t)(r0 + r) * kHeadDim + c0 + c] = sX[0][r * SXD + c];
     }
     __threadfence_block();
   }
