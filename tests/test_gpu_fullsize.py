@@ -1,0 +1,122 @@
+"""GPU parity at the full Llama-3.1-8B-shaped size, in the launch configuration
+the benchmark times: one arckv_compact call over all 256 layer-KV-head pairs
+(T=32768, 4096 reference queries, 10% retention, bf16, default parameters).
+
+The float64 oracle cannot run all 256 pairs, so three sampled pairs (first,
+middle, last; different layers and heads) are compared with it one by one;
+every pair is checked for the properties that hold at any size.
+"""
+import math
+import os
+import sys
+import time
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from tests.gpu_common import TOL_OUT, np64
+
+pytestmark = pytest.mark.gpu
+
+WL = synth.WORKLOADS["llama8b_bf16_T32768"]
+SAMPLED = (0, 131, 255)
+
+
+def log(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def A():
+    from paper_2609_36835_amd import arckv
+    return arckv
+
+
+@pytest.fixture(scope="module")
+def full():
+    wl = WL
+    td = torch.bfloat16
+    B, T, n, d = wl.pairs, wl.T, wl.n, wl.d
+    dev = torch.device("cuda:0")
+    K = torch.empty(B, T, d, dtype=td, device=dev)
+    V = torch.empty(B, T, d, dtype=td, device=dev)
+    Q = torch.empty(B, n, d, dtype=td, device=dev)
+    W1 = torch.empty(B, 64, 2 * d, dtype=td, device=dev)
+    b1 = torch.empty(B, 64, dtype=torch.float32, device=dev)
+    w2 = torch.empty(B, 64, dtype=torch.float32, device=dev)
+    b2 = torch.empty(B, dtype=torch.float32, device=dev)
+    threads = min(16, os.cpu_count() or 1)
+    t0 = time.time()
+    for b0 in range(0, B, wl.kv_heads):
+        idx = list(range(b0, b0 + wl.kv_heads))
+        arr = synth.workload_arrays(wl, pairs=idx, threads=threads)
+        sl = slice(b0, b0 + wl.kv_heads)
+        K[sl] = torch.from_numpy(arr["K"]).to(dev).to(td)
+        V[sl] = torch.from_numpy(arr["V"]).to(dev).to(td)
+        Q[sl] = torch.from_numpy(arr["Q"]).to(dev).to(td)
+        W1[sl] = torch.from_numpy(arr["W1"]).to(dev).to(td)
+        b1[sl] = torch.from_numpy(arr["b1"]).to(dev)
+        w2[sl] = torch.from_numpy(arr["w2"]).to(dev)
+        b2[sl] = torch.from_numpy(arr["b2"][:, 0]).to(dev)
+        if (b0 // wl.kv_heads) % 8 == 7:
+            log(f"[fullsize] inputs for {b0 + wl.kv_heads}/{B} pairs ({time.time() - t0:.0f}s)")
+    s = 1.0 / math.sqrt(d)
+    comp = A().Compactor(B, T, n, wl.rho, td, dev, scale=s)
+    log(f"[fullsize] arckv_compact B={B} T={T} n={n} t={comp.t}")
+    out = [x.clone() for x in comp(K, V, Q, W1, b1, w2, b2)]
+    scores = A().score(K, V, W1, b1, w2, b2)
+    torch.cuda.synchronize()
+    log("[fullsize] compaction done")
+    return wl, s, comp.t, out, np64(scores)
+
+
+@pytest.mark.timeout(900)
+def test_fullsize_all_pairs_properties(full):
+    wl, s, t, (anchors, Ck, beta, Cv, info), scores = full
+    assert t == 3277
+    info = info.cpu().numpy()
+    assert np.all(info == 0), np.argwhere(info != 0)[:8]
+    S = anchors.cpu().numpy()
+    assert S.shape == (wl.pairs, t)
+    assert np.all(S[:, 1:] > S[:, :-1]) and S.min() >= 0 and S.max() < wl.T
+    # the anchors are exactly the top-t of the scores the library computed
+    for b in range(wl.pairs):
+        assert S[b].tolist() == oracle.select_topt(scores[b], t).tolist(), b
+    bt = beta.float()
+    assert torch.isfinite(bt).all() and float(bt.min()) >= -30.0 and float(bt.max()) <= 30.0
+    assert torch.isfinite(Ck).all() and torch.isfinite(Cv).all()
+
+
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("b", SAMPLED)
+def test_fullsize_sampled_pair_matches_oracle(full, b):
+    wl, s, t, (anchors, Ck, beta, Cv, info), scores = full
+    layer, head = synth.pair_index(wl, b)
+    p = synth.pair_inputs(wl, layer, head)
+    h = {k: v.astype(np.float64) for k, v in p.items()}
+    t0 = time.time()
+    ref_scores = oracle.score_mlp(h["K"], h["V"], h["W1"], h["b1"], h["w2"], h["b2"][0])
+    sc = np.abs(ref_scores).max()
+    assert np.abs(scores[b] - ref_scores).max() <= 1e-5 * sc + 1e-6
+    S_gpu = anchors[b].cpu().numpy().astype(np.int64)
+    S_ref = oracle.select_topt(ref_scores, t)
+    use = None
+    if S_gpu.tolist() != S_ref.tolist():
+        kth = np.sort(ref_scores)[::-1][t - 1]
+        for j in set(S_gpu.tolist()) ^ set(S_ref.tolist()):
+            assert abs(ref_scores[j] - kth) <= 1e-5 * sc, j
+        use = S_gpu          # certified boundary near-tie: fit on the GPU's anchor set
+        log(f"  pair {b}: anchor sets differ at a certified near-tie; oracle refit on the GPU's anchors")
+    r = oracle.compact_pair(h["K"], h["V"], h["Q"], h["W1"], h["b1"], h["w2"], h["b2"][0], t=t, scale=s,
+                            scores=ref_scores, anchors=use, profile_dtype="bf16")
+    Q = h["Q"]
+    O_gpu = oracle.attend_compact(Q, np64(Ck[b]), np64(beta[b]), np64(Cv[b]), s)
+    O_ref = oracle.attend_compact(Q, r.C_k, r.beta, r.C_v, s)
+    err = oracle.row_rel_err(O_gpu, O_ref)
+    ck_err = np.abs(np64(Ck[b]) - r.C_k).max() / np.abs(r.C_k).max()
+    log(f"  pair {b} (layer {layer}, head {head}): O(Q_ref) max row rel err {err.max():.3e} "
+        f"(mean {err.mean():.2e}); C_k rel {ck_err:.2e}; oracle {time.time() - t0:.1f}s")
+    assert err.max() <= TOL_OUT["bf16"], err.max()
