@@ -152,7 +152,7 @@ def main():
     launches_per_step = max(cnt_assign // args.steps, 1)
     flops_per_launch = assign_flops(wl, t) / launches_per_step
     achieved = flops_per_launch / avg_launch_s / 1e12
-    roofline = {"bound": "mfma", "kernel": "k_gemm256<1,1,EpiArgmax256> (key-to-anchor assignment)",
+    roofline = {"bound": "mfma", "kernel": "k_gemm_big<4,2,2,4,64,1,1,EpiArgmaxBig> (key-to-anchor assignment)",
                 "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
                 "avg_launch_ms": round(avg_launch_s * 1e3, 3),

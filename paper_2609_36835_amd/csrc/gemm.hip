@@ -1,12 +1,13 @@
 // Instantiations of the batched TN contraction for the compaction stages.
 #include "gemm.hpp"
-#include "gemm256.hpp"
+#include "gemm_big.hpp"
 
 namespace arckv {
 
 // Anchor assignment (eq. anchor_assignment): S[r][j] = sum_i U_S[r][i] E^T[j][i];
 // per-(M-tile, key) packed argmax partials.  U [P][tp][np], Et [P][Tp][np].
-// M-tiles are 256 rows for bf16 (large-tile kernel) and 128 for fp32.
+// M-tiles are 256 rows for bf16 (large-tile kernel, 8 waves of 64 x 128) and
+// 128 for fp32.
 hipError_t launch_assign_gemm(int dtype, const void *U, const void *Et, uint64_t *part, int P, int t, int64_t tp,
                               int64_t Tp, int64_t np_, hipStream_t s) {
   GemmShape g;
@@ -23,9 +24,9 @@ hipError_t launch_assign_gemm(int dtype, const void *U, const void *Et, uint64_t
   g.syrk = false;
   g.group_m = 8;
   if (dtype == ARCKV_BF16) {
-    GemmShape256 g2{P, (int)tp, (int)Tp, (int)np_, tp * np_, 0, np_, Tp * np_, 0, np_, false, 4};
-    EpiArgmax256 e2{part, (tp / kLBM) * Tp, (int)Tp, t};
-    return launch_gemm256<1, 1>(g2, (const bf16 *)U, (const bf16 *)Et, e2, s);
+    BigShape g2{P, (int)tp, (int)Tp, (int)np_, tp * np_, 0, np_, Tp * np_, 0, np_, false, 4};
+    EpiArgmaxBig<4, 2, 2, 4> e2{part, (tp / 256) * Tp, (int)Tp, t};
+    return launch_gemm_big<4, 2, 2, 4, 64, 1, 1>(g2, (const bf16 *)U, (const bf16 *)Et, e2, s);
   }
   EpiArgmax e{part, (tp / kGBM) * Tp, (int)Tp, t};
   return launch_gemm<float, 1, 1>(g, (const float *)U, (const float *)Et, e, s);
@@ -44,9 +45,9 @@ hipError_t launch_gram(int dtype, const void *X, float *G, float *Gc, int P, int
   g.lda = g.ldb = np_;
   EpiSym e{G, Gc, tp * tp, (int)tp};
   if (dtype == ARCKV_BF16) {
-    GemmShape256 g2{P, (int)tp, (int)tp, (int)np_, 2 * tp * np_, tp * np_, np_, 2 * tp * np_, tp * np_, np_, true, 4};
-    EpiSym256 e2{G, Gc, tp * tp, (int)tp};
-    return launch_gemm256<2, 2>(g2, (const bf16 *)X, (const bf16 *)X, e2, s);
+    BigShape g2{P, (int)tp, (int)tp, (int)np_, 2 * tp * np_, tp * np_, np_, 2 * tp * np_, tp * np_, np_, true, 4};
+    EpiSymBig<2, 4> e2{G, Gc, tp * tp, (int)tp};
+    return launch_gemm_big<4, 2, 2, 4, 32, 2, 2>(g2, (const bf16 *)X, (const bf16 *)X, e2, s);
   }
   g.a_pair = g.b_pair = tp * np_;
   g.a_plane = g.b_plane = 0;

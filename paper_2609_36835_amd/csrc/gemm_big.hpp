@@ -1,0 +1,283 @@
+// Large-tile batched TN contraction on bf16 MFMA (32x32x16) for the big
+// contractions of the path: the anchor assignment (one bf16 plane) and the
+// split-bf16 Gram matrices (hi/lo planes, three products).
+//
+// C[M][N] = sum_k A[m][k] B[n][k], both operands K-contiguous.  A workgroup of
+// WM x WN waves owns a (32 WM TM) x (32 WN TN) tile; each wave a 32TM x 32TN
+// block of accumulators.  Operand slabs of BK elements go global -> LDS with
+// the CDNA4 direct-to-LDS loads (global_load_lds_dwordx4: lane l of a wave
+// writes bytes [16 l, 16 l + 16) of a 1 KB LDS run), so no VGPRs are spent on
+// staging.  Rows are stored unpadded and each row's 16-byte chunks are XOR-
+// swizzled with the row index, which makes the MFMA fragment reads (32 rows x
+// one chunk per half-wave) free of bank conflicts.  Two LDS stages: slab i+1 is
+// in flight while slab i feeds the MFMAs; fragments for k-step ks+1 are read
+// while the MFMAs of ks run.  One workgroup barrier per slab, without the
+// full memory fence of __syncthreads(), so the prefetch stays in flight.
+// Dimensions must be multiples of the tile; workgroups are remapped so that
+// each XCD owns a contiguous, M-grouped (or lower-triangular) range of tiles.
+#pragma once
+#include "gemm.hpp"
+
+namespace arckv {
+
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+struct BigShape {
+  int batch, M, N, K;
+  int64_t a_pair, a_plane, lda;   // elements
+  int64_t b_pair, b_plane, ldb;
+  bool syrk;                      // lower-triangular tiles only (nt <= mt)
+  int group_m;
+};
+
+template <int WM, int WN, int TM, int TN, int BK, int NA, int NB>
+struct BigCfg {
+  static constexpr int NW = WM * WN, THREADS = 64 * NW;
+  static constexpr int BM = 32 * WM * TM, BN = 32 * WN * TN;
+  static constexpr int RB = BK * 2;                 // LDS row bytes
+  static constexpr int CPR = BK / 8;                // 16-byte chunks per row
+  static constexpr int RPI = 1024 / RB;             // rows per 1 KB load run
+  static constexpr int A_BYTES = BM * RB, B_BYTES = BN * RB;
+  static constexpr int STAGE = NA * A_BYTES + NB * B_BYTES;
+  static constexpr int LDS = 2 * STAGE;
+  static constexpr int A_INST = A_BYTES / 1024 / NW, B_INST = B_BYTES / 1024 / NW;
+  static constexpr int KS = BK / 16;
+  static_assert(A_INST * NW * 1024 == A_BYTES && B_INST * NW * 1024 == B_BYTES, "load split");
+  static_assert(CPR == 4 || CPR == 8, "BK must be 32 or 64");
+  static_assert(LDS <= 160 * 1024 - 16 * 1024, "LDS budget");
+  // chunk swizzle: 16 consecutive rows at one logical chunk cover all 64 banks
+  __device__ static __forceinline__ int swz(int row) { return (row * RB / 256) & (CPR - 1); }
+};
+
+template <int BM, int BN>
+__device__ inline void big_tile(const BigShape &g, int64_t tile, int &p, int &mt, int &nt) {
+  const int MT = g.M / BM, NT = g.N / BN;
+  if (g.syrk) {
+    const int64_t per = (int64_t)MT * (MT + 1) / 2;
+    p = (int)(tile / per);
+    const int64_t r = tile % per;
+    int m = (int)((sqrt(8.0 * (double)r + 1.0) - 1.0) * 0.5);
+    while ((int64_t)m * (m + 1) / 2 > r) --m;
+    while ((int64_t)(m + 1) * (m + 2) / 2 <= r) ++m;
+    mt = m;
+    nt = (int)(r - (int64_t)m * (m + 1) / 2);
+    return;
+  }
+  const int64_t per = (int64_t)MT * NT;
+  p = (int)(tile / per);
+  const int64_t r = tile % per;
+  const int gm = g.group_m;
+  const int64_t per_group = (int64_t)gm * NT;
+  const int grp = (int)(r / per_group);
+  const int first_m = grp * gm;
+  const int gsize = min(MT - first_m, gm);
+  const int64_t rr = r % per_group;
+  mt = first_m + (int)(rr % gsize);
+  nt = (int)(rr / gsize);
+}
+
+inline int64_t big_tiles(const BigShape &g, int BM, int BN) {
+  const int64_t MT = g.M / BM, NT = g.N / BN;
+  return (int64_t)g.batch * (g.syrk ? MT * (MT + 1) / 2 : MT * NT);
+}
+
+// Workgroup barrier without a memory fence; the empty asm statements keep the
+// compiler from moving LDS accesses across it.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+template <int WM, int WN, int TM, int TN, int BK, int NA, int NB, class Epi>
+__global__ void __launch_bounds__(64 * WM * WN, 1) k_gemm_big(BigShape g, const bf16 *__restrict__ A,
+                                                              const bf16 *__restrict__ B, Epi epi) {
+  using C = BigCfg<WM, WN, TM, TN, BK, NA, NB>;
+  extern __shared__ __attribute__((aligned(1024))) char big_smem[];
+
+  const int64_t tile = xcd_remap(blockIdx.x, gridDim.x);
+  int p, mt, nt;
+  big_tile<C::BM, C::BN>(g, tile, p, mt, nt);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / WN, wn = wave % WN;
+  const int h = lane >> 5, col = lane & 31;
+  const bf16 *Ab = A + (size_t)p * g.a_pair + (size_t)mt * C::BM * g.lda;
+  const bf16 *Bb = B + (size_t)p * g.b_pair + (size_t)nt * C::BN * g.ldb;
+
+  // Per-lane source offsets of this wave's load runs: run gi covers rows
+  // [gi RPI, gi RPI + RPI); lane l fills physical chunk l % CPR of row
+  // gi RPI + l / CPR, i.e. logical chunk (l % CPR) ^ swz(row).
+  int64_t offA[C::A_INST], offB[C::B_INST];
+#pragma unroll
+  for (int i = 0; i < C::A_INST; ++i) {
+    const int row = (wave * C::A_INST + i) * C::RPI + lane / C::CPR;
+    offA[i] = (int64_t)row * g.lda + 8 * ((lane % C::CPR) ^ C::swz(row));
+  }
+#pragma unroll
+  for (int i = 0; i < C::B_INST; ++i) {
+    const int row = (wave * C::B_INST + i) * C::RPI + lane / C::CPR;
+    offB[i] = (int64_t)row * g.ldb + 8 * ((lane % C::CPR) ^ C::swz(row));
+  }
+  auto issue = [&](int slab, int st) {
+    const int k0 = slab * BK;
+    char *s = big_smem + st * C::STAGE;
+#pragma unroll
+    for (int q = 0; q < NA; ++q)
+#pragma unroll
+      for (int i = 0; i < C::A_INST; ++i)
+        __builtin_amdgcn_global_load_lds((const void *)(Ab + q * g.a_plane + offA[i] + k0),
+                                         (lds_void_t *)(s + q * C::A_BYTES + (wave * C::A_INST + i) * 1024), 16, 0,
+                                         0);
+#pragma unroll
+    for (int q = 0; q < NB; ++q)
+#pragma unroll
+      for (int i = 0; i < C::B_INST; ++i)
+        __builtin_amdgcn_global_load_lds(
+            (const void *)(Bb + q * g.b_plane + offB[i] + k0),
+            (lds_void_t *)(s + NA * C::A_BYTES + q * C::B_BYTES + (wave * C::B_INST + i) * 1024), 16, 0, 0);
+  };
+
+  int rowA[TM], rowB[TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i) rowA[i] = wm * 32 * TM + 32 * i + col;
+#pragma unroll
+  for (int j = 0; j < TN; ++j) rowB[j] = wn * 32 * TN + 32 * j + col;
+  auto rd = [&](const char *s, int ks, bf16x8 (&fa)[NA][TM], bf16x8 (&fb)[NB][TN]) {
+    const int c = 2 * ks + h;
+#pragma unroll
+    for (int q = 0; q < NA; ++q)
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+        fa[q][i] = *reinterpret_cast<const bf16x8 *>(s + q * C::A_BYTES + rowA[i] * C::RB +
+                                                     16 * (c ^ C::swz(rowA[i])));
+#pragma unroll
+    for (int q = 0; q < NB; ++q)
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+        fb[q][j] = *reinterpret_cast<const bf16x8 *>(s + NA * C::A_BYTES + q * C::B_BYTES + rowB[j] * C::RB +
+                                                     16 * (c ^ C::swz(rowB[j])));
+  };
+
+  f32x16 acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j) acc[i][j] = zero16();
+
+  const int nk = g.K / BK;
+  issue(0, 0);
+  for (int i = 0; i < nk; ++i) {
+    // this wave's runs of slab i have landed; after the barrier every wave's
+    // have, and every wave is done reading slab i-1 (the stage refilled next)
+    __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));   // vmcnt(0) only
+    lds_barrier();
+    if (i + 1 < nk) issue(i + 1, (i + 1) & 1);
+    const char *s = big_smem + (i & 1) * C::STAGE;
+    bf16x8 fa[2][NA][TM], fb[2][NB][TN];
+    rd(s, 0, fa[0], fb[0]);
+#pragma unroll
+    for (int ks = 0; ks < C::KS; ++ks) {
+      if (ks + 1 < C::KS) rd(s, ks + 1, fa[(ks + 1) & 1], fb[(ks + 1) & 1]);
+      const int cur = ks & 1;
+#pragma unroll
+      for (int ii = 0; ii < TM; ++ii)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+          acc[ii][j] = Mfma<bf16>::mma(fa[cur][0][ii], fb[cur][0][j], acc[ii][j]);
+          if constexpr (NB > 1) acc[ii][j] = Mfma<bf16>::mma(fa[cur][0][ii], fb[cur][1][j], acc[ii][j]);
+          if constexpr (NA > 1) acc[ii][j] = Mfma<bf16>::mma(fa[cur][1][ii], fb[cur][0][j], acc[ii][j]);
+        }
+    }
+    asm volatile("" ::: "memory");
+  }
+  __syncthreads();
+  epi(acc, p, mt * C::BM + wm * 32 * TM, nt * C::BN + wn * 32 * TN, mt, nt, lane, wm, wn);
+}
+
+// ------------------------------------------------------------------ epilogues
+// Anchor assignment: rows anchors r, columns keys j.  Packed (similarity,
+// lowest r) maxima per (M-tile, key); similarities are >= 0, so their float
+// bits order like unsigned integers.
+template <int WM, int WN, int TM, int TN>
+struct EpiArgmaxBig {
+  uint64_t *part;       // [P][MT][Np]
+  int64_t pair_stride;  // MT * Np
+  int Np, t;
+  __device__ __forceinline__ void operator()(f32x16 (&acc)[TM][TN], int p, int row0, int col0, int mt, int nt,
+                                             int lane, int wm, int wn) const {
+    constexpr int BN = 32 * WN * TN;
+    __shared__ uint64_t red[WM][BN];
+    const int h = lane >> 5, col = lane & 31;
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+      uint64_t best = 0ull;
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int r = row0 + 32 * i + acc_row(v, lane);
+          const uint64_t key =
+              ((uint64_t)__float_as_uint(acc[i][j][v]) << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)r);
+          best = (r < t && key > best) ? key : best;
+        }
+      const uint64_t o = __shfl_xor(best, 32, 64);
+      best = o > best ? o : best;
+      if (h == 0) red[wm][wn * 32 * TN + 32 * j + col] = best;
+    }
+    __syncthreads();
+    for (int c = threadIdx.x; c < BN; c += 64 * WM * WN) {
+      uint64_t best = red[0][c];
+#pragma unroll
+      for (int w = 1; w < WM; ++w) best = red[w][c] > best ? red[w][c] : best;
+      part[(size_t)p * pair_stride + (size_t)mt * Np + (size_t)nt * BN + c] = best;
+    }
+  }
+};
+
+// Symmetric Gram: write the tile to G and Gc, and its transpose above the diagonal.
+template <int TM, int TN>
+struct EpiSymBig {
+  float *G, *Gc;
+  int64_t pair_stride;
+  int ld;
+  __device__ __forceinline__ void operator()(f32x16 (&acc)[TM][TN], int p, int row0, int col0, int mt, int nt,
+                                             int lane, int, int) const {
+    const int h = lane >> 5, col = lane & 31;
+    float *Gp = G + (size_t)p * pair_stride, *Gcp = Gc + (size_t)p * pair_stride;
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        const int c = col0 + 32 * j + col;
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int r0 = row0 + 32 * i + 8 * g + 4 * h;
+          const f32x4 v = {acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]};
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            Gp[(size_t)(r0 + e) * ld + c] = v[e];
+            Gcp[(size_t)(r0 + e) * ld + c] = v[e];
+          }
+          if (mt != nt) {
+            *reinterpret_cast<f32x4 *>(Gp + (size_t)c * ld + r0) = v;
+            *reinterpret_cast<f32x4 *>(Gcp + (size_t)c * ld + r0) = v;
+          }
+        }
+      }
+  }
+};
+
+template <int WM, int WN, int TM, int TN, int BK, int NA, int NB, class Epi>
+hipError_t launch_gemm_big(const BigShape &g, const bf16 *A, const bf16 *B, const Epi &epi, hipStream_t s) {
+  using C = BigCfg<WM, WN, TM, TN, BK, NA, NB>;
+  if (g.M % C::BM || g.N % C::BN || g.K % BK) return hipErrorInvalidValue;
+  const int64_t tiles = big_tiles(g, C::BM, C::BN);
+  if (tiles == 0) return hipSuccess;
+  auto kern = k_gemm_big<WM, WN, TM, TN, BK, NA, NB, Epi>;
+  hipError_t e = hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(kern, dim3((unsigned)tiles), dim3(C::THREADS), C::LDS, s, g, A, B, epi);
+  return hipGetLastError();
+}
+
+}  // namespace arckv
