@@ -57,7 +57,7 @@ hipError_t launch_transpose_planes(int dtype, const void *PT, void *P, int B, in
 hipError_t launch_hvec(const float *LT, const float *z, const float *m, int B, int n, int t, int64_t tp, int64_t np_,
                        double *h, hipStream_t s);
 hipError_t launch_cholesky(float *Gw, const float *Gc, int B, int t, int64_t ld, float delta0, int max_esc,
-                           FitState st, hipStream_t s);
+                           FitState st, float *dinv, hipStream_t s);
 hipError_t launch_trsv(const float *Gw, int B, int64_t ld, const double *rhs, double *y, double *x, double *acc,
                        const int32_t *info, hipStream_t s);
 hipError_t launch_residual_vec(const float *Gc, int B, int64_t ld, int t, const double *rhs, const double *x,
@@ -171,7 +171,7 @@ struct Plan {
   // chunk region (offsets relative to chunk base)
   int64_t Ckp;
   int64_t Et, U, part, offsets, cursor, perm;            // merge phase
-  int64_t PhiT, LT, Gw, Gc, h, w, y, x, res, u, YT, Bm, X, R, Y2, XT, Pm, UT;  // fit phase
+  int64_t PhiT, LT, Gw, Gc, dinv, h, w, y, x, res, u, YT, Bm, X, R, Y2, XT, Pm, UT;  // fit phase
   int64_t chunk_bytes;
 };
 
@@ -209,6 +209,7 @@ static Plan make_plan(const Dims &d, int64_t P) {
   pl.LT = f.take(P * d.tp * d.np_ * 4);
   pl.Gw = f.take(P * d.tp * d.tp * 4);
   pl.Gc = f.take(P * d.tp * d.tp * 4);
+  pl.dinv = f.take(P * 64 * 64 * 4);
   pl.h = f.take(P * d.tp * 8);
   pl.w = f.take(P * d.tp * 8);
   pl.y = f.take(P * d.tp * 8);
@@ -356,7 +357,8 @@ static arckv_status run_fit_bias_chunk(const Ctx &c, int b0, int P, const void *
                              stream));
   STAGE(ST_GRAM_G, launch_gram(d.dtype, PhiT, Gw, Gc, P, d.tp, d.np_, stream));
   STAGE(ST_HVEC, launch_hvec(LT, zc, mc, P, d.n, d.t, d.tp, d.np_, h, stream));
-  STAGE(ST_CHOL_G, launch_cholesky(Gw, Gc, P, d.t, d.tp, fp.delta_beta, fp.max_escalations, st, stream));
+  STAGE(ST_CHOL_G, launch_cholesky(Gw, Gc, P, d.t, d.tp, fp.delta_beta, fp.max_escalations, st,
+                                   c.chunk<float>(c.pl.dinv), stream));
   {
     StageScope _sc(ST_SOLVE_W, stream);
     if (launch_trsv(Gw, P, d.tp, h, y, w, nullptr, st.info, stream) != hipSuccess) return ARCKV_ERR_HIP;
@@ -401,7 +403,8 @@ static arckv_status run_fit_values_chunk(const Ctx &c, int b0, int P, const floa
       return ARCKV_ERR_HIP;
     if (launch_rhs_gemm(d.dtype, PT, YT, Bm, P, d.tp, d.np_, stream) != hipSuccess) return ARCKV_ERR_HIP;
   }
-  STAGE(ST_CHOL_A, launch_cholesky(Gw, Gc, P, d.t, d.tp, fp.delta_v, fp.max_escalations, st, stream));
+  STAGE(ST_CHOL_A, launch_cholesky(Gw, Gc, P, d.t, d.tp, fp.delta_v, fp.max_escalations, st,
+                                   c.chunk<float>(c.pl.dinv), stream));
   {
     StageScope _sc(ST_SOLVE_V, stream);
     if (launch_trsm(true, Gw, P, d.tp, Bm, Y2, st.info, stream) != hipSuccess) return ARCKV_ERR_HIP;

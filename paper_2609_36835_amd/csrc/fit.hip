@@ -5,8 +5,10 @@
 // block with zero right-hand side, so padded unknowns solve to 0):
 //   k_ridge_init     lam = delta * tr(M)/t, write M + lam I into the work copy
 //   Cholesky         right-looking, float32, two-level blocking:
-//                      k_chol_diag    factor a 64 x 64 diagonal block in LDS
+//                      k_chol_diag    factor a 64 x 64 diagonal block in
+//                                     registers (one wave) and invert it
 //                      k_chol_panel   L_ik = A_ik L_kk^-T for row blocks i > k
+//                                     (fp32 MFMA with the inverse)
 //                      k_chol_upd     A -= L L^T over a panel's columns
 //                                     (fp32 MFMA, 128 x 128 tiles), once per
 //                                     64 columns inside a 256-wide outer panel
@@ -142,54 +144,144 @@ __device__ void update_tile(const float *sA, const float *sB, float *C, int64_t 
   }
 }
 
-__global__ void __launch_bounds__(256) k_chol_panel(float *__restrict__ Gw, int64_t ld, int k,
-                                                    const int32_t *__restrict__ info) {
-  __shared__ float sL[kNB * kSD], sX[kNB * kSD];
-  const int b = blockIdx.y;
+// Factor the 64 x 64 diagonal block k in place and write L_kk^-1 (one wave
+// per pair).  Lane r keeps row r of the block in registers; the pivot and the
+// finished column entries are broadcast with readlane, so the 64 column steps
+// need no LDS traffic or barriers.  Right-looking: after column c is scaled,
+// a[s] -= L[r][c] L[s][c] for s > c (entries above the diagonal are updated
+// too and ignored).  The inverse is formed column-per-lane by forward
+// substitution, x[r] = (e_r - sum_{q<r} L[r][q] x[q]) / L[r][r]; its upper
+// triangle comes out zero.
+__global__ void __launch_bounds__(64) k_chol_diag(float *__restrict__ Gw, int64_t ld, int k,
+                                                  int32_t *__restrict__ info, float *__restrict__ dinv) {
+  const int b = blockIdx.x, lane = threadIdx.x;
   if (info[b] != 0) return;
-  const int i = k + 1 + blockIdx.x;
-  float *G = Gw + (size_t)b * ld * ld;
-  load_tile(sL, G + (size_t)k * kNB * ld + k * kNB, ld);
-  load_tile(sX, G + (size_t)i * kNB * ld + k * kNB, ld);
-  trsm_tile(sL, sX);
-  store_tile(sX, G + (size_t)i * kNB * ld + k * kNB, ld);
+  float *D = Gw + (size_t)b * ld * ld + (size_t)k * kNB * ld + (size_t)k * kNB;
+  float a[kNB];
+#pragma unroll
+  for (int s4 = 0; s4 < kNB / 4; ++s4) {
+    const f32x4 v = *reinterpret_cast<const f32x4 *>(D + (size_t)lane * ld + 4 * s4);
+    a[4 * s4] = v[0];
+    a[4 * s4 + 1] = v[1];
+    a[4 * s4 + 2] = v[2];
+    a[4 * s4 + 3] = v[3];
+  }
+  auto bcast = [](float v, int src) { return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), src)); };
+  float rdiag[kNB];
+#pragma unroll
+  for (int c = 0; c < kNB; ++c) {
+    const float piv = bcast(a[c], c);
+    if (!(piv > 0.0f) || !isfinite(piv)) {
+      if (lane == 0) info[b] = k * kNB + c + 1;
+      return;
+    }
+    const float d = sqrtf(piv), inv = 1.0f / d;
+    rdiag[c] = inv;
+    a[c] = lane == c ? d : (lane > c ? a[c] * inv : a[c]);
+#pragma unroll
+    for (int s2 = c + 1; s2 < kNB; ++s2) a[s2] = fmaf(-a[c], bcast(a[c], s2), a[s2]);
+  }
+#pragma unroll
+  for (int s2 = 0; s2 < kNB; ++s2)
+    if (s2 <= lane) D[(size_t)lane * ld + s2] = a[s2];
+  float x[kNB];
+#pragma unroll
+  for (int r = 0; r < kNB; ++r) {
+    float acc = r == lane ? 1.0f : 0.0f;
+#pragma unroll
+    for (int q = 0; q < r; ++q) acc = fmaf(-bcast(a[q], r), x[q], acc);
+    x[r] = acc * rdiag[r];
+  }
+  float *Xi = dinv + (size_t)b * kNB * kNB;
+#pragma unroll
+  for (int r = 0; r < kNB; ++r) Xi[r * kNB + lane] = x[r];
 }
 
-// Factor the 64 x 64 diagonal block k in place (one workgroup per pair).
-__global__ void __launch_bounds__(256) k_chol_diag(float *__restrict__ Gw, int64_t ld, int k,
-                                                   int32_t *__restrict__ info) {
-  __shared__ float sD[kNB * kSD];
-  const int b = blockIdx.x;
+// Panel: L_ik = A_ik L_kk^-T for the rows below diagonal block k, as an fp32
+// MFMA product with the inverse from k_chol_diag.  A workgroup takes 128 rows
+// (4 waves x 32 rows x 64 columns).
+__global__ void __launch_bounds__(256) k_chol_panel(float *__restrict__ Gw, int64_t ld, int k,
+                                                    const float *__restrict__ dinv,
+                                                    const int32_t *__restrict__ info) {
+  __shared__ float sLi[kNB * kSD], sA[128 * kSD];
+  const int b = blockIdx.y;
   if (info[b] != 0) return;
-  float *D = Gw + (size_t)b * ld * ld + (size_t)k * kNB * ld + k * kNB;
-  load_tile(sD, D, ld);
-  const int fail = factor_tile(sD);
-  if (fail >= 0) {
-    if (threadIdx.x == 0) info[b] = k * kNB + fail + 1;
-    return;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, h = lane >> 5, col = lane & 31;
+  const int64_t rb = (int64_t)(k + 1) * kNB + 128 * (int64_t)blockIdx.x;
+  float *G = Gw + (size_t)b * ld * ld;
+  const float *Li = dinv + (size_t)b * kNB * kNB;
+  for (int e = tid; e < kNB * kNB / 4; e += 256) {
+    const int r = e / 16, c4 = (e % 16) * 4;
+    const f32x4 v = *reinterpret_cast<const f32x4 *>(Li + r * kNB + c4);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) sLi[r * kSD + c4 + q] = v[q];
   }
-  store_tile(sD, D, ld);
+  for (int e = tid; e < 128 * kNB / 4; e += 256) {
+    const int r = e / 16, c4 = (e % 16) * 4;
+    f32x4 v = {0.f, 0.f, 0.f, 0.f};
+    if (rb + r < ld) v = *reinterpret_cast<const f32x4 *>(G + (size_t)(rb + r) * ld + (size_t)k * kNB + c4);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) sA[r * kSD + c4 + q] = v[q];
+  }
+  __syncthreads();
+  f32x16 acc0 = zero16(), acc1 = zero16();
+#pragma unroll
+  for (int ks = 0; ks < kNB / 2; ++ks) {
+    const float fa = sA[(32 * wave + col) * kSD + 2 * ks + h];
+    acc0 = Mfma<float>::mma(fa, sLi[col * kSD + 2 * ks + h], acc0);
+    acc1 = Mfma<float>::mma(fa, sLi[(32 + col) * kSD + 2 * ks + h], acc1);
+  }
+#pragma unroll
+  for (int v = 0; v < 16; ++v) {
+    const int64_t r = rb + 32 * wave + acc_row(v, lane);
+    if (r < ld) {
+      G[(size_t)r * ld + (size_t)k * kNB + col] = acc0[v];
+      G[(size_t)r * ld + (size_t)k * kNB + 32 + col] = acc1[v];
+    }
+  }
 }
 
 // Trailing update of the blocked factorisation on fp32 MFMA:
 //   G[r][c] -= sum_{q in [q0, q0+kw)} L[r][q] L[c][q]
-// for r in [r_lo, ld), c in [c_lo, c_hi), with 128 x 128 output tiles (4
-// waves of 64 x 64) starting at (r_lo, c_lo); tiles entirely above the
-// diagonal exit at once, and rows/columns past the region are masked.  The L
-// operands are the finished panel columns [q0, q0+kw), streamed through LDS
-// in slabs of 32.
-__global__ void __launch_bounds__(256) k_chol_upd(float *__restrict__ Gw, int64_t ld, int r_lo, int c_lo, int c_hi,
-                                                  int q0, int kw, int n_ct, const int32_t *__restrict__ info) {
+// for r in [r_lo, ld), c in [r_lo, c_hi), c <= r (up to the 64-wide diagonal
+// block), with 128 x 128 output tiles (4 waves of 64 x 64).  Only tiles on or
+// below the diagonal are launched: row tile ti holds column tiles
+// tj < min(ti + 1, n_ct); workgroups are remapped so each XCD owns a
+// contiguous range of (pair, tile).  The L operands are the finished panel
+// columns [q0, q0+kw), streamed through LDS in slabs of 32.
+__device__ inline void chol_upd_tile(int64_t idx, int n_ct, int &ti, int &tj) {
+  const int64_t tri = (int64_t)n_ct * (n_ct + 1) / 2;
+  if (idx < tri) {
+    int m = (int)((sqrt(8.0 * (double)idx + 1.0) - 1.0) * 0.5);
+    while ((int64_t)m * (m + 1) / 2 > idx) --m;
+    while ((int64_t)(m + 1) * (m + 2) / 2 <= idx) ++m;
+    ti = m;
+    tj = (int)(idx - (int64_t)m * (m + 1) / 2);
+  } else {
+    const int64_t r = idx - tri;
+    ti = n_ct + (int)(r / n_ct);
+    tj = (int)(r % n_ct);
+  }
+}
+
+__host__ __device__ inline int64_t chol_upd_tiles(int n_rt, int n_ct) {
+  return (int64_t)n_ct * (n_ct + 1) / 2 + (int64_t)(n_rt - n_ct) * n_ct;
+}
+
+__global__ void __launch_bounds__(256) k_chol_upd(float *__restrict__ Gw, int64_t ld, int r_lo, int c_hi, int q0,
+                                                  int kw, int n_rt, int n_ct, const int32_t *__restrict__ info) {
   // LDS rows of 33 floats: the 4-byte fragment reads of 32 consecutive rows
   // then fall in 32 distinct banks.  Two buffers; the next slab is fetched into
   // registers while the current one is consumed.
   constexpr int TB = 128, BKc = 32, SLc = BKc + 1, CHc = TB * BKc / 4 / 256;
   __shared__ float sA[2][TB * SLc], sB[2][TB * SLc];
-  const int b = blockIdx.y;
+  const int64_t per = chol_upd_tiles(n_rt, n_ct);
+  const int64_t tile = xcd_remap(blockIdx.x, gridDim.x);
+  const int b = (int)(tile / per);
   if (info[b] != 0) return;
-  const int ti = blockIdx.x / n_ct, tj = blockIdx.x % n_ct;
-  const int rb = r_lo + TB * ti, cb = c_lo + TB * tj;
-  if (cb > rb + TB - 1) return;               // entirely above the diagonal
+  int ti, tj;
+  chol_upd_tile(tile % per, n_ct, ti, tj);
+  const int rb = r_lo + TB * ti, cb = r_lo + TB * tj;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1, h = lane >> 5, col = lane & 31;
   float *G = Gw + (size_t)b * ld * ld;
@@ -245,6 +337,22 @@ __global__ void __launch_bounds__(256) k_chol_upd(float *__restrict__ Gw, int64_
     __syncthreads();
     bf ^= 1;
   }
+  // Read-modify-write of the tile: every old value is loaded (unconditionally,
+  // from a clamped in-range address) before any store, so the loads pipeline
+  // instead of paying one memory round trip each.
+  const int64_t lm = ld - 1;
+  float old[2][2][16];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int64_t c = cb + wn * 64 + 32 * j + col, cc = c < lm ? c : lm;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int64_t r = rb + wm * 64 + 32 * i + acc_row(v, lane), rr = r < lm ? r : lm;
+        old[i][j][v] = __builtin_nontemporal_load(&G[rr * ld + cc]);
+      }
+    }
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
@@ -253,7 +361,7 @@ __global__ void __launch_bounds__(256) k_chol_upd(float *__restrict__ Gw, int64_
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
         const int r = rb + wm * 64 + 32 * i + acc_row(v, lane);
-        if (r < ld && c < c_hi && c <= r + 63) G[(size_t)r * ld + c] -= acc[i][j][v];
+        if (r < ld && c < c_hi && c <= r + 63) G[(size_t)r * ld + c] = old[i][j][v] - acc[i][j][v];
       }
     }
 }
@@ -762,7 +870,7 @@ hipError_t launch_hvec(const float *LT, const float *z, const float *m, int B, i
 
 // Ridge + factorisation (+ escalation) of the work copy Gw of Gc.
 hipError_t launch_cholesky(float *Gw, const float *Gc, int B, int t, int64_t ld, float delta0, int max_esc,
-                           FitState st, hipStream_t s) {
+                           FitState st, float *dinv, hipStream_t s) {
   hipLaunchKernelGGL(k_ridge_init, dim3(B), dim3(256), 0, s, Gw, Gc, t, ld, delta0, st);
   // Two-level right-looking blocking: 64-wide diagonal factor + panel solve
   // steps inside 256-wide outer panels; inside an outer panel only its own
@@ -775,19 +883,20 @@ hipError_t launch_cholesky(float *Gw, const float *Gc, int B, int t, int64_t ld,
     const int K1 = (int)(K0 + kOuter < ld ? K0 + kOuter : ld);
     for (int c = K0; c < K1; c += kNB) {
       const int k = c / kNB;
-      hipLaunchKernelGGL(k_chol_diag, dim3(B), dim3(256), 0, s, Gw, ld, k, st.info);
+      hipLaunchKernelGGL(k_chol_diag, dim3(B), dim3(64), 0, s, Gw, ld, k, st.info, dinv);
       const int rem = nrb - k - 1;
-      if (rem > 0) hipLaunchKernelGGL(k_chol_panel, dim3(rem, B), dim3(256), 0, s, Gw, ld, k, st.info);
+      if (rem > 0)
+        hipLaunchKernelGGL(k_chol_panel, dim3((rem + 1) / 2, B), dim3(256), 0, s, Gw, ld, k, dinv, st.info);
       if (c + kNB < K1) {
         const int r_lo = c + kNB, n_rt = (int)((ld - r_lo + 127) / 128), n_ct = (K1 - r_lo + 127) / 128;
-        hipLaunchKernelGGL(k_chol_upd, dim3(n_rt * n_ct, B), dim3(256), 0, s, Gw, ld, r_lo, r_lo, K1, c, kNB, n_ct,
-                           st.info);
+        hipLaunchKernelGGL(k_chol_upd, dim3((unsigned)(chol_upd_tiles(n_rt, n_ct) * B)), dim3(256), 0, s, Gw, ld,
+                           r_lo, K1, c, kNB, n_rt, n_ct, st.info);
       }
     }
     if (K1 < ld) {
       const int n_rt = (int)((ld - K1 + 127) / 128), n_ct = n_rt;
-      hipLaunchKernelGGL(k_chol_upd, dim3(n_rt * n_ct, B), dim3(256), 0, s, Gw, ld, K1, K1, (int)ld, K0,
-                         K1 - K0, n_ct, st.info);
+      hipLaunchKernelGGL(k_chol_upd, dim3((unsigned)(chol_upd_tiles(n_rt, n_ct) * B)), dim3(256), 0, s, Gw, ld, K1,
+                         (int)ld, K0, K1 - K0, n_rt, n_ct, st.info);
     }
   }
   if (max_esc > 0) hipLaunchKernelGGL(k_chol_escalate, dim3(B), dim3(256), 0, s, Gw, Gc, t, ld, max_esc, st);
