@@ -68,8 +68,8 @@ hipError_t launch_phat(int dtype, const float *LT, const float *beta_ws, int B, 
                        int64_t np_, void *out, hipStream_t s);
 hipError_t launch_transpose128(int dtype, const float *in, int B, int rows, int64_t in_pair, int64_t rows_pad,
                                void *out, int64_t out_pair, hipStream_t s);
-hipError_t launch_trsm(bool fwd, const float *Gw, int B, int64_t ld, const float *R, float *X, const int32_t *info,
-                       hipStream_t s);
+hipError_t launch_trsm(bool fwd, const float *Gw, const float *dinv, int B, int64_t ld, const float *R, float *X,
+                       const int32_t *info, hipStream_t s);
 hipError_t launch_add(float *x, const float *dx, int B, int64_t n_per, const int32_t *info, hipStream_t s);
 hipError_t launch_values_out(const float *Xp, int B, int64_t tp, int t, const int32_t *info, float *Cv,
                              hipStream_t s);
@@ -209,7 +209,7 @@ static Plan make_plan(const Dims &d, int64_t P) {
   pl.LT = f.take(P * d.tp * d.np_ * 4);
   pl.Gw = f.take(P * d.tp * d.tp * 4);
   pl.Gc = f.take(P * d.tp * d.tp * 4);
-  pl.dinv = f.take(P * 64 * 64 * 4);
+  pl.dinv = f.take(P * d.tp * 64 * 4);   // one 64 x 64 inverse per diagonal block
   pl.h = f.take(P * d.tp * 8);
   pl.w = f.take(P * d.tp * 8);
   pl.y = f.take(P * d.tp * 8);
@@ -388,7 +388,7 @@ static arckv_status run_fit_values_chunk(const Ctx &c, int b0, int P, const floa
   float *LT = c.chunk<float>(c.pl.LT), *Gw = c.chunk<float>(c.pl.Gw), *Gc = c.chunk<float>(c.pl.Gc);
   void *YT = c.chunk<char>(c.pl.YT);
   float *Bm = c.chunk<float>(c.pl.Bm), *X = c.chunk<float>(c.pl.X), *R = c.chunk<float>(c.pl.R);
-  float *Y2 = c.chunk<float>(c.pl.Y2);
+  float *Y2 = c.chunk<float>(c.pl.Y2), *dinv = c.chunk<float>(c.pl.dinv);
   void *XT = c.chunk<char>(c.pl.XT), *Pm = c.chunk<char>(c.pl.Pm), *UT = c.chunk<char>(c.pl.UT);
   const float *Yc = Y + (size_t)b0 * d.n * kHeadDimH;
   const int64_t pl = d.dtype == ARCKV_BF16 ? 2 : 1;
@@ -403,12 +403,11 @@ static arckv_status run_fit_values_chunk(const Ctx &c, int b0, int P, const floa
       return ARCKV_ERR_HIP;
     if (launch_rhs_gemm(d.dtype, PT, YT, Bm, P, d.tp, d.np_, stream) != hipSuccess) return ARCKV_ERR_HIP;
   }
-  STAGE(ST_CHOL_A, launch_cholesky(Gw, Gc, P, d.t, d.tp, fp.delta_v, fp.max_escalations, st,
-                                   c.chunk<float>(c.pl.dinv), stream));
+  STAGE(ST_CHOL_A, launch_cholesky(Gw, Gc, P, d.t, d.tp, fp.delta_v, fp.max_escalations, st, dinv, stream));
   {
     StageScope _sc(ST_SOLVE_V, stream);
-    if (launch_trsm(true, Gw, P, d.tp, Bm, Y2, st.info, stream) != hipSuccess) return ARCKV_ERR_HIP;
-    if (launch_trsm(false, Gw, P, d.tp, Y2, X, st.info, stream) != hipSuccess) return ARCKV_ERR_HIP;
+    if (launch_trsm(true, Gw, dinv, P, d.tp, Bm, Y2, st.info, stream) != hipSuccess) return ARCKV_ERR_HIP;
+    if (launch_trsm(false, Gw, dinv, P, d.tp, Y2, X, st.info, stream) != hipSuccess) return ARCKV_ERR_HIP;
     // refinement against the data: R = P^T (Y - P X) - lam X
     if (fp.refine_steps > 0 && launch_transpose_planes(d.dtype, PT, Pm, P, d.tp, d.np_, stream) != hipSuccess)
       return ARCKV_ERR_HIP;
@@ -418,8 +417,8 @@ static arckv_status run_fit_values_chunk(const Ctx &c, int b0, int P, const floa
         return ARCKV_ERR_HIP;
       if (launch_value_residual(d.dtype, XT, Pm, PT, Yc, UT, X, st.lam, R, P, d.n, d.tp, d.np_, stream) != hipSuccess)
         return ARCKV_ERR_HIP;
-      if (launch_trsm(true, Gw, P, d.tp, R, Y2, st.info, stream) != hipSuccess) return ARCKV_ERR_HIP;
-      if (launch_trsm(false, Gw, P, d.tp, Y2, R, st.info, stream) != hipSuccess) return ARCKV_ERR_HIP;
+      if (launch_trsm(true, Gw, dinv, P, d.tp, R, Y2, st.info, stream) != hipSuccess) return ARCKV_ERR_HIP;
+      if (launch_trsm(false, Gw, dinv, P, d.tp, Y2, R, st.info, stream) != hipSuccess) return ARCKV_ERR_HIP;
       if (launch_add(X, R, P, d.tp * kHeadDimH, st.info, stream) != hipSuccess) return ARCKV_ERR_HIP;
     }
     if (launch_values_out(X, P, d.tp, d.t, st.info, Cv + (size_t)b0 * d.t * kHeadDimH, stream) != hipSuccess)

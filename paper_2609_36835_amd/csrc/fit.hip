@@ -144,14 +144,32 @@ __device__ void update_tile(const float *sA, const float *sB, float *C, int64_t 
   }
 }
 
-// Factor the 64 x 64 diagonal block k in place and write L_kk^-1 (one wave
-// per pair).  Lane r keeps row r of the block in registers; the pivot and the
-// finished column entries are broadcast with readlane, so the 64 column steps
-// need no LDS traffic or barriers.  Right-looking: after column c is scaled,
-// a[s] -= L[r][c] L[s][c] for s > c (entries above the diagonal are updated
-// too and ignored).  The inverse is formed column-per-lane by forward
-// substitution, x[r] = (e_r - sum_{q<r} L[r][q] x[q]) / L[r][r]; its upper
-// triangle comes out zero.
+// Inverse of a factored 64 x 64 lower-triangular block whose row `lane` is
+// held in a[] by lane `lane` of the wave; rdiag[r] = 1 / L[r][r].  Forward
+// substitution column-per-lane, x[r] = (e_r - sum_{q<r} L[r][q] x[q]) L[r][r]^-1
+// with L[r][q] broadcast from lane r; the upper triangle comes out zero.  Row
+// r of the inverse is written to Xi[r][0..63].
+__device__ __forceinline__ void tri_inverse_64(const float (&a)[kNB], const float (&rdiag)[kNB], int lane,
+                                               float *__restrict__ Xi) {
+  auto bcast = [](float v, int src) { return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), src)); };
+  float x[kNB];
+#pragma unroll
+  for (int r = 0; r < kNB; ++r) {
+    float acc = r == lane ? 1.0f : 0.0f;
+#pragma unroll
+    for (int q = 0; q < r; ++q) acc = fmaf(-bcast(a[q], r), x[q], acc);
+    x[r] = acc * rdiag[r];
+  }
+#pragma unroll
+  for (int r = 0; r < kNB; ++r) Xi[r * kNB + lane] = x[r];
+}
+
+// Factor the 64 x 64 diagonal block k in place and write L_kk^-1 to
+// dinv[b][k] (one wave per pair).  Lane r keeps row r of the block in
+// registers; the pivot and the finished column entries are broadcast with
+// readlane, so the 64 column steps need no LDS traffic or barriers.
+// Right-looking: after column c is scaled, a[s] -= L[r][c] L[s][c] for s > c
+// (entries above the diagonal are updated too and ignored).
 __global__ void __launch_bounds__(64) k_chol_diag(float *__restrict__ Gw, int64_t ld, int k,
                                                   int32_t *__restrict__ info, float *__restrict__ dinv) {
   const int b = blockIdx.x, lane = threadIdx.x;
@@ -184,17 +202,25 @@ __global__ void __launch_bounds__(64) k_chol_diag(float *__restrict__ Gw, int64_
 #pragma unroll
   for (int s2 = 0; s2 < kNB; ++s2)
     if (s2 <= lane) D[(size_t)lane * ld + s2] = a[s2];
-  float x[kNB];
+  tri_inverse_64(a, rdiag, lane, dinv + ((size_t)b * (ld / kNB) + k) * kNB * kNB);
+}
+
+// Diagonal-block inverses of a finished factor, for pairs whose factorisation
+// went through the escalation path (delta differs from its initial value).
+__global__ void __launch_bounds__(64) k_chol_dinv_escalated(const float *__restrict__ Gw, int64_t ld, float delta0,
+                                                            const float *__restrict__ delta,
+                                                            const int32_t *__restrict__ info,
+                                                            float *__restrict__ dinv) {
+  const int k = blockIdx.x, b = blockIdx.y, lane = threadIdx.x;
+  if (info[b] != 0 || delta[b] == delta0) return;
+  const float *D = Gw + (size_t)b * ld * ld + (size_t)k * kNB * ld + (size_t)k * kNB;
+  float a[kNB], rdiag[kNB];
 #pragma unroll
-  for (int r = 0; r < kNB; ++r) {
-    float acc = r == lane ? 1.0f : 0.0f;
+  for (int s2 = 0; s2 < kNB; ++s2) a[s2] = s2 <= lane ? D[(size_t)lane * ld + s2] : 0.0f;
+  auto bcast = [](float v, int src) { return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), src)); };
 #pragma unroll
-    for (int q = 0; q < r; ++q) acc = fmaf(-bcast(a[q], r), x[q], acc);
-    x[r] = acc * rdiag[r];
-  }
-  float *Xi = dinv + (size_t)b * kNB * kNB;
-#pragma unroll
-  for (int r = 0; r < kNB; ++r) Xi[r * kNB + lane] = x[r];
+  for (int r = 0; r < kNB; ++r) rdiag[r] = 1.0f / bcast(a[r], r);
+  tri_inverse_64(a, rdiag, lane, dinv + ((size_t)b * (ld / kNB) + k) * kNB * kNB);
 }
 
 // Panel: L_ik = A_ik L_kk^-T for the rows below diagonal block k, as an fp32
@@ -209,7 +235,7 @@ __global__ void __launch_bounds__(256) k_chol_panel(float *__restrict__ Gw, int6
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, h = lane >> 5, col = lane & 31;
   const int64_t rb = (int64_t)(k + 1) * kNB + 128 * (int64_t)blockIdx.x;
   float *G = Gw + (size_t)b * ld * ld;
-  const float *Li = dinv + (size_t)b * kNB * kNB;
+  const float *Li = dinv + ((size_t)b * (ld / kNB) + k) * kNB * kNB;
   for (int e = tid; e < kNB * kNB / 4; e += 256) {
     const int r = e / 16, c4 = (e % 16) * 4;
     const f32x4 v = *reinterpret_cast<const f32x4 *>(Li + r * kNB + c4);
@@ -740,15 +766,17 @@ __global__ void __launch_bounds__(256) k_trsm(const float *__restrict__ Gw, int6
   }
 }
 
-// MFMA variant of the 128-rhs substitution: two workgroups per pair, 64
-// columns each; 64-row blocks.  The update  acc = sum_p L_blk,p X_p  (forward)
-// or  sum_p L_p,blk^T X_p  (backward) runs on fp32 MFMA 32x32x2 with the L
-// tile and the X tile staged in LDS (4 waves = 2 row tiles x 2 column tiles);
-// the 64 x 64 diagonal block is then solved column-parallel in LDS.
+// 128-rhs triangular solve on fp32 MFMA: L X = R (forward) or L^T X = R
+// (backward), two workgroups per pair with 64 columns each, 64-row blocks.
+// For block kb the update  acc = sum_p L_kb,p X_p  (forward) or
+// sum_p L_p,kb^T X_p  (backward) is an MFMA product with the L tile and the X
+// tile staged in LDS (4 waves = 2 row tiles x 2 column tiles); the block is then
+// X_kb = D (R_kb - acc) with D = L_kb,kb^-1 (forward) or its transpose
+// (backward), the diagonal-block inverses written by the factorisation.
 template <bool FWD>
 __global__ void __launch_bounds__(256) k_trsm_mfma(const float *__restrict__ Gw, int64_t ld,
-                                                   const float *__restrict__ R, float *__restrict__ X,
-                                                   const int32_t *__restrict__ info) {
+                                                   const float *__restrict__ dinv, const float *__restrict__ R,
+                                                   float *__restrict__ X, const int32_t *__restrict__ info) {
   constexpr int RB = 64, NC = 64, SLD = RB + 1, SXD = NC + 1;
   __shared__ float sL[2][RB * SLD];
   __shared__ float sX[2][RB * SXD];
@@ -760,6 +788,7 @@ __global__ void __launch_bounds__(256) k_trsm_mfma(const float *__restrict__ Gw,
   const float *Rb = R + (size_t)b * ld * kHeadDim;
   float *Xb = X + (size_t)b * ld * kHeadDim;
   const int nb = (int)(ld / RB);
+  const float *Db = dinv + (size_t)b * nb * RB * RB;
   f32x4 rl[4], rx[4];
   // tile (i, k) of the operand: forward L[r0+i][p0+k], backward L[p0+k][r0+i]
   auto fetch = [&](int r0, int p0) {
@@ -807,37 +836,32 @@ __global__ void __launch_bounds__(256) k_trsm_mfma(const float *__restrict__ Gw,
       bf ^= 1;
     }
     __syncthreads();
-    // right-hand side minus update, into sX[0]; diagonal block into sL[0] (transposed for backward)
+    // right-hand side minus update into sX[0]; D into sL[0] (row r = output row)
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
       const int r = 32 * wr + acc_row(v, lane), c = 32 * wc + col;
       sX[0][r * SXD + c] = Rb[(size_t)(r0 + r) * kHeadDim + c0 + c] - acc[v];
     }
-    for (int e = tid; e < RB * RB; e += 256) {
-      const int i = e / RB, k = e % RB;
-      sL[0][i * SLD + k] = FWD ? L[(size_t)(r0 + i) * ld + r0 + k] : L[(size_t)(r0 + k) * ld + r0 + i];
-    }
-    __syncthreads();
-    if (tid < NC) {
-      const int c = tid;
-      if (FWD) {
-        for (int r = 0; r < RB; ++r) {
-          float v = sX[0][r * SXD + c];
-          for (int q = 0; q < r; ++q) v -= sL[0][r * SLD + q] * sX[0][q * SXD + c];
-          sX[0][r * SXD + c] = v / sL[0][r * SLD + r];
-        }
-      } else {
-        for (int r = RB - 1; r >= 0; --r) {
-          float v = sX[0][r * SXD + c];
-          for (int q = r + 1; q < RB; ++q) v -= sL[0][r * SLD + q] * sX[0][q * SXD + c];
-          sX[0][r * SXD + c] = v / sL[0][r * SLD + r];
-        }
+    const float *Dk = Db + (size_t)kb * RB * RB;
+    for (int e = tid; e < RB * RB / 4; e += 256) {
+      const int i = e / 16, k4 = (e % 16) * 4;
+      const f32x4 v = *reinterpret_cast<const f32x4 *>(Dk + i * RB + k4);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        if (FWD) sL[0][i * SLD + k4 + q] = v[q];
+        else sL[0][(k4 + q) * SLD + i] = v[q];
       }
     }
     __syncthreads();
-    for (int e = tid; e < RB * NC; e += 256) {
-      const int r = e / NC, c = e % NC;
-      Xb[(size_t)(r0 + r) * kHeadDim + c0 + c] = sX[0][r * SXD + c];
+    f32x16 out = zero16();
+#pragma unroll 8
+    for (int ks = 0; ks < RB / 2; ++ks)
+      out = Mfma<float>::mma(sL[0][(32 * wr + col) * SLD + 2 * ks + h], sX[0][(2 * ks + h) * SXD + 32 * wc + col],
+                             out);
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int r = 32 * wr + acc_row(v, lane), c = 32 * wc + col;
+      Xb[(size_t)(r0 + r) * kHeadDim + c0 + c] = out[v];
     }
     __threadfence_block();
   }
@@ -899,7 +923,10 @@ hipError_t launch_cholesky(float *Gw, const float *Gc, int B, int t, int64_t ld,
                          (int)ld, K0, K1 - K0, n_rt, n_ct, st.info);
     }
   }
-  if (max_esc > 0) hipLaunchKernelGGL(k_chol_escalate, dim3(B), dim3(256), 0, s, Gw, Gc, t, ld, max_esc, st);
+  if (max_esc > 0) {
+    hipLaunchKernelGGL(k_chol_escalate, dim3(B), dim3(256), 0, s, Gw, Gc, t, ld, max_esc, st);
+    hipLaunchKernelGGL(k_chol_dinv_escalated, dim3(nrb, B), dim3(64), 0, s, Gw, ld, delta0, st.delta, st.info, dinv);
+  }
   return hipGetLastError();
 }
 
@@ -964,13 +991,13 @@ hipError_t launch_transpose128(int dtype, const float *in, int B, int rows, int6
   return hipGetLastError();
 }
 
-hipError_t launch_trsm(bool fwd, const float *Gw, int B, int64_t ld, const float *R, float *X, const int32_t *info,
-                       hipStream_t s) {
+hipError_t launch_trsm(bool fwd, const float *Gw, const float *dinv, int B, int64_t ld, const float *R, float *X,
+                       const int32_t *info, hipStream_t s) {
   dim3 grid(kHeadDim / 64, B);
   if (fwd)
-    hipLaunchKernelGGL(k_trsm_mfma<true>, grid, dim3(256), 0, s, Gw, ld, R, X, info);
+    hipLaunchKernelGGL(k_trsm_mfma<true>, grid, dim3(256), 0, s, Gw, ld, dinv, R, X, info);
   else
-    hipLaunchKernelGGL(k_trsm_mfma<false>, grid, dim3(256), 0, s, Gw, ld, R, X, info);
+    hipLaunchKernelGGL(k_trsm_mfma<false>, grid, dim3(256), 0, s, Gw, ld, dinv, R, X, info);
   return hipGetLastError();
 }
 

@@ -67,3 +67,36 @@ def test_tiny_and_ragged_shapes(T, n_pos, rho):
             assert np.isfinite(np64(beta[b])).all()
         if info[b, 1] == 0:
             assert np.isfinite(np64(Cv[b])).all()
+
+
+def test_escalated_value_fit_matches_oracle_at_used_ridge():
+    """More compact keys than reference queries (t = 600 > n = 256) makes the
+    value-fit Gram rank-deficient; with a 1e-9 relative ridge the float32
+    factorisation fails and the ridge is escalated (x10 per retry).  The solve
+    that follows must use the escalated factor: compare with the float64 fit
+    at the ridge the library reports.  Ill-conditioned (ridge ~1e-5 of the
+    mean diagonal), so the bar is 1e-3 rather than the well-posed 1e-4."""
+    wl = synth.custom("esc", kv_heads=2, T=2000, q_heads_per_kv=2, n_pos=128, rho=0.3, dtype="f32", rope=True)
+    dev, host = make_inputs(wl)
+    s = 1.0 / math.sqrt(128)
+    t = oracle.budget(wl.T, wl.rho)
+    assert t > wl.n
+    refs = [oracle.compact_pair(host["K"][b], host["V"][b], host["Q"][b], host["W1"][b], host["b1"][b],
+                                host["w2"][b], host["b2"][b], t=t, scale=s) for b in range(wl.pairs)]
+    Ck = np.stack([r.C_k for r in refs]).astype(np.float32)
+    beta = np.stack([r.beta for r in refs]).astype(np.float32)
+    Y = np.stack([r.Y for r in refs]).astype(np.float32)
+    params = A().default_params(delta_v=1e-9, max_escalations=6)
+    Cv, info, dused = A().fit_values(dev["Q"], torch.from_numpy(Ck).cuda(), torch.from_numpy(beta).cuda(),
+                                     torch.from_numpy(Y).cuda(), params=params, scale=s, T=wl.T)
+    Cv, info, dused = np64(Cv), info.cpu().numpy(), dused.cpu().numpy()
+    assert np.all(info == 0), info
+    assert np.all(dused > 1e-9), dused        # every pair went through the escalation path
+    for b in range(wl.pairs):
+        Q = host["Q"][b]
+        vf = oracle.fit_values(Q, Ck[b].astype(np.float64), beta[b].astype(np.float64), Y[b].astype(np.float64), s,
+                               delta=float(dused[b]))
+        err = oracle.row_rel_err(oracle.attend_compact(Q, Ck[b], beta[b], Cv[b], s),
+                                 oracle.attend_compact(Q, Ck[b], beta[b], vf.C_v, s)).max()
+        print(f"  pair {b}: ridge escalated to {dused[b]:.1e}; output max row rel err {err:.3e}", flush=True)
+        assert err <= 1e-3, (b, err)
