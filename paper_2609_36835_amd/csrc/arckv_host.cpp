@@ -58,10 +58,8 @@ hipError_t launch_hvec(const float *LT, const float *z, const float *m, int B, i
                        double *h, hipStream_t s);
 hipError_t launch_cholesky(float *Gw, const float *Gc, int B, int t, int64_t ld, float delta0, int max_esc,
                            FitState st, float *dinv, hipStream_t s);
-hipError_t launch_trsv(const float *Gw, int B, int64_t ld, const double *rhs, double *y, double *x, double *acc,
-                       const int32_t *info, hipStream_t s);
-hipError_t launch_residual_vec(const float *Gc, int B, int64_t ld, int t, const double *rhs, const double *x,
-                               const float *lam, double *res, const int32_t *info, hipStream_t s);
+hipError_t launch_trsv(const float *Gw, const float *dinv, int B, int64_t ld, const double *rhs, double *sw,
+                       double *y, double *x, double *acc, const int32_t *info, hipStream_t s);
 hipError_t launch_bias_finalize(const double *w, int B, int64_t ld, int t, float eps, float bmin, float bmax,
                                 const int32_t *info, float *beta, float *beta_ws, hipStream_t s);
 hipError_t launch_phat(int dtype, const float *LT, const float *beta_ws, int B, int n, int t, int64_t tp,
@@ -171,7 +169,7 @@ struct Plan {
   // chunk region (offsets relative to chunk base)
   int64_t Ckp;
   int64_t Et, U, part, offsets, cursor, perm;            // merge phase
-  int64_t PhiT, LT, Gw, Gc, dinv, h, w, y, x, res, u, YT, Bm, X, R, Y2, XT, Pm, UT;  // fit phase
+  int64_t PhiT, LT, Gw, Gc, dinv, h, w, y, x, res, sw, u, YT, Bm, X, R, Y2, XT, Pm, UT;  // fit phase
   int64_t chunk_bytes;
 };
 
@@ -215,6 +213,7 @@ static Plan make_plan(const Dims &d, int64_t P) {
   pl.y = f.take(P * d.tp * 8);
   pl.x = f.take(P * d.tp * 8);
   pl.res = f.take(P * d.tp * 8);
+  pl.sw = f.take(P * d.tp * 8);
   pl.u = f.take(P * d.np_ * 8);
   pl.YT = f.take(P * kHeadDimH * d.np_ * 4);
   pl.Bm = f.take(P * d.tp * kHeadDimH * 4);
@@ -352,22 +351,22 @@ static arckv_status run_fit_bias_chunk(const Ctx &c, int b0, int P, const void *
   void *PhiT = c.chunk<char>(c.pl.PhiT);
   float *LT = c.chunk<float>(c.pl.LT), *Gw = c.chunk<float>(c.pl.Gw), *Gc = c.chunk<float>(c.pl.Gc);
   double *h = c.chunk<double>(c.pl.h), *w = c.chunk<double>(c.pl.w), *y = c.chunk<double>(c.pl.y);
-  double *x = c.chunk<double>(c.pl.x), *res = c.chunk<double>(c.pl.res);
+  double *x = c.chunk<double>(c.pl.x), *res = c.chunk<double>(c.pl.res), *sw = c.chunk<double>(c.pl.sw);
+  float *dinv = c.chunk<float>(c.pl.dinv);
   STAGE(ST_PHIC, launch_phic(d.dtype, Qc, c.chunk<char>(c.pl.Ckp), zc, PhiT, LT, P, d.t, d.n, d.tp, d.np_, c.scale,
                              stream));
   STAGE(ST_GRAM_G, launch_gram(d.dtype, PhiT, Gw, Gc, P, d.tp, d.np_, stream));
   STAGE(ST_HVEC, launch_hvec(LT, zc, mc, P, d.n, d.t, d.tp, d.np_, h, stream));
-  STAGE(ST_CHOL_G, launch_cholesky(Gw, Gc, P, d.t, d.tp, fp.delta_beta, fp.max_escalations, st,
-                                   c.chunk<float>(c.pl.dinv), stream));
+  STAGE(ST_CHOL_G, launch_cholesky(Gw, Gc, P, d.t, d.tp, fp.delta_beta, fp.max_escalations, st, dinv, stream));
   {
     StageScope _sc(ST_SOLVE_W, stream);
-    if (launch_trsv(Gw, P, d.tp, h, y, w, nullptr, st.info, stream) != hipSuccess) return ARCKV_ERR_HIP;
+    if (launch_trsv(Gw, dinv, P, d.tp, h, sw, y, w, nullptr, st.info, stream) != hipSuccess) return ARCKV_ERR_HIP;
     // refinement against the data: res = Phi_C^T (m - Phi_C w) - lam w
     double *u = c.chunk<double>(c.pl.u);
     for (int it = 0; it < fp.refine_steps; ++it) {
       if (launch_mass_residual(LT, zc, mc, w, st.lam, P, d.n, d.t, d.tp, d.np_, u, res, st.info, stream) != hipSuccess)
         return ARCKV_ERR_HIP;
-      if (launch_trsv(Gw, P, d.tp, res, y, x, w, st.info, stream) != hipSuccess) return ARCKV_ERR_HIP;
+      if (launch_trsv(Gw, dinv, P, d.tp, res, sw, y, x, w, st.info, stream) != hipSuccess) return ARCKV_ERR_HIP;
     }
     if (launch_bias_finalize(w, P, d.tp, d.t, fp.eps_w, fp.b_min, fp.b_max, st.info, beta + (size_t)b0 * d.t,
                              c.pers<float>(c.pl.beta_ws) + (size_t)b0 * d.tp, stream) != hipSuccess)

@@ -451,100 +451,62 @@ __global__ void __launch_bounds__(256) k_chol_escalate(float *__restrict__ Gw, c
 }
 
 // --------------------------------------------------------------- one right-hand side
-__device__ inline double readlane_f64(double v, int lane) {
-  const int64_t bits = __double_as_longlong(v);
-  const int lo = __builtin_amdgcn_readlane((int)(bits & 0xFFFFFFFF), lane);
-  const int hi = __builtin_amdgcn_readlane((int)(bits >> 32), lane);
-  return __longlong_as_double(((int64_t)hi << 32) | (uint32_t)lo);
-}
-
-// Forward L y = rhs, then backward L^T x = y, float64 accumulation; x written
-// to `x` (and added to `acc` if non-null).  One workgroup per pair, 64-row
-// blocks.  Off-diagonal products: each lane accumulates 16 rows over a strided
-// set of columns and a single LDS pass reduces them; diagonal blocks: column
-// substitution in one wave with the solved value broadcast by readlane.
-__global__ void __launch_bounds__(256) k_trsv(const float *__restrict__ Gw, int64_t ld, const double *__restrict__ rhs,
-                                              double *__restrict__ y, double *__restrict__ x,
-                                              double *__restrict__ acc, const int32_t *__restrict__ info) {
-  __shared__ double red[kNB][kNB + 1];
-  __shared__ float sD[kNB * kSD];
-  __shared__ double sb[kNB];
-  const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+// One-rhs triangular solves, float64 vectors, right-looking over 64-row
+// blocks with one launch per block j, so that every block row below (forward)
+// or above (backward) is updated by its own workgroup:
+//   forward  L y = rhs:   y_j = D_j s_j,   s_i -= L_ij y_j      (i > j)
+//   backward L^T x = y:   x_j = D_j^T y_j, y_i -= L_ji^T x_j    (i < j)
+// D_j is the inverse of diagonal block j from the factorisation.  Each
+// workgroup recomputes the block solution (a 64 x 64 product) and updates its
+// target block; workgroup 0 also writes the solution (and adds it to `acc` on
+// the backward pass when given).  Forward step 0 reads the rhs, later steps the
+// work vector s; the backward pass updates y in place.
+template <bool FWD>
+__global__ void __launch_bounds__(256) k_trsv_step(const float *__restrict__ Gw, const float *__restrict__ dinv,
+                                                   int64_t ld, int j, const double *__restrict__ rhs,
+                                                   double *__restrict__ work, double *__restrict__ out,
+                                                   double *__restrict__ acc, const int32_t *__restrict__ info) {
+  __shared__ double sv[kNB], sol[kNB], red[4][kNB];
+  const int b = blockIdx.y, g = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   if (info[b] != 0) return;
+  const int nb = (int)(ld / kNB);
+  const int i = FWD ? j + 1 + g : g;                       // target block
+  const bool has_target = FWD ? i < nb : i < j;
   const float *L = Gw + (size_t)b * ld * ld;
-  const double *rb = rhs + (size_t)b * ld;
-  double *yb = y + (size_t)b * ld, *xb = x + (size_t)b * ld;
-  const int nrb = (int)(ld / kNB);
-  for (int kb = 0; kb < nrb; ++kb) {
-    const int r0 = kb * kNB;
-    double part[16];
+  const float *D = dinv + ((size_t)b * nb + j) * kNB * kNB;
+  const double *src = (FWD && j == 0) ? rhs + (size_t)b * ld : work + (size_t)b * ld;
+  if (tid < kNB) sv[tid] = src[(size_t)j * kNB + tid];
+  __syncthreads();
+  double part = 0.0;
 #pragma unroll
-    for (int q = 0; q < 16; ++q) part[q] = 0.0;
-    for (int c = lane; c < r0; c += 64) {
-      const double yc = yb[c];
+  for (int e = 0; e < 16; ++e) {
+    const int q = 16 * wave + e;
+    part += (double)(FWD ? D[lane * kNB + q] : D[q * kNB + lane]) * sv[q];
+  }
+  red[wave][lane] = part;
+  __syncthreads();
+  if (tid < kNB) sol[tid] = red[0][tid] + red[1][tid] + red[2][tid] + red[3][tid];
+  __syncthreads();
+  if (g == 0 && tid < kNB) {
+    out[(size_t)b * ld + (size_t)j * kNB + tid] = sol[tid];
+    if (!FWD && acc) acc[(size_t)b * ld + (size_t)j * kNB + tid] += sol[tid];
+  }
+  if (!has_target) return;
+  part = 0.0;
 #pragma unroll
-      for (int q = 0; q < 16; ++q) part[q] += (double)L[(size_t)(r0 + 16 * wave + q) * ld + c] * yc;
-    }
-#pragma unroll
-    for (int q = 0; q < 16; ++q) red[16 * wave + q][lane] = part[q];
-    for (int e = tid; e < kNB * kNB; e += 256) sD[(e / kNB) * kSD + e % kNB] = L[(size_t)(r0 + e / kNB) * ld + r0 + e % kNB];
-    __syncthreads();
-    if (wave == 0) {
-      double s = 0.0;
-      for (int c = 0; c < 64; ++c) s += red[lane][c];
-      double bv = rb[r0 + lane] - s, yv = 0.0;
-      for (int q = 0; q < kNB; ++q) {
-        const double v = bv / (double)sD[q * kSD + q];
-        const double yq = readlane_f64(v, q);
-        if (lane == q) yv = yq;
-        if (lane > q) bv -= (double)sD[lane * kSD + q] * yq;
-      }
-      yb[r0 + lane] = yv;
-    }
-    __threadfence_block();
-    __syncthreads();
+  for (int e = 0; e < 16; ++e) {
+    const int q = 16 * wave + e;
+    const float l = FWD ? L[((size_t)i * kNB + lane) * ld + (size_t)j * kNB + q]
+                        : L[((size_t)j * kNB + q) * ld + (size_t)i * kNB + lane];
+    part += (double)l * sol[q];
   }
-  for (int kb = nrb - 1; kb >= 0; --kb) {
-    const int c0 = kb * kNB;
-    const int c = tid & 63, g = tid >> 6;
-    double s = 0.0;
-    for (int64_t i = c0 + kNB + g; i < ld; i += 4) s += (double)L[(size_t)i * ld + c0 + c] * xb[i];
-    red[g][c] = s;
-    for (int e = tid; e < kNB * kNB; e += 256) sD[(e / kNB) * kSD + e % kNB] = L[(size_t)(c0 + e / kNB) * ld + c0 + e % kNB];
-    __syncthreads();
-    if (wave == 0) {
-      double bv = yb[c0 + lane] - (red[0][lane] + red[1][lane] + red[2][lane] + red[3][lane]), xv = 0.0;
-      for (int q = kNB - 1; q >= 0; --q) {
-        const double v = bv / (double)sD[q * kSD + q];
-        const double xq = readlane_f64(v, q);
-        if (lane == q) xv = xq;
-        if (lane < q) bv -= (double)sD[q * kSD + lane] * xq;
-      }
-      xb[c0 + lane] = xv;
-      if (acc) acc[(size_t)b * ld + c0 + lane] += xv;
-    }
-    __threadfence_block();
-    __syncthreads();
+  red[wave][lane] = part;     // red is free: every thread read it before the last barrier
+  __syncthreads();
+  if (tid < kNB) {
+    const size_t e = (size_t)b * ld + (size_t)i * kNB + tid;
+    const double base = (FWD && j == 0) ? rhs[e] : work[e];
+    work[e] = base - (red[0][tid] + red[1][tid] + red[2][tid] + red[3][tid]);
   }
-}
-
-// res = rhs - (Gc + lam I) x over the first t rows (padded rows: 0), float64.
-__global__ void __launch_bounds__(256) k_residual_vec(const float *__restrict__ Gc, int64_t ld, int t,
-                                                      const double *__restrict__ rhs, const double *__restrict__ x,
-                                                      const float *__restrict__ lam, double *__restrict__ res,
-                                                      const int32_t *__restrict__ info) {
-  const int b = blockIdx.y, lane = threadIdx.x & 63;
-  const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (r >= ld || info[b] != 0) return;
-  double s = 0.0;
-  if (r < t) {
-    const float *row = Gc + ((size_t)b * ld + r) * ld;
-    const double *xb = x + (size_t)b * ld;
-    for (int c = lane; c < t; c += 64) s += (double)row[c] * xb[c];
-    s = wave_sum(s);
-    s = rhs[(size_t)b * ld + r] - s - (double)lam[b] * xb[r];
-  }
-  if (lane == 0) res[(size_t)b * ld + r] = s;
 }
 
 // Refinement residual of the mass fit computed from the data, not from the
@@ -930,15 +892,21 @@ hipError_t launch_cholesky(float *Gw, const float *Gc, int B, int t, int64_t ld,
   return hipGetLastError();
 }
 
-hipError_t launch_trsv(const float *Gw, int B, int64_t ld, const double *rhs, double *y, double *x, double *acc,
-                       const int32_t *info, hipStream_t s) {
-  hipLaunchKernelGGL(k_trsv, dim3(B), dim3(256), 0, s, Gw, ld, rhs, y, x, acc, info);
-  return hipGetLastError();
-}
-
-hipError_t launch_residual_vec(const float *Gc, int B, int64_t ld, int t, const double *rhs, const double *x,
-                               const float *lam, double *res, const int32_t *info, hipStream_t s) {
-  hipLaunchKernelGGL(k_residual_vec, dim3((unsigned)(ld / 4), B), dim3(256), 0, s, Gc, ld, t, rhs, x, lam, res, info);
+// Forward L y = rhs then backward L^T x = y; sw and y are work vectors
+// [B][ld]; x receives the solution, acc (optional) accumulates it.
+hipError_t launch_trsv(const float *Gw, const float *dinv, int B, int64_t ld, const double *rhs, double *sw,
+                       double *y, double *x, double *acc, const int32_t *info, hipStream_t s) {
+  const int nb = (int)(ld / kNB);
+  for (int j = 0; j < nb; ++j) {
+    const int ng = nb - 1 - j > 0 ? nb - 1 - j : 1;
+    hipLaunchKernelGGL(k_trsv_step<true>, dim3(ng, B), dim3(256), 0, s, Gw, dinv, ld, j, rhs, sw, y,
+                       (double *)nullptr, info);
+  }
+  for (int j = nb - 1; j >= 0; --j) {
+    const int ng = j > 0 ? j : 1;
+    hipLaunchKernelGGL(k_trsv_step<false>, dim3(ng, B), dim3(256), 0, s, Gw, dinv, ld, j, (const double *)nullptr,
+                       y, x, acc, info);
+  }
   return hipGetLastError();
 }
 
