@@ -6,15 +6,15 @@
 // Flash-style single pass over the keys with an online maximum.  Each wave
 // owns 32 queries and computes D[key][query] = K Q^T, so every lane holds one
 // query column: its running max/sum live in registers.  The probabilities are
-// fed back as the B operand of Y^T[c][q] += V^T[c][key] P^T[key][q]; the MFMA
-// k-slots are permuted to match the accumulator layout, and V^T is staged in
-// LDS with the same key order.
+// fed back as the B operand of Y^T[c][q] += V^T[c][key] P^T[key][q].
+// fp32 inputs: the MFMA k-slots are permuted to match the accumulator layout,
+// and V^T is staged in LDS with the same key order (k_rowstats<float>).
+// bf16 inputs: see k_rowstats_bf16 below.
 #include "common.hpp"
 
 namespace arckv {
 
 template <typename T> struct RowstatsCfg;
-template <> struct RowstatsCfg<bf16> { static constexpr int NSUB = 2; };   // 64 keys per tile
 template <> struct RowstatsCfg<float> { static constexpr int NSUB = 1; };  // 32 keys per tile
 
 template <typename T>
@@ -147,15 +147,202 @@ __global__ void __launch_bounds__(256) k_rowstats(const T *__restrict__ K, const
   }
 }
 
+
+// ---------------------------------------------------------------- bf16 path
+// 256 queries per workgroup (8 waves x 32), 64-key tiles in two LDS stages.
+// K tiles arrive with the direct-to-LDS loads, rows of 256 bytes with their
+// 16-byte chunks XOR-swizzled by (row & 15), so the fragment reads of 16
+// consecutive rows hit distinct banks.  V tiles are transposed on the way in
+// (each thread loads a column pair of 8 keys and writes two 16-byte runs) into
+// V^T[c][key] rows of 128 bytes, chunk-swizzled by ((c >> 1) & 7).
+// P^T is the B operand of Y^T += V^T P^T with k-slot e of lane half h standing
+// for key 8h + e of the 16-key step; the accumulator layout of S leaves half of
+// those keys in the other half-wave, so four bf16 values are exchanged with a
+// cross-half shuffle per k-step.  Workgroups are remapped so the query tiles of
+// one pair share an XCD (and its L2 copy of that pair's keys and values).
+constexpr int kRsQ = 256, kRsK = 64;
+constexpr int kRsKBytes = kRsK * kHeadDim * 2;            // 16 KB
+constexpr int kRsStage = 2 * kRsKBytes;                   // K tile + V^T tile
+
+typedef __attribute__((address_space(3))) void rs_lds_t;
+
+__global__ void __launch_bounds__(512, 1) k_rowstats_bf16(const bf16 *__restrict__ K, const bf16 *__restrict__ V,
+                                                          const bf16 *__restrict__ Q, float *__restrict__ z,
+                                                          float *__restrict__ m, float *__restrict__ Y, int Tn, int n,
+                                                          float scale, int qtiles) {
+  __shared__ __attribute__((aligned(1024))) char sbuf[2 * kRsStage];
+  const int64_t tile = xcd_remap(blockIdx.x, gridDim.x);
+  const int b = (int)(tile / qtiles), qt = (int)(tile % qtiles);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int h = lane >> 5, col = lane & 31;
+  const int q = qt * kRsQ + wave * 32 + col;
+  const bool qvalid = q < n;
+  const bf16 *Kb = K + (size_t)b * Tn * kHeadDim;
+  const bf16 *Vb = V + (size_t)b * Tn * kHeadDim;
+
+  bf16x8 qf[kHeadDim / 16];
+  {
+    const bf16 *qrow = Q + ((size_t)b * n + (qvalid ? q : 0)) * kHeadDim;
+#pragma unroll
+    for (int ks = 0; ks < kHeadDim / 16; ++ks)
+      qf[ks] = qvalid ? *reinterpret_cast<const bf16x8 *>(qrow + ks * 16 + 8 * h) : Mfma<bf16>::zero();
+  }
+  // K: run gi (2 per wave) covers rows 4 gi .. 4 gi + 3; lane l fills physical
+  // chunk l % 16 of row 4 gi + l / 16 with logical chunk (l % 16) ^ row.
+  int koff[2], krow[2];
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    const int gi = wave * 2 + u, row = 4 * gi + lane / 16;
+    krow[u] = row;
+    koff[u] = 8 * ((lane % 16) ^ (row & 15));
+  }
+  auto issue_k = [&](int k0, int st) {
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int key = min(k0 + krow[u], Tn - 1);
+      __builtin_amdgcn_global_load_lds((const void *)(Kb + (size_t)key * kHeadDim + koff[u]),
+                                       (rs_lds_t *)(sbuf + st * kRsStage + (wave * 2 + u) * 1024), 16, 0, 0);
+    }
+  };
+  // V: thread -> column pair cp (c = 2 cp) and key group kg (keys 8 kg .. 8 kg + 7)
+  const int cp = tid & 63, kg = tid >> 6;
+  uint32_t vr[8];
+  auto load_v = [&](int k0) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int key = min(k0 + 8 * kg + e, Tn - 1);
+      vr[e] = *reinterpret_cast<const uint32_t *>(Vb + (size_t)key * kHeadDim + 2 * cp);
+    }
+  };
+  auto store_vt = [&](int st) {
+    char *vt = sbuf + st * kRsStage + kRsKBytes;
+    const int c = 2 * cp, ph = kg ^ ((c >> 1) & 7);
+    uint32_t lo[4], hi[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      lo[e] = (vr[2 * e] & 0xFFFFu) | (vr[2 * e + 1] << 16);
+      hi[e] = (vr[2 * e] >> 16) | (vr[2 * e + 1] & 0xFFFF0000u);
+    }
+    *reinterpret_cast<uint4 *>(vt + c * 128 + 16 * ph) = make_uint4(lo[0], lo[1], lo[2], lo[3]);
+    *reinterpret_cast<uint4 *>(vt + (c + 1) * 128 + 16 * ph) = make_uint4(hi[0], hi[1], hi[2], hi[3]);
+  };
+
+  const float c2 = scale * 1.4426950408889634f;   // exp(s x) = exp2(c2 x)
+  float run_max = -INFINITY, run_sum = 0.0f;
+  f32x16 accY[4];
+#pragma unroll
+  for (int cs = 0; cs < 4; ++cs) accY[cs] = zero16();
+
+  const int nt = (Tn + kRsK - 1) / kRsK;
+  issue_k(0, 0);
+  load_v(0);
+  store_vt(0);
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  for (int i = 0; i < nt; ++i) {
+    const int k0 = i * kRsK, st = i & 1;
+    const bool more = i + 1 < nt;
+    if (more) {
+      issue_k(k0 + kRsK, st ^ 1);
+      load_v(k0 + kRsK);
+    }
+    const char *sk = sbuf + st * kRsStage, *svt = sk + kRsKBytes;
+    f32x16 accS[2];
+#pragma unroll
+    for (int ms = 0; ms < 2; ++ms) {
+      accS[ms] = zero16();
+      const int row = 32 * ms + col;
+#pragma unroll
+      for (int ks = 0; ks < kHeadDim / 16; ++ks) {
+        const bf16x8 a = *reinterpret_cast<const bf16x8 *>(sk + row * 256 + 16 * ((2 * ks + h) ^ (row & 15)));
+        accS[ms] = Mfma<bf16>::mma(a, qf[ks], accS[ms]);
+      }
+    }
+    float bmax = -INFINITY;
+#pragma unroll
+    for (int ms = 0; ms < 2; ++ms)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        if (k0 + 32 * ms + acc_row(v, lane) >= Tn) accS[ms][v] = -INFINITY;
+        bmax = fmaxf(bmax, accS[ms][v]);
+      }
+    bmax = fmaxf(bmax, __shfl_xor(bmax, 32, 64));
+    const float new_max = fmaxf(run_max, bmax);
+    const float alpha = exp2f((run_max - new_max) * c2);
+    run_max = new_max;
+    float psum = 0.0f;
+#pragma unroll
+    for (int ms = 0; ms < 2; ++ms)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const float p = exp2f((accS[ms][v] - new_max) * c2);
+        accS[ms][v] = p;
+        psum += p;
+      }
+    run_sum = run_sum * alpha + psum;
+#pragma unroll
+    for (int cs = 0; cs < 4; ++cs)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) accY[cs][v] *= alpha;
+#pragma unroll
+    for (int kk = 0; kk < kRsK / 16; ++kk) {
+      const int ms = kk >> 1, base = 8 * (kk & 1);
+      uint32_t pk[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const bf16 x0 = (bf16)accS[ms][base + 2 * e], x1 = (bf16)accS[ms][base + 2 * e + 1];
+        pk[e] = (uint32_t)__builtin_bit_cast(uint16_t, x0) | ((uint32_t)__builtin_bit_cast(uint16_t, x1) << 16);
+      }
+      // pk[0..1]: own keys 4h + 0..3, pk[2..3]: own keys 8 + 4h + 0..3 (of this 16-key step)
+      const uint32_t s0 = h == 0 ? pk[2] : pk[0], s1 = h == 0 ? pk[3] : pk[1];
+      const uint32_t r0 = (uint32_t)__shfl_xor((int)s0, 32, 64), r1 = (uint32_t)__shfl_xor((int)s1, 32, 64);
+      uint32_t bw[4];
+      bw[0] = h == 0 ? pk[0] : r0;
+      bw[1] = h == 0 ? pk[1] : r1;
+      bw[2] = h == 0 ? r0 : pk[2];
+      bw[3] = h == 0 ? r1 : pk[3];
+      bf16x8 pf;
+      __builtin_memcpy(&pf, bw, 16);
+#pragma unroll
+      for (int cs = 0; cs < 4; ++cs) {
+        const int c = 32 * cs + col;
+        const bf16x8 vf = *reinterpret_cast<const bf16x8 *>(svt + c * 128 + 16 * ((2 * kk + h) ^ ((c >> 1) & 7)));
+        accY[cs] = Mfma<bf16>::mma(vf, pf, accY[cs]);
+      }
+    }
+    if (more) store_vt(st ^ 1);
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+  }
+  run_sum += __shfl_xor(run_sum, 32, 64);
+  if (!qvalid) return;
+  const float inv = 1.0f / run_sum;
+  float *yrow = Y + ((size_t)b * n + q) * kHeadDim;
+#pragma unroll
+  for (int cs = 0; cs < 4; ++cs)
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      f32x4 o = {accY[cs][4 * g] * inv, accY[cs][4 * g + 1] * inv, accY[cs][4 * g + 2] * inv,
+                 accY[cs][4 * g + 3] * inv};
+      *reinterpret_cast<f32x4 *>(yrow + 32 * cs + 8 * g + 4 * h) = o;
+    }
+  if (h == 0) {
+    z[(size_t)b * n + q] = run_max * scale;
+    m[(size_t)b * n + q] = run_sum;
+  }
+}
+
 hipError_t launch_rowstats(int dtype, const void *K, const void *V, const void *Q, float *z, float *m, float *Y,
                            int B, int T, int n, float scale, hipStream_t s) {
+  if (dtype == ARCKV_BF16) {
+    const int qtiles = (n + kRsQ - 1) / kRsQ;
+    hipLaunchKernelGGL(k_rowstats_bf16, dim3((unsigned)(qtiles * B)), dim3(512), 0, s, (const bf16 *)K,
+                       (const bf16 *)V, (const bf16 *)Q, z, m, Y, T, n, scale, qtiles);
+    return hipGetLastError();
+  }
   dim3 grid((n + 127) / 128, B);
-  if (dtype == ARCKV_BF16)
-    hipLaunchKernelGGL(k_rowstats<bf16>, grid, dim3(256), 0, s, (const bf16 *)K, (const bf16 *)V, (const bf16 *)Q,
-                       z, m, Y, T, n, scale);
-  else
-    hipLaunchKernelGGL(k_rowstats<float>, grid, dim3(256), 0, s, (const float *)K, (const float *)V,
-                       (const float *)Q, z, m, Y, T, n, scale);
+  hipLaunchKernelGGL(k_rowstats<float>, grid, dim3(256), 0, s, (const float *)K, (const float *)V, (const float *)Q, z,
+                     m, Y, T, n, scale);
   return hipGetLastError();
 }
 
