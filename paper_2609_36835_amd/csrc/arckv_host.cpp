@@ -28,21 +28,22 @@ hipError_t launch_select(const float *scores, int B, int T, int t, int32_t *anch
                          hipStream_t s);
 hipError_t launch_rowstats(int dtype, const void *K, const void *V, const void *Q, float *z, float *m, float *Y,
                            int B, int T, int n, float scale, hipStream_t s);
-hipError_t launch_profiles(int dtype, const void *Q, const void *K, const float *zmerge, void *Et, float *phi,
-                           int B, int T, int n, int64_t Tp, int64_t np_, float scale, hipStream_t s);
+hipError_t launch_profiles(int dtype, const void *Q, const void *K, const float *zmerge, const int32_t *anchors,
+                           int t, void *Et, void *U, float *ssq, float *phi, int B, int T, int n, int64_t Tp,
+                           int64_t tp, int64_t np_, float scale, hipStream_t s);
 hipError_t launch_phic(int dtype, const void *Q, const void *Ckp, const float *z, void *PhiT, float *LT, int B, int t,
                        int n, int64_t tp, int64_t np_, float scale, hipStream_t s);
 hipError_t launch_zmax(const float *z, int B, int n, float *zmax, hipStream_t s);
 hipError_t launch_anchor_of(const int32_t *anchors, int B, int T, int t, int32_t *anchor_of, hipStream_t s);
-hipError_t launch_anchor_profiles(int dtype, const void *Et, const int32_t *anchors, void *U, int B, int t,
-                                  int64_t Tp, int64_t np_, int64_t tp, hipStream_t s);
-hipError_t launch_assign_finalize(const uint64_t *part, int MT, int64_t Np, const int32_t *anchor_of, int B, int T,
-                                  int32_t *kappa, hipStream_t s);
+hipError_t launch_anchor_profiles(int dtype, void *U, const float *ssq, int B, int t, int64_t np_, int64_t tp,
+                                  hipStream_t s);
+hipError_t launch_assign_finalize(const uint64_t *part, int MT, int64_t Np, const int32_t *anchor_of,
+                                  const int32_t *anchors, int B, int T, int t, int32_t *kappa, hipStream_t s);
 hipError_t launch_group_merge(int dtype, const void *K, const float *phi, const int32_t *kappa,
                               const int32_t *anchors, int B, int T, int t, int64_t tp, float lambda,
                               int32_t *offsets, int32_t *cursor, int32_t *perm, float *Ck, void *Ckp, hipStream_t s);
 hipError_t launch_assign_gemm(int dtype, const void *U, const void *Et, uint64_t *part, int P, int t, int64_t tp,
-                              int64_t Tp, int64_t np_, hipStream_t s);
+                              int64_t N, int64_t Et_rows, int64_t np_, hipStream_t s);
 hipError_t launch_gram(int dtype, const void *X, float *G, float *Gc, int P, int64_t tp, int64_t np_, hipStream_t s);
 hipError_t launch_rhs_gemm(int dtype, const void *PT, const void *YT, float *Bm, int P, int64_t tp, int64_t np_,
                            hipStream_t s);
@@ -168,7 +169,7 @@ struct Plan {
   int64_t persistent_bytes;
   // chunk region (offsets relative to chunk base)
   int64_t Ckp;
-  int64_t Et, U, part, offsets, cursor, perm;            // merge phase
+  int64_t Et, U, ssq, part, offsets, cursor, perm;       // merge phase
   int64_t PhiT, LT, Gw, Gc, dinv, h, w, y, x, res, sw, u, YT, Bm, X, R, Y2, XT, Pm, UT;  // fit phase
   int64_t chunk_bytes;
 };
@@ -198,6 +199,7 @@ static Plan make_plan(const Dims &d, int64_t P) {
   Bump m = c;
   pl.Et = m.take(P * d.Tp * d.np_ * d.esz);
   pl.U = m.take(P * d.tp * d.np_ * d.esz);
+  pl.ssq = m.take(P * d.tp * 4);
   pl.part = m.take(P * d.MT * d.Tp * 8);
   pl.offsets = m.take(P * (int64_t)(d.t + 1) * 4);
   pl.cursor = m.take(P * (int64_t)d.t * 4);
@@ -313,12 +315,15 @@ static arckv_status run_merge_chunk(const Ctx &c, int b0, int P, const void *K, 
   void *Et = c.chunk<char>(c.pl.Et);
   void *U = c.chunk<char>(c.pl.U);
   uint64_t *part = c.chunk<uint64_t>(c.pl.part);
-  STAGE(ST_PROFILES, launch_profiles(d.dtype, Qc, Kc, zmax + b0, Et, phi + (size_t)b0 * d.T, P, d.T, d.n, d.Tp,
-                                     d.np_, c.scale, stream));
-  STAGE(ST_ANCHOR_PROF, launch_anchor_profiles(d.dtype, Et, anc, U, P, d.t, d.Tp, d.np_, d.tp, stream));
-  STAGE(ST_ASSIGN, launch_assign_gemm(d.dtype, U, Et, part, P, d.t, d.tp, d.Tp, d.np_, stream));
+  float *ssq = c.chunk<float>(c.pl.ssq);
+  // the assignment runs over the T - t non-anchor keys (compacted E^T rows)
+  const int64_t Tc = rup(d.T - d.t, kPadH);
+  STAGE(ST_PROFILES, launch_profiles(d.dtype, Qc, Kc, zmax + b0, anc, d.t, Et, U, ssq, phi + (size_t)b0 * d.T, P,
+                                     d.T, d.n, d.Tp, d.tp, d.np_, c.scale, stream));
+  STAGE(ST_ANCHOR_PROF, launch_anchor_profiles(d.dtype, U, ssq, P, d.t, d.np_, d.tp, stream));
+  STAGE(ST_ASSIGN, launch_assign_gemm(d.dtype, U, Et, part, P, d.t, d.tp, Tc, d.Tp, d.np_, stream));
   const int mt_used = (int)(d.dtype == ARCKV_BF16 ? d.tp / 256 : d.tp / 128);
-  STAGE(ST_FINALIZE, launch_assign_finalize(part, mt_used, d.Tp, anchor_of + (size_t)b0 * d.T, P, d.T,
+  STAGE(ST_FINALIZE, launch_assign_finalize(part, mt_used, Tc, anchor_of + (size_t)b0 * d.T, anc, P, d.T, d.t,
                                             kappa + (size_t)b0 * d.T, stream));
   STAGE(ST_MERGE, launch_group_merge(d.dtype, Kc, phi + (size_t)b0 * d.T, kappa + (size_t)b0 * d.T, anc, P, d.T,
                                      d.t, d.tp, lambda_m, c.chunk<int32_t>(c.pl.offsets),

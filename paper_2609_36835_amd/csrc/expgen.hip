@@ -4,6 +4,10 @@
 // MODE_PROFILE (Section 3.4, eq. response_profile / mass_centroid):
 //   E^T[j][i] = exp(s q_i.k_j - z_merge) for every cached key j,
 //   phi_j = (1/n) sum_i E[i][j].
+//   Rows are routed by key: an anchor s_r writes its (unnormalised) profile to
+//   row r of U and the sum of squares of the stored values to ssq[r]; every
+//   other key j writes to row j - #{anchors < j} of the compacted E^T, so the
+//   assignment contraction runs over the T - t non-anchor keys only.
 // MODE_PHIC (Appendix A.9):
 //   L^T[r][i]   = s q_i.c_r            (logits of the compact keys, fp32)
 //   Phi^T[r][i] = exp(L - z_i)         (z_i: full-cache row maxima)
@@ -23,7 +27,8 @@ __global__ void __launch_bounds__(256) k_expgen(const T *__restrict__ Q, const v
                                                 const float *__restrict__ shift, void *__restrict__ out,
                                                 int64_t out_pair_stride, int64_t out_plane_stride,
                                                 float *__restrict__ aux, int64_t aux_pair_stride, int n,
-                                                int n_pad, float scale) {
+                                                int n_pad, float scale, const int32_t *__restrict__ anchors, int t,
+                                                void *__restrict__ uout, float *__restrict__ ssq, int64_t tp) {
   using M = Mfma<T>;
   constexpr int KPL = M::KPL, KSTEP = M::KSTEP, NKS = kHeadDim / KSTEP;
   constexpr bool SPLIT_B = (MODE == MODE_PHIC) && sizeof(T) == 2;   // compact keys kept as bf16 hi + lo
@@ -47,14 +52,36 @@ __global__ void __launch_bounds__(256) k_expgen(const T *__restrict__ Q, const v
   const T *Qb = Q + (size_t)b * n * kHeadDim;
   const float c2 = scale * 1.4426950408889634f;
   const float zshift = (MODE == MODE_PROFILE) ? shift[b] : 0.0f;
-  float rowsum = 0.0f;
+  float rowsum = 0.0f, sumsq = 0.0f;
+  // PROFILE destination of this lane's key: >= 0 compacted E^T row, <= -2
+  // anchor -(r + 2), -1 none (padding key)
+  int dest = -1;
+  if (MODE == MODE_PROFILE && rvalid) {
+    const int32_t *S = anchors + (size_t)b * t;
+    int lo = 0, hi = t;
+    while (lo < hi) {
+      const int mid = (lo + hi) >> 1;
+      if (S[mid] < row) lo = mid + 1;
+      else hi = mid;
+    }
+    dest = (lo < t && S[lo] == row) ? -(lo + 2) : row - lo;
+  }
+  // base pointer of staged row rr of this wave (MODE_PROFILE), or null
+  auto row_dst = [&](int rr, int i0) -> T * {
+    const int d = __shfl(dest, rr, 64);
+    if (d == -1) return nullptr;
+    T *base = d >= 0 ? reinterpret_cast<T *>(out) + (size_t)b * out_pair_stride + (size_t)d * n_pad
+                     : reinterpret_cast<T *>(uout) + ((size_t)b * tp + (size_t)(-d - 2)) * n_pad;
+    return base + i0;
+  };
 
   // Output tiles (this wave's 32 rows x 64 queries) are staged in LDS so that
   // global stores are whole 128/256-byte row segments.
   constexpr int SO = 64 + 4;                               // staging row (4-byte words)
   __shared__ float sOut[4][32 * SO];
   float *so = sOut[wave];
-  auto flush_f32 = [&](const float (&v)[2][16], float *dst_base) {   // dst_base: row 0 of this wave, col i0
+  // dst_base: row 0 of this wave at column i0; routed: rows go to row_dst()
+  auto flush_f32 = [&](const float (&v)[2][16], float *dst_base, bool routed, int i0) {
 #pragma unroll
     for (int ms = 0; ms < 2; ++ms)
 #pragma unroll
@@ -64,11 +91,12 @@ __global__ void __launch_bounds__(256) k_expgen(const T *__restrict__ Q, const v
     for (int pass = 0; pass < 8; ++pass) {             // 32 rows x 16 chunks of 16 B
       const int chunk = pass * 64 + lane, r = chunk / 16, c4 = (chunk % 16) * 4;
       const f32x4 w = {so[r * SO + c4], so[r * SO + c4 + 1], so[r * SO + c4 + 2], so[r * SO + c4 + 3]};
-      *reinterpret_cast<f32x4 *>(dst_base + (size_t)r * n_pad + c4) = w;
+      float *dst = routed ? reinterpret_cast<float *>(row_dst(r, i0)) : dst_base + (size_t)r * n_pad;
+      if (dst) *reinterpret_cast<f32x4 *>(dst + c4) = w;
     }
     __syncthreads();
   };
-  auto flush_bf16 = [&](const float (&v)[2][16], int part, bf16 *dst_base) {   // part: 0 value, 1 hi, 2 lo
+  auto flush_bf16 = [&](const float (&v)[2][16], int part, bf16 *dst_base, bool routed, int i0) {   // part: 0 value, 1 hi, 2 lo
     bf16 *sb = reinterpret_cast<bf16 *>(so);
 #pragma unroll
     for (int ms = 0; ms < 2; ++ms)
@@ -82,8 +110,8 @@ __global__ void __launch_bounds__(256) k_expgen(const T *__restrict__ Q, const v
 #pragma unroll
     for (int pass = 0; pass < 4; ++pass) {             // 32 rows x 8 chunks of 16 B
       const int chunk = pass * 64 + lane, r = chunk / 8, c8 = (chunk % 8) * 8;
-      *reinterpret_cast<bf16x8 *>(dst_base + (size_t)r * n_pad + c8) =
-          *reinterpret_cast<const bf16x8 *>(&sb[r * (2 * SO) + c8]);
+      bf16 *dst = routed ? reinterpret_cast<bf16 *>(row_dst(r, i0)) : dst_base + (size_t)r * n_pad;
+      if (dst) *reinterpret_cast<bf16x8 *>(dst + c8) = *reinterpret_cast<const bf16x8 *>(&sb[r * (2 * SO) + c8]);
     }
     __syncthreads();
   };
@@ -115,6 +143,8 @@ __global__ void __launch_bounds__(256) k_expgen(const T *__restrict__ Q, const v
         if (MODE == MODE_PROFILE) {
           val[ms][vv] = ok ? exp2f(acc[vv] * c2 - zshift * 1.4426950408889634f) : 0.0f;
           rowsum += val[ms][vv];
+          const float stored = sizeof(T) == 2 ? (float)(bf16)val[ms][vv] : val[ms][vv];
+          sumsq = fmaf(stored, stored, sumsq);
           lg[ms][vv] = 0.0f;
         } else {
           lg[ms][vv] = ok ? acc[vv] * scale : 0.0f;
@@ -124,35 +154,42 @@ __global__ void __launch_bounds__(256) k_expgen(const T *__restrict__ Q, const v
     }
     __syncthreads();   // sQ is refilled at the next i0; sOut is free
     char *ob = reinterpret_cast<char *>(out);
+    constexpr bool routed = MODE == MODE_PROFILE;
     if constexpr (sizeof(T) == 4) {
-      flush_f32(val, reinterpret_cast<float *>(ob) + (size_t)b * out_pair_stride + (size_t)row0 * n_pad + i0);
+      flush_f32(val, reinterpret_cast<float *>(ob) + (size_t)b * out_pair_stride + (size_t)row0 * n_pad + i0, routed,
+                i0);
     } else if constexpr (MODE == MODE_PROFILE) {
-      flush_bf16(val, 0, reinterpret_cast<bf16 *>(ob) + (size_t)b * out_pair_stride + (size_t)row0 * n_pad + i0);
+      flush_bf16(val, 0, nullptr, true, i0);
     } else {
       bf16 *o = reinterpret_cast<bf16 *>(ob) + (size_t)b * out_pair_stride + (size_t)row0 * n_pad + i0;
-      flush_bf16(val, 1, o);
-      flush_bf16(val, 2, o + out_plane_stride);
+      flush_bf16(val, 1, o, false, i0);
+      flush_bf16(val, 2, o + out_plane_stride, false, i0);
     }
-    if (MODE == MODE_PHIC) flush_f32(lg, aux + (size_t)b * aux_pair_stride + (size_t)row0 * n_pad + i0);
+    if (MODE == MODE_PHIC) flush_f32(lg, aux + (size_t)b * aux_pair_stride + (size_t)row0 * n_pad + i0, false, i0);
   }
   if (MODE == MODE_PROFILE) {
     rowsum += __shfl_xor(rowsum, 32, 64);
+    sumsq += __shfl_xor(sumsq, 32, 64);
     if (h == 0 && rvalid) aux[(size_t)b * aux_pair_stride + row] = rowsum / (float)n;
+    if (h == 0 && dest <= -2) ssq[(size_t)b * tp + (-dest - 2)] = sumsq;
   }
 }
 
-// E^T [B][Tp][np] (T = bf16 or float) and phi [B][T].
-hipError_t launch_profiles(int dtype, const void *Q, const void *K, const float *zmerge, void *Et, float *phi,
-                           int B, int T, int n, int64_t Tp, int64_t np_, float scale, hipStream_t s) {
+// Compacted E^T [B][Tp][np] (rows of the non-anchor keys; T = bf16 or
+// float), unnormalised anchor profiles U [B][tp][np] with their sums of
+// squares ssq [B][tp], and phi [B][T].
+hipError_t launch_profiles(int dtype, const void *Q, const void *K, const float *zmerge, const int32_t *anchors,
+                           int t, void *Et, void *U, float *ssq, float *phi, int B, int T, int n, int64_t Tp,
+                           int64_t tp, int64_t np_, float scale, hipStream_t s) {
   dim3 grid(Tp / 128, B);
   if (dtype == ARCKV_BF16)
     hipLaunchKernelGGL((k_expgen<bf16, MODE_PROFILE>), grid, dim3(256), 0, s, (const bf16 *)Q, K,
                        (int64_t)T * kHeadDim, (int64_t)0, T, zmerge, Et, Tp * np_, (int64_t)0, phi, (int64_t)T, n,
-                       (int)np_, scale);
+                       (int)np_, scale, anchors, t, U, ssq, tp);
   else
     hipLaunchKernelGGL((k_expgen<float, MODE_PROFILE>), grid, dim3(256), 0, s, (const float *)Q, K,
                        (int64_t)T * kHeadDim, (int64_t)0, T, zmerge, Et, Tp * np_, (int64_t)0, phi, (int64_t)T,
-                       n, (int)np_, scale);
+                       n, (int)np_, scale, anchors, t, U, ssq, tp);
   return hipGetLastError();
 }
 
@@ -163,11 +200,11 @@ hipError_t launch_phic(int dtype, const void *Q, const void *Ckp, const float *z
   if (dtype == ARCKV_BF16)
     hipLaunchKernelGGL((k_expgen<bf16, MODE_PHIC>), grid, dim3(256), 0, s, (const bf16 *)Q, Ckp,
                        2 * tp * kHeadDim, tp * kHeadDim, t, z, PhiT, 2 * tp * np_, tp * np_, LT, tp * np_, n,
-                       (int)np_, scale);
+                       (int)np_, scale, (const int32_t *)nullptr, 0, (void *)nullptr, (float *)nullptr, tp);
   else
     hipLaunchKernelGGL((k_expgen<float, MODE_PHIC>), grid, dim3(256), 0, s, (const float *)Q, Ckp,
                        tp * kHeadDim, (int64_t)0, t, z, PhiT, tp * np_, (int64_t)0, LT, tp * np_, n, (int)np_,
-                       scale);
+                       scale, (const int32_t *)nullptr, 0, (void *)nullptr, (float *)nullptr, tp);
   return hipGetLastError();
 }
 

@@ -5,30 +5,32 @@
 namespace arckv {
 
 // Anchor assignment (eq. anchor_assignment): S[r][j] = sum_i U_S[r][i] E^T[j][i];
-// per-(M-tile, key) packed argmax partials.  U [P][tp][np], Et [P][Tp][np].
+// per-(M-tile, key) packed argmax partials [P][MT][N].  U [P][tp][np], Et
+// [P][Et_rows][np] with the first N rows used (the compacted non-anchor keys).
 // M-tiles are 256 rows for bf16 (large-tile kernel, 8 waves of 64 x 128) and
 // 128 for fp32.
 hipError_t launch_assign_gemm(int dtype, const void *U, const void *Et, uint64_t *part, int P, int t, int64_t tp,
-                              int64_t Tp, int64_t np_, hipStream_t s) {
+                              int64_t N, int64_t Et_rows, int64_t np_, hipStream_t s) {
+  if (N == 0) return hipSuccess;
   GemmShape g;
   g.batch = P;
   g.M = (int)tp;
-  g.N = (int)Tp;
+  g.N = (int)N;
   g.K = (int)np_;
   g.a_pair = tp * np_;
   g.a_plane = 0;
   g.lda = np_;
-  g.b_pair = Tp * np_;
+  g.b_pair = Et_rows * np_;
   g.b_plane = 0;
   g.ldb = np_;
   g.syrk = false;
   g.group_m = 8;
   if (dtype == ARCKV_BF16) {
-    BigShape g2{P, (int)tp, (int)Tp, (int)np_, tp * np_, 0, np_, Tp * np_, 0, np_, false, 4};
-    EpiArgmaxBig<4, 2, 2, 4> e2{part, (tp / 256) * Tp, (int)Tp, t};
+    BigShape g2{P, (int)tp, (int)N, (int)np_, tp * np_, 0, np_, Et_rows * np_, 0, np_, false, 4};
+    EpiArgmaxBig<4, 2, 2, 4> e2{part, (tp / 256) * N, (int)N, t};
     return launch_gemm_big<4, 2, 2, 4, 64, 1, 1>(g2, (const bf16 *)U, (const bf16 *)Et, e2, s);
   }
-  EpiArgmax e{part, (tp / kGBM) * Tp, (int)Tp, t};
+  EpiArgmax e{part, (tp / kGBM) * N, (int)N, t};
   return launch_gemm<float, 1, 1>(g, (const float *)U, (const float *)Et, e, s);
 }
 

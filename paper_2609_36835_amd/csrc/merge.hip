@@ -3,7 +3,8 @@
 //  k_zmax            z_merge = max_i z_i (the global logit maximum equals the
 //                    largest full-cache row maximum, eq. response_profile)
 //  k_anchor_of       position -> anchor slot (or -1)
-//  k_anchor_profiles U_S rows: E^T[s_r] / ||E^T[s_r]|| (anchor response profiles)
+//  k_anchor_profiles U_S rows: E^T[s_r] / ||E^T[s_r]|| (anchor response profiles),
+//                    normalising the rows the profile pass wrote
 //  k_assign_finalize kappa_j from the per-tile packed argmax; anchors map to
 //                    themselves (eq. anchor_assignment)
 //  k_group_sort      stable counting sort of positions by group (deterministic)
@@ -39,11 +40,12 @@ __global__ void __launch_bounds__(256) k_anchor_scatter(const int32_t *__restric
   if (r < t) anchor_of[(size_t)b * T + anchors[(size_t)b * t + r]] = r;
 }
 
-// One wave per anchor row: U_S[r][i] = E^T[s_r][i] / ||E^T[s_r][:]||; rows r >= t are zero.
+// One wave per anchor row: U_S[r][i] = E^T[s_r][i] / ||E^T[s_r][:]||, in place
+// on the unnormalised rows the profile pass wrote (ssq[r] = sum of squares of
+// the stored values); rows r >= t are zero.
 template <typename T>
-__global__ void __launch_bounds__(256) k_anchor_profiles(const T *__restrict__ Et, const int32_t *__restrict__ anchors,
-                                                         T *__restrict__ U, int t, int64_t Tp, int64_t np_,
-                                                         int64_t tp) {
+__global__ void __launch_bounds__(256) k_anchor_profiles(T *__restrict__ U, const float *__restrict__ ssq, int t,
+                                                         int64_t np_, int64_t tp) {
   const int b = blockIdx.y, lane = threadIdx.x & 63;
   const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (r >= tp) return;
@@ -52,27 +54,32 @@ __global__ void __launch_bounds__(256) k_anchor_profiles(const T *__restrict__ E
     for (int64_t i = lane; i < np_; i += 64) urow[i] = (T)0.0f;
     return;
   }
-  const T *erow = Et + ((size_t)b * Tp + anchors[(size_t)b * t + r]) * np_;
-  float ss = 0.0f;
-  for (int64_t i = lane; i < np_; i += 64) {
-    float e = to_f(erow[i]);
-    ss = fmaf(e, e, ss);
-  }
-  ss = wave_sum(ss);
+  const float ss = ssq[(size_t)b * tp + r];
   const float inv = ss > 0.0f ? 1.0f / sqrtf(ss) : 0.0f;
-  for (int64_t i = lane; i < np_; i += 64) urow[i] = (T)(to_f(erow[i]) * inv);
+  for (int64_t i = lane; i < np_; i += 64) urow[i] = (T)(to_f(urow[i]) * inv);
 }
 
+// kappa_j: anchors map to themselves; any other key takes the best packed
+// (similarity, lowest r) over the M-tiles at its compacted column
+// j - #{anchors < j}.
 __global__ void __launch_bounds__(256) k_assign_finalize(const uint64_t *__restrict__ part, int MT, int64_t Np,
-                                                         const int32_t *__restrict__ anchor_of, int T,
+                                                         const int32_t *__restrict__ anchor_of,
+                                                         const int32_t *__restrict__ anchors, int T, int t,
                                                          int32_t *__restrict__ kappa) {
   const int b = blockIdx.y;
   const int j = blockIdx.x * 256 + threadIdx.x;
   if (j >= T) return;
   int32_t a = anchor_of[(size_t)b * T + j];
   if (a < 0) {
+    const int32_t *S = anchors + (size_t)b * t;
+    int lo = 0, hi = t;
+    while (lo < hi) {
+      const int mid = (lo + hi) >> 1;
+      if (S[mid] < j) lo = mid + 1;
+      else hi = mid;
+    }
     uint64_t best = 0;
-    const uint64_t *pp = part + (size_t)b * MT * Np + j;
+    const uint64_t *pp = part + (size_t)b * MT * Np + (j - lo);
     for (int mt = 0; mt < MT; ++mt) {
       uint64_t v = pp[(size_t)mt * Np];
       best = v > best ? v : best;
@@ -198,22 +205,20 @@ hipError_t launch_anchor_of(const int32_t *anchors, int B, int T, int t, int32_t
   return hipGetLastError();
 }
 
-hipError_t launch_anchor_profiles(int dtype, const void *Et, const int32_t *anchors, void *U, int B, int t,
-                                  int64_t Tp, int64_t np_, int64_t tp, hipStream_t s) {
+hipError_t launch_anchor_profiles(int dtype, void *U, const float *ssq, int B, int t, int64_t np_, int64_t tp,
+                                  hipStream_t s) {
   dim3 grid((unsigned)(tp / 4), B);
   if (dtype == ARCKV_BF16)
-    hipLaunchKernelGGL(k_anchor_profiles<bf16>, grid, dim3(256), 0, s, (const bf16 *)Et, anchors, (bf16 *)U, t, Tp,
-                       np_, tp);
+    hipLaunchKernelGGL(k_anchor_profiles<bf16>, grid, dim3(256), 0, s, (bf16 *)U, ssq, t, np_, tp);
   else
-    hipLaunchKernelGGL(k_anchor_profiles<float>, grid, dim3(256), 0, s, (const float *)Et, anchors, (float *)U, t,
-                       Tp, np_, tp);
+    hipLaunchKernelGGL(k_anchor_profiles<float>, grid, dim3(256), 0, s, (float *)U, ssq, t, np_, tp);
   return hipGetLastError();
 }
 
-hipError_t launch_assign_finalize(const uint64_t *part, int MT, int64_t Np, const int32_t *anchor_of, int B, int T,
-                                  int32_t *kappa, hipStream_t s) {
-  hipLaunchKernelGGL(k_assign_finalize, dim3((T + 255) / 256, B), dim3(256), 0, s, part, MT, Np, anchor_of, T,
-                     kappa);
+hipError_t launch_assign_finalize(const uint64_t *part, int MT, int64_t Np, const int32_t *anchor_of,
+                                  const int32_t *anchors, int B, int T, int t, int32_t *kappa, hipStream_t s) {
+  hipLaunchKernelGGL(k_assign_finalize, dim3((T + 255) / 256, B), dim3(256), 0, s, part, MT, Np, anchor_of, anchors,
+                     T, t, kappa);
   return hipGetLastError();
 }
 

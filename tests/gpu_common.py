@@ -57,3 +57,28 @@ def assignment_gap(Q, K, S, scale, j, pdt):
     sim = ej @ US
     top = np.sort(sim)[::-1]
     return 0.0 if len(top) < 2 else (top[0] - top[1]) / max(abs(top[0]), 1e-300)
+
+
+def gpu_assignment(K, V, Q, anchors, scale):
+    """kappa as arckv_compact computes it for one pair: the GPU row maxima z
+    (arckv_rowstats) feed arckv_merge on the GPU's anchors.  K, V, Q: [1][...]
+    device tensors, anchors [1][t] int32."""
+    from paper_2609_36835_amd import arckv
+    import oracle
+    z, _, _ = arckv.rowstats(K, V, Q, scale=scale)
+    _, kappa, _ = arckv.merge(K, Q, z, anchors, lambda_m=oracle.LAMBDA_M, scale=scale)
+    return kappa[0].cpu().numpy().astype(np.int64)
+
+
+def certify_flips(kappa_gpu, kappa_ref, Q, K, anchors, scale, pdt, log=print):
+    """Assignment differences must be near-ties within one storage-precision
+    rounding term (2^-7 relative for bf16 profiles, 2^-23 + n 2^-24 for fp32)
+    and rare (at most max(1, T/1000))."""
+    rel_tie = 2.0 ** -7 if pdt == "bf16" else 2.0 ** -23 + Q.shape[0] * 2.0 ** -24
+    flips = np.flatnonzero(kappa_gpu != kappa_ref)
+    for j in flips:
+        gap = assignment_gap(Q, K, anchors, scale, j, pdt)
+        log(f"    key {j}: gpu anchor {kappa_gpu[j]}, oracle anchor {kappa_ref[j]}, relative gap {gap:.2e}")
+        assert gap <= rel_tie, (j, gap)
+    assert len(flips) <= max(1, len(K) // 1000), len(flips)
+    return len(flips)

@@ -15,7 +15,8 @@ import torch
 
 import oracle
 import synth
-from tests.gpu_common import TOL_OUT, assignment_gap, make_inputs, np64, profile_dtype, scale_of
+from tests.gpu_common import (TOL_OUT, assignment_gap, certify_flips, gpu_assignment, make_inputs, np64,
+                               profile_dtype, scale_of)
 
 pytestmark = pytest.mark.gpu
 
@@ -196,18 +197,28 @@ def test_compact_end_to_end(case):
     wl, dev, host, s, t, ref = case
     anchors, Ck, beta, Cv, info = A().compact(dev["K"], dev["V"], dev["Q"], dev["W1"], dev["b1"], dev["w2"],
                                               dev["b2"], wl.rho, scale=s)
+    anchors_d = anchors
     anchors, Ck, beta, Cv, info = anchors.cpu().numpy(), np64(Ck), np64(beta), np64(Cv), info.cpu().numpy()
     assert np.all(info == 0), info
     for b in range(wl.pairs):
         r = ref[b]
-        Q = host["Q"][b]
-        if anchors[b].tolist() != r.anchors.tolist():
-            pytest.skip("anchor sets differ at a certified near-tie; end-to-end outputs are not comparable")
+        Q, K = host["Q"][b], host["K"][b]
+        S = anchors[b].astype(np.int64)
+        if S.tolist() != r.anchors.tolist():       # boundary near-tie (certified in the select tests)
+            log(f"  pair {b}: anchor sets differ at a near-tie; oracle refits on the GPU's anchors")
+        # the oracle refits on the GPU's anchors and assignment once every
+        # difference is certified as a near-tie of the stored profiles
+        kap_gpu = gpu_assignment(dev["K"][b:b + 1].contiguous(), dev["V"][b:b + 1].contiguous(),
+                                 dev["Q"][b:b + 1].contiguous(), anchors_d[b:b + 1].contiguous(), s)
+        kap_ref, _, _ = oracle.profiles_assign_phi(Q, K, S, s, profile_dtype(wl))
+        certify_flips(kap_gpu, kap_ref, Q, K, S, s, profile_dtype(wl), log=log)
+        rr = oracle.compact_pair(K, host["V"][b], Q, host["W1"][b], host["b1"][b], host["w2"][b], host["b2"][b],
+                                 t=t, scale=s, anchors=S, kappa=kap_gpu, profile_dtype=profile_dtype(wl))
         O_gpu = oracle.attend_compact(Q, Ck[b], beta[b], Cv[b], s)
-        O_ref = oracle.attend_compact(Q, r.C_k, r.beta, r.C_v, s)
+        O_ref = oracle.attend_compact(Q, rr.C_k, rr.beta, rr.C_v, s)
         err = oracle.row_rel_err(O_gpu, O_ref)
         Qh = synth.heldout_queries(wl, *synth.pair_index(wl, b)).astype(np.float64)
-        Oh = oracle.attend_full(Qh, host["K"][b], host["V"][b], s)
+        Oh = oracle.attend_full(Qh, K, host["V"][b], s)
         held_gpu = oracle.row_rel_err(oracle.attend_compact(Qh, Ck[b], beta[b], Cv[b], s), Oh).mean()
         held_ref = oracle.row_rel_err(oracle.attend_compact(Qh, r.C_k, r.beta, r.C_v, s), Oh).mean()
         log(f"  pair {b}: O(Q_ref) max row rel err {err.max():.3e} (mean {err.mean():.2e}); held-out rel "
