@@ -175,6 +175,183 @@ __global__ void __launch_bounds__(256) k_expgen(const T *__restrict__ Q, const v
   }
 }
 
+// ---------------------------------------------------------------- bf16 path
+// Same products as k_expgen, for bf16 inputs, with the query tiles double-
+// buffered: tile i+1 (64 queries x 256 B) goes global -> LDS with the
+// direct-to-LDS loads while tile i's products are formed (rows stored unpadded,
+// 16-byte chunks XOR-swizzled by (row & 15) so the fragment reads of 16
+// consecutive rows hit distinct banks).  One barrier per query tile hands the
+// next Q stage over, after the products and before the stores.  Each wave
+// stages its 32 x 64 output block in a private LDS area, so no workgroup
+// barrier guards the staging.
+typedef __attribute__((address_space(3))) void eg_lds_t;
+
+template <int MODE>
+__global__ void __launch_bounds__(256) k_expgen_bf16(const bf16 *__restrict__ Q, const bf16 *__restrict__ Bsrc,
+                                                     int64_t b_pair_stride, int64_t b_plane_stride, int b_rows,
+                                                     const float *__restrict__ shift, bf16 *__restrict__ out,
+                                                     int64_t out_pair_stride, int64_t out_plane_stride,
+                                                     float *__restrict__ aux, int64_t aux_pair_stride, int n,
+                                                     int n_pad, float scale, const int32_t *__restrict__ anchors,
+                                                     int t, bf16 *__restrict__ uout, float *__restrict__ ssq,
+                                                     int64_t tp) {
+  constexpr int NB = MODE == MODE_PHIC ? 2 : 1;           // compact keys kept as bf16 hi + lo
+  constexpr int NKS = kHeadDim / 16;
+  constexpr int QB = 64 * kHeadDim * 2;                   // one Q stage (16 KB)
+  // staging: bf16 rows of 64 + 8 (profile) or fp32 rows of 64 + 4 (phic)
+  constexpr int SO_F = 64 + 4, SO_H = 64 + 8;
+  constexpr int STG = MODE == MODE_PHIC ? 32 * SO_F * 4 : 32 * SO_H * 2;
+  __shared__ __attribute__((aligned(1024))) char sQ[2 * QB];
+  __shared__ __attribute__((aligned(16))) char sOut[4 * STG];
+
+  const int b = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int h = lane >> 5, col = lane & 31;
+  const int row = blockIdx.x * 128 + wave * 32 + col;   // key j or compact-key r
+  const bool rvalid = row < b_rows;
+  const bf16 *Bp = Bsrc + (size_t)b * b_pair_stride;
+  bf16x8 bf[NB][NKS];
+#pragma unroll
+  for (int p = 0; p < NB; ++p)
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks)
+      bf[p][ks] = rvalid ? *reinterpret_cast<const bf16x8 *>(Bp + p * b_plane_stride + (size_t)row * kHeadDim +
+                                                              ks * 16 + 8 * h)
+                         : Mfma<bf16>::zero();
+  const bf16 *Qb = Q + (size_t)b * n * kHeadDim;
+  const float c2 = scale * 1.4426950408889634f;
+  const float zs2 = MODE == MODE_PROFILE ? shift[b] * 1.4426950408889634f : 0.0f;
+  float rowsum = 0.0f, sumsq = 0.0f;
+  int dest = -1;   // profile: >= 0 compacted E^T row, <= -2 anchor -(r + 2), -1 none
+  if (MODE == MODE_PROFILE && rvalid) {
+    const int32_t *S = anchors + (size_t)b * t;
+    int lo = 0, hi = t;
+    while (lo < hi) {
+      const int mid = (lo + hi) >> 1;
+      if (S[mid] < row) lo = mid + 1;
+      else hi = mid;
+    }
+    dest = (lo < t && S[lo] == row) ? -(lo + 2) : row - lo;
+  }
+  // Q stage loads: run 4 wave + u covers tile rows 4 (4 wave + u) .. + 3; lane l
+  // fills physical chunk l % 16 of its row with logical chunk (l % 16) ^ row.
+  // Rows past n read row n - 1 (their outputs are masked).
+  auto issue_q = [&](int i0, int st) {
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int r = 4 * (4 * wave + u) + lane / 16;
+      const int qrow = min(i0 + r, n - 1);
+      const bf16 *src = Qb + (size_t)qrow * kHeadDim + 8 * ((lane % 16) ^ (r & 15));
+      __builtin_amdgcn_global_load_lds((const void *)src, (eg_lds_t *)(sQ + st * QB + (4 * wave + u) * 1024), 16,
+                                       0, 0);
+    }
+  };
+  char *so = sOut + wave * STG;
+  auto wave_fence = [] { asm volatile("" ::: "memory"); };
+  const int row0 = blockIdx.x * 128 + wave * 32;
+  auto row_dst = [&](int rr, int i0) -> bf16 * {
+    const int d = __shfl(dest, rr, 64);
+    if (d == -1) return nullptr;
+    bf16 *base = d >= 0 ? out + (size_t)b * out_pair_stride + (size_t)d * n_pad
+                        : uout + ((size_t)b * tp + (size_t)(-d - 2)) * n_pad;
+    return base + i0;
+  };
+  // stage v (rows = this wave's 32 outputs, 64 query columns) and copy out
+  auto flush_bf16 = [&](const float (&v)[2][16], int part, bf16 *dst_base, bool routed, int i0) {
+    bf16 *sb = reinterpret_cast<bf16 *>(so);
+    wave_fence();
+#pragma unroll
+    for (int ms = 0; ms < 2; ++ms)
+#pragma unroll
+      for (int vv = 0; vv < 16; ++vv) {
+        bf16 hi, lo;
+        split_bf16(v[ms][vv], hi, lo);
+        sb[col * SO_H + 32 * ms + acc_row(vv, lane)] = part == 2 ? lo : hi;
+      }
+    wave_fence();
+#pragma unroll
+    for (int pass = 0; pass < 4; ++pass) {             // 32 rows x 8 chunks of 16 B
+      const int chunk = pass * 64 + lane, r = chunk / 8, c8 = (chunk % 8) * 8;
+      bf16 *dst = routed ? row_dst(r, i0) : dst_base + (size_t)r * n_pad;
+      const bf16x8 w = *reinterpret_cast<const bf16x8 *>(&sb[r * SO_H + c8]);
+      if (dst) *reinterpret_cast<bf16x8 *>(dst + c8) = w;
+    }
+    wave_fence();
+  };
+  auto flush_f32 = [&](const float (&v)[2][16], float *dst_base) {
+    float *sf = reinterpret_cast<float *>(so);
+    wave_fence();
+#pragma unroll
+    for (int ms = 0; ms < 2; ++ms)
+#pragma unroll
+      for (int vv = 0; vv < 16; ++vv) sf[col * SO_F + 32 * ms + acc_row(vv, lane)] = v[ms][vv];
+    wave_fence();
+#pragma unroll
+    for (int pass = 0; pass < 8; ++pass) {             // 32 rows x 16 chunks of 16 B
+      const int chunk = pass * 64 + lane, r = chunk / 16, c4 = (chunk % 16) * 4;
+      const f32x4 w = {sf[r * SO_F + c4], sf[r * SO_F + c4 + 1], sf[r * SO_F + c4 + 2], sf[r * SO_F + c4 + 3]};
+      *reinterpret_cast<f32x4 *>(dst_base + (size_t)r * n_pad + c4) = w;
+    }
+    wave_fence();
+  };
+
+  const int ntile = n_pad / 64;
+  issue_q(0, 0);
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  for (int it = 0; it < ntile; ++it) {
+    const int i0 = it * 64, st = it & 1;
+    if (it + 1 < ntile) issue_q(i0 + 64, st ^ 1);
+    const char *sq = sQ + st * QB;
+    float val[2][16], lg[2][16];
+#pragma unroll
+    for (int ms = 0; ms < 2; ++ms) {
+      f32x16 acc = zero16();
+      const int r = 32 * ms + col;
+#pragma unroll
+      for (int ks = 0; ks < NKS; ++ks) {
+        const bf16x8 a = *reinterpret_cast<const bf16x8 *>(sq + r * 256 + 16 * ((2 * ks + h) ^ (r & 15)));
+#pragma unroll
+        for (int p = 0; p < NB; ++p) acc = Mfma<bf16>::mma(a, bf[p][ks], acc);
+      }
+#pragma unroll
+      for (int vv = 0; vv < 16; ++vv) {
+        const int i = i0 + 32 * ms + acc_row(vv, lane);
+        const bool ok = rvalid && i < n;
+        if (MODE == MODE_PROFILE) {
+          val[ms][vv] = ok ? exp2f(acc[vv] * c2 - zs2) : 0.0f;
+          rowsum += val[ms][vv];
+          const float stored = (float)(bf16)val[ms][vv];
+          sumsq = fmaf(stored, stored, sumsq);
+        } else {
+          lg[ms][vv] = ok ? acc[vv] * scale : 0.0f;
+          // shift (the row maxima z) is null when only the logits are wanted
+          val[ms][vv] = ok ? expf(lg[ms][vv] - (shift ? shift[(size_t)b * n + i] : 0.0f)) : 0.0f;
+        }
+      }
+    }
+    // the next Q stage has landed (this wave's loads, and every wave's after
+    // the barrier), and every wave is done reading stage st
+    __builtin_amdgcn_s_waitcnt(0);
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+    if constexpr (MODE == MODE_PROFILE) {
+      flush_bf16(val, 0, nullptr, true, i0);
+    } else {
+      bf16 *o = out + (size_t)b * out_pair_stride + (size_t)row0 * n_pad + i0;
+      flush_bf16(val, 1, o, false, i0);
+      flush_bf16(val, 2, o + out_plane_stride, false, i0);
+      flush_f32(lg, aux + (size_t)b * aux_pair_stride + (size_t)row0 * n_pad + i0);
+    }
+  }
+  if (MODE == MODE_PROFILE) {
+    rowsum += __shfl_xor(rowsum, 32, 64);
+    sumsq += __shfl_xor(sumsq, 32, 64);
+    if (h == 0 && rvalid) aux[(size_t)b * aux_pair_stride + row] = rowsum / (float)n;
+    if (h == 0 && dest <= -2) ssq[(size_t)b * tp + (-dest - 2)] = sumsq;
+  }
+}
+
 // Compacted E^T [B][Tp][np] (rows of the non-anchor keys; T = bf16 or
 // float), unnormalised anchor profiles U [B][tp][np] with their sums of
 // squares ssq [B][tp], and phi [B][T].
@@ -183,9 +360,9 @@ hipError_t launch_profiles(int dtype, const void *Q, const void *K, const float 
                            int64_t tp, int64_t np_, float scale, hipStream_t s) {
   dim3 grid(Tp / 128, B);
   if (dtype == ARCKV_BF16)
-    hipLaunchKernelGGL((k_expgen<bf16, MODE_PROFILE>), grid, dim3(256), 0, s, (const bf16 *)Q, K,
-                       (int64_t)T * kHeadDim, (int64_t)0, T, zmerge, Et, Tp * np_, (int64_t)0, phi, (int64_t)T, n,
-                       (int)np_, scale, anchors, t, U, ssq, tp);
+    hipLaunchKernelGGL((k_expgen_bf16<MODE_PROFILE>), grid, dim3(256), 0, s, (const bf16 *)Q, (const bf16 *)K,
+                       (int64_t)T * kHeadDim, (int64_t)0, T, zmerge, (bf16 *)Et, Tp * np_, (int64_t)0, phi,
+                       (int64_t)T, n, (int)np_, scale, anchors, t, (bf16 *)U, ssq, tp);
   else
     hipLaunchKernelGGL((k_expgen<float, MODE_PROFILE>), grid, dim3(256), 0, s, (const float *)Q, K,
                        (int64_t)T * kHeadDim, (int64_t)0, T, zmerge, Et, Tp * np_, (int64_t)0, phi, (int64_t)T,
@@ -198,9 +375,9 @@ hipError_t launch_phic(int dtype, const void *Q, const void *Ckp, const float *z
                        int n, int64_t tp, int64_t np_, float scale, hipStream_t s) {
   dim3 grid(tp / 128, B);
   if (dtype == ARCKV_BF16)
-    hipLaunchKernelGGL((k_expgen<bf16, MODE_PHIC>), grid, dim3(256), 0, s, (const bf16 *)Q, Ckp,
-                       2 * tp * kHeadDim, tp * kHeadDim, t, z, PhiT, 2 * tp * np_, tp * np_, LT, tp * np_, n,
-                       (int)np_, scale, (const int32_t *)nullptr, 0, (void *)nullptr, (float *)nullptr, tp);
+    hipLaunchKernelGGL((k_expgen_bf16<MODE_PHIC>), grid, dim3(256), 0, s, (const bf16 *)Q, (const bf16 *)Ckp,
+                       2 * tp * kHeadDim, tp * kHeadDim, t, z, (bf16 *)PhiT, 2 * tp * np_, tp * np_, LT, tp * np_,
+                       n, (int)np_, scale, (const int32_t *)nullptr, 0, (bf16 *)nullptr, (float *)nullptr, tp);
   else
     hipLaunchKernelGGL((k_expgen<float, MODE_PHIC>), grid, dim3(256), 0, s, (const float *)Q, Ckp,
                        tp * kHeadDim, (int64_t)0, t, z, PhiT, tp * np_, (int64_t)0, LT, tp * np_, n, (int)np_,
