@@ -58,7 +58,7 @@ hipError_t launch_transpose_planes(int dtype, const void *PT, void *P, int B, in
 hipError_t launch_hvec(const float *LT, const float *z, const float *m, int B, int n, int t, int64_t tp, int64_t np_,
                        double *h, hipStream_t s);
 hipError_t launch_cholesky(float *Gw, const float *Gc, int B, int t, int64_t ld, float delta0, int max_esc,
-                           FitState st, float *dinv, hipStream_t s);
+                           FitState st, float *dinv, void *lsplit, hipStream_t s);
 hipError_t launch_trsv(const float *Gw, const float *dinv, int B, int64_t ld, const double *rhs, double *sw,
                        double *y, double *x, double *acc, const int32_t *info, hipStream_t s);
 hipError_t launch_bias_finalize(const double *w, int B, int64_t ld, int t, float eps, float bmin, float bmax,
@@ -170,7 +170,7 @@ struct Plan {
   // chunk region (offsets relative to chunk base)
   int64_t Ckp;
   int64_t Et, U, ssq, part, offsets, cursor, perm;       // merge phase
-  int64_t PhiT, LT, Gw, Gc, dinv, h, w, y, x, res, sw, u, YT, Bm, X, R, Y2, XT, Pm, UT;  // fit phase
+  int64_t PhiT, LT, Gw, Gc, dinv, lsplit, h, w, y, x, res, sw, u, YT, Bm, X, R, Y2, XT, Pm, UT;  // fit phase
   int64_t chunk_bytes;
 };
 
@@ -210,6 +210,7 @@ static Plan make_plan(const Dims &d, int64_t P) {
   pl.Gw = f.take(P * d.tp * d.tp * 4);
   pl.Gc = f.take(P * d.tp * d.tp * 4);
   pl.dinv = f.take(P * d.tp * 64 * 4);   // one 64 x 64 inverse per diagonal block
+  pl.lsplit = f.take(P * 3 * d.tp * 256 * 2);   // bf16 hi/mid/lo planes of one 256-column panel
   pl.h = f.take(P * d.tp * 8);
   pl.w = f.take(P * d.tp * 8);
   pl.y = f.take(P * d.tp * 8);
@@ -362,7 +363,8 @@ static arckv_status run_fit_bias_chunk(const Ctx &c, int b0, int P, const void *
                              stream));
   STAGE(ST_GRAM_G, launch_gram(d.dtype, PhiT, Gw, Gc, P, d.tp, d.np_, stream));
   STAGE(ST_HVEC, launch_hvec(LT, zc, mc, P, d.n, d.t, d.tp, d.np_, h, stream));
-  STAGE(ST_CHOL_G, launch_cholesky(Gw, Gc, P, d.t, d.tp, fp.delta_beta, fp.max_escalations, st, dinv, stream));
+  STAGE(ST_CHOL_G, launch_cholesky(Gw, Gc, P, d.t, d.tp, fp.delta_beta, fp.max_escalations, st, dinv,
+                                   c.chunk<char>(c.pl.lsplit), stream));
   {
     StageScope _sc(ST_SOLVE_W, stream);
     if (launch_trsv(Gw, dinv, P, d.tp, h, sw, y, w, nullptr, st.info, stream) != hipSuccess) return ARCKV_ERR_HIP;
@@ -407,7 +409,8 @@ static arckv_status run_fit_values_chunk(const Ctx &c, int b0, int P, const floa
       return ARCKV_ERR_HIP;
     if (launch_rhs_gemm(d.dtype, PT, YT, Bm, P, d.tp, d.np_, stream) != hipSuccess) return ARCKV_ERR_HIP;
   }
-  STAGE(ST_CHOL_A, launch_cholesky(Gw, Gc, P, d.t, d.tp, fp.delta_v, fp.max_escalations, st, dinv, stream));
+  STAGE(ST_CHOL_A, launch_cholesky(Gw, Gc, P, d.t, d.tp, fp.delta_v, fp.max_escalations, st, dinv,
+                                   c.chunk<char>(c.pl.lsplit), stream));
   {
     StageScope _sc(ST_SOLVE_V, stream);
     if (launch_trsm(true, Gw, dinv, P, d.tp, Bm, Y2, st.info, stream) != hipSuccess) return ARCKV_ERR_HIP;

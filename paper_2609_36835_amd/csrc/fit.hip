@@ -21,6 +21,7 @@
 //                    (value fit), for iterative refinement
 #include "common.hpp"
 #include "gemm.hpp"
+#include "gemm_big.hpp"
 
 namespace arckv {
 
@@ -391,6 +392,69 @@ __global__ void __launch_bounds__(256) k_chol_upd(float *__restrict__ Gw, int64_
       }
     }
 }
+
+// Outer trailing update as a bf16 MFMA contraction: the finished 256-column
+// panel L[K1:ld, K0:K1] is split exactly into three bf16 planes (x = hi + mid
+// + lo, 8 significant bits each), and G -= L L^T takes the six products whose
+// plane indices sum to at most 2 (the dropped terms are below 2^-23 of |x y|),
+// so it reproduces the fp32 update at fp32 accuracy on the bf16 MFMA rate.
+// Planes: Ls [P][3][ld][256], row r holding L[r][K0:K0+256].
+__global__ void __launch_bounds__(256) k_chol_split3(const float *__restrict__ Gw, int64_t ld, int K0, int K1,
+                                                     bf16 *__restrict__ Ls, const int32_t *__restrict__ info) {
+  const int b = blockIdx.y;
+  if (info[b] != 0) return;
+  const int64_t e = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 4;   // 4 consecutive columns
+  const int64_t r = K1 + e / 256, q = e % 256;
+  if (r >= ld) return;
+  const f32x4 v = *reinterpret_cast<const f32x4 *>(Gw + (size_t)b * ld * ld + (size_t)r * ld + K0 + q);
+  bf16 *base = Ls + (size_t)b * 3 * ld * 256 + (size_t)r * 256 + q;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const bf16 hi = (bf16)v[k];
+    const float r1 = v[k] - (float)hi;
+    const bf16 mid = (bf16)r1;
+    const bf16 lo = (bf16)(r1 - (float)mid);
+    base[k] = hi;
+    base[(size_t)ld * 256 + k] = mid;
+    base[(size_t)2 * ld * 256 + k] = lo;
+  }
+}
+
+// G[K1 + r][K1 + c] -= acc for the tile's entries with c <= r + 63 (the lower
+// triangle, up to whole diagonal 64-blocks); every old value is loaded before
+// any store so the loads pipeline.
+template <int TM, int TN>
+struct EpiCholUpd {
+  float *G;
+  int64_t ld;
+  int K1;
+  const int32_t *info;
+  __device__ __forceinline__ void operator()(f32x16 (&acc)[TM][TN], int p, int row0, int col0, int, int, int lane,
+                                             int, int) const {
+    if (info[p] != 0) return;
+    float *Gp = G + (size_t)p * ld * ld + (size_t)K1 * ld + K1;
+    const int col = lane & 31;
+    float old[TM][TN][16];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int r = row0 + 32 * i + acc_row(v, lane), c = col0 + 32 * j + col;
+          old[i][j][v] = __builtin_nontemporal_load(&Gp[(size_t)r * ld + c]);
+        }
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int r = row0 + 32 * i + acc_row(v, lane), c = col0 + 32 * j + col;
+          if (c <= r + 63) Gp[(size_t)r * ld + c] = old[i][j][v] - acc[i][j][v];
+        }
+  }
+};
 
 // Whole factorisation in one workgroup (escalation path).
 __device__ int factor_matrix_single(float *G, int64_t ld, int nrb, float *sA, float *sB) {
@@ -856,7 +920,7 @@ hipError_t launch_hvec(const float *LT, const float *z, const float *m, int B, i
 
 // Ridge + factorisation (+ escalation) of the work copy Gw of Gc.
 hipError_t launch_cholesky(float *Gw, const float *Gc, int B, int t, int64_t ld, float delta0, int max_esc,
-                           FitState st, float *dinv, hipStream_t s) {
+                           FitState st, float *dinv, void *lsplit, hipStream_t s) {
   hipLaunchKernelGGL(k_ridge_init, dim3(B), dim3(256), 0, s, Gw, Gc, t, ld, delta0, st);
   // Two-level right-looking blocking: 64-wide diagonal factor + panel solve
   // steps inside 256-wide outer panels; inside an outer panel only its own
@@ -880,9 +944,16 @@ hipError_t launch_cholesky(float *Gw, const float *Gc, int B, int t, int64_t ld,
       }
     }
     if (K1 < ld) {
-      const int n_rt = (int)((ld - K1 + 127) / 128), n_ct = n_rt;
-      hipLaunchKernelGGL(k_chol_upd, dim3((unsigned)(chol_upd_tiles(n_rt, n_ct) * B)), dim3(256), 0, s, Gw, ld, K1,
-                         (int)ld, K0, K1 - K0, n_rt, n_ct, st.info);
+      // rank-256 trailing update on bf16 MFMA with the split panel (see k_chol_split3)
+      bf16 *Ls = reinterpret_cast<bf16 *>(lsplit);
+      const int64_t rows = ld - K1;
+      hipLaunchKernelGGL(k_chol_split3, dim3((unsigned)(rows * 256 / 4 / 256), B), dim3(256), 0, s, Gw, ld, K0, K1,
+                         Ls, st.info);
+      BigShape g{B, (int)rows, (int)rows, kOuter, 3 * ld * 256, ld * 256, 256, 3 * ld * 256, ld * 256, 256, true, 4};
+      EpiCholUpd<1, 2> e{Gw, ld, K1, st.info};
+      const hipError_t err =
+          launch_gemm_big<4, 2, 1, 2, 32, 3, 3>(g, Ls + (size_t)K1 * 256, Ls + (size_t)K1 * 256, e, s);
+      if (err != hipSuccess) return err;
     }
   }
   if (max_esc > 0) {

@@ -1,6 +1,9 @@
 // Large-tile batched TN contraction on bf16 MFMA (32x32x16) for the big
-// contractions of the path: the anchor assignment (one bf16 plane) and the
-// split-bf16 Gram matrices (hi/lo planes, three products).
+// contractions of the path: the anchor assignment (one bf16 plane), the
+// split-bf16 Gram matrices (hi/lo planes, three products) and the Cholesky
+// trailing updates (hi/mid/lo planes of an fp32 panel, the six products whose
+// plane indices sum to at most 2, which reproduce the fp32 product to within
+// about 2^-23 relative).
 //
 // C[M][N] = sum_k A[m][k] B[n][k], both operands K-contiguous.  A workgroup of
 // WM x WN waves owns a (32 WM TM) x (32 WN TN) tile; each wave a 32TM x 32TN
@@ -44,6 +47,7 @@ struct BigCfg {
   static constexpr int KS = BK / 16;
   static_assert(A_INST * NW * 1024 == A_BYTES && B_INST * NW * 1024 == B_BYTES, "load split");
   static_assert(CPR == 4 || CPR == 8, "BK must be 32 or 64");
+  static_assert(NA == NB || NA == 1 || NB == 1, "plane counts");
   static_assert(LDS <= 160 * 1024 - 16 * 1024, "LDS budget");
   // chunk swizzle: 16 consecutive rows at one logical chunk cover all 64 banks
   __device__ static __forceinline__ int swz(int row) { return (row * RB / 256) & (CPR - 1); }
@@ -186,6 +190,11 @@ __global__ void __launch_bounds__(64 * WM * WN, 1) k_gemm_big(BigShape g, const 
           acc[ii][j] = Mfma<bf16>::mma(fa[cur][0][ii], fb[cur][0][j], acc[ii][j]);
           if constexpr (NB > 1) acc[ii][j] = Mfma<bf16>::mma(fa[cur][0][ii], fb[cur][1][j], acc[ii][j]);
           if constexpr (NA > 1) acc[ii][j] = Mfma<bf16>::mma(fa[cur][1][ii], fb[cur][0][j], acc[ii][j]);
+          if constexpr (NA > 2 && NB > 2) {
+            acc[ii][j] = Mfma<bf16>::mma(fa[cur][0][ii], fb[cur][2][j], acc[ii][j]);
+            acc[ii][j] = Mfma<bf16>::mma(fa[cur][2][ii], fb[cur][0][j], acc[ii][j]);
+            acc[ii][j] = Mfma<bf16>::mma(fa[cur][1][ii], fb[cur][1][j], acc[ii][j]);
+          }
         }
     }
     asm volatile("" ::: "memory");
