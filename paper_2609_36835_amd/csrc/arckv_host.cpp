@@ -31,8 +31,9 @@ hipError_t launch_rowstats(int dtype, const void *K, const void *V, const void *
 hipError_t launch_profiles(int dtype, const void *Q, const void *K, const float *zmerge, const int32_t *anchors,
                            int t, void *Et, void *U, float *ssq, float *phi, int B, int T, int n, int64_t Tp,
                            int64_t tp, int64_t np_, float scale, hipStream_t s);
-hipError_t launch_phic(int dtype, const void *Q, const void *Ckp, const float *z, void *PhiT, float *LT, int B, int t,
-                       int n, int64_t tp, int64_t np_, float scale, hipStream_t s);
+hipError_t launch_phic(int dtype, const void *Q, const void *Ckp, const float *z, void *PhiT, float *LT,
+                       const float *m, double *h, int B, int t, int n, int64_t tp, int64_t np_, float scale,
+                       hipStream_t s);
 hipError_t launch_zmax(const float *z, int B, int n, float *zmax, hipStream_t s);
 hipError_t launch_anchor_of(const int32_t *anchors, int B, int T, int t, int32_t *anchor_of, hipStream_t s);
 hipError_t launch_anchor_profiles(int dtype, void *U, const float *ssq, int B, int t, int64_t np_, int64_t tp,
@@ -53,10 +54,6 @@ hipError_t launch_value_residual(int dtype, const void *XT, const void *Pm, cons
 hipError_t launch_mass_residual(const float *LT, const float *z, const float *m, const double *w, const float *lam,
                                 int B, int n, int t, int64_t tp, int64_t np_, double *u, double *res,
                                 const int32_t *info, hipStream_t s);
-hipError_t launch_transpose_planes(int dtype, const void *PT, void *P, int B, int64_t rows, int64_t cols,
-                                   hipStream_t s);
-hipError_t launch_hvec(const float *LT, const float *z, const float *m, int B, int n, int t, int64_t tp, int64_t np_,
-                       double *h, hipStream_t s);
 hipError_t launch_cholesky(float *Gw, const float *Gc, int B, int t, int64_t ld, float delta0, int max_esc,
                            FitState st, float *dinv, void *lsplit, hipStream_t s);
 hipError_t launch_trsv(const float *Gw, const float *dinv, int B, int64_t ld, const double *rhs, double *sw,
@@ -64,7 +61,7 @@ hipError_t launch_trsv(const float *Gw, const float *dinv, int B, int64_t ld, co
 hipError_t launch_bias_finalize(const double *w, int B, int64_t ld, int t, float eps, float bmin, float bmax,
                                 const int32_t *info, float *beta, float *beta_ws, hipStream_t s);
 hipError_t launch_phat(int dtype, const float *LT, const float *beta_ws, int B, int n, int t, int64_t tp,
-                       int64_t np_, void *out, hipStream_t s);
+                       int64_t np_, void *out, void *outm, hipStream_t s);
 hipError_t launch_transpose128(int dtype, const float *in, int B, int rows, int64_t in_pair, int64_t rows_pad,
                                void *out, int64_t out_pair, hipStream_t s);
 hipError_t launch_trsm(bool fwd, const float *Gw, const float *dinv, int B, int64_t ld, const float *R, float *X,
@@ -78,12 +75,12 @@ hipError_t launch_copy_f32(const float *src, float *dst, int B, hipStream_t s);
 // ------------------------------------------------------------------ timing
 enum Stage {
   ST_SCORE, ST_SELECT, ST_ROWSTATS, ST_ZMAX, ST_PROFILES, ST_ANCHOR_PROF, ST_ASSIGN, ST_FINALIZE, ST_MERGE,
-  ST_PHIC, ST_GRAM_G, ST_HVEC, ST_CHOL_G, ST_SOLVE_W, ST_PHAT, ST_GRAM_A, ST_RHS, ST_CHOL_A, ST_SOLVE_V,
+  ST_PHIC, ST_GRAM_G, ST_CHOL_G, ST_SOLVE_W, ST_PHAT, ST_GRAM_A, ST_RHS, ST_CHOL_A, ST_SOLVE_V,
   ST_COUNT
 };
 static const char *kStageNames[ST_COUNT] = {
     "score", "select", "rowstats", "zmax", "profiles", "anchor_profiles", "assign_gemm", "assign_finalize",
-    "merge", "phic", "gram_G", "hvec", "chol_G", "solve_beta", "phat", "gram_A", "rhs_B", "chol_A", "solve_values"};
+    "merge", "phic", "gram_G", "chol_G", "solve_beta", "phat", "gram_A", "rhs_B", "chol_A", "solve_values"};
 
 struct TimingState {
   std::mutex mu;
@@ -359,10 +356,10 @@ static arckv_status run_fit_bias_chunk(const Ctx &c, int b0, int P, const void *
   double *h = c.chunk<double>(c.pl.h), *w = c.chunk<double>(c.pl.w), *y = c.chunk<double>(c.pl.y);
   double *x = c.chunk<double>(c.pl.x), *res = c.chunk<double>(c.pl.res), *sw = c.chunk<double>(c.pl.sw);
   float *dinv = c.chunk<float>(c.pl.dinv);
-  STAGE(ST_PHIC, launch_phic(d.dtype, Qc, c.chunk<char>(c.pl.Ckp), zc, PhiT, LT, P, d.t, d.n, d.tp, d.np_, c.scale,
-                             stream));
+  // Phi_C^T (split planes), the logits L^T, and h = Phi_C^T m in one pass
+  STAGE(ST_PHIC, launch_phic(d.dtype, Qc, c.chunk<char>(c.pl.Ckp), zc, PhiT, LT, mc, h, P, d.t, d.n, d.tp, d.np_,
+                             c.scale, stream));
   STAGE(ST_GRAM_G, launch_gram(d.dtype, PhiT, Gw, Gc, P, d.tp, d.np_, stream));
-  STAGE(ST_HVEC, launch_hvec(LT, zc, mc, P, d.n, d.t, d.tp, d.np_, h, stream));
   STAGE(ST_CHOL_G, launch_cholesky(Gw, Gc, P, d.t, d.tp, fp.delta_beta, fp.max_escalations, st, dinv,
                                    c.chunk<char>(c.pl.lsplit), stream));
   {
@@ -399,8 +396,9 @@ static arckv_status run_fit_values_chunk(const Ctx &c, int b0, int P, const floa
   const float *Yc = Y + (size_t)b0 * d.n * kHeadDimH;
   const int64_t pl = d.dtype == ARCKV_BF16 ? 2 : 1;
   const int64_t yt_pair = (d.dtype == ARCKV_BF16 ? 2 : 1) * (int64_t)kHeadDimH * d.np_;
+  // P^T for the Gram and right-hand side, and P (query-major) for the refinement residuals
   STAGE(ST_PHAT, launch_phat(d.dtype, LT, c.pers<float>(c.pl.beta_ws) + (size_t)b0 * d.tp, P, d.n, d.t, d.tp,
-                             d.np_, PT, stream));
+                             d.np_, PT, fp.refine_steps > 0 ? Pm : nullptr, stream));
   STAGE(ST_GRAM_A, launch_gram(d.dtype, PT, Gw, Gc, P, d.tp, d.np_, stream));
   {
     StageScope _sc(ST_RHS, stream);
@@ -416,8 +414,6 @@ static arckv_status run_fit_values_chunk(const Ctx &c, int b0, int P, const floa
     if (launch_trsm(true, Gw, dinv, P, d.tp, Bm, Y2, st.info, stream) != hipSuccess) return ARCKV_ERR_HIP;
     if (launch_trsm(false, Gw, dinv, P, d.tp, Y2, X, st.info, stream) != hipSuccess) return ARCKV_ERR_HIP;
     // refinement against the data: R = P^T (Y - P X) - lam X
-    if (fp.refine_steps > 0 && launch_transpose_planes(d.dtype, PT, Pm, P, d.tp, d.np_, stream) != hipSuccess)
-      return ARCKV_ERR_HIP;
     for (int it = 0; it < fp.refine_steps; ++it) {
       if (launch_transpose128(d.dtype, X, P, (int)d.tp, d.tp * kHeadDimH, d.tp, XT, pl * d.tp * kHeadDimH, stream) !=
           hipSuccess)
@@ -601,7 +597,7 @@ arckv_status arckv_fit_values(const arckv_problem *prob, const void *Q_ref, cons
     // logits of the compact keys (the exp-part is unused here; z only shifts it)
     const char *Qc = (const char *)Q_ref + (size_t)b0 * d.n * kHeadDimH * c.in_esz();
     STAGE(ST_PHIC, launch_phic(d.dtype, Qc, c.chunk<char>(c.pl.Ckp), nullptr, c.chunk<char>(c.pl.PhiT),
-                               c.chunk<float>(c.pl.LT), Pc, d.t, d.n, d.tp, d.np_, c.scale, stream));
+                               c.chunk<float>(c.pl.LT), nullptr, nullptr, Pc, d.t, d.n, d.tp, d.np_, c.scale, stream));
     FitState st = fit_state(c, c.pl.st_a, c.pl.info_a, b0);
     CHECK(run_fit_values_chunk(c, b0, Pc, Y, *p, C_v, st));
   }

@@ -28,7 +28,8 @@ __global__ void __launch_bounds__(256) k_expgen(const T *__restrict__ Q, const v
                                                 int64_t out_pair_stride, int64_t out_plane_stride,
                                                 float *__restrict__ aux, int64_t aux_pair_stride, int n,
                                                 int n_pad, float scale, const int32_t *__restrict__ anchors, int t,
-                                                void *__restrict__ uout, float *__restrict__ ssq, int64_t tp) {
+                                                void *__restrict__ uout, float *__restrict__ ssq, int64_t tp,
+                                                const float *__restrict__ mvec, double *__restrict__ hout) {
   using M = Mfma<T>;
   constexpr int KPL = M::KPL, KSTEP = M::KSTEP, NKS = kHeadDim / KSTEP;
   constexpr bool SPLIT_B = (MODE == MODE_PHIC) && sizeof(T) == 2;   // compact keys kept as bf16 hi + lo
@@ -53,6 +54,7 @@ __global__ void __launch_bounds__(256) k_expgen(const T *__restrict__ Q, const v
   const float c2 = scale * 1.4426950408889634f;
   const float zshift = (MODE == MODE_PROFILE) ? shift[b] : 0.0f;
   float rowsum = 0.0f, sumsq = 0.0f;
+  double hsum = 0.0;   // PHIC: h_r = sum_i Phi[i][r] m_i (when hout is given)
   // PROFILE destination of this lane's key: >= 0 compacted E^T row, <= -2
   // anchor -(r + 2), -1 none (padding key)
   int dest = -1;
@@ -149,6 +151,7 @@ __global__ void __launch_bounds__(256) k_expgen(const T *__restrict__ Q, const v
         } else {
           lg[ms][vv] = ok ? acc[vv] * scale : 0.0f;
           val[ms][vv] = ok ? expf(lg[ms][vv] - (shift ? shift[(size_t)b * n + i] : 0.0f)) : 0.0f;
+          if (hout && ok) hsum += (double)val[ms][vv] * (double)mvec[(size_t)b * n + i];
         }
       }
     }
@@ -173,6 +176,10 @@ __global__ void __launch_bounds__(256) k_expgen(const T *__restrict__ Q, const v
     if (h == 0 && rvalid) aux[(size_t)b * aux_pair_stride + row] = rowsum / (float)n;
     if (h == 0 && dest <= -2) ssq[(size_t)b * tp + (-dest - 2)] = sumsq;
   }
+  if (MODE == MODE_PHIC && hout) {
+    hsum += __shfl_xor(hsum, 32, 64);
+    if (h == 0) hout[(size_t)b * tp + row] = hsum;
+  }
 }
 
 // ---------------------------------------------------------------- bf16 path
@@ -194,7 +201,8 @@ __global__ void __launch_bounds__(256) k_expgen_bf16(const bf16 *__restrict__ Q,
                                                      float *__restrict__ aux, int64_t aux_pair_stride, int n,
                                                      int n_pad, float scale, const int32_t *__restrict__ anchors,
                                                      int t, bf16 *__restrict__ uout, float *__restrict__ ssq,
-                                                     int64_t tp) {
+                                                     int64_t tp, const float *__restrict__ mvec,
+                                                     double *__restrict__ hout) {
   constexpr int NB = MODE == MODE_PHIC ? 2 : 1;           // compact keys kept as bf16 hi + lo
   constexpr int NKS = kHeadDim / 16;
   constexpr int QB = 64 * kHeadDim * 2;                   // one Q stage (16 KB)
@@ -221,6 +229,7 @@ __global__ void __launch_bounds__(256) k_expgen_bf16(const bf16 *__restrict__ Q,
   const float c2 = scale * 1.4426950408889634f;
   const float zs2 = MODE == MODE_PROFILE ? shift[b] * 1.4426950408889634f : 0.0f;
   float rowsum = 0.0f, sumsq = 0.0f;
+  double hsum = 0.0;   // PHIC: h_r = sum_i Phi[i][r] m_i (when hout is given)
   int dest = -1;   // profile: >= 0 compacted E^T row, <= -2 anchor -(r + 2), -1 none
   if (MODE == MODE_PROFILE && rvalid) {
     const int32_t *S = anchors + (size_t)b * t;
@@ -326,6 +335,7 @@ __global__ void __launch_bounds__(256) k_expgen_bf16(const bf16 *__restrict__ Q,
           lg[ms][vv] = ok ? acc[vv] * scale : 0.0f;
           // shift (the row maxima z) is null when only the logits are wanted
           val[ms][vv] = ok ? expf(lg[ms][vv] - (shift ? shift[(size_t)b * n + i] : 0.0f)) : 0.0f;
+          if (hout && ok) hsum += (double)val[ms][vv] * (double)mvec[(size_t)b * n + i];
         }
       }
     }
@@ -350,6 +360,10 @@ __global__ void __launch_bounds__(256) k_expgen_bf16(const bf16 *__restrict__ Q,
     if (h == 0 && rvalid) aux[(size_t)b * aux_pair_stride + row] = rowsum / (float)n;
     if (h == 0 && dest <= -2) ssq[(size_t)b * tp + (-dest - 2)] = sumsq;
   }
+  if (MODE == MODE_PHIC && hout) {
+    hsum += __shfl_xor(hsum, 32, 64);
+    if (h == 0) hout[(size_t)b * tp + row] = hsum;
+  }
 }
 
 // Compacted E^T [B][Tp][np] (rows of the non-anchor keys; T = bf16 or
@@ -362,26 +376,29 @@ hipError_t launch_profiles(int dtype, const void *Q, const void *K, const float 
   if (dtype == ARCKV_BF16)
     hipLaunchKernelGGL((k_expgen_bf16<MODE_PROFILE>), grid, dim3(256), 0, s, (const bf16 *)Q, (const bf16 *)K,
                        (int64_t)T * kHeadDim, (int64_t)0, T, zmerge, (bf16 *)Et, Tp * np_, (int64_t)0, phi,
-                       (int64_t)T, n, (int)np_, scale, anchors, t, (bf16 *)U, ssq, tp);
+                       (int64_t)T, n, (int)np_, scale, anchors, t, (bf16 *)U, ssq, tp, (const float *)nullptr,
+                       (double *)nullptr);
   else
     hipLaunchKernelGGL((k_expgen<float, MODE_PROFILE>), grid, dim3(256), 0, s, (const float *)Q, K,
                        (int64_t)T * kHeadDim, (int64_t)0, T, zmerge, Et, Tp * np_, (int64_t)0, phi, (int64_t)T,
-                       n, (int)np_, scale, anchors, t, U, ssq, tp);
+                       n, (int)np_, scale, anchors, t, U, ssq, tp, (const float *)nullptr, (double *)nullptr);
   return hipGetLastError();
 }
 
 // Ckp: padded compact keys [B][planes][tp][128]; Phi^T [B][planes][tp][np]; L^T [B][tp][np].
-hipError_t launch_phic(int dtype, const void *Q, const void *Ckp, const float *z, void *PhiT, float *LT, int B, int t,
-                       int n, int64_t tp, int64_t np_, float scale, hipStream_t s) {
+// With m and h given, also h_r = sum_i Phi[i][r] m_i (float64) [B][tp].
+hipError_t launch_phic(int dtype, const void *Q, const void *Ckp, const float *z, void *PhiT, float *LT,
+                       const float *m, double *h, int B, int t, int n, int64_t tp, int64_t np_, float scale,
+                       hipStream_t s) {
   dim3 grid(tp / 128, B);
   if (dtype == ARCKV_BF16)
     hipLaunchKernelGGL((k_expgen_bf16<MODE_PHIC>), grid, dim3(256), 0, s, (const bf16 *)Q, (const bf16 *)Ckp,
                        2 * tp * kHeadDim, tp * kHeadDim, t, z, (bf16 *)PhiT, 2 * tp * np_, tp * np_, LT, tp * np_,
-                       n, (int)np_, scale, (const int32_t *)nullptr, 0, (bf16 *)nullptr, (float *)nullptr, tp);
+                       n, (int)np_, scale, (const int32_t *)nullptr, 0, (bf16 *)nullptr, (float *)nullptr, tp, m, h);
   else
     hipLaunchKernelGGL((k_expgen<float, MODE_PHIC>), grid, dim3(256), 0, s, (const float *)Q, Ckp,
                        tp * kHeadDim, (int64_t)0, t, z, PhiT, tp * np_, (int64_t)0, LT, tp * np_, n, (int)np_,
-                       scale, (const int32_t *)nullptr, 0, (void *)nullptr, (float *)nullptr, tp);
+                       scale, (const int32_t *)nullptr, 0, (void *)nullptr, (float *)nullptr, tp, m, h);
   return hipGetLastError();
 }
 

@@ -35,24 +35,6 @@ struct FitState {
   int32_t *info;   // [P]
 };
 
-// --------------------------------------------------------------- h = Phi_C^T m
-// h_r = sum_i exp(L^T[r][i] - z_i) m_i in float64, one wave per row.
-__global__ void __launch_bounds__(256) k_hvec(const float *__restrict__ LT, const float *__restrict__ z,
-                                              const float *__restrict__ m, int n, int t, int64_t tp, int64_t np_,
-                                              double *__restrict__ h) {
-  const int b = blockIdx.y, lane = threadIdx.x & 63;
-  const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (r >= tp) return;
-  double acc = 0.0;
-  if (r < t) {
-    const float *row = LT + ((size_t)b * tp + r) * np_;
-    for (int i = lane; i < n; i += 64)
-      acc += (double)expf(row[i] - z[(size_t)b * n + i]) * (double)m[(size_t)b * n + i];
-    acc = wave_sum(acc);
-  }
-  if (lane == 0) h[(size_t)b * tp + r] = acc;
-}
-
 // --------------------------------------------------------------- ridge
 __global__ void __launch_bounds__(256) k_ridge_init(float *__restrict__ Gw, const float *__restrict__ Gc, int t,
                                                     int64_t ld, float delta0, FitState st) {
@@ -581,18 +563,30 @@ __global__ void __launch_bounds__(256) k_mass_resid_rows(const float *__restrict
                                                          const float *__restrict__ m, const double *__restrict__ w,
                                                          int n, int t, int64_t tp, int64_t np_,
                                                          double *__restrict__ u, const int32_t *__restrict__ info) {
-  const int b = blockIdx.y;
-  const int i = blockIdx.x * 256 + threadIdx.x;
-  if (i >= np_ || info[b] != 0) return;
-  double acc = 0.0;
+  // 64 queries per workgroup; wave s sums the compact keys r = s (mod 4) with
+  // two accumulators, and the four partial sums meet in LDS
+  __shared__ double red[4][64];
+  const int b = blockIdx.y, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int i = blockIdx.x * 64 + lane;
+  if (info[b] != 0) return;
+  double a0 = 0.0, a1 = 0.0;
   if (i < n) {
     const float *L = LT + (size_t)b * tp * np_ + i;
     const double *wb = w + (size_t)b * tp;
     const float zi = z[(size_t)b * n + i];
-    for (int r = 0; r < t; ++r) acc += (double)expf(L[(size_t)r * np_] - zi) * wb[r];
-    acc = (double)m[(size_t)b * n + i] - acc;
+    int r = wave;
+    for (; r + 4 < t; r += 8) {
+      a0 += (double)expf(L[(size_t)r * np_] - zi) * wb[r];
+      a1 += (double)expf(L[(size_t)(r + 4) * np_] - zi) * wb[r + 4];
+    }
+    if (r < t) a0 += (double)expf(L[(size_t)r * np_] - zi) * wb[r];
   }
-  u[(size_t)b * np_ + i] = acc;
+  red[wave][lane] = a0 + a1;
+  __syncthreads();
+  if (wave == 0 && i < np_) {
+    const double acc = red[0][lane] + red[1][lane] + red[2][lane] + red[3][lane];
+    u[(size_t)b * np_ + i] = i < n ? (double)m[(size_t)b * n + i] - acc : 0.0;
+  }
 }
 
 // Stage 2 (one wave per compact key r): res_r = sum_i Phi[i][r] u_i - lam w_r.
@@ -607,35 +601,18 @@ __global__ void __launch_bounds__(256) k_mass_resid_cols(const float *__restrict
   double acc = 0.0;
   if (r < t) {
     const float *row = LT + ((size_t)b * tp + r) * np_;
-    for (int i = lane; i < n; i += 64)
-      acc += (double)expf(row[i] - z[(size_t)b * n + i]) * u[(size_t)b * np_ + i];
-    acc = wave_sum(acc) - (double)lam[b] * w[(size_t)b * tp + r];
+    const float *zb = z + (size_t)b * n;
+    const double *ub = u + (size_t)b * np_;
+    double a1 = 0.0;
+    int i = lane;
+    for (; i + 64 < n; i += 128) {
+      acc += (double)expf(row[i] - zb[i]) * ub[i];
+      a1 += (double)expf(row[i + 64] - zb[i + 64]) * ub[i + 64];
+    }
+    if (i < n) acc += (double)expf(row[i] - zb[i]) * ub[i];
+    acc = wave_sum(acc + a1) - (double)lam[b] * w[(size_t)b * tp + r];
   }
   if (lane == 0) res[(size_t)b * tp + r] = acc;
-}
-
-// out[c][r] = in[r][c] for [rows][cols] matrices (2- or 4-byte elements, all
-// dims multiples of 64), `planes` consecutive planes per pair.
-template <typename E>
-__global__ void __launch_bounds__(256) k_transpose2d(const E *__restrict__ in, E *__restrict__ out, int64_t rows,
-                                                     int64_t cols, int planes) {
-  __shared__ E s[64][65];
-  const int b = blockIdx.z;
-  const int64_t r0 = (int64_t)blockIdx.y * 64, c0 = (int64_t)blockIdx.x * 64;
-  for (int q = 0; q < planes; ++q) {
-    const E *ip = in + ((size_t)b * planes + q) * rows * cols;
-    E *op = out + ((size_t)b * planes + q) * rows * cols;
-    __syncthreads();
-    for (int e = threadIdx.x; e < 64 * 64; e += 256) {
-      const int rr = e / 64, cc = e % 64;
-      s[rr][cc] = ip[(size_t)(r0 + rr) * cols + c0 + cc];
-    }
-    __syncthreads();
-    for (int e = threadIdx.x; e < 64 * 64; e += 256) {
-      const int cc = e / 64, rr = e % 64;
-      op[(size_t)(c0 + cc) * rows + r0 + rr] = s[rr][cc];
-    }
-  }
 }
 
 // beta = clip(log(max(max(w, 0), eps)), bmin, bmax); NaN for failed pairs.
@@ -661,19 +638,27 @@ __global__ void __launch_bounds__(256) k_bias_finalize(const double *__restrict_
 }
 
 // --------------------------------------------------------------- value-fit operands
-// P^T[r][i] = softmax_r(L^T[r][i] + beta_r) for r < t, i < n (own column max);
-// split into bf16 hi/lo planes (or fp32).  One thread per query.
+// P^T[r][i] = softmax_r(L^T[r][i] + beta_r) for r < t, i < n (own column max),
+// split into bf16 hi/lo planes (or fp32), written in both layouts the value fit
+// contracts over: PT [planes][tp][np] and, if Pm is given, Pm [planes][np][tp].
+// A workgroup takes 64 queries: each wave first runs an online max/sum over the
+// compact keys r = wave (mod 4) and the four partial (max, sum) pairs are
+// merged in LDS; then the 64 x 64 (r, i) tiles are formed, stored row-wise into
+// PT and, through an LDS transpose, into Pm.
 template <typename T>
 __global__ void __launch_bounds__(256) k_phat(const float *__restrict__ LT, const float *__restrict__ beta, int n,
-                                              int t, int64_t tp, int64_t np_, void *__restrict__ out) {
-  const int b = blockIdx.y;
-  const int i = blockIdx.x * 256 + threadIdx.x;
-  if (i >= np_) return;
+                                              int t, int64_t tp, int64_t np_, void *__restrict__ out,
+                                              void *__restrict__ outm) {
+  constexpr int PL = sizeof(T) == 2 ? 2 : 1;
+  __shared__ float smx[4][64], ssum[4][64];
+  __shared__ T sp[PL][64][64 + 8];
+  const int b = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int i0 = blockIdx.x * 64, i = i0 + lane;
   const float *L = LT + (size_t)b * tp * np_ + i;
   const float *bb = beta + (size_t)b * tp;
   float mx = -INFINITY, sum = 0.0f;
   if (i < n)
-    for (int r = 0; r < t; ++r) {
+    for (int r = wave; r < t; r += 4) {
       const float x = L[(size_t)r * np_] + bb[r];
       if (x > mx) {
         sum = sum * expf(mx - x) + 1.0f;
@@ -682,15 +667,50 @@ __global__ void __launch_bounds__(256) k_phat(const float *__restrict__ LT, cons
         sum += expf(x - mx);
       }
     }
-  const float inv = (i < n && sum > 0.0f) ? 1.0f / sum : 0.0f;
-  for (int64_t r = 0; r < tp; ++r) {
-    const float p = (i < n && r < t) ? expf(L[(size_t)r * np_] + bb[r] - mx) * inv : 0.0f;
-    if constexpr (sizeof(T) == 2) {
-      bf16 *o = reinterpret_cast<bf16 *>(out) + (size_t)b * 2 * tp * np_ + (size_t)r * np_ + i;
-      split_bf16(p, o[0], o[tp * np_]);
-    } else {
-      reinterpret_cast<float *>(out)[(size_t)b * tp * np_ + (size_t)r * np_ + i] = p;
+  smx[wave][lane] = mx;
+  ssum[wave][lane] = sum;
+  __syncthreads();
+  float M = fmaxf(fmaxf(smx[0][lane], smx[1][lane]), fmaxf(smx[2][lane], smx[3][lane]));
+  float S = 0.0f;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) S += smx[q][lane] == -INFINITY ? 0.0f : ssum[q][lane] * expf(smx[q][lane] - M);
+  const float inv = (i < n && S > 0.0f) ? 1.0f / S : 0.0f;
+  T *PT = reinterpret_cast<T *>(out) + (size_t)b * PL * tp * np_;
+  T *Pm = reinterpret_cast<T *>(outm) + (size_t)b * PL * tp * np_;
+  constexpr int EPV = 16 / sizeof(T);                     // elements per 16-byte store
+  typedef __attribute__((ext_vector_type(4))) uint32_t u32x4;
+  for (int64_t r0 = 0; r0 < tp; r0 += 64) {
+    __syncthreads();   // the previous tile's stores have read sp
+#pragma unroll 4
+    for (int e = 0; e < 16; ++e) {
+      const int rr = 16 * wave + e;
+      const int64_t r = r0 + rr;
+      const float p = (i < n && r < t) ? expf(L[(size_t)r * np_] + bb[r] - M) * inv : 0.0f;
+      if constexpr (PL == 2) {
+        bf16 hi, lo;
+        split_bf16(p, hi, lo);
+        sp[0][lane][rr] = hi;
+        sp[1][lane][rr] = lo;
+      } else {
+        sp[0][lane][rr] = p;
+      }
     }
+    __syncthreads();
+    // P^T rows r0 + rr, columns i0 .. i0 + 63 (gathered down the tile)
+    for (int e = tid; e < PL * 64 * (64 / EPV); e += 256) {
+      const int q = e / (64 * (64 / EPV)), rr = (e / (64 / EPV)) % 64, c = (e % (64 / EPV)) * EPV;
+      T v[EPV];
+#pragma unroll
+      for (int k = 0; k < EPV; ++k) v[k] = sp[q][c + k][rr];
+      *reinterpret_cast<u32x4 *>(&PT[(size_t)q * tp * np_ + (size_t)(r0 + rr) * np_ + i0 + c]) =
+          *reinterpret_cast<const u32x4 *>(v);
+    }
+    if (outm)   // P rows i0 + row, columns r0 .. r0 + 63
+      for (int e = tid; e < PL * 64 * (64 / EPV); e += 256) {
+        const int q = e / (64 * (64 / EPV)), row = (e / (64 / EPV)) % 64, c = (e % (64 / EPV)) * EPV;
+        *reinterpret_cast<u32x4 *>(&Pm[(size_t)q * np_ * tp + (size_t)(i0 + row) * tp + r0 + c]) =
+            *reinterpret_cast<const u32x4 *>(&sp[q][row][c]);
+      }
   }
 }
 
@@ -912,12 +932,6 @@ __global__ void __launch_bounds__(256) k_values_out(const float *__restrict__ Xp
 }
 
 // ------------------------------------------------------------------ launchers
-hipError_t launch_hvec(const float *LT, const float *z, const float *m, int B, int n, int t, int64_t tp, int64_t np_,
-                       double *h, hipStream_t s) {
-  hipLaunchKernelGGL(k_hvec, dim3((unsigned)(tp / 4), B), dim3(256), 0, s, LT, z, m, n, t, tp, np_, h);
-  return hipGetLastError();
-}
-
 // Ridge + factorisation (+ escalation) of the work copy Gw of Gc.
 hipError_t launch_cholesky(float *Gw, const float *Gc, int B, int t, int64_t ld, float delta0, int max_esc,
                            FitState st, float *dinv, void *lsplit, hipStream_t s) {
@@ -984,22 +998,10 @@ hipError_t launch_trsv(const float *Gw, const float *dinv, int B, int64_t ld, co
 hipError_t launch_mass_residual(const float *LT, const float *z, const float *m, const double *w, const float *lam,
                                 int B, int n, int t, int64_t tp, int64_t np_, double *u, double *res,
                                 const int32_t *info, hipStream_t s) {
-  hipLaunchKernelGGL(k_mass_resid_rows, dim3((unsigned)(np_ / 256), B), dim3(256), 0, s, LT, z, m, w, n, t, tp, np_,
+  hipLaunchKernelGGL(k_mass_resid_rows, dim3((unsigned)(np_ / 64), B), dim3(256), 0, s, LT, z, m, w, n, t, tp, np_,
                      u, info);
   hipLaunchKernelGGL(k_mass_resid_cols, dim3((unsigned)(tp / 4), B), dim3(256), 0, s, LT, z, u, w, lam, n, t, tp,
                      np_, res, info);
-  return hipGetLastError();
-}
-
-// P [B][planes][cols][rows] from PT [B][planes][rows][cols].
-hipError_t launch_transpose_planes(int dtype, const void *PT, void *P, int B, int64_t rows, int64_t cols,
-                                   hipStream_t s) {
-  dim3 grid((unsigned)(cols / 64), (unsigned)(rows / 64), B);
-  if (dtype == ARCKV_BF16)
-    hipLaunchKernelGGL(k_transpose2d<uint16_t>, grid, dim3(256), 0, s, (const uint16_t *)PT, (uint16_t *)P, rows,
-                       cols, 2);
-  else
-    hipLaunchKernelGGL(k_transpose2d<float>, grid, dim3(256), 0, s, (const float *)PT, (float *)P, rows, cols, 1);
   return hipGetLastError();
 }
 
@@ -1011,12 +1013,12 @@ hipError_t launch_bias_finalize(const double *w, int B, int64_t ld, int t, float
 }
 
 hipError_t launch_phat(int dtype, const float *LT, const float *beta_ws, int B, int n, int t, int64_t tp,
-                       int64_t np_, void *out, hipStream_t s) {
-  dim3 grid((unsigned)((np_ + 255) / 256), B);
+                       int64_t np_, void *out, void *outm, hipStream_t s) {
+  dim3 grid((unsigned)(np_ / 64), B);
   if (dtype == ARCKV_BF16)
-    hipLaunchKernelGGL(k_phat<bf16>, grid, dim3(256), 0, s, LT, beta_ws, n, t, tp, np_, out);
+    hipLaunchKernelGGL(k_phat<bf16>, grid, dim3(256), 0, s, LT, beta_ws, n, t, tp, np_, out, outm);
   else
-    hipLaunchKernelGGL(k_phat<float>, grid, dim3(256), 0, s, LT, beta_ws, n, t, tp, np_, out);
+    hipLaunchKernelGGL(k_phat<float>, grid, dim3(256), 0, s, LT, beta_ws, n, t, tp, np_, out, outm);
   return hipGetLastError();
 }
 
