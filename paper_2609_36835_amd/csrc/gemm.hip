@@ -69,11 +69,10 @@ hipError_t launch_rhs_gemm(int dtype, const void *PT, const void *YT, float *Bm,
   g.lda = g.ldb = np_;
   EpiStore e{Bm, tp * kHeadDim, kHeadDim, nullptr, nullptr};
   if (dtype == ARCKV_BF16) {
-    g.a_pair = 2 * tp * np_;
-    g.a_plane = tp * np_;
-    g.b_pair = 2 * (int64_t)kHeadDim * np_;
-    g.b_plane = (int64_t)kHeadDim * np_;
-    return launch_gemm<bf16, 2, 2>(g, (const bf16 *)PT, (const bf16 *)YT, e, s);
+    BigShape g2{P, (int)tp, kHeadDim, (int)np_, 2 * tp * np_, tp * np_, np_, 2 * (int64_t)kHeadDim * np_,
+                (int64_t)kHeadDim * np_, np_, false, (int)(tp / 256)};
+    EpiStoreBig<2, 2> e2{Bm, tp * kHeadDim, kHeadDim, nullptr, nullptr};
+    return launch_gemm_big<4, 2, 2, 2, 32, 2, 2>(g2, (const bf16 *)PT, (const bf16 *)YT, e2, s);
   }
   g.a_pair = tp * np_;
   g.a_plane = 0;
@@ -106,8 +105,10 @@ hipError_t launch_value_residual(int dtype, const void *XT, const void *Pm, cons
   g1.ldb = tp;
   hipError_t e;
   if (split) {
-    EpiValueResid<true> ep{UT, pl * kHeadDim * np_, kHeadDim * np_, (int)np_, n, Y};
-    e = launch_gemm<bf16, 2, 2>(g1, (const bf16 *)XT, (const bf16 *)Pm, ep, s);
+    BigShape gb{P, kHeadDim, (int)np_, (int)tp, pl * kHeadDim * tp, kHeadDim * tp, tp, pl * np_ * tp, np_ * tp, tp,
+                false, 1};
+    EpiValueResidBig<2, 2> ep{(bf16 *)UT, pl * kHeadDim * np_, kHeadDim * np_, (int)np_, n, Y};
+    e = launch_gemm_big<2, 4, 2, 2, 32, 2, 2>(gb, (const bf16 *)XT, (const bf16 *)Pm, ep, s);
   } else {
     EpiValueResid<false> ep{UT, kHeadDim * np_, 0, (int)np_, n, Y};
     e = launch_gemm<float, 1, 1>(g1, (const float *)XT, (const float *)Pm, ep, s);
@@ -127,7 +128,12 @@ hipError_t launch_value_residual(int dtype, const void *XT, const void *Pm, cons
   g2.b_plane = split ? kHeadDim * np_ : 0;
   g2.ldb = np_;
   EpiStore e2{R, tp * kHeadDim, kHeadDim, X, lam};
-  if (split) return launch_gemm<bf16, 2, 2>(g2, (const bf16 *)PT, (const bf16 *)UT, e2, s);
+  if (split) {
+    BigShape gb{P, (int)tp, kHeadDim, (int)np_, pl * tp * np_, tp * np_, np_, pl * kHeadDim * np_, kHeadDim * np_, np_,
+                false, (int)(tp / 256)};
+    EpiStoreBig<2, 2> eb{R, tp * kHeadDim, kHeadDim, X, lam};
+    return launch_gemm_big<4, 2, 2, 2, 32, 2, 2>(gb, (const bf16 *)PT, (const bf16 *)UT, eb, s);
+  }
   return launch_gemm<float, 1, 1>(g2, (const float *)PT, (const float *)UT, e2, s);
 }
 

@@ -276,6 +276,70 @@ struct EpiSymBig {
   }
 };
 
+// out[r][c] = acc (minus lam[p] X[r][c] when X is given), fp32 [P][rows][ld].
+template <int TM, int TN>
+struct EpiStoreBig {
+  float *out;
+  int64_t pair_stride;
+  int ld;
+  const float *X;      // nullptr: plain store
+  const float *lam;    // [P]
+  __device__ __forceinline__ void operator()(f32x16 (&acc)[TM][TN], int p, int row0, int col0, int, int, int lane,
+                                             int, int) const {
+    const size_t base = (size_t)p * pair_stride;
+    const int col = lane & 31;
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        const int c = col0 + 32 * j + col;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int r = row0 + 32 * i + acc_row(v, lane);
+          const size_t o = base + (size_t)r * ld + c;
+          float val = acc[i][j][v];
+          if (X) val -= lam[p] * X[o];
+          out[o] = val;
+        }
+      }
+  }
+};
+
+// U^T[c][q] = Y[q][c] - acc[c][q] (rows c < 128, columns queries q; zero for
+// q >= n), stored as bf16 hi/lo planes [P][2][128][ld].
+template <int TM, int TN>
+struct EpiValueResidBig {
+  bf16 *out;
+  int64_t pair_stride, plane_stride;   // elements
+  int ld, n;
+  const float *Y;                      // [P][n][128]
+  __device__ __forceinline__ void operator()(f32x16 (&acc)[TM][TN], int p, int row0, int col0, int, int, int lane,
+                                             int, int) const {
+    const int h = lane >> 5, col = lane & 31;
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        const int q = col0 + 32 * j + col;
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int c0 = row0 + 32 * i + 8 * g + 4 * h;
+          f32x4 y = {0.f, 0.f, 0.f, 0.f};
+          if (q < n) y = *reinterpret_cast<const f32x4 *>(Y + ((size_t)p * n + q) * kHeadDim + c0);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float u = q < n ? y[e] - acc[i][j][4 * g + e] : 0.0f;
+            const size_t o = (size_t)p * pair_stride + (size_t)(c0 + e) * ld + q;
+            bf16 hi, lo;
+            split_bf16(u, hi, lo);
+            out[o] = hi;
+            out[o + plane_stride] = lo;
+          }
+        }
+      }
+  }
+};
+
 template <int WM, int WN, int TM, int TN, int BK, int NA, int NB, class Epi>
 hipError_t launch_gemm_big(const BigShape &g, const bf16 *A, const bf16 *B, const Epi &epi, hipStream_t s) {
   using C = BigCfg<WM, WN, TM, TN, BK, NA, NB>;
