@@ -193,8 +193,20 @@ __global__ void __launch_bounds__(256) k_expgen(const T *__restrict__ Q, const v
 // barrier guards the staging.
 typedef __attribute__((address_space(3))) void eg_lds_t;
 
+// LDS of k_expgen_bf16: two Q stages of 64 rows (16 KB each), four wave-private
+// staging areas of 32 rows (bf16 rows of 64 + 8 in profile mode, fp32 rows of
+// 64 + 4 in phic mode), and in phic mode z_i and m_i of both Q stages.
 template <int MODE>
-__global__ void __launch_bounds__(256) k_expgen_bf16(const bf16 *__restrict__ Q, const bf16 *__restrict__ Bsrc,
+constexpr int eg_stage_bytes() {
+  return MODE == MODE_PHIC ? 32 * (64 + 4) * 4 : 32 * (64 + 8) * 2;
+}
+template <int MODE>
+constexpr size_t eg_lds_bytes() {
+  return 2 * 64 * kHeadDim * 2 + 4 * eg_stage_bytes<MODE>() + (MODE == MODE_PHIC ? 2 * 2 * 64 * 4 : 0);
+}
+
+template <int MODE>
+__global__ void __launch_bounds__(256, 2) k_expgen_bf16(const bf16 *__restrict__ Q, const bf16 *__restrict__ Bsrc,
                                                      int64_t b_pair_stride, int64_t b_plane_stride, int b_rows,
                                                      const float *__restrict__ shift, bf16 *__restrict__ out,
                                                      int64_t out_pair_stride, int64_t out_plane_stride,
@@ -208,9 +220,14 @@ __global__ void __launch_bounds__(256) k_expgen_bf16(const bf16 *__restrict__ Q,
   constexpr int QB = 64 * kHeadDim * 2;                   // one Q stage (16 KB)
   // staging: bf16 rows of 64 + 8 (profile) or fp32 rows of 64 + 4 (phic)
   constexpr int SO_F = 64 + 4, SO_H = 64 + 8;
-  constexpr int STG = MODE == MODE_PHIC ? 32 * SO_F * 4 : 32 * SO_H * 2;
-  __shared__ __attribute__((aligned(1024))) char sQ[2 * QB];
-  __shared__ __attribute__((aligned(16))) char sOut[4 * STG];
+  constexpr int STG = eg_stage_bytes<MODE>();
+  // Dynamic LDS (eg_lds_bytes<MODE>): two Q stages, four wave-private output
+  // staging areas, and in phic mode z_i and m_i of both Q stages.  A dynamic
+  // array also keeps the compiler from waiting for every direct-to-LDS load
+  // in flight before each LDS read, which would serialise the prefetch.
+  extern __shared__ __attribute__((aligned(1024))) char eg_smem[];
+  char *sQ = eg_smem, *sOut = eg_smem + 2 * QB;
+  float *sZ = reinterpret_cast<float *>(sOut + 4 * STG), *sM = sZ + 128;   // [stage][64]
 
   const int b = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int h = lane >> 5, col = lane & 31;
@@ -230,7 +247,11 @@ __global__ void __launch_bounds__(256) k_expgen_bf16(const bf16 *__restrict__ Q,
   const float zs2 = MODE == MODE_PROFILE ? shift[b] * 1.4426950408889634f : 0.0f;
   float rowsum = 0.0f, sumsq = 0.0f;
   double hsum = 0.0;   // PHIC: h_r = sum_i Phi[i][r] m_i (when hout is given)
-  int dest = -1;   // profile: >= 0 compacted E^T row, <= -2 anchor -(r + 2), -1 none
+  // profile: >= 0 compacted E^T row, <= -2 anchor -(r + 2).  Padding keys
+  // j >= T write their (zero) rows to row j - t >= T - t, past the rows of the
+  // real keys (those rows only feed assignment columns that are never read), so
+  // every lane stores unconditionally and the per-tile store count is fixed.
+  int dest = row - t;
   if (MODE == MODE_PROFILE && rvalid) {
     const int32_t *S = anchors + (size_t)b * t;
     int lo = 0, hi = t;
@@ -253,13 +274,19 @@ __global__ void __launch_bounds__(256) k_expgen_bf16(const bf16 *__restrict__ Q,
       __builtin_amdgcn_global_load_lds((const void *)src, (eg_lds_t *)(sQ + st * QB + (4 * wave + u) * 1024), 16,
                                        0, 0);
     }
+    // phic: the stage's z_i (and m_i) ride along, so the loop body issues no
+    // vector-memory loads of its own
+    if (MODE == MODE_PHIC && wave == 0) {
+      const size_t iq = (size_t)b * n + min(i0 + lane, n - 1);
+      if (shift) __builtin_amdgcn_global_load_lds((const void *)(shift + iq), (eg_lds_t *)(sZ + 64 * st), 4, 0, 0);
+      if (hout) __builtin_amdgcn_global_load_lds((const void *)(mvec + iq), (eg_lds_t *)(sM + 64 * st), 4, 0, 0);
+    }
   };
   char *so = sOut + wave * STG;
   auto wave_fence = [] { asm volatile("" ::: "memory"); };
   const int row0 = blockIdx.x * 128 + wave * 32;
   auto row_dst = [&](int rr, int i0) -> bf16 * {
     const int d = __shfl(dest, rr, 64);
-    if (d == -1) return nullptr;
     bf16 *base = d >= 0 ? out + (size_t)b * out_pair_stride + (size_t)d * n_pad
                         : uout + ((size_t)b * tp + (size_t)(-d - 2)) * n_pad;
     return base + i0;
@@ -281,8 +308,7 @@ __global__ void __launch_bounds__(256) k_expgen_bf16(const bf16 *__restrict__ Q,
     for (int pass = 0; pass < 4; ++pass) {             // 32 rows x 8 chunks of 16 B
       const int chunk = pass * 64 + lane, r = chunk / 8, c8 = (chunk % 8) * 8;
       bf16 *dst = routed ? row_dst(r, i0) : dst_base + (size_t)r * n_pad;
-      const bf16x8 w = *reinterpret_cast<const bf16x8 *>(&sb[r * SO_H + c8]);
-      if (dst) *reinterpret_cast<bf16x8 *>(dst + c8) = w;
+      *reinterpret_cast<bf16x8 *>(dst + c8) = *reinterpret_cast<const bf16x8 *>(&sb[r * SO_H + c8]);
     }
     wave_fence();
   };
@@ -304,6 +330,8 @@ __global__ void __launch_bounds__(256) k_expgen_bf16(const bf16 *__restrict__ Q,
   };
 
   const int ntile = n_pad / 64;
+  // without z (logits only) the shift is zero; the stages stay zero-filled
+  if (MODE == MODE_PHIC && !shift && tid < 128) sZ[tid] = 0.0f;
   issue_q(0, 0);
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
@@ -332,19 +360,21 @@ __global__ void __launch_bounds__(256) k_expgen_bf16(const bf16 *__restrict__ Q,
           const float stored = (float)(bf16)val[ms][vv];
           sumsq = fmaf(stored, stored, sumsq);
         } else {
+          // evaluated on every lane (masked lanes see finite inputs), then
+          // selected, so the exponential stays free of branches
           lg[ms][vv] = ok ? acc[vv] * scale : 0.0f;
-          // shift (the row maxima z) is null when only the logits are wanted
-          val[ms][vv] = ok ? expf(lg[ms][vv] - (shift ? shift[(size_t)b * n + i] : 0.0f)) : 0.0f;
-          if (hout && ok) hsum += (double)val[ms][vv] * (double)mvec[(size_t)b * n + i];
+          const float e = expf(lg[ms][vv] - sZ[64 * st + 32 * ms + acc_row(vv, lane)]);
+          val[ms][vv] = ok ? e : 0.0f;
         }
       }
     }
-    // the next Q stage has landed (this wave's loads, and every wave's after
-    // the barrier), and every wave is done reading stage st
-    __builtin_amdgcn_s_waitcnt(0);
-    asm volatile("" ::: "memory");
-    __builtin_amdgcn_s_barrier();
-    asm volatile("" ::: "memory");
+    if (MODE == MODE_PHIC && hout) {   // masked entries of val are zero
+#pragma unroll
+      for (int ms = 0; ms < 2; ++ms)
+#pragma unroll
+        for (int vv = 0; vv < 16; ++vv)
+          hsum += (double)val[ms][vv] * (double)sM[64 * st + 32 * ms + acc_row(vv, lane)];
+    }
     if constexpr (MODE == MODE_PROFILE) {
       flush_bf16(val, 0, nullptr, true, i0);
     } else {
@@ -353,6 +383,16 @@ __global__ void __launch_bounds__(256) k_expgen_bf16(const bf16 *__restrict__ Q,
       flush_bf16(val, 2, o + out_plane_stride, false, i0);
       flush_f32(lg, aux + (size_t)b * aux_pair_stride + (size_t)row0 * n_pad + i0);
     }
+    // The next Q stage has landed: it was issued before this tile's stores (4
+    // per lane in profile mode, 4 + 4 + 8 in phic mode, all unconditional) and
+    // the vector-memory counter retires in issue order, so waiting until only
+    // the stores may be outstanding suffices.  After the barrier every wave's
+    // share has landed and every wave is done reading stage st.
+    if constexpr (MODE == MODE_PROFILE) __builtin_amdgcn_s_waitcnt(4 | (7 << 4) | (15 << 8));        // vmcnt(4)
+    else __builtin_amdgcn_s_waitcnt(0 | (1 << 14) | (7 << 4) | (15 << 8));                            // vmcnt(16)
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
   }
   if (MODE == MODE_PROFILE) {
     rowsum += __shfl_xor(rowsum, 32, 64);
@@ -369,16 +409,24 @@ __global__ void __launch_bounds__(256) k_expgen_bf16(const bf16 *__restrict__ Q,
 // Compacted E^T [B][Tp][np] (rows of the non-anchor keys; T = bf16 or
 // float), unnormalised anchor profiles U [B][tp][np] with their sums of
 // squares ssq [B][tp], and phi [B][T].
+template <int MODE>
+static hipError_t eg_set_lds() {
+  return hipFuncSetAttribute((const void *)k_expgen_bf16<MODE>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                             (int)eg_lds_bytes<MODE>());
+}
+
 hipError_t launch_profiles(int dtype, const void *Q, const void *K, const float *zmerge, const int32_t *anchors,
                            int t, void *Et, void *U, float *ssq, float *phi, int B, int T, int n, int64_t Tp,
                            int64_t tp, int64_t np_, float scale, hipStream_t s) {
   dim3 grid(Tp / 128, B);
-  if (dtype == ARCKV_BF16)
-    hipLaunchKernelGGL((k_expgen_bf16<MODE_PROFILE>), grid, dim3(256), 0, s, (const bf16 *)Q, (const bf16 *)K,
+  if (dtype == ARCKV_BF16) {
+    hipError_t e = eg_set_lds<MODE_PROFILE>();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((k_expgen_bf16<MODE_PROFILE>), grid, dim3(256), eg_lds_bytes<MODE_PROFILE>(), s, (const bf16 *)Q, (const bf16 *)K,
                        (int64_t)T * kHeadDim, (int64_t)0, T, zmerge, (bf16 *)Et, Tp * np_, (int64_t)0, phi,
                        (int64_t)T, n, (int)np_, scale, anchors, t, (bf16 *)U, ssq, tp, (const float *)nullptr,
                        (double *)nullptr);
-  else
+  } else
     hipLaunchKernelGGL((k_expgen<float, MODE_PROFILE>), grid, dim3(256), 0, s, (const float *)Q, K,
                        (int64_t)T * kHeadDim, (int64_t)0, T, zmerge, Et, Tp * np_, (int64_t)0, phi, (int64_t)T,
                        n, (int)np_, scale, anchors, t, U, ssq, tp, (const float *)nullptr, (double *)nullptr);
@@ -390,12 +438,15 @@ hipError_t launch_profiles(int dtype, const void *Q, const void *K, const float 
 hipError_t launch_phic(int dtype, const void *Q, const void *Ckp, const float *z, void *PhiT, float *LT,
                        const float *m, double *h, int B, int t, int n, int64_t tp, int64_t np_, float scale,
                        hipStream_t s) {
+  if (h && !m) return hipErrorInvalidValue;   // h = Phi_C^T m needs m
   dim3 grid(tp / 128, B);
-  if (dtype == ARCKV_BF16)
-    hipLaunchKernelGGL((k_expgen_bf16<MODE_PHIC>), grid, dim3(256), 0, s, (const bf16 *)Q, (const bf16 *)Ckp,
+  if (dtype == ARCKV_BF16) {
+    hipError_t e = eg_set_lds<MODE_PHIC>();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((k_expgen_bf16<MODE_PHIC>), grid, dim3(256), eg_lds_bytes<MODE_PHIC>(), s, (const bf16 *)Q, (const bf16 *)Ckp,
                        2 * tp * kHeadDim, tp * kHeadDim, t, z, (bf16 *)PhiT, 2 * tp * np_, tp * np_, LT, tp * np_,
                        n, (int)np_, scale, (const int32_t *)nullptr, 0, (bf16 *)nullptr, (float *)nullptr, tp, m, h);
-  else
+  } else
     hipLaunchKernelGGL((k_expgen<float, MODE_PHIC>), grid, dim3(256), 0, s, (const float *)Q, Ckp,
                        tp * kHeadDim, (int64_t)0, t, z, PhiT, tp * np_, (int64_t)0, LT, tp * np_, n, (int)np_,
                        scale, (const int32_t *)nullptr, 0, (void *)nullptr, (float *)nullptr, tp, m, h);
