@@ -258,32 +258,44 @@ __global__ void __launch_bounds__(512, 1) k_rowstats_bf16(const bf16 *__restrict
         accS[ms] = Mfma<bf16>::mma(a, qf[ks], accS[ms]);
       }
     }
+    if (k0 + kRsK > Tn) {   // last tile: keys past Tn get no weight
+#pragma unroll
+      for (int ms = 0; ms < 2; ++ms)
+#pragma unroll
+        for (int v = 0; v < 16; ++v)
+          if (k0 + 32 * ms + acc_row(v, lane) >= Tn) accS[ms][v] = -INFINITY;
+    }
     float bmax = -INFINITY;
 #pragma unroll
     for (int ms = 0; ms < 2; ++ms)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        if (k0 + 32 * ms + acc_row(v, lane) >= Tn) accS[ms][v] = -INFINITY;
-        bmax = fmaxf(bmax, accS[ms][v]);
-      }
+      for (int v = 0; v < 16; ++v) bmax = fmaxf(bmax, accS[ms][v]);
     bmax = fmaxf(bmax, __shfl_xor(bmax, 32, 64));
     const float new_max = fmaxf(run_max, bmax);
-    const float alpha = exp2f((run_max - new_max) * c2);
+    // The accumulators are rescaled only when some row's maximum grew (rare
+    // after the first tiles); unchanged rows take alpha = 1.  The exponentials
+    // are the hardware base-2 ones: arguments are <= 0 and a result below the
+    // smallest normal float is negligible next to the running sum (>= 1).
+    if (__ballot(new_max > run_max)) {
+      const float alpha = __builtin_amdgcn_exp2f((run_max - new_max) * c2);
+      run_sum *= alpha;
+#pragma unroll
+      for (int cs = 0; cs < 4; ++cs)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) accY[cs][v] *= alpha;
+    }
     run_max = new_max;
+    const float mc2 = new_max * c2;
     float psum = 0.0f;
 #pragma unroll
     for (int ms = 0; ms < 2; ++ms)
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
-        const float p = exp2f((accS[ms][v] - new_max) * c2);
+        const float p = __builtin_amdgcn_exp2f(fmaf(accS[ms][v], c2, -mc2));
         accS[ms][v] = p;
         psum += p;
       }
-    run_sum = run_sum * alpha + psum;
-#pragma unroll
-    for (int cs = 0; cs < 4; ++cs)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) accY[cs][v] *= alpha;
+    run_sum += psum;
 #pragma unroll
     for (int kk = 0; kk < kRsK / 16; ++kk) {
       const int ms = kk >> 1, base = 8 * (kk & 1);
