@@ -24,8 +24,7 @@ struct FitState {
 
 hipError_t launch_score(int dtype, const void *K, const void *V, const void *W1, const float *b1, const float *w2,
                         const float *b2, float *scores, int B, int T, hipStream_t s);
-hipError_t launch_select(const float *scores, int B, int T, int t, int32_t *anchors, int32_t *anchor_of,
-                         hipStream_t s);
+hipError_t launch_select(const float *scores, int B, int T, int t, int32_t *anchors, hipStream_t s);
 hipError_t launch_rowstats(int dtype, const void *K, const void *V, const void *Q, float *z, float *m, float *Y,
                            int B, int T, int n, float scale, hipStream_t s);
 hipError_t launch_profiles(int dtype, const void *Q, const void *K, const float *zmerge, const int32_t *anchors,
@@ -35,11 +34,10 @@ hipError_t launch_phic(int dtype, const void *Q, const void *Ckp, const float *z
                        const float *m, double *h, int B, int t, int n, int64_t tp, int64_t np_, float scale,
                        hipStream_t s);
 hipError_t launch_zmax(const float *z, int B, int n, float *zmax, hipStream_t s);
-hipError_t launch_anchor_of(const int32_t *anchors, int B, int T, int t, int32_t *anchor_of, hipStream_t s);
 hipError_t launch_anchor_profiles(int dtype, void *U, const float *ssq, int B, int t, int64_t np_, int64_t tp,
                                   hipStream_t s);
-hipError_t launch_assign_finalize(const uint64_t *part, int MT, int64_t Np, const int32_t *anchor_of,
-                                  const int32_t *anchors, int B, int T, int t, int32_t *kappa, hipStream_t s);
+hipError_t launch_assign_finalize(const uint64_t *part, int MT, int64_t Np, const int32_t *anchors, int B, int T,
+                                  int t, int32_t *kappa, hipStream_t s);
 hipError_t launch_group_merge(int dtype, const void *K, const float *phi, const int32_t *kappa,
                               const int32_t *anchors, int B, int T, int t, int64_t tp, float lambda,
                               int32_t *offsets, int32_t *cursor, int32_t *perm, float *Ck, void *Ckp, hipStream_t s);
@@ -162,7 +160,7 @@ struct Bump {
 // Persistent per-pair arrays ([B]-sized) followed by a chunk region for P pairs.
 struct Plan {
   // persistent
-  int64_t scores, z, m, Y, zmax, anchor_of, kappa, phi, beta_ws, info_g, info_a, st_g, st_a;
+  int64_t scores, z, m, Y, zmax, kappa, phi, beta_ws, info_g, info_a, st_g, st_a;
   int64_t persistent_bytes;
   // chunk region (offsets relative to chunk base)
   int64_t Ckp;
@@ -180,7 +178,6 @@ static Plan make_plan(const Dims &d, int64_t P) {
   pl.m = a.take(B * d.n * 4);
   pl.Y = a.take(B * d.n * kHeadDimH * 4);
   pl.zmax = a.take(B * 4);
-  pl.anchor_of = a.take(B * d.T * 4);
   pl.kappa = a.take(B * d.T * 4);
   pl.phi = a.take(B * d.T * 4);
   pl.beta_ws = a.take(B * d.tp * 4);
@@ -301,10 +298,10 @@ struct Ctx {
   int64_t in_esz() const { return d.dtype == ARCKV_BF16 ? 2 : 4; }
 };
 
-// Merge stage for pairs [b0, b0+P): needs zmax and anchor_of for those pairs.
+// Merge stage for pairs [b0, b0+P): needs zmax for those pairs.
 static arckv_status run_merge_chunk(const Ctx &c, int b0, int P, const void *K, const void *Q,
                                     const int32_t *anchors, float lambda_m, float *Ck, int32_t *kappa, float *phi,
-                                    const float *zmax, const int32_t *anchor_of) {
+                                    const float *zmax) {
   const Dims &d = c.d;
   hipStream_t stream = c.stream;
   const char *Kc = (const char *)K + (size_t)b0 * d.T * kHeadDimH * c.in_esz();
@@ -321,8 +318,7 @@ static arckv_status run_merge_chunk(const Ctx &c, int b0, int P, const void *K, 
   STAGE(ST_ANCHOR_PROF, launch_anchor_profiles(d.dtype, U, ssq, P, d.t, d.np_, d.tp, stream));
   STAGE(ST_ASSIGN, launch_assign_gemm(d.dtype, U, Et, part, P, d.t, d.tp, Tc, d.Tp, d.np_, stream));
   const int mt_used = (int)(d.dtype == ARCKV_BF16 ? d.tp / 256 : d.tp / 128);
-  STAGE(ST_FINALIZE, launch_assign_finalize(part, mt_used, Tc, anchor_of + (size_t)b0 * d.T, anc, P, d.T, d.t,
-                                            kappa + (size_t)b0 * d.T, stream));
+  STAGE(ST_FINALIZE, launch_assign_finalize(part, mt_used, Tc, anc, P, d.T, d.t, kappa + (size_t)b0 * d.T, stream));
   STAGE(ST_MERGE, launch_group_merge(d.dtype, Kc, phi + (size_t)b0 * d.T, kappa + (size_t)b0 * d.T, anc, P, d.T,
                                      d.t, d.tp, lambda_m, c.chunk<int32_t>(c.pl.offsets),
                                      c.chunk<int32_t>(c.pl.cursor), c.chunk<int32_t>(c.pl.perm),
@@ -492,7 +488,7 @@ arckv_status arckv_select(const arckv_problem *prob, const float *scores, int32_
   if (!scores || !anchors || t < 1 || t > prob->T) return ARCKV_ERR_INVALID_ARG;
   (void)ws;
   (void)ws_bytes;
-  STAGE(ST_SELECT, launch_select(scores, prob->B, prob->T, t, anchors, nullptr, stream));
+  STAGE(ST_SELECT, launch_select(scores, prob->B, prob->T, t, anchors, stream));
   return ARCKV_OK;
 }
 
@@ -522,14 +518,12 @@ arckv_status arckv_merge(const arckv_problem *prob, const void *K, const void *Q
   c.scale = eff_scale(prob);
   c.stream = stream;
   float *zmax = c.pers<float>(c.pl.zmax);
-  int32_t *anchor_of = c.pers<int32_t>(c.pl.anchor_of);
   int32_t *kappa = assign ? assign : c.pers<int32_t>(c.pl.kappa);
   float *phiw = phi ? phi : c.pers<float>(c.pl.phi);
   STAGE(ST_ZMAX, launch_zmax(z, c.d.B, c.d.n, zmax, stream));
-  if (launch_anchor_of(anchors, c.d.B, c.d.T, t, anchor_of, stream) != hipSuccess) return ARCKV_ERR_HIP;
   for (int b0 = 0; b0 < c.d.B; b0 += (int)P) {
     const int Pc = (int)(c.d.B - b0 < P ? c.d.B - b0 : P);
-    CHECK(run_merge_chunk(c, b0, Pc, K, Q_ref, anchors, lambda_m, C_k, kappa, phiw, zmax, anchor_of));
+    CHECK(run_merge_chunk(c, b0, Pc, K, Q_ref, anchors, lambda_m, C_k, kappa, phiw, zmax));
   }
   return ARCKV_OK;
 }
@@ -636,14 +630,14 @@ arckv_status arckv_compact(const arckv_problem *prob, const void *K, const void 
   float *scores = c.pers<float>(c.pl.scores);
   float *z = c.pers<float>(c.pl.z), *m = c.pers<float>(c.pl.m), *Y = c.pers<float>(c.pl.Y);
   float *zmax = c.pers<float>(c.pl.zmax), *phi = c.pers<float>(c.pl.phi);
-  int32_t *anchor_of = c.pers<int32_t>(c.pl.anchor_of), *kappa = c.pers<int32_t>(c.pl.kappa);
+  int32_t *kappa = c.pers<int32_t>(c.pl.kappa);
   STAGE(ST_SCORE, launch_score(d.dtype, K, V, ix->W1, ix->b1, ix->w2, ix->b2, scores, d.B, d.T, stream));
-  STAGE(ST_SELECT, launch_select(scores, d.B, d.T, t, anchors, anchor_of, stream));
+  STAGE(ST_SELECT, launch_select(scores, d.B, d.T, t, anchors, stream));
   STAGE(ST_ROWSTATS, launch_rowstats(d.dtype, K, V, Q_ref, z, m, Y, d.B, d.T, d.n, c.scale, stream));
   STAGE(ST_ZMAX, launch_zmax(z, d.B, d.n, zmax, stream));
   for (int b0 = 0; b0 < d.B; b0 += (int)P) {
     const int Pc = (int)(d.B - b0 < P ? d.B - b0 : P);
-    CHECK(run_merge_chunk(c, b0, Pc, K, Q_ref, anchors, p->lambda_m, C_k, kappa, phi, zmax, anchor_of));
+    CHECK(run_merge_chunk(c, b0, Pc, K, Q_ref, anchors, p->lambda_m, C_k, kappa, phi, zmax));
     CHECK(run_fit_bias_chunk(c, b0, Pc, Q_ref, z, m, *p, beta, fit_state(c, c.pl.st_g, c.pl.info_g, b0)));
     CHECK(run_fit_values_chunk(c, b0, Pc, Y, *p, C_v, fit_state(c, c.pl.st_a, c.pl.info_a, b0)));
   }

@@ -2,7 +2,6 @@
 //
 //  k_zmax            z_merge = max_i z_i (the global logit maximum equals the
 //                    largest full-cache row maximum, eq. response_profile)
-//  k_anchor_of       position -> anchor slot (or -1)
 //  k_anchor_profiles U_S rows: E^T[s_r] / ||E^T[s_r]|| (anchor response profiles),
 //                    normalising the rows the profile pass wrote
 //  k_assign_finalize kappa_j from the per-tile packed argmax; anchors map to
@@ -26,20 +25,6 @@ __global__ void __launch_bounds__(256) k_zmax(const float *__restrict__ z, int n
   if (tid == 0) zmax[b] = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
 }
 
-__global__ void __launch_bounds__(256) k_anchor_of(const int32_t *__restrict__ anchors, int T, int t,
-                                                   int32_t *__restrict__ anchor_of) {
-  const int b = blockIdx.y;
-  const int j = blockIdx.x * 256 + threadIdx.x;
-  if (j < T) anchor_of[(size_t)b * T + j] = -1;
-}
-
-__global__ void __launch_bounds__(256) k_anchor_scatter(const int32_t *__restrict__ anchors, int T, int t,
-                                                        int32_t *__restrict__ anchor_of) {
-  const int b = blockIdx.y;
-  const int r = blockIdx.x * 256 + threadIdx.x;
-  if (r < t) anchor_of[(size_t)b * T + anchors[(size_t)b * t + r]] = r;
-}
-
 // One wave per anchor row: U_S[r][i] = E^T[s_r][i] / ||E^T[s_r][:]||, in place
 // on the unnormalised rows the profile pass wrote (ssq[r] = sum of squares of
 // the stored values); rows r >= t are zero.
@@ -61,23 +46,22 @@ __global__ void __launch_bounds__(256) k_anchor_profiles(T *__restrict__ U, cons
 
 // kappa_j: anchors map to themselves; any other key takes the best packed
 // (similarity, lowest r) over the M-tiles at its compacted column
-// j - #{anchors < j}.
+// j - #{anchors < j}.  Both come from one binary search of the ascending anchors.
 __global__ void __launch_bounds__(256) k_assign_finalize(const uint64_t *__restrict__ part, int MT, int64_t Np,
-                                                         const int32_t *__restrict__ anchor_of,
                                                          const int32_t *__restrict__ anchors, int T, int t,
                                                          int32_t *__restrict__ kappa) {
   const int b = blockIdx.y;
   const int j = blockIdx.x * 256 + threadIdx.x;
   if (j >= T) return;
-  int32_t a = anchor_of[(size_t)b * T + j];
-  if (a < 0) {
-    const int32_t *S = anchors + (size_t)b * t;
-    int lo = 0, hi = t;
-    while (lo < hi) {
-      const int mid = (lo + hi) >> 1;
-      if (S[mid] < j) lo = mid + 1;
-      else hi = mid;
-    }
+  const int32_t *S = anchors + (size_t)b * t;
+  int lo = 0, hi = t;   // lo = #{anchors < j}
+  while (lo < hi) {
+    const int mid = (lo + hi) >> 1;
+    if (S[mid] < j) lo = mid + 1;
+    else hi = mid;
+  }
+  int32_t a = lo;
+  if (lo >= t || S[lo] != j) {
     uint64_t best = 0;
     const uint64_t *pp = part + (size_t)b * MT * Np + (j - lo);
     for (int mt = 0; mt < MT; ++mt) {
@@ -199,11 +183,6 @@ hipError_t launch_zmax(const float *z, int B, int n, float *zmax, hipStream_t s)
   return hipGetLastError();
 }
 
-hipError_t launch_anchor_of(const int32_t *anchors, int B, int T, int t, int32_t *anchor_of, hipStream_t s) {
-  hipLaunchKernelGGL(k_anchor_of, dim3((T + 255) / 256, B), dim3(256), 0, s, anchors, T, t, anchor_of);
-  hipLaunchKernelGGL(k_anchor_scatter, dim3((t + 255) / 256, B), dim3(256), 0, s, anchors, T, t, anchor_of);
-  return hipGetLastError();
-}
 
 hipError_t launch_anchor_profiles(int dtype, void *U, const float *ssq, int B, int t, int64_t np_, int64_t tp,
                                   hipStream_t s) {
@@ -215,10 +194,10 @@ hipError_t launch_anchor_profiles(int dtype, void *U, const float *ssq, int B, i
   return hipGetLastError();
 }
 
-hipError_t launch_assign_finalize(const uint64_t *part, int MT, int64_t Np, const int32_t *anchor_of,
-                                  const int32_t *anchors, int B, int T, int t, int32_t *kappa, hipStream_t s) {
-  hipLaunchKernelGGL(k_assign_finalize, dim3((T + 255) / 256, B), dim3(256), 0, s, part, MT, Np, anchor_of, anchors,
-                     T, t, kappa);
+hipError_t launch_assign_finalize(const uint64_t *part, int MT, int64_t Np, const int32_t *anchors, int B, int T,
+                                  int t, int32_t *kappa, hipStream_t s) {
+  hipLaunchKernelGGL(k_assign_finalize, dim3((T + 255) / 256, B), dim3(256), 0, s, part, MT, Np, anchors, T, t,
+                     kappa);
   return hipGetLastError();
 }
 

@@ -1,11 +1,22 @@
 // Top-t anchor selection, S = TopK(scores, t) per pair (Section 3.3).
 //
-// One workgroup per pair.  Scores become order-preserving uint32 keys
-// (score_key).  A 4-pass, 8-bit radix select finds the key K* of the t-th
-// largest element and how many elements equal to K* must be kept; a final
-// pass over positions in ascending order keeps every key > K* and the
-// lowest-indexed ties, using ballot prefix sums, so the output is ascending and
-// bit-exact.
+// One workgroup of 1024 threads per pair.  Scores become order-preserving
+// uint32 keys (score_key).  Lane l of wave w owns the KPT consecutive positions
+// starting at (64 w + l) KPT, so positions ascend with (wave, lane, i).  When
+// T <= 32768 the keys are read once, coalesced, through a padded LDS copy and
+// then stay in registers; longer caches re-read them from memory (L2) on every
+// pass.
+//
+// A 3-pass radix select (digits of 11, 11 and 10 bits from the top) finds the
+// key K* of the t-th largest element and how many elements equal to K* must be
+// kept (the lowest positions win ties): each pass histograms the keys that
+// match the digits found so far, and a block-wide suffix scan over the bins
+// picks the next digit.  The leading digit is wide because real-valued scores
+// share their sign and leading exponent bits; a narrow one would send almost
+// every key to a handful of bins, and same-address LDS atomics serialise.
+// One block scan of the per-lane (greater, equal) counts then gives every lane
+// its output offset, and each lane writes its selected positions in order, so
+// the output is ascending and bit-exact.
 #include "common.hpp"
 
 namespace arckv {
@@ -13,84 +24,137 @@ namespace arckv {
 namespace {
 constexpr int kSelThreads = 1024;
 constexpr int kSelWaves = kSelThreads / 64;
-}
+constexpr int kSelBins = 2048;   // widest digit: 11 bits
+constexpr int kSelPasses = 3;
 
+// Digit p of the key (from the top): bits [shift, shift + width).
+__device__ inline int sel_shift(int p) { return p == 0 ? 21 : p == 1 ? 10 : 0; }
+__device__ inline int sel_width(int p) { return p == 2 ? 10 : 11; }
+
+// Inclusive prefix sum over the 64 lanes of a wave.
+__device__ inline uint32_t wave_incl_scan(uint32_t v, int lane) {
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const uint32_t o = __shfl_up(v, off, 64);
+    v += lane >= off ? o : 0u;
+  }
+  return v;
+}
+}  // namespace
+
+// KPT: keys per lane held in registers (T <= 1024 KPT); 0 = read from memory.
+template <int KPT>
 __global__ void __launch_bounds__(kSelThreads) k_select_topt(const float *__restrict__ scores, int T, int t,
-                                                             int32_t *__restrict__ anchors,
-                                                             int32_t *__restrict__ anchor_of) {
-  __shared__ uint32_t hist[kSelWaves][256];
+                                                             int32_t *__restrict__ anchors) {
+  extern __shared__ uint32_t sel_keys[];   // [T + T/32] padded key copy (KPT > 0)
+  __shared__ uint32_t hist[kSelBins];
+  __shared__ uint32_t s_wtot[2][kSelWaves];
   __shared__ uint32_t s_prefix, s_remaining;
-  __shared__ uint32_t wave_tot[2][kSelWaves];
   const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const float *s = scores + (size_t)b * T;
-  uint32_t prefix = 0, mask = 0, remaining = (uint32_t)t;
-  for (int shift = 24; shift >= 0; shift -= 8) {
-    for (int i = tid; i < kSelWaves * 256; i += kSelThreads) (&hist[0][0])[i] = 0;
+  const int per = KPT > 0 ? KPT : (T + kSelThreads - 1) / kSelThreads;   // positions per lane
+  const int p0 = tid * per;
+  uint32_t kr[KPT > 0 ? KPT : 1];
+  if constexpr (KPT > 0) {
+    // position p lives at LDS word p + p / 32, so both the coalesced fill and
+    // the per-lane reads of 32 consecutive positions are free of bank conflicts
+    for (int p = tid; p < T; p += kSelThreads) sel_keys[p + (p >> 5)] = score_key(s[p]);
     __syncthreads();
-    for (int j = tid; j < T; j += kSelThreads) {
-      uint32_t k = score_key(s[j]);
-      if ((k & mask) == prefix) atomicAdd(&hist[wave][(k >> shift) & 255u], 1u);
+#pragma unroll
+    for (int i = 0; i < KPT; ++i) {
+      const int p = p0 + i;
+      kr[i] = p < T ? sel_keys[p + (p >> 5)] : 0u;
     }
-    __syncthreads();
-    if (tid < 256) {  // fold the per-wave histograms
-      uint32_t c = 0;
-      for (int w = 0; w < kSelWaves; ++w) c += hist[w][tid];
-      hist[0][tid] = c;
-    }
-    __syncthreads();
-    if (tid == 0) {   // walk digits from the top until `remaining` falls inside a bin
-      uint32_t above = 0;
-      int dg = 255;
-      for (; dg > 0; --dg) {
-        if (above + hist[0][dg] >= remaining) break;
-        above += hist[0][dg];
+  }
+  // f(key, position, valid) over this lane's positions in ascending order
+  auto for_each = [&](auto &&f) {
+    if constexpr (KPT > 0) {
+#pragma unroll
+      for (int i = 0; i < KPT; ++i) f(kr[i], p0 + i, p0 + i < T);
+    } else {
+      for (int i = 0; i < per; ++i) {
+        const int p = p0 + i;
+        const bool v = p < T;
+        f(v ? score_key(s[p]) : 0u, p, v);
       }
-      s_prefix = prefix | ((uint32_t)dg << shift);
-      s_remaining = remaining - above;
+    }
+  };
+
+  uint32_t prefix = 0, mask = 0, remaining = (uint32_t)t;
+  for (int pass = 0; pass < kSelPasses; ++pass) {
+    const int shift = sel_shift(pass);
+    const uint32_t dmask = (1u << sel_width(pass)) - 1u;
+    for (int i = tid; i < kSelBins; i += kSelThreads) hist[i] = 0;
+    __syncthreads();
+    for_each([&](uint32_t k, int, bool v) {
+      if (v && (k & mask) == prefix) atomicAdd(&hist[(k >> shift) & dmask], 1u);
+    });
+    __syncthreads();
+    // thread i holds digits d_hi = 2047 - 2i and d_lo = 2046 - 2i; the inclusive
+    // scan over i counts the matching keys with digit >= d_lo
+    const int d_hi = kSelBins - 1 - 2 * tid, d_lo = d_hi - 1;
+    const uint32_t c_hi = hist[d_hi], c_lo = hist[d_lo], c = c_hi + c_lo;
+    uint32_t incl = wave_incl_scan(c, lane);
+    if (lane == 63) s_wtot[0][wave] = incl;
+    __syncthreads();
+    for (int w = 0; w < wave; ++w) incl += s_wtot[0][w];
+    // exactly one thread has (keys above its digits) < remaining <= (keys at or above them)
+    const uint32_t above = incl - c;
+    if (incl >= remaining && above < remaining) {
+      const bool hi = above + c_hi >= remaining;
+      s_prefix = prefix | ((uint32_t)(hi ? d_hi : d_lo) << shift);
+      s_remaining = remaining - (hi ? above : above + c_hi);
     }
     __syncthreads();
     prefix = s_prefix;
     remaining = s_remaining;
-    mask |= 255u << shift;
-    __syncthreads();
+    mask |= dmask << shift;
   }
-  // prefix = K*, remaining = number of K*-ties to keep (lowest positions first)
+  // prefix = K*; keep every key > K* and the first `remaining` keys == K*
   const uint32_t kstar = prefix;
-  uint32_t eq_base = 0, out_base = 0;
-  const uint64_t lanemask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-  for (int j0 = 0; j0 < T; j0 += kSelThreads) {
-    const int j = j0 + tid;
-    uint32_t k = j < T ? score_key(s[j]) : 0u;
-    const bool in = j < T;
-    const bool eq = in && k == kstar;
-    uint64_t beq = __ballot(eq);
-    uint32_t eq_rank_w = __popcll(beq & lanemask);
-    if (lane == 0) wave_tot[0][wave] = __popcll(beq);
-    __syncthreads();
-    uint32_t eq_before = eq_base;
-    for (int w = 0; w < wave; ++w) eq_before += wave_tot[0][w];
-    uint32_t eq_rank = eq_before + eq_rank_w;
-    const bool sel = in && (k > kstar || (eq && eq_rank < remaining));
-    uint64_t bsel = __ballot(sel);
-    if (lane == 0) wave_tot[1][wave] = __popcll(bsel);
-    __syncthreads();
-    uint32_t out_before = out_base;
-    for (int w = 0; w < wave; ++w) out_before += wave_tot[1][w];
-    uint32_t pos = out_before + __popcll(bsel & lanemask);
-    if (sel && pos < (uint32_t)t) anchors[(size_t)b * t + pos] = j;
-    if (anchor_of && in) anchor_of[(size_t)b * T + j] = sel ? (int32_t)pos : -1;
-    uint32_t eq_tot = 0, sel_tot = 0;
-    for (int w = 0; w < kSelWaves; ++w) { eq_tot += wave_tot[0][w]; sel_tot += wave_tot[1][w]; }
-    eq_base += eq_tot;
-    out_base += sel_tot;
-    __syncthreads();
+  uint32_t gt = 0, eq = 0;
+  for_each([&](uint32_t k, int, bool v) {
+    gt += v && k > kstar;
+    eq += v && k == kstar;
+  });
+  const uint32_t gt_in = wave_incl_scan(gt, lane), eq_in = wave_incl_scan(eq, lane);
+  if (lane == 63) {
+    s_wtot[0][wave] = gt_in;
+    s_wtot[1][wave] = eq_in;
   }
+  __syncthreads();
+  uint32_t gt_before = gt_in - gt, eq_before = eq_in - eq;
+  for (int w = 0; w < wave; ++w) {
+    gt_before += s_wtot[0][w];
+    eq_before += s_wtot[1][w];
+  }
+  uint32_t out = gt_before + min(eq_before, remaining);
+  uint32_t eq_seen = eq_before;
+  int32_t *dst = anchors + (size_t)b * t;
+  for_each([&](uint32_t k, int p, bool v) {
+    const bool is_eq = v && k == kstar;
+    const bool sel = v && (k > kstar || (is_eq && eq_seen < remaining));
+    if (sel && out < (uint32_t)t) dst[out] = p;   // out < t by construction
+    out += sel;
+    eq_seen += is_eq;
+  });
 }
 
-hipError_t launch_select(const float *scores, int B, int T, int t, int32_t *anchors, int32_t *anchor_of,
-                         hipStream_t s) {
-  hipLaunchKernelGGL(k_select_topt, dim3(B), dim3(kSelThreads), 0, s, scores, T, t, anchors, anchor_of);
-  return hipGetLastError();
+hipError_t launch_select(const float *scores, int B, int T, int t, int32_t *anchors, hipStream_t s) {
+  const int per_lane = (T + kSelThreads - 1) / kSelThreads;
+  auto go = [&](auto kern, bool cached) {
+    const size_t lds = cached ? (size_t)(T + T / 32 + 1) * sizeof(uint32_t) : 0;
+    if (lds > 48 * 1024) {
+      hipError_t e = hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+      if (e != hipSuccess) return e;
+    }
+    hipLaunchKernelGGL(kern, dim3(B), dim3(kSelThreads), lds, s, scores, T, t, anchors);
+    return hipGetLastError();
+  };
+  if (per_lane <= 8) return go(k_select_topt<8>, true);
+  if (per_lane <= 16) return go(k_select_topt<16>, true);
+  if (per_lane <= 32) return go(k_select_topt<32>, true);
+  return go(k_select_topt<0>, false);
 }
 
 }  // namespace arckv
