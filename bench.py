@@ -96,9 +96,17 @@ def cpu_baseline(wl, t, budget_s=25.0):
 
 
 COPY_BYTES = 1 << 30
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "assign_gemm_llama8b_bf16_T32768_traffic.json")
-TRAFFIC_SOURCES = ("paper_2609_36835_amd/csrc/gemm_big.hpp", "paper_2609_36835_amd/csrc/gemm.hip",
-                   "paper_2609_36835_amd/csrc/common.hpp")
+PEAK_HBM_GBS = 8000.0            # MI355X HBM3E
+# Counter-derived HBM traffic per launch, committed under profiles/ together with
+# the hash of the sources of the kernels they were taken on.
+TRAFFIC = {
+    "assign": (os.path.join(ROOT, "profiles", "assign_gemm_llama8b_bf16_T32768_traffic.json"),
+               ("paper_2609_36835_amd/csrc/gemm_big.hpp", "paper_2609_36835_amd/csrc/gemm.hip",
+                "paper_2609_36835_amd/csrc/common.hpp")),
+    "score_select": (os.path.join(ROOT, "profiles", "score_select_llama8b_bf16_T32768_traffic.json"),
+                     ("paper_2609_36835_amd/csrc/score.hip", "paper_2609_36835_amd/csrc/select.hip",
+                      "paper_2609_36835_amd/csrc/common.hpp")),
+}
 
 
 def copy_calibration():
@@ -112,26 +120,34 @@ def copy_calibration():
     print(json.dumps({"copy_calibration_bytes": COPY_BYTES}), flush=True)
 
 
-def sources_sha256():
+def sources_sha256(sources):
     import hashlib
     hsh = hashlib.sha256()
-    for rel in TRAFFIC_SOURCES:
+    for rel in sources:
         with open(os.path.join(ROOT, rel), "rb") as f:
             hsh.update(f.read())
     return hsh.hexdigest()
 
 
-def measured_traffic(wl):
-    """HBM bytes per assignment launch from the committed counter runs, or None when the kernel's sources
-    have changed since they were taken (or the workload differs)."""
+def measured_traffic(which, wl):
+    """HBM bytes per launch from the committed counter runs, or None when the kernels' sources have changed
+    since they were taken (or the workload differs)."""
+    path, sources = TRAFFIC[which]
     try:
-        with open(TRAFFIC_FILE) as f:
+        with open(path) as f:
             rec = json.load(f)
     except (OSError, ValueError):
         return None
-    if rec.get("workload") != wl.name or rec.get("source_sha256") != sources_sha256():
+    if rec.get("workload") != wl.name or rec.get("source_sha256") != sources_sha256(sources):
         return None
     return rec.get("traffic_bytes_per_launch")
+
+
+def score_select_bytes(wl, t):
+    """Algorithmic HBM bytes of scoring + selection for all pairs: read K and V, write the scores, read them
+    back, write the anchors."""
+    esz = 2 if wl.dtype == "bf16" else 4
+    return wl.pairs * (wl.T * (2 * wl.d * esz + 4 + 4) + 4 * t)
 
 
 def main():
@@ -197,11 +213,21 @@ def main():
     launches_per_step = max(cnt_assign // args.steps, 1)
     flops_per_launch = assign_flops(wl, t) / launches_per_step
     achieved = flops_per_launch / avg_launch_s / 1e12
-    roofline = {"bound": "mfma", "kernel": "k_gemm_big<4,2,2,4,64,1,1,EpiArgmaxBig> (key-to-anchor assignment)",
+    roofline = {"bound": "mfma", "kernel": "k_gemm_big<4,2,2,4,64,1,1,2,EpiArgmaxBig> (key-to-anchor assignment)",
                 "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": measured_traffic(wl),
+                "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": measured_traffic("assign", wl),
                 "avg_launch_ms": round(avg_launch_s * 1e3, 3),
                 "algorithmic_flops_per_launch": flops_per_launch}
+    # scoring + selection against HBM: algorithmic bytes / (score + select launch durations)
+    ms_sc, cnt_sc = stages["score"]
+    ms_se, cnt_se = stages["select"]
+    ss_s = (ms_sc / max(cnt_sc, 1) + ms_se / max(cnt_se, 1)) / 1e3
+    ss_bytes = score_select_bytes(wl, t)
+    ss_gbs = ss_bytes / ss_s / 1e9
+    roofline_ss = {"bound": "hbm", "kernel": "k_score_bf16 + k_select_topt (scoring and top-t selection)",
+                   "achieved": round(ss_gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                   "frac": round(ss_gbs / PEAK_HBM_GBS, 4), "traffic": measured_traffic("score_select", wl),
+                   "avg_launch_ms": round(ss_s * 1e3, 4), "algorithmic_bytes_per_launch": ss_bytes}
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -219,6 +245,7 @@ def main():
                    "T": wl.T, "n_ref": wl.n, "t": t, "rho": wl.rho, "head_dim": wl.d,
                    "pair_chunk": args.pair_chunk or wl.pairs},
         "roofline": roofline,
+        "roofline_score_select": roofline_ss,
         "cpu_baseline": cpu,
         "stage_ms_per_step": {k: round(v[0] / args.steps, 3) for k, v in stages.items() if v[1]},
     }

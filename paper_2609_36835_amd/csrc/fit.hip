@@ -966,7 +966,7 @@ hipError_t launch_cholesky(float *Gw, const float *Gc, int B, int t, int64_t ld,
       BigShape g{B, (int)rows, (int)rows, kOuter, 3 * ld * 256, ld * 256, 256, 3 * ld * 256, ld * 256, 256, true, 4};
       EpiCholUpd<1, 2> e{Gw, ld, K1, st.info};
       const hipError_t err =
-          launch_gemm_big<4, 2, 1, 2, 32, 3, 3>(g, Ls + (size_t)K1 * 256, Ls + (size_t)K1 * 256, e, s);
+          launch_gemm_big<4, 2, 1, 2, 32, 3, 3, 2>(g, Ls + (size_t)K1 * 256, Ls + (size_t)K1 * 256, e, s);
       if (err != hipSuccess) return err;
     }
   }

@@ -28,7 +28,7 @@ hipError_t launch_assign_gemm(int dtype, const void *U, const void *Et, uint64_t
   if (dtype == ARCKV_BF16) {
     BigShape g2{P, (int)tp, (int)N, (int)np_, tp * np_, 0, np_, Et_rows * np_, 0, np_, false, (int)(tp / 256)};
     EpiArgmaxBig<4, 2, 2, 4> e2{part, (tp / 256) * N, (int)N, t};
-    return launch_gemm_big<4, 2, 2, 4, 64, 1, 1>(g2, (const bf16 *)U, (const bf16 *)Et, e2, s);
+    return launch_gemm_big<4, 2, 2, 4, 64, 1, 1, 2>(g2, (const bf16 *)U, (const bf16 *)Et, e2, s);
   }
   EpiArgmax e{part, (tp / kGBM) * N, (int)N, t};
   return launch_gemm<float, 1, 1>(g, (const float *)U, (const float *)Et, e, s);
@@ -49,7 +49,7 @@ hipError_t launch_gram(int dtype, const void *X, float *G, float *Gc, int P, int
   if (dtype == ARCKV_BF16) {
     BigShape g2{P, (int)tp, (int)tp, (int)np_, 2 * tp * np_, tp * np_, np_, 2 * tp * np_, tp * np_, np_, true, 4};
     EpiSymBig<2, 4> e2{G, Gc, tp * tp, (int)tp};
-    return launch_gemm_big<4, 2, 2, 4, 32, 2, 2>(g2, (const bf16 *)X, (const bf16 *)X, e2, s);
+    return launch_gemm_big<4, 2, 2, 4, 32, 2, 2, 2>(g2, (const bf16 *)X, (const bf16 *)X, e2, s);
   }
   g.a_pair = g.b_pair = tp * np_;
   g.a_plane = g.b_plane = 0;
@@ -72,7 +72,7 @@ hipError_t launch_rhs_gemm(int dtype, const void *PT, const void *YT, float *Bm,
     BigShape g2{P, (int)tp, kHeadDim, (int)np_, 2 * tp * np_, tp * np_, np_, 2 * (int64_t)kHeadDim * np_,
                 (int64_t)kHeadDim * np_, np_, false, (int)(tp / 256)};
     EpiStoreBig<2, 2> e2{Bm, tp * kHeadDim, kHeadDim, nullptr, nullptr};
-    return launch_gemm_big<4, 2, 2, 2, 32, 2, 2>(g2, (const bf16 *)PT, (const bf16 *)YT, e2, s);
+    return launch_gemm_big<4, 2, 2, 2, 32, 2, 2, 2>(g2, (const bf16 *)PT, (const bf16 *)YT, e2, s);
   }
   g.a_pair = tp * np_;
   g.a_plane = 0;
@@ -108,7 +108,7 @@ hipError_t launch_value_residual(int dtype, const void *XT, const void *Pm, cons
     BigShape gb{P, kHeadDim, (int)np_, (int)tp, pl * kHeadDim * tp, kHeadDim * tp, tp, pl * np_ * tp, np_ * tp, tp,
                 false, 1};
     EpiValueResidBig<2, 2> ep{(bf16 *)UT, pl * kHeadDim * np_, kHeadDim * np_, (int)np_, n, Y};
-    e = launch_gemm_big<2, 4, 2, 2, 32, 2, 2>(gb, (const bf16 *)XT, (const bf16 *)Pm, ep, s);
+    e = launch_gemm_big<2, 4, 2, 2, 32, 2, 2, 2>(gb, (const bf16 *)XT, (const bf16 *)Pm, ep, s);
   } else {
     EpiValueResid<false> ep{UT, kHeadDim * np_, 0, (int)np_, n, Y};
     e = launch_gemm<float, 1, 1>(g1, (const float *)XT, (const float *)Pm, ep, s);
@@ -132,7 +132,7 @@ hipError_t launch_value_residual(int dtype, const void *XT, const void *Pm, cons
     BigShape gb{P, (int)tp, kHeadDim, (int)np_, pl * tp * np_, tp * np_, np_, pl * kHeadDim * np_, kHeadDim * np_, np_,
                 false, (int)(tp / 256)};
     EpiStoreBig<2, 2> eb{R, tp * kHeadDim, kHeadDim, X, lam};
-    return launch_gemm_big<4, 2, 2, 2, 32, 2, 2>(gb, (const bf16 *)PT, (const bf16 *)UT, eb, s);
+    return launch_gemm_big<4, 2, 2, 2, 32, 2, 2, 2>(gb, (const bf16 *)PT, (const bf16 *)UT, eb, s);
   }
   return launch_gemm<float, 1, 1>(g2, (const float *)PT, (const float *)UT, e2, s);
 }

@@ -12,9 +12,10 @@
 // writes bytes [16 l, 16 l + 16) of a 1 KB LDS run), so no VGPRs are spent on
 // staging.  Rows are stored unpadded and each row's 16-byte chunks are XOR-
 // swizzled with the row index, which makes the MFMA fragment reads (32 rows x
-// one chunk per half-wave) free of bank conflicts.  Two LDS stages: slab i+1 is
-// in flight while slab i feeds the MFMAs; fragments for k-step ks+1 are read
-// while the MFMAs of ks run.  One workgroup barrier per slab, without the
+// one chunk per half-wave) free of bank conflicts.  NS LDS stages: slabs
+// i+1 .. i+NS-1 are in flight while slab i feeds the MFMAs (a counted vmcnt
+// wait lets the younger slabs stay outstanding); fragments for k-step ks+1 are
+// read while the MFMAs of ks run.  One workgroup barrier per slab, without the
 // full memory fence of __syncthreads(), so the prefetch stays in flight.
 // Dimensions must be multiples of the tile; workgroups are remapped so that
 // each XCD owns a contiguous, M-grouped (or lower-triangular) range of tiles.
@@ -33,7 +34,7 @@ struct BigShape {
   int group_m;
 };
 
-template <int WM, int WN, int TM, int TN, int BK, int NA, int NB>
+template <int WM, int WN, int TM, int TN, int BK, int NA, int NB, int NS = 2>
 struct BigCfg {
   static constexpr int NW = WM * WN, THREADS = 64 * NW;
   static constexpr int BM = 32 * WM * TM, BN = 32 * WN * TN;
@@ -42,13 +43,15 @@ struct BigCfg {
   static constexpr int RPI = 1024 / RB;             // rows per 1 KB load run
   static constexpr int A_BYTES = BM * RB, B_BYTES = BN * RB;
   static constexpr int STAGE = NA * A_BYTES + NB * B_BYTES;
-  static constexpr int LDS = 2 * STAGE;
+  static constexpr int LDS = NS * STAGE;
   static constexpr int A_INST = A_BYTES / 1024 / NW, B_INST = B_BYTES / 1024 / NW;
+  static constexpr int SLAB_INST = NA * A_INST + NB * B_INST;   // load instructions per slab per wave
   static constexpr int KS = BK / 16;
   static_assert(A_INST * NW * 1024 == A_BYTES && B_INST * NW * 1024 == B_BYTES, "load split");
   static_assert(CPR == 4 || CPR == 8, "BK must be 32 or 64");
   static_assert(NA == NB || NA == 1 || NB == 1, "plane counts");
   static_assert(LDS <= 160 * 1024 - 16 * 1024, "LDS budget");
+  static_assert(NS >= 2 && (NS - 2) * SLAB_INST < 64, "stages");
   // chunk swizzle: 16 consecutive rows at one logical chunk cover all 64 banks
   __device__ static __forceinline__ int swz(int row) { return (row * RB / 256) & (CPR - 1); }
 };
@@ -85,6 +88,14 @@ inline int64_t big_tiles(const BigShape &g, int BM, int BN) {
   return (int64_t)g.batch * (g.syrk ? MT * (MT + 1) / 2 : MT * NT);
 }
 
+// s_waitcnt until at most N vector-memory instructions of this wave are
+// outstanding (expcnt and lgkmcnt left unconstrained).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
 // Workgroup barrier without a memory fence; the empty asm statements keep the
 // compiler from moving LDS accesses across it.
 __device__ __forceinline__ void lds_barrier() {
@@ -93,10 +104,10 @@ __device__ __forceinline__ void lds_barrier() {
   asm volatile("" ::: "memory");
 }
 
-template <int WM, int WN, int TM, int TN, int BK, int NA, int NB, class Epi>
+template <int WM, int WN, int TM, int TN, int BK, int NA, int NB, int NS, class Epi>
 __global__ void __launch_bounds__(64 * WM * WN, 1) k_gemm_big(BigShape g, const bf16 *__restrict__ A,
                                                               const bf16 *__restrict__ B, Epi epi) {
-  using C = BigCfg<WM, WN, TM, TN, BK, NA, NB>;
+  using C = BigCfg<WM, WN, TM, TN, BK, NA, NB, NS>;
   extern __shared__ __attribute__((aligned(1024))) char big_smem[];
 
   const int64_t tile = xcd_remap(blockIdx.x, gridDim.x);
@@ -169,14 +180,21 @@ __global__ void __launch_bounds__(64 * WM * WN, 1) k_gemm_big(BigShape g, const 
     for (int j = 0; j < TN; ++j) acc[i][j] = zero16();
 
   const int nk = g.K / BK;
-  issue(0, 0);
+#pragma unroll
+  for (int st = 0; st < NS - 1; ++st)
+    if (st < nk) issue(st, st);
   for (int i = 0; i < nk; ++i) {
-    // this wave's runs of slab i have landed; after the barrier every wave's
-    // have, and every wave is done reading slab i-1 (the stage refilled next)
-    __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8));   // vmcnt(0) only
+    // this wave's runs of slab i have landed (the younger slabs i+1 ..
+    // i+NS-2 may still be in flight); after the barrier every wave's have, and
+    // every wave is done reading slab i-1, whose stage is refilled next
+    if (i + NS - 2 < nk) wait_vmcnt<(NS - 2) * C::SLAB_INST>();
+    else if constexpr (NS > 2) {   // last slabs: wait conservatively
+      if (i + 1 < nk) wait_vmcnt<C::SLAB_INST>();
+      else wait_vmcnt<0>();
+    }
     lds_barrier();
-    if (i + 1 < nk) issue(i + 1, (i + 1) & 1);
-    const char *s = big_smem + (i & 1) * C::STAGE;
+    if (i + NS - 1 < nk) issue(i + NS - 1, (i + NS - 1) % NS);
+    const char *s = big_smem + (i % NS) * C::STAGE;
     bf16x8 fa[2][NA][TM], fb[2][NB][TN];
     rd(s, 0, fa[0], fb[0]);
 #pragma unroll
@@ -340,13 +358,13 @@ struct EpiValueResidBig {
   }
 };
 
-template <int WM, int WN, int TM, int TN, int BK, int NA, int NB, class Epi>
+template <int WM, int WN, int TM, int TN, int BK, int NA, int NB, int NS, class Epi>
 hipError_t launch_gemm_big(const BigShape &g, const bf16 *A, const bf16 *B, const Epi &epi, hipStream_t s) {
-  using C = BigCfg<WM, WN, TM, TN, BK, NA, NB>;
+  using C = BigCfg<WM, WN, TM, TN, BK, NA, NB, NS>;
   if (g.M % C::BM || g.N % C::BN || g.K % BK) return hipErrorInvalidValue;
   const int64_t tiles = big_tiles(g, C::BM, C::BN);
   if (tiles == 0) return hipSuccess;
-  auto kern = k_gemm_big<WM, WN, TM, TN, BK, NA, NB, Epi>;
+  auto kern = k_gemm_big<WM, WN, TM, TN, BK, NA, NB, NS, Epi>;
   hipError_t e = hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(kern, dim3((unsigned)tiles), dim3(C::THREADS), C::LDS, s, g, A, B, epi);
