@@ -185,6 +185,28 @@ arckv_status arckv_compact(const arckv_problem *prob, const void *K, const void 
                            float *C_k, float *beta, float *C_v, int32_t *info,
                            void *ws, size_t ws_bytes, hipStream_t stream);
 
+/* Decode-time attention over a compacted block followed by an optional
+ * uncompressed block (eq. compact_attention; the joint form of Appendix A.7,
+ * eq. concatenated_attention_preservation, which appends zero bias for the
+ * uncompressed rows).  For each pair p (one sequence and KV head) and each of
+ * its G query rows q (the query heads sharing that KV head):
+ *   out[p][q] = softmax([s q C_k^T + beta, s q K_f^T]) [C_v; V_f]
+ * with s = scale (<= 0 selects 1/sqrt(d)).  The consumer of arckv_compact's
+ * output; with beta = NULL, C_k = K, C_v = V and F = 0 it is full-cache
+ * attention.
+ *   Q        [P][G][d] bfloat16, d = 128; G in {1, 2, 4, 8}.
+ *   C_k, C_v [P][t][d] bfloat16 (may be NULL when t = 0).
+ *   beta     [P][t] float32, or NULL for zero bias.
+ *   K_f, V_f [P][F][d] bfloat16 (may be NULL when F = 0).
+ *   out      [P][G][d] float32.
+ * Requires t, F >= 0 and t + F >= 1; all arrays 16-byte aligned.  Workspace:
+ * arckv_attend_workspace_size(P, G, t, F) bytes (per-chunk partial results).
+ * Reads every key and value row once. */
+arckv_status arckv_attend_workspace_size(int32_t P, int32_t G, int32_t t, int32_t F, size_t *bytes);
+arckv_status arckv_attend(int32_t P, int32_t G, int32_t t, int32_t F, float scale, const void *Q,
+                          const void *C_k, const float *beta, const void *C_v, const void *K_f,
+                          const void *V_f, float *out, void *ws, size_t ws_bytes, hipStream_t stream);
+
 /* Human-readable name of a status code (static string). */
 const char *arckv_status_string(arckv_status s);
 

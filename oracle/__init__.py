@@ -7,6 +7,6 @@ from .core import *  # noqa: F401,F403
 from .core import (budget, gelu, score_mlp, pool_rms, select_topt, logits, global_logit_max,
                    response_profiles, assign, mass_weights, profiles_assign_phi, merge_keys,
                    rowstats, ridge_cholesky_solve, CholeskyFailure, phi_c, nnls_gram, fit_bias,
-                   compact_probs, fit_values, round_to, attend_compact, attend_full, row_rel_err,
+                   compact_probs, fit_values, round_to, attend_compact, attend_full, attend_joint, row_rel_err,
                    compact_pair, PairResult, BiasFit, ValueFit, LAMBDA_M, DELTA_BETA, DELTA_V,
                    EPS_W, B_MIN, B_MAX, MAX_ESCALATIONS)

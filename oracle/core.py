@@ -20,6 +20,9 @@ step by step from the paper's equations:
   O7  mass bias fit          eq. (mass_fit), Appendix A.9
   O8  compact value fit      eq. (value_lstsq), Appendix A.9
   O9  compact attention      eq. (compact_attention), Section 3.1
+  O10 joint decode attention eq. (concatenated_attention_preservation),
+                             Appendix A.7: compact block with bias beta,
+                             then an uncompressed block with zero bias
 
 Readings where the paper is silent (budget rounding, tie rules, ridge
 defaults, guards) are documented on the functions that take them.
@@ -406,6 +409,24 @@ def attend_compact(Q, C_k, beta, C_v, scale: float) -> np.ndarray:
 def attend_full(Q, K, V, scale: float) -> np.ndarray:
     """eq. (full_attention): softmax(Q K^T) V."""
     return rowstats(Q, K, V, scale)[2]
+
+
+def attend_joint(Q, C_k, beta, C_v, K_f, V_f, scale: float) -> np.ndarray:
+    """eq. (concatenated_attention_preservation), right-hand side: one softmax
+    over the concatenated logits [s Q C_k^T + 1 beta^T, s Q K_f^T] (zero bias on
+    the uncompressed rows) applied to [C_v; V_f].  Either block may be empty
+    (t = 0 or F = 0 rows); beta = None means zero bias."""
+    Q = np.asarray(Q, np.float64)
+    d = Q.shape[1]
+    C_k = np.zeros((0, d)) if C_k is None else np.asarray(C_k, np.float64)
+    C_v = np.zeros((0, d)) if C_v is None else np.asarray(C_v, np.float64)
+    K_f = np.zeros((0, d)) if K_f is None else np.asarray(K_f, np.float64)
+    V_f = np.zeros((0, d)) if V_f is None else np.asarray(V_f, np.float64)
+    b = np.zeros(C_k.shape[0]) if beta is None else np.asarray(beta, np.float64)
+    X = np.concatenate([scale * (Q @ C_k.T) + b[None, :], scale * (Q @ K_f.T)], axis=1)
+    X -= X.max(axis=1, keepdims=True)
+    E = np.exp(X)
+    return (E / E.sum(axis=1, keepdims=True)) @ np.concatenate([C_v, V_f], axis=0)
 
 
 def row_rel_err(O_test, O_ref) -> np.ndarray:

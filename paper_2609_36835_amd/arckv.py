@@ -25,6 +25,7 @@ ENTRY_POINTS = (
     "arckv_default_params", "arckv_budget", "arckv_workspace_size", "arckv_score", "arckv_select",
     "arckv_rowstats", "arckv_merge", "arckv_fit_bias", "arckv_fit_values", "arckv_compact",
     "arckv_status_string", "arckv_set_timing", "arckv_stage_times", "arckv_reset_timing",
+    "arckv_attend_workspace_size", "arckv_attend",
 )
 
 
@@ -79,6 +80,8 @@ def lib():
         L.arckv_set_timing.argtypes = [i32]
         L.arckv_stage_times.argtypes = [i32, P(ctypes.c_char_p), P(ctypes.c_double), P(i32), P(i32)]
         L.arckv_reset_timing.argtypes = []
+        L.arckv_attend_workspace_size.argtypes = [i32, i32, i32, i32, P(sz)]
+        L.arckv_attend.argtypes = [i32, i32, i32, i32, ctypes.c_float, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
         for name in ENTRY_POINTS:
             getattr(L, name).restype = ctypes.c_int if name != "arckv_status_string" else ctypes.c_char_p
         _LIB = L
@@ -232,6 +235,40 @@ def fit_values(Q, C_k, beta, Y, params: Optional[FitParams] = None, scale=None, 
                                   ctypes.byref(params), _ptr(Cv), _ptr(info), _ptr(dused), _ptr(ws), nbytes,
                                   _stream()), "arckv_fit_values")
     return Cv, info, dused
+
+
+def attend_workspace_size(P: int, G: int, t: int, F: int) -> int:
+    out = ctypes.c_size_t()
+    _check(lib().arckv_attend_workspace_size(int(P), int(G), int(t), int(F), ctypes.byref(out)),
+           "arckv_attend_workspace_size")
+    return out.value
+
+
+class Attender:
+    """Holds the output and workspace for repeated arckv_attend calls of one shape."""
+
+    def __init__(self, P, G, t, F=0, device="cuda", scale=None):
+        self.P, self.G, self.t, self.F = int(P), int(G), int(t), int(F)
+        self.scale = float(scale) if scale else 0.0
+        dev = torch.device(device)
+        self.out = torch.empty(self.P, self.G, 128, dtype=torch.float32, device=dev)
+        self.ws_bytes = attend_workspace_size(self.P, self.G, self.t, self.F)
+        self.ws = _workspace(self.ws_bytes, dev)
+
+    def __call__(self, Q, C_k, beta, C_v, K_f=None, V_f=None):
+        _check(lib().arckv_attend(self.P, self.G, self.t, self.F, self.scale, _ptr(Q), _ptr(C_k), _ptr(beta),
+                                  _ptr(C_v), _ptr(K_f), _ptr(V_f), _ptr(self.out), _ptr(self.ws), self.ws_bytes,
+                                  _stream()), "arckv_attend")
+        return self.out
+
+
+def attend(Q, C_k, beta, C_v, K_f=None, V_f=None, scale=None) -> torch.Tensor:
+    """Decode attention softmax([s Q C_k^T + beta, s Q K_f^T]) [C_v; V_f] per pair:
+    Q [P][G][128], C_k/C_v [P][t][128], beta [P][t] or None, K_f/V_f [P][F][128] or None (bf16; beta fp32)."""
+    P, G, _ = Q.shape
+    t = C_k.shape[1] if C_k is not None else 0
+    F = K_f.shape[1] if K_f is not None else 0
+    return Attender(P, G, t, F, Q.device, scale)(Q, C_k, beta, C_v, K_f, V_f)
 
 
 class Compactor:

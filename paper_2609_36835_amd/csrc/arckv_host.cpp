@@ -69,16 +69,21 @@ hipError_t launch_values_out(const float *Xp, int B, int64_t tp, int t, const in
                              hipStream_t s);
 hipError_t launch_copy_info(const int32_t *a, const int32_t *b, int B, int32_t *info, hipStream_t s);
 hipError_t launch_copy_f32(const float *src, float *dst, int B, hipStream_t s);
+int attend_chunks(int t, int F);
+hipError_t launch_attend(int P, int G, int t, int F, float scale, const void *Q, const void *Ck, const float *beta,
+                         const void *Cv, const void *Kf, const void *Vf, float *part_o, float *part_ml, float *out,
+                         hipStream_t s);
 
 // ------------------------------------------------------------------ timing
 enum Stage {
   ST_SCORE, ST_SELECT, ST_ROWSTATS, ST_ZMAX, ST_PROFILES, ST_ANCHOR_PROF, ST_ASSIGN, ST_FINALIZE, ST_MERGE,
-  ST_PHIC, ST_GRAM_G, ST_CHOL_G, ST_SOLVE_W, ST_PHAT, ST_GRAM_A, ST_RHS, ST_CHOL_A, ST_SOLVE_V,
+  ST_PHIC, ST_GRAM_G, ST_CHOL_G, ST_SOLVE_W, ST_PHAT, ST_GRAM_A, ST_RHS, ST_CHOL_A, ST_SOLVE_V, ST_ATTEND,
   ST_COUNT
 };
 static const char *kStageNames[ST_COUNT] = {
     "score", "select", "rowstats", "zmax", "profiles", "anchor_profiles", "assign_gemm", "assign_finalize",
-    "merge", "phic", "gram_G", "chol_G", "solve_beta", "phat", "gram_A", "rhs_B", "chol_A", "solve_values"};
+    "merge", "phic", "gram_G", "chol_G", "solve_beta", "phat", "gram_A", "rhs_B", "chol_A", "solve_values",
+    "attend"};
 
 struct TimingState {
   std::mutex mu;
@@ -643,6 +648,47 @@ arckv_status arckv_compact(const arckv_problem *prob, const void *K, const void 
   }
   if (launch_copy_info(c.pers<int32_t>(c.pl.info_g), c.pers<int32_t>(c.pl.info_a), d.B, info, stream) != hipSuccess)
     return ARCKV_ERR_HIP;
+  return ARCKV_OK;
+}
+
+static arckv_status check_attend(int32_t P, int32_t G, int32_t t, int32_t F) {
+  if (P < 1 || t < 0 || F < 0 || (int64_t)t + F < 1) return ARCKV_ERR_INVALID_ARG;
+  if ((int64_t)t + F > (1ll << 30)) return ARCKV_ERR_UNSUPPORTED;
+  if (G != 1 && G != 2 && G != 4 && G != 8) return ARCKV_ERR_UNSUPPORTED;
+  return ARCKV_OK;
+}
+
+static size_t attend_ws_bytes(int32_t P, int32_t G, int32_t t, int32_t F) {
+  const size_t nch = (size_t)attend_chunks(t, F);
+  return rup((int64_t)((size_t)P * nch * G * kHeadDimH * 4), 256) + rup((int64_t)((size_t)P * nch * G * 2 * 4), 256);
+}
+
+arckv_status arckv_attend_workspace_size(int32_t P, int32_t G, int32_t t, int32_t F, size_t *bytes) {
+  CHECK(check_attend(P, G, t, F));
+  if (!bytes) return ARCKV_ERR_INVALID_ARG;
+  *bytes = attend_ws_bytes(P, G, t, F);
+  return ARCKV_OK;
+}
+
+arckv_status arckv_attend(int32_t P, int32_t G, int32_t t, int32_t F, float scale, const void *Q, const void *C_k,
+                          const float *beta, const void *C_v, const void *K_f, const void *V_f, float *out, void *ws,
+                          size_t ws_bytes, hipStream_t stream) {
+  CHECK(check_attend(P, G, t, F));
+  if (!Q || !out) return ARCKV_ERR_INVALID_ARG;
+  if (t > 0 && (!C_k || !C_v)) return ARCKV_ERR_INVALID_ARG;
+  if (F > 0 && (!K_f || !V_f)) return ARCKV_ERR_INVALID_ARG;
+  if (!isfinite(scale)) return ARCKV_ERR_INVALID_ARG;
+  if (!aligned(Q, 16) || (C_k && !aligned(C_k, 16)) || (C_v && !aligned(C_v, 16)) || (K_f && !aligned(K_f, 16)) ||
+      (V_f && !aligned(V_f, 16)))
+    return ARCKV_ERR_INVALID_ARG;
+  if (!ws || !aligned(ws, 256) || ws_bytes < attend_ws_bytes(P, G, t, F)) return ARCKV_ERR_WORKSPACE;
+  const float s = scale > 0.0f ? scale : 1.0f / sqrtf((float)kHeadDimH);
+  const size_t nch = (size_t)attend_chunks(t, F);
+  float *part_o = reinterpret_cast<float *>(ws);
+  float *part_ml = reinterpret_cast<float *>((char *)ws + rup((int64_t)((size_t)P * nch * G * kHeadDimH * 4), 256));
+  STAGE(ST_ATTEND, launch_attend(P, G, t, F, s, Q, t > 0 ? C_k : nullptr, t > 0 ? beta : nullptr,
+                                 t > 0 ? C_v : nullptr, F > 0 ? K_f : nullptr, F > 0 ? V_f : nullptr, part_o, part_ml,
+                                 out, stream));
   return ARCKV_OK;
 }
 

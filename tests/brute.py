@@ -131,6 +131,21 @@ def compact_attend(Q, C_k, beta, C_v, scale):
     return out
 
 
+def joint_attend(Q, C_k, beta, C_v, K_f, V_f, scale):
+    """One softmax over the compact keys (logit + beta_r) followed by the
+    uncompressed keys (logit + 0), by explicit loops."""
+    keys = [(c, b, v) for c, b, v in zip(C_k, beta, C_v)] + [(k, 0.0, v) for k, v in zip(K_f, V_f)]
+    out = []
+    for q in Q:
+        x = [scale * dot(q, k) + b for k, b, _ in keys]
+        mx = max(x)
+        w = [math.exp(v - mx) for v in x]
+        s = sum(w)
+        d = len(keys[0][2])
+        out.append([sum(w[j] * float(keys[j][2][c]) for j in range(len(keys))) / s for c in range(d)])
+    return out
+
+
 def round_bf16(x):
     """Nearest-even bfloat16 value of float x (via its float32 bit pattern)."""
     import struct

@@ -146,3 +146,32 @@ def test_product_path_has_no_oracle_or_fallback():
     src = open(os.path.join(os.path.dirname(A.__file__), "arckv.py")).read()
     assert "oracle" not in src.replace("oracle/", "")
     assert "numpy" not in src
+
+
+def test_attend_workspace_and_validation():
+    assert A.attend_workspace_size(512, 4, 6554, 0) > 0
+    assert A.attend_workspace_size(512, 4, 6554, 100) >= A.attend_workspace_size(512, 4, 6554, 0)
+    for args, st in [((0, 4, 10, 0), A.ERR_INVALID_ARG), ((1, 4, 0, 0), A.ERR_INVALID_ARG),
+                     ((1, 4, -1, 5), A.ERR_INVALID_ARG), ((1, 4, 5, -1), A.ERR_INVALID_ARG),
+                     ((1, 3, 10, 0), A.ERR_UNSUPPORTED), ((1, 16, 10, 0), A.ERR_UNSUPPORTED)]:
+        with pytest.raises(A.ArckvError) as e:
+            A.attend_workspace_size(*args)
+        assert e.value.status == st, args
+    L = A.lib()
+    fake = ctypes.c_void_p(0x1000)      # never dereferenced: validation fails first
+    nws = A.attend_workspace_size(2, 4, 10, 0)
+    # missing pointers, unaligned pointers and a short workspace are rejected before any HIP call
+    assert L.arckv_attend(2, 4, 10, 0, 0.0, None, fake, None, fake, None, None, fake, fake, nws, None) == \
+        A.ERR_INVALID_ARG
+    assert L.arckv_attend(2, 4, 10, 0, 0.0, fake, None, None, fake, None, None, fake, fake, nws, None) == \
+        A.ERR_INVALID_ARG
+    assert L.arckv_attend(2, 4, 10, 3, 0.0, fake, fake, None, fake, None, None, fake, fake, nws, None) == \
+        A.ERR_INVALID_ARG
+    assert L.arckv_attend(2, 4, 10, 0, 0.0, ctypes.c_void_p(0x1002), fake, None, fake, None, None, fake, fake, nws,
+                          None) == A.ERR_INVALID_ARG
+    assert L.arckv_attend(2, 4, 10, 0, float("nan"), fake, fake, None, fake, None, None, fake, fake, nws, None) == \
+        A.ERR_INVALID_ARG
+    assert L.arckv_attend(2, 4, 10, 0, 0.0, fake, fake, None, fake, None, None, fake, fake, nws - 1, None) == \
+        A.ERR_WORKSPACE
+    assert L.arckv_attend(2, 4, 10, 0, 0.0, fake, fake, None, fake, None, None, fake, ctypes.c_void_p(0x1010), nws,
+                          None) == A.ERR_WORKSPACE

@@ -425,3 +425,62 @@ def test_assignment_in_storage_precision_bruteforce(dt):
     rnd = brute.round_bf16 if dt == "bf16" else (lambda v: float(np.float32(v)))
     kap, _, _ = oracle.profiles_assign_phi(Q, K, S, 0.6, profile_dtype=dt)
     assert kap.tolist() == brute.assign_rounded(Q.tolist(), K.tolist(), S.tolist(), 0.6, rnd)
+
+
+# ----------------------------------------------------------------- O10 joint decode attention
+def _joint_case(seed, t=7, F=5, n=4, d=6):
+    g = rng(seed)
+    return (g.standard_normal((n, d)), g.standard_normal((t, d)), g.uniform(-2, 2, t), g.standard_normal((t, d)),
+            g.standard_normal((F, d)), g.standard_normal((F, d)))
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_joint_attention_bruteforce(seed):
+    Q, Ck, b, Cv, Kf, Vf = _joint_case(seed)
+    s = 0.7
+    got = oracle.attend_joint(Q, Ck, b, Cv, Kf, Vf, s)
+    ref = np.array(brute.joint_attend(Q.tolist(), Ck.tolist(), b.tolist(), Cv.tolist(), Kf.tolist(), Vf.tolist(), s))
+    np.testing.assert_allclose(got, ref, rtol=1e-12, atol=1e-12)
+
+
+def test_joint_attention_block_decomposition():
+    """softmax over two concatenated blocks = the mass-weighted mix of each block's
+    own softmax output (Z_C O_C + Z_F O_F) / (Z_C + Z_F), with the masses of
+    eq. block_attention_mass (Z_C includes the bias)."""
+    Q, Ck, b, Cv, Kf, Vf = _joint_case(3, t=9, F=4)
+    s = 0.5
+    got = oracle.attend_joint(Q, Ck, b, Cv, Kf, Vf, s)
+    for i, q in enumerate(Q):
+        wc = np.array([math.exp(s * float(q @ c) + bb) for c, bb in zip(Ck, b)])
+        wf = np.array([math.exp(s * float(q @ k)) for k in Kf])
+        Oc, Of = wc @ Cv / wc.sum(), wf @ Vf / wf.sum()
+        mix = (wc.sum() * Oc + wf.sum() * Of) / (wc.sum() + wf.sum())
+        np.testing.assert_allclose(got[i], mix, rtol=1e-12, atol=1e-13)
+
+
+def test_joint_attention_split_full_cache_is_full_attention():
+    """With zero bias, a cache split into a 'compact' prefix and an uncompressed
+    suffix attends exactly like the whole cache (row statistics' Y)."""
+    g = rng(4)
+    K, V, Q = g.standard_normal((13, 6)), g.standard_normal((13, 6)), g.standard_normal((5, 6))
+    s = 0.8
+    _, _, Y = oracle.rowstats(Q, K, V, s)
+    for a in (0, 1, 6, 13):
+        got = oracle.attend_joint(Q, K[:a], np.zeros(a), V[:a], K[a:], V[a:], s)
+        np.testing.assert_allclose(got, Y, rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(oracle.attend_joint(Q, K, None, V, None, None, s), Y, rtol=1e-12, atol=1e-13)
+
+
+def test_joint_attention_bias_shift():
+    """A constant c added to every beta leaves a lone compact block unchanged and,
+    next to an uncompressed block, multiplies the compact block's mass by e^c."""
+    Q, Ck, b, Cv, Kf, Vf = _joint_case(5)
+    s, c = 0.6, 1.3
+    np.testing.assert_allclose(oracle.attend_joint(Q, Ck, b + c, Cv, None, None, s),
+                               oracle.attend_joint(Q, Ck, b, Cv, None, None, s), rtol=1e-12, atol=1e-13)
+    got = oracle.attend_joint(Q, Ck, b + c, Cv, Kf, Vf, s)
+    for i, q in enumerate(Q):
+        wc = np.exp(s * (Ck @ q) + b)
+        wf = np.exp(s * (Kf @ q))
+        mix = (math.exp(c) * (wc @ Cv) + wf @ Vf) / (math.exp(c) * wc.sum() + wf.sum())
+        np.testing.assert_allclose(got[i], mix, rtol=1e-12, atol=1e-13)
