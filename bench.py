@@ -150,6 +150,58 @@ def score_select_bytes(wl, t):
     return wl.pairs * (wl.T * (2 * wl.d * esz + 4 + 4) + 4 * t)
 
 
+DECODE_CONTEXTS = (4096, 8192, 16384, 32768)
+
+
+def decode_bench(reps=20, warmup=3):
+    """One decode step of attention for one layer at batch 64 (64 sequences x 8 KV heads = 512 pairs, 4 query
+    heads per KV head): full-cache attention (C_k = K, C_v = V, no bias) against the compact cache at rho = 0.2
+    with its bias, both through arckv_attend.  Synthetic bf16 caches; returns one JSON-able dict."""
+    import torch
+    from paper_2609_36835_amd import arckv
+    dev = torch.device("cuda:0")
+    P, G, d = 64 * 8, 4, 128
+    g = torch.Generator(device=dev)
+    g.manual_seed(0)
+    rows = []
+    for T in DECODE_CONTEXTS:
+        t = arckv.budget(T, 0.2)
+        res = {"context": T, "t": t}
+        for label, L, with_beta in (("full", T, False), ("compact", t, True)):
+            K = torch.randn(P, L, d, device=dev, dtype=torch.bfloat16, generator=g)
+            V = torch.randn(P, L, d, device=dev, dtype=torch.bfloat16, generator=g)
+            Q = torch.randn(P, G, d, device=dev, dtype=torch.bfloat16, generator=g)
+            beta = (torch.rand(P, L, device=dev, generator=g) * 6 - 3) if with_beta else None
+            att = arckv.Attender(P, G, L, 0, dev)
+            for _ in range(warmup):
+                att(Q, K, beta, V)
+            torch.cuda.synchronize()
+            arckv.reset_timing()
+            arckv.set_timing(True)
+            for _ in range(reps):
+                att(Q, K, beta, V)
+            torch.cuda.synchronize()
+            arckv.set_timing(False)
+            ms, cnt = arckv.stage_times()["attend"]
+            us = 1e3 * ms / cnt
+            nbytes = P * L * d * 2 * 2 + (P * L * 4 if with_beta else 0) + P * G * d * (2 + 4)
+            res[f"{label}_us"] = round(us, 2)
+            res[f"{label}_GBps"] = round(nbytes / (us * 1e-6) / 1e9, 1)
+            res[f"{label}_hbm_frac"] = round(nbytes / (us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4)
+            log(f"[decode] T={T} {label}: L={L} {us:.1f} us/layer, {res[f'{label}_GBps']:.0f} GB/s")
+            del K, V, Q, beta, att
+            torch.cuda.empty_cache()
+        res["speedup"] = round(res["full_us"] / res["compact_us"], 3)
+        res["ms_per_token_32_layers"] = {"full": round(32 * res["full_us"] / 1e3, 3),
+                                         "compact": round(32 * res["compact_us"] / 1e3, 3)}
+        rows.append(res)
+    return {"metric": "decode attention latency per layer (batch 64, Llama-3.1-8B shapes, rho = 0.2 compact cache "
+                      "with fitted bias vs full cache)", "unit": "us", "higher_is_better": False, "n_gpus": 1,
+            "dtype": "bf16", "data": "synthetic (random bf16 caches and queries)",
+            "config": {"workload": "decode_b64_llama8b", "pairs": P, "query_heads_per_kv": G, "rho": 0.2},
+            "kernel": "k_attend_partial<4> + k_attend_combine", "peak_hbm_GBps": PEAK_HBM_GBS, "rows": rows}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -161,7 +213,12 @@ def main():
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device copy (3 times), the reference kernel that scales the "
                          "FETCH_SIZE / WRITE_SIZE counters to bytes")
+    ap.add_argument("--decode", action="store_true",
+                    help="instead of compaction, time decode attention over full and compact caches (batch 64)")
     args = ap.parse_args()
+    if args.decode:
+        print(json.dumps(decode_bench()), flush=True)
+        return
     if args.copy_calibration:
         copy_calibration()
         return
