@@ -99,6 +99,9 @@ typedef struct {
                           * not from the float32 Gram, so the solves converge to the
                           * least-squares solutions of the exact normal equations. */
   int32_t pair_chunk;    /* pairs processed together by arckv_compact (0 = all B); sizes the workspace */
+  int32_t select_chunk;  /* 0 = global top-t (default).  L > 0: when T > 10,000, anchors are the union of
+                          * each L-position chunk's local top-t_c (Appendix A.3), so arckv_compact keeps
+                          * arckv_select_count(T, t, L) anchors; merge and fits stay global. */
 } arckv_fit_params;
 
 /* Fill *p with the defaults listed above.  Returns ARCKV_ERR_INVALID_ARG on NULL. */
@@ -127,6 +130,30 @@ arckv_status arckv_score(const arckv_problem *prob, const void *K, const void *V
  * Bit-exact by construction.  Needs 1 <= t <= T. */
 arckv_status arckv_select(const arckv_problem *prob, const float *scores, int32_t t,
                           int32_t *anchors, void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* Per-pair budgets of eq. per_head_budget (host only, no GPU work):
+ * t_out[i] = clip_[1,T](floor(a_i / sum(a) * P * t)) for P pairs with weights
+ * a (host array, finite, >= 0, not all zero) and nominal per-pair budget t. */
+arckv_status arckv_budgets(int32_t P, const double *a, int32_t t, int64_t T, int32_t *t_out);
+
+/* Realised anchor count of chunked selection (Appendix A.3; host only):
+ * sum over chunks c of length T_c of clip_[1,T_c](round(t T_c / T)) (rounded
+ * half up) when chunk_len > 0 and T > 10,000, otherwise t. */
+arckv_status arckv_select_count(int64_t T, int32_t t, int32_t chunk_len, int32_t *t_real);
+
+/* Stage 1b, general form: per-pair budgets and/or chunked selection.
+ *   t_pair     [B] device array of per-pair budgets (e.g. from arckv_budgets),
+ *              or NULL for the uniform budget t; entries are clipped to [1, T].
+ *   chunk_len  0 = global top-t; L > 0 = Appendix A.3 chunking when T > 10,000.
+ *   anchors    [B][t_stride] output: each row holds the pair's anchors ascending,
+ *              then -1 up to t_stride.  t_stride must cover every pair's realised
+ *              count (arckv_select_count of its budget); rows are truncated, never
+ *              overrun, if it does not.  With t_pair NULL a short t_stride is
+ *              rejected (ARCKV_ERR_INVALID_ARG).
+ * The order of S and the tie rules are those of arckv_select. */
+arckv_status arckv_select_ex(const arckv_problem *prob, const float *scores, int32_t t,
+                             const int32_t *t_pair, int32_t chunk_len, int32_t t_stride,
+                             int32_t *anchors, hipStream_t stream);
 
 /* Full-cache row statistics (Appendix A.9): with l_ij = s q_i.k_j,
  *   z [B][n]     z_i = max_j l_ij over the whole cache,
@@ -175,8 +202,9 @@ arckv_status arckv_fit_values(const arckv_problem *prob, const void *Q_ref, cons
                               float *delta_used, void *ws, size_t ws_bytes, hipStream_t stream);
 
 /* The whole per-context path for B pairs: score, select, row statistics,
- * merge, mass fit, value fit.  t = arckv_budget(T, rho) is written to *t_out
- * (host pointer) before any device work.  Outputs: anchors [B][t], C_k [B][t][d],
+ * merge, mass fit, value fit.  t = arckv_budget(T, rho) (or, with
+ * p->select_chunk, arckv_select_count of it) is written to *t_out (host
+ * pointer) before any device work.  Outputs: anchors [B][t], C_k [B][t][d],
  * beta [B][t], C_v [B][t][d], info [B][2] (mass-fit, value-fit status as above).
  * Pairs are processed p->pair_chunk at a time (0 = all at once). */
 arckv_status arckv_compact(const arckv_problem *prob, const void *K, const void *V,

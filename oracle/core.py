@@ -9,7 +9,8 @@ Everything here works on one layer-KV-head pair (the paper treats pairs
 independently, Method section and Appendix A.2) in float64 numpy, written
 step by step from the paper's equations:
 
-  O0  budget                 Appendix A.2 (per-head budget), A.3 (chunk rounding)
+  O0  budget                 Appendix A.2 (per-head budget, eq. per_head_budget),
+                             A.3 (chunk budgets)
   O1  token scores           the scoring MLP on concat(k_j, v_j); pooling by
                              eq. (indexer_pooling), Section 3.3
   O2  top-t anchors          S = TopK(s, t), Section 3.3 / eq. (persistent_support)
@@ -55,6 +56,34 @@ def budget(T: int, rho: float) -> int:
     """
     t = int(math.floor(float(rho) * float(T) + 0.5))
     return min(int(T), max(1, t))
+
+
+def budgets_per_pair(a, t: int, T: int) -> np.ndarray:
+    """eq. (per_head_budget): t_p = clip_[1,T](floor(a_p |P| t)) with the weights
+    a normalised to sum to 1 over the |P| pairs (Section 3.5)."""
+    a = np.asarray(a, np.float64)
+    if a.ndim != 1 or a.size == 0 or not np.all(np.isfinite(a)) or np.any(a < 0) or a.sum() <= 0:
+        raise ValueError("weights must be finite, non-negative and not all zero")
+    a = a / a.sum()
+    return np.clip(np.floor(a * a.size * t), 1, T).astype(np.int64)
+
+
+CHUNK_THRESHOLD = 10000   # chunking applies when T > 10,000 (Appendix A.3)
+
+
+def chunk_budgets(t: int, T: int, chunk_len: int):
+    """Appendix A.3: with chunks of chunk_len positions (when chunk_len > 0 and
+    T > 10,000), chunk c of length T_c keeps t_c = clip_[1,T_c](round(t T_c / T))
+    anchors; otherwise one chunk keeps t.  Returns [(start, T_c, t_c)].
+    Reading: round() is round-half-up, as for the budget (O0)."""
+    if chunk_len <= 0 or T <= CHUNK_THRESHOLD:
+        return [(0, T, t)]
+    out = []
+    for start in range(0, T, chunk_len):
+        Tc = min(chunk_len, T - start)
+        tc = int(math.floor(t * Tc / T + 0.5))
+        out.append((start, Tc, min(Tc, max(1, tc))))
+    return out
 
 
 # --------------------------------------------------------------------------- O1
@@ -107,6 +136,14 @@ def select_topt(scores, t: int) -> np.ndarray:
     # primary key: NaN last, then -score; secondary: index (lexsort: last key primary)
     order = np.lexsort((np.arange(T), np.where(nan, 0.0, -s), nan))
     return np.sort(order[:t]).astype(np.int64)
+
+
+def select_topt_chunked(scores, t: int, chunk_len: int) -> np.ndarray:
+    """Appendix A.3: the union of each chunk's local top-t_c (chunk_budgets),
+    ascending; the global top-t when chunking does not apply."""
+    s = np.asarray(scores, np.float64)
+    parts = [start + select_topt(s[start:start + Tc], tc) for start, Tc, tc in chunk_budgets(t, s.shape[0], chunk_len)]
+    return np.concatenate(parts).astype(np.int64)
 
 
 # --------------------------------------------------------------------------- O3-O5

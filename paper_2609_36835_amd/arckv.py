@@ -25,7 +25,7 @@ ENTRY_POINTS = (
     "arckv_default_params", "arckv_budget", "arckv_workspace_size", "arckv_score", "arckv_select",
     "arckv_rowstats", "arckv_merge", "arckv_fit_bias", "arckv_fit_values", "arckv_compact",
     "arckv_status_string", "arckv_set_timing", "arckv_stage_times", "arckv_reset_timing",
-    "arckv_attend_workspace_size", "arckv_attend",
+    "arckv_attend_workspace_size", "arckv_attend", "arckv_budgets", "arckv_select_count", "arckv_select_ex",
 )
 
 
@@ -49,7 +49,8 @@ class FitParams(ctypes.Structure):
     _fields_ = [("lambda_m", ctypes.c_float), ("delta_beta", ctypes.c_float), ("delta_v", ctypes.c_float),
                 ("eps_w", ctypes.c_float), ("b_min", ctypes.c_float), ("b_max", ctypes.c_float),
                 ("bias_mode", ctypes.c_int32), ("max_escalations", ctypes.c_int32),
-                ("refine_steps", ctypes.c_int32), ("pair_chunk", ctypes.c_int32)]
+                ("refine_steps", ctypes.c_int32), ("pair_chunk", ctypes.c_int32),
+                ("select_chunk", ctypes.c_int32)]
 
 
 _LIB = None
@@ -81,6 +82,9 @@ def lib():
         L.arckv_stage_times.argtypes = [i32, P(ctypes.c_char_p), P(ctypes.c_double), P(i32), P(i32)]
         L.arckv_reset_timing.argtypes = []
         L.arckv_attend_workspace_size.argtypes = [i32, i32, i32, i32, P(sz)]
+        L.arckv_budgets.argtypes = [i32, P(ctypes.c_double), i32, ctypes.c_int64, P(i32)]
+        L.arckv_select_count.argtypes = [ctypes.c_int64, i32, i32, P(i32)]
+        L.arckv_select_ex.argtypes = [P(Problem), vp, i32, vp, i32, i32, vp, vp]
         L.arckv_attend.argtypes = [i32, i32, i32, i32, ctypes.c_float, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
         for name in ENTRY_POINTS:
             getattr(L, name).restype = ctypes.c_int if name != "arckv_status_string" else ctypes.c_char_p
@@ -177,6 +181,35 @@ def select(scores: torch.Tensor, t: int) -> torch.Tensor:
     out = torch.empty(B, t, dtype=torch.int32, device=scores.device)
     _check(lib().arckv_select(ctypes.byref(prob), _ptr(scores), int(t), _ptr(out), None, 0, _stream()),
            "arckv_select")
+    return out
+
+
+def budgets(a, t: int, T: int):
+    """eq. per_head_budget: per-pair budgets (host list) from weights a."""
+    n = len(a)
+    arr = (ctypes.c_double * n)(*[float(x) for x in a])
+    out = (ctypes.c_int32 * n)()
+    _check(lib().arckv_budgets(n, arr, int(t), int(T), out), "arckv_budgets")
+    return list(out)
+
+
+def select_count(T: int, t: int, chunk_len: int) -> int:
+    out = ctypes.c_int32()
+    _check(lib().arckv_select_count(int(T), int(t), int(chunk_len), ctypes.byref(out)), "arckv_select_count")
+    return out.value
+
+
+def select_ex(scores: torch.Tensor, t: int, t_pair: Optional[torch.Tensor] = None, chunk_len: int = 0,
+              t_stride: Optional[int] = None) -> torch.Tensor:
+    """Per-pair budgets (t_pair, int32 [B] on the GPU) and/or chunked selection; rows padded with -1."""
+    B, T = scores.shape
+    if t_stride is None:
+        tmax = int(t_pair.max().item()) if t_pair is not None else t
+        t_stride = select_count(T, tmax, chunk_len) + (B if t_pair is not None and chunk_len else 0)
+    prob = Problem(B, T, 1, 128, F32, 0.0)
+    out = torch.empty(B, t_stride, dtype=torch.int32, device=scores.device)
+    _check(lib().arckv_select_ex(ctypes.byref(prob), _ptr(scores), int(t), _ptr(t_pair), int(chunk_len),
+                                 int(t_stride), _ptr(out), _stream()), "arckv_select_ex")
     return out
 
 
@@ -280,6 +313,8 @@ class Compactor:
         self.rho = float(rho)
         self.params = params or default_params()
         self.t = budget(T, rho)
+        if self.params.select_chunk:
+            self.t = select_count(T, self.t, self.params.select_chunk)
         dev = torch.device(device)
         self.anchors = torch.empty(B, self.t, dtype=torch.int32, device=dev)
         self.C_k = torch.empty(B, self.t, 128, dtype=torch.float32, device=dev)

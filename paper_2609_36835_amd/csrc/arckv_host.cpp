@@ -25,6 +25,23 @@ struct FitState {
 hipError_t launch_score(int dtype, const void *K, const void *V, const void *W1, const float *b1, const float *w2,
                         const float *b2, float *scores, int B, int T, hipStream_t s);
 hipError_t launch_select(const float *scores, int B, int T, int t, int32_t *anchors, hipStream_t s);
+hipError_t launch_select_ex(const float *scores, int B, int T, int t, const int32_t *t_pair, int chunk_len,
+                            int t_stride, int32_t *anchors, hipStream_t s);
+constexpr int kChunkThresholdH = 10000;   // chunked selection applies when T > 10,000
+
+// Realised anchor count of chunked selection (Appendix A.3), in double exactly as
+// the select kernel computes each chunk's share.
+static int64_t chunked_count(int64_t T, int64_t t, int64_t chunk_len) {
+  if (chunk_len <= 0 || T <= kChunkThresholdH) return t;
+  int64_t total = 0;
+  for (int64_t start = 0; start < T; start += chunk_len) {
+    const int64_t Tc = T - start < chunk_len ? T - start : chunk_len;
+    int64_t v = (int64_t)floor((double)t * (double)Tc / (double)T + 0.5);
+    v = v < 1 ? 1 : (v > Tc ? Tc : v);
+    total += v;
+  }
+  return total;
+}
 hipError_t launch_rowstats(int dtype, const void *K, const void *V, const void *Q, float *z, float *m, float *Y,
                            int B, int T, int n, float scale, hipStream_t s);
 hipError_t launch_profiles(int dtype, const void *Q, const void *K, const float *zmerge, const int32_t *anchors,
@@ -272,6 +289,7 @@ static arckv_status check_params(const arckv_fit_params *p) {
   if (p->max_escalations < 0 || p->max_escalations > 6) return ARCKV_ERR_INVALID_ARG;
   if (p->refine_steps < 0 || p->refine_steps > 4) return ARCKV_ERR_INVALID_ARG;
   if (p->pair_chunk < 0) return ARCKV_ERR_INVALID_ARG;
+  if (p->select_chunk < 0) return ARCKV_ERR_INVALID_ARG;
   return ARCKV_OK;
 }
 
@@ -450,6 +468,7 @@ arckv_status arckv_default_params(arckv_fit_params *p) {
   p->max_escalations = 3;
   p->refine_steps = 2;
   p->pair_chunk = 0;
+  p->select_chunk = 0;
   return ARCKV_OK;
 }
 
@@ -470,9 +489,35 @@ arckv_status arckv_workspace_size(const arckv_problem *prob, int32_t t, const ar
   arckv_default_params(&def);
   if (!p) p = &def;
   CHECK(check_params(p));
-  Dims d = make_dims(prob, t);
+  // with chunked selection t is the nominal budget: size for the realised count
+  const int64_t tr = chunked_count(prob->T, t, p->select_chunk);
+  Dims d = make_dims(prob, (int32_t)(tr > t ? tr : t));
   int64_t P = p->pair_chunk > 0 && p->pair_chunk < d.B ? p->pair_chunk : d.B;
   *bytes = plan_total(d, P);
+  return ARCKV_OK;
+}
+
+arckv_status arckv_budgets(int32_t P, const double *a, int32_t t, int64_t T, int32_t *t_out) {
+  if (P < 1 || !a || !t_out || t < 1 || T < 1) return ARCKV_ERR_INVALID_ARG;
+  if (T > (1ll << 30)) return ARCKV_ERR_UNSUPPORTED;
+  double sum = 0.0;
+  for (int32_t i = 0; i < P; ++i) {
+    if (!isfinite(a[i]) || a[i] < 0.0) return ARCKV_ERR_INVALID_ARG;
+    sum += a[i];
+  }
+  if (!(sum > 0.0) || !isfinite(sum)) return ARCKV_ERR_INVALID_ARG;
+  for (int32_t i = 0; i < P; ++i) {
+    double v = floor(a[i] / sum * (double)P * (double)t);
+    v = v < 1.0 ? 1.0 : (v > (double)T ? (double)T : v);
+    t_out[i] = (int32_t)v;
+  }
+  return ARCKV_OK;
+}
+
+arckv_status arckv_select_count(int64_t T, int32_t t, int32_t chunk_len, int32_t *t_real) {
+  if (!t_real || T < 1 || t < 1 || t > T || chunk_len < 0) return ARCKV_ERR_INVALID_ARG;
+  if (T > (1ll << 30)) return ARCKV_ERR_UNSUPPORTED;
+  *t_real = (int32_t)chunked_count(T, t, chunk_len);
   return ARCKV_OK;
 }
 
@@ -494,6 +539,15 @@ arckv_status arckv_select(const arckv_problem *prob, const float *scores, int32_
   (void)ws;
   (void)ws_bytes;
   STAGE(ST_SELECT, launch_select(scores, prob->B, prob->T, t, anchors, stream));
+  return ARCKV_OK;
+}
+
+arckv_status arckv_select_ex(const arckv_problem *prob, const float *scores, int32_t t, const int32_t *t_pair,
+                             int32_t chunk_len, int32_t t_stride, int32_t *anchors, hipStream_t stream) {
+  CHECK(check_problem(prob));
+  if (!scores || !anchors || t < 1 || t > prob->T || chunk_len < 0 || t_stride < 1) return ARCKV_ERR_INVALID_ARG;
+  if (!t_pair && t_stride < chunked_count(prob->T, t, chunk_len)) return ARCKV_ERR_INVALID_ARG;
+  STAGE(ST_SELECT, launch_select_ex(scores, prob->B, prob->T, t, t_pair, chunk_len, t_stride, anchors, stream));
   return ARCKV_OK;
 }
 
@@ -622,6 +676,8 @@ arckv_status arckv_compact(const arckv_problem *prob, const void *K, const void 
   if (!aligned(K, 16) || !aligned(V, 16) || !aligned(Q_ref, 16) || !aligned(ix->W1, 16)) return ARCKV_ERR_INVALID_ARG;
   int32_t t = 0;
   CHECK(arckv_budget(prob->T, rho, &t));
+  const int32_t t_nominal = t;
+  t = (int32_t)chunked_count(prob->T, t, p->select_chunk);   // realised count under chunked selection
   Ctx c;
   c.d = make_dims(prob, t);
   int64_t P = 0;
@@ -637,7 +693,7 @@ arckv_status arckv_compact(const arckv_problem *prob, const void *K, const void 
   float *zmax = c.pers<float>(c.pl.zmax), *phi = c.pers<float>(c.pl.phi);
   int32_t *kappa = c.pers<int32_t>(c.pl.kappa);
   STAGE(ST_SCORE, launch_score(d.dtype, K, V, ix->W1, ix->b1, ix->w2, ix->b2, scores, d.B, d.T, stream));
-  STAGE(ST_SELECT, launch_select(scores, d.B, d.T, t, anchors, stream));
+  STAGE(ST_SELECT, launch_select_ex(scores, d.B, d.T, t_nominal, nullptr, p->select_chunk, t, anchors, stream));
   STAGE(ST_ROWSTATS, launch_rowstats(d.dtype, K, V, Q_ref, z, m, Y, d.B, d.T, d.n, c.scale, stream));
   STAGE(ST_ZMAX, launch_zmax(z, d.B, d.n, zmax, stream));
   for (int b0 = 0; b0 < d.B; b0 += (int)P) {

@@ -1,6 +1,9 @@
-// Top-t anchor selection, S = TopK(scores, t) per pair (Section 3.3).
+// Top-t anchor selection, S = TopK(scores, t) per pair (Section 3.3), with the
+// optional per-pair budgets of eq. per_head_budget and the chunked selection of
+// Appendix A.3 (the union of each chunk's local top-t_c,
+// t_c = clip_[1,T_c](round(t T_c / T)), rounded half up).
 //
-// One workgroup of 1024 threads per pair.  Scores become order-preserving
+// One workgroup of 1024 threads per (pair, chunk).  Scores become order-preserving
 // uint32 keys (score_key).  Lane l of wave w owns the KPT consecutive positions
 // starting at (64 w + l) KPT, so positions ascend with (wave, lane, i).  When
 // T <= 32768 the keys are read once, coalesced, through a padded LDS copy and
@@ -26,6 +29,14 @@ constexpr int kSelThreads = 1024;
 constexpr int kSelWaves = kSelThreads / 64;
 constexpr int kSelBins = 2048;   // widest digit: 11 bits
 constexpr int kSelPasses = 3;
+constexpr int kSelChunkThreshold = 10000;   // chunked selection applies when T > 10,000
+
+// Anchors kept by a chunk of length Tc out of T for a pair budget tb; computed
+// in double exactly as on the host, so both agree on every rounding.
+__device__ inline int chunk_budget(int tb, int T, int Tc) {
+  const int v = (int)floor((double)tb * (double)Tc / (double)T + 0.5);
+  return min(Tc, max(1, v));
+}
 
 // Digit p of the key (from the top): bits [shift, shift + width).
 __device__ inline int sel_shift(int p) { return p == 0 ? 21 : p == 1 ? 10 : 0; }
@@ -42,16 +53,33 @@ __device__ inline uint32_t wave_incl_scan(uint32_t v, int lane) {
 }
 }  // namespace
 
-// KPT: keys per lane held in registers (T <= 1024 KPT); 0 = read from memory.
+struct SelArgs {
+  int T;                   // positions per pair
+  int t;                   // budget of every pair (when t_pair is null)
+  const int32_t *t_pair;   // per-pair budgets [B] (device), or null
+  int chunk_len;           // chunk length when nchunks > 1
+  int nchunks;             // chunks per pair (1 = global top-t)
+  int t_stride;            // row length of the anchors output
+};
+
+// KPT: keys per lane held in registers (chunk length <= 1024 KPT); 0 = read from memory.
 template <int KPT>
-__global__ void __launch_bounds__(kSelThreads) k_select_topt(const float *__restrict__ scores, int T, int t,
+__global__ void __launch_bounds__(kSelThreads) k_select_topt(const float *__restrict__ scores, SelArgs a,
                                                              int32_t *__restrict__ anchors) {
-  extern __shared__ uint32_t sel_keys[];   // [T + T/32] padded key copy (KPT > 0)
+  extern __shared__ uint32_t sel_keys[];   // [Tc + Tc/32] padded key copy (KPT > 0)
   __shared__ uint32_t hist[kSelBins];
   __shared__ uint32_t s_wtot[2][kSelWaves];
   __shared__ uint32_t s_prefix, s_remaining;
-  const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const float *s = scores + (size_t)b * T;
+  const int b = blockIdx.x / a.nchunks, chunk = blockIdx.x % a.nchunks;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // this workgroup's segment [seg0, seg0 + T) of the pair and its budget t
+  const int tb = a.t_pair ? min(max(a.t_pair[b], 1), a.T) : a.t;
+  const int seg0 = chunk * a.chunk_len;
+  const int T = a.nchunks > 1 ? min(a.chunk_len, a.T - seg0) : a.T;
+  const int t = a.nchunks > 1 ? chunk_budget(tb, a.T, T) : tb;
+  int off = 0;   // anchors kept by the earlier chunks of the pair
+  for (int c = 0; c < chunk; ++c) off += chunk_budget(tb, a.T, min(a.chunk_len, a.T - c * a.chunk_len));
+  const float *s = scores + (size_t)b * a.T + seg0;
   const int per = KPT > 0 ? KPT : (T + kSelThreads - 1) / kSelThreads;   // positions per lane
   const int p0 = tid * per;
   uint32_t kr[KPT > 0 ? KPT : 1];
@@ -130,31 +158,51 @@ __global__ void __launch_bounds__(kSelThreads) k_select_topt(const float *__rest
   }
   uint32_t out = gt_before + min(eq_before, remaining);
   uint32_t eq_seen = eq_before;
-  int32_t *dst = anchors + (size_t)b * t;
+  int32_t *dst = anchors + (size_t)b * a.t_stride;
+  const uint32_t lim = (uint32_t)min(off + t, a.t_stride);   // off + out < off + t by construction
+  out += (uint32_t)off;
   for_each([&](uint32_t k, int p, bool v) {
     const bool is_eq = v && k == kstar;
     const bool sel = v && (k > kstar || (is_eq && eq_seen < remaining));
-    if (sel && out < (uint32_t)t) dst[out] = p;   // out < t by construction
+    if (sel && out < lim) dst[out] = seg0 + p;
     out += sel;
     eq_seen += is_eq;
   });
+  // the pair's last chunk pads its row past the realised count
+  if (chunk == a.nchunks - 1)
+    for (int i = off + t + tid; i < a.t_stride; i += kSelThreads) dst[i] = -1;
 }
 
-hipError_t launch_select(const float *scores, int B, int T, int t, int32_t *anchors, hipStream_t s) {
-  const int per_lane = (T + kSelThreads - 1) / kSelThreads;
+// chunk_len <= 0 or T <= 10000: global top-t.  t_pair (device, nullable)
+// overrides t per pair; rows of `anchors` are t_stride long, padded with -1.
+hipError_t launch_select_ex(const float *scores, int B, int T, int t, const int32_t *t_pair, int chunk_len,
+                            int t_stride, int32_t *anchors, hipStream_t s) {
+  SelArgs a;
+  a.T = T;
+  a.t = t;
+  a.t_pair = t_pair;
+  a.nchunks = (chunk_len > 0 && T > kSelChunkThreshold) ? (T + chunk_len - 1) / chunk_len : 1;
+  a.chunk_len = a.nchunks > 1 ? chunk_len : T;
+  a.t_stride = t_stride;
+  const int seg = a.nchunks > 1 ? a.chunk_len : T;
+  const int per_lane = (seg + kSelThreads - 1) / kSelThreads;
   auto go = [&](auto kern, bool cached) {
-    const size_t lds = cached ? (size_t)(T + T / 32 + 1) * sizeof(uint32_t) : 0;
+    const size_t lds = cached ? (size_t)(seg + seg / 32 + 1) * sizeof(uint32_t) : 0;
     if (lds > 48 * 1024) {
       hipError_t e = hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
       if (e != hipSuccess) return e;
     }
-    hipLaunchKernelGGL(kern, dim3(B), dim3(kSelThreads), lds, s, scores, T, t, anchors);
+    hipLaunchKernelGGL(kern, dim3((unsigned)(B * a.nchunks)), dim3(kSelThreads), lds, s, scores, a, anchors);
     return hipGetLastError();
   };
   if (per_lane <= 8) return go(k_select_topt<8>, true);
   if (per_lane <= 16) return go(k_select_topt<16>, true);
   if (per_lane <= 32) return go(k_select_topt<32>, true);
   return go(k_select_topt<0>, false);
+}
+
+hipError_t launch_select(const float *scores, int B, int T, int t, int32_t *anchors, hipStream_t s) {
+  return launch_select_ex(scores, B, T, t, nullptr, 0, t, anchors, s);
 }
 
 }  // namespace arckv

@@ -175,3 +175,31 @@ def test_attend_workspace_and_validation():
         A.ERR_WORKSPACE
     assert L.arckv_attend(2, 4, 10, 0, 0.0, fake, fake, None, fake, None, None, fake, ctypes.c_void_p(0x1010), nws,
                           None) == A.ERR_WORKSPACE
+
+
+def test_budgets_and_select_count_match_oracle():
+    import numpy as np
+    import oracle
+    g = np.random.default_rng(0)
+    for T in (5000, 10000, 10001, 12000, 20001, 50000, 131072):
+        for t in (1, 77, max(1, T // 10), T // 3):
+            for L in (0, 4096, 7000, 8192, 200000):
+                want = sum(c[2] for c in oracle.chunk_budgets(t, T, L))
+                assert A.select_count(T, t, L) == want, (T, t, L)
+    for P in (1, 8, 256):
+        w = g.uniform(0, 1, P)
+        assert A.budgets(list(w), 3277, 32768) == oracle.budgets_per_pair(w, 3277, 32768).tolist()
+    assert A.budgets([0, 0.5, 9.5], 10, 20) == [1, 1, 20]
+    for a, t, T in (([0, 0], 10, 20), ([-1, 2], 10, 20), ([float("nan")], 5, 10), ([1], 0, 10)):
+        with pytest.raises(A.ArckvError):
+            A.budgets(a, t, T)
+    with pytest.raises(A.ArckvError):
+        A.select_count(100, 101, 0)
+
+
+def test_workspace_covers_chunked_count():
+    p = A.problem_from_dims(2, 131072, 512)
+    nominal = A.budget(131072, 0.01)
+    assert A.select_count(131072, nominal, 8192) > nominal
+    assert A.workspace_size(p, nominal, A.default_params(select_chunk=8192)) >= \
+        A.workspace_size(p, A.select_count(131072, nominal, 8192))

@@ -484,3 +484,56 @@ def test_joint_attention_bias_shift():
         wf = np.exp(s * (Kf @ q))
         mix = (math.exp(c) * (wc @ Cv) + wf @ Vf) / (math.exp(c) * wc.sum() + wf.sum())
         np.testing.assert_allclose(got[i], mix, rtol=1e-12, atol=1e-13)
+
+
+# ----------------------------------------------------------------- O0/O2 per-pair budgets, chunked selection
+def test_budgets_per_pair_closed_form():
+    # uniform weights give every pair the nominal budget
+    assert oracle.budgets_per_pair(np.ones(8), 819, 8192).tolist() == [819] * 8
+    # a = (1, 2, 3, 4)/10, |P| t = 400: floor(40, 80, 120, 160)
+    assert oracle.budgets_per_pair([1, 2, 3, 4], 100, 1000).tolist() == [40, 80, 120, 160]
+    # floor then clip to [1, T]: a = (0, 0.5, 9.5)/10 with |P| t = 30 -> floor(0, 1.5, 28.5) -> (1, 1, 28), T = 20 -> 20
+    assert oracle.budgets_per_pair([0, 0.5, 9.5], 10, 20).tolist() == [1, 1, 20]
+    g = rng(3)
+    a = g.uniform(0, 1, 256)
+    tb = oracle.budgets_per_pair(a, 3277, 32768)
+    assert 256 * 3277 - 256 <= tb.sum() <= 256 * 3277          # floor loses < 1 per pair
+    with pytest.raises(ValueError):
+        oracle.budgets_per_pair([0, 0], 10, 20)
+
+
+def test_chunk_budgets_values():
+    # below the threshold, or chunking off: one chunk with the nominal budget
+    assert oracle.chunk_budgets(819, 8192, 8192) == [(0, 8192, 819)]
+    assert oracle.chunk_budgets(3277, 32768, 0) == [(0, 32768, 3277)]
+    # 32768 = 4 x 8192; 3277 * 8192 / 32768 = 819.25 -> 819 each
+    assert oracle.chunk_budgets(3277, 32768, 8192) == [(0, 8192, 819), (8192, 8192, 819), (16384, 8192, 819),
+                                                       (24576, 8192, 819)]
+    # 131072 = 16 x 8192; 1311 / 16 = 81.94 -> 82 each, 1312 realised
+    cb = oracle.chunk_budgets(1311, 131072, 8192)
+    assert len(cb) == 16 and all(c[2] == 82 for c in cb)
+    # ragged last chunk: 12000 = 8192 + 3808; 100 * 8192 / 12000 = 68.27 -> 68, 100 * 3808 / 12000 = 31.73 -> 32
+    assert oracle.chunk_budgets(100, 12000, 8192) == [(0, 8192, 68), (8192, 3808, 32)]
+    # a single chunk covering everything keeps t; tiny t is clipped up to one per chunk
+    assert oracle.chunk_budgets(500, 12000, 20000) == [(0, 12000, 500)]
+    assert [c[2] for c in oracle.chunk_budgets(1, 40000, 8192)] == [1] * 5
+    # chunks tile [0, T)
+    for T, L in [(10001, 8192), (131072, 8192), (50000, 7000)]:
+        cb = oracle.chunk_budgets(T // 10, T, L)
+        assert cb[0][0] == 0 and sum(c[1] for c in cb) == T
+        assert all(a[0] + a[1] == b[0] for a, b in zip(cb, cb[1:]))
+
+
+@pytest.mark.parametrize("T,t,L,seed", [(12000, 1200, 8192, 0), (20001, 77, 5000, 1), (9000, 900, 4096, 2)])
+def test_chunked_select_bruteforce(T, t, L, seed):
+    g = rng(seed)
+    s = np.round(g.standard_normal(T), 2)          # many duplicates: ties resolved by position
+    got = oracle.select_topt_chunked(s, t, L)
+    ref = []
+    for start, Tc, tc in oracle.chunk_budgets(t, T, L):
+        idx = sorted(range(start, start + Tc), key=lambda j: (-s[j], j))[:tc]
+        ref += sorted(idx)
+    assert got.tolist() == ref
+    assert np.all(np.diff(got) > 0)
+    if T <= oracle.CHUNK_THRESHOLD:
+        assert got.tolist() == oracle.select_topt(s, t).tolist()
