@@ -21,6 +21,9 @@ step by step from the paper's equations:
   O7  mass bias fit          eq. (mass_fit), Appendix A.9
   O8  compact value fit      eq. (value_lstsq), Appendix A.9
   O9  compact attention      eq. (compact_attention), Section 3.1
+  O1' value-aware indexer    eq. (value_context), (indexer_projection),
+                             (pairwise_index_score) of Appendix A.1, pooled
+                             by eq. (indexer_pooling)
   O10 joint decode attention eq. (concatenated_attention_preservation),
                              Appendix A.7: compact block with bias beta,
                              then an uncompressed block with zero bias
@@ -118,6 +121,80 @@ def pool_rms(I_rows: np.ndarray) -> np.ndarray:
     e = np.exp(I_rows - zmax)
     pi = e / e.sum(axis=1, keepdims=True)
     return np.sqrt(np.mean(pi * pi, axis=0))
+
+
+# --------------------------------------------------------------------------- O1' value-aware indexer
+@dataclasses.dataclass
+class DSAIndexer:
+    """Per-pair parameters of the value-aware indexer (Appendix A.1,
+    eq. indexer_parameters and value_indexer_parameters):
+    L_q, L_k [H_I d_I][d]; L_x [H_I][d_x]; b_x [H_I]; U_q, U_k, U_v [d_A][d];
+    L_c [H_I d_I][d_A]; L_v [H_I d_I][d]."""
+    L_q: np.ndarray
+    L_k: np.ndarray
+    L_x: np.ndarray
+    b_x: np.ndarray
+    U_q: np.ndarray
+    U_k: np.ndarray
+    U_v: np.ndarray
+    L_c: np.ndarray
+    L_v: np.ndarray
+
+    @property
+    def H_I(self):
+        return self.L_x.shape[0]
+
+    @property
+    def d_I(self):
+        return self.L_q.shape[0] // self.L_x.shape[0]
+
+
+RMS_EPS = 1e-6        # eq. indexer_projection: N(z) = z / sqrt(||z||^2 / d_I + 1e-6)
+LEAKY_SLOPE = 0.1     # eq. pairwise_index_score: LeakyReLU_{0.1}
+
+
+def rms_blocks(Z: np.ndarray, H: int, dI: int) -> np.ndarray:
+    """Parameter-free RMS normalisation of each width-d_I block of the rows of Z."""
+    Zb = np.asarray(Z, np.float64).reshape(Z.shape[0], H, dI)
+    return (Zb / np.sqrt((Zb * Zb).sum(axis=2, keepdims=True) / dI + RMS_EPS)).reshape(Z.shape[0], H * dI)
+
+
+def leaky_relu(x, slope: float = LEAKY_SLOPE):
+    return np.where(x >= 0, x, slope * x)
+
+
+def dsa_logits(Q, X, K, V, ix: DSAIndexer, n_pos: int, scale_a: float, rnd=None) -> np.ndarray:
+    """Indexer logits I [n][T] for reference rows i = (g, r) ordered [query
+    head][position] (r = i mod n_pos), whose activation x_r (rows of X) is
+    shared by the query heads at position r.
+
+      value context   c_i = softmax_j(s_A (U_q q_i).(U_k k_j)) (U_v v_j)      eq. value_context
+      projections     qbar_i = N(L_q q_i + L_c c_i), kbar_j = N(L_k k_j + L_v v_j),
+                      w_i = L_x x_r + b_x                                    eq. indexer_projection
+      logits          I_ij = sum_a w_ia LeakyReLU(qbar_ia . kbar_ja / sqrt(d_I))  eq. pairwise_index_score
+
+    s_A is the logit scale of the value-attention head (reading: 1/sqrt(d_A),
+    as for every attention logit here).  ``rnd`` (e.g. round_to(., "bf16"))
+    is applied where a low-precision implementation stores intermediates: the
+    projected q, k, v of the value head, the context c, and qbar, kbar."""
+    r = rnd if rnd is not None else (lambda a: a)
+    Q, X, K, V = (np.asarray(a, np.float64) for a in (Q, X, K, V))
+    H, dI = ix.H_I, ix.d_I
+    qa = r(Q @ ix.U_q.T)
+    ka = r(K @ ix.U_k.T)
+    va = r(V @ ix.U_v.T)
+    Lg = scale_a * (qa @ ka.T)
+    Lg -= Lg.max(axis=1, keepdims=True)
+    A = np.exp(Lg)
+    c = r((A / A.sum(axis=1, keepdims=True)) @ va)
+    qbar = r(rms_blocks(Q @ ix.L_q.T + c @ ix.L_c.T, H, dI))
+    kbar = r(rms_blocks(K @ ix.L_k.T + V @ ix.L_v.T, H, dI))
+    w = (X @ ix.L_x.T + ix.b_x)[np.arange(Q.shape[0]) % n_pos]          # [n][H]
+    I = np.zeros((Q.shape[0], K.shape[0]))
+    for a in range(H):
+        blk = slice(a * dI, (a + 1) * dI)
+        I += w[:, a:a + 1] * leaky_relu(qbar[:, blk] @ kbar[:, blk].T / math.sqrt(dI))
+    return I
 
 
 # --------------------------------------------------------------------------- O2

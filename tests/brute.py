@@ -146,6 +146,46 @@ def joint_attend(Q, C_k, beta, C_v, K_f, V_f, scale):
     return out
 
 
+def dsa_logits(Q, X, K, V, P, n_pos, scale_a, H, dI):
+    """Value-aware indexer logits by explicit loops (P: dict of parameter lists)."""
+    def mat(Mx, x):
+        return [sum(float(Mx[o][c]) * float(x[c]) for c in range(len(x))) for o in range(len(Mx))]
+    n, T = len(Q), len(K)
+    qa = [mat(P["U_q"], q) for q in Q]
+    ka = [mat(P["U_k"], k) for k in K]
+    va = [mat(P["U_v"], v) for v in V]
+    cs = []
+    for i in range(n):
+        lg = [scale_a * dot(qa[i], ka[j]) for j in range(T)]
+        mx = max(lg)
+        e = [math.exp(x - mx) for x in lg]
+        z = sum(e)
+        cs.append([sum(e[j] * va[j][c] for j in range(T)) / z for c in range(len(va[0]))])
+
+    def rms(z):
+        out = []
+        for a in range(H):
+            blk = z[a * dI:(a + 1) * dI]
+            den = math.sqrt(sum(x * x for x in blk) / dI + 1e-6)
+            out += [x / den for x in blk]
+        return out
+    qbar = [rms([u + w for u, w in zip(mat(P["L_q"], Q[i]), mat(P["L_c"], cs[i]))]) for i in range(n)]
+    kbar = [rms([u + w for u, w in zip(mat(P["L_k"], K[j]), mat(P["L_v"], V[j]))]) for j in range(T)]
+    out = []
+    for i in range(n):
+        x = X[i % n_pos]
+        w = [sum(float(P["L_x"][a][c]) * float(x[c]) for c in range(len(x))) + float(P["b_x"][a]) for a in range(H)]
+        row = []
+        for j in range(T):
+            tot = 0.0
+            for a in range(H):
+                sc = sum(qbar[i][a * dI + c] * kbar[j][a * dI + c] for c in range(dI)) / math.sqrt(dI)
+                tot += w[a] * (sc if sc >= 0 else 0.1 * sc)
+            row.append(tot)
+        out.append(row)
+    return out
+
+
 def round_bf16(x):
     """Nearest-even bfloat16 value of float x (via its float32 bit pattern)."""
     import struct

@@ -5,6 +5,7 @@ Each test checks the oracle against a brute-force loop written separately
 routine that solves the same problem another way, or a value printed in the
 workload definitions.  No GPU involved.
 """
+import dataclasses
 import math
 import os
 
@@ -537,3 +538,83 @@ def test_chunked_select_bruteforce(T, t, L, seed):
     assert np.all(np.diff(got) > 0)
     if T <= oracle.CHUNK_THRESHOLD:
         assert got.tolist() == oracle.select_topt(s, t).tolist()
+
+
+# ----------------------------------------------------------------- O1' value-aware indexer
+def _dsa_case(seed, n_pos=3, G=2, T=7, d=5, dx=6, H=2, dI=3, dA=4, zero_value=False):
+    g = rng(seed)
+    ix = oracle.DSAIndexer(
+        L_q=g.standard_normal((H * dI, d)), L_k=g.standard_normal((H * dI, d)), L_x=g.standard_normal((H, dx)),
+        b_x=g.standard_normal(H), U_q=g.standard_normal((dA, d)) / math.sqrt(d),
+        U_k=g.standard_normal((dA, d)) / math.sqrt(d), U_v=g.standard_normal((dA, d)) / math.sqrt(d),
+        L_c=np.zeros((H * dI, dA)) if zero_value else g.standard_normal((H * dI, dA)),
+        L_v=np.zeros((H * dI, d)) if zero_value else g.standard_normal((H * dI, d)))
+    Q = g.standard_normal((G * n_pos, d))
+    X = g.standard_normal((n_pos, dx))
+    K = g.standard_normal((T, d))
+    V = g.standard_normal((T, d))
+    return Q, X, K, V, ix, n_pos
+
+
+@pytest.mark.parametrize("seed", [0, 1])
+def test_dsa_logits_bruteforce(seed):
+    Q, X, K, V, ix, n_pos = _dsa_case(seed)
+    got = oracle.dsa_logits(Q, X, K, V, ix, n_pos, 0.5)
+    P = {k: getattr(ix, k).tolist() for k in ("L_q", "L_k", "L_x", "b_x", "U_q", "U_k", "U_v", "L_c", "L_v")}
+    ref = np.array(brute.dsa_logits(Q.tolist(), X.tolist(), K.tolist(), V.tolist(), P, n_pos, 0.5, ix.H_I, ix.d_I))
+    np.testing.assert_allclose(got, ref, rtol=1e-11, atol=1e-11)
+
+
+def test_dsa_zero_value_path_reproduces_query_key_logits():
+    """With L_c = L_v = 0 (their initialisation) the logits are those of the
+    query-key-only scorer (Appendix A.1): sum_a w_a LeakyReLU(N(L_q q)_a . N(L_k k)_a / sqrt(d_I)),
+    whatever U_q, U_k, U_v are."""
+    Q, X, K, V, ix, n_pos = _dsa_case(2, T=9, zero_value=True)
+    got = oracle.dsa_logits(Q, X, K, V, ix, n_pos, 1.0)
+    H, dI = ix.H_I, ix.d_I
+    ref = np.zeros_like(got)
+    for i, q in enumerate(Q):
+        w = ix.L_x @ X[i % n_pos] + ix.b_x
+        qb = (ix.L_q @ q).reshape(H, dI)
+        qb /= np.sqrt((qb ** 2).mean(axis=1, keepdims=True) + 1e-6)
+        for j, k in enumerate(K):
+            kb = (ix.L_k @ k).reshape(H, dI)
+            kb /= np.sqrt((kb ** 2).mean(axis=1, keepdims=True) + 1e-6)
+            sc = (qb * kb).sum(axis=1) / math.sqrt(dI)
+            ref[i, j] = float(w @ np.maximum(sc, 0.1 * sc))
+    np.testing.assert_allclose(got, ref, rtol=1e-12, atol=1e-12)
+    # and the value head's weights do not enter
+    ix2 = dataclasses.replace(ix, U_q=ix.U_q * 3.0, U_v=-ix.U_v)
+    np.testing.assert_allclose(oracle.dsa_logits(Q, X, K, V, ix2, n_pos, 1.0), got, rtol=1e-12, atol=1e-12)
+
+
+def test_dsa_building_blocks():
+    g = rng(4)
+    Z = g.standard_normal((5, 12)) * 7.0
+    N = oracle.rms_blocks(Z, 3, 4).reshape(5, 3, 4)
+    ms = (Z.reshape(5, 3, 4) ** 2).mean(axis=2)
+    np.testing.assert_allclose((N ** 2).mean(axis=2), ms / (ms + 1e-6), rtol=1e-12)   # unit RMS up to the guard
+    assert np.all(np.sign(N) == np.sign(Z.reshape(5, 3, 4)))
+    x = np.array([-2.0, -0.5, 0.0, 0.5, 3.0])
+    np.testing.assert_array_equal(oracle.leaky_relu(x), [-0.2, -0.05, 0.0, 0.5, 3.0])
+    # the value context is the full attention of the projected cache (row statistics' Y)
+    Q, X, K, V, ix, n_pos = _dsa_case(5, T=11)
+    qa, ka, va = Q @ ix.U_q.T, K @ ix.U_k.T, V @ ix.U_v.T
+    _, _, Y = oracle.rowstats(qa, ka, va, 0.7)
+    A = np.exp(0.7 * qa @ ka.T)
+    np.testing.assert_allclose((A / A.sum(axis=1, keepdims=True)) @ va, Y, rtol=1e-12)
+
+
+def test_pool_rms_properties():
+    g = rng(6)
+    I = g.standard_normal((6, 9))
+    s = oracle.pool_rms(I)
+    pi = np.exp(I) / np.exp(I).sum(axis=1, keepdims=True)
+    np.testing.assert_allclose(s, np.sqrt((pi ** 2).mean(axis=0)), rtol=1e-12)
+    # identical rows reduce to that row's softmax (the query-independent scorer's case)
+    row = g.standard_normal(9)
+    np.testing.assert_allclose(oracle.pool_rms(np.tile(row, (4, 1))), np.exp(row) / np.exp(row).sum(), rtol=1e-12)
+    # a constant added to a row leaves the pooled scores unchanged
+    I2 = I.copy()
+    I2[2] += 5.0
+    np.testing.assert_allclose(oracle.pool_rms(I2), s, rtol=1e-12)
