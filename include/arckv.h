@@ -124,6 +124,40 @@ arckv_status arckv_workspace_size(const arckv_problem *prob, int32_t t,
 arckv_status arckv_score(const arckv_problem *prob, const void *K, const void *V,
                          const arckv_indexer *ix, float *scores, hipStream_t stream);
 
+/* The value-aware indexer of Appendix A.1 (eq. value_context,
+ * indexer_projection, pairwise_index_score) with H_I = 8 index heads of width
+ * d_I = 128 and a value head of width d_A = 128.  All matrices bfloat16,
+ * row-major, per pair (B pairs in a call):
+ *   L_q, L_k, L_c, L_v [B][1024][128];  U_q, U_k, U_v [B][128][128];
+ *   L_x [B][8][d_x];  b_x [B][8] float32;
+ *   X_ref [B / x_group][n_pos][d_x]: the activation x_r of reference position r,
+ *   shared by the query heads of a position and by the x_group consecutive
+ *   pairs of one layer (its KV heads).
+ * Q_ref rows are ordered [query head][position], so row i uses x_{i mod n_pos}. */
+typedef struct {
+  int32_t n_pos;      /* reference positions; n must be a multiple of n_pos */
+  int32_t d_x;        /* activation width, >= 1 */
+  int32_t x_group;    /* pairs sharing one X_ref block, >= 1 */
+  float scale_a;      /* logit scale of the value head; <= 0 selects 1/sqrt(d_A) */
+  const void *X_ref;
+  const void *L_q, *L_k, *L_x;
+  const float *b_x;
+  const void *U_q, *U_k, *U_v;
+  const void *L_c, *L_v;
+} arckv_dsa_indexer;
+
+/* Workspace for arckv_score_dsa with pair_chunk pairs in flight (0 = all B). */
+arckv_status arckv_dsa_workspace_size(const arckv_problem *prob, int32_t pair_chunk, size_t *bytes);
+
+/* Stage 1a with the value-aware indexer: pooled scores s_j of eq.
+ * indexer_pooling, s_j = sqrt(mean_i softmax_j(I_i,:)_j^2), for every cached
+ * token of every pair -> scores [B][T] float32 (rank them with arckv_select).
+ * K, V, Q_ref bfloat16 only.  Intermediates (the value head's projections and
+ * context, qbar, kbar) are stored in bfloat16; accumulation is float32. */
+arckv_status arckv_score_dsa(const arckv_problem *prob, const void *K, const void *V,
+                             const void *Q_ref, const arckv_dsa_indexer *ix, float *scores,
+                             void *ws, size_t ws_bytes, hipStream_t stream);
+
 /* Stage 1b: anchors S = TopK(scores, t) per pair (Section 3.3, eq.
  * persistent_support), written ascending to anchors [B][t].  Order: larger
  * score first, ties to the lower index, -0 equal to +0, NaN below every number.
@@ -234,6 +268,15 @@ arckv_status arckv_attend_workspace_size(int32_t P, int32_t G, int32_t t, int32_
 arckv_status arckv_attend(int32_t P, int32_t G, int32_t t, int32_t F, float scale, const void *Q,
                           const void *C_k, const float *beta, const void *C_v, const void *K_f,
                           const void *V_f, float *out, void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* arckv_compact with the scoring stage replaced by caller-supplied scores
+ * [B][T] float32 (for instance from arckv_score_dsa): select, row statistics,
+ * merge and both fits exactly as arckv_compact. */
+arckv_status arckv_compact_scored(const arckv_problem *prob, const void *K, const void *V,
+                                  const void *Q_ref, const float *scores, double rho,
+                                  const arckv_fit_params *p, int32_t *t_out, int32_t *anchors,
+                                  float *C_k, float *beta, float *C_v, int32_t *info,
+                                  void *ws, size_t ws_bytes, hipStream_t stream);
 
 /* Human-readable name of a status code (static string). */
 const char *arckv_status_string(arckv_status s);

@@ -26,6 +26,7 @@ ENTRY_POINTS = (
     "arckv_rowstats", "arckv_merge", "arckv_fit_bias", "arckv_fit_values", "arckv_compact",
     "arckv_status_string", "arckv_set_timing", "arckv_stage_times", "arckv_reset_timing",
     "arckv_attend_workspace_size", "arckv_attend", "arckv_budgets", "arckv_select_count", "arckv_select_ex",
+    "arckv_dsa_workspace_size", "arckv_score_dsa", "arckv_compact_scored",
 )
 
 
@@ -51,6 +52,14 @@ class FitParams(ctypes.Structure):
                 ("bias_mode", ctypes.c_int32), ("max_escalations", ctypes.c_int32),
                 ("refine_steps", ctypes.c_int32), ("pair_chunk", ctypes.c_int32),
                 ("select_chunk", ctypes.c_int32)]
+
+
+class DSAIndexer(ctypes.Structure):
+    _fields_ = [("n_pos", ctypes.c_int32), ("d_x", ctypes.c_int32), ("x_group", ctypes.c_int32),
+                ("scale_a", ctypes.c_float), ("X_ref", ctypes.c_void_p), ("L_q", ctypes.c_void_p),
+                ("L_k", ctypes.c_void_p), ("L_x", ctypes.c_void_p), ("b_x", ctypes.c_void_p),
+                ("U_q", ctypes.c_void_p), ("U_k", ctypes.c_void_p), ("U_v", ctypes.c_void_p),
+                ("L_c", ctypes.c_void_p), ("L_v", ctypes.c_void_p)]
 
 
 _LIB = None
@@ -85,6 +94,10 @@ def lib():
         L.arckv_budgets.argtypes = [i32, P(ctypes.c_double), i32, ctypes.c_int64, P(i32)]
         L.arckv_select_count.argtypes = [ctypes.c_int64, i32, i32, P(i32)]
         L.arckv_select_ex.argtypes = [P(Problem), vp, i32, vp, i32, i32, vp, vp]
+        L.arckv_dsa_workspace_size.argtypes = [P(Problem), i32, P(sz)]
+        L.arckv_score_dsa.argtypes = [P(Problem), vp, vp, vp, P(DSAIndexer), vp, vp, sz, vp]
+        L.arckv_compact_scored.argtypes = [P(Problem), vp, vp, vp, vp, ctypes.c_double, P(FitParams), P(i32),
+                                           vp, vp, vp, vp, vp, vp, sz, vp]
         L.arckv_attend.argtypes = [i32, i32, i32, i32, ctypes.c_float, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
         for name in ENTRY_POINTS:
             getattr(L, name).restype = ctypes.c_int if name != "arckv_status_string" else ctypes.c_char_p
@@ -302,6 +315,47 @@ def attend(Q, C_k, beta, C_v, K_f=None, V_f=None, scale=None) -> torch.Tensor:
     t = C_k.shape[1] if C_k is not None else 0
     F = K_f.shape[1] if K_f is not None else 0
     return Attender(P, G, t, F, Q.device, scale)(Q, C_k, beta, C_v, K_f, V_f)
+
+
+DSA_FIELDS = ("L_q", "L_k", "L_x", "b_x", "U_q", "U_k", "U_v", "L_c", "L_v")
+
+
+def dsa_indexer(X_ref, params: dict, n_pos: int, x_group: int = 1, scale_a: Optional[float] = None) -> DSAIndexer:
+    """params: tensors L_q, L_k, L_c, L_v [B][1024][128], U_q/U_k/U_v [B][128][128], L_x [B][8][d_x] (bf16) and
+    b_x [B][8] (fp32); X_ref [B / x_group][n_pos][d_x] bf16."""
+    return DSAIndexer(int(n_pos), int(X_ref.shape[-1]), int(x_group), float(scale_a) if scale_a else 0.0,
+                      _ptr(X_ref), *[_ptr(params[k]) for k in DSA_FIELDS])
+
+
+def dsa_workspace_size(prob: Problem, pair_chunk: int = 0) -> int:
+    out = ctypes.c_size_t()
+    _check(lib().arckv_dsa_workspace_size(ctypes.byref(prob), int(pair_chunk), ctypes.byref(out)),
+           "arckv_dsa_workspace_size")
+    return out.value
+
+
+def score_dsa(K, V, Q, X_ref, params: dict, n_pos: int, x_group: int = 1, scale_a=None, pair_chunk: int = 0):
+    """Pooled value-aware-indexer scores [B][T] (arckv_score_dsa)."""
+    prob = problem(K, Q)
+    ix = dsa_indexer(X_ref, params, n_pos, x_group, scale_a)
+    out = torch.empty(K.shape[0], K.shape[1], dtype=torch.float32, device=K.device)
+    nbytes = dsa_workspace_size(prob, pair_chunk)
+    ws = _workspace(nbytes, K.device)
+    _check(lib().arckv_score_dsa(ctypes.byref(prob), _ptr(K), _ptr(V), _ptr(Q), ctypes.byref(ix), _ptr(out), _ptr(ws),
+                                 nbytes, _stream()), "arckv_score_dsa")
+    return out
+
+
+def compact_scored(K, V, Q, scores, rho, scale=None, params: Optional[FitParams] = None):
+    """arckv_compact_scored: the compaction path on given scores; returns (anchors, C_k, beta, C_v, info)."""
+    B, T, _ = K.shape
+    c = Compactor(B, T, Q.shape[1], rho, K.dtype, K.device, scale, params)
+    t_out = ctypes.c_int32()
+    _check(lib().arckv_compact_scored(ctypes.byref(c.prob), _ptr(K), _ptr(V), _ptr(Q), _ptr(scores), c.rho,
+                                      ctypes.byref(c.params), ctypes.byref(t_out), _ptr(c.anchors), _ptr(c.C_k),
+                                      _ptr(c.beta), _ptr(c.C_v), _ptr(c.info), _ptr(c.ws), c.ws_bytes, _stream()),
+           "arckv_compact_scored")
+    return c.anchors, c.C_k, c.beta, c.C_v, c.info
 
 
 class Compactor:

@@ -11,6 +11,7 @@
 #include "arckv.h"
 
 namespace arckv {
+typedef uint16_t bf16_t_;   // bfloat16 storage, opaque on the host
 constexpr int kHeadDimH = 128;
 constexpr int64_t kPadH = 256;
 inline int64_t rup(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
@@ -87,6 +88,14 @@ hipError_t launch_values_out(const float *Xp, int B, int64_t tp, int t, const in
 hipError_t launch_copy_info(const int32_t *a, const int32_t *b, int B, int32_t *info, hipStream_t s);
 hipError_t launch_copy_f32(const float *src, float *dst, int B, hipStream_t s);
 int attend_chunks(int t, int F);
+hipError_t launch_dsa_proj(const void *X1, const void *X2, bool x2_f32, const void *W1, const void *W2, int B,
+                           int nrows, int n_blocks, bool norm, void *out, hipStream_t s);
+hipError_t launch_dsa_w(const void *X, const void *Lx, const float *bx, int B, int n_pos, int dx, int x_group,
+                        int p_off, float *w, hipStream_t s);
+hipError_t launch_dsa_index(int pass, const void *qbar, const void *kbar, const float *w, int B, int n, int n_pos,
+                            int T, float *z, float *m, float *part, hipStream_t s);
+hipError_t launch_dsa_pool(const float *part, int B, int n, int T, float *scores, hipStream_t s);
+int dsa_query_blocks(int n);
 hipError_t launch_attend(int P, int G, int t, int F, float scale, const void *Q, const void *Ck, const float *beta,
                          const void *Cv, const void *Kf, const void *Vf, float *part_o, float *part_ml, float *out,
                          hipStream_t s);
@@ -95,12 +104,12 @@ hipError_t launch_attend(int P, int G, int t, int F, float scale, const void *Q,
 enum Stage {
   ST_SCORE, ST_SELECT, ST_ROWSTATS, ST_ZMAX, ST_PROFILES, ST_ANCHOR_PROF, ST_ASSIGN, ST_FINALIZE, ST_MERGE,
   ST_PHIC, ST_GRAM_G, ST_CHOL_G, ST_SOLVE_W, ST_PHAT, ST_GRAM_A, ST_RHS, ST_CHOL_A, ST_SOLVE_V, ST_ATTEND,
-  ST_COUNT
+  ST_DSA_PROJ, ST_DSA_VALUE, ST_DSA_INDEX, ST_COUNT
 };
 static const char *kStageNames[ST_COUNT] = {
     "score", "select", "rowstats", "zmax", "profiles", "anchor_profiles", "assign_gemm", "assign_finalize",
     "merge", "phic", "gram_G", "chol_G", "solve_beta", "phat", "gram_A", "rhs_B", "chol_A", "solve_values",
-    "attend"};
+    "attend", "dsa_proj", "dsa_value_head", "dsa_index"};
 
 struct TimingState {
   std::mutex mu;
@@ -661,19 +670,25 @@ arckv_status arckv_fit_values(const arckv_problem *prob, const void *Q_ref, cons
   return ARCKV_OK;
 }
 
-arckv_status arckv_compact(const arckv_problem *prob, const void *K, const void *V, const void *Q_ref,
-                           const arckv_indexer *ix, double rho, const arckv_fit_params *p, int32_t *t_out,
-                           int32_t *anchors, float *C_k, float *beta, float *C_v, int32_t *info, void *ws,
-                           size_t ws_bytes, hipStream_t stream) {
+// arckv_compact (ix given) and arckv_compact_scored (scores_in given).
+static arckv_status compact_impl(const arckv_problem *prob, const void *K, const void *V, const void *Q_ref,
+                                 const arckv_indexer *ix, const float *scores_in, double rho,
+                                 const arckv_fit_params *p, int32_t *t_out, int32_t *anchors, float *C_k,
+                                 float *beta, float *C_v, int32_t *info, void *ws, size_t ws_bytes,
+                                 hipStream_t stream) {
   arckv_fit_params def;
   arckv_default_params(&def);
   if (!p) p = &def;
   CHECK(check_problem(prob));
   CHECK(check_params(p));
-  if (!K || !V || !Q_ref || !ix || !t_out || !anchors || !C_k || !beta || !C_v || !info) return ARCKV_ERR_INVALID_ARG;
-  if (!ix->W1 || !ix->b1 || !ix->w2 || !ix->b2) return ARCKV_ERR_INVALID_ARG;
-  if (ix->hidden != 64 || ix->w1_dtype != prob->dtype) return ARCKV_ERR_UNSUPPORTED;
-  if (!aligned(K, 16) || !aligned(V, 16) || !aligned(Q_ref, 16) || !aligned(ix->W1, 16)) return ARCKV_ERR_INVALID_ARG;
+  if (!K || !V || !Q_ref || !t_out || !anchors || !C_k || !beta || !C_v || !info) return ARCKV_ERR_INVALID_ARG;
+  if (!ix && !scores_in) return ARCKV_ERR_INVALID_ARG;
+  if (ix) {
+    if (!ix->W1 || !ix->b1 || !ix->w2 || !ix->b2) return ARCKV_ERR_INVALID_ARG;
+    if (ix->hidden != 64 || ix->w1_dtype != prob->dtype) return ARCKV_ERR_UNSUPPORTED;
+    if (!aligned(ix->W1, 16)) return ARCKV_ERR_INVALID_ARG;
+  }
+  if (!aligned(K, 16) || !aligned(V, 16) || !aligned(Q_ref, 16)) return ARCKV_ERR_INVALID_ARG;
   int32_t t = 0;
   CHECK(arckv_budget(prob->T, rho, &t));
   const int32_t t_nominal = t;
@@ -688,11 +703,13 @@ arckv_status arckv_compact(const arckv_problem *prob, const void *K, const void 
   c.scale = eff_scale(prob);
   c.stream = stream;
   const Dims &d = c.d;
-  float *scores = c.pers<float>(c.pl.scores);
+  const float *scores = scores_in ? scores_in : c.pers<float>(c.pl.scores);
   float *z = c.pers<float>(c.pl.z), *m = c.pers<float>(c.pl.m), *Y = c.pers<float>(c.pl.Y);
   float *zmax = c.pers<float>(c.pl.zmax), *phi = c.pers<float>(c.pl.phi);
   int32_t *kappa = c.pers<int32_t>(c.pl.kappa);
-  STAGE(ST_SCORE, launch_score(d.dtype, K, V, ix->W1, ix->b1, ix->w2, ix->b2, scores, d.B, d.T, stream));
+  if (ix)
+    STAGE(ST_SCORE, launch_score(d.dtype, K, V, ix->W1, ix->b1, ix->w2, ix->b2, c.pers<float>(c.pl.scores), d.B, d.T,
+                                 stream));
   STAGE(ST_SELECT, launch_select_ex(scores, d.B, d.T, t_nominal, nullptr, p->select_chunk, t, anchors, stream));
   STAGE(ST_ROWSTATS, launch_rowstats(d.dtype, K, V, Q_ref, z, m, Y, d.B, d.T, d.n, c.scale, stream));
   STAGE(ST_ZMAX, launch_zmax(z, d.B, d.n, zmax, stream));
@@ -745,6 +762,120 @@ arckv_status arckv_attend(int32_t P, int32_t G, int32_t t, int32_t F, float scal
   STAGE(ST_ATTEND, launch_attend(P, G, t, F, s, Q, t > 0 ? C_k : nullptr, t > 0 ? beta : nullptr,
                                  t > 0 ? C_v : nullptr, F > 0 ? K_f : nullptr, F > 0 ? V_f : nullptr, part_o, part_ml,
                                  out, stream));
+  return ARCKV_OK;
+}
+
+arckv_status arckv_compact(const arckv_problem *prob, const void *K, const void *V, const void *Q_ref,
+                           const arckv_indexer *ix, double rho, const arckv_fit_params *p, int32_t *t_out,
+                           int32_t *anchors, float *C_k, float *beta, float *C_v, int32_t *info, void *ws,
+                           size_t ws_bytes, hipStream_t stream) {
+  if (!ix) return ARCKV_ERR_INVALID_ARG;
+  return compact_impl(prob, K, V, Q_ref, ix, nullptr, rho, p, t_out, anchors, C_k, beta, C_v, info, ws, ws_bytes,
+                      stream);
+}
+
+arckv_status arckv_compact_scored(const arckv_problem *prob, const void *K, const void *V, const void *Q_ref,
+                                  const float *scores, double rho, const arckv_fit_params *p, int32_t *t_out,
+                                  int32_t *anchors, float *C_k, float *beta, float *C_v, int32_t *info, void *ws,
+                                  size_t ws_bytes, hipStream_t stream) {
+  if (!scores) return ARCKV_ERR_INVALID_ARG;
+  return compact_impl(prob, K, V, Q_ref, nullptr, scores, rho, p, t_out, anchors, C_k, beta, C_v, info, ws,
+                      ws_bytes, stream);
+}
+
+// ---------------------------------------------------------------- value-aware indexer
+struct DsaPlan {
+  int64_t ka, va, qa, c, za, ma, qbar, kbar, w, z, m, part, bytes;
+};
+
+static DsaPlan dsa_plan(int64_t P, int64_t T, int64_t n, int64_t n_pos) {
+  DsaPlan d;
+  Bump b;
+  d.ka = b.take(P * T * 128 * 2);
+  d.va = b.take(P * T * 128 * 2);
+  d.qa = b.take(P * n * 128 * 2);
+  d.c = b.take(P * n * 128 * 4);
+  d.za = b.take(P * n * 4);
+  d.ma = b.take(P * n * 4);
+  d.qbar = b.take(P * n * 1024 * 2);
+  d.kbar = b.take(P * T * 1024 * 2);
+  d.w = b.take(P * n_pos * 8 * 4);
+  d.z = b.take(P * n * 4);
+  d.m = b.take(P * n * 4);
+  d.part = b.take(P * (int64_t)dsa_query_blocks((int)n) * T * 4);
+  d.bytes = b.off;
+  return d;
+}
+
+arckv_status arckv_dsa_workspace_size(const arckv_problem *prob, int32_t pair_chunk, size_t *bytes) {
+  CHECK(check_problem(prob));
+  if (!bytes || pair_chunk < 0) return ARCKV_ERR_INVALID_ARG;
+  const int64_t P = pair_chunk > 0 && pair_chunk < prob->B ? pair_chunk : prob->B;
+  *bytes = (size_t)dsa_plan(P, prob->T, prob->n, prob->n).bytes;   // sized for n_pos = n, the largest allowed
+  return ARCKV_OK;
+}
+
+arckv_status arckv_score_dsa(const arckv_problem *prob, const void *K, const void *V, const void *Q_ref,
+                             const arckv_dsa_indexer *ix, float *scores, void *ws, size_t ws_bytes,
+                             hipStream_t stream) {
+  CHECK(check_problem(prob));
+  if (prob->dtype != ARCKV_BF16) return ARCKV_ERR_UNSUPPORTED;
+  if (!K || !V || !Q_ref || !ix || !scores) return ARCKV_ERR_INVALID_ARG;
+  if (!ix->X_ref || !ix->L_q || !ix->L_k || !ix->L_x || !ix->b_x || !ix->U_q || !ix->U_k || !ix->U_v || !ix->L_c ||
+      !ix->L_v)
+    return ARCKV_ERR_INVALID_ARG;
+  if (ix->n_pos < 1 || prob->n % ix->n_pos != 0 || ix->d_x < 1 || ix->x_group < 1 || !isfinite(ix->scale_a))
+    return ARCKV_ERR_INVALID_ARG;
+  const void *al[] = {K, V, Q_ref, ix->L_q, ix->L_k, ix->U_q, ix->U_k, ix->U_v, ix->L_c, ix->L_v};
+  for (const void *q : al)
+    if (!aligned(q, 16)) return ARCKV_ERR_INVALID_ARG;
+  if (!ws || !aligned(ws, 256)) return ARCKV_ERR_WORKSPACE;
+  const int64_t B = prob->B, T = prob->T, n = prob->n;
+  // largest chunk of pairs whose plan fits
+  int64_t P = B;
+  while (P > 1 && (size_t)dsa_plan(P, T, n, ix->n_pos).bytes > ws_bytes) P = (P + 1) / 2;
+  if ((size_t)dsa_plan(P, T, n, ix->n_pos).bytes > ws_bytes) return ARCKV_ERR_WORKSPACE;
+  const DsaPlan pl = dsa_plan(P, T, n, ix->n_pos);
+  char *w0 = (char *)ws;
+  const float sa = ix->scale_a > 0.0f ? ix->scale_a : 1.0f / sqrtf(128.0f);
+  for (int64_t b0 = 0; b0 < B; b0 += P) {
+    const int Pc = (int)(B - b0 < P ? B - b0 : P);
+    const bf16_t_ *Kc = (const bf16_t_ *)K + b0 * T * 128, *Vc = (const bf16_t_ *)V + b0 * T * 128;
+    const bf16_t_ *Qc = (const bf16_t_ *)Q_ref + b0 * n * 128;
+    auto mat = [&](const void *base, int64_t per) { return (const bf16_t_ *)base + b0 * per; };
+    {
+      StageScope _sc(ST_DSA_PROJ, stream);
+      if (launch_dsa_proj(Kc, nullptr, false, mat(ix->U_k, 128 * 128), nullptr, Pc, (int)T, 1, false, w0 + pl.ka,
+                          stream) != hipSuccess ||
+          launch_dsa_proj(Vc, nullptr, false, mat(ix->U_v, 128 * 128), nullptr, Pc, (int)T, 1, false, w0 + pl.va,
+                          stream) != hipSuccess ||
+          launch_dsa_proj(Qc, nullptr, false, mat(ix->U_q, 128 * 128), nullptr, Pc, (int)n, 1, false, w0 + pl.qa,
+                          stream) != hipSuccess)
+        return ARCKV_ERR_HIP;
+    }
+    STAGE(ST_DSA_VALUE, launch_rowstats(ARCKV_BF16, w0 + pl.ka, w0 + pl.va, w0 + pl.qa, (float *)(w0 + pl.za),
+                                        (float *)(w0 + pl.ma), (float *)(w0 + pl.c), Pc, (int)T, (int)n, sa, stream));
+    {
+      StageScope _sc(ST_DSA_PROJ, stream);
+      if (launch_dsa_proj(Kc, Vc, false, mat(ix->L_k, 1024 * 128), mat(ix->L_v, 1024 * 128), Pc, (int)T, 8, true,
+                          w0 + pl.kbar, stream) != hipSuccess ||
+          launch_dsa_proj(Qc, w0 + pl.c, true, mat(ix->L_q, 1024 * 128), mat(ix->L_c, 1024 * 128), Pc, (int)n, 8,
+                          true, w0 + pl.qbar, stream) != hipSuccess ||
+          launch_dsa_w(ix->X_ref, mat(ix->L_x, 8 * (int64_t)ix->d_x), ix->b_x + b0 * 8, Pc, ix->n_pos, ix->d_x,
+                       ix->x_group, (int)b0, (float *)(w0 + pl.w), stream) != hipSuccess)
+        return ARCKV_ERR_HIP;
+    }
+    {
+      StageScope _sc(ST_DSA_INDEX, stream);
+      float *z = (float *)(w0 + pl.z), *m = (float *)(w0 + pl.m), *part = (float *)(w0 + pl.part);
+      if (launch_dsa_index(1, w0 + pl.qbar, w0 + pl.kbar, (float *)(w0 + pl.w), Pc, (int)n, ix->n_pos, (int)T, z, m,
+                           part, stream) != hipSuccess ||
+          launch_dsa_index(2, w0 + pl.qbar, w0 + pl.kbar, (float *)(w0 + pl.w), Pc, (int)n, ix->n_pos, (int)T, z, m,
+                           part, stream) != hipSuccess ||
+          launch_dsa_pool(part, Pc, (int)n, (int)T, scores + b0 * T, stream) != hipSuccess)
+        return ARCKV_ERR_HIP;
+    }
+  }
   return ARCKV_OK;
 }
 

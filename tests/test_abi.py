@@ -203,3 +203,26 @@ def test_workspace_covers_chunked_count():
     assert A.select_count(131072, nominal, 8192) > nominal
     assert A.workspace_size(p, nominal, A.default_params(select_chunk=8192)) >= \
         A.workspace_size(p, A.select_count(131072, nominal, 8192))
+
+
+def test_dsa_validation():
+    p = A.problem_from_dims(2, 300, 96)
+    assert A.dsa_workspace_size(p) > A.dsa_workspace_size(p, pair_chunk=1) > 0
+    L = A.lib()
+    fake = ctypes.c_void_p(0x1000)
+    ix = A.DSAIndexer(48, 96, 1, 0.0, *([fake] * 10))
+    nbytes = A.dsa_workspace_size(p)
+    # fp32 inputs are not supported; n must be a multiple of n_pos; a null weight is rejected
+    p32 = A.problem_from_dims(2, 300, 96, dtype=A.F32)
+    assert L.arckv_score_dsa(ctypes.byref(p32), fake, fake, fake, ctypes.byref(ix), fake, fake, nbytes, None) == \
+        A.ERR_UNSUPPORTED
+    bad = A.DSAIndexer(50, 96, 1, 0.0, *([fake] * 10))
+    assert L.arckv_score_dsa(ctypes.byref(p), fake, fake, fake, ctypes.byref(bad), fake, fake, nbytes, None) == \
+        A.ERR_INVALID_ARG
+    nul = A.DSAIndexer(48, 96, 1, 0.0, *([fake] * 9 + [None]))
+    assert L.arckv_score_dsa(ctypes.byref(p), fake, fake, fake, ctypes.byref(nul), fake, fake, nbytes, None) == \
+        A.ERR_INVALID_ARG
+    assert L.arckv_score_dsa(ctypes.byref(p), fake, fake, fake, ctypes.byref(ix), fake, ctypes.c_void_p(0x1010),
+                             nbytes, None) == A.ERR_WORKSPACE
+    assert L.arckv_compact_scored(ctypes.byref(p), fake, fake, fake, None, 0.1, None, ctypes.byref(ctypes.c_int32()),
+                                  fake, fake, fake, fake, fake, fake, 1 << 20, None) == A.ERR_INVALID_ARG
