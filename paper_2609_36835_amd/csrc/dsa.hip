@@ -162,44 +162,52 @@ __global__ void __launch_bounds__(256) k_dsa_index(const bf16 *__restrict__ qbar
   float run_m[2] = {-INFINITY, -INFINITY}, run_s[2] = {0.0f, 0.0f};   // PASS 1
   const bf16 *kb = kbar + (size_t)p * T * (kDsaH * kDsaW) + 8 * h;
   const int nkb = (T + kDsaKB - 1) / kDsaKB;
+  // a ring of four heads' key fragments (128 VGPRs): head a's slot is refilled
+  // with head a + 4 (the next block's head a - 4 in the second half) right
+  // after use, so every load has four heads of MFMAs to land
+  constexpr int RING = 4;
+  bf16x8 af[RING][8];
+  auto fetch = [&](int kbk_, int a, bf16x8 (&f)[8]) {
+    const int key = kbk_ * kDsaKB + wave * 32 + col;
+    const bf16 *krow = kb + (size_t)(key < T ? key : 0) * (kDsaH * kDsaW) + a * kDsaW;
+#pragma unroll
+    for (int ks = 0; ks < 8; ++ks) f[ks] = key < T ? load_frag(krow + 16 * ks) : Mfma<bf16>::zero();
+  };
+#pragma unroll
+  for (int a = 0; a < RING; ++a) fetch(0, a, af[a]);
   for (int kbk = 0; kbk < nkb; ++kbk) {
-    const int key = kbk * kDsaKB + wave * 32 + col;   // A-operand row of this lane
-    const bool kval = key < T;
-    const bf16 *krow = kb + (size_t)(kval ? key : 0) * (kDsaH * kDsaW);
+    // the query embeddings are re-read from LDS in every key block (not held in registers)
+    asm volatile("" ::: "memory");
     float I[2][16];
 #pragma unroll
     for (int nt = 0; nt < 2; ++nt)
 #pragma unroll
       for (int v = 0; v < 16; ++v) I[nt][v] = 0.0f;
-    // head a: S = kbar_a qbar_a^T for both query tiles, I += (w_a / sqrt d_I) LeakyReLU(S)
-    auto head = [&](int a, const bf16x8 (&af)[8]) {
-#pragma unroll
-      for (int nt = 0; nt < 2; ++nt) {
-        const int q = 32 * nt + col;
-        f32x16 acc = zero16();
-#pragma unroll
-        for (int ks = 0; ks < 8; ++ks) {
-          const int c = 16 * a + 2 * ks + h;
-          const int phys = (c & ~15) | ((c ^ q) & 15);
-          acc = Mfma<bf16>::mma(af[ks], *reinterpret_cast<const bf16x8 *>(sq + q * 2048 + phys * 16), acc);
-        }
-        const float wa = sw[q * kDsaH + a];
-#pragma unroll
-        for (int v = 0; v < 16; ++v) I[nt][v] = fmaf(wa, fmaxf(acc[v], kLeaky * acc[v]), I[nt][v]);
-      }
-    };
-    auto fetch = [&](int a, bf16x8 (&af)[8]) {
-#pragma unroll
-      for (int ks = 0; ks < 8; ++ks) af[ks] = kval ? load_frag(krow + a * kDsaW + 16 * ks) : Mfma<bf16>::zero();
-    };
-    bf16x8 af0[8], af1[8];
-    fetch(0, af0);
 #pragma unroll 1
-    for (int a = 0; a < kDsaH; a += 2) {   // the next head's key fragments load during this head
-      fetch(a + 1, af1);
-      head(a, af0);
-      if (a + 2 < kDsaH) fetch(a + 2, af0);
-      head(a + 1, af1);
+    for (int a0 = 0; a0 < kDsaH; a0 += RING) {
+      asm volatile("" ::: "memory");
+#pragma unroll
+      for (int i = 0; i < RING; ++i) {
+        const int a = a0 + i;
+        // head a: S = kbar_a qbar_a^T for both query tiles, I += (w_a / sqrt d_I) LeakyReLU(S)
+#pragma unroll
+        for (int nt = 0; nt < 2; ++nt) {
+          const int q = 32 * nt + col;
+          f32x16 acc = zero16();
+#pragma unroll
+          for (int ks = 0; ks < 8; ++ks) {
+            const int c = 16 * a + 2 * ks + h;
+            const int phys = (c & ~15) | ((c ^ q) & 15);
+            acc = Mfma<bf16>::mma(af[i][ks], *reinterpret_cast<const bf16x8 *>(sq + q * 2048 + phys * 16), acc);
+          }
+          const float wa = sw[q * kDsaH + a];
+#pragma unroll
+          for (int v = 0; v < 16; ++v) I[nt][v] = fmaf(wa, fmaxf(acc[v], kLeaky * acc[v]), I[nt][v]);
+        }
+        // refill the slot: head a + RING of this block, or head i of the next block
+        if (a0 == 0) fetch(kbk, RING + i, af[i]);
+        else if (kbk + 1 < nkb) fetch(kbk + 1, i, af[i]);
+      }
     }
     // lane (h, col): keys kbk 128 + 32 wave + 8 g + 4 h + e, query column 32 nt + col
     const int kbase = kbk * kDsaKB + wave * 32 + 4 * h;
