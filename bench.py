@@ -288,6 +288,8 @@ def main():
     ap.add_argument("--pair-chunk", type=int, default=0)
     ap.add_argument("--select-chunk", type=int, default=0,
                     help="chunked anchor selection (chunks of this many positions when T > 10000); 0 = global top-t")
+    ap.add_argument("--bias-mode", type=int, default=0, choices=(0, 1),
+                    help="mass fit: 0 = projected least squares (the paper's), 1 = exact non-negative least squares")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device copy (3 times), the reference kernel that scales the "
                          "FETCH_SIZE / WRITE_SIZE counters to bytes")
@@ -319,7 +321,8 @@ def main():
     dev = torch.device("cuda:0")
     log(f"[bench] workload {wl.name}: pairs={wl.pairs} T={wl.T} n={wl.n} rho={wl.rho} dtype={wl.dtype}")
     K, V, Q, W1, b1, w2, b2 = load_inputs(wl, dev)
-    params = arckv.default_params(pair_chunk=args.pair_chunk, select_chunk=args.select_chunk)
+    params = arckv.default_params(pair_chunk=args.pair_chunk, select_chunk=args.select_chunk,
+                                  bias_mode=args.bias_mode)
     comp = arckv.Compactor(wl.pairs, wl.T, wl.n, wl.rho, K.dtype, dev, scale=1.0 / math.sqrt(wl.d), params=params)
     t = comp.t
     log(f"[bench] t={t}, workspace {comp.ws_bytes / 2**30:.1f} GiB")
@@ -384,7 +387,8 @@ def main():
                                   "random-init scoring MLP)",
         "config": {"workload": wl.name, "pairs": wl.pairs, "layers": wl.layers, "kv_heads": wl.kv_heads,
                    "T": wl.T, "n_ref": wl.n, "t": t, "rho": wl.rho, "head_dim": wl.d,
-                   "pair_chunk": args.pair_chunk or wl.pairs, "select_chunk": args.select_chunk},
+                   "pair_chunk": args.pair_chunk or wl.pairs, "select_chunk": args.select_chunk,
+                   "bias_mode": args.bias_mode},
         "roofline": roofline,
         "roofline_score_select": roofline_ss,
         "cpu_baseline": cpu,

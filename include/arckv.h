@@ -92,7 +92,9 @@ typedef struct {
   float delta_v;         /* relative ridge of the value fit: lambda_v = delta_v*tr(A)/t; default 1e-3 */
   float eps_w;           /* epsilon_w of eq. mass_fit; default 1e-12 */
   float b_min, b_max;    /* clip range of beta; default [-30, 30] */
-  int32_t bias_mode;     /* 0 = projected least squares (eq. mass_fit); other values unsupported */
+  int32_t bias_mode;     /* 0 = projected least squares (eq. mass_fit, the paper's: w* = max(w~, 0));
+                          * 1 = exact non-negative least squares on the same ridged system, by block
+                          * principal pivoting; other values unsupported */
   int32_t max_escalations; /* ridge x10 retries after a failed Cholesky pivot, 0..6; default 3 */
   int32_t refine_steps;  /* iterative-refinement steps after each Cholesky solve, 0..4; default 2.
                           * Each step recomputes the residual from the data (Phi_C, P_hat),
@@ -102,6 +104,8 @@ typedef struct {
   int32_t select_chunk;  /* 0 = global top-t (default).  L > 0: when T > 10,000, anchors are the union of
                           * each L-position chunk's local top-t_c (Appendix A.3), so arckv_compact keeps
                           * arckv_select_count(T, t, L) anchors; merge and fits stay global. */
+  int32_t nnls_max_iter; /* bias_mode 1: pivoting iterations (one masked Cholesky solve each), 1..256;
+                          * default 32.  A pair not settled by then reports info = -2. */
 } arckv_fit_params;
 
 /* Fill *p with the defaults listed above.  Returns ARCKV_ERR_INVALID_ARG on NULL. */
@@ -215,9 +219,14 @@ arckv_status arckv_merge(const arckv_problem *prob, const void *K, const void *Q
  * Phi_C = exp(s Q C_k^T - z 1^T): w~ solves (G + delta_beta tr(G)/t I) w = h,
  * G = Phi_C^T Phi_C, h = Phi_C^T m, by Cholesky (float32) plus refinement;
  * beta = clip(log max(max(w~, 0), eps_w), b_min, b_max).
+ * With p->bias_mode = 1, w* instead minimises w^T (G + lam I) w / 2 - h^T w over
+ * w >= 0 (lam the ridge settled by the factorisation above), found by block
+ * principal pivoting: each iteration refactors the system restricted to the
+ * current free set and solves it with refinement against the data.
  *   beta  [B][t] output.
  *   info  [B] output: 0 = ok, k > 0 = Cholesky pivot k failed after all ridge
- *         escalations (beta is then NaN).
+ *         escalations, -2 = bias_mode 1 did not settle within nnls_max_iter
+ *         iterations (beta is NaN in both cases).
  *   delta_used [B] output (may be NULL): the relative ridge actually used. */
 arckv_status arckv_fit_bias(const arckv_problem *prob, const void *Q_ref, const float *C_k,
                             int32_t t, const float *z, const float *m,

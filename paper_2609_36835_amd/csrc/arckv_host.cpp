@@ -74,6 +74,12 @@ hipError_t launch_cholesky(float *Gw, const float *Gc, int B, int t, int64_t ld,
                            FitState st, float *dinv, void *lsplit, hipStream_t s);
 hipError_t launch_trsv(const float *Gw, const float *dinv, int B, int64_t ld, const double *rhs, double *sw,
                        double *y, double *x, double *acc, const int32_t *info, hipStream_t s);
+hipError_t launch_cholesky_factor(float *Gw, const float *Gc, int B, int t, int64_t ld, float delta0, int max_esc,
+                                  FitState st, float *dinv, void *lsplit, hipStream_t s);
+hipError_t launch_nnls(const float *Gc, float *Gw, const double *h, const float *LT, const float *z, const float *m,
+                       int B, int n, int t, int64_t tp, int64_t np_, int max_iter, int refine_steps, FitState st,
+                       float *dinv, void *lsplit, int32_t *F, double *x, double *yv, int32_t *state, double *rhs,
+                       double *sw, double *yw, double *dx, double *u, double *res, hipStream_t s);
 hipError_t launch_bias_finalize(const double *w, int B, int64_t ld, int t, float eps, float bmin, float bmax,
                                 const int32_t *info, float *beta, float *beta_ws, hipStream_t s);
 hipError_t launch_phat(int dtype, const float *LT, const float *beta_ws, int B, int n, int t, int64_t tp,
@@ -197,6 +203,7 @@ struct Plan {
   int64_t Ckp;
   int64_t Et, U, ssq, part, offsets, cursor, perm;       // merge phase
   int64_t PhiT, LT, Gw, Gc, dinv, lsplit, h, w, y, x, res, sw, u, YT, Bm, X, R, Y2, XT, Pm, UT;  // fit phase
+  int64_t nF, nstate, ny, nrhs, ndx;   // exact NNLS (bias_mode 1)
   int64_t chunk_bytes;
 };
 
@@ -251,6 +258,11 @@ static Plan make_plan(const Dims &d, int64_t P) {
   pl.XT = f.take(P * d.tp * kHeadDimH * 4);
   pl.Pm = f.take(P * d.tp * d.np_ * 4);
   pl.UT = f.take(P * kHeadDimH * d.np_ * 4);
+  pl.nF = f.take(P * d.tp * 4);
+  pl.nstate = f.take(P * 16);
+  pl.ny = f.take(P * d.tp * 8);
+  pl.nrhs = f.take(P * d.tp * 8);
+  pl.ndx = f.take(P * d.tp * 8);
   (void)phase0;
   pl.chunk_bytes = m.off > f.off ? m.off : f.off;
   return pl;
@@ -294,7 +306,8 @@ static arckv_status check_params(const arckv_fit_params *p) {
   if (!(p->delta_v >= 0.0f) || !isfinite(p->delta_v)) return ARCKV_ERR_INVALID_ARG;
   if (!(p->eps_w > 0.0f) || !isfinite(p->eps_w)) return ARCKV_ERR_INVALID_ARG;
   if (!(p->b_min <= p->b_max) || !isfinite(p->b_min) || !isfinite(p->b_max)) return ARCKV_ERR_INVALID_ARG;
-  if (p->bias_mode != 0) return ARCKV_ERR_UNSUPPORTED;
+  if (p->bias_mode != 0 && p->bias_mode != 1) return ARCKV_ERR_UNSUPPORTED;
+  if (p->nnls_max_iter < 1 || p->nnls_max_iter > 256) return ARCKV_ERR_INVALID_ARG;
   if (p->max_escalations < 0 || p->max_escalations > 6) return ARCKV_ERR_INVALID_ARG;
   if (p->refine_steps < 0 || p->refine_steps > 4) return ARCKV_ERR_INVALID_ARG;
   if (p->pair_chunk < 0) return ARCKV_ERR_INVALID_ARG;
@@ -392,13 +405,23 @@ static arckv_status run_fit_bias_chunk(const Ctx &c, int b0, int P, const void *
                                    c.chunk<char>(c.pl.lsplit), stream));
   {
     StageScope _sc(ST_SOLVE_W, stream);
-    if (launch_trsv(Gw, dinv, P, d.tp, h, sw, y, w, nullptr, st.info, stream) != hipSuccess) return ARCKV_ERR_HIP;
-    // refinement against the data: res = Phi_C^T (m - Phi_C w) - lam w
     double *u = c.chunk<double>(c.pl.u);
-    for (int it = 0; it < fp.refine_steps; ++it) {
-      if (launch_mass_residual(LT, zc, mc, w, st.lam, P, d.n, d.t, d.tp, d.np_, u, res, st.info, stream) != hipSuccess)
+    if (fp.bias_mode == 1) {
+      // exact NNLS on the ridged system whose ridge the factorisation above settled
+      if (launch_nnls(Gc, Gw, h, LT, zc, mc, P, d.n, d.t, d.tp, d.np_, fp.nnls_max_iter, fp.refine_steps, st, dinv,
+                      c.chunk<char>(c.pl.lsplit), c.chunk<int32_t>(c.pl.nF), w, c.chunk<double>(c.pl.ny),
+                      c.chunk<int32_t>(c.pl.nstate), c.chunk<double>(c.pl.nrhs), sw, y, c.chunk<double>(c.pl.ndx),
+                      u, res, stream) != hipSuccess)
         return ARCKV_ERR_HIP;
-      if (launch_trsv(Gw, dinv, P, d.tp, res, sw, y, x, w, st.info, stream) != hipSuccess) return ARCKV_ERR_HIP;
+    } else {
+      if (launch_trsv(Gw, dinv, P, d.tp, h, sw, y, w, nullptr, st.info, stream) != hipSuccess) return ARCKV_ERR_HIP;
+      // refinement against the data: res = Phi_C^T (m - Phi_C w) - lam w
+      for (int it = 0; it < fp.refine_steps; ++it) {
+        if (launch_mass_residual(LT, zc, mc, w, st.lam, P, d.n, d.t, d.tp, d.np_, u, res, st.info, stream) !=
+            hipSuccess)
+          return ARCKV_ERR_HIP;
+        if (launch_trsv(Gw, dinv, P, d.tp, res, sw, y, x, w, st.info, stream) != hipSuccess) return ARCKV_ERR_HIP;
+      }
     }
     if (launch_bias_finalize(w, P, d.tp, d.t, fp.eps_w, fp.b_min, fp.b_max, st.info, beta + (size_t)b0 * d.t,
                              c.pers<float>(c.pl.beta_ws) + (size_t)b0 * d.tp, stream) != hipSuccess)
@@ -478,6 +501,7 @@ arckv_status arckv_default_params(arckv_fit_params *p) {
   p->refine_steps = 2;
   p->pair_chunk = 0;
   p->select_chunk = 0;
+  p->nnls_max_iter = 32;
   return ARCKV_OK;
 }
 

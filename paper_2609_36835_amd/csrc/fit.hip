@@ -931,11 +931,160 @@ __global__ void __launch_bounds__(256) k_values_out(const float *__restrict__ Xp
   Cv[(size_t)b * t * kHeadDim + e] = info[b] != 0 ? NAN : Xp[(size_t)b * tp * kHeadDim + e];
 }
 
+// --------------------------------------------------------------- exact NNLS (bias_mode 1)
+// Block principal pivoting (Judice & Pires 1994, in the single-right-hand-side
+// form of Kim & Park 2011) for min ||Phi_C w - m||^2 + lam ||w||^2, w >= 0, the
+// ridged system of the projected fit.  Per pair: F (passive set, 1 = free), x,
+// y = (G + lam I) x - h from the data residual, and the state
+// {best infeasible count N, backup budget p, done, spare}.
+constexpr int32_t kNnlsSkip = -0x40000000;   // info marker of a pair that has converged
+
+__global__ void __launch_bounds__(256) k_nnls_init(const double *__restrict__ h, int t, int64_t tp,
+                                                   const int32_t *__restrict__ info, int32_t *__restrict__ F,
+                                                   double *__restrict__ x, double *__restrict__ y,
+                                                   int32_t *__restrict__ state) {
+  const int b = blockIdx.y;
+  const int64_t r = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (r < tp) {
+    F[(size_t)b * tp + r] = 0;
+    x[(size_t)b * tp + r] = 0.0;
+    y[(size_t)b * tp + r] = r < t ? -h[(size_t)b * tp + r] : 0.0;
+  }
+  if (r == 0) {
+    state[4 * b] = t + 1;
+    state[4 * b + 1] = 3;
+    state[4 * b + 2] = info[b] != 0;   // a failed projected fit is not iterated
+    state[4 * b + 3] = 0;
+  }
+}
+
+// One workgroup per pair: the infeasible set V = {free x < -tol} u {bound y < -tol},
+// then the exchange rule: all of V while |V| improves on the best count (or the
+// backup budget lasts), otherwise only its largest index.  Marks the pair done
+// (and skipped by the factor and solve kernels) when V is empty.
+__global__ void __launch_bounds__(256) k_nnls_update(const double *__restrict__ x, const double *__restrict__ y,
+                                                     const double *__restrict__ h, int t, int64_t tp,
+                                                     int32_t *__restrict__ F, int32_t *__restrict__ state,
+                                                     int32_t *__restrict__ info) {
+  __shared__ double sx[4], sh[4];
+  __shared__ int32_t scnt[4], smax[4];
+  __shared__ int32_t s_mode;   // 0 none, 1 all of V, 2 the largest index only
+  __shared__ int32_t s_j;
+  const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  if (state[4 * b + 2] || info[b] != 0) return;   // settled, or a factorisation failed
+  const double *xb = x + (size_t)b * tp, *yb = y + (size_t)b * tp, *hb = h + (size_t)b * tp;
+  int32_t *Fb = F + (size_t)b * tp;
+  double mx = 0.0, mh = 0.0;
+  for (int r = tid; r < t; r += 256) {
+    mx = fmax(mx, fabs(xb[r]));
+    mh = fmax(mh, fabs(hb[r]));
+  }
+  for (int o = 32; o >= 1; o >>= 1) {
+    mx = fmax(mx, __shfl_xor(mx, o, 64));
+    mh = fmax(mh, __shfl_xor(mh, o, 64));
+  }
+  if (lane == 0) {
+    sx[wave] = mx;
+    sh[wave] = mh;
+  }
+  __syncthreads();
+  // tolerances: float32-level relative to the solution and right-hand side scales
+  const double tx = 1e-6 * fmax(fmax(sx[0], sx[1]), fmax(sx[2], sx[3]));
+  const double ty = 1e-6 * fmax(fmax(sh[0], sh[1]), fmax(sh[2], sh[3]));
+  auto infeasible = [&](int r) { return Fb[r] ? xb[r] < -tx : yb[r] < -ty; };
+  int32_t cnt = 0, jmax = -1;
+  for (int r = tid; r < t; r += 256)
+    if (infeasible(r)) {
+      ++cnt;
+      jmax = r;
+    }
+  for (int o = 32; o >= 1; o >>= 1) {
+    cnt += __shfl_xor(cnt, o, 64);
+    jmax = max(jmax, __shfl_xor(jmax, o, 64));
+  }
+  if (lane == 0) {
+    scnt[wave] = cnt;
+    smax[wave] = jmax;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    const int32_t V = scnt[0] + scnt[1] + scnt[2] + scnt[3];
+    s_j = max(max(smax[0], smax[1]), max(smax[2], smax[3]));
+    int32_t mode = 0;
+    if (V == 0) {
+      state[4 * b + 2] = 1;
+      info[b] = kNnlsSkip;
+    } else if (V < state[4 * b]) {
+      state[4 * b] = V;
+      state[4 * b + 1] = 3;
+      mode = 1;
+    } else if (state[4 * b + 1] >= 1) {
+      state[4 * b + 1] -= 1;
+      mode = 1;
+    } else {
+      mode = 2;
+    }
+    s_mode = mode;
+  }
+  __syncthreads();
+  if (s_mode == 1) {
+    // infeasible(r) reads only F[r], which this thread alone owns
+    for (int r = tid; r < t; r += 256)
+      if (infeasible(r)) Fb[r] ^= 1;
+  } else if (s_mode == 2 && tid == 0) {
+    Fb[s_j] ^= 1;
+  }
+}
+
+// Work copy of the passive system: G_ij + lam [i = j] on F x F, identity elsewhere.
+__global__ void __launch_bounds__(256) k_nnls_gram(const float *__restrict__ Gc, const int32_t *__restrict__ F,
+                                                   const FitState st, int t, int64_t ld, float *__restrict__ Gw) {
+  const int b = blockIdx.y;
+  if (st.info[b] != 0) return;
+  const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (e >= ld * ld) return;
+  const int64_t i = e / ld, j = e % ld;
+  const size_t o = (size_t)b * ld * ld + e;
+  const int32_t *Fb = F + (size_t)b * ld;
+  const bool fi = i < t && Fb[i], fj = j < t && Fb[j];
+  Gw[o] = (fi && fj) ? Gc[o] + (i == j ? st.lam[b] : 0.0f) : (i == j ? 1.0f : 0.0f);
+}
+
+// mode 0: out = F ? in : 0 (right-hand side, refinement residual);
+// mode 1: out = F ? 0 : -in (y = -(residual) on the bound variables).
+__global__ void __launch_bounds__(256) k_nnls_mask(const double *__restrict__ in, const int32_t *__restrict__ F,
+                                                   int64_t tp, int mode, const int32_t *__restrict__ info,
+                                                   double *__restrict__ out) {
+  const int b = blockIdx.y;
+  const int64_t r = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (r >= tp || info[b] != 0) return;
+  const size_t o = (size_t)b * tp + r;
+  const bool f = F[o] != 0;
+  out[o] = mode == 0 ? (f ? in[o] : 0.0) : (f ? 0.0 : -in[o]);
+}
+
+// After the iterations: converged pairs are ok again; pairs still iterating get -2.
+__global__ void k_nnls_finish(const int32_t *__restrict__ state, int B, int32_t *__restrict__ info) {
+  const int b = blockIdx.x * 256 + threadIdx.x;
+  if (b >= B) return;
+  if (info[b] == kNnlsSkip) info[b] = 0;
+  else if (info[b] == 0 && !state[4 * b + 2]) info[b] = -2;
+}
+
 // ------------------------------------------------------------------ launchers
 // Ridge + factorisation (+ escalation) of the work copy Gw of Gc.
+hipError_t launch_cholesky_factor(float *Gw, const float *Gc, int B, int t, int64_t ld, float delta0, int max_esc,
+                                  FitState st, float *dinv, void *lsplit, hipStream_t s);
+
 hipError_t launch_cholesky(float *Gw, const float *Gc, int B, int t, int64_t ld, float delta0, int max_esc,
                            FitState st, float *dinv, void *lsplit, hipStream_t s) {
   hipLaunchKernelGGL(k_ridge_init, dim3(B), dim3(256), 0, s, Gw, Gc, t, ld, delta0, st);
+  return launch_cholesky_factor(Gw, Gc, B, t, ld, delta0, max_esc, st, dinv, lsplit, s);
+}
+
+// Factor the prepared work copy Gw in place (no ridge set-up); escalation as above.
+hipError_t launch_cholesky_factor(float *Gw, const float *Gc, int B, int t, int64_t ld, float delta0, int max_esc,
+                                  FitState st, float *dinv, void *lsplit, hipStream_t s) {
   // Two-level right-looking blocking: 64-wide diagonal factor + panel solve
   // steps inside 256-wide outer panels; inside an outer panel only its own
   // columns are updated, and the trailing matrix is updated once per outer
@@ -1002,6 +1151,38 @@ hipError_t launch_mass_residual(const float *LT, const float *z, const float *m,
                      u, info);
   hipLaunchKernelGGL(k_mass_resid_cols, dim3((unsigned)(tp / 4), B), dim3(256), 0, s, LT, z, u, w, lam, n, t, tp,
                      np_, res, info);
+  return hipGetLastError();
+}
+
+hipError_t launch_nnls(const float *Gc, float *Gw, const double *h, const float *LT, const float *z, const float *m,
+                       int B, int n, int t, int64_t tp, int64_t np_, int max_iter, int refine_steps, FitState st,
+                       float *dinv, void *lsplit, int32_t *F, double *x, double *yv, int32_t *state, double *rhs,
+                       double *sw, double *yw, double *dx, double *u, double *res, hipStream_t s) {
+  const dim3 gv((unsigned)((tp + 255) / 256), (unsigned)B);
+  hipLaunchKernelGGL(k_nnls_init, gv, dim3(256), 0, s, h, t, tp, st.info, F, x, yv, state);
+  for (int it = 0;; ++it) {
+    // the update after the last solve only checks feasibility (and marks done)
+    hipLaunchKernelGGL(k_nnls_update, dim3(B), dim3(256), 0, s, x, yv, h, t, tp, F, state, st.info);
+    if (it == max_iter) break;
+    hipLaunchKernelGGL(k_nnls_gram, dim3((unsigned)((tp * tp + 255) / 256), (unsigned)B), dim3(256), 0, s, Gc, F, st,
+                       t, tp, Gw);
+    hipError_t e = launch_cholesky_factor(Gw, Gc, B, t, tp, 0.0f, 0, st, dinv, lsplit, s);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_nnls_mask, gv, dim3(256), 0, s, h, F, tp, 0, st.info, rhs);
+    e = launch_trsv(Gw, dinv, B, tp, rhs, sw, yw, x, nullptr, st.info, s);
+    if (e != hipSuccess) return e;
+    for (int rs = 0; rs <= refine_steps; ++rs) {
+      // residual of the full ridged system from the data: h - (G + lam I) x
+      e = launch_mass_residual(LT, z, m, x, st.lam, B, n, t, tp, np_, u, res, st.info, s);
+      if (e != hipSuccess) return e;
+      if (rs == refine_steps) break;
+      hipLaunchKernelGGL(k_nnls_mask, gv, dim3(256), 0, s, res, F, tp, 0, st.info, dx);
+      e = launch_trsv(Gw, dinv, B, tp, dx, sw, yw, dx, x, st.info, s);
+      if (e != hipSuccess) return e;
+    }
+    hipLaunchKernelGGL(k_nnls_mask, gv, dim3(256), 0, s, res, F, tp, 1, st.info, yv);
+  }
+  hipLaunchKernelGGL(k_nnls_finish, dim3((unsigned)((B + 255) / 256)), dim3(256), 0, s, state, B, st.info);
   return hipGetLastError();
 }
 

@@ -57,6 +57,7 @@ def test_default_params():
     assert p.lambda_m == pytest.approx(0.25) and p.delta_beta == pytest.approx(1e-6)
     assert p.delta_v == pytest.approx(1e-3) and p.eps_w == pytest.approx(1e-12)
     assert (p.b_min, p.b_max, p.bias_mode, p.max_escalations, p.refine_steps) == (-30.0, 30.0, 0, 3, 2)
+    assert (p.pair_chunk, p.select_chunk, p.nnls_max_iter) == (0, 0, 32)
 
 
 def ws(prob, t, params=None):
@@ -89,7 +90,9 @@ def test_workspace_validation_and_monotonicity():
     ("lambda_m", 1.5, A.ERR_INVALID_ARG), ("lambda_m", -0.1, A.ERR_INVALID_ARG),
     ("delta_beta", -1.0, A.ERR_INVALID_ARG), ("delta_v", float("nan"), A.ERR_INVALID_ARG),
     ("eps_w", 0.0, A.ERR_INVALID_ARG), ("b_min", 40.0, A.ERR_INVALID_ARG),
-    ("bias_mode", 1, A.ERR_UNSUPPORTED), ("max_escalations", 7, A.ERR_INVALID_ARG),
+    ("bias_mode", 2, A.ERR_UNSUPPORTED), ("bias_mode", -1, A.ERR_UNSUPPORTED),
+    ("nnls_max_iter", 0, A.ERR_INVALID_ARG), ("nnls_max_iter", 257, A.ERR_INVALID_ARG),
+    ("max_escalations", 7, A.ERR_INVALID_ARG),
     ("refine_steps", -1, A.ERR_INVALID_ARG), ("pair_chunk", -2, A.ERR_INVALID_ARG),
 ])
 def test_param_validation(field, value, code):
@@ -128,7 +131,7 @@ def test_entry_points_reject_bad_arguments_without_gpu():
         (L.arckv_merge(r(prob), fake, fake, fake, fake, 10, 0.25, fake, None, None, ctypes.c_void_p(0x10000), 16,
                        None), A.ERR_WORKSPACE),              # workspace too small
         (L.arckv_merge(r(prob), fake, fake, fake, fake, 10, 1.5, fake, None, None, fake, 0, None), A.ERR_INVALID_ARG),
-        (L.arckv_fit_bias(r(prob), fake, fake, 10, fake, fake, r(A.default_params(bias_mode=1)), fake, fake, None,
+        (L.arckv_fit_bias(r(prob), fake, fake, 10, fake, fake, r(A.default_params(bias_mode=2)), fake, fake, None,
                           fake, 0, None), A.ERR_UNSUPPORTED),
         (L.arckv_fit_values(r(prob), fake, fake, fake, 10, None, r(par), fake, fake, None, fake, 0, None),
          A.ERR_INVALID_ARG),
