@@ -11,7 +11,8 @@
  *   2. assign every key to the anchor with the most similar normalised
  *      attention-response profile and merge each group into one compact key
  *      inside the group's convex hull (Section 3.4);
- *   3. fit the mass bias beta by projected least squares (Appendix A.9, eq. mass_fit);
+ *   3. fit the mass bias beta by projected least squares (Appendix A.9, eq. mass_fit;
+ *      optionally by exact non-negative least squares);
  *   4. fit the compact values C_v by ridge least squares (Appendix A.9, eq. value_lstsq).
  *
  * Conventions shared by every entry point
@@ -28,7 +29,10 @@
  *    undefined on entry and exit; it must not be shared by calls that may
  *    overlap in time.
  *  - All device work is enqueued on the caller's stream; no entry point
- *    synchronises the host.  Results are valid once the stream reaches them.
+ *    synchronises the host, with one exception: the exact non-negative mass
+ *    fit (arckv_fit_params.bias_mode = 1) reads two integers back once per
+ *    pivoting iteration, to size the next iteration's system and to stop when
+ *    every pair has settled.  Results are valid once the stream reaches them.
  *  - Argument errors are returned synchronously BEFORE any HIP call, so they can
  *    be checked on a machine without a GPU.  A failed kernel launch returns
  *    ARCKV_ERR_HIP.  Numerical failures are reported asynchronously in the

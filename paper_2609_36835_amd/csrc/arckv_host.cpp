@@ -22,6 +22,13 @@ struct FitState {
   float *delta;
   int32_t *info;
 };
+struct NnlsWork {
+  int32_t *F, *idx, *bidx, *pos;
+  int32_t *nf, *nb;
+  int32_t *state;
+  int32_t *red;
+  double *y, *rf, *xf;
+};
 
 hipError_t launch_score(int dtype, const void *K, const void *V, const void *W1, const float *b1, const float *w2,
                         const float *b2, float *scores, int B, int T, hipStream_t s);
@@ -69,7 +76,9 @@ hipError_t launch_value_residual(int dtype, const void *XT, const void *Pm, cons
                                  hipStream_t s);
 hipError_t launch_mass_residual(const float *LT, const float *z, const float *m, const double *w, const float *lam,
                                 int B, int n, int t, int64_t tp, int64_t np_, double *u, double *res,
-                                const int32_t *info, hipStream_t s);
+                                const int32_t *info, hipStream_t s, const int32_t *row_list = nullptr,
+                                const int32_t *row_count = nullptr, const int32_t *col_list = nullptr,
+                                const int32_t *col_count = nullptr);
 hipError_t launch_cholesky(float *Gw, const float *Gc, int B, int t, int64_t ld, float delta0, int max_esc,
                            FitState st, float *dinv, void *lsplit, hipStream_t s);
 hipError_t launch_trsv(const float *Gw, const float *dinv, int B, int64_t ld, const double *rhs, double *sw,
@@ -78,8 +87,8 @@ hipError_t launch_cholesky_factor(float *Gw, const float *Gc, int B, int t, int6
                                   FitState st, float *dinv, void *lsplit, hipStream_t s);
 hipError_t launch_nnls(const float *Gc, float *Gw, const double *h, const float *LT, const float *z, const float *m,
                        int B, int n, int t, int64_t tp, int64_t np_, int max_iter, int refine_steps, FitState st,
-                       float *dinv, void *lsplit, int32_t *F, double *x, double *yv, int32_t *state, double *rhs,
-                       double *sw, double *yw, double *dx, double *u, double *res, hipStream_t s);
+                       float *dinv, void *lsplit, NnlsWork nw, double *x, double *sw, double *yw, double *u,
+                       double *res, hipStream_t s);
 hipError_t launch_bias_finalize(const double *w, int B, int64_t ld, int t, float eps, float bmin, float bmax,
                                 const int32_t *info, float *beta, float *beta_ws, hipStream_t s);
 hipError_t launch_phat(int dtype, const float *LT, const float *beta_ws, int B, int n, int t, int64_t tp,
@@ -203,7 +212,7 @@ struct Plan {
   int64_t Ckp;
   int64_t Et, U, ssq, part, offsets, cursor, perm;       // merge phase
   int64_t PhiT, LT, Gw, Gc, dinv, lsplit, h, w, y, x, res, sw, u, YT, Bm, X, R, Y2, XT, Pm, UT;  // fit phase
-  int64_t nF, nstate, ny, nrhs, ndx;   // exact NNLS (bias_mode 1)
+  int64_t nF, nidx, nbidx, npos, nnf, nnb, nstate, nred, ny, nrhs, ndx;   // exact NNLS (bias_mode 1)
   int64_t chunk_bytes;
 };
 
@@ -259,7 +268,13 @@ static Plan make_plan(const Dims &d, int64_t P) {
   pl.Pm = f.take(P * d.tp * d.np_ * 4);
   pl.UT = f.take(P * kHeadDimH * d.np_ * 4);
   pl.nF = f.take(P * d.tp * 4);
+  pl.nidx = f.take(P * d.tp * 4);
+  pl.nbidx = f.take(P * d.tp * 4);
+  pl.npos = f.take(P * d.tp * 4);
+  pl.nnf = f.take(P * 4);
+  pl.nnb = f.take(P * 4);
   pl.nstate = f.take(P * 16);
+  pl.nred = f.take(16);
   pl.ny = f.take(P * d.tp * 8);
   pl.nrhs = f.take(P * d.tp * 8);
   pl.ndx = f.take(P * d.tp * 8);
@@ -406,22 +421,24 @@ static arckv_status run_fit_bias_chunk(const Ctx &c, int b0, int P, const void *
   {
     StageScope _sc(ST_SOLVE_W, stream);
     double *u = c.chunk<double>(c.pl.u);
-    if (fp.bias_mode == 1) {
-      // exact NNLS on the ridged system whose ridge the factorisation above settled
-      if (launch_nnls(Gc, Gw, h, LT, zc, mc, P, d.n, d.t, d.tp, d.np_, fp.nnls_max_iter, fp.refine_steps, st, dinv,
-                      c.chunk<char>(c.pl.lsplit), c.chunk<int32_t>(c.pl.nF), w, c.chunk<double>(c.pl.ny),
-                      c.chunk<int32_t>(c.pl.nstate), c.chunk<double>(c.pl.nrhs), sw, y, c.chunk<double>(c.pl.ndx),
-                      u, res, stream) != hipSuccess)
+    if (launch_trsv(Gw, dinv, P, d.tp, h, sw, y, w, nullptr, st.info, stream) != hipSuccess) return ARCKV_ERR_HIP;
+    // refinement against the data: res = Phi_C^T (m - Phi_C w) - lam w
+    for (int it = 0; it < fp.refine_steps; ++it) {
+      if (launch_mass_residual(LT, zc, mc, w, st.lam, P, d.n, d.t, d.tp, d.np_, u, res, st.info, stream) !=
+          hipSuccess)
         return ARCKV_ERR_HIP;
-    } else {
-      if (launch_trsv(Gw, dinv, P, d.tp, h, sw, y, w, nullptr, st.info, stream) != hipSuccess) return ARCKV_ERR_HIP;
-      // refinement against the data: res = Phi_C^T (m - Phi_C w) - lam w
-      for (int it = 0; it < fp.refine_steps; ++it) {
-        if (launch_mass_residual(LT, zc, mc, w, st.lam, P, d.n, d.t, d.tp, d.np_, u, res, st.info, stream) !=
-            hipSuccess)
-          return ARCKV_ERR_HIP;
-        if (launch_trsv(Gw, dinv, P, d.tp, res, sw, y, x, w, st.info, stream) != hipSuccess) return ARCKV_ERR_HIP;
-      }
+      if (launch_trsv(Gw, dinv, P, d.tp, res, sw, y, x, w, st.info, stream) != hipSuccess) return ARCKV_ERR_HIP;
+    }
+    if (fp.bias_mode == 1) {
+      // exact NNLS on the ridged system whose ridge the factorisation above
+      // settled, pivoting from the unconstrained solution w
+      NnlsWork nw{c.chunk<int32_t>(c.pl.nF),  c.chunk<int32_t>(c.pl.nidx),   c.chunk<int32_t>(c.pl.nbidx),
+                  c.chunk<int32_t>(c.pl.npos), c.chunk<int32_t>(c.pl.nnf),    c.chunk<int32_t>(c.pl.nnb),
+                  c.chunk<int32_t>(c.pl.nstate), c.chunk<int32_t>(c.pl.nred), c.chunk<double>(c.pl.ny),
+                  c.chunk<double>(c.pl.nrhs),  c.chunk<double>(c.pl.ndx)};
+      if (launch_nnls(Gc, Gw, h, LT, zc, mc, P, d.n, d.t, d.tp, d.np_, fp.nnls_max_iter, fp.refine_steps, st, dinv,
+                      c.chunk<char>(c.pl.lsplit), nw, w, sw, y, u, res, stream) != hipSuccess)
+        return ARCKV_ERR_HIP;
     }
     if (launch_bias_finalize(w, P, d.tp, d.t, fp.eps_w, fp.b_min, fp.b_max, st.info, beta + (size_t)b0 * d.t,
                              c.pers<float>(c.pl.beta_ws) + (size_t)b0 * d.tp, stream) != hipSuccess)

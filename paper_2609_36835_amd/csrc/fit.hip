@@ -35,6 +35,15 @@ struct FitState {
   int32_t *info;   // [P]
 };
 
+// Work arrays of the exact non-negative fit ([P][tp] unless noted).
+struct NnlsWork {
+  int32_t *F, *idx, *bidx, *pos;   // free flags, free and bound lists, slot of each key
+  int32_t *nf, *nb;                // [P] free- and bound-set sizes
+  int32_t *state;           // [P][4]
+  int32_t *red;             // [2] max free-set size, unsettled pairs
+  double *y, *rf, *xf;      // dual, compressed right-hand side and solution
+};
+
 // --------------------------------------------------------------- ridge
 __global__ void __launch_bounds__(256) k_ridge_init(float *__restrict__ Gw, const float *__restrict__ Gc, int t,
                                                     int64_t ld, float delta0, FitState st) {
@@ -411,6 +420,7 @@ struct EpiCholUpd {
   int64_t ld;
   int K1;
   const int32_t *info;
+  __device__ __forceinline__ bool skip(int p) const { return info[p] != 0; }
   __device__ __forceinline__ void operator()(f32x16 (&acc)[TM][TN], int p, int row0, int col0, int, int, int lane,
                                              int, int) const {
     if (info[p] != 0) return;
@@ -558,11 +568,17 @@ __global__ void __launch_bounds__(256) k_trsv_step(const float *__restrict__ Gw,
 // Refinement residual of the mass fit computed from the data, not from the
 // float32 Gram: res = Phi_C^T (m - Phi_C w) - lam w with Phi_C = exp(L^T - z)
 // re-evaluated in fp32 and every sum in float64.
+// Optional key lists restrict either stage to a subset of the compact keys
+// (list [P][tp], count [P]): the exact non-negative fit sums only over its free
+// keys (w = 0 elsewhere) and needs each residual only on one side of its
+// partition.  Without a list every key r < t takes part.
 // Stage 1 (one thread per query i): u_i = m_i - sum_{r<t} Phi[i][r] w_r.
 __global__ void __launch_bounds__(256) k_mass_resid_rows(const float *__restrict__ LT, const float *__restrict__ z,
                                                          const float *__restrict__ m, const double *__restrict__ w,
                                                          int n, int t, int64_t tp, int64_t np_,
-                                                         double *__restrict__ u, const int32_t *__restrict__ info) {
+                                                         double *__restrict__ u, const int32_t *__restrict__ info,
+                                                         const int32_t *__restrict__ list,
+                                                         const int32_t *__restrict__ count) {
   // 64 queries per workgroup; wave s sums the compact keys r = s (mod 4) with
   // two accumulators, and the four partial sums meet in LDS
   __shared__ double red[4][64];
@@ -574,12 +590,24 @@ __global__ void __launch_bounds__(256) k_mass_resid_rows(const float *__restrict
     const float *L = LT + (size_t)b * tp * np_ + i;
     const double *wb = w + (size_t)b * tp;
     const float zi = z[(size_t)b * n + i];
-    int r = wave;
-    for (; r + 4 < t; r += 8) {
-      a0 += (double)expf(L[(size_t)r * np_] - zi) * wb[r];
-      a1 += (double)expf(L[(size_t)(r + 4) * np_] - zi) * wb[r + 4];
+    if (list) {
+      const int32_t *lb = list + (size_t)b * tp;
+      const int c = count[b];
+      int k = wave;
+      for (; k + 4 < c; k += 8) {
+        const int r0 = lb[k], r1 = lb[k + 4];
+        a0 += (double)expf(L[(size_t)r0 * np_] - zi) * wb[r0];
+        a1 += (double)expf(L[(size_t)r1 * np_] - zi) * wb[r1];
+      }
+      if (k < c) a0 += (double)expf(L[(size_t)lb[k] * np_] - zi) * wb[lb[k]];
+    } else {
+      int r = wave;
+      for (; r + 4 < t; r += 8) {
+        a0 += (double)expf(L[(size_t)r * np_] - zi) * wb[r];
+        a1 += (double)expf(L[(size_t)(r + 4) * np_] - zi) * wb[r + 4];
+      }
+      if (r < t) a0 += (double)expf(L[(size_t)r * np_] - zi) * wb[r];
     }
-    if (r < t) a0 += (double)expf(L[(size_t)r * np_] - zi) * wb[r];
   }
   red[wave][lane] = a0 + a1;
   __syncthreads();
@@ -590,14 +618,21 @@ __global__ void __launch_bounds__(256) k_mass_resid_rows(const float *__restrict
 }
 
 // Stage 2 (one wave per compact key r): res_r = sum_i Phi[i][r] u_i - lam w_r.
+// With a list, wave k handles key list[k] (k < count) and writes only there.
 __global__ void __launch_bounds__(256) k_mass_resid_cols(const float *__restrict__ LT, const float *__restrict__ z,
                                                          const double *__restrict__ u, const double *__restrict__ w,
                                                          const float *__restrict__ lam, int n, int t, int64_t tp,
                                                          int64_t np_, double *__restrict__ res,
-                                                         const int32_t *__restrict__ info) {
+                                                         const int32_t *__restrict__ info,
+                                                         const int32_t *__restrict__ list,
+                                                         const int32_t *__restrict__ count) {
   const int b = blockIdx.y, lane = threadIdx.x & 63;
-  const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
+  int r = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (r >= tp || info[b] != 0) return;
+  if (list) {
+    if (r >= count[b]) return;
+    r = list[(size_t)b * tp + r];
+  }
   double acc = 0.0;
   if (r < t) {
     const float *row = LT + ((size_t)b * tp + r) * np_;
@@ -936,19 +971,20 @@ __global__ void __launch_bounds__(256) k_values_out(const float *__restrict__ Xp
 // form of Kim & Park 2011) for min ||Phi_C w - m||^2 + lam ||w||^2, w >= 0, the
 // ridged system of the projected fit.  Per pair: F (passive set, 1 = free), x,
 // y = (G + lam I) x - h from the data residual, and the state
-// {best infeasible count N, backup budget p, done, spare}.
+// {best infeasible count N, backup budget p, done, spare}.  The iteration starts
+// from the unconstrained solution (F = every key), which the projected fit has
+// already computed; each later iteration solves the free-set system compressed
+// to its |F| x |F| block.
 constexpr int32_t kNnlsSkip = -0x40000000;   // info marker of a pair that has converged
 
-__global__ void __launch_bounds__(256) k_nnls_init(const double *__restrict__ h, int t, int64_t tp,
-                                                   const int32_t *__restrict__ info, int32_t *__restrict__ F,
-                                                   double *__restrict__ x, double *__restrict__ y,
+__global__ void __launch_bounds__(256) k_nnls_init(int t, int64_t tp, const int32_t *__restrict__ info,
+                                                   int32_t *__restrict__ F, double *__restrict__ y,
                                                    int32_t *__restrict__ state) {
   const int b = blockIdx.y;
   const int64_t r = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (r < tp) {
-    F[(size_t)b * tp + r] = 0;
-    x[(size_t)b * tp + r] = 0.0;
-    y[(size_t)b * tp + r] = r < t ? -h[(size_t)b * tp + r] : 0.0;
+    F[(size_t)b * tp + r] = r < t;
+    y[(size_t)b * tp + r] = 0.0;
   }
   if (r == 0) {
     state[4 * b] = t + 1;
@@ -1024,6 +1060,7 @@ __global__ void __launch_bounds__(256) k_nnls_update(const double *__restrict__ 
     } else {
       mode = 2;
     }
+    state[4 * b + 3] += mode != 0;   // iterations taken
     s_mode = mode;
   }
   __syncthreads();
@@ -1036,31 +1073,106 @@ __global__ void __launch_bounds__(256) k_nnls_update(const double *__restrict__ 
   }
 }
 
-// Work copy of the passive system: G_ij + lam [i = j] on F x F, identity elsewhere.
-__global__ void __launch_bounds__(256) k_nnls_gram(const float *__restrict__ Gc, const int32_t *__restrict__ F,
-                                                   const FitState st, int t, int64_t ld, float *__restrict__ Gw) {
+__global__ void k_nnls_zero(int32_t *__restrict__ red) {
+  if (threadIdx.x < 2) red[threadIdx.x] = 0;
+}
+
+// Free list of every unsettled pair: idx[k] = the k-th free key (ascending),
+// pos[r] = its slot or -1, nf = |F|; red = {max nf, unsettled pairs}.
+// Free and bound lists of every unsettled pair: idx[k] = the k-th free key,
+// bidx[k] = the k-th bound key (both ascending), pos[r] = the free slot of r or
+// -1; nf = |F|, nb = t - |F|; red = {max nf, unsettled pairs}.
+__global__ void __launch_bounds__(256) k_nnls_index(const int32_t *__restrict__ F, int t, int64_t tp,
+                                                    const int32_t *__restrict__ info, int32_t *__restrict__ idx,
+                                                    int32_t *__restrict__ bidx, int32_t *__restrict__ pos,
+                                                    int32_t *__restrict__ nf, int32_t *__restrict__ nb,
+                                                    int32_t *__restrict__ red) {
+  __shared__ int32_t wsum[4];
+  __shared__ int32_t base;
+  const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  if (info[b] != 0) return;   // settled or failed
+  if (tid == 0) base = 0;
+  __syncthreads();
+  const int32_t *Fb = F + (size_t)b * tp;
+  int32_t *ib = idx + (size_t)b * tp, *bb = bidx + (size_t)b * tp, *pb = pos + (size_t)b * tp;
+  for (int64_t r0 = 0; r0 < tp; r0 += 256) {
+    const int64_t r = r0 + tid;
+    const bool f = r < t && Fb[r] != 0;
+    const uint64_t m = __ballot(f);
+    if (lane == 0) wsum[wave] = __popcll(m);
+    __syncthreads();
+    int32_t before = base + __popcll(m & ((1ull << lane) - 1ull));   // free keys below r
+    for (int w = 0; w < wave; ++w) before += wsum[w];
+    if (f) ib[before] = (int32_t)r;
+    else if (r < t) bb[r - before] = (int32_t)r;
+    if (r < tp) pb[r] = f ? before : -1;
+    __syncthreads();
+    if (tid == 0) base += wsum[0] + wsum[1] + wsum[2] + wsum[3];
+    __syncthreads();
+  }
+  if (tid == 0) {
+    nf[b] = base;
+    nb[b] = t - base;
+    atomicMax(&red[0], base);
+    atomicAdd(&red[1], 1);
+  }
+}
+
+// Compressed free-set system [ldf][ldf]: G_{idx_i idx_j} + lam [i = j] for
+// i, j < nf, identity beyond.
+__global__ void __launch_bounds__(256) k_nnls_gather_gram(const float *__restrict__ Gc, int64_t tp,
+                                                          const int32_t *__restrict__ idx,
+                                                          const int32_t *__restrict__ nf, const FitState st,
+                                                          int64_t ldf, float *__restrict__ Gw) {
   const int b = blockIdx.y;
   if (st.info[b] != 0) return;
   const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (e >= ld * ld) return;
-  const int64_t i = e / ld, j = e % ld;
-  const size_t o = (size_t)b * ld * ld + e;
-  const int32_t *Fb = F + (size_t)b * ld;
-  const bool fi = i < t && Fb[i], fj = j < t && Fb[j];
-  Gw[o] = (fi && fj) ? Gc[o] + (i == j ? st.lam[b] : 0.0f) : (i == j ? 1.0f : 0.0f);
+  if (e >= ldf * ldf) return;
+  const int64_t i = e / ldf, j = e % ldf;
+  const int32_t n = nf[b];
+  float v = i == j ? 1.0f : 0.0f;
+  if (i < n && j < n) {
+    const int32_t *ib = idx + (size_t)b * tp;
+    v = Gc[(size_t)b * tp * tp + (size_t)ib[i] * tp + ib[j]] + (i == j ? st.lam[b] : 0.0f);
+  }
+  Gw[(size_t)b * ldf * ldf + e] = v;
 }
 
-// mode 0: out = F ? in : 0 (right-hand side, refinement residual);
-// mode 1: out = F ? 0 : -in (y = -(residual) on the bound variables).
-__global__ void __launch_bounds__(256) k_nnls_mask(const double *__restrict__ in, const int32_t *__restrict__ F,
-                                                   int64_t tp, int mode, const int32_t *__restrict__ info,
-                                                   double *__restrict__ out) {
+// out[k] = in[idx_k] for k < nf, 0 beyond (a compressed right-hand side).
+__global__ void __launch_bounds__(256) k_nnls_gather_vec(const double *__restrict__ in, int64_t tp,
+                                                         const int32_t *__restrict__ idx,
+                                                         const int32_t *__restrict__ nf,
+                                                         const int32_t *__restrict__ info, int64_t ldf,
+                                                         double *__restrict__ out) {
+  const int b = blockIdx.y;
+  const int64_t k = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (k >= ldf || info[b] != 0) return;
+  out[(size_t)b * ldf + k] = k < nf[b] ? in[(size_t)b * tp + idx[(size_t)b * tp + k]] : 0.0;
+}
+
+// x[r] = xf[pos_r] on free keys and 0 on bound ones (acc: x[r] += ...).
+__global__ void __launch_bounds__(256) k_nnls_scatter(const double *__restrict__ xf, int64_t ldf,
+                                                      const int32_t *__restrict__ pos, int64_t tp,
+                                                      const int32_t *__restrict__ info, int acc,
+                                                      double *__restrict__ x) {
+  const int b = blockIdx.y;
+  const int64_t r = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (r >= tp || info[b] != 0) return;
+  const int32_t p = pos[(size_t)b * tp + r];
+  const double v = p >= 0 ? xf[(size_t)b * ldf + p] : 0.0;
+  double *o = x + (size_t)b * tp + r;
+  *o = acc ? *o + v : v;
+}
+
+// y = -(data residual) on bound keys, 0 on free ones.
+__global__ void __launch_bounds__(256) k_nnls_dual(const double *__restrict__ res, const int32_t *__restrict__ F,
+                                                   int64_t tp, const int32_t *__restrict__ info,
+                                                   double *__restrict__ y) {
   const int b = blockIdx.y;
   const int64_t r = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (r >= tp || info[b] != 0) return;
   const size_t o = (size_t)b * tp + r;
-  const bool f = F[o] != 0;
-  out[o] = mode == 0 ? (f ? in[o] : 0.0) : (f ? 0.0 : -in[o]);
+  y[o] = F[o] ? 0.0 : -res[o];
 }
 
 // After the iterations: converged pairs are ok again; pairs still iterating get -2.
@@ -1146,43 +1258,60 @@ hipError_t launch_trsv(const float *Gw, const float *dinv, int B, int64_t ld, co
 
 hipError_t launch_mass_residual(const float *LT, const float *z, const float *m, const double *w, const float *lam,
                                 int B, int n, int t, int64_t tp, int64_t np_, double *u, double *res,
-                                const int32_t *info, hipStream_t s) {
+                                const int32_t *info, hipStream_t s, const int32_t *row_list,
+                                const int32_t *row_count, const int32_t *col_list, const int32_t *col_count) {
   hipLaunchKernelGGL(k_mass_resid_rows, dim3((unsigned)(np_ / 64), B), dim3(256), 0, s, LT, z, m, w, n, t, tp, np_,
-                     u, info);
+                     u, info, row_list, row_count);
   hipLaunchKernelGGL(k_mass_resid_cols, dim3((unsigned)(tp / 4), B), dim3(256), 0, s, LT, z, u, w, lam, n, t, tp,
-                     np_, res, info);
+                     np_, res, info, col_list, col_count);
   return hipGetLastError();
 }
 
+// Pivoting iterations on the projected fit's refined solution x (in place).
+// Each iteration reads back {largest free set, unsettled pairs} to size the
+// compressed system and to stop once every pair has settled, so this
+// synchronises the stream once per iteration.
 hipError_t launch_nnls(const float *Gc, float *Gw, const double *h, const float *LT, const float *z, const float *m,
                        int B, int n, int t, int64_t tp, int64_t np_, int max_iter, int refine_steps, FitState st,
-                       float *dinv, void *lsplit, int32_t *F, double *x, double *yv, int32_t *state, double *rhs,
-                       double *sw, double *yw, double *dx, double *u, double *res, hipStream_t s) {
+                       float *dinv, void *lsplit, NnlsWork nw, double *x, double *sw, double *yw, double *u,
+                       double *res, hipStream_t s) {
   const dim3 gv((unsigned)((tp + 255) / 256), (unsigned)B);
-  hipLaunchKernelGGL(k_nnls_init, gv, dim3(256), 0, s, h, t, tp, st.info, F, x, yv, state);
+  hipLaunchKernelGGL(k_nnls_init, gv, dim3(256), 0, s, t, tp, st.info, nw.F, nw.y, nw.state);
+  hipError_t e;
   for (int it = 0;; ++it) {
     // the update after the last solve only checks feasibility (and marks done)
-    hipLaunchKernelGGL(k_nnls_update, dim3(B), dim3(256), 0, s, x, yv, h, t, tp, F, state, st.info);
+    hipLaunchKernelGGL(k_nnls_update, dim3(B), dim3(256), 0, s, x, nw.y, h, t, tp, nw.F, nw.state, st.info);
     if (it == max_iter) break;
-    hipLaunchKernelGGL(k_nnls_gram, dim3((unsigned)((tp * tp + 255) / 256), (unsigned)B), dim3(256), 0, s, Gc, F, st,
-                       t, tp, Gw);
-    hipError_t e = launch_cholesky_factor(Gw, Gc, B, t, tp, 0.0f, 0, st, dinv, lsplit, s);
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k_nnls_mask, gv, dim3(256), 0, s, h, F, tp, 0, st.info, rhs);
-    e = launch_trsv(Gw, dinv, B, tp, rhs, sw, yw, x, nullptr, st.info, s);
-    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_nnls_zero, dim3(1), dim3(64), 0, s, nw.red);
+    hipLaunchKernelGGL(k_nnls_index, dim3(B), dim3(256), 0, s, nw.F, t, tp, st.info, nw.idx, nw.bidx, nw.pos,
+                       nw.nf, nw.nb, nw.red);
+    int32_t red[2] = {0, 0};
+    if ((e = hipMemcpyAsync(red, nw.red, sizeof(red), hipMemcpyDeviceToHost, s)) != hipSuccess) return e;
+    if ((e = hipStreamSynchronize(s)) != hipSuccess) return e;
+    if (red[1] == 0) break;   // every pair has settled (or failed)
+    const int64_t ldf = red[0] > 256 ? (red[0] + 255) / 256 * 256 : 256;
+    const dim3 gf((unsigned)((ldf + 255) / 256), (unsigned)B);
+    hipLaunchKernelGGL(k_nnls_gather_gram, dim3((unsigned)((ldf * ldf + 255) / 256), (unsigned)B), dim3(256), 0, s,
+                       Gc, tp, nw.idx, nw.nf, st, ldf, Gw);
+    if ((e = launch_cholesky_factor(Gw, Gc, B, t, ldf, 0.0f, 0, st, dinv, lsplit, s)) != hipSuccess) return e;
     for (int rs = 0; rs <= refine_steps; ++rs) {
-      // residual of the full ridged system from the data: h - (G + lam I) x
-      e = launch_mass_residual(LT, z, m, x, st.lam, B, n, t, tp, np_, u, res, st.info, s);
-      if (e != hipSuccess) return e;
-      if (rs == refine_steps) break;
-      hipLaunchKernelGGL(k_nnls_mask, gv, dim3(256), 0, s, res, F, tp, 0, st.info, dx);
-      e = launch_trsv(Gw, dinv, B, tp, dx, sw, yw, dx, x, st.info, s);
-      if (e != hipSuccess) return e;
+      // rs = 0 solves for x from h; later steps solve for a correction from the
+      // residual of the full ridged system against the data, h - (G + lam I) x
+      hipLaunchKernelGGL(k_nnls_gather_vec, gf, dim3(256), 0, s, rs == 0 ? h : res, tp, nw.idx, nw.nf, st.info, ldf,
+                         nw.rf);
+      if ((e = launch_trsv(Gw, dinv, B, ldf, nw.rf, sw, yw, nw.xf, nullptr, st.info, s)) != hipSuccess) return e;
+      hipLaunchKernelGGL(k_nnls_scatter, gv, dim3(256), 0, s, nw.xf, ldf, nw.pos, tp, st.info, rs > 0 ? 1 : 0, x);
+      // x vanishes off F, so Phi_C x sums over the free keys; the residual is
+      // needed on the free keys for a correction, on the bound keys (the dual)
+      // after the last one
+      const bool last = rs == refine_steps;
+      if ((e = launch_mass_residual(LT, z, m, x, st.lam, B, n, t, tp, np_, u, res, st.info, s, nw.idx, nw.nf,
+                                    last ? nw.bidx : nw.idx, last ? nw.nb : nw.nf)) != hipSuccess)
+        return e;
     }
-    hipLaunchKernelGGL(k_nnls_mask, gv, dim3(256), 0, s, res, F, tp, 1, st.info, yv);
+    hipLaunchKernelGGL(k_nnls_dual, gv, dim3(256), 0, s, res, nw.F, tp, st.info, nw.y);
   }
-  hipLaunchKernelGGL(k_nnls_finish, dim3((unsigned)((B + 255) / 256)), dim3(256), 0, s, state, B, st.info);
+  hipLaunchKernelGGL(k_nnls_finish, dim3((unsigned)((B + 255) / 256)), dim3(256), 0, s, nw.state, B, st.info);
   return hipGetLastError();
 }
 

@@ -20,6 +20,9 @@
 // Dimensions must be multiples of the tile; workgroups are remapped so that
 // each XCD owns a contiguous, M-grouped (or lower-triangular) range of tiles.
 #pragma once
+#include <type_traits>
+#include <utility>
+
 #include "gemm.hpp"
 
 namespace arckv {
@@ -104,6 +107,13 @@ __device__ __forceinline__ void lds_barrier() {
   asm volatile("" ::: "memory");
 }
 
+// An epilogue may expose skip(p): the whole tile is skipped for pair p (a
+// factorisation that failed or no longer needs updating).
+template <typename E, typename = void>
+struct epi_has_skip : std::false_type {};
+template <typename E>
+struct epi_has_skip<E, std::void_t<decltype(std::declval<const E &>().skip(0))>> : std::true_type {};
+
 template <int WM, int WN, int TM, int TN, int BK, int NA, int NB, int NS, class Epi>
 __global__ void __launch_bounds__(64 * WM * WN, 1) k_gemm_big(BigShape g, const bf16 *__restrict__ A,
                                                               const bf16 *__restrict__ B, Epi epi) {
@@ -113,6 +123,9 @@ __global__ void __launch_bounds__(64 * WM * WN, 1) k_gemm_big(BigShape g, const 
   const int64_t tile = xcd_remap(blockIdx.x, gridDim.x);
   int p, mt, nt;
   big_tile<C::BM, C::BN>(g, tile, p, mt, nt);
+  if constexpr (epi_has_skip<Epi>::value) {
+    if (epi.skip(p)) return;   // uniform over the workgroup: no barrier has run yet
+  }
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WN, wn = wave % WN;
   const int h = lane >> 5, col = lane & 31;
