@@ -572,53 +572,65 @@ __global__ void __launch_bounds__(256) k_trsv_step(const float *__restrict__ Gw,
 // (list [P][tp], count [P]): the exact non-negative fit sums only over its free
 // keys (w = 0 elsewhere) and needs each residual only on one side of its
 // partition.  Without a list every key r < t takes part.
-// Stage 1 (one thread per query i): u_i = m_i - sum_{r<t} Phi[i][r] w_r.
+// Stage 1: u_i = m_i - sum_{r<t} Phi[i][r] w_r.  256 queries per workgroup,
+// four per lane (16-byte loads of the L^T rows); wave s sums the compact keys
+// r = s (mod 4) with two accumulator sets, and the four partial sums meet in LDS.
 __global__ void __launch_bounds__(256) k_mass_resid_rows(const float *__restrict__ LT, const float *__restrict__ z,
                                                          const float *__restrict__ m, const double *__restrict__ w,
                                                          int n, int t, int64_t tp, int64_t np_,
                                                          double *__restrict__ u, const int32_t *__restrict__ info,
                                                          const int32_t *__restrict__ list,
                                                          const int32_t *__restrict__ count) {
-  // 64 queries per workgroup; wave s sums the compact keys r = s (mod 4) with
-  // two accumulators, and the four partial sums meet in LDS
-  __shared__ double red[4][64];
-  const int b = blockIdx.y, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int i = blockIdx.x * 64 + lane;
+  __shared__ double red[4][256];
+  const int b = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   if (info[b] != 0) return;
-  double a0 = 0.0, a1 = 0.0;
-  if (i < n) {
-    const float *L = LT + (size_t)b * tp * np_ + i;
+  const int i0 = blockIdx.x * 256 + 4 * lane;
+  double a0[4] = {0.0, 0.0, 0.0, 0.0}, a1[4] = {0.0, 0.0, 0.0, 0.0};
+  if (i0 < n) {
+    const float *L = LT + (size_t)b * tp * np_ + i0;   // L^T rows are zero beyond n
     const double *wb = w + (size_t)b * tp;
-    const float zi = z[(size_t)b * n + i];
+    float zi[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) zi[k] = i0 + k < n ? z[(size_t)b * n + i0 + k] : 0.0f;
+    auto term = [&](int r, double (&a)[4]) {
+      const f32x4 v = *reinterpret_cast<const f32x4 *>(L + (size_t)r * np_);
+      const double wr = wb[r];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) a[k] += (double)expf(v[k] - zi[k]) * wr;
+    };
     if (list) {
       const int32_t *lb = list + (size_t)b * tp;
       const int c = count[b];
       int k = wave;
       for (; k + 4 < c; k += 8) {
-        const int r0 = lb[k], r1 = lb[k + 4];
-        a0 += (double)expf(L[(size_t)r0 * np_] - zi) * wb[r0];
-        a1 += (double)expf(L[(size_t)r1 * np_] - zi) * wb[r1];
+        term(lb[k], a0);
+        term(lb[k + 4], a1);
       }
-      if (k < c) a0 += (double)expf(L[(size_t)lb[k] * np_] - zi) * wb[lb[k]];
+      if (k < c) term(lb[k], a0);
     } else {
       int r = wave;
       for (; r + 4 < t; r += 8) {
-        a0 += (double)expf(L[(size_t)r * np_] - zi) * wb[r];
-        a1 += (double)expf(L[(size_t)(r + 4) * np_] - zi) * wb[r + 4];
+        term(r, a0);
+        term(r + 4, a1);
       }
-      if (r < t) a0 += (double)expf(L[(size_t)r * np_] - zi) * wb[r];
+      if (r < t) term(r, a0);
     }
   }
-  red[wave][lane] = a0 + a1;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) red[wave][4 * lane + k] = a0[k] + a1[k];
   __syncthreads();
-  if (wave == 0 && i < np_) {
-    const double acc = red[0][lane] + red[1][lane] + red[2][lane] + red[3][lane];
+  const int i = blockIdx.x * 256 + tid;
+  if (i < np_) {
+    const double acc = red[0][tid] + red[1][tid] + red[2][tid] + red[3][tid];
     u[(size_t)b * np_ + i] = i < n ? (double)m[(size_t)b * n + i] - acc : 0.0;
   }
 }
 
-// Stage 2 (one wave per compact key r): res_r = sum_i Phi[i][r] u_i - lam w_r.
-// With a list, wave k handles key list[k] (k < count) and writes only there.
+// Stage 2: res_r = sum_i Phi[i][r] u_i - lam w_r.  Each wave takes four
+// compact keys (16 per workgroup) so that the z and u loads are shared by
+// them; four queries per lane per step (16-byte loads of the L^T rows and of
+// u).  With a list, slot k handles key list[k] (k < count) and writes only there.
+constexpr int kResKeys = 4;   // compact keys per wave
 __global__ void __launch_bounds__(256) k_mass_resid_cols(const float *__restrict__ LT, const float *__restrict__ z,
                                                          const double *__restrict__ u, const double *__restrict__ w,
                                                          const float *__restrict__ lam, int n, int t, int64_t tp,
@@ -626,28 +638,53 @@ __global__ void __launch_bounds__(256) k_mass_resid_cols(const float *__restrict
                                                          const int32_t *__restrict__ info,
                                                          const int32_t *__restrict__ list,
                                                          const int32_t *__restrict__ count) {
+  typedef __attribute__((__vector_size__(2 * sizeof(double)))) double f64x2;
   const int b = blockIdx.y, lane = threadIdx.x & 63;
-  int r = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (r >= tp || info[b] != 0) return;
-  if (list) {
-    if (r >= count[b]) return;
-    r = list[(size_t)b * tp + r];
+  const int k0 = (blockIdx.x * 4 + (threadIdx.x >> 6)) * kResKeys;   // first slot of this wave
+  if (k0 >= tp || info[b] != 0) return;
+  const int lim = list ? count[b] : t;   // slots k < lim are live keys
+  if (k0 >= lim) {
+    if (!list && lane < kResKeys) res[(size_t)b * tp + k0 + lane] = 0.0;   // padding keys r >= t
+    return;
   }
-  double acc = 0.0;
-  if (r < t) {
-    const float *row = LT + ((size_t)b * tp + r) * np_;
-    const float *zb = z + (size_t)b * n;
-    const double *ub = u + (size_t)b * np_;
-    double a1 = 0.0;
-    int i = lane;
-    for (; i + 64 < n; i += 128) {
-      acc += (double)expf(row[i] - zb[i]) * ub[i];
-      a1 += (double)expf(row[i + 64] - zb[i + 64]) * ub[i + 64];
+  int r[kResKeys];
+  const float *row[kResKeys];
+#pragma unroll
+  for (int q = 0; q < kResKeys; ++q) {
+    const int k = k0 + q < lim ? k0 + q : lim - 1;   // dead slots repeat a live key, unstored
+    r[q] = list ? list[(size_t)b * tp + k] : k;
+    row[q] = LT + ((size_t)b * tp + r[q]) * np_;
+  }
+  const float *zb = z + (size_t)b * n;
+  const double *ub = u + (size_t)b * np_;   // zero beyond n
+  double acc[kResKeys] = {0.0, 0.0, 0.0, 0.0};
+  for (int i0 = 4 * lane; i0 < n; i0 += 256) {
+    const f64x2 u01 = *reinterpret_cast<const f64x2 *>(ub + i0);
+    const f64x2 u23 = *reinterpret_cast<const f64x2 *>(ub + i0 + 2);
+    const double uu[4] = {u01[0], u01[1], u23[0], u23[1]};
+    float zz[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) zz[e] = zb[i0 + e < n ? i0 + e : n - 1];
+#pragma unroll
+    for (int q = 0; q < kResKeys; ++q) {
+      const f32x4 v = *reinterpret_cast<const f32x4 *>(row[q] + i0);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const double term = (double)expf(v[e] - zz[e]) * uu[e];
+        acc[q] += i0 + e < n ? term : 0.0;
+      }
     }
-    if (i < n) acc += (double)expf(row[i] - zb[i]) * ub[i];
-    acc = wave_sum(acc + a1) - (double)lam[b] * w[(size_t)b * tp + r];
   }
-  if (lane == 0) res[(size_t)b * tp + r] = acc;
+#pragma unroll
+  for (int q = 0; q < kResKeys; ++q) {
+    const double sum = wave_sum(acc[q]);
+    if (lane == 0 && k0 + q < lim)
+      res[(size_t)b * tp + r[q]] = sum - (double)lam[b] * w[(size_t)b * tp + r[q]];
+  }
+  if (!list && lane >= kResKeys && lane < 2 * kResKeys) {   // padding keys r >= t within this wave's slots
+    const int k = k0 + lane - kResKeys;
+    if (k >= lim && k < tp) res[(size_t)b * tp + k] = 0.0;
+  }
 }
 
 // beta = clip(log(max(max(w, 0), eps)), bmin, bmax); NaN for failed pairs.
@@ -1260,10 +1297,10 @@ hipError_t launch_mass_residual(const float *LT, const float *z, const float *m,
                                 int B, int n, int t, int64_t tp, int64_t np_, double *u, double *res,
                                 const int32_t *info, hipStream_t s, const int32_t *row_list,
                                 const int32_t *row_count, const int32_t *col_list, const int32_t *col_count) {
-  hipLaunchKernelGGL(k_mass_resid_rows, dim3((unsigned)(np_ / 64), B), dim3(256), 0, s, LT, z, m, w, n, t, tp, np_,
+  hipLaunchKernelGGL(k_mass_resid_rows, dim3((unsigned)(np_ / 256), B), dim3(256), 0, s, LT, z, m, w, n, t, tp, np_,
                      u, info, row_list, row_count);
-  hipLaunchKernelGGL(k_mass_resid_cols, dim3((unsigned)(tp / 4), B), dim3(256), 0, s, LT, z, u, w, lam, n, t, tp,
-                     np_, res, info, col_list, col_count);
+  hipLaunchKernelGGL(k_mass_resid_cols, dim3((unsigned)(tp / (4 * kResKeys)), B), dim3(256), 0, s, LT, z, u, w, lam,
+                     n, t, tp, np_, res, info, col_list, col_count);
   return hipGetLastError();
 }
 
