@@ -1170,7 +1170,9 @@ __global__ void __launch_bounds__(256) k_nnls_gather_gram(const float *__restric
   float v = i == j ? 1.0f : 0.0f;
   if (i < n && j < n) {
     const int32_t *ib = idx + (size_t)b * tp;
-    v = Gc[(size_t)b * tp * tp + (size_t)ib[i] * tp + ib[j]] + (i == j ? st.lam[b] : 0.0f);
+    // the free list ascends, so i >= j reads the stored lower triangle
+    const int64_t hi = i >= j ? i : j, lo = i >= j ? j : i;
+    v = Gc[(size_t)b * tp * tp + (size_t)ib[hi] * tp + ib[lo]] + (i == j ? st.lam[b] : 0.0f);
   }
   Gw[(size_t)b * ldf * ldf + e] = v;
 }

@@ -274,13 +274,15 @@ struct EpiArgmaxBig {
   }
 };
 
-// Symmetric Gram: write the tile to G and Gc, and its transpose above the diagonal.
+// Symmetric Gram: write the lower tile to G and Gc.  The strict upper triangle
+// outside the diagonal tiles is left unwritten: the factorisation, the solves
+// and the free-set gathers read the lower triangle only.
 template <int TM, int TN>
 struct EpiSymBig {
   float *G, *Gc;
   int64_t pair_stride;
   int ld;
-  __device__ __forceinline__ void operator()(f32x16 (&acc)[TM][TN], int p, int row0, int col0, int mt, int nt,
+  __device__ __forceinline__ void operator()(f32x16 (&acc)[TM][TN], int p, int row0, int col0, int, int,
                                              int lane, int, int) const {
     const int h = lane >> 5, col = lane & 31;
     float *Gp = G + (size_t)p * pair_stride, *Gcp = Gc + (size_t)p * pair_stride;
@@ -297,10 +299,6 @@ struct EpiSymBig {
           for (int e = 0; e < 4; ++e) {
             Gp[(size_t)(r0 + e) * ld + c] = v[e];
             Gcp[(size_t)(r0 + e) * ld + c] = v[e];
-          }
-          if (mt != nt) {
-            *reinterpret_cast<f32x4 *>(Gp + (size_t)c * ld + r0) = v;
-            *reinterpret_cast<f32x4 *>(Gcp + (size_t)c * ld + r0) = v;
           }
         }
       }
