@@ -15,8 +15,10 @@
 //   k_dsa_index     I_ij = sum_a w_ia LeakyReLU(qbar_ia . kbar_ja / sqrt(d_I))
 //                   (eq. pairwise_index_score) for 64 queries per workgroup,
 //                   whose qbar rows stay in LDS while the workgroup sweeps all
-//                   keys (each wave 32 keys of a 128-key block, the next head's
-//                   key fragments prefetched during the current head).  Pass 1
+//                   keys (eight waves, two per SIMD so that one wave's
+//                   LeakyReLU epilogue overlaps the other's MFMAs; each wave 32
+//                   keys of a 256-key block, the next heads' key fragments
+//                   prefetched during the current ones).  Pass 1
 //                   keeps each row's softmax max and sum; pass 2 adds
 //                   pi_ij^2 = exp(2 (I_ij - z_i)) / m_i^2 over the workgroup's
 //                   queries into a per-(query block, key) partial.
@@ -29,7 +31,9 @@ namespace {
 constexpr int kDsaH = 8;            // index heads H_I
 constexpr int kDsaW = 128;          // d_I = d_A
 constexpr int kDsaQB = 64;          // queries per index workgroup
-constexpr int kDsaKB = 128;         // keys per sweep step (32 per wave)
+constexpr int kDsaWaves = 8;        // index workgroup: 8 waves (two per SIMD) share one LDS query block
+constexpr int kDsaKT = 1;           // 32-key tiles per wave (each LDS query fragment feeds kDsaKT MFMAs)
+constexpr int kDsaKB = kDsaWaves * 32 * kDsaKT;   // keys per sweep step
 constexpr float kLeaky = 0.1f;
 constexpr float kRmsEps = 1e-6f;
 
@@ -124,27 +128,27 @@ __global__ void __launch_bounds__(64) k_dsa_w(const bf16 *__restrict__ X, const 
 // grid (ceil(n / 64), B); LDS: the block's qbar rows [64][1024] bf16 (16-byte
 // chunks swizzled within each head's 256-byte run), w and the row statistics.
 template <int PASS>
-__global__ void __launch_bounds__(256) k_dsa_index(const bf16 *__restrict__ qbar, const bf16 *__restrict__ kbar,
+__global__ void __launch_bounds__(64 * kDsaWaves) __attribute__((amdgpu_waves_per_eu(2, 2))) k_dsa_index(const bf16 *__restrict__ qbar, const bf16 *__restrict__ kbar,
                                                    const float *__restrict__ wpos, int n, int n_pos, int T,
                                                    float *__restrict__ z, float *__restrict__ m,
                                                    float *__restrict__ part) {
   extern __shared__ __attribute__((aligned(16))) char dsa_smem[];
   char *sq = dsa_smem;                                                  // 64 x 2048 B
   float *sw = reinterpret_cast<float *>(dsa_smem + kDsaQB * 2048);     // [64][8]
-  float *sred = sw + kDsaQB * kDsaH;                                    // [4 waves][64][2]
+  float *sred = sw + kDsaQB * kDsaH;                                    // [waves][64][2]
   const int p = blockIdx.y, q0 = blockIdx.x * kDsaQB;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int h = lane >> 5, col = lane & 31;
   const float inv_sqrt = 1.0f / sqrtf((float)kDsaW);
   // ---- stage qbar rows (missing rows read as zero) and the head weights w / sqrt(d_I)
-  for (int e = tid; e < kDsaQB * 128; e += 256) {
+  for (int e = tid; e < kDsaQB * 128; e += 64 * kDsaWaves) {
     const int q = e >> 7, c = e & 127;
     bf16x8 v = Mfma<bf16>::zero();
     if (q0 + q < n) v = load_frag(qbar + ((size_t)p * n + q0 + q) * (kDsaH * kDsaW) + 8 * c);
     const int phys = (c & ~15) | ((c ^ q) & 15);
     *reinterpret_cast<bf16x8 *>(sq + q * 2048 + phys * 16) = v;
   }
-  for (int e = tid; e < kDsaQB * kDsaH; e += 256) {
+  for (int e = tid; e < kDsaQB * kDsaH; e += 64 * kDsaWaves) {
     const int q = e / kDsaH, a = e % kDsaH;
     sw[e] = q0 + q < n ? wpos[((size_t)p * n_pos + (q0 + q) % n_pos) * kDsaH + a] * inv_sqrt : 0.0f;
   }
@@ -162,93 +166,117 @@ __global__ void __launch_bounds__(256) k_dsa_index(const bf16 *__restrict__ qbar
   float run_m[2] = {-INFINITY, -INFINITY}, run_s[2] = {0.0f, 0.0f};   // PASS 1
   const bf16 *kb = kbar + (size_t)p * T * (kDsaH * kDsaW) + 8 * h;
   const int nkb = (T + kDsaKB - 1) / kDsaKB;
-  // a ring of four heads' key fragments (128 VGPRs): head a's slot is refilled
-  // with head a + 4 (the next block's head a - 4 in the second half) right
-  // after use, so every load has four heads of MFMAs to land
-  constexpr int RING = 4;
-  bf16x8 af[RING][8];
-  auto fetch = [&](int kbk_, int a, bf16x8 (&f)[8]) {
-    const int key = kbk_ * kDsaKB + wave * 32 + col;
-    const bf16 *krow = kb + (size_t)(key < T ? key : 0) * (kDsaH * kDsaW) + a * kDsaW;
+  // a ring of two heads' key fragments for the wave's key tiles (128 VGPRs):
+  // head a's slot is refilled with head a + 2 (or, for the last two heads, the
+  // next block's first two) right after use, so every load has a head of MFMAs
+  // to land
+  constexpr int RING = 2;
+  bf16x8 af[RING][kDsaKT][8];
+  auto fetch = [&](int kbk_, int a, bf16x8 (&f)[kDsaKT][8]) {
 #pragma unroll
-    for (int ks = 0; ks < 8; ++ks) f[ks] = key < T ? load_frag(krow + 16 * ks) : Mfma<bf16>::zero();
+    for (int kt = 0; kt < kDsaKT; ++kt) {
+      const int key = kbk_ * kDsaKB + wave * (32 * kDsaKT) + 32 * kt + col;
+      const bf16 *krow = kb + (size_t)(key < T ? key : 0) * (kDsaH * kDsaW) + a * kDsaW;
+#pragma unroll
+      for (int ks = 0; ks < 8; ++ks) f[kt][ks] = key < T ? load_frag(krow + 16 * ks) : Mfma<bf16>::zero();
+    }
   };
 #pragma unroll
   for (int a = 0; a < RING; ++a) fetch(0, a, af[a]);
   for (int kbk = 0; kbk < nkb; ++kbk) {
     // the query embeddings are re-read from LDS in every key block (not held in registers)
     asm volatile("" ::: "memory");
-    float I[2][16];
+    float I[2][kDsaKT][16];
 #pragma unroll
     for (int nt = 0; nt < 2; ++nt)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) I[nt][v] = 0.0f;
+      for (int kt = 0; kt < kDsaKT; ++kt)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) I[nt][kt][v] = 0.0f;
 #pragma unroll 1
     for (int a0 = 0; a0 < kDsaH; a0 += RING) {
       asm volatile("" ::: "memory");
 #pragma unroll
       for (int i = 0; i < RING; ++i) {
         const int a = a0 + i;
-        // head a: S = kbar_a qbar_a^T for both query tiles, I += (w_a / sqrt d_I) LeakyReLU(S)
+        // head a: S = kbar_a qbar_a^T for both query tiles and every key tile,
+        // I += (w_a / sqrt d_I) LeakyReLU(S); each query fragment read from LDS
+        // serves all key tiles
 #pragma unroll
         for (int nt = 0; nt < 2; ++nt) {
           const int q = 32 * nt + col;
-          f32x16 acc = zero16();
+          f32x16 acc[kDsaKT];
+#pragma unroll
+          for (int kt = 0; kt < kDsaKT; ++kt) acc[kt] = zero16();
 #pragma unroll
           for (int ks = 0; ks < 8; ++ks) {
             const int c = 16 * a + 2 * ks + h;
             const int phys = (c & ~15) | ((c ^ q) & 15);
-            acc = Mfma<bf16>::mma(af[i][ks], *reinterpret_cast<const bf16x8 *>(sq + q * 2048 + phys * 16), acc);
-          }
-          const float wa = sw[q * kDsaH + a];
+            const bf16x8 qf = *reinterpret_cast<const bf16x8 *>(sq + q * 2048 + phys * 16);
 #pragma unroll
-          for (int v = 0; v < 16; ++v) I[nt][v] = fmaf(wa, fmaxf(acc[v], kLeaky * acc[v]), I[nt][v]);
+            for (int kt = 0; kt < kDsaKT; ++kt) acc[kt] = Mfma<bf16>::mma(af[i][kt][ks], qf, acc[kt]);
+          }
+          // w LeakyReLU(x) = w (1 + slope)/2 x + w (1 - slope)/2 |x|: two FMAs, |x| a free operand modifier
+          const float wa = sw[q * kDsaH + a];
+          const float wp = wa * (0.5f * (1.0f + kLeaky)), wn = wa * (0.5f * (1.0f - kLeaky));
+#pragma unroll
+          for (int kt = 0; kt < kDsaKT; ++kt)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) I[nt][kt][v] = fmaf(wn, fabsf(acc[kt][v]), fmaf(wp, acc[kt][v], I[nt][kt][v]));
         }
-        // refill the slot: head a + RING of this block, or head i of the next block
-        if (a0 == 0) fetch(kbk, RING + i, af[i]);
-        else if (kbk + 1 < nkb) fetch(kbk + 1, i, af[i]);
+        // refill the slot: head a + RING of this block, or the next block's head a + RING - H
+        if (a + RING < kDsaH) fetch(kbk, a + RING, af[i]);
+        else if (kbk + 1 < nkb) fetch(kbk + 1, a + RING - kDsaH, af[i]);
       }
     }
-    // lane (h, col): keys kbk 128 + 32 wave + 8 g + 4 h + e, query column 32 nt + col
-    const int kbase = kbk * kDsaKB + wave * 32 + 4 * h;
+    // lane (h, col): keys kbk kDsaKB + 32 (kDsaKT wave + kt) + 8 g + 4 h + e, query column 32 nt + col
+    const int kbase = kbk * kDsaKB + wave * (32 * kDsaKT) + 4 * h;
+    auto key_of = [&](int kt, int v) { return kbase + 32 * kt + 8 * (v >> 2) + (v & 3); };
     if (PASS == 1) {
 #pragma unroll
       for (int nt = 0; nt < 2; ++nt) {
         float tm = -INFINITY;
 #pragma unroll
-        for (int v = 0; v < 16; ++v)
-          if (kbase + 8 * (v >> 2) + (v & 3) < T) tm = fmaxf(tm, I[nt][v]);
+        for (int kt = 0; kt < kDsaKT; ++kt)
+#pragma unroll
+          for (int v = 0; v < 16; ++v)
+            if (key_of(kt, v) < T) tm = fmaxf(tm, I[nt][kt][v]);
         const float nm = fmaxf(run_m[nt], tm);
         float ts = 0.0f;
 #pragma unroll
-        for (int v = 0; v < 16; ++v)
-          if (kbase + 8 * (v >> 2) + (v & 3) < T) ts += __expf(I[nt][v] - nm);
+        for (int kt = 0; kt < kDsaKT; ++kt)
+#pragma unroll
+          for (int v = 0; v < 16; ++v)
+            if (key_of(kt, v) < T) ts += __expf(I[nt][kt][v] - nm);
         run_s[nt] = (run_m[nt] == -INFINITY ? 0.0f : run_s[nt] * __expf(run_m[nt] - nm)) + ts;
         run_m[nt] = nm;
       }
     } else {
       // pi^2 summed over this workgroup's 64 queries, per key
-      float cs[16];
+      float *pp = part + ((size_t)p * gridDim.x + blockIdx.x) * T;
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        float x = 0.0f;
-#pragma unroll
-        for (int nt = 0; nt < 2; ++nt) x += __expf(2.0f * (I[nt][v] - zq[nt])) * im2[nt];
-        cs[v] = x;
-      }
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        float x = cs[v];
-#pragma unroll
-        for (int o = 1; o < 32; o <<= 1) x += __shfl_xor(x, o, 64);
-        cs[v] = x;
-      }
-      if (col == 0) {
-        float *pp = part + ((size_t)p * gridDim.x + blockIdx.x) * T;
+      for (int kt = 0; kt < kDsaKT; ++kt) {
+        float cs[16];
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
-          const int k = kbase + 8 * (v >> 2) + (v & 3);
-          if (k < T) pp[k] = cs[v];
+          float x = 0.0f;
+#pragma unroll
+          for (int nt = 0; nt < 2; ++nt) x += __expf(2.0f * (I[nt][kt][v] - zq[nt])) * im2[nt];
+          cs[v] = x;
+        }
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          float x = cs[v];
+#pragma unroll
+          for (int o = 1; o < 32; o <<= 1) x += __shfl_xor(x, o, 64);
+          cs[v] = x;
+        }
+        if (col == 0) {
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            const int k = key_of(kt, v);
+            if (k < T) pp[k] = cs[v];
+          }
         }
       }
     }
@@ -270,10 +298,10 @@ __global__ void __launch_bounds__(256) k_dsa_index(const bf16 *__restrict__ qbar
     if (tid < kDsaQB && q0 + tid < n) {
       float M = -INFINITY;
 #pragma unroll
-      for (int w = 0; w < 4; ++w) M = fmaxf(M, sred[(w * kDsaQB + tid) * 2]);
+      for (int w = 0; w < kDsaWaves; ++w) M = fmaxf(M, sred[(w * kDsaQB + tid) * 2]);
       float S = 0.0f;
 #pragma unroll
-      for (int w = 0; w < 4; ++w) {
+      for (int w = 0; w < kDsaWaves; ++w) {
         const float mw = sred[(w * kDsaQB + tid) * 2];
         if (mw != -INFINITY) S += sred[(w * kDsaQB + tid) * 2 + 1] * __expf(mw - M);
       }
@@ -319,7 +347,9 @@ hipError_t launch_dsa_w(const void *X, const void *Lx, const float *bx, int B, i
   return hipGetLastError();
 }
 
-size_t dsa_index_lds() { return (size_t)kDsaQB * 2048 + (size_t)kDsaQB * kDsaH * 4 + 4 * kDsaQB * 2 * 4; }
+size_t dsa_index_lds() {
+  return (size_t)kDsaQB * 2048 + (size_t)kDsaQB * kDsaH * 4 + (size_t)kDsaWaves * kDsaQB * 2 * 4;
+}
 int dsa_query_blocks(int n) { return (n + kDsaQB - 1) / kDsaQB; }
 
 hipError_t launch_dsa_index(int pass, const void *qbar, const void *kbar, const float *w, int B, int n, int n_pos,
@@ -332,10 +362,10 @@ hipError_t launch_dsa_index(int pass, const void *qbar, const void *kbar, const 
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
   if (pass == 1)
-    hipLaunchKernelGGL(k1, grid, dim3(256), lds, s, (const bf16 *)qbar, (const bf16 *)kbar, w, n, n_pos, T, z, m,
+    hipLaunchKernelGGL(k1, grid, dim3(64 * kDsaWaves), lds, s, (const bf16 *)qbar, (const bf16 *)kbar, w, n, n_pos, T, z, m,
                        part);
   else
-    hipLaunchKernelGGL(k2, grid, dim3(256), lds, s, (const bf16 *)qbar, (const bf16 *)kbar, w, n, n_pos, T, z, m,
+    hipLaunchKernelGGL(k2, grid, dim3(64 * kDsaWaves), lds, s, (const bf16 *)qbar, (const bf16 *)kbar, w, n, n_pos, T, z, m,
                        part);
   return hipGetLastError();
 }
