@@ -9,8 +9,8 @@
 //
 // HBM-bound: every key and value row is read once.  Split-key ("flash
 // decoding") in two kernels:
-//   k_attend_partial  a workgroup of 4 waves takes 256 consecutive keys of
-//                     the concatenated block; each wave scores its 64 keys
+//   k_attend_partial  a workgroup of 4 waves takes 128 consecutive keys of
+//                     the concatenated block; each wave scores its 32 keys
 //                     against the G queries on MFMA 16x16x32 (keys as rows,
 //                     queries as zero-padded columns), takes the softmax of
 //                     its chunk, and accumulates P V on the VALU (each lane
@@ -25,7 +25,8 @@
 namespace arckv {
 
 namespace {
-constexpr int kAttChunk = 256;   // keys per workgroup (64 per wave)
+constexpr int kAttKPW = 32;                 // keys per wave
+constexpr int kAttChunk = 4 * kAttKPW;      // keys per workgroup
 
 typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4_t;
 
@@ -49,29 +50,30 @@ __global__ void __launch_bounds__(256) k_attend_partial(int t, int F, float scal
                                                          const bf16 *__restrict__ Vf, float *__restrict__ part_o,
                                                          float *__restrict__ part_ml, int nch) {
   static_assert(G >= 1 && G <= 8, "query rows per pair");
-  __shared__ float sP[4][64][G];                 // probabilities of each wave's 64 keys
+  __shared__ float sP[4][kAttKPW][G];            // probabilities of each wave's keys
   __shared__ float sO[4][G][kHeadDim];           // per-wave partial outputs
   __shared__ float sM[4][G], sL[4][G];
   const int p = blockIdx.y, ch = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int L = t + F;
-  const int key0 = ch * kAttChunk + wave * 64;
+  const int key0 = ch * kAttChunk + wave * kAttKPW;
   const int g = lane >> 4, r = lane & 15;        // MFMA lane coordinates
 
   // ---- issue every load of the chunk: K as MFMA A fragments (key rows), V rows
   // for the PV pass (lane = key group g (keys key0 + 4 i + g) x dims 8 r .. 8 r + 7)
   const bf16x8 zero8 = Mfma<bf16>::zero();
-  bf16x8 kf[4][4];
+  constexpr int KT = kAttKPW / 16, VI = kAttKPW / 4;
+  bf16x8 kf[KT][4];
 #pragma unroll
-  for (int kt = 0; kt < 4; ++kt) {
+  for (int kt = 0; kt < KT; ++kt) {
     const bf16 *row = att_row(Ck, Kf, p, t, F, key0 + 16 * kt + r);
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks)
       kf[kt][ks] = row ? *reinterpret_cast<const bf16x8 *>(row + 32 * ks + 8 * g) : zero8;
   }
-  bf16x8 vf[16];
+  bf16x8 vf[VI];
 #pragma unroll
-  for (int i = 0; i < 16; ++i) {
+  for (int i = 0; i < VI; ++i) {
     const bf16 *row = att_row(Cv, Vf, p, t, F, key0 + 4 * i + g);
     vf[i] = row ? *reinterpret_cast<const bf16x8 *>(row + 8 * r) : zero8;
   }
@@ -82,9 +84,9 @@ __global__ void __launch_bounds__(256) k_attend_partial(int t, int F, float scal
     qf[ks] = r < G ? *reinterpret_cast<const bf16x8 *>(Q + ((size_t)p * G + r) * kHeadDim + 32 * ks + 8 * g) : zero8;
 
   // ---- logits: lane (g, r) holds keys key0 + 16 kt + 4 g + j (j < 4) for query r
-  float sv[16];
+  float sv[VI];
 #pragma unroll
-  for (int kt = 0; kt < 4; ++kt) {
+  for (int kt = 0; kt < KT; ++kt) {
     f32x4_t acc = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) acc = mfma16(kf[kt][ks], qf[ks], acc);
@@ -96,16 +98,16 @@ __global__ void __launch_bounds__(256) k_attend_partial(int t, int F, float scal
       sv[4 * kt + j] = key < L ? fmaf(scale, acc[j], b) : -INFINITY;
     }
   }
-  // ---- softmax of the wave's 64 keys per query (reduce the lane's 16, then over g)
+  // ---- softmax of the wave's keys per query (reduce the lane's VI, then over g)
   float m = sv[0];
 #pragma unroll
-  for (int i = 1; i < 16; ++i) m = fmaxf(m, sv[i]);
+  for (int i = 1; i < VI; ++i) m = fmaxf(m, sv[i]);
   m = fmaxf(m, __shfl_xor(m, 16, 64));
   m = fmaxf(m, __shfl_xor(m, 32, 64));
   const float mref = m == -INFINITY ? 0.0f : m;   // a wave past the end keeps zero mass
   float l = 0.0f;
 #pragma unroll
-  for (int i = 0; i < 16; ++i) {
+  for (int i = 0; i < VI; ++i) {
     sv[i] = __expf(sv[i] - mref);
     l += sv[i];
   }
@@ -113,7 +115,7 @@ __global__ void __launch_bounds__(256) k_attend_partial(int t, int F, float scal
   l += __shfl_xor(l, 32, 64);
   if (r < G) {
 #pragma unroll
-    for (int kt = 0; kt < 4; ++kt)
+    for (int kt = 0; kt < KT; ++kt)
 #pragma unroll
       for (int j = 0; j < 4; ++j) sP[wave][16 * kt + 4 * g + j][r] = sv[4 * kt + j];
     if (g == 0) {
@@ -129,7 +131,7 @@ __global__ void __launch_bounds__(256) k_attend_partial(int t, int F, float scal
 #pragma unroll
     for (int e = 0; e < 8; ++e) o[q][e] = 0.0f;
 #pragma unroll
-  for (int i = 0; i < 16; ++i) {
+  for (int i = 0; i < VI; ++i) {
     float pq[G];
 #pragma unroll
     for (int q = 0; q < G; ++q) pq[q] = sP[wave][4 * i + g][q];
