@@ -216,3 +216,22 @@ def test_nnls_kkt_at_full_shape():
         log(f"  pair {b}: t={t}, free {n_free}, KKT on {on:.2e} off {off:.2e}")
         assert 0 < n_free < t
         assert on <= KKT_TOL["bf16"] and off <= KKT_TOL["bf16"], (b, on, off)
+
+
+def test_nnls_chunk_invariant(case):
+    """The exact fit in pair chunks of one (each chunk sizes its own compressed
+    system) gives the same compaction as all pairs together."""
+    wl, dev, host, s, t, ref = case
+    if wl.pairs < 2:
+        pytest.skip("needs two pairs")
+    args = (dev["K"], dev["V"], dev["Q"], dev["W1"], dev["b1"], dev["w2"], dev["b2"], wl.rho)
+    out_all = A().compact(*args, scale=s, params=A().default_params(bias_mode=1))
+    out_one = A().compact(*args, scale=s, params=A().default_params(bias_mode=1, pair_chunk=1))
+    names = ("anchors", "C_k", "beta", "C_v", "info")
+    for name, a, b in zip(names, out_all, out_one):
+        a, b = a.cpu().numpy(), b.cpu().numpy()
+        if name in ("anchors", "info"):
+            np.testing.assert_array_equal(a, b, err_msg=name)
+        else:
+            np.testing.assert_allclose(a, b, rtol=0, atol=1e-6 * max(1.0, float(np.abs(a).max())), err_msg=name)
+    log(f"  {wl.name}: chunked and unchunked exact fits agree")
