@@ -143,6 +143,50 @@ def measured_traffic(which, wl):
     return rec.get("traffic_bytes_per_launch")
 
 
+def stage_rooflines(wl, t, stages, steps, refine_steps=2):
+    """Per-stage roofline: the algorithmic work of each stage for all pairs (flops of the contractions at the
+    arithmetic's own peak, or HBM bytes), divided by the stage's event-timed duration per step.  Contractions on
+    split bf16 operands (the Grams, the value right-hand side) count their algorithmic flops once against the
+    bf16 peak although they issue 2-3 products; the float32-accurate Cholesky and triangular solves are priced
+    at the fp32 peak."""
+    B, T, n, d = wl.pairs, wl.T, wl.n, wl.d
+    esz = 2 if wl.dtype == "bf16" else 4
+    r = refine_steps
+    work = {   # stage: (unit, amount for all pairs, peak)
+        "rowstats": ("flop", 4.0 * n * T * d * B, PEAK_BF16_TFLOPS),
+        "profiles": ("byte", (T * n * 2 + T * d * esz + n * d * esz + 4 * T) * B, PEAK_HBM_GBS),
+        "anchor_profiles": ("byte", 2.0 * t * n * 2 * B, PEAK_HBM_GBS),
+        "assign_gemm": ("flop", assign_flops(wl, t), PEAK_BF16_TFLOPS),
+        "merge": ("byte", (T * d * esz + 8 * T + 2 * t * d * 4) * B, PEAK_HBM_GBS),
+        "phic": ("byte", (8.0 * t * n + n * d * esz + 4 * n) * B, PEAK_HBM_GBS),
+        "gram_G": ("flop", 1.0 * n * t * (t + 1) * B, PEAK_BF16_TFLOPS),
+        "chol_G": ("flop", t ** 3 / 3.0 * B, PEAK_FP32_TFLOPS),
+        # one solve and r refinements: L read twice per solve, L^T twice per residual
+        "solve_beta": ("byte", ((r + 1) * 2 * 4.0 * t * t / 2 + r * 2 * 4.0 * t * n) * B, PEAK_HBM_GBS),
+        "phat": ("byte", (2 * 4.0 * t * n + 4 * 2.0 * t * n) * B, PEAK_HBM_GBS),
+        "gram_A": ("flop", 1.0 * n * t * (t + 1) * B, PEAK_BF16_TFLOPS),
+        "rhs_B": ("flop", 2.0 * n * t * d * B, PEAK_BF16_TFLOPS),
+        "chol_A": ("flop", t ** 3 / 3.0 * B, PEAK_FP32_TFLOPS),
+        # (r + 1) solves of two triangular sweeps with d right-hand sides, r residuals of two contractions
+        "solve_values": ("flop", ((r + 1) * 2 * t * t * d + r * 2 * 2.0 * n * t * d) * B, PEAK_FP32_TFLOPS),
+    }
+    out = {}
+    for name, (unit, amount, peak) in work.items():
+        ms, cnt = stages.get(name, (0.0, 0))
+        if not cnt:
+            continue
+        sec = ms / 1e3 / steps
+        if unit == "flop":
+            ach = amount / sec / 1e12
+            out[name] = {"bound": "mfma", "ms": round(ms / steps, 3), "algorithmic_tflop": round(amount / 1e12, 3),
+                         "achieved": round(ach, 1), "peak": peak, "unit": "TFLOP/s", "frac": round(ach / peak, 4)}
+        else:
+            ach = amount / sec / 1e9
+            out[name] = {"bound": "hbm", "ms": round(ms / steps, 3), "algorithmic_gb": round(amount / 1e9, 3),
+                         "achieved": round(ach, 1), "peak": peak, "unit": "GB/s", "frac": round(ach / peak, 4)}
+    return out
+
+
 def score_select_bytes(wl, t):
     """Algorithmic HBM bytes of scoring + selection for all pairs: read K and V, write the scores, read them
     back, write the anchors."""
@@ -393,6 +437,7 @@ def main():
         "roofline_score_select": roofline_ss,
         "cpu_baseline": cpu,
         "stage_ms_per_step": {k: round(v[0] / args.steps, 3) for k, v in stages.items() if v[1]},
+        "stage_roofline": stage_rooflines(wl, t, stages, args.steps, params.refine_steps),
     }
     print(json.dumps(out), flush=True)
 
