@@ -21,6 +21,8 @@
  *  - All array arguments are DEVICE pointers owned by the caller, row-major and
  *    contiguous: K, V [B][T][d]; Q_ref [B][n][d] (each pair's n rows ordered
  *    [query head][position]); per-pair vectors [B][len].  Inputs are read-only.
+ *    K, V, Q_ref, Y, W1 and C_k move in 16-byte vectors and must be 16-byte
+ *    aligned (ARCKV_ERR_INVALID_ARG otherwise).
  *  - K, V and Q_ref share one element type (arckv_problem.dtype): float32 or
  *    bfloat16.  Only d = 128 is supported.  Outputs are float32 (indices int32).
  *  - The library never allocates device memory.  Entry points that need scratch

@@ -617,7 +617,7 @@ arckv_status arckv_merge(const arckv_problem *prob, const void *K, const void *Q
   CHECK(check_problem(prob));
   if (!K || !Q_ref || !z || !anchors || !C_k || t < 1 || t > prob->T) return ARCKV_ERR_INVALID_ARG;
   if (!(lambda_m >= 0.0f && lambda_m <= 1.0f)) return ARCKV_ERR_INVALID_ARG;
-  if (!aligned(K, 16) || !aligned(Q_ref, 16)) return ARCKV_ERR_INVALID_ARG;
+  if (!aligned(K, 16) || !aligned(Q_ref, 16) || !aligned(C_k, 16)) return ARCKV_ERR_INVALID_ARG;
   Ctx c;
   c.d = make_dims(prob, t);
   int64_t P = 0;
@@ -729,7 +729,7 @@ static arckv_status compact_impl(const arckv_problem *prob, const void *K, const
     if (ix->hidden != 64 || ix->w1_dtype != prob->dtype) return ARCKV_ERR_UNSUPPORTED;
     if (!aligned(ix->W1, 16)) return ARCKV_ERR_INVALID_ARG;
   }
-  if (!aligned(K, 16) || !aligned(V, 16) || !aligned(Q_ref, 16)) return ARCKV_ERR_INVALID_ARG;
+  if (!aligned(K, 16) || !aligned(V, 16) || !aligned(Q_ref, 16) || !aligned(C_k, 16)) return ARCKV_ERR_INVALID_ARG;
   int32_t t = 0;
   CHECK(arckv_budget(prob->T, rho, &t));
   const int32_t t_nominal = t;

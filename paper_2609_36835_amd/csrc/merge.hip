@@ -138,42 +138,84 @@ __global__ void __launch_bounds__(256) k_group_merge(const E *__restrict__ K, co
                                                      const int32_t *__restrict__ anchors, int T, int t,
                                                      int64_t tp, float lambda, float *__restrict__ Ck,
                                                      void *__restrict__ Ckp) {
+  // One wave per group r.  The group mass is a wave reduction over its members;
+  // the weighted sum takes four members at a time, lane (kq, dl) = (lane / 16,
+  // lane % 16) owning member beg + kq + 4 i and dims 8 dl .. 8 dl + 7 (16-byte
+  // rows for bf16), and the four partial sums meet in two shuffles.  Every sum
+  // runs in a fixed order, so results are deterministic.
   const int b = blockIdx.y, lane = threadIdx.x & 63;
   const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (r >= tp) return;
-  const int d0 = 2 * lane;
-  float c0 = 0.0f, c1 = 0.0f;
+  const int kq = lane >> 4, d0 = 8 * (lane & 15);
+  float c[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) c[e] = 0.0f;
   if (r < t) {
     const int32_t beg = offsets[(size_t)b * (t + 1) + r], end = offsets[(size_t)b * (t + 1) + r + 1];
     const int32_t *pm = perm + (size_t)b * T;
     const float *ph = phi + (size_t)b * T;
     const int32_t s = anchors[(size_t)b * t + r];
     float mass = 0.0f;
-    for (int32_t q = beg; q < end; ++q) mass += ph[pm[q]];
-    const E *Kb = K + (size_t)b * T * kHeadDim;
-    float wsum = 0.0f, a0 = 0.0f, a1 = 0.0f;
-    for (int32_t q = beg; q < end; ++q) {
+    for (int32_t q = beg + lane; q < end; q += 64) mass += ph[pm[q]];
+    mass = wave_sum(mass);
+    const E *Kb = K + (size_t)b * T * kHeadDim + d0;
+    float wsum = 0.0f, acc[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[e] = 0.0f;
+    for (int32_t q = beg + kq; q < end; q += 4) {
       const int32_t j = pm[q];
       float alpha = (mass > 0.0f) ? lambda * (ph[j] / mass) : 0.0f;
       if (j == s) alpha += (mass > 0.0f) ? (1.0f - lambda) : 1.0f;
       wsum += alpha;
-      a0 = fmaf(alpha, to_f(Kb[(size_t)j * kHeadDim + d0]), a0);
-      a1 = fmaf(alpha, to_f(Kb[(size_t)j * kHeadDim + d0 + 1]), a1);
+      const E *kr = Kb + (size_t)j * kHeadDim;
+      float kv[8];
+      if constexpr (sizeof(E) == 2) {
+        const bf16x8 v = *reinterpret_cast<const bf16x8 *>(kr);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) kv[e] = (float)v[e];
+      } else {
+        const f32x4 v0 = *reinterpret_cast<const f32x4 *>(kr), v1 = *reinterpret_cast<const f32x4 *>(kr + 4);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          kv[e] = v0[e];
+          kv[4 + e] = v1[e];
+        }
+      }
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[e] = fmaf(alpha, kv[e], acc[e]);
     }
-    c0 = a0 / wsum;
-    c1 = a1 / wsum;
-    Ck[((size_t)b * t + r) * kHeadDim + d0] = c0;
-    Ck[((size_t)b * t + r) * kHeadDim + d0 + 1] = c1;
+    wsum += __shfl_xor(wsum, 16, 64);
+    wsum += __shfl_xor(wsum, 32, 64);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      acc[e] += __shfl_xor(acc[e], 16, 64);
+      acc[e] += __shfl_xor(acc[e], 32, 64);
+      c[e] = acc[e] / wsum;
+    }
+    if (kq == 0) {
+      float *o = Ck + ((size_t)b * t + r) * kHeadDim + d0;
+      *reinterpret_cast<f32x4 *>(o) = f32x4{c[0], c[1], c[2], c[3]};
+      *reinterpret_cast<f32x4 *>(o + 4) = f32x4{c[4], c[5], c[6], c[7]};
+    }
   }
+  if (kq != 0) return;
   if constexpr (sizeof(E) == 2) {
-    bf16 *hi = reinterpret_cast<bf16 *>(Ckp) + ((size_t)b * 2 * tp + r) * kHeadDim;
+    bf16 *hi = reinterpret_cast<bf16 *>(Ckp) + ((size_t)b * 2 * tp + r) * kHeadDim + d0;
     bf16 *lo = hi + tp * kHeadDim;
-    split_bf16(c0, hi[d0], lo[d0]);
-    split_bf16(c1, hi[d0 + 1], lo[d0 + 1]);
+    bf16x8 vh, vl;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      bf16 h, l;
+      split_bf16(c[e], h, l);
+      vh[e] = h;
+      vl[e] = l;
+    }
+    *reinterpret_cast<bf16x8 *>(hi) = vh;
+    *reinterpret_cast<bf16x8 *>(lo) = vl;
   } else {
-    float *o = reinterpret_cast<float *>(Ckp) + ((size_t)b * tp + r) * kHeadDim;
-    o[d0] = c0;
-    o[d0 + 1] = c1;
+    float *o = reinterpret_cast<float *>(Ckp) + ((size_t)b * tp + r) * kHeadDim + d0;
+    *reinterpret_cast<f32x4 *>(o) = f32x4{c[0], c[1], c[2], c[3]};
+    *reinterpret_cast<f32x4 *>(o + 4) = f32x4{c[4], c[5], c[6], c[7]};
   }
 }
 

@@ -131,6 +131,8 @@ def test_entry_points_reject_bad_arguments_without_gpu():
         (L.arckv_merge(r(prob), fake, fake, fake, fake, 10, 0.25, fake, None, None, ctypes.c_void_p(0x10000), 16,
                        None), A.ERR_WORKSPACE),              # workspace too small
         (L.arckv_merge(r(prob), fake, fake, fake, fake, 10, 1.5, fake, None, None, fake, 0, None), A.ERR_INVALID_ARG),
+        (L.arckv_merge(r(prob), fake, fake, fake, fake, 10, 0.25, odd, None, None, fake, 1 << 40, None),
+         A.ERR_INVALID_ARG),                                 # misaligned C_k
         (L.arckv_fit_bias(r(prob), fake, fake, 10, fake, fake, r(A.default_params(bias_mode=2)), fake, fake, None,
                           fake, 0, None), A.ERR_UNSUPPORTED),
         (L.arckv_fit_values(r(prob), fake, fake, fake, 10, None, r(par), fake, fake, None, fake, 0, None),
@@ -139,6 +141,8 @@ def test_entry_points_reject_bad_arguments_without_gpu():
                          fake, ctypes.c_void_p(0x10000), 1 << 40, None), A.ERR_INVALID_ARG),
         (L.arckv_compact(r(prob), fake, fake, fake, r(ix), 0.1, r(par), r(t_out), fake, fake, fake, fake, fake,
                          ctypes.c_void_p(0x10000), 1024, None), A.ERR_WORKSPACE),
+        (L.arckv_compact(r(prob), fake, fake, fake, r(ix), 0.1, r(par), r(t_out), fake, odd, fake, fake, fake,
+                         ctypes.c_void_p(0x10000), 1 << 40, None), A.ERR_INVALID_ARG),   # misaligned C_k
     ]
     for i, (got, want) in enumerate(cases):
         assert got == want, (i, got, want)
