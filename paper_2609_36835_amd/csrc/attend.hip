@@ -9,13 +9,13 @@
 //
 // HBM-bound: every key and value row is read once.  Split-key ("flash
 // decoding") in two kernels:
-//   k_attend_partial  a workgroup of 4 waves takes 128 consecutive keys of
+//   k_attend_partial  a workgroup of 8 waves takes 256 consecutive keys of
 //                     the concatenated block; each wave scores its 32 keys
 //                     against the G queries on MFMA 16x16x32 (keys as rows,
 //                     queries as zero-padded columns), takes the softmax of
 //                     its chunk, and accumulates P V on the VALU (each lane
 //                     owns 8 dims of 4 interleaved keys, probabilities
-//                     broadcast from LDS).  The four waves' (max, sum, o) are
+//                     broadcast from LDS).  The eight waves' (max, sum, o) are
 //                     merged in LDS into one partial per workgroup.  All of
 //                     the chunk's K and V loads are issued up front.
 //   k_attend_combine  merges the partials of a pair with the usual
@@ -26,7 +26,8 @@ namespace arckv {
 
 namespace {
 constexpr int kAttKPW = 32;                 // keys per wave
-constexpr int kAttChunk = 4 * kAttKPW;      // keys per workgroup
+constexpr int kAttW = 8;                    // waves per workgroup
+constexpr int kAttChunk = kAttW * kAttKPW;  // keys per workgroup
 
 typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4_t;
 
@@ -44,15 +45,15 @@ __device__ inline const bf16 *att_row(const bf16 *C, const bf16 *Fx, int p, int 
 }  // namespace
 
 template <int G>
-__global__ void __launch_bounds__(256) k_attend_partial(int t, int F, float scale, const bf16 *__restrict__ Q,
+__global__ void __launch_bounds__(64 * kAttW) k_attend_partial(int t, int F, float scale, const bf16 *__restrict__ Q,
                                                          const bf16 *__restrict__ Ck, const float *__restrict__ beta,
                                                          const bf16 *__restrict__ Cv, const bf16 *__restrict__ Kf,
                                                          const bf16 *__restrict__ Vf, float *__restrict__ part_o,
                                                          float *__restrict__ part_ml, int nch) {
   static_assert(G >= 1 && G <= 8, "query rows per pair");
-  __shared__ float sP[4][kAttKPW][G];            // probabilities of each wave's keys
-  __shared__ float sO[4][G][kHeadDim];           // per-wave partial outputs
-  __shared__ float sM[4][G], sL[4][G];
+  __shared__ float sP[kAttW][kAttKPW][G];       // probabilities of each wave's keys
+  __shared__ float sO[kAttW][G][kHeadDim];      // per-wave partial outputs
+  __shared__ float sM[kAttW][G], sL[kAttW][G];
   const int p = blockIdx.y, ch = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int L = t + F;
@@ -158,18 +159,18 @@ __global__ void __launch_bounds__(256) k_attend_partial(int t, int F, float scal
       for (int e = 0; e < 8; ++e) sO[wave][q][8 * r + e] = o[q][e];
   }
   __syncthreads();
-  // ---- merge the four waves: one partial (max, sum, o) per query for the chunk
+  // ---- merge the waves: one partial (max, sum, o) per query for the chunk
   float *po = part_o + (((size_t)p * nch + ch) * G) * kHeadDim;
   float *pml = part_ml + (((size_t)p * nch + ch) * G) * 2;
-  for (int idx = tid; idx < G * kHeadDim; idx += 256) {
+  for (int idx = tid; idx < G * kHeadDim; idx += 64 * kAttW) {
     const int q = idx / kHeadDim, dim = idx % kHeadDim;
     float M = sM[0][q];
 #pragma unroll
-    for (int w = 1; w < 4; ++w) M = fmaxf(M, sM[w][q]);
+    for (int w = 1; w < kAttW; ++w) M = fmaxf(M, sM[w][q]);
     const float Mref = M == -INFINITY ? 0.0f : M;
     float acc = 0.0f, lsum = 0.0f;
 #pragma unroll
-    for (int w = 0; w < 4; ++w) {
+    for (int w = 0; w < kAttW; ++w) {
       const float f = sM[w][q] == -INFINITY ? 0.0f : __expf(sM[w][q] - Mref);
       acc = fmaf(f, sO[w][q][dim], acc);
       lsum = fmaf(f, sL[w][q], lsum);
@@ -212,7 +213,7 @@ hipError_t launch_attend(int P, int G, int t, int F, float scale, const void *Q,
   const int nch = attend_chunks(t, F);
   dim3 grid((unsigned)nch, (unsigned)P);
   auto go = [&](auto kern) {
-    hipLaunchKernelGGL(kern, grid, dim3(256), 0, s, t, F, scale, (const bf16 *)Q, (const bf16 *)Ck, beta,
+    hipLaunchKernelGGL(kern, grid, dim3(64 * kAttW), 0, s, t, F, scale, (const bf16 *)Q, (const bf16 *)Ck, beta,
                        (const bf16 *)Cv, (const bf16 *)Kf, (const bf16 *)Vf, part_o, part_ml, nch);
   };
   switch (G) {
