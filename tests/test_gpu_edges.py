@@ -1,4 +1,4 @@
-"""GPU edge cases: full retention, a single anchor, tiny caches, ridge-free fits."""
+"""GPU edge cases: full retention, a single anchor, tiny caches, ridge-free fits, the exact fit where it cannot bind."""
 import math
 
 import numpy as np
@@ -100,3 +100,24 @@ def test_escalated_value_fit_matches_oracle_at_used_ridge():
                                  oracle.attend_compact(Q, Ck[b], beta[b], vf.C_v, s)).max()
         print(f"  pair {b}: ridge escalated to {dused[b]:.1e}; output max row rel err {err:.3e}", flush=True)
         assert err <= 1e-3, (b, err)
+
+
+def test_exact_fit_degenerate_cases():
+    """The exact non-negative fit where the constraints cannot bind: full
+    retention (C_k = K, so w = 1 fits the mass exactly: beta = 0) and a single
+    anchor (a scalar least-squares weight, positive): both must agree with the
+    projected fit."""
+    wl = synth.custom("full1", kv_heads=2, T=48, q_heads_per_kv=2, n_pos=64, dtype="f32", rope=True)
+    dev, host, s, (anchors, Ck, beta, Cv, info) = run(wl, 1.0, delta_beta=0.0, delta_v=0.0, bias_mode=1)
+    assert np.all(info.numpy() == 0), info
+    assert np.abs(np64(beta)).max() < 1e-3, np.abs(np64(beta)).max()
+    for b in range(wl.pairs):
+        K, V = host["K"][b], host["V"][b]
+        Qh = synth.heldout_queries(wl, 0, b).astype(np.float64)
+        Oc = oracle.attend_compact(Qh, np64(Ck[b]), np64(beta[b]), np64(Cv[b]), s)
+        assert oracle.row_rel_err(Oc, oracle.attend_full(Qh, K, V, s)).max() < 1e-3
+    wl = synth.custom("t1e", kv_heads=1, T=300, q_heads_per_kv=1, n_pos=64, dtype="f32", rope=False)
+    _, _, _, out0 = run(wl, 0.001)
+    _, _, _, out1 = run(wl, 0.001, bias_mode=1)
+    assert np.all(out1[4].numpy() == 0)
+    np.testing.assert_allclose(np64(out1[2]), np64(out0[2]), rtol=0, atol=1e-5)
