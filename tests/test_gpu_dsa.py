@@ -114,3 +114,48 @@ def test_compact_on_dsa_scores():
                                  oracle.attend_compact(Q[b], rr.C_k, rr.beta, rr.C_v, s))
         print(f"  pair {b}: O(Q_ref) max row rel err {err.max():.3e}", flush=True)
         assert err.max() <= TOL_OUT["bf16"], (b, err.max())
+
+
+def test_dsa_full_shape_sampled_pair():
+    """The 32K-context workload in the benchmark's launch configuration (256
+    pairs, T = 32768, n = 4096, d_x = 4096, random weights with the value path
+    active): one sampled pair's pooled scores against the float64 oracle."""
+    import os
+    import sys
+    sys.path.insert(0, os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
+    import bench
+    import synth
+    wl = synth.WORKLOADS["llama8b_bf16_T32768"]
+    dev = torch.device("cuda:0")
+    K, V, Q, _, _, _, _ = bench.load_inputs(wl, dev)
+    B, T, n, d = wl.pairs, wl.T, wl.n, wl.d
+    dx, n_pos = 4096, wl.n_pos
+    g = torch.Generator(device=dev)
+    g.manual_seed(5)
+    r = lambda *sh, std: (torch.randn(*sh, device=dev, generator=g) * std).to(torch.bfloat16)
+    P = {"L_q": r(B, 1024, d, std=d ** -0.5), "L_k": r(B, 1024, d, std=d ** -0.5), "L_x": r(B, 8, dx, std=dx ** -0.5),
+         "b_x": torch.zeros(B, 8, device=dev), "U_q": r(B, 128, d, std=d ** -0.5), "U_k": r(B, 128, d, std=d ** -0.5),
+         "U_v": r(B, 128, d, std=d ** -0.5), "L_c": r(B, 1024, 128, std=128 ** -0.5),
+         "L_v": r(B, 1024, d, std=d ** -0.5)}
+    X = r(wl.layers, n_pos, dx, std=1.0)
+    s_gpu = A().score_dsa(K, V, Q, X, P, n_pos, x_group=wl.kv_heads)
+    torch.cuda.synchronize()
+    b = 137
+    print(f"dsa full shape: B={B} T={T} n={n}; oracle on pair {b}", flush=True)
+    host = lambda x: x.float().cpu().numpy().astype(np.float64)
+    ix = oracle.DSAIndexer(**{k: host(v[b]) for k, v in P.items()})
+    I = oracle.dsa_logits(host(Q[b]), host(X[b // wl.kv_heads]), host(K[b]), host(V[b]), ix, n_pos,
+                          1.0 / math.sqrt(128), rnd=lambda a: oracle.round_to(a, "bf16"))
+    s_ref = oracle.pool_rms(I)
+    del I
+    sg = np64(s_gpu[b])
+    rel = np.abs(sg - s_ref) / s_ref.max()
+    print(f"    pair {b}: max |ds| / max s = {rel.max():.2e}", flush=True)
+    assert rel.max() <= S_TOL_VALUE, rel.max()
+    t = oracle.budget(T, wl.rho)
+    S_gpu = set(oracle.select_topt(sg, t).tolist())
+    S_ref = set(oracle.select_topt(s_ref, t).tolist())
+    boundary = np.sort(s_ref)[::-1][t - 1]
+    for j in S_gpu ^ S_ref:
+        assert abs(s_ref[j] - boundary) <= 2 * S_TOL_VALUE * s_ref.max(), j
+    print(f"    pair {b}: top-{t} differs at {len(S_gpu ^ S_ref) // 2} certified near-ties", flush=True)
