@@ -140,7 +140,7 @@ arckv_status arckv_score(const arckv_problem *prob, const void *K, const void *V
  * row-major, per pair (B pairs in a call):
  *   L_q, L_k, L_c, L_v [B][1024][128];  U_q, U_k, U_v [B][128][128];
  *   L_x [B][8][d_x];  b_x [B][8] float32;
- *   X_ref [B / x_group][n_pos][d_x]: the activation x_r of reference position r,
+ *   X_ref [ceil(B / x_group)][n_pos][d_x]: the activation x_r of reference position r,
  *   shared by the query heads of a position and by the x_group consecutive
  *   pairs of one layer (its KV heads).
  * Q_ref rows are ordered [query head][position], so row i uses x_{i mod n_pos}. */

@@ -684,7 +684,7 @@ arckv_status arckv_fit_values(const arckv_problem *prob, const void *Q_ref, cons
   arckv_default_params(&def);
   if (!p) p = &def;
   if (!Q_ref || !beta || !Y || !C_v || !info) return ARCKV_ERR_INVALID_ARG;
-  if (!aligned(Q_ref, 16)) return ARCKV_ERR_INVALID_ARG;
+  if (!aligned(Q_ref, 16) || !aligned(Y, 16)) return ARCKV_ERR_INVALID_ARG;
   Ctx c;
   int64_t P = 0;
   CHECK(fit_common(prob, C_k, t, p, ws, ws_bytes, stream, c, P));

@@ -137,6 +137,8 @@ def test_entry_points_reject_bad_arguments_without_gpu():
                           fake, 0, None), A.ERR_UNSUPPORTED),
         (L.arckv_fit_values(r(prob), fake, fake, fake, 10, None, r(par), fake, fake, None, fake, 0, None),
          A.ERR_INVALID_ARG),
+        (L.arckv_fit_values(r(prob), fake, fake, fake, 10, odd, r(par), fake, fake, None, ctypes.c_void_p(0x10000),
+                            1 << 40, None), A.ERR_INVALID_ARG),                                  # misaligned Y
         (L.arckv_compact(r(prob), fake, fake, fake, r(ix), float("nan"), r(par), r(t_out), fake, fake, fake, fake,
                          fake, ctypes.c_void_p(0x10000), 1 << 40, None), A.ERR_INVALID_ARG),
         (L.arckv_compact(r(prob), fake, fake, fake, r(ix), 0.1, r(par), r(t_out), fake, fake, fake, fake, fake,

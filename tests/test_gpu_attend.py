@@ -65,3 +65,34 @@ def test_attend_without_bias_is_full_attention():
 def test_attend_decode_shape_32k_at_20_percent():
     # one pair of the 32K-context decode workload: t = round(0.2 * 32768) = 6554 compact rows
     run_case(2, 4, 6554, 0, seed=11)
+
+
+@pytest.mark.parametrize("label", ["full", "compact"])
+def test_attend_bench_launch_sampled_pairs(label):
+    """The decode launch the benchmark times: batch 64 x 8 KV heads = 512 pairs, 4 query heads per KV head,
+    a 32K context either whole (L = 32768, no bias) or compacted at rho = 0.2 (t = 6554, bias in [-3, 3]).
+    Inputs drawn on the device as the benchmark draws them; sampled pairs (first, last, and six more spread
+    over the batch) are checked against the float64 oracle one by one."""
+    from paper_2609_36835_amd import arckv
+    P, G, d, T = 512, 4, 128, 32768
+    L = T if label == "full" else arckv.budget(T, 0.2)
+    dev = torch.device("cuda:0")
+    g = torch.Generator(device=dev)
+    g.manual_seed(7)
+    K = torch.randn(P, L, d, device=dev, dtype=torch.bfloat16, generator=g)
+    V = torch.randn(P, L, d, device=dev, dtype=torch.bfloat16, generator=g)
+    Q = torch.randn(P, G, d, device=dev, dtype=torch.bfloat16, generator=g)
+    beta = (torch.rand(P, L, device=dev, generator=g) * 6 - 3) if label == "compact" else None
+    print(f"attend bench launch {label}: P={P} G={G} L={L}", flush=True)
+    att = arckv.Attender(P, G, L, 0, dev)
+    out = att(Q, K, beta, V).cpu().numpy().astype(np.float64)
+    torch.cuda.synchronize()
+    s = 1.0 / math.sqrt(d)
+    worst = 0.0
+    for p in (0, 1, 97, 200, 255, 256, 421, P - 1):
+        h = lambda x: x[p].float().cpu().numpy().astype(np.float64)
+        ref = oracle.attend_joint(h(Q), h(K), None if beta is None else h(beta), h(V), None, None, s)
+        worst = max(worst, float(oracle.row_rel_err(out[p], ref).max()))
+    print(f"    max row rel err over sampled pairs {worst:.2e}", flush=True)
+    assert worst <= TOL, worst
+    assert np.isfinite(out).all()
