@@ -26,7 +26,8 @@ hipError_t launch_assign_gemm(int dtype, const void *U, const void *Et, uint64_t
   g.syrk = false;
   g.group_m = 8;
   if (dtype == ARCKV_BF16) {
-    BigShape g2{P, (int)tp, (int)N, (int)np_, tp * np_, 0, np_, Et_rows * np_, 0, np_, false, (int)(tp / 256)};
+    // tile order: groups of 7 anchor tiles walk the key tiles (about 7 x 4.5 tiles per XCD at a time)
+    BigShape g2{P, (int)tp, (int)N, (int)np_, tp * np_, 0, np_, Et_rows * np_, 0, np_, false, 7};
     EpiArgmaxBig<4, 2, 2, 4> e2{part, (tp / 256) * N, (int)N, t};
     return launch_gemm_big<4, 2, 2, 4, 64, 1, 1, 2>(g2, (const bf16 *)U, (const bf16 *)Et, e2, s);
   }
