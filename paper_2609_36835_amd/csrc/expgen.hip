@@ -15,6 +15,8 @@
 // A workgroup owns 128 output rows (keys or compact keys) whose fragments stay
 // in registers, and sweeps all query tiles through LDS.  Padding rows/columns
 // of the workspace are written as zeros.
+#include <type_traits>
+
 #include "common.hpp"
 
 namespace arckv {
@@ -332,6 +334,15 @@ __global__ void __launch_bounds__(256, 2) k_expgen_bf16(const bf16 *__restrict__
   const int ntile = n_pad / 64;
   // without z (logits only) the shift is zero; the stages stay zero-filled
   if (MODE == MODE_PHIC && !shift && tid < 128) sZ[tid] = 0.0f;
+  // profile: destination row of each of this lane's four store passes (row
+  // 8 pass + lane / 8 of the wave), fixed over the query sweep
+  bf16 *prow[4];
+  if constexpr (MODE == MODE_PROFILE) {
+#pragma unroll
+    for (int pass = 0; pass < 4; ++pass) prow[pass] = row_dst(8 * pass + lane / 8, 0);
+  }
+  // wave-uniform: this wave's 32 rows are all real keys
+  const bool rows_full = row0 + 32 <= b_rows;
   issue_q(0, 0);
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
@@ -339,6 +350,62 @@ __global__ void __launch_bounds__(256, 2) k_expgen_bf16(const bf16 *__restrict__
     const int i0 = it * 64, st = it & 1;
     if (it + 1 < ntile) issue_q(i0 + 64, st ^ 1);
     const char *sq = sQ + st * QB;
+    if constexpr (MODE == MODE_PROFILE) {
+      // E = 2^(acc c2 - zs2) by the hardware exponential (results below 2^-126
+      // flush to zero); masks only on ragged tiles; each pair of rows rounded
+      // to bf16 once, for both the stored profile and its sum of squares
+      uint32_t pk[2][8];
+      auto products = [&](auto full_c) {
+        constexpr bool FULL = decltype(full_c)::value;
+#pragma unroll
+        for (int ms = 0; ms < 2; ++ms) {
+          f32x16 acc = zero16();
+          const int r = 32 * ms + col;
+#pragma unroll
+          for (int ks = 0; ks < NKS; ++ks) {
+            const bf16x8 a = *reinterpret_cast<const bf16x8 *>(sq + r * 256 + 16 * ((2 * ks + h) ^ (r & 15)));
+            acc = Mfma<bf16>::mma(a, bf[0][ks], acc);
+          }
+#pragma unroll
+          for (int u = 0; u < 8; ++u) {
+            float e0 = __builtin_amdgcn_exp2f(fmaf(acc[2 * u], c2, -zs2));
+            float e1 = __builtin_amdgcn_exp2f(fmaf(acc[2 * u + 1], c2, -zs2));
+            if constexpr (!FULL) {
+              const int i = i0 + 32 * ms + acc_row(2 * u, lane);   // rows i and i + 1
+              e0 = rvalid && i < n ? e0 : 0.0f;
+              e1 = rvalid && i + 1 < n ? e1 : 0.0f;
+            }
+            rowsum += e0;
+            rowsum += e1;
+            const bf16x2 b2 = {(bf16)e0, (bf16)e1};
+            uint32_t w = __builtin_bit_cast(uint32_t, b2);
+            asm volatile("" : "+v"(w));   // unpack the rounded pair rather than round each value again
+            const float s0 = __uint_as_float(w << 16), s1 = __uint_as_float(w & 0xFFFF0000u);
+            sumsq = fmaf(s1, s1, fmaf(s0, s0, sumsq));
+            pk[ms][u] = w;
+          }
+        }
+      };
+      // wave-uniform: a whole tile of real keys and queries needs no masks
+      if (__builtin_amdgcn_readfirstlane((int)(rows_full && i0 + 64 <= n)))
+        products(std::true_type{});
+      else
+        products(std::false_type{});
+      bf16 *sb = reinterpret_cast<bf16 *>(so);
+      wave_fence();
+#pragma unroll
+      for (int ms = 0; ms < 2; ++ms)
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          *reinterpret_cast<uint32_t *>(&sb[col * SO_H + 32 * ms + acc_row(2 * u, lane)]) = pk[ms][u];
+      wave_fence();
+#pragma unroll
+      for (int pass = 0; pass < 4; ++pass) {             // 32 rows x 8 chunks of 16 B
+        const int chunk = pass * 64 + lane, r = chunk / 8, c8 = (chunk % 8) * 8;
+        *reinterpret_cast<bf16x8 *>(prow[pass] + i0 + c8) = *reinterpret_cast<const bf16x8 *>(&sb[r * SO_H + c8]);
+      }
+      wave_fence();
+    } else {
     float val[2][16], lg[2][16];
 #pragma unroll
     for (int ms = 0; ms < 2; ++ms) {
@@ -354,34 +421,24 @@ __global__ void __launch_bounds__(256, 2) k_expgen_bf16(const bf16 *__restrict__
       for (int vv = 0; vv < 16; ++vv) {
         const int i = i0 + 32 * ms + acc_row(vv, lane);
         const bool ok = rvalid && i < n;
-        if (MODE == MODE_PROFILE) {
-          val[ms][vv] = ok ? exp2f(acc[vv] * c2 - zs2) : 0.0f;
-          rowsum += val[ms][vv];
-          const float stored = (float)(bf16)val[ms][vv];
-          sumsq = fmaf(stored, stored, sumsq);
-        } else {
-          // evaluated on every lane (masked lanes see finite inputs), then
-          // selected, so the exponential stays free of branches
-          lg[ms][vv] = ok ? acc[vv] * scale : 0.0f;
-          const float e = expf(lg[ms][vv] - sZ[64 * st + 32 * ms + acc_row(vv, lane)]);
-          val[ms][vv] = ok ? e : 0.0f;
-        }
+        // evaluated on every lane (masked lanes see finite inputs), then
+        // selected, so the exponential stays free of branches
+        lg[ms][vv] = ok ? acc[vv] * scale : 0.0f;
+        const float e = expf(lg[ms][vv] - sZ[64 * st + 32 * ms + acc_row(vv, lane)]);
+        val[ms][vv] = ok ? e : 0.0f;
       }
     }
-    if (MODE == MODE_PHIC && hout) {   // masked entries of val are zero
+    if (hout) {   // masked entries of val are zero
 #pragma unroll
       for (int ms = 0; ms < 2; ++ms)
 #pragma unroll
         for (int vv = 0; vv < 16; ++vv)
           hsum += (double)val[ms][vv] * (double)sM[64 * st + 32 * ms + acc_row(vv, lane)];
     }
-    if constexpr (MODE == MODE_PROFILE) {
-      flush_bf16(val, 0, nullptr, true, i0);
-    } else {
-      bf16 *o = out + (size_t)b * out_pair_stride + (size_t)row0 * n_pad + i0;
-      flush_bf16(val, 1, o, false, i0);
-      flush_bf16(val, 2, o + out_plane_stride, false, i0);
-      flush_f32(lg, aux + (size_t)b * aux_pair_stride + (size_t)row0 * n_pad + i0);
+    bf16 *o = out + (size_t)b * out_pair_stride + (size_t)row0 * n_pad + i0;
+    flush_bf16(val, 1, o, false, i0);
+    flush_bf16(val, 2, o + out_plane_stride, false, i0);
+    flush_f32(lg, aux + (size_t)b * aux_pair_stride + (size_t)row0 * n_pad + i0);
     }
     // The next Q stage has landed: it was issued before this tile's stores (4
     // per lane in profile mode, 4 + 4 + 8 in phic mode, all unconditional) and

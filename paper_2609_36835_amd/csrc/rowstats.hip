@@ -302,17 +302,20 @@ __global__ void __launch_bounds__(512, 1) k_rowstats_bf16(const bf16 *__restrict
       uint32_t pk[4];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const bf16 x0 = (bf16)accS[ms][base + 2 * e], x1 = (bf16)accS[ms][base + 2 * e + 1];
-        pk[e] = (uint32_t)__builtin_bit_cast(uint16_t, x0) | ((uint32_t)__builtin_bit_cast(uint16_t, x1) << 16);
+        const bf16x2 x = {(bf16)accS[ms][base + 2 * e], (bf16)accS[ms][base + 2 * e + 1]};
+        pk[e] = __builtin_bit_cast(uint32_t, x);
       }
-      // pk[0..1]: own keys 4h + 0..3, pk[2..3]: own keys 8 + 4h + 0..3 (of this 16-key step)
-      const uint32_t s0 = h == 0 ? pk[2] : pk[0], s1 = h == 0 ? pk[3] : pk[1];
-      const uint32_t r0 = (uint32_t)__shfl_xor((int)s0, 32, 64), r1 = (uint32_t)__shfl_xor((int)s1, 32, 64);
+      // pk[0..1]: own keys 4h + 0..3, pk[2..3]: own keys 8 + 4h + 0..3 (of this
+      // 16-key step).  The half-wave swap exchanges the upper half-wave's
+      // pk[0..1] with the lower half-wave's pk[2..3], so that every lane then
+      // holds keys 8h + 0..7 of its query in order.
+      const auto x02 = __builtin_amdgcn_permlane32_swap(pk[0], pk[2], false, false);
+      const auto x13 = __builtin_amdgcn_permlane32_swap(pk[1], pk[3], false, false);
       uint32_t bw[4];
-      bw[0] = h == 0 ? pk[0] : r0;
-      bw[1] = h == 0 ? pk[1] : r1;
-      bw[2] = h == 0 ? r0 : pk[2];
-      bw[3] = h == 0 ? r1 : pk[3];
+      bw[0] = x02[0];
+      bw[1] = x13[0];
+      bw[2] = x02[1];
+      bw[3] = x13[1];
       bf16x8 pf;
       __builtin_memcpy(&pf, bw, 16);
 #pragma unroll
