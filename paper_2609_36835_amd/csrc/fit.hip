@@ -412,8 +412,8 @@ __global__ void __launch_bounds__(256) k_chol_split3(const float *__restrict__ G
 }
 
 // G[K1 + r][K1 + c] -= acc for the tile's entries with c <= r + 63 (the lower
-// triangle, up to whole diagonal 64-blocks); every old value is loaded before
-// any store so the loads pipeline.
+// triangle, up to whole diagonal 64-blocks); per row block of the wave, every
+// old value is loaded before any store so the loads pipeline.
 template <int TM, int TN>
 struct EpiCholUpd {
   float *G;
@@ -426,25 +426,24 @@ struct EpiCholUpd {
     if (info[p] != 0) return;
     float *Gp = G + (size_t)p * ld * ld + (size_t)K1 * ld + K1;
     const int col = lane & 31;
-    float old[TM][TN][16];
 #pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-      for (int j = 0; j < TN; ++j)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int r = row0 + 32 * i + acc_row(v, lane), c = col0 + 32 * j + col;
-          old[i][j][v] = __builtin_nontemporal_load(&Gp[(size_t)r * ld + c]);
-        }
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
+    for (int i = 0; i < TM; ++i) {
+      float old[TN][16];
 #pragma unroll
       for (int j = 0; j < TN; ++j)
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
           const int r = row0 + 32 * i + acc_row(v, lane), c = col0 + 32 * j + col;
-          if (c <= r + 63) Gp[(size_t)r * ld + c] = old[i][j][v] - acc[i][j][v];
+          old[j][v] = __builtin_nontemporal_load(&Gp[(size_t)r * ld + c]);
         }
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int r = row0 + 32 * i + acc_row(v, lane), c = col0 + 32 * j + col;
+          if (c <= r + 63) Gp[(size_t)r * ld + c] = old[j][v] - acc[i][j][v];
+        }
+    }
   }
 };
 
@@ -1263,10 +1262,17 @@ hipError_t launch_cholesky_factor(float *Gw, const float *Gc, int B, int t, int6
       const int64_t rows = ld - K1;
       hipLaunchKernelGGL(k_chol_split3, dim3((unsigned)(rows * 256 / 4 / 256), B), dim3(256), 0, s, Gw, ld, K0, K1,
                          Ls, st.info);
-      BigShape g{B, (int)rows, (int)rows, kOuter, 3 * ld * 256, ld * 256, 256, 3 * ld * 256, ld * 256, 256, true, 4};
-      EpiCholUpd<1, 2> e{Gw, ld, K1, st.info};
+      // The six products with plane indices summing to at most 2 as one
+      // contraction over K = 6 x 256: segments (hi,hi) (hi,mid) (mid,hi)
+      // (hi,lo) (lo,hi) (mid,mid), so 256 x 256 tiles fit the LDS.
+      BigShape g{B, (int)rows, (int)rows, 6 * kOuter, 3 * ld * 256, ld * 256, 256, 3 * ld * 256, ld * 256, 256, true,
+                 4};
+      g.kseg = kOuter;
+      g.sega = 0u | (0u << 2) | (1u << 4) | (0u << 6) | (2u << 8) | (1u << 10);
+      g.segb = 0u | (1u << 2) | (0u << 4) | (2u << 6) | (0u << 8) | (1u << 10);
+      EpiCholUpd<2, 4> e{Gw, ld, K1, st.info};
       const hipError_t err =
-          launch_gemm_big<4, 2, 1, 2, 32, 3, 3, 2>(g, Ls + (size_t)K1 * 256, Ls + (size_t)K1 * 256, e, s);
+          launch_gemm_big<4, 2, 2, 4, 64, 1, 1, 2>(g, Ls + (size_t)K1 * 256, Ls + (size_t)K1 * 256, e, s);
       if (err != hipSuccess) return err;
     }
   }

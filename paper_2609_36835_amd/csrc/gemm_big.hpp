@@ -35,6 +35,12 @@ struct BigShape {
   int64_t b_pair, b_plane, ldb;
   bool syrk;                      // lower-triangular tiles only (nt <= mt)
   int group_m;
+  // Segmented K (single-plane configurations): K = segments x kseg, and
+  // segment s reads plane (sega >> 2s) & 3 of A and (segb >> 2s) & 3 of B at
+  // columns 0 .. kseg - 1.  One accumulation then sums several plane products
+  // (kseg = 0: plain K).
+  int kseg = 0;
+  uint32_t sega = 0, segb = 0;
 };
 
 template <int WM, int WN, int TM, int TN, int BK, int NA, int NB, int NS = 2>
@@ -148,12 +154,18 @@ __global__ void __launch_bounds__(64 * WM * WN, 1) k_gemm_big(BigShape g, const 
   }
   auto issue = [&](int slab, int st) {
     const int k0 = slab * BK;
+    int64_t ka = k0, kb = k0;
+    if (g.kseg) {   // wave-uniform: a slab never straddles two segments
+      const int sg = k0 / g.kseg, kk = k0 - sg * g.kseg;
+      ka = (int64_t)((g.sega >> (2 * sg)) & 3u) * g.a_plane + kk;
+      kb = (int64_t)((g.segb >> (2 * sg)) & 3u) * g.b_plane + kk;
+    }
     char *s = big_smem + st * C::STAGE;
 #pragma unroll
     for (int q = 0; q < NA; ++q)
 #pragma unroll
       for (int i = 0; i < C::A_INST; ++i)
-        __builtin_amdgcn_global_load_lds((const void *)(Ab + q * g.a_plane + offA[i] + k0),
+        __builtin_amdgcn_global_load_lds((const void *)(Ab + q * g.a_plane + offA[i] + ka),
                                          (lds_void_t *)(s + q * C::A_BYTES + (wave * C::A_INST + i) * 1024), 16, 0,
                                          0);
 #pragma unroll
@@ -161,7 +173,7 @@ __global__ void __launch_bounds__(64 * WM * WN, 1) k_gemm_big(BigShape g, const 
 #pragma unroll
       for (int i = 0; i < C::B_INST; ++i)
         __builtin_amdgcn_global_load_lds(
-            (const void *)(Bb + q * g.b_plane + offB[i] + k0),
+            (const void *)(Bb + q * g.b_plane + offB[i] + kb),
             (lds_void_t *)(s + NA * C::A_BYTES + q * C::B_BYTES + (wave * C::B_INST + i) * 1024), 16, 0, 0);
   };
 
@@ -373,6 +385,8 @@ template <int WM, int WN, int TM, int TN, int BK, int NA, int NB, int NS, class 
 hipError_t launch_gemm_big(const BigShape &g, const bf16 *A, const bf16 *B, const Epi &epi, hipStream_t s) {
   using C = BigCfg<WM, WN, TM, TN, BK, NA, NB, NS>;
   if (g.M % C::BM || g.N % C::BN || g.K % BK) return hipErrorInvalidValue;
+  if (g.kseg && (NA != 1 || NB != 1 || g.kseg % BK || g.K % g.kseg || g.K / g.kseg > 16))
+    return hipErrorInvalidValue;
   const int64_t tiles = big_tiles(g, C::BM, C::BN);
   if (tiles == 0) return hipSuccess;
   auto kern = k_gemm_big<WM, WN, TM, TN, BK, NA, NB, NS, Epi>;
