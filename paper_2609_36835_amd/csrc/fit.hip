@@ -722,29 +722,49 @@ __global__ void __launch_bounds__(256) k_phat(const float *__restrict__ LT, cons
                                               void *__restrict__ outm) {
   constexpr int PL = sizeof(T) == 2 ? 2 : 1;
   __shared__ float smx[4][64], ssum[4][64];
-  __shared__ T sp[PL][64][64 + 8];
+  __shared__ __attribute__((aligned(16))) T sp[PL][64][64 + 8];
   const int b = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int i0 = blockIdx.x * 64, i = i0 + lane;
   const float *L = LT + (size_t)b * tp * np_ + i;
   const float *bb = beta + (size_t)b * tp;
+  // exp(d) for d = x - max <= 0 as the hardware 2^(d log2(e)); the online max
+  // advances eight keys at a time and rescales the running sum only when the
+  // lane's maximum grew.
+  constexpr float kLog2e = 1.4426950408889634f;
   float mx = -INFINITY, sum = 0.0f;
-  if (i < n)
-    for (int r = wave; r < t; r += 4) {
+  if (i < n) {
+    int r = wave;
+    for (; r + 28 < t; r += 32) {
+      float x[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) x[u] = L[(size_t)(r + 4 * u) * np_] + bb[r + 4 * u];
+      float cm = x[0];
+#pragma unroll
+      for (int u = 1; u < 8; ++u) cm = fmaxf(cm, x[u]);
+      if (cm > mx) {
+        sum *= __builtin_amdgcn_exp2f((mx - cm) * kLog2e);
+        mx = cm;
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) sum += __builtin_amdgcn_exp2f((x[u] - mx) * kLog2e);
+    }
+    for (; r < t; r += 4) {
       const float x = L[(size_t)r * np_] + bb[r];
       if (x > mx) {
-        sum = sum * expf(mx - x) + 1.0f;
+        sum *= __builtin_amdgcn_exp2f((mx - x) * kLog2e);
         mx = x;
-      } else {
-        sum += expf(x - mx);
       }
+      sum += __builtin_amdgcn_exp2f((x - mx) * kLog2e);
     }
+  }
   smx[wave][lane] = mx;
   ssum[wave][lane] = sum;
   __syncthreads();
-  float M = fmaxf(fmaxf(smx[0][lane], smx[1][lane]), fmaxf(smx[2][lane], smx[3][lane]));
+  const float M = fmaxf(fmaxf(smx[0][lane], smx[1][lane]), fmaxf(smx[2][lane], smx[3][lane]));
   float S = 0.0f;
 #pragma unroll
-  for (int q = 0; q < 4; ++q) S += smx[q][lane] == -INFINITY ? 0.0f : ssum[q][lane] * expf(smx[q][lane] - M);
+  for (int q = 0; q < 4; ++q)
+    S += smx[q][lane] == -INFINITY ? 0.0f : ssum[q][lane] * __builtin_amdgcn_exp2f((smx[q][lane] - M) * kLog2e);
   const float inv = (i < n && S > 0.0f) ? 1.0f / S : 0.0f;
   T *PT = reinterpret_cast<T *>(out) + (size_t)b * PL * tp * np_;
   T *Pm = reinterpret_cast<T *>(outm) + (size_t)b * PL * tp * np_;
@@ -752,18 +772,29 @@ __global__ void __launch_bounds__(256) k_phat(const float *__restrict__ LT, cons
   typedef __attribute__((ext_vector_type(4))) uint32_t u32x4;
   for (int64_t r0 = 0; r0 < tp; r0 += 64) {
     __syncthreads();   // the previous tile's stores have read sp
-#pragma unroll 4
-    for (int e = 0; e < 16; ++e) {
-      const int rr = 16 * wave + e;
-      const int64_t r = r0 + rr;
-      const float p = (i < n && r < t) ? expf(L[(size_t)r * np_] + bb[r] - M) * inv : 0.0f;
+#pragma unroll
+    for (int e4 = 0; e4 < 16; e4 += 4) {   // four consecutive keys per LDS write
+      float pv[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int64_t r = r0 + 16 * wave + e4 + e;
+        pv[e] = (i < n && r < t)
+                    ? __builtin_amdgcn_exp2f((L[(size_t)r * np_] + bb[r] - M) * kLog2e) * inv
+                    : 0.0f;
+      }
+      const int rr = 16 * wave + e4;
       if constexpr (PL == 2) {
-        bf16 hi, lo;
-        split_bf16(p, hi, lo);
-        sp[0][lane][rr] = hi;
-        sp[1][lane][rr] = lo;
+        bf16x4 hi, lo;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          hi[e] = (bf16)pv[e];
+          lo[e] = (bf16)(pv[e] - (float)hi[e]);
+        }
+        *reinterpret_cast<bf16x4 *>(&sp[0][lane][rr]) = hi;
+        *reinterpret_cast<bf16x4 *>(&sp[1][lane][rr]) = lo;
       } else {
-        sp[0][lane][rr] = p;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) sp[0][lane][rr + e] = pv[e];
       }
     }
     __syncthreads();
