@@ -1196,13 +1196,13 @@ __global__ void __launch_bounds__(256) k_nnls_gather_gram(const float *__restric
   const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (e >= ldf * ldf) return;
   const int64_t i = e / ldf, j = e % ldf;
+  // the factorisation reads the lower triangle only
+  if (j > i) return;
   const int32_t n = nf[b];
   float v = i == j ? 1.0f : 0.0f;
-  if (i < n && j < n) {
+  if (i < n) {   // then j <= i < n; the free list ascends, so (idx_i, idx_j) is in the stored lower triangle
     const int32_t *ib = idx + (size_t)b * tp;
-    // the free list ascends, so i >= j reads the stored lower triangle
-    const int64_t hi = i >= j ? i : j, lo = i >= j ? j : i;
-    v = Gc[(size_t)b * tp * tp + (size_t)ib[hi] * tp + ib[lo]] + (i == j ? st.lam[b] : 0.0f);
+    v = Gc[(size_t)b * tp * tp + (size_t)ib[i] * tp + ib[j]] + (i == j ? st.lam[b] : 0.0f);
   }
   Gw[(size_t)b * ldf * ldf + e] = v;
 }
