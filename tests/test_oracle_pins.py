@@ -618,3 +618,43 @@ def test_pool_rms_properties():
     I2 = I.copy()
     I2[2] += 5.0
     np.testing.assert_allclose(oracle.pool_rms(I2), s, rtol=1e-12)
+
+
+# ------------------------------------------- chunked key sweeps and Phi_C
+@pytest.mark.parametrize("chunk_elems", [7, 60, 1 << 25])
+def test_global_logit_max_and_rowstats_across_key_chunks(monkeypatch, chunk_elems):
+    """eq. response_profile's z_merge and Appendix A.9's row statistics are
+    streamed over key chunks; with chunks of 1..3 keys (several boundaries,
+    a ragged last chunk) they must equal the brute-force loops over the whole
+    logit matrix."""
+    K, V, Q, *_ = small_pair(seed=7, T=17, n=9, d=5)
+    s = 0.37
+    monkeypatch.setattr(oracle.core, "_CHUNK_ELEMS", chunk_elems)
+    L = brute.logits(Q, K, s)
+    assert oracle.global_logit_max(Q, K, s) == pytest.approx(max(max(row) for row in L), rel=0, abs=1e-12)
+    z, m, Y = oracle.rowstats(Q, K, V, s)
+    zb, mb, Yb = brute.rowstats(Q, K, V, s)
+    np.testing.assert_allclose(z, zb, rtol=0, atol=1e-12)
+    np.testing.assert_allclose(m, mb, rtol=1e-12, atol=0)
+    np.testing.assert_allclose(Y, Yb, rtol=1e-10, atol=1e-12)
+
+
+def test_phi_c_closed_forms():
+    """Appendix A.9's Phi_C = exp(s Q C_k^T - z): with C_k = K its row sums are
+    the mass targets m (the definition of m); its entries match an explicit
+    exponential loop; and for compact keys inside the convex hull of the keys
+    every entry lies in (0, 1], because q . c is a convex combination of the
+    q . k_j and z_i is their maximum."""
+    K, V, Q, *_ = small_pair(seed=8, T=14, n=11, d=6)
+    s = 0.41
+    z, m, _ = oracle.rowstats(Q, K, V, s)
+    P = oracle.phi_c(Q, K, z, s)
+    np.testing.assert_allclose(P.sum(axis=1), m, rtol=1e-12, atol=0)
+    L = brute.logits(Q, K, s)
+    for i in range(Q.shape[0]):
+        for j in range(K.shape[0]):
+            assert P[i, j] == pytest.approx(math.exp(L[i][j] - z[i]), rel=1e-12)
+    g = rng(9)
+    A = g.dirichlet(np.ones(K.shape[0]), size=5)   # 5 convex combinations of the keys
+    Pc = oracle.phi_c(Q, A @ K, z, s)
+    assert np.all(Pc > 0.0) and np.all(Pc <= 1.0 + 1e-12)
