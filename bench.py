@@ -143,12 +143,13 @@ def measured_traffic(which, wl):
     return rec.get("traffic_bytes_per_launch")
 
 
-def stage_rooflines(wl, t, stages, steps, refine_steps=2):
+def stage_rooflines(wl, t, stages, steps, refine_steps=2, bias_mode=0):
     """Per-stage roofline: the algorithmic work of each stage for all pairs (flops of the contractions at the
     arithmetic's own peak, or HBM bytes), divided by the stage's event-timed duration per step.  Contractions on
     split bf16 operands (the Grams, the value right-hand side) count their algorithmic flops once against the
     bf16 peak although they issue 2-3 products; the float32-accurate Cholesky and triangular solves are priced
-    at the fp32 peak."""
+    at the fp32 peak.  With the exact non-negative fit (bias_mode 1) the beta solve is a data-dependent number of
+    pivoting iterations, so it is reported without a price."""
     B, T, n, d = wl.pairs, wl.T, wl.n, wl.d
     esz = 2 if wl.dtype == "bf16" else 4
     r = refine_steps
@@ -171,6 +172,12 @@ def stage_rooflines(wl, t, stages, steps, refine_steps=2):
         "solve_values": ("flop", ((r + 1) * 2 * t * t * d + r * 2 * 2.0 * n * t * d) * B, PEAK_FP32_TFLOPS),
     }
     out = {}
+    if bias_mode == 1:
+        del work["solve_beta"]
+        ms, cnt = stages.get("solve_beta", (0.0, 0))
+        if cnt:
+            out["solve_beta"] = {"ms": round(ms / steps, 3),
+                                 "note": "exact NNLS: pivoting iterations depend on the data; not priced"}
     for name, (unit, amount, peak) in work.items():
         ms, cnt = stages.get(name, (0.0, 0))
         if not cnt:
@@ -437,7 +444,7 @@ def main():
         "roofline_score_select": roofline_ss,
         "cpu_baseline": cpu,
         "stage_ms_per_step": {k: round(v[0] / args.steps, 3) for k, v in stages.items() if v[1]},
-        "stage_roofline": stage_rooflines(wl, t, stages, args.steps, params.refine_steps),
+        "stage_roofline": stage_rooflines(wl, t, stages, args.steps, params.refine_steps, args.bias_mode),
     }
     print(json.dumps(out), flush=True)
 
