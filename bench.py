@@ -68,16 +68,32 @@ def assign_flops(wl, t):
     return 2.0 * wl.n * (wl.T - t) * t * wl.pairs
 
 
-def cpu_baseline(wl, t, budget_s=25.0):
-    """The float64 oracle on a bounded sample of the same workload (whole pairs)."""
+def blas_info():
+    """The BLAS numpy links (vendor, version, threading) and its thread count."""
+    try:
+        from threadpoolctl import threadpool_info
+        pools = [p for p in threadpool_info() if p.get("user_api") == "blas"]
+        if pools:
+            p = pools[0]
+            return {"vendor": p.get("internal_api"), "version": p.get("version"),
+                    "threading": p.get("threading_layer"), "threads": p.get("num_threads")}
+    except Exception:   # threadpoolctl missing or unable to inspect
+        pass
+    return {"vendor": "unknown"}
+
+
+def cpu_baseline(wl, t, budget_s=30.0):
+    """The float64 oracle timed on the host cores: one whole layer (every KV head of layer 0) of the same workload,
+    scaled to all pairs, plus the 1-pair fp32 workload on all threads and on one thread."""
     import oracle
     try:
         cores = len(os.sched_getaffinity(0))
     except AttributeError:
         cores = os.cpu_count() or 1
     s = 1.0 / math.sqrt(wl.d)
+    blas = blas_info()
     done, t_used = 0, 0.0
-    while done < wl.pairs:
+    while done < min(wl.kv_heads, wl.pairs):
         layer, head = synth.pair_index(wl, done)
         p = synth.pair_inputs(wl, layer, head)
         h = {k: v.astype(np.float64) for k, v in p.items()}
@@ -86,13 +102,32 @@ def cpu_baseline(wl, t, budget_s=25.0):
         t_used += time.perf_counter() - t0
         done += 1
         log(f"[cpu_baseline] oracle pair {done}: {t_used:.1f}s cumulative")
-        if t_used >= budget_s * 0.5:
+        if t_used >= budget_s * 2:
             break
     per_pair = t_used / done
     value = wl.T / (per_pair * wl.pairs)
+
+    def tiny_time():
+        w1 = synth.WORKLOADS["tiny_f32_T1024"]
+        p = synth.pair_inputs(w1, 0, 0)
+        h = {k: v.astype(np.float64) for k, v in p.items()}
+        t0 = time.perf_counter()
+        oracle.compact_pair(h["K"], h["V"], h["Q"], h["W1"], h["b1"], h["w2"], h["b2"][0],
+                            t=oracle.budget(w1.T, w1.rho), scale=s)
+        return time.perf_counter() - t0
+    tiny_all = tiny_time()
+    try:
+        from threadpoolctl import threadpool_limits
+        with threadpool_limits(limits=1):
+            tiny_one = tiny_time()
+    except Exception:   # no thread control: report none
+        tiny_one = None
     return {"value": value, "unit": "tokens/s", "cores": cores, "kind": "oracle",
-            "sample": f"{done} of {wl.pairs} pairs (layer 0) of the same workload, float64 numpy oracle, "
-                      f"{per_pair:.2f} s/pair, scaled to all {wl.pairs} pairs"}
+            "sample": f"{done} of {wl.pairs} pairs (layer 0, every KV head) of the same workload, float64 numpy "
+                      f"oracle, {per_pair:.2f} s/pair, extrapolated to all {wl.pairs} pairs",
+            "blas": blas, "seconds_per_pair": round(per_pair, 3),
+            "tiny_f32_T1024_seconds": {"all_threads": round(tiny_all, 4),
+                                       "one_thread": None if tiny_one is None else round(tiny_one, 4)}}
 
 
 COPY_BYTES = 1 << 30
@@ -144,32 +179,40 @@ def measured_traffic(which, wl):
 
 
 def stage_rooflines(wl, t, stages, steps, refine_steps=2, bias_mode=0):
-    """Per-stage roofline: the algorithmic work of each stage for all pairs (flops of the contractions at the
-    arithmetic's own peak, or HBM bytes), divided by the stage's event-timed duration per step.  Contractions on
-    split bf16 operands (the Grams, the value right-hand side) count their algorithmic flops once against the
-    bf16 peak although they issue 2-3 products; the float32-accurate Cholesky and triangular solves are priced
-    at the fp32 peak.  With the exact non-negative fit (bias_mode 1) the beta solve is a data-dependent number of
-    pivoting iterations, so it is reported without a price."""
+    """Per-stage roofline.  `algorithmic_*` is the method's own work for all pairs (the flops of a contraction,
+    or the HBM bytes a stage must move), and `frac` prices it at the arithmetic's peak over the stage's
+    event-timed duration per step.  Where the implementation issues more than that, `issued_*` / `issued_frac`
+    report what it runs:
+      - the Grams and the value right-hand side on split bf16 operands issue three bf16 products per term;
+      - the two solves include `refine_steps` refinement steps against the data (each a residual and another
+        solve), which the method itself does not need: its solve is one forward and one backward triangular
+        sweep (mass fit: L read twice, 4 t^2 bytes per pair; value fit: 2 t^2 d flops per pair);
+      - the profile pass materialises E^T (2 bytes per entry) for the assignment contraction: its algorithmic work
+        is the logit contraction (2 n T d flops), the store is the implementation's.
+    The assignment passes after the contraction (finalize, refine, exact) and the precise anchor profiles are
+    the certification of the argmax; they are reported by time.  With the exact non-negative fit (bias_mode 1)
+    the beta solve is a data-dependent number of pivoting iterations and is not priced."""
     B, T, n, d = wl.pairs, wl.T, wl.n, wl.d
     esz = 2 if wl.dtype == "bf16" else 4
     r = refine_steps
-    work = {   # stage: (unit, amount for all pairs, peak)
-        "rowstats": ("flop", 4.0 * n * T * d * B, PEAK_BF16_TFLOPS),
-        "profiles": ("byte", (T * n * 2 + T * d * esz + n * d * esz + 4 * T) * B, PEAK_HBM_GBS),
-        "anchor_profiles": ("byte", 2.0 * t * n * 2 * B, PEAK_HBM_GBS),
-        "assign_gemm": ("flop", assign_flops(wl, t), PEAK_BF16_TFLOPS),
-        "merge": ("byte", (T * d * esz + 8 * T + 2 * t * d * 4) * B, PEAK_HBM_GBS),
-        "phic": ("byte", (8.0 * t * n + n * d * esz + 4 * n) * B, PEAK_HBM_GBS),
-        "gram_G": ("flop", 1.0 * n * t * (t + 1) * B, PEAK_BF16_TFLOPS),
-        "chol_G": ("flop", t ** 3 / 3.0 * B, PEAK_FP32_TFLOPS),
-        # one solve and r refinements: L read twice per solve, L^T twice per residual
-        "solve_beta": ("byte", ((r + 1) * 2 * 4.0 * t * t / 2 + r * 2 * 4.0 * t * n) * B, PEAK_HBM_GBS),
-        "phat": ("byte", (2 * 4.0 * t * n + 4 * 2.0 * t * n) * B, PEAK_HBM_GBS),
-        "gram_A": ("flop", 1.0 * n * t * (t + 1) * B, PEAK_BF16_TFLOPS),
-        "rhs_B": ("flop", 2.0 * n * t * d * B, PEAK_BF16_TFLOPS),
-        "chol_A": ("flop", t ** 3 / 3.0 * B, PEAK_FP32_TFLOPS),
-        # (r + 1) solves of two triangular sweeps with d right-hand sides, r residuals of two contractions
-        "solve_values": ("flop", ((r + 1) * 2 * t * t * d + r * 2 * 2.0 * n * t * d) * B, PEAK_FP32_TFLOPS),
+    split = 3.0 if wl.dtype == "bf16" else 1.0
+    work = {   # stage: (unit, algorithmic amount for all pairs, peak, issued amount or None)
+        "rowstats": ("flop", 4.0 * n * T * d * B, PEAK_BF16_TFLOPS, None),
+        "profiles": ("flop", 2.0 * n * T * d * B, PEAK_BF16_TFLOPS, None),
+        "anchor_profiles": ("flop", 2.0 * n * t * d * B, PEAK_BF16_TFLOPS, None),
+        "assign_gemm": ("flop", assign_flops(wl, t), PEAK_BF16_TFLOPS, None),
+        "merge": ("byte", (T * d * esz + 8 * T + 2 * t * d * 4) * B, PEAK_HBM_GBS, None),
+        "phic": ("flop", 2.0 * n * t * d * B, PEAK_BF16_TFLOPS, None),
+        "gram_G": ("flop", 1.0 * n * t * (t + 1) * B, PEAK_BF16_TFLOPS, split * n * t * (t + 1) * B),
+        "chol_G": ("flop", t ** 3 / 3.0 * B, PEAK_FP32_TFLOPS, None),
+        "solve_beta": ("byte", 4.0 * t * t * B, PEAK_HBM_GBS,
+                       ((r + 1) * 4.0 * t * t + r * 2 * 4.0 * t * n) * B),
+        "phat": ("byte", (2 * 4.0 * t * n + 4 * 2.0 * t * n) * B, PEAK_HBM_GBS, None),
+        "gram_A": ("flop", 1.0 * n * t * (t + 1) * B, PEAK_BF16_TFLOPS, split * n * t * (t + 1) * B),
+        "rhs_B": ("flop", 2.0 * n * t * d * B, PEAK_BF16_TFLOPS, split * 2.0 * n * t * d * B),
+        "chol_A": ("flop", t ** 3 / 3.0 * B, PEAK_FP32_TFLOPS, None),
+        "solve_values": ("flop", 2.0 * t * t * d * B, PEAK_FP32_TFLOPS,
+                         ((r + 1) * 2.0 * t * t * d + r * 2 * 2.0 * n * t * d) * B),
     }
     out = {}
     if bias_mode == 1:
@@ -178,20 +221,57 @@ def stage_rooflines(wl, t, stages, steps, refine_steps=2, bias_mode=0):
         if cnt:
             out["solve_beta"] = {"ms": round(ms / steps, 3),
                                  "note": "exact NNLS: pivoting iterations depend on the data; not priced"}
-    for name, (unit, amount, peak) in work.items():
+    for name, (unit, amount, peak, issued) in work.items():
         ms, cnt = stages.get(name, (0.0, 0))
         if not cnt:
             continue
         sec = ms / 1e3 / steps
-        if unit == "flop":
-            ach = amount / sec / 1e12
-            out[name] = {"bound": "mfma", "ms": round(ms / steps, 3), "algorithmic_tflop": round(amount / 1e12, 3),
-                         "achieved": round(ach, 1), "peak": peak, "unit": "TFLOP/s", "frac": round(ach / peak, 4)}
-        else:
-            ach = amount / sec / 1e9
-            out[name] = {"bound": "hbm", "ms": round(ms / steps, 3), "algorithmic_gb": round(amount / 1e9, 3),
-                         "achieved": round(ach, 1), "peak": peak, "unit": "GB/s", "frac": round(ach / peak, 4)}
+        scale, u, b = (1e12, "TFLOP/s", "mfma") if unit == "flop" else (1e9, "GB/s", "hbm")
+        ach = amount / sec / scale
+        key = "algorithmic_tflop" if unit == "flop" else "algorithmic_gb"
+        e = {"bound": b, "ms": round(ms / steps, 3), key: round(amount / scale, 3), "achieved": round(ach, 1),
+             "peak": peak, "unit": u, "frac": round(ach / peak, 4)}
+        if issued is not None:
+            e["issued_" + key.split("_")[1]] = round(issued / scale, 3)
+            e["issued_frac"] = round(issued / sec / scale / peak, 4)
+        out[name] = e
+    for name in ("assign_finalize", "assign_refine", "assign_exact", "zmax", "score", "select"):
+        ms, cnt = stages.get(name, (0.0, 0))
+        if cnt and name not in out:
+            out[name] = {"ms": round(ms / steps, 3)}
     return out
+
+
+def quality(wl, t, outs, pairs=(0, -1)):
+    """Diagnostics of the compaction on sampled pairs (float64, from the GPU's outputs; not gated):
+    the mass-fit residual E_mass = ||Phi_C w* - m|| / ||m|| (w* = exp(beta)) of eq. mass_fit, the mean per-row
+    relative l2 error against full attention on Q_ref and on 256 held-out queries, and the same errors of the
+    hard-subset baseline (attention over the t selected tokens' own keys and values, no bias)."""
+    import oracle
+    anchors = outs[0].cpu().numpy().astype(np.int64)
+    Ck, beta, Cv = (x.cpu().double().numpy() for x in outs[1:])
+    s = 1.0 / math.sqrt(wl.d)
+    res = []
+    for b in pairs:
+        b = b % wl.pairs
+        layer, head = synth.pair_index(wl, b)
+        p = synth.pair_inputs(wl, layer, head)
+        K, V, Q = (p[k].astype(np.float64) for k in ("K", "V", "Q"))
+        Qh = synth.heldout_queries(wl, layer, head).astype(np.float64)
+        z, m, Y = oracle.rowstats(Q, K, V, s)
+        Oh = oracle.attend_full(Qh, K, V, s)
+        PhiC = oracle.phi_c(Q, Ck[b], z, s)
+        e_mass = float(np.linalg.norm(PhiC @ np.exp(beta[b]) - m) / np.linalg.norm(m))
+        S = anchors[b]
+        comp_ref = oracle.row_rel_err(oracle.attend_compact(Q, Ck[b], beta[b], Cv[b], s), Y).mean()
+        comp_held = oracle.row_rel_err(oracle.attend_compact(Qh, Ck[b], beta[b], Cv[b], s), Oh).mean()
+        hard_ref = oracle.row_rel_err(oracle.attend_full(Q, K[S], V[S], s), Y).mean()
+        hard_held = oracle.row_rel_err(oracle.attend_full(Qh, K[S], V[S], s), Oh).mean()
+        res.append({"pair": b, "E_mass": round(e_mass, 5), "rel_l2_ref": round(float(comp_ref), 5),
+                    "rel_l2_heldout": round(float(comp_held), 5), "hard_subset_rel_l2_ref": round(float(hard_ref), 5),
+                    "hard_subset_rel_l2_heldout": round(float(hard_held), 5)})
+        log(f"[quality] pair {b}: {res[-1]}")
+    return res
 
 
 def score_select_bytes(wl, t):
@@ -408,7 +488,8 @@ def main():
     launches_per_step = max(cnt_assign // args.steps, 1)
     flops_per_launch = assign_flops(wl, t) / launches_per_step
     achieved = flops_per_launch / avg_launch_s / 1e12
-    roofline = {"bound": "mfma", "kernel": "k_gemm_big<4,2,2,4,64,1,1,2,EpiArgmaxBig> (key-to-anchor assignment)",
+    roofline = {"bound": "mfma", "kernel": "k_gemm_big<4,2,2,4,64,1,1,2,f16,EpiArgmaxBig> (key-to-anchor assignment, "
+                                      "fp16 operands)",
                 "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": measured_traffic("assign", wl),
                 "avg_launch_ms": round(avg_launch_s * 1e3, 3),
@@ -424,10 +505,19 @@ def main():
                    "frac": round(ss_gbs / PEAK_HBM_GBS, 4), "traffic": measured_traffic("score_select", wl),
                    "avg_launch_ms": round(ss_s * 1e3, 4), "algorithmic_bytes_per_launch": ss_bytes}
 
+    st = comp.assign_stats().cpu().numpy()
+    keys = wl.pairs * max(1, wl.T - t)
+    assign_stats = {"flagged_frac": round(float(st[:, 0].sum()) / keys, 5),
+                    "float64_frac": round(float(st[:, 1].sum()) / keys, 6),
+                    "candidates_per_flagged": round(float(st[:, 2].sum()) / max(1, int(st[:, 0].sum())), 3),
+                    "undecided": int(st[:, 3].sum())}
+    outs = [x.clone() for x in (comp.anchors, comp.C_k, comp.beta, comp.C_v)]
     cpu = None
+    qual = None
     if not args.no_cpu_baseline:
         del K, V, Q, comp
         torch.cuda.empty_cache()
+        qual = quality(wl, t, outs)
         cpu = cpu_baseline(wl, t)
 
     out = {
@@ -445,6 +535,8 @@ def main():
         "cpu_baseline": cpu,
         "stage_ms_per_step": {k: round(v[0] / args.steps, 3) for k, v in stages.items() if v[1]},
         "stage_roofline": stage_rooflines(wl, t, stages, args.steps, params.refine_steps, args.bias_mode),
+        "assignment": assign_stats,
+        "quality": qual,
     }
     print(json.dumps(out), flush=True)
 

@@ -28,8 +28,8 @@
  *  - The library never allocates device memory.  Entry points that need scratch
  *    take a caller-owned device workspace (ws, ws_bytes) of at least
  *    arckv_workspace_size() bytes, 256-byte aligned.  Its contents are
- *    undefined on entry and exit; it must not be shared by calls that may
- *    overlap in time.
+ *    undefined on entry and exit (apart from the counters arckv_assign_stats
+ *    reads); it must not be shared by calls that may overlap in time.
  *  - All device work is enqueued on the caller's stream; no entry point
  *    synchronises the host, with one exception: the exact non-negative mass
  *    fit (arckv_fit_params.bias_mode = 1) reads two integers back once per
@@ -292,6 +292,26 @@ arckv_status arckv_compact_scored(const arckv_problem *prob, const void *K, cons
                                   const arckv_fit_params *p, int32_t *t_out, int32_t *anchors,
                                   float *C_k, float *beta, float *C_v, int32_t *info,
                                   void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* Statistics of the key-to-anchor decision of the most recent arckv_merge,
+ * arckv_compact or arckv_compact_scored call that used this workspace with
+ * this problem and anchor count t (Section 3.4, eq. anchor_assignment).  The
+ * argmax is decided in up to three passes: an fp16 (bf16 inputs) or fp32
+ * contraction whose per-similarity rounding error is bounded, so every key
+ * with a single anchor inside the bound is decided there; a refine pass over
+ * the flagged keys' candidate anchors with logits accurate to about 1e-6; and
+ * a float64 pass for the keys the refine pass cannot separate (equal float64
+ * similarities go to the lowest r).  Copies [B][8] int32 to the device array
+ * stats, per pair: [0] keys flagged after the first pass, [1] keys decided in
+ * float64, [2] candidate anchors of the flagged keys (a whole anchor tile
+ * counts 256), [3] keys left undecided (more candidates than the later passes
+ * take; such a key keeps the best similarity of the last pass that saw it, and
+ * 0 is expected), [4] and [5] the undecided ones of the first and of the
+ * refine pass, [6] keys sent to the refine pass, [7] flagged keys with a whole
+ * anchor tile among their candidates.  Those counters are the only workspace
+ * contents that outlive a call. */
+arckv_status arckv_assign_stats(const arckv_problem *prob, int32_t t, const void *ws, size_t ws_bytes,
+                                int32_t *stats, hipStream_t stream);
 
 /* Human-readable name of a status code (static string). */
 const char *arckv_status_string(arckv_status s);

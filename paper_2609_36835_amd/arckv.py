@@ -26,7 +26,7 @@ ENTRY_POINTS = (
     "arckv_rowstats", "arckv_merge", "arckv_fit_bias", "arckv_fit_values", "arckv_compact",
     "arckv_status_string", "arckv_set_timing", "arckv_stage_times", "arckv_reset_timing",
     "arckv_attend_workspace_size", "arckv_attend", "arckv_budgets", "arckv_select_count", "arckv_select_ex",
-    "arckv_dsa_workspace_size", "arckv_score_dsa", "arckv_compact_scored",
+    "arckv_dsa_workspace_size", "arckv_score_dsa", "arckv_compact_scored", "arckv_assign_stats",
 )
 
 
@@ -99,6 +99,7 @@ def lib():
         L.arckv_compact_scored.argtypes = [P(Problem), vp, vp, vp, vp, ctypes.c_double, P(FitParams), P(i32),
                                            vp, vp, vp, vp, vp, vp, sz, vp]
         L.arckv_attend.argtypes = [i32, i32, i32, i32, ctypes.c_float, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+        L.arckv_assign_stats.argtypes = [P(Problem), i32, vp, sz, vp, vp]
         for name in ENTRY_POINTS:
             getattr(L, name).restype = ctypes.c_int if name != "arckv_status_string" else ctypes.c_char_p
         _LIB = L
@@ -237,7 +238,15 @@ def rowstats(K, V, Q, scale=None):
     return z, m, Y
 
 
-def merge(K, Q, z, anchors, lambda_m=0.25, scale=None, ws_bytes: Optional[int] = None):
+def assign_stats(prob: Problem, t: int, ws: torch.Tensor, ws_bytes: int) -> torch.Tensor:
+    """arckv_assign_stats: [B][8] int32 counters of the last assignment run on ws (include/arckv.h)."""
+    out = torch.empty(prob.B, 8, dtype=torch.int32, device=ws.device)
+    _check(lib().arckv_assign_stats(ctypes.byref(prob), int(t), _ptr(ws), int(ws_bytes), _ptr(out), _stream()),
+           "arckv_assign_stats")
+    return out
+
+
+def merge(K, Q, z, anchors, lambda_m=0.25, scale=None, ws_bytes: Optional[int] = None, return_stats=False):
     prob = problem(K, Q, scale)
     t = anchors.shape[1]
     B, T, d = K.shape
@@ -248,6 +257,8 @@ def merge(K, Q, z, anchors, lambda_m=0.25, scale=None, ws_bytes: Optional[int] =
     ws = _workspace(nbytes, K.device)
     _check(lib().arckv_merge(ctypes.byref(prob), _ptr(K), _ptr(Q), _ptr(z), _ptr(anchors), int(t), float(lambda_m),
                              _ptr(Ck), _ptr(kappa), _ptr(phi), _ptr(ws), nbytes, _stream()), "arckv_merge")
+    if return_stats:
+        return Ck, kappa, phi, assign_stats(prob, t, ws, nbytes)
     return Ck, kappa, phi
 
 
@@ -388,12 +399,17 @@ class Compactor:
         assert t_out.value == self.t
         return self.anchors, self.C_k, self.beta, self.C_v, self.info
 
+    def assign_stats(self) -> torch.Tensor:
+        """[B][8] assignment counters of the last call (arckv_assign_stats)."""
+        return assign_stats(self.prob, self.t, self.ws, self.ws_bytes)
 
-def compact(K, V, Q, W1, b1, w2, b2, rho, scale=None, params: Optional[FitParams] = None):
-    """One-shot arckv_compact: returns (anchors, C_k, beta, C_v, info)."""
+
+def compact(K, V, Q, W1, b1, w2, b2, rho, scale=None, params: Optional[FitParams] = None, return_stats=False):
+    """One-shot arckv_compact: returns (anchors, C_k, beta, C_v, info) (+ assignment stats)."""
     B, T, _ = K.shape
     c = Compactor(B, T, Q.shape[1], rho, K.dtype, K.device, scale, params)
-    return c(K, V, Q, W1, b1, w2, b2)
+    out = c(K, V, Q, W1, b1, w2, b2)
+    return (*out, c.assign_stats()) if return_stats else out
 
 
 def set_timing(enable: bool):

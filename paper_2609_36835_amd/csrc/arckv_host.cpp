@@ -9,6 +9,7 @@
 #include <hip/hip_runtime.h>
 
 #include "arckv.h"
+#include "assign.hpp"
 
 namespace arckv {
 typedef uint16_t bf16_t_;   // bfloat16 storage, opaque on the host
@@ -53,21 +54,34 @@ static int64_t chunked_count(int64_t T, int64_t t, int64_t chunk_len) {
 hipError_t launch_rowstats(int dtype, const void *K, const void *V, const void *Q, float *z, float *m, float *Y,
                            int B, int T, int n, float scale, hipStream_t s);
 hipError_t launch_profiles(int dtype, const void *Q, const void *K, const float *zmerge, const int32_t *anchors,
-                           int t, void *Et, void *U, float *ssq, float *phi, int B, int T, int n, int64_t Tp,
-                           int64_t tp, int64_t np_, float scale, hipStream_t s);
+                           int t, void *Et, float *phi, int B, int T, int n, int64_t Tp, int64_t np_, float scale,
+                           hipStream_t s);
 hipError_t launch_phic(int dtype, const void *Q, const void *Ckp, const float *z, void *PhiT, float *LT,
                        const float *m, double *h, int B, int t, int n, int64_t tp, int64_t np_, float scale,
                        hipStream_t s);
 hipError_t launch_zmax(const float *z, int B, int n, float *zmax, hipStream_t s);
-hipError_t launch_anchor_profiles(int dtype, void *U, const float *ssq, int B, int t, int64_t np_, int64_t tp,
-                                  hipStream_t s);
-hipError_t launch_assign_finalize(const uint64_t *part, int MT, int64_t Np, const int32_t *anchors, int B, int T,
-                                  int t, int32_t *kappa, hipStream_t s);
+hipError_t launch_pair_norms(int dtype, const void *Q, const void *K, const int32_t *anchors, int P, int n, int T,
+                             int t, void *pn, hipStream_t s);
+hipError_t launch_anchor_profiles(int dtype, const void *Q, const void *K, const int32_t *anchors,
+                                  const float *zmerge, int P, int n, int T, int t, int64_t tp, int64_t np_,
+                                  float scale, float *Ua, double *anorm, void *U, hipStream_t s);
+hipError_t launch_assign_finalize(int dtype, const void *K, const uint64_t *part1, const uint64_t *part2,
+                                  const uint32_t *part3, int MT, int TR, int64_t Np, const int32_t *anchors,
+                                  const float *phi, const float *zmerge, const void *pn, int P, int T, int t, int n,
+                                  float scale, int32_t *kappa, const AssignLists &L, hipStream_t s);
+hipError_t launch_assign_refine(int dtype, const void *Q, const void *K, const float *zmerge, const void *pn,
+                                const float *Ua, const double *anorm, int P, int T, int t, int n, int64_t tp,
+                                int64_t np_, float scale, int32_t *kappa, const AssignLists &L, hipStream_t s);
+hipError_t launch_assign_exact(int dtype, const void *Q, const void *K, const int32_t *anchors, const float *zmerge,
+                               int P, int T, int t, int n, float scale, int32_t *kappa, const AssignLists &L,
+                               hipStream_t s);
+hipError_t launch_fill_i32(int32_t *p, int64_t count, int32_t v, hipStream_t s);
 hipError_t launch_group_merge(int dtype, const void *K, const float *phi, const int32_t *kappa,
                               const int32_t *anchors, int B, int T, int t, int64_t tp, float lambda,
                               int32_t *offsets, int32_t *cursor, int32_t *perm, float *Ck, void *Ckp, hipStream_t s);
-hipError_t launch_assign_gemm(int dtype, const void *U, const void *Et, uint64_t *part, int P, int t, int64_t tp,
-                              int64_t N, int64_t Et_rows, int64_t np_, hipStream_t s);
+hipError_t launch_assign_gemm(int dtype, const void *U, const void *Et, uint64_t *part1, uint64_t *part2,
+                              uint32_t *part3, int P, int t, int64_t tp, int64_t N, int64_t Et_rows, int64_t np_,
+                              hipStream_t s);
 hipError_t launch_gram(int dtype, const void *X, float *G, float *Gc, int P, int64_t tp, int64_t np_, hipStream_t s);
 hipError_t launch_rhs_gemm(int dtype, const void *PT, const void *YT, float *Bm, int P, int64_t tp, int64_t np_,
                            hipStream_t s);
@@ -119,12 +133,12 @@ hipError_t launch_attend(int P, int G, int t, int F, float scale, const void *Q,
 enum Stage {
   ST_SCORE, ST_SELECT, ST_ROWSTATS, ST_ZMAX, ST_PROFILES, ST_ANCHOR_PROF, ST_ASSIGN, ST_FINALIZE, ST_MERGE,
   ST_PHIC, ST_GRAM_G, ST_CHOL_G, ST_SOLVE_W, ST_PHAT, ST_GRAM_A, ST_RHS, ST_CHOL_A, ST_SOLVE_V, ST_ATTEND,
-  ST_DSA_PROJ, ST_DSA_VALUE, ST_DSA_INDEX, ST_COUNT
+  ST_DSA_PROJ, ST_DSA_VALUE, ST_DSA_INDEX, ST_ASSIGN_REFINE, ST_ASSIGN_EXACT, ST_COUNT
 };
 static const char *kStageNames[ST_COUNT] = {
     "score", "select", "rowstats", "zmax", "profiles", "anchor_profiles", "assign_gemm", "assign_finalize",
     "merge", "phic", "gram_G", "chol_G", "solve_beta", "phat", "gram_A", "rhs_B", "chol_A", "solve_values",
-    "attend", "dsa_proj", "dsa_value_head", "dsa_index"};
+    "attend", "dsa_proj", "dsa_value_head", "dsa_index", "assign_refine", "assign_exact"};
 
 struct TimingState {
   std::mutex mu;
@@ -194,6 +208,11 @@ static Dims make_dims(const arckv_problem *p, int t) {
   return d;
 }
 
+// Capacity of the assignment's candidate pool, per cached key of a pair (about 1
+// candidate per key at the 32K workload; a key whose list does not fit keeps its
+// first-pass decision and is counted as undecided).
+constexpr int64_t kPoolPerKey = 8;
+
 struct Bump {
   int64_t off = 0;
   int64_t take(int64_t bytes) {
@@ -206,11 +225,13 @@ struct Bump {
 // Persistent per-pair arrays ([B]-sized) followed by a chunk region for P pairs.
 struct Plan {
   // persistent
-  int64_t scores, z, m, Y, zmax, kappa, phi, beta_ws, info_g, info_a, st_g, st_a;
+  int64_t scores, z, m, Y, zmax, kappa, phi, beta_ws, info_g, info_a, st_g, st_a, astats;
   int64_t persistent_bytes;
   // chunk region (offsets relative to chunk base)
   int64_t Ckp;
-  int64_t Et, U, ssq, part, offsets, cursor, perm;       // merge phase
+  int64_t Et, U, Ua, anorm, pn, part1, part2, part3, fcnt, fkey, foff, fn, pcnt, pool, psim, dcnt, dkey, dn,
+      dent;   // merge phase
+  int64_t offsets, cursor, perm;
   int64_t PhiT, LT, Gw, Gc, dinv, lsplit, h, w, y, x, res, sw, u, YT, Bm, X, R, Y2, XT, Pm, UT;  // fit phase
   int64_t nF, nidx, nbidx, npos, nnf, nnb, nstate, nred, ny, nrhs, ndx;   // exact NNLS (bias_mode 1)
   int64_t chunk_bytes;
@@ -232,6 +253,7 @@ static Plan make_plan(const Dims &d, int64_t P) {
   pl.info_a = a.take(B * 4);
   pl.st_g = a.take(B * 16);    // trace (8) + lam (4) + delta (4)
   pl.st_a = a.take(B * 16);
+  pl.astats = a.take(B * kAssignStats * 4);  // assignment statistics [B][kAssignStats]
   pl.persistent_bytes = a.off;
 
   Bump c;
@@ -240,8 +262,23 @@ static Plan make_plan(const Dims &d, int64_t P) {
   Bump m = c;
   pl.Et = m.take(P * d.Tp * d.np_ * d.esz);
   pl.U = m.take(P * d.tp * d.np_ * d.esz);
-  pl.ssq = m.take(P * d.tp * 4);
-  pl.part = m.take(P * d.MT * d.Tp * 8);
+  pl.Ua = m.take(P * d.tp * d.np_ * 4);       // precise anchor profiles (fp32)
+  pl.anorm = m.take(P * d.tp * 8);
+  pl.pn = m.take(P * 16);
+  pl.part1 = m.take(P * d.MT * d.Tp * 8);     // top-3 partials per (anchor tile, key)
+  pl.part2 = m.take(P * d.MT * d.Tp * 8);
+  pl.part3 = m.take(P * d.MT * d.Tp * 4);
+  pl.fcnt = m.take(P * 4);
+  pl.fkey = m.take(P * d.Tp * 4);
+  pl.foff = m.take(P * d.Tp * 4);
+  pl.fn = m.take(P * d.Tp * 4);
+  pl.pcnt = m.take(P * 4);
+  pl.pool = m.take(P * kPoolPerKey * d.Tp * 4);   // candidate pool: kPoolPerKey entries per key on average
+  pl.psim = m.take(P * kPoolPerKey * d.Tp * 8);
+  pl.dcnt = m.take(P * 4);
+  pl.dkey = m.take(P * d.Tp * 4);
+  pl.dn = m.take(P * d.Tp * 4);
+  pl.dent = m.take(P * d.Tp * 16 * 4);
   pl.offsets = m.take(P * (int64_t)(d.t + 1) * 4);
   pl.cursor = m.take(P * (int64_t)d.t * 4);
   pl.perm = m.take(P * (int64_t)d.T * 4);
@@ -369,16 +406,34 @@ static arckv_status run_merge_chunk(const Ctx &c, int b0, int P, const void *K, 
   const int32_t *anc = anchors + (size_t)b0 * d.t;
   void *Et = c.chunk<char>(c.pl.Et);
   void *U = c.chunk<char>(c.pl.U);
-  uint64_t *part = c.chunk<uint64_t>(c.pl.part);
-  float *ssq = c.chunk<float>(c.pl.ssq);
-  // the assignment runs over the T - t non-anchor keys (compacted E^T rows)
+  float *Ua = c.chunk<float>(c.pl.Ua);
+  double *anorm = c.chunk<double>(c.pl.anorm);
+  void *pn = c.chunk<char>(c.pl.pn);
+  uint64_t *part1 = c.chunk<uint64_t>(c.pl.part1), *part2 = c.chunk<uint64_t>(c.pl.part2);
+  uint32_t *part3 = c.chunk<uint32_t>(c.pl.part3);
+  AssignLists L{c.chunk<int32_t>(c.pl.fcnt), c.chunk<int32_t>(c.pl.fkey),  c.chunk<int32_t>(c.pl.foff),
+                c.chunk<int32_t>(c.pl.fn),   c.chunk<int32_t>(c.pl.pcnt),  c.chunk<int32_t>(c.pl.pool),
+                c.chunk<double>(c.pl.psim),  kPoolPerKey * d.Tp,           c.chunk<int32_t>(c.pl.dcnt),
+                c.chunk<int32_t>(c.pl.dkey), c.chunk<int32_t>(c.pl.dn),    c.chunk<int32_t>(c.pl.dent),
+                c.pers<int32_t>(c.pl.astats) + (size_t)b0 * kAssignStats, d.Tp};
+  const float *zm = zmax + b0;
+  int32_t *kap = kappa + (size_t)b0 * d.T;
+  const float *phib = phi + (size_t)b0 * d.T;
+  // the assignment contraction runs over the T - t non-anchor keys (compacted E^T rows)
   const int64_t Tc = rup(d.T - d.t, kPadH);
-  STAGE(ST_PROFILES, launch_profiles(d.dtype, Qc, Kc, zmax + b0, anc, d.t, Et, U, ssq, phi + (size_t)b0 * d.T, P,
-                                     d.T, d.n, d.Tp, d.tp, d.np_, c.scale, stream));
-  STAGE(ST_ANCHOR_PROF, launch_anchor_profiles(d.dtype, U, ssq, P, d.t, d.np_, d.tp, stream));
-  STAGE(ST_ASSIGN, launch_assign_gemm(d.dtype, U, Et, part, P, d.t, d.tp, Tc, d.Tp, d.np_, stream));
-  const int mt_used = (int)(d.dtype == ARCKV_BF16 ? d.tp / 256 : d.tp / 128);
-  STAGE(ST_FINALIZE, launch_assign_finalize(part, mt_used, Tc, anc, P, d.T, d.t, kappa + (size_t)b0 * d.T, stream));
+  const int TR = d.dtype == ARCKV_BF16 ? 256 : 128;               // anchor rows per contraction tile
+  const int mt_used = (int)(d.tp / TR);
+  STAGE(ST_PROFILES, launch_profiles(d.dtype, Qc, Kc, zm, anc, d.t, Et, phi + (size_t)b0 * d.T, P, d.T, d.n, d.Tp,
+                                     d.np_, c.scale, stream));
+  STAGE(ST_ANCHOR_PROF, launch_pair_norms(d.dtype, Qc, Kc, anc, P, d.n, d.T, d.t, pn, stream));
+  STAGE(ST_ANCHOR_PROF, launch_anchor_profiles(d.dtype, Qc, Kc, anc, zm, P, d.n, d.T, d.t, d.tp, d.np_, c.scale, Ua,
+                                               anorm, U, stream));
+  STAGE(ST_ASSIGN, launch_assign_gemm(d.dtype, U, Et, part1, part2, part3, P, d.t, d.tp, Tc, d.Tp, d.np_, stream));
+  STAGE(ST_FINALIZE, launch_assign_finalize(d.dtype, Kc, part1, part2, part3, mt_used, TR, Tc, anc, phib, zm, pn, P,
+                                            d.T, d.t, d.n, c.scale, kap, L, stream));
+  STAGE(ST_ASSIGN_REFINE, launch_assign_refine(d.dtype, Qc, Kc, zm, pn, Ua, anorm, P, d.T, d.t, d.n, d.tp, d.np_,
+                                               c.scale, kap, L, stream));
+  STAGE(ST_ASSIGN_EXACT, launch_assign_exact(d.dtype, Qc, Kc, anc, zm, P, d.T, d.t, d.n, c.scale, kap, L, stream));
   STAGE(ST_MERGE, launch_group_merge(d.dtype, Kc, phi + (size_t)b0 * d.T, kappa + (size_t)b0 * d.T, anc, P, d.T,
                                      d.t, d.tp, lambda_m, c.chunk<int32_t>(c.pl.offsets),
                                      c.chunk<int32_t>(c.pl.cursor), c.chunk<int32_t>(c.pl.perm),
@@ -929,6 +984,19 @@ const char *arckv_status_string(arckv_status s) {
     case ARCKV_ERR_HIP: return "HIP runtime error";
   }
   return "unknown status";
+}
+
+arckv_status arckv_assign_stats(const arckv_problem *prob, int32_t t, const void *ws, size_t ws_bytes,
+                                int32_t *stats, hipStream_t stream) {
+  CHECK(check_problem(prob));
+  if (!ws || !stats || t < 1 || t > prob->T) return ARCKV_ERR_INVALID_ARG;
+  const Dims d = make_dims(prob, t);
+  if (!aligned(ws, 256) || ws_bytes < plan_total(d, 1)) return ARCKV_ERR_WORKSPACE;
+  const Plan pl = make_plan(d, 1);   // the persistent region does not depend on the chunk size
+  if (hipMemcpyAsync(stats, (const char *)ws + pl.astats, (size_t)prob->B * kAssignStats * 4, hipMemcpyDeviceToDevice, stream) !=
+      hipSuccess)
+    return ARCKV_ERR_HIP;
+  return ARCKV_OK;
 }
 
 arckv_status arckv_set_timing(int32_t enable) {

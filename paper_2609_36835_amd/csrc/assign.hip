@@ -1,0 +1,844 @@
+// Key-to-anchor assignment with a certified argmax (Section 3.4,
+// eq. anchor_assignment; ties to the lowest r).
+//
+// The bulk similarity contraction S[r][j] = sum_i U_S[i][r] E[i][j] runs on
+// fp16 (bf16 inputs) or fp32 (fp32 inputs) operands; rounding the operands can
+// reorder two anchors whose similarities to a key are close.  Every key is
+// therefore decided in up to three passes, each a certified filter for the next:
+//
+//  A  the contraction keeps, per (anchor tile, key), the two best similarities
+//     and the third value (EpiArgmax*).  With eta the relative and alpha the
+//     absolute error bound of one similarity, no anchor r with
+//     S_A(r) < (S_A(best) - alpha)(1 - eta)/(1 + eta) - alpha can be the argmax.
+//     A key with exactly one anchor above that threshold is decided; the others
+//     are flagged, with the best two of each tile above the threshold, or the
+//     whole tile where its third value reaches it, as candidates
+//     (k_assign_finalize).
+//  C  flagged keys are re-scored against their candidates: for bf16 inputs from
+//     logits formed on MFMA with one fp32 accumulator per 16-wide slice of the
+//     head dimension, summed in float64, so the logit error is at most
+//     gamma_16 s sum_k |q_k k_k|; exponentials with float64 range reduction; dot
+//     products in float64 (for fp32 inputs, float64 logits).  Keys that still
+//     have more than one survivor go on (k_assign_refine).
+//  D  float64 throughout: logits, exponentials, norms and dot products
+//     (k_assign_exact).  Equal float64 similarities go to the lower r.
+//
+// The bounds are stated on the functions that use them.
+#include "assign.hpp"
+#include "common.hpp"
+
+namespace arckv {
+
+constexpr int kAssignMaxD = 16;   // candidate entries of one key in the float64 pass (assign.hpp)
+constexpr double kU32 = 5.9604644775390625e-08;   // 2^-24, unit roundoff of fp32
+constexpr double kU16 = 4.8828125e-04;            // 2^-11, unit roundoff of fp16
+
+__device__ inline double gamma_m(double m) { return m * kU32 / (1.0 - m * kU32); }
+
+// Per-pair constants of the error bounds.
+struct AssignPair {
+  double qmax;   // max_i ||q_i||_2
+  double amax;   // max_r ||k_{s_r}||_2
+};
+
+// ---------------------------------------------------------------- norms
+// pn[b] = {max_i ||q_i||, max_r ||k_{s_r}||}, in float64, rounded up by one part
+// in 1e12 so that the bounds built on them stay upper bounds.
+template <typename E>
+__global__ void __launch_bounds__(256) k_pair_norms(const E *__restrict__ Q, const E *__restrict__ K,
+                                                    const int32_t *__restrict__ anchors, int n, int T, int t,
+                                                    AssignPair *__restrict__ pn) {
+  __shared__ double red[2][4];
+  const int b = blockIdx.x, tid = threadIdx.x;
+  double mq = 0.0, ma = 0.0;
+  for (int i = tid; i < n; i += 256) {
+    const E *q = Q + ((size_t)b * n + i) * kHeadDim;
+    double ss = 0.0;
+    for (int k = 0; k < kHeadDim; ++k) {
+      const double v = (double)(float)q[k];
+      ss = fma(v, v, ss);
+    }
+    mq = fmax(mq, ss);
+  }
+  for (int r = tid; r < t; r += 256) {
+    const E *kr = K + ((size_t)b * T + anchors[(size_t)b * t + r]) * kHeadDim;
+    double ss = 0.0;
+    for (int k = 0; k < kHeadDim; ++k) {
+      const double v = (double)(float)kr[k];
+      ss = fma(v, v, ss);
+    }
+    ma = fmax(ma, ss);
+  }
+  for (int m = 32; m >= 1; m >>= 1) {
+    mq = fmax(mq, __shfl_xor(mq, m, 64));
+    ma = fmax(ma, __shfl_xor(ma, m, 64));
+  }
+  if ((tid & 63) == 0) {
+    red[0][tid >> 6] = mq;
+    red[1][tid >> 6] = ma;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    double a = 0.0, c = 0.0;
+    for (int w = 0; w < 4; ++w) {
+      a = fmax(a, red[0][w]);
+      c = fmax(c, red[1][w]);
+    }
+    pn[b].qmax = sqrt(a) * (1.0 + 1e-12);
+    pn[b].amax = sqrt(c) * (1.0 + 1e-12);
+  }
+}
+
+// exp(x) for x <= ~0 in float64 range reduction around the hardware base-2
+// exponential: x log2(e) = k + f, f in [0, 1), exp(x) = 2^f 2^k.  Relative error
+// at most 2^-22 (v_exp_f32 within 1 ulp on [1, 2), f rounded to fp32 within
+// 2^-25 absolute, and the products in float64).
+__device__ inline double exp_reduced(double x) {
+  const double y = x * 1.4426950408889634074;
+  const double k = floor(y);
+  const float f = (float)(y - k);
+  return ldexp((double)__builtin_amdgcn_exp2f(f), (int)k);
+}
+constexpr double kExpReducedErr = 2.384185791015625e-07;   // 2^-22
+
+// ---------------------------------------------------------------- anchor profiles
+// Precise anchor profiles e_ir = exp(s q_i.k_{s_r} - z_merge) for bf16 inputs:
+// the logit is formed on MFMA with a fresh fp32 accumulator for each 16-wide
+// slice of the head dimension (products of bf16 values are exact in fp32, so
+// each slice sum is within gamma_16 sum_slice |q_k k_k| of exact) and the eight
+// slices are added in float64.  Ua [P][tp][np] float32 (zero for i >= n),
+// anorm [P][tp] = ||e_r||_2 in float64 from the unrounded values.  A workgroup
+// owns 128 anchors (32 per wave, kept as MFMA B fragments) and sweeps all
+// queries in tiles of 64.
+__global__ void __launch_bounds__(256) k_prof_anchor_bf16(const bf16 *__restrict__ Q, const bf16 *__restrict__ K,
+                                                          const int32_t *__restrict__ anchors,
+                                                          const float *__restrict__ zmerge, int n, int T, int t,
+                                                          int64_t tp, int64_t np_, double scale,
+                                                          float *__restrict__ Ua, double *__restrict__ anorm) {
+  constexpr int SQ = kHeadDim + 8;
+  __shared__ __attribute__((aligned(16))) bf16 sQ[64 * SQ];
+  const int b = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int h = lane >> 5, col = lane & 31;
+  const int r = blockIdx.x * 128 + wave * 32 + col;
+  const bool rvalid = r < t;
+  bf16x8 bfr[8];
+  const bf16 *kr = K + ((size_t)b * T + (rvalid ? anchors[(size_t)b * t + r] : 0)) * kHeadDim;
+#pragma unroll
+  for (int ks = 0; ks < 8; ++ks)
+    bfr[ks] = rvalid ? *reinterpret_cast<const bf16x8 *>(kr + ks * 16 + 8 * h) : Mfma<bf16>::zero();
+  const double zm = (double)zmerge[b];
+  const bf16 *Qb = Q + (size_t)b * n * kHeadDim;
+  float *urow = Ua + ((size_t)b * tp + (rvalid ? r : 0)) * np_;
+  double ss = 0.0;
+  for (int i0 = 0; i0 < np_; i0 += 64) {
+    __syncthreads();
+    for (int c = tid; c < 64 * 16; c += 256) {
+      const int rr = c / 16, cc = (c % 16) * 8;
+      f32x4 v = {0.f, 0.f, 0.f, 0.f};
+      if (i0 + rr < n) v = *reinterpret_cast<const f32x4 *>(Qb + (size_t)(i0 + rr) * kHeadDim + cc);
+      *reinterpret_cast<f32x4 *>(&sQ[rr * SQ + cc]) = v;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int ms = 0; ms < 2; ++ms) {
+      f32x16 acc[8];
+      const bf16 *arow = &sQ[(32 * ms + col) * SQ + 8 * h];
+#pragma unroll
+      for (int ks = 0; ks < 8; ++ks)
+        acc[ks] = Mfma<bf16>::mma(*reinterpret_cast<const bf16x8 *>(arow + ks * 16), bfr[ks], zero16());
+      float e[16];
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        double l = 0.0;
+#pragma unroll
+        for (int ks = 0; ks < 8; ++ks) l += (double)acc[ks][v];
+        const int i = i0 + 32 * ms + acc_row(v, lane);
+        const double ev = i < n ? exp_reduced(scale * l - zm) : 0.0;
+        ss = fma(ev, ev, ss);
+        e[v] = (float)ev;
+      }
+      if (rvalid) {
+#pragma unroll
+        for (int g = 0; g < 4; ++g)
+          *reinterpret_cast<f32x4 *>(urow + i0 + 32 * ms + 8 * g + 4 * h) =
+              f32x4{e[4 * g], e[4 * g + 1], e[4 * g + 2], e[4 * g + 3]};
+      }
+    }
+  }
+  ss += __shfl_xor(ss, 32, 64);
+  if (rvalid && h == 0) anorm[(size_t)b * tp + r] = sqrt(ss);
+}
+
+// fp32 inputs: the same profiles with float64 logits and exponentials (one
+// workgroup per anchor, one thread per query).
+__global__ void __launch_bounds__(256) k_prof_anchor_f32(const float *__restrict__ Q, const float *__restrict__ K,
+                                                         const int32_t *__restrict__ anchors,
+                                                         const float *__restrict__ zmerge, int n, int T, int t,
+                                                         int64_t tp, int64_t np_, double scale,
+                                                         float *__restrict__ Ua, double *__restrict__ anorm) {
+  __shared__ double kr[kHeadDim];
+  __shared__ double red[4];
+  const int b = blockIdx.y, r = blockIdx.x, tid = threadIdx.x;
+  if (tid < kHeadDim) kr[tid] = (double)K[((size_t)b * T + anchors[(size_t)b * t + r]) * kHeadDim + tid];
+  __syncthreads();
+  const double zm = (double)zmerge[b];
+  float *urow = Ua + ((size_t)b * tp + r) * np_;
+  double ss = 0.0;
+  for (int64_t i = tid; i < np_; i += 256) {
+    double ev = 0.0;
+    if (i < n) {
+      const float *q = Q + ((size_t)b * n + i) * kHeadDim;
+      double l = 0.0;
+      for (int k = 0; k < kHeadDim; ++k) l = fma((double)q[k], kr[k], l);
+      ev = exp(scale * l - zm);
+    }
+    ss = fma(ev, ev, ss);
+    urow[i] = (float)ev;
+  }
+  ss = wave_sum(ss);
+  if ((tid & 63) == 0) red[tid >> 6] = ss;
+  __syncthreads();
+  if (tid == 0) anorm[(size_t)b * tp + r] = sqrt(red[0] + red[1] + red[2] + red[3]);
+}
+
+// The contraction's anchor operand U [P][tp][np]: Ua / anorm, stored in fp16
+// scaled by 2^15 for bf16 inputs (one rounding of the fp32 product) or in
+// fp32; rows r >= t and columns i >= n are zero.  One wave per row.
+template <typename T>
+__global__ void __launch_bounds__(256) k_anchor_u(const float *__restrict__ Ua, const double *__restrict__ anorm,
+                                                  int n, int t, int64_t tp, int64_t np_, float uscale,
+                                                  T *__restrict__ U) {
+  const int b = blockIdx.y, lane = threadIdx.x & 63;
+  const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (r >= tp) return;
+  T *urow = U + ((size_t)b * tp + r) * np_;
+  const float *arow = Ua + ((size_t)b * tp + r) * np_;
+  const double nr = r < t ? anorm[(size_t)b * tp + r] : 0.0;
+  const float inv = nr > 0.0 ? (float)((double)uscale / nr) : 0.0f;
+  for (int64_t i = lane; i < np_; i += 64) urow[i] = (T)(r < t && i < n ? arow[i] * inv : 0.0f);
+}
+
+// ---------------------------------------------------------------- pass A bounds
+// Relative (eta) and absolute (alpha, in the units of the stored similarity)
+// error bound of one pass-A similarity of key j, whose key has norm kn and mass
+// weight phi.  Every term of S(j, r) = sum_i E_ij U_ir is >= 0, so a relative
+// bound on each term bounds the sum.
+//  bf16 inputs, fp16 operands scaled by 2^15 (S_A = 2^30 S):
+//   E'  logit on MFMA, fp32 accumulation over d: gamma_128 s ||q|| ||k_j||;
+//       exponent argument formed in fp32 and v_exp_f32 (1 ulp); fp16 rounding.
+//   U'  the precise profile (gamma_16 s ||q|| ||k_r|| + 2^-22, stored fp32),
+//       divided by its float64 norm (same bound, unrounded), a fp32 product and
+//       one fp16 rounding.
+//   fp16 x fp16 products are exact in fp32; the fp32 accumulation of n >= 0
+//   terms adds gamma_n.  Operands below the fp16 normal range (E' or U' < 2^-14)
+//   carry an absolute error <= 2^-25 instead: alpha = 2^-25 (||U'_r||_1 + ||E'_j||_1)
+//   <= 2^-10 (sqrt(n) + n phi_j), with ||U_r||_2 = 1.
+//  fp32 inputs: fp32 products are rounded (u each, d + 2 terms in the logit and
+//   one in every product of the contraction); the anchor operand is the float64
+//   profile rounded to fp32 and normalised in fp32.
+struct BoundA {
+  double eta, alpha;
+};
+
+__device__ inline BoundA bound_a(bool bf16in, int n, double s, double zm, const AssignPair &pn, double kn,
+                                 double phi) {
+  const double A = s * pn.qmax * kn * 1.4426950408889634 * 1.001;   // |logit| log2(e) bound of the key
+  BoundA o;
+  if (bf16in) {
+    const double Z = fabs(zm) * 1.4426950408889634 + (double)kProfLog2Scale;
+    const double e_key = gamma_m(kHeadDim) * s * pn.qmax * kn + 0.6931471805599453 * kU32 * (3.0 * A + 4.0 * Z) +
+                         2.0 * kU32;
+    const double e_anc = gamma_m(16) * s * pn.qmax * pn.amax + kExpReducedErr;
+    const double eE = (1.0 + e_key) * (1.0 + kU16) - 1.0;
+    const double eU = (1.0 + e_anc + kU32) / (1.0 - e_anc) * (1.0 + 2.0 * kU32) * (1.0 + kU16) - 1.0;
+    o.eta = (1.0 + eE) * (1.0 + eU) * (1.0 + gamma_m(n)) - 1.0;
+    o.alpha = 9.765625e-04 * 1.01 * (sqrt((double)n) + (double)n * phi * 1.001) + (double)n * 1e-18;
+  } else {
+    const double Z = fabs(zm) * 1.4426950408889634;
+    const double e_key = gamma_m(kHeadDim + 2) * s * pn.qmax * kn +
+                         0.6931471805599453 * kU32 * (3.0 * A + 4.0 * Z) + 2.0 * kU32;
+    const double eU = 3.0 * kU32 + 1e-14;
+    o.eta = (1.0 + e_key) * (1.0 + eU) * (1.0 + kU32) * (1.0 + gamma_m(n)) - 1.0;
+    o.alpha = (double)n * 1e-36;
+  }
+  return o;
+}
+
+__device__ inline float threshold_a(float s1, const BoundA &bd) {
+  const double th = ((double)s1 - bd.alpha) * (1.0 - bd.eta) / (1.0 + bd.eta) - bd.alpha;
+  // round down so that a similarity equal to the exact threshold is kept
+  return (float)th - fabsf((float)th) * 1.2e-7f - 1e-37f;
+}
+
+template <typename E>
+__device__ inline double row_norm(const E *x) {
+  double ss = 0.0;
+  for (int k = 0; k < kHeadDim; ++k) {
+    const double v = (double)(float)x[k];
+    ss = fma(v, v, ss);
+  }
+  return sqrt(ss) * (1.0 + 1e-12);
+}
+
+// Candidate anchors of one key after pass A.  For each anchor tile the best
+// two above the threshold are candidates; a tile whose third value reaches the
+// threshold may hold more, and contributes all its anchors ("overflow").
+struct CandA {
+  int singles, overflow;
+  float th;
+  uint64_t g1;
+};
+
+__device__ inline CandA cand_a(const uint64_t *p1, const uint64_t *p2, const uint32_t *p3, int64_t stride, int MT,
+                               int t, float th_or_nan, uint64_t g1) {
+  CandA c;
+  c.g1 = g1;
+  c.th = th_or_nan;
+  c.singles = 0;
+  c.overflow = 0;
+  for (int mt = 0; mt < MT; ++mt) {
+    const uint64_t a = p1[(size_t)mt * stride], b2 = p2[(size_t)mt * stride];
+    const float v3 = __uint_as_float(p3[(size_t)mt * stride]);
+    if (v3 >= c.th) {
+      ++c.overflow;
+      continue;
+    }
+    if (a != 0ull && packed_r(a) < (uint32_t)t && packed_sim(a) >= c.th) ++c.singles;
+    if (b2 != 0ull && packed_r(b2) < (uint32_t)t && packed_sim(b2) >= c.th) ++c.singles;
+  }
+  return c;
+}
+
+__device__ inline void push_d(const AssignLists &L, int b, int j, const int32_t *ent, int k) {
+  const int slot = atomicAdd(&L.dcnt[b], 1);
+  L.dkey[(size_t)b * L.cap + slot] = j;
+  L.dn[(size_t)b * L.cap + slot] = k;
+  for (int e = 0; e < k; ++e) L.dent[((size_t)b * L.cap + slot) * kAssignMaxD + e] = ent[e];
+  atomicAdd(&L.stats[b * kAssignStats + 1], 1);
+}
+
+// Pass A decision, one thread per position j: anchors map to themselves
+// (eq. anchor_assignment); a key with one candidate takes it; the others take
+// the pass-A best for now, and their candidates go to the pair's pool for
+// pass C.  Anchor tiles have TR rows.
+template <typename E>
+__global__ void __launch_bounds__(256) k_assign_finalize(
+    const uint64_t *__restrict__ part1, const uint64_t *__restrict__ part2, const uint32_t *__restrict__ part3,
+    int MT, int64_t Np, const int32_t *__restrict__ anchors, const E *__restrict__ K, const float *__restrict__ phi,
+    const float *__restrict__ zmerge, const AssignPair *__restrict__ pn, int T, int t, int n, int TR, double s,
+    int32_t *__restrict__ kappa, AssignLists L) {
+  const int b = blockIdx.y;
+  const int j = blockIdx.x * 256 + threadIdx.x;
+  if (j >= T) return;
+  const int32_t *S = anchors + (size_t)b * t;
+  int lo = 0, hi = t;   // lo = #{anchors < j}
+  while (lo < hi) {
+    const int mid = (lo + hi) >> 1;
+    if (S[mid] < j) lo = mid + 1;
+    else hi = mid;
+  }
+  if (lo < t && S[lo] == j) {
+    kappa[(size_t)b * T + j] = lo;
+    return;
+  }
+  const size_t c = (size_t)b * MT * Np + (size_t)(j - lo);
+  const uint64_t *p1 = part1 + c, *p2 = part2 + c;
+  const uint32_t *p3 = part3 + c;
+  uint64_t g1 = 0;
+  for (int mt = 0; mt < MT; ++mt) g1 = max(g1, p1[(size_t)mt * Np]);
+  const uint32_t r1 = packed_r(g1);
+  const double kn = row_norm(K + ((size_t)b * T + j) * kHeadDim);
+  const BoundA bd = bound_a(sizeof(E) == 2, n, s, (double)zmerge[b], pn[b], kn, (double)phi[(size_t)b * T + j]);
+  const float th = threshold_a(packed_sim(g1), bd);
+  const CandA ca = cand_a(p1, p2, p3, Np, MT, t, th, g1);
+  kappa[(size_t)b * T + j] = (int32_t)(r1 < (uint32_t)t ? r1 : 0u);
+  if (ca.overflow == 0 && ca.singles == 1) return;
+  int32_t *st = L.stats + (size_t)b * kAssignStats;
+  atomicAdd(&st[0], 1);
+  if (ca.overflow) atomicAdd(&st[7], 1);
+  // the key's candidates: the best two above the threshold of each tile, or
+  // every anchor of a tile whose third value reaches it
+  int nc = 0;
+  for (int mt = 0; mt < MT; ++mt) {
+    if (__uint_as_float(p3[(size_t)mt * Np]) >= th) {
+      nc += min(t, (mt + 1) * TR) - mt * TR;
+      continue;
+    }
+    const uint64_t a = p1[(size_t)mt * Np], a2 = p2[(size_t)mt * Np];
+    nc += (a != 0ull && packed_r(a) < (uint32_t)t && packed_sim(a) >= th);
+    nc += (a2 != 0ull && packed_r(a2) < (uint32_t)t && packed_sim(a2) >= th);
+  }
+  atomicAdd(&st[2], nc);
+  if (nc == 0) {   // no finite similarity reaches the threshold (non-finite input): the pass-A best stands
+    atomicAdd(&st[3], 1);
+    atomicAdd(&st[4], 1);
+    return;
+  }
+  const int off = atomicAdd(&L.pcnt[b], nc);
+  if ((int64_t)off + nc > L.pcap) {   // pool full: the key keeps its pass-A best
+    atomicAdd(&st[3], 1);
+    atomicAdd(&st[4], 1);
+    return;
+  }
+  int32_t *pl = L.pool + (size_t)b * L.pcap + off;
+  int k = 0;
+  for (int mt = 0; mt < MT; ++mt) {
+    if (__uint_as_float(p3[(size_t)mt * Np]) >= th) {
+      for (int r = mt * TR; r < min(t, (mt + 1) * TR); ++r) pl[k++] = r;
+      continue;
+    }
+    const uint64_t a = p1[(size_t)mt * Np], a2 = p2[(size_t)mt * Np];
+    if (a != 0ull && packed_r(a) < (uint32_t)t && packed_sim(a) >= th) pl[k++] = (int32_t)packed_r(a);
+    if (a2 != 0ull && packed_r(a2) < (uint32_t)t && packed_sim(a2) >= th) pl[k++] = (int32_t)packed_r(a2);
+  }
+  const int slot = atomicAdd(&L.fcnt[b], 1);
+  L.fkey[(size_t)b * L.cap + slot] = j;
+  L.foff[(size_t)b * L.cap + slot] = off;
+  L.fn[(size_t)b * L.cap + slot] = nc;
+  atomicAdd(&st[6], 1);
+}
+
+// ---------------------------------------------------------------- pass C
+// Refine the keys queued by pass A.  A workgroup takes 64 queued keys of one
+// pair and their candidates from the pool, in chunks of CAP.  For every query
+// tile of 64 the keys' profiles are formed and staged in LDS as fp32; each
+// candidate pair accumulates sum_i e_ij e_ir in float64 against the anchor's
+// stored profile, and the similarity e_j . e_r / ||e_r|| goes back to the pool.
+//  bf16 inputs: logits on MFMA as in k_prof_anchor_bf16 (one accumulator per
+//   16-wide slice, summed in float64; exponentials within 2^-22).  Bound of one
+//   similarity: (1 + eps_k)(1 + eps_a)/(1 - eps_n) - 1 with eps_k = gamma_16 s
+//   ||q|| ||k_j|| + 2^-22 + u (fp32 staging), eps_a = gamma_16 s ||q|| max ||k_r||
+//   + 2^-22 + u, eps_n the same without the staging term.
+//  fp32 inputs: float64 logits and exponentials; the bound is the fp32
+//   rounding of the staged and stored profiles.
+// A key whose best similarity exceeds every other candidate's by more than the
+// bound on both is decided; the survivors of the others go to pass D.
+// Work distribution: a fixed grid of kRefineBlocks workgroups per pair, each
+// taking the groups of 64 queued keys g = blockIdx.x, blockIdx.x + kRefineBlocks, ...
+// A candidate's dot product is split over 16 lanes that read 16-byte pieces of
+// one anchor row (256 contiguous bytes per query tile) and reduce at the end.
+constexpr int kRefineBlocks = 32;
+
+template <typename E>
+__global__ void __launch_bounds__(256) k_assign_refine(const E *__restrict__ Q, const E *__restrict__ K,
+                                                       const float *__restrict__ zmerge,
+                                                       const AssignPair *__restrict__ pn,
+                                                       const float *__restrict__ Ua, const double *__restrict__ anorm,
+                                                       int T, int t, int n, int64_t tp, int64_t np_, double s,
+                                                       int32_t *__restrict__ kappa, AssignLists L) {
+  constexpr bool BF = sizeof(E) == 2;
+  constexpr int NK = 64, CAP = 256, NSLOT = CAP / 16, SE = 64 + 4, SQF = kHeadDim + 4;
+  __shared__ int32_t kpos[NK], koff[NK], kbase[NK + 1];
+  __shared__ int32_t cr[CAP];
+  __shared__ uint8_t ck[CAP];
+  __shared__ double kn[NK];
+  __shared__ __attribute__((aligned(16))) float eT[NK * SE];
+  __shared__ __attribute__((aligned(16))) float sQf[BF ? 4 : 64 * SQF];   // fp32 inputs: the query tile
+  const int b = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int h = lane >> 5, col = lane & 31;
+  const int gid = tid >> 4, li = tid & 15;   // candidate lane group and lane within it
+  const int F = L.fcnt[b];
+  const AssignPair pp = pn[b];
+  const double zm = (double)zmerge[b];
+  const E *Qb = Q + (size_t)b * n * kHeadDim;
+  const float *Uab = Ua + (size_t)b * tp * np_;
+  int32_t *pool = L.pool + (size_t)b * L.pcap;
+  double *psim = L.psim + (size_t)b * L.pcap;
+  const int kb = 32 * (wave & 1), qb = 32 * (wave >> 1);   // MFMA tile: keys kb.., queries qb.. of a query tile
+  for (int f0 = blockIdx.x * NK; f0 < F; f0 += kRefineBlocks * NK) {   // uniform over the workgroup
+    const int nk = min(NK, F - f0);
+    __syncthreads();   // the previous group is done with the shared arrays
+    if (tid < NK) {
+      kpos[tid] = -1;
+      koff[tid] = 0;
+      if (tid < nk) {
+        const size_t q = (size_t)b * L.cap + f0 + tid;
+        kpos[tid] = L.fkey[q];
+        koff[tid] = L.foff[q];
+        kn[tid] = row_norm(K + ((size_t)b * T + kpos[tid]) * kHeadDim);
+      }
+    }
+    __syncthreads();
+    if (tid == 0) {
+      int acc = 0;
+      for (int k = 0; k < NK; ++k) {
+        kbase[k] = acc;
+        acc += k < nk ? L.fn[(size_t)b * L.cap + f0 + k] : 0;
+      }
+      kbase[NK] = acc;
+    }
+    __syncthreads();
+    const int total = kbase[NK];
+    const int kp = kpos[kb + col];
+    const E *krow = K + ((size_t)b * T + (kp >= 0 ? kp : 0)) * kHeadDim;
+    bf16x8 bfr[8];
+    if constexpr (BF) {
+#pragma unroll
+      for (int ks = 0; ks < 8; ++ks)
+        bfr[ks] = kp >= 0 ? *reinterpret_cast<const bf16x8 *>(reinterpret_cast<const bf16 *>(krow) + ks * 16 + 8 * h)
+                          : Mfma<bf16>::zero();
+    }
+    for (int c0 = 0; c0 < total; c0 += CAP) {
+      const int cn = min(CAP, total - c0);
+      __syncthreads();   // the previous chunk is done with cr / ck
+      for (int c = tid; c < cn; c += 256) {
+        const int g = c0 + c;
+        int lo = 0, hi = NK;   // the key k with kbase[k] <= g < kbase[k + 1]
+        while (hi - lo > 1) {
+          const int mid = (lo + hi) >> 1;
+          if (kbase[mid] <= g) lo = mid;
+          else hi = mid;
+        }
+        ck[c] = (uint8_t)lo;
+        cr[c] = pool[koff[lo] + g - kbase[lo]];
+      }
+      double dacc[NSLOT];
+#pragma unroll
+      for (int u = 0; u < NSLOT; ++u) dacc[u] = 0.0;
+      for (int i0 = 0; i0 < np_; i0 += 64) {
+        double l[16];
+        if constexpr (BF) {
+          const int iq = i0 + qb + col;
+          bf16x8 afr[8];
+#pragma unroll
+          for (int ks = 0; ks < 8; ++ks)
+            afr[ks] = iq < n ? *reinterpret_cast<const bf16x8 *>(reinterpret_cast<const bf16 *>(Qb) +
+                                                                 (size_t)iq * kHeadDim + ks * 16 + 8 * h)
+                             : Mfma<bf16>::zero();
+          f32x16 acc[8];
+#pragma unroll
+          for (int ks = 0; ks < 8; ++ks) acc[ks] = Mfma<bf16>::mma(afr[ks], bfr[ks], zero16());
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            double x = 0.0;
+#pragma unroll
+            for (int ks = 0; ks < 8; ++ks) x += (double)acc[ks][v];
+            l[v] = x;
+          }
+          __syncthreads();   // the previous tile's dot products are done with eT
+        } else {
+          __syncthreads();   // the previous tile is done with sQf and eT
+          for (int x = tid; x < 64 * kHeadDim; x += 256) {
+            const int rr = x / kHeadDim, cc = x % kHeadDim;
+            sQf[rr * SQF + cc] = i0 + rr < n ? (float)Qb[(size_t)(i0 + rr) * kHeadDim + cc] : 0.0f;
+          }
+          __syncthreads();
+#pragma unroll
+          for (int v = 0; v < 16; ++v) l[v] = 0.0;
+          for (int k = 0; k < kHeadDim; k += 4) {
+            const f32x4 kv = *reinterpret_cast<const f32x4 *>(reinterpret_cast<const float *>(krow) + k);
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+              const f32x4 qv = *reinterpret_cast<const f32x4 *>(&sQf[(qb + acc_row(v, lane)) * SQF + k]);
+#pragma unroll
+              for (int e = 0; e < 4; ++e) l[v] = fma((double)qv[e], (double)kv[e], l[v]);
+            }
+          }
+        }
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int qi = qb + acc_row(v, lane);
+          float ev = 0.0f;
+          if (i0 + qi < n) ev = BF ? (float)exp_reduced(s * l[v] - zm) : (float)exp(s * l[v] - zm);
+          eT[(kb + col) * SE + qi] = ev;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int u = 0; u < NSLOT; ++u) {
+          const int c = u * 16 + gid;
+          if (c < cn) {
+            const f32x4 e4 = *reinterpret_cast<const f32x4 *>(&eT[(int)ck[c] * SE + 4 * li]);
+            const f32x4 w = *reinterpret_cast<const f32x4 *>(Uab + (size_t)cr[c] * np_ + i0 + 4 * li);
+            double d = dacc[u];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) d = fma((double)e4[e], (double)w[e], d);
+            dacc[u] = d;
+          }
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < NSLOT; ++u) {
+        double d = dacc[u];
+        for (int m = 8; m >= 1; m >>= 1) d += __shfl_xor(d, m, 64);
+        const int c = u * 16 + gid;
+        if (li == 0 && c < cn) {
+          const int k = ck[c];
+          psim[koff[k] + c0 + c - kbase[k]] = d / anorm[(size_t)b * tp + cr[c]];
+        }
+      }
+    }
+    __syncthreads();   // every similarity of the group's keys is in the pool
+    if (tid < nk && kbase[tid + 1] > kbase[tid]) {
+      const int j = kpos[tid], o = koff[tid], m = kbase[tid + 1] - kbase[tid];
+      int best = 0;
+      for (int c = 1; c < m; ++c)
+        if (psim[o + c] > psim[o + best] || (psim[o + c] == psim[o + best] && pool[o + c] < pool[o + best]))
+          best = c;
+      double eta;
+      if constexpr (BF) {
+        const double g16 = gamma_m(16) * s * pp.qmax;
+        const double ek = g16 * kn[tid] + kExpReducedErr + kU32;
+        const double ea = g16 * pp.amax + kExpReducedErr + kU32;
+        const double en = g16 * pp.amax + kExpReducedErr;
+        eta = (1.0 + ek) * (1.0 + ea) / (1.0 - en) * (1.0 + 1e-12) - 1.0;
+      } else {
+        eta = 2.0 * kU32 + 1e-12;
+      }
+      const double bs = psim[o + best];
+      const double thc = bs * (1.0 - eta) / (1.0 + eta) - 1e-300;
+      int32_t surv[kAssignMaxD];
+      int ns = 0;
+      bool over = false;
+      for (int c = 0; c < m; ++c)
+        if (psim[o + c] >= thc) {
+          if (ns == kAssignMaxD) over = true;
+          else surv[ns++] = pool[o + c];
+        }
+      kappa[(size_t)b * T + j] = pool[o + best];
+      if (over) {   // (equal similarities of duplicate anchors) the lowest r among the largest stands
+        atomicAdd(&L.stats[b * kAssignStats + 3], 1);
+        atomicAdd(&L.stats[b * kAssignStats + 5], 1);
+      } else if (ns > 1) {
+        push_d(L, b, j, surv, ns);
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------- pass D
+// Float64 decision for the remaining keys: logits as float64 sums of exact
+// products, exp in float64, norms and dot products in float64; the largest
+// similarity wins and equal ones go to the lower r.  A key's entries are the
+// anchors that survived pass C.  A fixed grid of kExactBlocks workgroups per
+// pair takes groups of kExactGroup queued keys (group g = blockIdx.x,
+// blockIdx.x + kExactBlocks, ...); a group's keys and candidate anchors (up to
+// 32 vectors) share one sweep over the queries in tiles of 32, and a key with
+// more candidates than fit continues in the next sweep.
+constexpr int kExactBlocks = 64, kExactGroup = 8;
+
+template <typename E>
+__global__ void __launch_bounds__(256) k_assign_exact(const E *__restrict__ Q, const E *__restrict__ K,
+                                                      const int32_t *__restrict__ anchors,
+                                                      const float *__restrict__ zmerge, int T, int t, int n, double s,
+                                                      int32_t *__restrict__ kappa, AssignLists L) {
+  constexpr int NV = 32, NQ = 32, SK = kHeadDim + 1;
+  __shared__ float sK[NV * SK];
+  __shared__ float sQ[NQ * SK];
+  __shared__ double sE[NV * (NQ + 1)];
+  __shared__ int32_t vpos[NV], vown[NV], vr[NV];
+  __shared__ double vdot[NV], vnn[NV];
+  // batch segments: first and one-past-last vector, continues, final
+  __shared__ int32_t sg_v0[NV], sg_v1[NV], sg_cont[NV], sg_final[NV];
+  __shared__ int32_t nv_s, nseg_s, di_s, ci_s, done_s;
+  __shared__ double run_sim;
+  __shared__ int32_t run_r;
+  const int b = blockIdx.y, tid = threadIdx.x;
+  const int D = L.dcnt[b];
+  const int32_t *S = anchors + (size_t)b * t;
+  const double zm = (double)zmerge[b];
+  const E *Qb = Q + (size_t)b * n * kHeadDim;
+  auto n_cand = [&](int di) { return L.dn[(size_t)b * L.cap + di]; };
+  auto cand_at = [&](int di, int ci) { return L.dent[((size_t)b * L.cap + di) * kAssignMaxD + ci]; };
+  // register tile of the logit pass: vectors tv, tv + 16 and queries tq, tq + 16
+  const int tv = tid >> 4, tq = tid & 15;
+  for (int g0 = blockIdx.x * kExactGroup; g0 < D; g0 += kExactBlocks * kExactGroup) {
+    const int g1 = min(D, g0 + kExactGroup);
+    __syncthreads();   // every thread has left the previous group's loop
+    if (tid == 0) {
+      di_s = g0;
+      ci_s = 0;
+      done_s = 0;
+    }
+    __syncthreads();
+    while (!done_s) {
+      if (tid == 0) {   // build the next batch from keys di_s .. g1 - 1
+        int nv = 0, ns = 0, di = di_s, ci = ci_s;
+        while (di < g1 && nv + 2 <= NV) {
+          const int nck = n_cand(di);
+          sg_cont[ns] = ci > 0;
+          sg_v0[ns] = nv;
+          vpos[nv] = L.dkey[(size_t)b * L.cap + di];
+          vown[nv] = -1;
+          vr[nv] = -1;
+          const int kv = nv++;
+          while (nv < NV && ci < nck) {
+            const int r = cand_at(di, ci++);
+            vpos[nv] = S[r];
+            vown[nv] = kv;
+            vr[nv] = r;
+            ++nv;
+          }
+          sg_v1[ns] = nv;
+          sg_final[ns] = ci >= nck;
+          ++ns;
+          if (ci >= nck) {
+            ++di;
+            ci = 0;
+          }
+        }
+        nv_s = nv;
+        nseg_s = ns;
+        di_s = di;
+        ci_s = ci;
+      }
+      __syncthreads();
+      const int nv = nv_s;
+      for (int x = tid; x < NV * kHeadDim; x += 256) {
+        const int v = x / kHeadDim, k = x % kHeadDim;
+        sK[v * SK + k] = v < nv ? (float)K[((size_t)b * T + vpos[v]) * kHeadDim + k] : 0.0f;
+      }
+      if (tid < NV) {
+        vdot[tid] = 0.0;
+        vnn[tid] = 0.0;
+      }
+      for (int i0 = 0; i0 < n; i0 += NQ) {
+        __syncthreads();
+        for (int x = tid; x < NQ * kHeadDim; x += 256) {
+          const int q = x / kHeadDim, k = x % kHeadDim;
+          sQ[q * SK + k] = i0 + q < n ? (float)Qb[(size_t)(i0 + q) * kHeadDim + k] : 0.0f;
+        }
+        __syncthreads();
+        double l00 = 0.0, l01 = 0.0, l10 = 0.0, l11 = 0.0;
+        for (int k = 0; k < kHeadDim; ++k) {
+          const double a0 = (double)sK[tv * SK + k], a1 = (double)sK[(tv + 16) * SK + k];
+          const double q0 = (double)sQ[tq * SK + k], q1 = (double)sQ[(tq + 16) * SK + k];
+          l00 = fma(a0, q0, l00);
+          l01 = fma(a0, q1, l01);
+          l10 = fma(a1, q0, l10);
+          l11 = fma(a1, q1, l11);
+        }
+        const bool in0 = i0 + tq < n, in1 = i0 + tq + 16 < n;
+        sE[tv * (NQ + 1) + tq] = tv < nv && in0 ? exp(s * l00 - zm) : 0.0;
+        sE[tv * (NQ + 1) + tq + 16] = tv < nv && in1 ? exp(s * l01 - zm) : 0.0;
+        sE[(tv + 16) * (NQ + 1) + tq] = tv + 16 < nv && in0 ? exp(s * l10 - zm) : 0.0;
+        sE[(tv + 16) * (NQ + 1) + tq + 16] = tv + 16 < nv && in1 ? exp(s * l11 - zm) : 0.0;
+        __syncthreads();
+        if (tid < nv && vown[tid] >= 0) {
+          const int o = vown[tid];
+          double d = vdot[tid], nn = vnn[tid];
+          for (int q = 0; q < NQ; ++q) {
+            const double ev = sE[tid * (NQ + 1) + q];
+            d = fma(sE[o * (NQ + 1) + q], ev, d);
+            nn = fma(ev, ev, nn);
+          }
+          vdot[tid] = d;
+          vnn[tid] = nn;
+        }
+      }
+      __syncthreads();
+      if (tid == 0) {
+        for (int g = 0; g < nseg_s; ++g) {
+          double bs = sg_cont[g] ? run_sim : -1.0;
+          int br = sg_cont[g] ? run_r : 0x7FFFFFFF;
+          for (int v = sg_v0[g] + 1; v < sg_v1[g]; ++v) {
+            const double sim = vnn[v] > 0.0 ? vdot[v] / sqrt(vnn[v]) : 0.0;
+            if (sim > bs || (sim == bs && vr[v] < br)) {
+              bs = sim;
+              br = vr[v];
+            }
+          }
+          if (sg_final[g] && br != 0x7FFFFFFF) kappa[(size_t)b * T + vpos[sg_v0[g]]] = br;
+          else {
+            run_sim = bs;
+            run_r = br;
+          }
+        }
+        done_s = di_s >= g1;
+      }
+      __syncthreads();
+    }
+  }
+}
+
+// ---------------------------------------------------------------- launchers
+hipError_t launch_pair_norms(int dtype, const void *Q, const void *K, const int32_t *anchors, int P, int n, int T,
+                             int t, void *pn, hipStream_t s) {
+  if (dtype == ARCKV_BF16)
+    hipLaunchKernelGGL(k_pair_norms<bf16>, dim3(P), dim3(256), 0, s, (const bf16 *)Q, (const bf16 *)K, anchors, n,
+                       T, t, (AssignPair *)pn);
+  else
+    hipLaunchKernelGGL(k_pair_norms<float>, dim3(P), dim3(256), 0, s, (const float *)Q, (const float *)K, anchors,
+                       n, T, t, (AssignPair *)pn);
+  return hipGetLastError();
+}
+
+hipError_t launch_anchor_profiles(int dtype, const void *Q, const void *K, const int32_t *anchors,
+                                  const float *zmerge, int P, int n, int T, int t, int64_t tp, int64_t np_,
+                                  float scale, float *Ua, double *anorm, void *U, hipStream_t s) {
+  if (dtype == ARCKV_BF16) {
+    hipLaunchKernelGGL(k_prof_anchor_bf16, dim3((unsigned)((t + 127) / 128), P), dim3(256), 0, s, (const bf16 *)Q,
+                       (const bf16 *)K, anchors, zmerge, n, T, t, tp, np_, (double)scale, Ua, anorm);
+    if (hipGetLastError() != hipSuccess) return hipErrorLaunchFailure;
+    hipLaunchKernelGGL(k_anchor_u<f16>, dim3((unsigned)(tp / 4), P), dim3(256), 0, s, (const float *)Ua,
+                       (const double *)anorm, n, t, tp, np_, kProfScale, (f16 *)U);
+  } else {
+    hipLaunchKernelGGL(k_prof_anchor_f32, dim3((unsigned)t, P), dim3(256), 0, s, (const float *)Q, (const float *)K,
+                       anchors, zmerge, n, T, t, tp, np_, (double)scale, Ua, anorm);
+    if (hipGetLastError() != hipSuccess) return hipErrorLaunchFailure;
+    hipLaunchKernelGGL(k_anchor_u<float>, dim3((unsigned)(tp / 4), P), dim3(256), 0, s, (const float *)Ua,
+                       (const double *)anorm, n, t, tp, np_, 1.0f, (float *)U);
+  }
+  return hipGetLastError();
+}
+
+__global__ void k_fill_i32(int32_t *p, int64_t count, int32_t v) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i < count) p[i] = v;
+}
+
+hipError_t launch_fill_i32(int32_t *p, int64_t count, int32_t v, hipStream_t s) {
+  if (count <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_fill_i32, dim3((unsigned)((count + 255) / 256)), dim3(256), 0, s, p, count, v);
+  return hipGetLastError();
+}
+
+// Pass A decision (clears the counters first).  MT anchor tiles of TR rows;
+// Np = the partials' row stride (compacted key columns).
+hipError_t launch_assign_finalize(int dtype, const void *K, const uint64_t *part1, const uint64_t *part2,
+                                  const uint32_t *part3, int MT, int TR, int64_t Np, const int32_t *anchors,
+                                  const float *phi, const float *zmerge, const void *pn, int P, int T, int t, int n,
+                                  float scale, int32_t *kappa, const AssignLists &L, hipStream_t s) {
+  hipError_t e = launch_fill_i32(L.fcnt, P, 0, s);
+  if (e == hipSuccess) e = launch_fill_i32(L.dcnt, P, 0, s);
+  if (e == hipSuccess) e = launch_fill_i32(L.pcnt, P, 0, s);
+  if (e == hipSuccess) e = launch_fill_i32(L.stats, (int64_t)P * kAssignStats, 0, s);
+  if (e != hipSuccess) return e;
+  const dim3 gf((unsigned)((T + 255) / 256), P);
+  if (dtype == ARCKV_BF16)
+    hipLaunchKernelGGL(k_assign_finalize<bf16>, gf, dim3(256), 0, s, part1, part2, part3, MT, Np, anchors,
+                       (const bf16 *)K, phi, zmerge, (const AssignPair *)pn, T, t, n, TR, (double)scale, kappa, L);
+  else
+    hipLaunchKernelGGL(k_assign_finalize<float>, gf, dim3(256), 0, s, part1, part2, part3, MT, Np, anchors,
+                       (const float *)K, phi, zmerge, (const AssignPair *)pn, T, t, n, TR, (double)scale, kappa, L);
+  return hipGetLastError();
+}
+
+// Pass C (a grid of early exits where nothing is queued).
+hipError_t launch_assign_refine(int dtype, const void *Q, const void *K, const float *zmerge, const void *pn,
+                                const float *Ua, const double *anorm, int P, int T, int t, int n, int64_t tp,
+                                int64_t np_, float scale, int32_t *kappa, const AssignLists &L, hipStream_t s) {
+  if (T - t <= 0) return hipSuccess;
+  const dim3 g(kRefineBlocks, P);
+  if (dtype == ARCKV_BF16)
+    hipLaunchKernelGGL(k_assign_refine<bf16>, g, dim3(256), 0, s, (const bf16 *)Q, (const bf16 *)K, zmerge,
+                       (const AssignPair *)pn, Ua, anorm, T, t, n, tp, np_, (double)scale, kappa, L);
+  else
+    hipLaunchKernelGGL(k_assign_refine<float>, g, dim3(256), 0, s, (const float *)Q, (const float *)K, zmerge,
+                       (const AssignPair *)pn, Ua, anorm, T, t, n, tp, np_, (double)scale, kappa, L);
+  return hipGetLastError();
+}
+
+// Pass D.
+hipError_t launch_assign_exact(int dtype, const void *Q, const void *K, const int32_t *anchors, const float *zmerge,
+                               int P, int T, int t, int n, float scale, int32_t *kappa, const AssignLists &L,
+                               hipStream_t s) {
+  if (dtype == ARCKV_BF16)
+    hipLaunchKernelGGL(k_assign_exact<bf16>, dim3(kExactBlocks, P), dim3(256), 0, s, (const bf16 *)Q, (const bf16 *)K, anchors,
+                       zmerge, T, t, n, (double)scale, kappa, L);
+  else
+    hipLaunchKernelGGL(k_assign_exact<float>, dim3(kExactBlocks, P), dim3(256), 0, s, (const float *)Q, (const float *)K, anchors,
+                       zmerge, T, t, n, (double)scale, kappa, L);
+  return hipGetLastError();
+}
+
+}  // namespace arckv

@@ -1,0 +1,31 @@
+// Work lists of the certified key-to-anchor assignment (assign.hip), shared by
+// the kernels and the host-side stage sequencing.  All pointers are device
+// arrays for one chunk of P pairs.
+#pragma once
+#include <stdint.h>
+
+namespace arckv {
+
+constexpr int kAssignStats = 8;
+
+struct AssignLists {
+  int32_t *fcnt;    // [P] keys queued for the refine pass
+  int32_t *fkey;    // [P][cap]
+  int32_t *foff;    // [P][cap] first candidate of the queued key in the pool
+  int32_t *fn;      // [P][cap] its number of candidates
+  int32_t *pcnt;    // [P] candidates in the pool
+  int32_t *pool;    // [P][pcap] candidate anchors, contiguous per queued key
+  double *psim;     // [P][pcap] their refined similarities
+  int64_t pcap;     // pool capacity per pair
+  int32_t *dcnt;    // [P] keys queued for the float64 pass
+  int32_t *dkey;    // [P][cap]
+  int32_t *dn;      // [P][cap] entries per queued key
+  int32_t *dent;    // [P][cap][16] entries: anchor r >= 0, or -(tile + 1) for a whole anchor tile
+  int32_t *stats;   // [P][kAssignStats] (assign.hip): flagged after the first pass, sent to the float64
+                    // pass, candidates of the flagged keys, undecided (sum of the next two), undecided
+                    // in the first pass, undecided in the refine pass, sent to the refine pass, keys
+                    // whose pass-A candidates include a whole anchor tile
+  int64_t cap;      // key capacity per pair
+};
+
+}  // namespace arckv

@@ -2,12 +2,13 @@
 // so that the later contractions over queries read both operands K-contiguous.
 //
 // MODE_PROFILE (Section 3.4, eq. response_profile / mass_centroid):
-//   E^T[j][i] = exp(s q_i.k_j - z_merge) for every cached key j,
-//   phi_j = (1/n) sum_i E[i][j].
-//   Rows are routed by key: an anchor s_r writes its (unnormalised) profile to
-//   row r of U and the sum of squares of the stored values to ssq[r]; every
-//   other key j writes to row j - #{anchors < j} of the compacted E^T, so the
-//   assignment contraction runs over the T - t non-anchor keys only.
+//   E^T[j][i] = exp(s q_i.k_j - z_merge) for every cached key j that is not an
+//   anchor, phi_j = (1/n) sum_i E[i][j] for every key.  Non-anchor key j writes
+//   row j - #{anchors < j} of the compacted E^T, so the assignment contraction
+//   runs over the T - t non-anchor keys only.  For bf16 inputs E^T is stored in
+//   fp16 scaled by 2^15 (kProfScale; a power of two, so the scaling is exact and
+//   the fp16 normal range covers E >= 2^-29); for fp32 inputs in fp32.  The
+//   anchors' own profiles come from the precise anchor-profile pass.
 // MODE_PHIC (Appendix A.9):
 //   L^T[r][i]   = s q_i.c_r            (logits of the compact keys, fp32)
 //   Phi^T[r][i] = exp(L - z_i)         (z_i: full-cache row maxima)
@@ -55,7 +56,7 @@ __global__ void __launch_bounds__(256) k_expgen(const T *__restrict__ Q, const v
   const T *Qb = Q + (size_t)b * n * kHeadDim;
   const float c2 = scale * 1.4426950408889634f;
   const float zshift = (MODE == MODE_PROFILE) ? shift[b] : 0.0f;
-  float rowsum = 0.0f, sumsq = 0.0f;
+  float rowsum = 0.0f;
   double hsum = 0.0;   // PHIC: h_r = sum_i Phi[i][r] m_i (when hout is given)
   // PROFILE destination of this lane's key: >= 0 compacted E^T row, <= -2
   // anchor -(r + 2), -1 none (padding key)
@@ -73,10 +74,8 @@ __global__ void __launch_bounds__(256) k_expgen(const T *__restrict__ Q, const v
   // base pointer of staged row rr of this wave (MODE_PROFILE), or null
   auto row_dst = [&](int rr, int i0) -> T * {
     const int d = __shfl(dest, rr, 64);
-    if (d == -1) return nullptr;
-    T *base = d >= 0 ? reinterpret_cast<T *>(out) + (size_t)b * out_pair_stride + (size_t)d * n_pad
-                     : reinterpret_cast<T *>(uout) + ((size_t)b * tp + (size_t)(-d - 2)) * n_pad;
-    return base + i0;
+    if (d < 0) return nullptr;   // padding key or anchor: nothing stored
+    return reinterpret_cast<T *>(out) + (size_t)b * out_pair_stride + (size_t)d * n_pad + i0;
   };
 
   // Output tiles (this wave's 32 rows x 64 queries) are staged in LDS so that
@@ -147,8 +146,6 @@ __global__ void __launch_bounds__(256) k_expgen(const T *__restrict__ Q, const v
         if (MODE == MODE_PROFILE) {
           val[ms][vv] = ok ? exp2f(acc[vv] * c2 - zshift * 1.4426950408889634f) : 0.0f;
           rowsum += val[ms][vv];
-          const float stored = sizeof(T) == 2 ? (float)(bf16)val[ms][vv] : val[ms][vv];
-          sumsq = fmaf(stored, stored, sumsq);
           lg[ms][vv] = 0.0f;
         } else {
           lg[ms][vv] = ok ? acc[vv] * scale : 0.0f;
@@ -174,9 +171,7 @@ __global__ void __launch_bounds__(256) k_expgen(const T *__restrict__ Q, const v
   }
   if (MODE == MODE_PROFILE) {
     rowsum += __shfl_xor(rowsum, 32, 64);
-    sumsq += __shfl_xor(sumsq, 32, 64);
     if (h == 0 && rvalid) aux[(size_t)b * aux_pair_stride + row] = rowsum / (float)n;
-    if (h == 0 && dest <= -2) ssq[(size_t)b * tp + (-dest - 2)] = sumsq;
   }
   if (MODE == MODE_PHIC && hout) {
     hsum += __shfl_xor(hsum, 32, 64);
@@ -246,13 +241,15 @@ __global__ void __launch_bounds__(256, 2) k_expgen_bf16(const bf16 *__restrict__
                          : Mfma<bf16>::zero();
   const bf16 *Qb = Q + (size_t)b * n * kHeadDim;
   const float c2 = scale * 1.4426950408889634f;
-  const float zs2 = MODE == MODE_PROFILE ? shift[b] * 1.4426950408889634f : 0.0f;
-  float rowsum = 0.0f, sumsq = 0.0f;
+  // profile: E' = 2^15 E, folded into the exponent (exact)
+  const float zs2 = MODE == MODE_PROFILE ? shift[b] * 1.4426950408889634f - (float)kProfLog2Scale : 0.0f;
+  float rowsum = 0.0f;
   double hsum = 0.0;   // PHIC: h_r = sum_i Phi[i][r] m_i (when hout is given)
-  // profile: >= 0 compacted E^T row, <= -2 anchor -(r + 2).  Padding keys
-  // j >= T write their (zero) rows to row j - t >= T - t, past the rows of the
-  // real keys (those rows only feed assignment columns that are never read), so
-  // every lane stores unconditionally and the per-tile store count is fixed.
+  // profile: the compacted E^T row of a non-anchor key.  Padding keys j >= T
+  // write their (zero) rows to row j - t, in [T - t, Tp - t), and anchor r to
+  // row Tp - t + r, in [Tp - t, Tp): past the rows of the real keys, so those
+  // rows only feed assignment columns that are never read, and every lane
+  // stores unconditionally with a fixed per-tile store count.
   int dest = row - t;
   if (MODE == MODE_PROFILE && rvalid) {
     const int32_t *S = anchors + (size_t)b * t;
@@ -262,7 +259,7 @@ __global__ void __launch_bounds__(256, 2) k_expgen_bf16(const bf16 *__restrict__
       if (S[mid] < row) lo = mid + 1;
       else hi = mid;
     }
-    dest = (lo < t && S[lo] == row) ? -(lo + 2) : row - lo;
+    dest = (lo < t && S[lo] == row) ? (int)(out_pair_stride / n_pad) - t + lo : row - lo;
   }
   // Q stage loads: run 4 wave + u covers tile rows 4 (4 wave + u) .. + 3; lane l
   // fills physical chunk l % 16 of its row with logical chunk (l % 16) ^ row.
@@ -289,9 +286,7 @@ __global__ void __launch_bounds__(256, 2) k_expgen_bf16(const bf16 *__restrict__
   const int row0 = blockIdx.x * 128 + wave * 32;
   auto row_dst = [&](int rr, int i0) -> bf16 * {
     const int d = __shfl(dest, rr, 64);
-    bf16 *base = d >= 0 ? out + (size_t)b * out_pair_stride + (size_t)d * n_pad
-                        : uout + ((size_t)b * tp + (size_t)(-d - 2)) * n_pad;
-    return base + i0;
+    return out + (size_t)b * out_pair_stride + (size_t)d * n_pad + i0;
   };
   // stage v (rows = this wave's 32 outputs, 64 query columns) and copy out
   auto flush_bf16 = [&](const float (&v)[2][16], int part, bf16 *dst_base, bool routed, int i0) {
@@ -351,9 +346,9 @@ __global__ void __launch_bounds__(256, 2) k_expgen_bf16(const bf16 *__restrict__
     if (it + 1 < ntile) issue_q(i0 + 64, st ^ 1);
     const char *sq = sQ + st * QB;
     if constexpr (MODE == MODE_PROFILE) {
-      // E = 2^(acc c2 - zs2) by the hardware exponential (results below 2^-126
-      // flush to zero); masks only on ragged tiles; each pair of rows rounded
-      // to bf16 once, for both the stored profile and its sum of squares
+      // E' = 2^(acc c2 - zs2) by the hardware exponential (results below
+      // 2^-126 flush to zero); masks only on ragged tiles; each pair of rows
+      // rounded to fp16 (nearest even) once
       uint32_t pk[2][8];
       auto products = [&](auto full_c) {
         constexpr bool FULL = decltype(full_c)::value;
@@ -377,12 +372,8 @@ __global__ void __launch_bounds__(256, 2) k_expgen_bf16(const bf16 *__restrict__
             }
             rowsum += e0;
             rowsum += e1;
-            const bf16x2 b2 = {(bf16)e0, (bf16)e1};
-            uint32_t w = __builtin_bit_cast(uint32_t, b2);
-            asm volatile("" : "+v"(w));   // unpack the rounded pair rather than round each value again
-            const float s0 = __uint_as_float(w << 16), s1 = __uint_as_float(w & 0xFFFF0000u);
-            sumsq = fmaf(s1, s1, fmaf(s0, s0, sumsq));
-            pk[ms][u] = w;
+            const f16x2 h2 = {(f16)e0, (f16)e1};
+            pk[ms][u] = __builtin_bit_cast(uint32_t, h2);
           }
         }
       };
@@ -453,9 +444,7 @@ __global__ void __launch_bounds__(256, 2) k_expgen_bf16(const bf16 *__restrict__
   }
   if (MODE == MODE_PROFILE) {
     rowsum += __shfl_xor(rowsum, 32, 64);
-    sumsq += __shfl_xor(sumsq, 32, 64);
-    if (h == 0 && rvalid) aux[(size_t)b * aux_pair_stride + row] = rowsum / (float)n;
-    if (h == 0 && dest <= -2) ssq[(size_t)b * tp + (-dest - 2)] = sumsq;
+    if (h == 0 && rvalid) aux[(size_t)b * aux_pair_stride + row] = rowsum * (kProfInvScale / (float)n);
   }
   if (MODE == MODE_PHIC && hout) {
     hsum += __shfl_xor(hsum, 32, 64);
@@ -463,30 +452,30 @@ __global__ void __launch_bounds__(256, 2) k_expgen_bf16(const bf16 *__restrict__
   }
 }
 
-// Compacted E^T [B][Tp][np] (rows of the non-anchor keys; T = bf16 or
-// float), unnormalised anchor profiles U [B][tp][np] with their sums of
-// squares ssq [B][tp], and phi [B][T].
 template <int MODE>
 static hipError_t eg_set_lds() {
   return hipFuncSetAttribute((const void *)k_expgen_bf16<MODE>, hipFuncAttributeMaxDynamicSharedMemorySize,
                              (int)eg_lds_bytes<MODE>());
 }
 
+// Compacted E^T [B][Tp][np] of the non-anchor keys (fp16 scaled by 2^15 for
+// bf16 inputs, fp32 for fp32 inputs) and phi [B][T] of every key.
 hipError_t launch_profiles(int dtype, const void *Q, const void *K, const float *zmerge, const int32_t *anchors,
-                           int t, void *Et, void *U, float *ssq, float *phi, int B, int T, int n, int64_t Tp,
-                           int64_t tp, int64_t np_, float scale, hipStream_t s) {
+                           int t, void *Et, float *phi, int B, int T, int n, int64_t Tp, int64_t np_, float scale,
+                           hipStream_t s) {
   dim3 grid(Tp / 128, B);
   if (dtype == ARCKV_BF16) {
     hipError_t e = eg_set_lds<MODE_PROFILE>();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL((k_expgen_bf16<MODE_PROFILE>), grid, dim3(256), eg_lds_bytes<MODE_PROFILE>(), s, (const bf16 *)Q, (const bf16 *)K,
                        (int64_t)T * kHeadDim, (int64_t)0, T, zmerge, (bf16 *)Et, Tp * np_, (int64_t)0, phi,
-                       (int64_t)T, n, (int)np_, scale, anchors, t, (bf16 *)U, ssq, tp, (const float *)nullptr,
-                       (double *)nullptr);
+                       (int64_t)T, n, (int)np_, scale, anchors, t, (bf16 *)nullptr, (float *)nullptr, (int64_t)0,
+                       (const float *)nullptr, (double *)nullptr);
   } else
     hipLaunchKernelGGL((k_expgen<float, MODE_PROFILE>), grid, dim3(256), 0, s, (const float *)Q, K,
                        (int64_t)T * kHeadDim, (int64_t)0, T, zmerge, Et, Tp * np_, (int64_t)0, phi, (int64_t)T,
-                       n, (int)np_, scale, anchors, t, U, ssq, tp, (const float *)nullptr, (double *)nullptr);
+                       n, (int)np_, scale, anchors, t, (void *)nullptr, (float *)nullptr, (int64_t)0,
+                       (const float *)nullptr, (double *)nullptr);
   return hipGetLastError();
 }
 

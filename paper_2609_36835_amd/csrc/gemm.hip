@@ -5,13 +5,20 @@
 namespace arckv {
 
 // Anchor assignment (eq. anchor_assignment): S[r][j] = sum_i U_S[r][i] E^T[j][i];
-// per-(M-tile, key) packed argmax partials [P][MT][N].  U [P][tp][np], Et
-// [P][Et_rows][np] with the first N rows used (the compacted non-anchor keys).
-// M-tiles are 256 rows for bf16 (large-tile kernel, 8 waves of 64 x 128) and
-// 128 for fp32.
-hipError_t launch_assign_gemm(int dtype, const void *U, const void *Et, uint64_t *part, int P, int t, int64_t tp,
-                              int64_t N, int64_t Et_rows, int64_t np_, hipStream_t s) {
+// per-(M-tile, key) top-3 partials (EpiArgmax*) [P][MT][N].  U [P][tp][np],
+// Et [P][Et_rows][np] with the first N rows used (the compacted non-anchor
+// keys).  Operands are fp16 for bf16 inputs (large-tile kernel, M-tiles of 256
+// rows, 8 waves of 64 x 128) and fp32 for fp32 inputs (M-tiles of 128).
+hipError_t launch_assign_gemm(int dtype, const void *U, const void *Et, uint64_t *part1, uint64_t *part2,
+                              uint32_t *part3, int P, int t, int64_t tp, int64_t N, int64_t Et_rows, int64_t np_,
+                              hipStream_t s) {
   if (N == 0) return hipSuccess;
+  if (dtype == ARCKV_BF16) {
+    // tile order: groups of 7 anchor tiles walk the key tiles (about 7 x 4.5 tiles per XCD at a time)
+    BigShape g2{P, (int)tp, (int)N, (int)np_, tp * np_, 0, np_, Et_rows * np_, 0, np_, false, 7};
+    EpiArgmaxBig<4, 2, 2, 4> e2{part1, part2, part3, (tp / 256) * N, (int)N, t};
+    return launch_gemm_big<4, 2, 2, 4, 64, 1, 1, 2, f16>(g2, (const bf16 *)U, (const bf16 *)Et, e2, s);
+  }
   GemmShape g;
   g.batch = P;
   g.M = (int)tp;
@@ -25,13 +32,7 @@ hipError_t launch_assign_gemm(int dtype, const void *U, const void *Et, uint64_t
   g.ldb = np_;
   g.syrk = false;
   g.group_m = 8;
-  if (dtype == ARCKV_BF16) {
-    // tile order: groups of 7 anchor tiles walk the key tiles (about 7 x 4.5 tiles per XCD at a time)
-    BigShape g2{P, (int)tp, (int)N, (int)np_, tp * np_, 0, np_, Et_rows * np_, 0, np_, false, 7};
-    EpiArgmaxBig<4, 2, 2, 4> e2{part, (tp / 256) * N, (int)N, t};
-    return launch_gemm_big<4, 2, 2, 4, 64, 1, 1, 2>(g2, (const bf16 *)U, (const bf16 *)Et, e2, s);
-  }
-  EpiArgmax e{part, (tp / kGBM) * N, (int)N, t};
+  EpiArgmax e{part1, part2, part3, (tp / kGBM) * N, (int)N, t};
   return launch_gemm<float, 1, 1>(g, (const float *)U, (const float *)Et, e, s);
 }
 

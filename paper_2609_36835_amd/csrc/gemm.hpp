@@ -139,46 +139,57 @@ __global__ void __launch_bounds__(256) k_gemm_tn(GemmShape g, const T *__restric
 }
 
 // ------------------------------------------------------------------ epilogues
-// Rows are anchors r, columns keys j.  For each key, keep the best
-// (similarity, lowest r) as a packed 64-bit key and write one partial per
-// (M-tile, key).  Similarities are >= 0, so their float bits order like uints.
+// Rows are anchors r, columns keys j.  For each key, keep the best two
+// (similarity, lowest r) as packed 64-bit keys and the third similarity
+// (Top3), one partial per (M-tile, key).  Similarities are >= 0, so their float
+// bits order like uints.
 struct EpiArgmax {
-  uint64_t *part;       // [P][MT][Np]
-  int64_t pair_stride;  // MT * Np
+  uint64_t *part1, *part2;  // [P][MT][Np]
+  uint32_t *part3;          // [P][MT][Np]
+  int64_t pair_stride;      // MT * Np
   int Np, t;
   __device__ __forceinline__ void operator()(f32x16 (&acc)[2][2], int p, int row0, int col0, int mt, int nt, int lane,
                              int wm) const {
-    __shared__ uint64_t red[128];
+    __shared__ uint64_t red1[128], red2[128];
+    __shared__ uint32_t red3[128];
     const int h = lane >> 5, col = lane & 31;
-    uint64_t best[2] = {0ull, 0ull};
+    uint64_t k1[2], k2[2];
+    uint32_t k3[2];
     #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int j = 0; j < 2; ++j) {
+      Top3 tp;
+      tp.init();
       #pragma unroll
       for (int i = 0; i < 2; ++i)
         #pragma unroll
         for (int v = 0; v < 16; ++v) {
           const int r = row0 + 32 * i + acc_row(v, lane);
-          if (r < t) {
-            uint64_t key = ((uint64_t)__float_as_uint(acc[i][j][v]) << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)r);
-            best[j] = key > best[j] ? key : best[j];
-          }
+          tp.add(acc[i][j][v], (uint32_t)r, r < t);
         }
-    #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      uint64_t o = __shfl_xor(best[j], 32, 64);
-      best[j] = o > best[j] ? o : best[j];
+      k1[j] = pack_sim(tp.v1, tp.r1);
+      k2[j] = pack_sim(tp.v2, tp.r2);
+      k3[j] = tp.v3 < 0.0f ? 0u : __float_as_uint(tp.v3);
+      merge_top3(k1[j], k2[j], k3[j], __shfl_xor(k1[j], 32, 64), __shfl_xor(k2[j], 32, 64),
+                 __shfl_xor(k3[j], 32, 64));
     }
     const int cl = col0 - nt * kGBN;   // 0 or 64 within the block
     if (wm == 1 && h == 0)
       #pragma unroll
-      for (int j = 0; j < 2; ++j) red[cl + 32 * j + col] = best[j];
+      for (int j = 0; j < 2; ++j) {
+        red1[cl + 32 * j + col] = k1[j];
+        red2[cl + 32 * j + col] = k2[j];
+        red3[cl + 32 * j + col] = k3[j];
+      }
     __syncthreads();
     if (wm == 0 && h == 0)
       #pragma unroll
       for (int j = 0; j < 2; ++j) {
-        uint64_t o = red[cl + 32 * j + col];
-        uint64_t bb = o > best[j] ? o : best[j];
-        part[(size_t)p * pair_stride + (size_t)mt * Np + col0 + 32 * j + col] = bb;
+        const int c = cl + 32 * j + col;
+        merge_top3(k1[j], k2[j], k3[j], red1[c], red2[c], red3[c]);
+        const size_t o = (size_t)p * pair_stride + (size_t)mt * Np + col0 + 32 * j + col;
+        part1[o] = k1[j];
+        part2[o] = k2[j];
+        part3[o] = k3[j];
       }
   }
 };

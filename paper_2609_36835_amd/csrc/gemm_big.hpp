@@ -1,5 +1,5 @@
-// Large-tile batched TN contraction on bf16 MFMA (32x32x16) for the big
-// contractions of the path: the anchor assignment (one bf16 plane), the
+// Large-tile batched TN contraction on bf16 or fp16 MFMA (32x32x16) for the
+// big contractions of the path: the anchor assignment (one fp16 plane), the
 // split-bf16 Gram matrices (hi/lo planes, three products) and the Cholesky
 // trailing updates (hi/mid/lo planes of an fp32 panel, the six products whose
 // plane indices sum to at most 2, which reproduce the fp32 product to within
@@ -120,7 +120,7 @@ struct epi_has_skip : std::false_type {};
 template <typename E>
 struct epi_has_skip<E, std::void_t<decltype(std::declval<const E &>().skip(0))>> : std::true_type {};
 
-template <int WM, int WN, int TM, int TN, int BK, int NA, int NB, int NS, class Epi>
+template <int WM, int WN, int TM, int TN, int BK, int NA, int NB, int NS, typename E, class Epi>
 __global__ void __launch_bounds__(64 * WM * WN, 1) k_gemm_big(BigShape g, const bf16 *__restrict__ A,
                                                               const bf16 *__restrict__ B, Epi epi) {
   using C = BigCfg<WM, WN, TM, TN, BK, NA, NB, NS>;
@@ -230,13 +230,13 @@ __global__ void __launch_bounds__(64 * WM * WN, 1) k_gemm_big(BigShape g, const 
       for (int ii = 0; ii < TM; ++ii)
 #pragma unroll
         for (int j = 0; j < TN; ++j) {
-          acc[ii][j] = Mfma<bf16>::mma(fa[cur][0][ii], fb[cur][0][j], acc[ii][j]);
-          if constexpr (NB > 1) acc[ii][j] = Mfma<bf16>::mma(fa[cur][0][ii], fb[cur][1][j], acc[ii][j]);
-          if constexpr (NA > 1) acc[ii][j] = Mfma<bf16>::mma(fa[cur][1][ii], fb[cur][0][j], acc[ii][j]);
+          acc[ii][j] = mma16<E>(fa[cur][0][ii], fb[cur][0][j], acc[ii][j]);
+          if constexpr (NB > 1) acc[ii][j] = mma16<E>(fa[cur][0][ii], fb[cur][1][j], acc[ii][j]);
+          if constexpr (NA > 1) acc[ii][j] = mma16<E>(fa[cur][1][ii], fb[cur][0][j], acc[ii][j]);
           if constexpr (NA > 2 && NB > 2) {
-            acc[ii][j] = Mfma<bf16>::mma(fa[cur][0][ii], fb[cur][2][j], acc[ii][j]);
-            acc[ii][j] = Mfma<bf16>::mma(fa[cur][2][ii], fb[cur][0][j], acc[ii][j]);
-            acc[ii][j] = Mfma<bf16>::mma(fa[cur][1][ii], fb[cur][1][j], acc[ii][j]);
+            acc[ii][j] = mma16<E>(fa[cur][0][ii], fb[cur][2][j], acc[ii][j]);
+            acc[ii][j] = mma16<E>(fa[cur][2][ii], fb[cur][0][j], acc[ii][j]);
+            acc[ii][j] = mma16<E>(fa[cur][1][ii], fb[cur][1][j], acc[ii][j]);
           }
         }
     }
@@ -247,41 +247,57 @@ __global__ void __launch_bounds__(64 * WM * WN, 1) k_gemm_big(BigShape g, const 
 }
 
 // ------------------------------------------------------------------ epilogues
-// Anchor assignment: rows anchors r, columns keys j.  Packed (similarity,
-// lowest r) maxima per (M-tile, key); similarities are >= 0, so their float
-// bits order like unsigned integers.
+// Anchor assignment: rows anchors r, columns keys j.  For every (M-tile,
+// key) the best two similarities as packed keys and the third as float bits
+// (Top3), so a later pass can tell which anchors of the tile may be the
+// argmax once the rounding of the operands is accounted for.
 template <int WM, int WN, int TM, int TN>
 struct EpiArgmaxBig {
-  uint64_t *part;       // [P][MT][Np]
-  int64_t pair_stride;  // MT * Np
+  uint64_t *part1, *part2;  // [P][MT][Np]
+  uint32_t *part3;          // [P][MT][Np]
+  int64_t pair_stride;      // MT * Np
   int Np, t;
   __device__ __forceinline__ void operator()(f32x16 (&acc)[TM][TN], int p, int row0, int col0, int mt, int nt,
                                              int lane, int wm, int wn) const {
     constexpr int BN = 32 * WN * TN;
-    __shared__ uint64_t red[WM][BN];
+    // the operand stages are free once the contraction has finished (the
+    // caller synchronised the workgroup before the epilogue)
+    extern __shared__ __attribute__((aligned(1024))) char big_smem[];
+    uint64_t *red1 = reinterpret_cast<uint64_t *>(big_smem);    // [WM][BN]
+    uint64_t *red2 = red1 + WM * BN;                             // [WM][BN]
+    uint32_t *red3 = reinterpret_cast<uint32_t *>(red2 + WM * BN);
     const int h = lane >> 5, col = lane & 31;
 #pragma unroll
     for (int j = 0; j < TN; ++j) {
-      uint64_t best = 0ull;
+      Top3 tp;
+      tp.init();
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
           const int r = row0 + 32 * i + acc_row(v, lane);
-          const uint64_t key =
-              ((uint64_t)__float_as_uint(acc[i][j][v]) << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)r);
-          best = (r < t && key > best) ? key : best;
+          tp.add(acc[i][j][v], (uint32_t)r, r < t);
         }
-      const uint64_t o = __shfl_xor(best, 32, 64);
-      best = o > best ? o : best;
-      if (h == 0) red[wm][wn * 32 * TN + 32 * j + col] = best;
+      uint64_t k1 = pack_sim(tp.v1, tp.r1), k2 = pack_sim(tp.v2, tp.r2);
+      uint32_t k3 = tp.v3 < 0.0f ? 0u : __float_as_uint(tp.v3);
+      merge_top3(k1, k2, k3, __shfl_xor(k1, 32, 64), __shfl_xor(k2, 32, 64), __shfl_xor(k3, 32, 64));
+      if (h == 0) {
+        const int c = wm * BN + wn * 32 * TN + 32 * j + col;
+        red1[c] = k1;
+        red2[c] = k2;
+        red3[c] = k3;
+      }
     }
     __syncthreads();
     for (int c = threadIdx.x; c < BN; c += 64 * WM * WN) {
-      uint64_t best = red[0][c];
+      uint64_t k1 = red1[c], k2 = red2[c];
+      uint32_t k3 = red3[c];
 #pragma unroll
-      for (int w = 1; w < WM; ++w) best = red[w][c] > best ? red[w][c] : best;
-      part[(size_t)p * pair_stride + (size_t)mt * Np + (size_t)nt * BN + c] = best;
+      for (int w = 1; w < WM; ++w) merge_top3(k1, k2, k3, red1[w * BN + c], red2[w * BN + c], red3[w * BN + c]);
+      const size_t o = (size_t)p * pair_stride + (size_t)mt * Np + (size_t)nt * BN + c;
+      part1[o] = k1;
+      part2[o] = k2;
+      part3[o] = k3;
     }
   }
 };
@@ -381,7 +397,7 @@ struct EpiValueResidBig {
   }
 };
 
-template <int WM, int WN, int TM, int TN, int BK, int NA, int NB, int NS, class Epi>
+template <int WM, int WN, int TM, int TN, int BK, int NA, int NB, int NS, typename E = bf16, class Epi>
 hipError_t launch_gemm_big(const BigShape &g, const bf16 *A, const bf16 *B, const Epi &epi, hipStream_t s) {
   using C = BigCfg<WM, WN, TM, TN, BK, NA, NB, NS>;
   if (g.M % C::BM || g.N % C::BN || g.K % BK) return hipErrorInvalidValue;
@@ -389,7 +405,7 @@ hipError_t launch_gemm_big(const BigShape &g, const bf16 *A, const bf16 *B, cons
     return hipErrorInvalidValue;
   const int64_t tiles = big_tiles(g, C::BM, C::BN);
   if (tiles == 0) return hipSuccess;
-  auto kern = k_gemm_big<WM, WN, TM, TN, BK, NA, NB, NS, Epi>;
+  auto kern = k_gemm_big<WM, WN, TM, TN, BK, NA, NB, NS, E, Epi>;
   hipError_t e = hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(kern, dim3((unsigned)tiles), dim3(C::THREADS), C::LDS, s, g, A, B, epi);

@@ -1,11 +1,8 @@
-// Anchor assignment finalisation and convex key merge (Section 3.4).
+// Convex key merge (Section 3.4).
 //
 //  k_zmax            z_merge = max_i z_i (the global logit maximum equals the
 //                    largest full-cache row maximum, eq. response_profile)
-//  k_anchor_profiles U_S rows: E^T[s_r] / ||E^T[s_r]|| (anchor response profiles),
-//                    normalising the rows the profile pass wrote
-//  k_assign_finalize kappa_j from the per-tile packed argmax; anchors map to
-//                    themselves (eq. anchor_assignment)
+//  (the assignment itself, kappa, is in assign.hip)
 //  k_group_sort      stable counting sort of positions by group (deterministic)
 //  k_group_merge     c_r = sum_j alpha_rj k_j with alpha_rj = lambda phi_j / sum_G phi
 //                    + (1 - lambda)[j = s_r], renormalised to sum exactly to 1
@@ -23,54 +20,6 @@ __global__ void __launch_bounds__(256) k_zmax(const float *__restrict__ z, int n
   if ((tid & 63) == 0) red[tid >> 6] = v;
   __syncthreads();
   if (tid == 0) zmax[b] = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
-}
-
-// One wave per anchor row: U_S[r][i] = E^T[s_r][i] / ||E^T[s_r][:]||, in place
-// on the unnormalised rows the profile pass wrote (ssq[r] = sum of squares of
-// the stored values); rows r >= t are zero.
-template <typename T>
-__global__ void __launch_bounds__(256) k_anchor_profiles(T *__restrict__ U, const float *__restrict__ ssq, int t,
-                                                         int64_t np_, int64_t tp) {
-  const int b = blockIdx.y, lane = threadIdx.x & 63;
-  const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (r >= tp) return;
-  T *urow = U + ((size_t)b * tp + r) * np_;
-  if (r >= t) {
-    for (int64_t i = lane; i < np_; i += 64) urow[i] = (T)0.0f;
-    return;
-  }
-  const float ss = ssq[(size_t)b * tp + r];
-  const float inv = ss > 0.0f ? 1.0f / sqrtf(ss) : 0.0f;
-  for (int64_t i = lane; i < np_; i += 64) urow[i] = (T)(to_f(urow[i]) * inv);
-}
-
-// kappa_j: anchors map to themselves; any other key takes the best packed
-// (similarity, lowest r) over the M-tiles at its compacted column
-// j - #{anchors < j}.  Both come from one binary search of the ascending anchors.
-__global__ void __launch_bounds__(256) k_assign_finalize(const uint64_t *__restrict__ part, int MT, int64_t Np,
-                                                         const int32_t *__restrict__ anchors, int T, int t,
-                                                         int32_t *__restrict__ kappa) {
-  const int b = blockIdx.y;
-  const int j = blockIdx.x * 256 + threadIdx.x;
-  if (j >= T) return;
-  const int32_t *S = anchors + (size_t)b * t;
-  int lo = 0, hi = t;   // lo = #{anchors < j}
-  while (lo < hi) {
-    const int mid = (lo + hi) >> 1;
-    if (S[mid] < j) lo = mid + 1;
-    else hi = mid;
-  }
-  int32_t a = lo;
-  if (lo >= t || S[lo] != j) {
-    uint64_t best = 0;
-    const uint64_t *pp = part + (size_t)b * MT * Np + (j - lo);
-    for (int mt = 0; mt < MT; ++mt) {
-      uint64_t v = pp[(size_t)mt * Np];
-      best = v > best ? v : best;
-    }
-    a = (int32_t)(0xFFFFFFFFu - (uint32_t)(best & 0xFFFFFFFFull));
-  }
-  kappa[(size_t)b * T + j] = a;
 }
 
 // One wave per pair.  Produces offsets [t+1] and perm [T] (positions grouped by
@@ -225,23 +174,6 @@ hipError_t launch_zmax(const float *z, int B, int n, float *zmax, hipStream_t s)
   return hipGetLastError();
 }
 
-
-hipError_t launch_anchor_profiles(int dtype, void *U, const float *ssq, int B, int t, int64_t np_, int64_t tp,
-                                  hipStream_t s) {
-  dim3 grid((unsigned)(tp / 4), B);
-  if (dtype == ARCKV_BF16)
-    hipLaunchKernelGGL(k_anchor_profiles<bf16>, grid, dim3(256), 0, s, (bf16 *)U, ssq, t, np_, tp);
-  else
-    hipLaunchKernelGGL(k_anchor_profiles<float>, grid, dim3(256), 0, s, (float *)U, ssq, t, np_, tp);
-  return hipGetLastError();
-}
-
-hipError_t launch_assign_finalize(const uint64_t *part, int MT, int64_t Np, const int32_t *anchors, int B, int T,
-                                  int t, int32_t *kappa, hipStream_t s) {
-  hipLaunchKernelGGL(k_assign_finalize, dim3((T + 255) / 256, B), dim3(256), 0, s, part, MT, Np, anchors, T, t,
-                     kappa);
-  return hipGetLastError();
-}
 
 hipError_t launch_group_merge(int dtype, const void *K, const float *phi, const int32_t *kappa,
                               const int32_t *anchors, int B, int T, int t, int64_t tp, float lambda,

@@ -41,44 +41,51 @@ def np64(x):
     return x.detach().float().cpu().numpy().astype(np.float64)
 
 
-def profile_dtype(wl):
-    """The precision the GPU stores response profiles in (bf16 or fp32 inputs)."""
-    return "bf16" if wl.dtype == "bf16" else "f32"
+# An assignment difference between the GPU and the float64 oracle is accepted
+# only at a float64 near-tie: the library's last pass decides in float64
+# (logits from exact products, exponentials, norms and dot products in float64),
+# so the two can disagree only where the two anchors' float64 similarities
+# agree to within their rounding, about n 2^-52 relative (1e-12 at n = 4096).
+TIE_F64 = 1e-10
 
 
-def assignment_gap(Q, K, S, scale, j, pdt):
-    """Relative gap between key j's best and runner-up anchor similarity,
-    with profiles rounded to the storage precision pdt."""
+def assignment_gap(Q, K, S, scale, j, r_gpu, r_ref):
+    """Relative float64 gap of eq. anchor_assignment between the oracle's anchor
+    r_ref and the GPU's r_gpu for key j (>= 0 when r_ref is the argmax)."""
     import oracle
     zm = oracle.global_logit_max(Q, K, scale)
-    ES = oracle.round_to(np.exp(oracle.logits(Q, K[S], scale) - zm), pdt)
-    US = oracle.round_to(ES / np.linalg.norm(ES, axis=0)[None, :], pdt)
-    ej = oracle.round_to(np.exp(oracle.logits(Q, K[j:j + 1], scale) - zm), pdt)[:, 0]
-    sim = ej @ US
-    top = np.sort(sim)[::-1]
-    return 0.0 if len(top) < 2 else (top[0] - top[1]) / max(abs(top[0]), 1e-300)
+    _, US, _ = oracle.response_profiles(Q, K[np.asarray(S)[[r_gpu, r_ref]]], scale, zm)
+    e = np.exp(oracle.logits(Q, K[j:j + 1], scale) - zm)[:, 0]
+    sim = e @ US
+    return (sim[1] - sim[0]) / max(abs(sim[1]), 1e-300)
 
 
 def gpu_assignment(K, V, Q, anchors, scale):
-    """kappa as arckv_compact computes it for one pair: the GPU row maxima z
-    (arckv_rowstats) feed arckv_merge on the GPU's anchors.  K, V, Q: [1][...]
-    device tensors, anchors [1][t] int32."""
+    """kappa and the assignment counters (arckv_assign_stats) as arckv_compact
+    computes them for one pair: the GPU row maxima z (arckv_rowstats) feed
+    arckv_merge on the given anchors.  K, V, Q: [1][...] device tensors,
+    anchors [1][t] int32."""
     from paper_2609_36835_amd import arckv
     import oracle
     z, _, _ = arckv.rowstats(K, V, Q, scale=scale)
-    _, kappa, _ = arckv.merge(K, Q, z, anchors, lambda_m=oracle.LAMBDA_M, scale=scale)
-    return kappa[0].cpu().numpy().astype(np.int64)
+    _, kappa, _, st = arckv.merge(K, Q, z, anchors, lambda_m=oracle.LAMBDA_M, scale=scale, return_stats=True)
+    return kappa[0].cpu().numpy().astype(np.int64), st[0].cpu().numpy()
 
 
-def certify_flips(kappa_gpu, kappa_ref, Q, K, anchors, scale, pdt, log=print):
-    """Assignment differences must be near-ties within one storage-precision
-    rounding term (2^-7 relative for bf16 profiles, 2^-23 + n 2^-24 for fp32)
-    and rare (at most max(1, T/1000))."""
-    rel_tie = 2.0 ** -7 if pdt == "bf16" else 2.0 ** -23 + Q.shape[0] * 2.0 ** -24
+def certify_flips(kappa_gpu, kappa_ref, Q, K, anchors, scale, log=print):
+    """Every assignment difference from the float64 definition must be a float64
+    near-tie (TIE_F64).  Returns the number of differences."""
     flips = np.flatnonzero(kappa_gpu != kappa_ref)
     for j in flips:
-        gap = assignment_gap(Q, K, anchors, scale, j, pdt)
-        log(f"    key {j}: gpu anchor {kappa_gpu[j]}, oracle anchor {kappa_ref[j]}, relative gap {gap:.2e}")
-        assert gap <= rel_tie, (j, gap)
-    assert len(flips) <= max(1, len(K) // 1000), len(flips)
+        gap = assignment_gap(Q, K, anchors, scale, j, kappa_gpu[j], kappa_ref[j])
+        log(f"    key {j}: gpu anchor {kappa_gpu[j]}, oracle anchor {kappa_ref[j]}, float64 relative gap {gap:.2e}")
+        assert abs(gap) <= TIE_F64, (j, gap)
     return len(flips)
+
+
+def log_assign_stats(st, T, t, log=print):
+    """Counters of the three assignment passes; no key may be left undecided."""
+    keys = max(1, T - t)
+    log(f"    assignment: {st[0]} keys flagged by the fp16 bound ({st[0] / keys:.2%}; {st[6]} refined, {st[7]} with "
+        f"a whole tile), {st[1]} decided in float64 ({st[1] / keys:.3%}), {st[2]} candidates, {st[3]} undecided")
+    assert st[3] == 0, st

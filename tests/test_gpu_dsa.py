@@ -1,11 +1,14 @@
 """The value-aware indexer (Appendix A.1) and its pooled scores (eq.
-indexer_pooling) on the GPU against the float64 oracle, which rounds the
+indexer_pooling) on the GPU against the float64 oracle.
+
+Parity is against the plain float64 definition at the bf16-input bar (2e-2 of
+the largest pooled score); anchor-set differences must lie within twice the
+measured score deviation of the t-th score, the only way two scores that far
+from the boundary could swap.  A second, tighter check runs the oracle with the
 intermediates the GPU stores in bf16 (the value head's projections and context,
-qbar, kbar) at the same points.  With the value path at its initialisation
-(L_c = L_v = 0, Appendix A.1) only float32 summation order differs; with it
-active, the value context inherits the bf16 rounding of the attention
-probabilities inside the row-statistics kernel, which the oracle does not
-reproduce, so the bar is wider and anchor differences must be near-ties."""
+qbar, kbar) rounded at the same points, which leaves float32 summation order
+(and, with the value path active, the bf16 attention probabilities inside the
+row-statistics kernel) as the only difference."""
 import math
 
 import numpy as np
@@ -13,7 +16,7 @@ import pytest
 import torch
 
 import oracle
-from tests.gpu_common import TOL_OUT, certify_flips, gpu_assignment, np64
+from tests.gpu_common import TOL_OUT, certify_flips, gpu_assignment, log_assign_stats, np64
 
 pytestmark = pytest.mark.gpu
 
@@ -24,6 +27,7 @@ pytestmark = pytest.mark.gpu
 # bar allows a few of them.
 S_TOL_EXACT = 2e-3
 S_TOL_VALUE = 1e-2      # relative, value path active (measured <= 1.8e-3)
+S_TOL_PLAIN = TOL_OUT["bf16"]   # against the plain float64 definition
 
 
 def A():
@@ -58,11 +62,24 @@ def make_case(B, T, G, n_pos, dx, x_group, seed, zero_value):
     return P, K, V, Q, X, dev
 
 
-def oracle_scores(P, K, V, Q, X, b, n_pos, x_group, scale_a):
+def oracle_scores(P, K, V, Q, X, b, n_pos, x_group, scale_a, rounded=False):
     ix = oracle.DSAIndexer(**{k: v[b] for k, v in P.items()})
     I = oracle.dsa_logits(Q[b], X[b // x_group], K[b], V[b], ix, n_pos, scale_a,
-                          rnd=lambda a: oracle.round_to(a, "bf16"))
+                          rnd=(lambda a: oracle.round_to(a, "bf16")) if rounded else None)
     return oracle.pool_rms(I)
+
+
+def check_topt(s_gpu, s_ref, t, log=print):
+    """Top-t of the GPU scores vs the oracle's: a difference needs |s_ref[j] -
+    s_(t)| <= 2 max|s_gpu - s_ref| (both scores of a swapped pair lie within the
+    deviation of the boundary).  Returns the number of swaps."""
+    S_gpu = set(oracle.select_topt(s_gpu, t).tolist())
+    S_ref = set(oracle.select_topt(s_ref, t).tolist())
+    boundary = np.sort(s_ref)[::-1][t - 1]
+    band = 2.0 * np.abs(s_gpu - s_ref).max()
+    for j in S_gpu ^ S_ref:
+        assert abs(s_ref[j] - boundary) <= band, (j, abs(s_ref[j] - boundary), band)
+    return len(S_gpu ^ S_ref) // 2
 
 
 @pytest.mark.parametrize("B,T,G,n_pos,dx,x_group,zero_value", [
@@ -78,15 +95,14 @@ def test_dsa_scores_match_oracle(B, T, G, n_pos, dx, x_group, zero_value):
     for b in range(B):
         s_ref = oracle_scores(P, K, V, Q, X, b, n_pos, x_group, sa)
         rel = np.abs(s_gpu[b] - s_ref) / s_ref.max()
-        print(f"    pair {b}: max |ds| / max s = {rel.max():.2e}", flush=True)
-        assert rel.max() <= tol, (b, rel.max())
-        # top-t of the GPU scores vs the oracle's: differences only at near-ties
-        S_gpu = set(oracle.select_topt(s_gpu[b], t).tolist())
-        S_ref = set(oracle.select_topt(s_ref, t).tolist())
-        boundary = np.sort(s_ref)[::-1][t - 1]
-        for j in S_gpu ^ S_ref:
-            assert abs(s_ref[j] - boundary) <= 2 * tol * s_ref.max(), (b, j)
-        print(f"    pair {b}: top-{t} differs at {len(S_gpu ^ S_ref) // 2} certified near-ties", flush=True)
+        s_rnd = oracle_scores(P, K, V, Q, X, b, n_pos, x_group, sa, rounded=True)
+        rel_rnd = np.abs(s_gpu[b] - s_rnd) / s_rnd.max()
+        print(f"    pair {b}: max |ds| / max s = {rel.max():.2e} (float64 definition), {rel_rnd.max():.2e} "
+              f"(oracle rounding at the GPU's bf16 storage points)", flush=True)
+        assert rel.max() <= S_TOL_PLAIN, (b, rel.max())
+        assert rel_rnd.max() <= tol, (b, rel_rnd.max())
+        nsw = check_topt(s_gpu[b], s_ref, t)
+        print(f"    pair {b}: top-{t} differs from the float64 definition at {nsw} certified near-ties", flush=True)
 
 
 def test_compact_on_dsa_scores():
@@ -104,12 +120,13 @@ def test_compact_on_dsa_scores():
     for b in range(B):
         S = oracle.select_topt(sc[b], t)
         assert anchors[b].tolist() == S.tolist(), b
-        kap_gpu = gpu_assignment(Kd[b:b + 1].contiguous(), Vd[b:b + 1].contiguous(), Qd[b:b + 1].contiguous(),
-                                 anchors_d[b:b + 1].contiguous(), s)
-        kap_ref, _, _ = oracle.profiles_assign_phi(Q[b], K[b], S, s, "bf16")
-        certify_flips(kap_gpu, kap_ref, Q[b], K[b], S, s, "bf16")
-        rr = oracle.compact_pair(K[b], V[b], Q[b], None, None, None, None, t=t, scale=s, scores=sc[b], anchors=S,
-                                 kappa=kap_gpu, profile_dtype="bf16")
+        kap_gpu, st = gpu_assignment(Kd[b:b + 1].contiguous(), Vd[b:b + 1].contiguous(), Qd[b:b + 1].contiguous(),
+                                     anchors_d[b:b + 1].contiguous(), s)
+        log_assign_stats(st, T, t)
+        rr = oracle.compact_pair(K[b], V[b], Q[b], None, None, None, None, t=t, scale=s, scores=sc[b], anchors=S)
+        if certify_flips(kap_gpu, rr.kappa, Q[b], K[b], S, s):
+            rr = oracle.compact_pair(K[b], V[b], Q[b], None, None, None, None, t=t, scale=s, scores=sc[b],
+                                     anchors=S, kappa=kap_gpu)
         err = oracle.row_rel_err(oracle.attend_compact(Q[b], Ck[b], beta[b], Cv[b], s),
                                  oracle.attend_compact(Q[b], rr.C_k, rr.beta, rr.C_v, s))
         print(f"  pair {b}: O(Q_ref) max row rel err {err.max():.3e}", flush=True)
@@ -145,17 +162,13 @@ def test_dsa_full_shape_sampled_pair():
     host = lambda x: x.float().cpu().numpy().astype(np.float64)
     ix = oracle.DSAIndexer(**{k: host(v[b]) for k, v in P.items()})
     I = oracle.dsa_logits(host(Q[b]), host(X[b // wl.kv_heads]), host(K[b]), host(V[b]), ix, n_pos,
-                          1.0 / math.sqrt(128), rnd=lambda a: oracle.round_to(a, "bf16"))
+                          1.0 / math.sqrt(128))
     s_ref = oracle.pool_rms(I)
     del I
     sg = np64(s_gpu[b])
     rel = np.abs(sg - s_ref) / s_ref.max()
-    print(f"    pair {b}: max |ds| / max s = {rel.max():.2e}", flush=True)
-    assert rel.max() <= S_TOL_VALUE, rel.max()
+    print(f"    pair {b}: max |ds| / max s = {rel.max():.2e} (float64 definition)", flush=True)
+    assert rel.max() <= S_TOL_PLAIN, rel.max()
     t = oracle.budget(T, wl.rho)
-    S_gpu = set(oracle.select_topt(sg, t).tolist())
-    S_ref = set(oracle.select_topt(s_ref, t).tolist())
-    boundary = np.sort(s_ref)[::-1][t - 1]
-    for j in S_gpu ^ S_ref:
-        assert abs(s_ref[j] - boundary) <= 2 * S_TOL_VALUE * s_ref.max(), j
-    print(f"    pair {b}: top-{t} differs at {len(S_gpu ^ S_ref) // 2} certified near-ties", flush=True)
+    nsw = check_topt(sg, s_ref, t)
+    print(f"    pair {b}: top-{t} differs from the float64 definition at {nsw} certified near-ties", flush=True)

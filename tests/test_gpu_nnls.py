@@ -23,7 +23,7 @@ import torch
 
 import oracle
 import synth
-from tests.gpu_common import TOL_OUT, certify_flips, gpu_assignment, make_inputs, np64, profile_dtype, scale_of
+from tests.gpu_common import TOL_OUT, certify_flips, gpu_assignment, log_assign_stats, make_inputs, np64, scale_of
 
 pytestmark = pytest.mark.gpu
 
@@ -87,7 +87,7 @@ def case(request):
     s = scale_of(wl)
     t = oracle.budget(wl.T, wl.rho)
     ref = [oracle.compact_pair(host["K"][b], host["V"][b], host["Q"][b], host["W1"][b], host["b1"][b],
-                               host["w2"][b], host["b2"][b], t=t, scale=s, profile_dtype=profile_dtype(wl))
+                               host["w2"][b], host["b2"][b], t=t, scale=s)
            for b in range(wl.pairs)]
     return wl, dev, host, s, t, ref
 
@@ -166,13 +166,14 @@ def test_compact_with_nnls_end_to_end(case):
     for b in range(wl.pairs):
         Q, K = host["Q"][b], host["K"][b]
         S = anchors[b].astype(np.int64)
-        kap_gpu = gpu_assignment(dev["K"][b:b + 1].contiguous(), dev["V"][b:b + 1].contiguous(),
-                                 dev["Q"][b:b + 1].contiguous(), anchors_d[b:b + 1].contiguous(), s)
-        kap_ref, _, _ = oracle.profiles_assign_phi(Q, K, S, s, profile_dtype(wl))
-        certify_flips(kap_gpu, kap_ref, Q, K, S, s, profile_dtype(wl), log=log)
+        kap_gpu, st = gpu_assignment(dev["K"][b:b + 1].contiguous(), dev["V"][b:b + 1].contiguous(),
+                                     dev["Q"][b:b + 1].contiguous(), anchors_d[b:b + 1].contiguous(), s)
+        log_assign_stats(st, wl.T, t, log=log)
         rr = oracle.compact_pair(K, host["V"][b], Q, host["W1"][b], host["b1"][b], host["w2"][b], host["b2"][b],
-                                 t=t, scale=s, anchors=S, kappa=kap_gpu, profile_dtype=profile_dtype(wl),
-                                 bias_mode=1)
+                                 t=t, scale=s, anchors=S, bias_mode=1)
+        if certify_flips(kap_gpu, rr.kappa, Q, K, S, s, log=log):
+            rr = oracle.compact_pair(K, host["V"][b], Q, host["W1"][b], host["b1"][b], host["w2"][b], host["b2"][b],
+                                     t=t, scale=s, anchors=S, kappa=kap_gpu, bias_mode=1)
         err = oracle.row_rel_err(oracle.attend_compact(Q, Ck[b], beta[b], Cv[b], s),
                                  oracle.attend_compact(Q, rr.C_k, rr.beta, rr.C_v, s))
         O = oracle.attend_full(Q, K, host["V"][b], s)

@@ -15,8 +15,8 @@ import torch
 
 import oracle
 import synth
-from tests.gpu_common import (TOL_OUT, assignment_gap, certify_flips, gpu_assignment, make_inputs, np64,
-                               profile_dtype, scale_of)
+from tests.gpu_common import (TOL_OUT, certify_flips, gpu_assignment, log_assign_stats, make_inputs, np64,
+                               scale_of)
 
 pytestmark = pytest.mark.gpu
 
@@ -52,7 +52,7 @@ def case(request):
     ref = []
     for b in range(wl.pairs):
         ref.append(oracle.compact_pair(host["K"][b], host["V"][b], host["Q"][b], host["W1"][b], host["b1"][b],
-                                       host["w2"][b], host["b2"][b], t=t, scale=s, profile_dtype=profile_dtype(wl)))
+                                       host["w2"][b], host["b2"][b], t=t, scale=s))
     return wl, dev, host, s, t, ref
 
 
@@ -116,24 +116,18 @@ def test_merge_stagewise(case):
     wl, dev, host, s, t, ref = case
     anchors = torch.from_numpy(np.stack([r.anchors for r in ref]).astype(np.int32)).cuda()
     z = torch.from_numpy(np.stack([r.z for r in ref]).astype(np.float32)).cuda()
-    Ck, kappa, phi = A().merge(dev["K"], dev["Q"], z, anchors, lambda_m=oracle.LAMBDA_M, scale=s)
-    Ck, kappa, phi = np64(Ck), kappa.cpu().numpy(), np64(phi)
-    # The oracle takes the argmax on profiles rounded to the GPU's storage
-    # precision, so both sides decide kappa on the same stored values; what is
-    # left is fp32 accumulation order and rare one-ulp rounding differences of
-    # single profile entries.  A remaining flip must be a near-tie within one
-    # such ulp-sized term (2^-7 relative for bf16, 2^-23 + n 2^-24 for fp32).
-    rel_tie = 2.0 ** -7 if wl.dtype == "bf16" else 2.0 ** -23 + wl.n * 2.0 ** -24
+    Ck, kappa, phi, st = A().merge(dev["K"], dev["Q"], z, anchors, lambda_m=oracle.LAMBDA_M, scale=s,
+                                   return_stats=True)
+    Ck, kappa, phi, st = np64(Ck), kappa.cpu().numpy(), np64(phi), st.cpu().numpy()
+    # kappa against eq. anchor_assignment in float64; a difference must be a
+    # float64 near-tie (certify_flips)
     for b in range(wl.pairs):
         r = ref[b]
         K = host["K"][b]
         np.testing.assert_allclose(phi[b] / phi[b].sum(), r.phi / r.phi.sum(), rtol=1e-4, atol=1e-12)
-        flips = np.flatnonzero(kappa[b] != r.kappa)
-        log(f"  pair {b}: {len(flips)} assignment differences out of {len(K)}")
-        for j in flips:
-            gap = assignment_gap(host["Q"][b], K, r.anchors, s, j, profile_dtype(wl))
-            assert gap <= rel_tie, (b, j, gap)
-        assert len(flips) <= max(1, len(K) // 1000), (b, len(flips))
+        n_flip = certify_flips(kappa[b], r.kappa, host["Q"][b], K, r.anchors, s, log=log)
+        log(f"  pair {b}: {n_flip} assignment differences from the float64 oracle out of {len(K)}")
+        log_assign_stats(st[b], wl.T, t, log=log)
         assert np.all(kappa[b][r.anchors] == np.arange(t))
         # C_k against the oracle merge on the GPU's assignment
         ck_ref = oracle.merge_keys(K, r.phi, kappa[b].astype(np.int64), r.anchors, oracle.LAMBDA_M)
@@ -168,10 +162,18 @@ def test_fit_bias_stagewise(case):
         e_ref = np.linalg.norm(PhiC @ np.exp(bf.beta) - mm) / np.linalg.norm(mm)
         tol = 1e-4 if wl.dtype == "f32" else 5e-3
         assert abs(e_gpu - e_ref) <= tol * max(e_ref, 1e-3), (b, e_gpu, e_ref)
+        # element-wise on the significant weights (w* > 1e-2 max w*): measured
+        # up to 1.7e-4 on these cases, bound 2e-3 (the Grams and the Cholesky
+        # are fp32-accurate and refined against the data)
         big = bf.w_star > 1e-2 * bf.w_star.max()
         rel = np.abs(np.exp(beta[b][big]) - bf.w_star[big]) / bf.w_star[big]
-        log(f"  pair {b}: E_mass gpu {e_gpu:.6f} ref {e_ref:.6f}; w rel err on large weights "
+        log(f"  pair {b}: E_mass gpu {e_gpu:.6f} ref {e_ref:.6f}; w rel err on {big.sum()} large weights "
             f"median {np.median(rel):.2e} max {rel.max():.2e}")
+        assert rel.max() <= 2e-3, (b, rel.max())
+        # weights clipped to zero by the oracle stay negligible on the GPU
+        small = bf.w_star == 0.0
+        if small.any():
+            assert np.exp(beta[b][small]).max() <= 1e-3 * bf.w_star.max(), (b, np.exp(beta[b][small]).max())
 
 
 def test_fit_values_stagewise(case):
@@ -204,16 +206,23 @@ def test_compact_end_to_end(case):
         r = ref[b]
         Q, K = host["Q"][b], host["K"][b]
         S = anchors[b].astype(np.int64)
-        if S.tolist() != r.anchors.tolist():       # boundary near-tie (certified in the select tests)
-            log(f"  pair {b}: anchor sets differ at a near-tie; oracle refits on the GPU's anchors")
-        # the oracle refits on the GPU's anchors and assignment once every
-        # difference is certified as a near-tie of the stored profiles
-        kap_gpu = gpu_assignment(dev["K"][b:b + 1].contiguous(), dev["V"][b:b + 1].contiguous(),
-                                 dev["Q"][b:b + 1].contiguous(), anchors_d[b:b + 1].contiguous(), s)
-        kap_ref, _, _ = oracle.profiles_assign_phi(Q, K, S, s, profile_dtype(wl))
-        certify_flips(kap_gpu, kap_ref, Q, K, S, s, profile_dtype(wl), log=log)
-        rr = oracle.compact_pair(K, host["V"][b], Q, host["W1"][b], host["b1"][b], host["w2"][b], host["b2"][b],
-                                 t=t, scale=s, anchors=S, kappa=kap_gpu, profile_dtype=profile_dtype(wl))
+        rr = r
+        if S.tolist() != r.anchors.tolist():
+            # a boundary score near-tie (the anchor sets may differ only there):
+            # the oracle is rerun, from its own scores, on the GPU's anchors
+            kth = np.sort(r.scores)[::-1][t - 1]
+            for j in set(S.tolist()) ^ set(r.anchors.tolist()):
+                assert abs(r.scores[j] - kth) <= 1e-5 * np.abs(r.scores).max(), j
+            log(f"  pair {b}: anchor sets differ at a certified score near-tie; oracle rerun on the GPU's anchors")
+            rr = oracle.compact_pair(K, host["V"][b], Q, host["W1"][b], host["b1"][b], host["w2"][b], host["b2"][b],
+                                     t=t, scale=s, anchors=S)
+        kap_gpu, st = gpu_assignment(dev["K"][b:b + 1].contiguous(), dev["V"][b:b + 1].contiguous(),
+                                     dev["Q"][b:b + 1].contiguous(), anchors_d[b:b + 1].contiguous(), s)
+        log_assign_stats(st, wl.T, t, log=log)
+        if certify_flips(kap_gpu, rr.kappa, Q, K, S, s, log=log):
+            # only float64 ties differ: both choices satisfy the definition
+            rr = oracle.compact_pair(K, host["V"][b], Q, host["W1"][b], host["b1"][b], host["w2"][b],
+                                     host["b2"][b], t=t, scale=s, anchors=S, kappa=kap_gpu)
         O_gpu = oracle.attend_compact(Q, Ck[b], beta[b], Cv[b], s)
         O_ref = oracle.attend_compact(Q, rr.C_k, rr.beta, rr.C_v, s)
         err = oracle.row_rel_err(O_gpu, O_ref)

@@ -10,7 +10,7 @@ import torch
 
 import oracle
 import synth
-from tests.gpu_common import TOL_OUT, certify_flips, gpu_assignment, make_inputs, np64, profile_dtype
+from tests.gpu_common import TOL_OUT, certify_flips, gpu_assignment, log_assign_stats, make_inputs, np64
 
 pytestmark = pytest.mark.gpu
 
@@ -80,12 +80,14 @@ def test_compact_with_chunked_selection():
         S = oracle.select_topt_chunked(scores[b].astype(np.float64), t_nom, L)
         assert anchors[b].tolist() == S.tolist(), b
         Q, K = host["Q"][b], host["K"][b]
-        kap_gpu = gpu_assignment(dev["K"][b:b + 1].contiguous(), dev["V"][b:b + 1].contiguous(),
-                                 dev["Q"][b:b + 1].contiguous(), anchors_d[b:b + 1].contiguous(), s)
-        kap_ref, _, _ = oracle.profiles_assign_phi(Q, K, S, s, profile_dtype(wl))
-        certify_flips(kap_gpu, kap_ref, Q, K, S, s, profile_dtype(wl))
+        kap_gpu, st = gpu_assignment(dev["K"][b:b + 1].contiguous(), dev["V"][b:b + 1].contiguous(),
+                                     dev["Q"][b:b + 1].contiguous(), anchors_d[b:b + 1].contiguous(), s)
+        log_assign_stats(st, wl.T, t)
         rr = oracle.compact_pair(K, host["V"][b], Q, host["W1"][b], host["b1"][b], host["w2"][b], host["b2"][b],
-                                 t=t, scale=s, anchors=S, kappa=kap_gpu, profile_dtype=profile_dtype(wl))
+                                 t=t, scale=s, anchors=S)
+        if certify_flips(kap_gpu, rr.kappa, Q, K, S, s):
+            rr = oracle.compact_pair(K, host["V"][b], Q, host["W1"][b], host["b1"][b], host["w2"][b], host["b2"][b],
+                                     t=t, scale=s, anchors=S, kappa=kap_gpu)
         err = oracle.row_rel_err(oracle.attend_compact(Q, Ck[b], beta[b], Cv[b], s),
                                  oracle.attend_compact(Q, rr.C_k, rr.beta, rr.C_v, s))
         print(f"  pair {b}: O(Q_ref) max row rel err {err.max():.3e}", flush=True)
