@@ -41,6 +41,16 @@ struct AssignPair {
   double amax;   // max_r ||k_{s_r}||_2
 };
 
+// A fixed grid of nx workgroups per pair, remapped so that each XCD receives a
+// contiguous range of (pair, x): all workgroups of a pair share one L2 (the
+// pair's queries and anchor profiles are read by each of them).
+__device__ inline void pair_block(int nx, int P, int &x, int &b) {
+  const int64_t lin = (int64_t)blockIdx.y * gridDim.x + blockIdx.x;
+  const int64_t tile = xcd_remap(lin, (int64_t)nx * P);
+  b = (int)(tile / nx);
+  x = (int)(tile % nx);
+}
+
 // ---------------------------------------------------------------- norms
 // pn[b] = {max_i ||q_i||, max_r ||k_{s_r}||}, in float64, rounded up by one part
 // in 1e12 so that the bounds built on them stay upper bounds.
@@ -101,13 +111,26 @@ __device__ inline double exp_reduced(double x) {
 }
 constexpr double kExpReducedErr = 2.384185791015625e-07;   // 2^-22
 
+// Logit of one (query, key) element from the eight 16-wide slices of the head
+// dimension: each slice is one MFMA into a zero accumulator (products of bf16
+// values are exact in fp32, so a slice sum is within gamma_16 of the sum of its
+// |products|), and the eight slice sums are added in fp32 in a fixed order, so
+// the logit is within gamma_23 s sum_k |q_k k_k| <= gamma_23 s ||q|| ||k|| of exact.
+constexpr double kSliceTerms = 23.0;
+
+// Relative error bound of exp(s l - z) evaluated as 2^(l c2 - z2) with c2 = s
+// log2(e) and z2 = z log2(e) rounded to fp32, one fp32 fma and v_exp_f32 (1 ulp):
+// the exponent's absolute error is at most u (2 |l c2| + 2 |z2| + |result|)
+// and |result| <= |l c2| + |z2|.  A bounds |l c2|, Z bounds |z2|.
+__device__ inline double exp32_err(double A, double Z) {
+  return 0.6931471805599453 * kU32 * (3.0 * A + 3.0 * Z) + 2.0 * kU32;
+}
+
 // ---------------------------------------------------------------- anchor profiles
 // Precise anchor profiles e_ir = exp(s q_i.k_{s_r} - z_merge) for bf16 inputs:
-// the logit is formed on MFMA with a fresh fp32 accumulator for each 16-wide
-// slice of the head dimension (products of bf16 values are exact in fp32, so
-// each slice sum is within gamma_16 sum_slice |q_k k_k| of exact) and the eight
-// slices are added in float64.  Ua [P][tp][np] float32 (zero for i >= n),
-// anorm [P][tp] = ||e_r||_2 in float64 from the unrounded values.  A workgroup
+// logits from eight MFMA slices added in a fixed order (kSliceTerms), the
+// exponential in fp32 (exp32_err).  Ua [P][tp][np] float32 (zero for i >= n),
+// anorm [P][tp] = ||e_r||_2, accumulated in float64.  A workgroup
 // owns 128 anchors (32 per wave, kept as MFMA B fragments) and sweeps all
 // queries in tiles of 64.
 __global__ void __launch_bounds__(256) k_prof_anchor_bf16(const bf16 *__restrict__ Q, const bf16 *__restrict__ K,
@@ -126,7 +149,7 @@ __global__ void __launch_bounds__(256) k_prof_anchor_bf16(const bf16 *__restrict
 #pragma unroll
   for (int ks = 0; ks < 8; ++ks)
     bfr[ks] = rvalid ? *reinterpret_cast<const bf16x8 *>(kr + ks * 16 + 8 * h) : Mfma<bf16>::zero();
-  const double zm = (double)zmerge[b];
+  const float c2 = (float)(scale * 1.4426950408889634), zs2 = zmerge[b] * 1.4426950408889634f;
   const bf16 *Qb = Q + (size_t)b * n * kHeadDim;
   float *urow = Ua + ((size_t)b * tp + (rvalid ? r : 0)) * np_;
   double ss = 0.0;
@@ -141,21 +164,21 @@ __global__ void __launch_bounds__(256) k_prof_anchor_bf16(const bf16 *__restrict
     __syncthreads();
 #pragma unroll
     for (int ms = 0; ms < 2; ++ms) {
-      f32x16 acc[8];
       const bf16 *arow = &sQ[(32 * ms + col) * SQ + 8 * h];
+      f32x16 lsum = Mfma<bf16>::mma(*reinterpret_cast<const bf16x8 *>(arow), bfr[0], zero16());
 #pragma unroll
-      for (int ks = 0; ks < 8; ++ks)
-        acc[ks] = Mfma<bf16>::mma(*reinterpret_cast<const bf16x8 *>(arow + ks * 16), bfr[ks], zero16());
+      for (int ks = 1; ks < 8; ++ks) {
+        const f32x16 part = Mfma<bf16>::mma(*reinterpret_cast<const bf16x8 *>(arow + ks * 16), bfr[ks], zero16());
+#pragma unroll
+        for (int v = 0; v < 16; ++v) lsum[v] += part[v];
+      }
       float e[16];
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
-        double l = 0.0;
-#pragma unroll
-        for (int ks = 0; ks < 8; ++ks) l += (double)acc[ks][v];
         const int i = i0 + 32 * ms + acc_row(v, lane);
-        const double ev = i < n ? exp_reduced(scale * l - zm) : 0.0;
-        ss = fma(ev, ev, ss);
-        e[v] = (float)ev;
+        const float ev = i < n ? __builtin_amdgcn_exp2f(fmaf(lsum[v], c2, -zs2)) : 0.0f;
+        ss = fma((double)ev, (double)ev, ss);
+        e[v] = ev;
       }
       if (rvalid) {
 #pragma unroll
@@ -226,11 +249,11 @@ __global__ void __launch_bounds__(256) k_anchor_u(const float *__restrict__ Ua, 
 //  bf16 inputs, fp16 operands scaled by 2^15 (S_A = 2^30 S):
 //   E'  logit on MFMA, fp32 accumulation over d: gamma_128 s ||q|| ||k_j||;
 //       exponent argument formed in fp32 and v_exp_f32 (1 ulp); fp16 rounding.
-//   U'  the precise profile (gamma_16 s ||q|| ||k_r|| + 2^-22, stored fp32),
-//       divided by its float64 norm (same bound, unrounded), a fp32 product and
-//       one fp16 rounding.
+//   U'  the precise profile (gamma_23 s ||q|| ||k_r|| + exp32_err, fp32),
+//       divided by its float64 norm (same bound), a fp32 product and one fp16
+//       rounding.
 //   fp16 x fp16 products are exact in fp32; the fp32 accumulation of n >= 0
-//   terms adds gamma_n.  Operands below the fp16 normal range (E' or U' < 2^-14)
+//   terms adds gamma_n; the epilogue truncates the stored value by < 2^-18.  Operands below the fp16 normal range (E' or U' < 2^-14)
 //   carry an absolute error <= 2^-25 instead: alpha = 2^-25 (||U'_r||_1 + ||E'_j||_1)
 //   <= 2^-10 (sqrt(n) + n phi_j), with ||U_r||_2 = 1.
 //  fp32 inputs: fp32 products are rounded (u each, d + 2 terms in the logit and
@@ -248,10 +271,13 @@ __device__ inline BoundA bound_a(bool bf16in, int n, double s, double zm, const 
     const double Z = fabs(zm) * 1.4426950408889634 + (double)kProfLog2Scale;
     const double e_key = gamma_m(kHeadDim) * s * pn.qmax * kn + 0.6931471805599453 * kU32 * (3.0 * A + 4.0 * Z) +
                          2.0 * kU32;
-    const double e_anc = gamma_m(16) * s * pn.qmax * pn.amax + kExpReducedErr;
+    const double e_anc = gamma_m(kSliceTerms) * s * pn.qmax * pn.amax +
+                         exp32_err(s * pn.qmax * pn.amax * 1.4426950408889634 * 1.001, fabs(zm) * 1.4426950408889634);
     const double eE = (1.0 + e_key) * (1.0 + kU16) - 1.0;
     const double eU = (1.0 + e_anc + kU32) / (1.0 - e_anc) * (1.0 + 2.0 * kU32) * (1.0 + kU16) - 1.0;
-    o.eta = (1.0 + eE) * (1.0 + eU) * (1.0 + gamma_m(n)) - 1.0;
+    // the contraction's epilogue stores similarities with the low 5 bits
+    // cleared (relative truncation < 2^-18)
+    o.eta = (1.0 + eE) * (1.0 + eU) * (1.0 + gamma_m(n)) * (1.0 + 3.814697265625e-06) - 1.0;
     o.alpha = 9.765625e-04 * 1.01 * (sqrt((double)n) + (double)n * phi * 1.001) + (double)n * 1e-18;
   } else {
     const double Z = fabs(zm) * 1.4426950408889634;
@@ -400,52 +426,60 @@ __global__ void __launch_bounds__(256) k_assign_finalize(
 
 // ---------------------------------------------------------------- pass C
 // Refine the keys queued by pass A.  A workgroup takes 64 queued keys of one
-// pair and their candidates from the pool, in chunks of CAP.  For every query
-// tile of 64 the keys' profiles are formed and staged in LDS as fp32; each
-// candidate pair accumulates sum_i e_ij e_ir in float64 against the anchor's
-// stored profile, and the similarity e_j . e_r / ||e_r|| goes back to the pool.
-//  bf16 inputs: logits on MFMA as in k_prof_anchor_bf16 (one accumulator per
-//   16-wide slice, summed in float64; exponentials within 2^-22).  Bound of one
-//   similarity: (1 + eps_k)(1 + eps_a)/(1 - eps_n) - 1 with eps_k = gamma_16 s
-//   ||q|| ||k_j|| + 2^-22 + u (fp32 staging), eps_a = gamma_16 s ||q|| max ||k_r||
-//   + 2^-22 + u, eps_n the same without the staging term.
+// pair and their candidates from the pool, in chunks of CAP.  The keys'
+// profiles are formed in fp32 and each candidate pair accumulates
+// sum_i e_ij e_ir (fp32 products summed four at a time, then in float64)
+// against the anchor's stored profile; the similarity e_j . e_r / ||e_r|| goes
+// back to the pool.
+//  bf16 inputs: logits from eight MFMA slices as in k_prof_anchor_bf16
+//   (kSliceTerms), exponentials within exp32_err.  Bound of one similarity:
+//   (1 + eps_k)(1 + eps_a)/(1 - eps_a)(1 + gamma_4) - 1 with eps_k = gamma_23 s
+//   ||q|| ||k_j|| + exp32_err and eps_a the same with max ||k_r|| (profile and norm).
 //  fp32 inputs: float64 logits and exponentials; the bound is the fp32
-//   rounding of the staged and stored profiles.
+//   rounding of the two profiles and of the partial products.
 // A key whose best similarity exceeds every other candidate's by more than the
 // bound on both is decided; the survivors of the others go to pass D.
 // Work distribution: a fixed grid of kRefineBlocks workgroups per pair, each
-// taking the groups of 64 queued keys g = blockIdx.x, blockIdx.x + kRefineBlocks, ...
-// A candidate's dot product is split over 16 lanes that read 16-byte pieces of
-// one anchor row (256 contiguous bytes per query tile) and reduce at the end.
+// taking the groups of 64 queued keys g = blockIdx.x, blockIdx.x + kRefineBlocks,
+// ...  Each wave owns a quarter of the queries and works through it without
+// workgroup barriers: for 32 queries at a time it forms the 64 keys' profiles
+// (two 32 x 32 MFMA tiles) into a wave-private LDS tile and accumulates the
+// dot products of CAP candidates (two per lane); the four waves' partial sums
+// meet once at the end.
 constexpr int kRefineBlocks = 32;
 
 template <typename E>
-__global__ void __launch_bounds__(256) k_assign_refine(const E *__restrict__ Q, const E *__restrict__ K,
+__global__ void __launch_bounds__(256, 2) k_assign_refine(const E *__restrict__ Q, const E *__restrict__ K,
                                                        const float *__restrict__ zmerge,
                                                        const AssignPair *__restrict__ pn,
                                                        const float *__restrict__ Ua, const double *__restrict__ anorm,
                                                        int T, int t, int n, int64_t tp, int64_t np_, double s,
                                                        int32_t *__restrict__ kappa, AssignLists L) {
   constexpr bool BF = sizeof(E) == 2;
-  constexpr int NK = 64, CAP = 256, NSLOT = CAP / 16, SE = 64 + 4, SQF = kHeadDim + 4;
+  constexpr int NK = 64, CAP = 128, NQW = 32, SE = NQW + 4, NCL = CAP / 64;
+  constexpr int SKB = BF ? kHeadDim + 8 : kHeadDim + 4;   // key-row stride (elements)
   __shared__ int32_t kpos[NK], koff[NK], kbase[NK + 1];
   __shared__ int32_t cr[CAP];
   __shared__ uint8_t ck[CAP];
   __shared__ double kn[NK];
-  __shared__ __attribute__((aligned(16))) float eT[NK * SE];
-  __shared__ __attribute__((aligned(16))) float sQf[BF ? 4 : 64 * SQF];   // fp32 inputs: the query tile
-  const int b = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  __shared__ __attribute__((aligned(16))) E sK[NK * SKB];
+  __shared__ __attribute__((aligned(16))) float eW[4][NK * SE];   // wave-private profile tiles
+  __shared__ double red[4][CAP];
+  int bx, b;
+  pair_block(kRefineBlocks, gridDim.y, bx, b);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int h = lane >> 5, col = lane & 31;
-  const int gid = tid >> 4, li = tid & 15;   // candidate lane group and lane within it
   const int F = L.fcnt[b];
   const AssignPair pp = pn[b];
   const double zm = (double)zmerge[b];
+  const float c2 = (float)(s * 1.4426950408889634), zs2 = zmerge[b] * 1.4426950408889634f;
   const E *Qb = Q + (size_t)b * n * kHeadDim;
   const float *Uab = Ua + (size_t)b * tp * np_;
   int32_t *pool = L.pool + (size_t)b * L.pcap;
   double *psim = L.psim + (size_t)b * L.pcap;
-  const int kb = 32 * (wave & 1), qb = 32 * (wave >> 1);   // MFMA tile: keys kb.., queries qb.. of a query tile
-  for (int f0 = blockIdx.x * NK; f0 < F; f0 += kRefineBlocks * NK) {   // uniform over the workgroup
+  float *ew = eW[wave];
+  const int64_t qw = np_ / 4, qlo = wave * qw;   // this wave's queries
+  for (int f0 = bx * NK; f0 < F; f0 += kRefineBlocks * NK) {   // uniform over the workgroup
     const int nk = min(NK, F - f0);
     __syncthreads();   // the previous group is done with the shared arrays
     if (tid < NK) {
@@ -467,20 +501,15 @@ __global__ void __launch_bounds__(256) k_assign_refine(const E *__restrict__ Q, 
       }
       kbase[NK] = acc;
     }
+    for (int x = tid; x < NK * kHeadDim; x += 256) {   // the keys' rows (zero for empty slots)
+      const int k = x / kHeadDim, c = x % kHeadDim;
+      sK[k * SKB + c] = kpos[k] >= 0 ? K[((size_t)b * T + kpos[k]) * kHeadDim + c] : (E)0.0f;
+    }
     __syncthreads();
     const int total = kbase[NK];
-    const int kp = kpos[kb + col];
-    const E *krow = K + ((size_t)b * T + (kp >= 0 ? kp : 0)) * kHeadDim;
-    bf16x8 bfr[8];
-    if constexpr (BF) {
-#pragma unroll
-      for (int ks = 0; ks < 8; ++ks)
-        bfr[ks] = kp >= 0 ? *reinterpret_cast<const bf16x8 *>(reinterpret_cast<const bf16 *>(krow) + ks * 16 + 8 * h)
-                          : Mfma<bf16>::zero();
-    }
     for (int c0 = 0; c0 < total; c0 += CAP) {
       const int cn = min(CAP, total - c0);
-      __syncthreads();   // the previous chunk is done with cr / ck
+      __syncthreads();   // the previous chunk is done with cr / ck / red
       for (int c = tid; c < cn; c += 256) {
         const int g = c0 + c;
         int lo = 0, hi = NK;   // the key k with kbase[k] <= g < kbase[k + 1]
@@ -492,79 +521,94 @@ __global__ void __launch_bounds__(256) k_assign_refine(const E *__restrict__ Q, 
         ck[c] = (uint8_t)lo;
         cr[c] = pool[koff[lo] + g - kbase[lo]];
       }
-      double dacc[NSLOT];
+      __syncthreads();
+      int kc[NCL];
+      const float *uc[NCL];
+      double dc[NCL];
 #pragma unroll
-      for (int u = 0; u < NSLOT; ++u) dacc[u] = 0.0;
-      for (int i0 = 0; i0 < np_; i0 += 64) {
-        double l[16];
-        if constexpr (BF) {
-          const int iq = i0 + qb + col;
-          bf16x8 afr[8];
+      for (int u = 0; u < NCL; ++u) {
+        const int c = lane + 64 * u;
+        kc[u] = c < cn ? ck[c] : -1;
+        uc[u] = Uab + (size_t)(c < cn ? cr[c] : 0) * np_;
+        dc[u] = 0.0;
+      }
+      for (int64_t i0 = qlo; i0 < qlo + qw; i0 += NQW) {
+        const int iq = (int)i0 + col;   // this lane's query row of the MFMA A operand
+#pragma unroll 1
+        for (int kt = 0; kt < 2; ++kt) {
+          double l[BF ? 1 : 16];
+          if constexpr (!BF) {
 #pragma unroll
-          for (int ks = 0; ks < 8; ++ks)
-            afr[ks] = iq < n ? *reinterpret_cast<const bf16x8 *>(reinterpret_cast<const bf16 *>(Qb) +
-                                                                 (size_t)iq * kHeadDim + ks * 16 + 8 * h)
-                             : Mfma<bf16>::zero();
-          f32x16 acc[8];
+            for (int v = 0; v < 16; ++v) l[v] = 0.0;
+          }
+          f32x16 lsum;
+          if constexpr (BF) {
+            const bf16 *qrow = reinterpret_cast<const bf16 *>(Qb) + (size_t)(iq < n ? iq : 0) * kHeadDim + 8 * h;
+            const bf16 *krow = reinterpret_cast<const bf16 *>(sK) + (kt * 32 + col) * SKB + 8 * h;
 #pragma unroll
-          for (int ks = 0; ks < 8; ++ks) acc[ks] = Mfma<bf16>::mma(afr[ks], bfr[ks], zero16());
+            for (int ks = 0; ks < 8; ++ks) {
+              const bf16x8 a = iq < n ? *reinterpret_cast<const bf16x8 *>(qrow + ks * 16) : Mfma<bf16>::zero();
+              const bf16x8 bk = *reinterpret_cast<const bf16x8 *>(krow + ks * 16);
+              const f32x16 part = Mfma<bf16>::mma(a, bk, zero16());
+              if (ks == 0) lsum = part;
+              else {
+#pragma unroll
+                for (int v = 0; v < 16; ++v) lsum[v] += part[v];
+              }
+            }
+          } else {
+            const float *krow = reinterpret_cast<const float *>(sK) + (kt * 32 + col) * SKB;
+            for (int k = 0; k < kHeadDim; k += 4) {
+              const f32x4 kv = *reinterpret_cast<const f32x4 *>(krow + k);
+#pragma unroll
+              for (int v = 0; v < 16; ++v) {
+                const int qi = (int)i0 + acc_row(v, lane);
+                if (qi < n) {
+                  const f32x4 qv = *reinterpret_cast<const f32x4 *>(reinterpret_cast<const float *>(Qb) +
+                                                                   (size_t)qi * kHeadDim + k);
+#pragma unroll
+                  for (int e = 0; e < 4; ++e) l[v] = fma((double)qv[e], (double)kv[e], l[v]);
+                }
+              }
+            }
+          }
 #pragma unroll
           for (int v = 0; v < 16; ++v) {
-            double x = 0.0;
-#pragma unroll
-            for (int ks = 0; ks < 8; ++ks) x += (double)acc[ks][v];
-            l[v] = x;
+            const int qi = acc_row(v, lane);
+            float ev = 0.0f;
+            if (i0 + qi < n) {
+              if constexpr (BF) ev = __builtin_amdgcn_exp2f(fmaf(lsum[v], c2, -zs2));
+              else ev = (float)exp(s * l[v] - zm);
+            }
+            ew[(kt * 32 + col) * SE + qi] = ev;
           }
-          __syncthreads();   // the previous tile's dot products are done with eT
-        } else {
-          __syncthreads();   // the previous tile is done with sQf and eT
-          for (int x = tid; x < 64 * kHeadDim; x += 256) {
-            const int rr = x / kHeadDim, cc = x % kHeadDim;
-            sQf[rr * SQF + cc] = i0 + rr < n ? (float)Qb[(size_t)(i0 + rr) * kHeadDim + cc] : 0.0f;
-          }
-          __syncthreads();
+        }
+        __builtin_amdgcn_wave_barrier();   // the wave's LDS writes before its reads (in-order per wave)
+        asm volatile("" ::: "memory");
+#pragma unroll 2
+        for (int q4 = 0; q4 < NQW / 4; ++q4) {
 #pragma unroll
-          for (int v = 0; v < 16; ++v) l[v] = 0.0;
-          for (int k = 0; k < kHeadDim; k += 4) {
-            const f32x4 kv = *reinterpret_cast<const f32x4 *>(reinterpret_cast<const float *>(krow) + k);
+          for (int u = 0; u < NCL; ++u) {
+            if (kc[u] >= 0) {
+              const f32x4 e4 = *reinterpret_cast<const f32x4 *>(&ew[kc[u] * SE + 4 * q4]);
+              const f32x4 w = *reinterpret_cast<const f32x4 *>(uc[u] + i0 + 4 * q4);
+              float p4 = e4[0] * w[0];   // four non-negative products in fp32 (within gamma_4), then float64
 #pragma unroll
-            for (int v = 0; v < 16; ++v) {
-              const f32x4 qv = *reinterpret_cast<const f32x4 *>(&sQf[(qb + acc_row(v, lane)) * SQF + k]);
-#pragma unroll
-              for (int e = 0; e < 4; ++e) l[v] = fma((double)qv[e], (double)kv[e], l[v]);
+              for (int e = 1; e < 4; ++e) p4 = fmaf(e4[e], w[e], p4);
+              dc[u] += (double)p4;
             }
           }
         }
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int qi = qb + acc_row(v, lane);
-          float ev = 0.0f;
-          if (i0 + qi < n) ev = BF ? (float)exp_reduced(s * l[v] - zm) : (float)exp(s * l[v] - zm);
-          eT[(kb + col) * SE + qi] = ev;
-        }
-        __syncthreads();
-#pragma unroll
-        for (int u = 0; u < NSLOT; ++u) {
-          const int c = u * 16 + gid;
-          if (c < cn) {
-            const f32x4 e4 = *reinterpret_cast<const f32x4 *>(&eT[(int)ck[c] * SE + 4 * li]);
-            const f32x4 w = *reinterpret_cast<const f32x4 *>(Uab + (size_t)cr[c] * np_ + i0 + 4 * li);
-            double d = dacc[u];
-#pragma unroll
-            for (int e = 0; e < 4; ++e) d = fma((double)e4[e], (double)w[e], d);
-            dacc[u] = d;
-          }
-        }
+        __builtin_amdgcn_wave_barrier();   // reads done before the next tile overwrites the wave's tile
+        asm volatile("" ::: "memory");
       }
 #pragma unroll
-      for (int u = 0; u < NSLOT; ++u) {
-        double d = dacc[u];
-        for (int m = 8; m >= 1; m >>= 1) d += __shfl_xor(d, m, 64);
-        const int c = u * 16 + gid;
-        if (li == 0 && c < cn) {
-          const int k = ck[c];
-          psim[koff[k] + c0 + c - kbase[k]] = d / anorm[(size_t)b * tp + cr[c]];
-        }
+      for (int u = 0; u < NCL; ++u) red[wave][lane + 64 * u] = dc[u];
+      __syncthreads();
+      for (int c = tid; c < cn; c += 256) {
+        const double d = red[0][c] + red[1][c] + red[2][c] + red[3][c];
+        const int k = ck[c];
+        psim[koff[k] + c0 + c - kbase[k]] = d / anorm[(size_t)b * tp + cr[c]];
       }
     }
     __syncthreads();   // every similarity of the group's keys is in the pool
@@ -576,13 +620,12 @@ __global__ void __launch_bounds__(256) k_assign_refine(const E *__restrict__ Q, 
           best = c;
       double eta;
       if constexpr (BF) {
-        const double g16 = gamma_m(16) * s * pp.qmax;
-        const double ek = g16 * kn[tid] + kExpReducedErr + kU32;
-        const double ea = g16 * pp.amax + kExpReducedErr + kU32;
-        const double en = g16 * pp.amax + kExpReducedErr;
-        eta = (1.0 + ek) * (1.0 + ea) / (1.0 - en) * (1.0 + 1e-12) - 1.0;
+        const double g = gamma_m(kSliceTerms) * s * pp.qmax, Z = fabs(zm) * 1.4426950408889634;
+        const double ek = g * kn[tid] + exp32_err(s * pp.qmax * kn[tid] * 1.4426950408889634 * 1.001, Z);
+        const double ea = g * pp.amax + exp32_err(s * pp.qmax * pp.amax * 1.4426950408889634 * 1.001, Z);
+        eta = (1.0 + ek) * (1.0 + ea) / (1.0 - ea) * (1.0 + gamma_m(4)) * (1.0 + 1e-12) - 1.0;
       } else {
-        eta = 2.0 * kU32 + 1e-12;
+        eta = 3.0 * kU32 + gamma_m(4) + 1e-12;
       }
       const double bs = psim[o + best];
       const double thc = bs * (1.0 - eta) / (1.0 + eta) - 1e-300;
@@ -621,9 +664,9 @@ __global__ void __launch_bounds__(256) k_assign_exact(const E *__restrict__ Q, c
                                                       const int32_t *__restrict__ anchors,
                                                       const float *__restrict__ zmerge, int T, int t, int n, double s,
                                                       int32_t *__restrict__ kappa, AssignLists L) {
-  constexpr int NV = 32, NQ = 32, SK = kHeadDim + 1;
-  __shared__ float sK[NV * SK];
-  __shared__ float sQ[NQ * SK];
+  constexpr int NV = 32, NQ = 64, SK = kHeadDim + 4;
+  __shared__ __attribute__((aligned(16))) float sK[NV * SK];
+  __shared__ __attribute__((aligned(16))) float sQ[NQ * SK];
   __shared__ double sE[NV * (NQ + 1)];
   __shared__ int32_t vpos[NV], vown[NV], vr[NV];
   __shared__ double vdot[NV], vnn[NV];
@@ -632,16 +675,27 @@ __global__ void __launch_bounds__(256) k_assign_exact(const E *__restrict__ Q, c
   __shared__ int32_t nv_s, nseg_s, di_s, ci_s, done_s;
   __shared__ double run_sim;
   __shared__ int32_t run_r;
-  const int b = blockIdx.y, tid = threadIdx.x;
+  int bx, b;
+  pair_block(kExactBlocks, gridDim.y, bx, b);
+  const int tid = threadIdx.x;
   const int D = L.dcnt[b];
   const int32_t *S = anchors + (size_t)b * t;
   const double zm = (double)zmerge[b];
   const E *Qb = Q + (size_t)b * n * kHeadDim;
   auto n_cand = [&](int di) { return L.dn[(size_t)b * L.cap + di]; };
   auto cand_at = [&](int di, int ci) { return L.dent[((size_t)b * L.cap + di) * kAssignMaxD + ci]; };
-  // register tile of the logit pass: vectors tv, tv + 16 and queries tq, tq + 16
+  // register tile of the logit pass: vectors tv, tv + 16 and queries tq + 16 m, m = 0..3
   const int tv = tid >> 4, tq = tid & 15;
-  for (int g0 = blockIdx.x * kExactGroup; g0 < D; g0 += kExactBlocks * kExactGroup) {
+  // rows of 128 elements of E as 4 floats per thread-step (bf16: 4 values = 8 bytes)
+  auto load4 = [](const E *p) -> f32x4 {
+    if constexpr (sizeof(E) == 2) {
+      const bf16x4 v = *reinterpret_cast<const bf16x4 *>(p);
+      return f32x4{(float)v[0], (float)v[1], (float)v[2], (float)v[3]};
+    } else {
+      return *reinterpret_cast<const f32x4 *>(p);
+    }
+  };
+  for (int g0 = bx * kExactGroup; g0 < D; g0 += kExactBlocks * kExactGroup) {
     const int g1 = min(D, g0 + kExactGroup);
     __syncthreads();   // every thread has left the previous group's loop
     if (tid == 0) {
@@ -683,9 +737,10 @@ __global__ void __launch_bounds__(256) k_assign_exact(const E *__restrict__ Q, c
       }
       __syncthreads();
       const int nv = nv_s;
-      for (int x = tid; x < NV * kHeadDim; x += 256) {
-        const int v = x / kHeadDim, k = x % kHeadDim;
-        sK[v * SK + k] = v < nv ? (float)K[((size_t)b * T + vpos[v]) * kHeadDim + k] : 0.0f;
+      for (int x = tid; x < NV * kHeadDim / 4; x += 256) {
+        const int v = x / (kHeadDim / 4), k = 4 * (x % (kHeadDim / 4));
+        const f32x4 w = v < nv ? load4(K + ((size_t)b * T + vpos[v]) * kHeadDim + k) : f32x4{0.f, 0.f, 0.f, 0.f};
+        *reinterpret_cast<f32x4 *>(&sK[v * SK + k]) = w;
       }
       if (tid < NV) {
         vdot[tid] = 0.0;
@@ -693,25 +748,37 @@ __global__ void __launch_bounds__(256) k_assign_exact(const E *__restrict__ Q, c
       }
       for (int i0 = 0; i0 < n; i0 += NQ) {
         __syncthreads();
-        for (int x = tid; x < NQ * kHeadDim; x += 256) {
-          const int q = x / kHeadDim, k = x % kHeadDim;
-          sQ[q * SK + k] = i0 + q < n ? (float)Qb[(size_t)(i0 + q) * kHeadDim + k] : 0.0f;
+        for (int x = tid; x < NQ * kHeadDim / 4; x += 256) {
+          const int q = x / (kHeadDim / 4), k = 4 * (x % (kHeadDim / 4));
+          const f32x4 w = i0 + q < n ? load4(Qb + (size_t)(i0 + q) * kHeadDim + k) : f32x4{0.f, 0.f, 0.f, 0.f};
+          *reinterpret_cast<f32x4 *>(&sQ[q * SK + k]) = w;
         }
         __syncthreads();
-        double l00 = 0.0, l01 = 0.0, l10 = 0.0, l11 = 0.0;
-        for (int k = 0; k < kHeadDim; ++k) {
-          const double a0 = (double)sK[tv * SK + k], a1 = (double)sK[(tv + 16) * SK + k];
-          const double q0 = (double)sQ[tq * SK + k], q1 = (double)sQ[(tq + 16) * SK + k];
-          l00 = fma(a0, q0, l00);
-          l01 = fma(a0, q1, l01);
-          l10 = fma(a1, q0, l10);
-          l11 = fma(a1, q1, l11);
+        double l[2][4];
+#pragma unroll
+        for (int a = 0; a < 2; ++a)
+#pragma unroll
+          for (int m = 0; m < 4; ++m) l[a][m] = 0.0;
+        for (int k = 0; k < kHeadDim; k += 4) {
+          const f32x4 k0 = *reinterpret_cast<const f32x4 *>(&sK[tv * SK + k]);
+          const f32x4 k1 = *reinterpret_cast<const f32x4 *>(&sK[(tv + 16) * SK + k]);
+#pragma unroll
+          for (int m = 0; m < 4; ++m) {
+            const f32x4 qv = *reinterpret_cast<const f32x4 *>(&sQ[(tq + 16 * m) * SK + k]);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              l[0][m] = fma((double)k0[e], (double)qv[e], l[0][m]);
+              l[1][m] = fma((double)k1[e], (double)qv[e], l[1][m]);
+            }
+          }
         }
-        const bool in0 = i0 + tq < n, in1 = i0 + tq + 16 < n;
-        sE[tv * (NQ + 1) + tq] = tv < nv && in0 ? exp(s * l00 - zm) : 0.0;
-        sE[tv * (NQ + 1) + tq + 16] = tv < nv && in1 ? exp(s * l01 - zm) : 0.0;
-        sE[(tv + 16) * (NQ + 1) + tq] = tv + 16 < nv && in0 ? exp(s * l10 - zm) : 0.0;
-        sE[(tv + 16) * (NQ + 1) + tq + 16] = tv + 16 < nv && in1 ? exp(s * l11 - zm) : 0.0;
+#pragma unroll
+        for (int a = 0; a < 2; ++a)
+#pragma unroll
+          for (int m = 0; m < 4; ++m) {
+            const int v = tv + 16 * a, q = tq + 16 * m;
+            sE[v * (NQ + 1) + q] = v < nv && i0 + q < n ? exp(s * l[a][m] - zm) : 0.0;
+          }
         __syncthreads();
         if (tid < nv && vown[tid] >= 0) {
           const int o = vown[tid];

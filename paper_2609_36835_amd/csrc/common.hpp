@@ -125,6 +125,8 @@ struct Top3 {
     r2 = nr2;
   }
 };
+// Median of three (the compiler forms v_med3_u32 from this pattern).
+__device__ inline uint32_t med3u(uint32_t a, uint32_t b, uint32_t c) { return max(min(a, b), min(max(a, b), c)); }
 __device__ inline uint64_t pack_sim(float v, uint32_t r) {
   return v < 0.0f ? 0ull : (((uint64_t)__float_as_uint(v) << 32) | (uint64_t)(0xFFFFFFFFu - r));
 }

@@ -267,19 +267,33 @@ struct EpiArgmaxBig {
     uint64_t *red2 = red1 + WM * BN;                             // [WM][BN]
     uint32_t *red3 = reinterpret_cast<uint32_t *>(red2 + WM * BN);
     const int h = lane >> 5, col = lane & 31;
+    // Per lane and column, the top three of its 32 values as uint32 keys: the
+    // similarity's bits with the low 5 cleared (a relative truncation below
+    // 2^-18, which the decision bound includes) and 31 - position in the low 5,
+    // so max / med3 keep the larger value and, among equal keys, the lower r.
+    const bool all_valid = row0 + 32 * TM <= t;   // wave-uniform
 #pragma unroll
     for (int j = 0; j < TN; ++j) {
-      Top3 tp;
-      tp.init();
+      uint32_t q1 = 0u, q2 = 0u, q3 = 0u;
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
-          const int r = row0 + 32 * i + acc_row(v, lane);
-          tp.add(acc[i][j][v], (uint32_t)r, r < t);
+          uint32_t key = (__float_as_uint(acc[i][j][v]) & ~31u) | (uint32_t)(31 - (16 * i + v));
+          if (!all_valid) key = row0 + 32 * i + acc_row(v, lane) < t ? key : 0u;
+          const uint32_t n2 = med3u(q1, q2, key);
+          q3 = med3u(q2, q3, key);
+          q2 = n2;
+          q1 = max(q1, key);
         }
-      uint64_t k1 = pack_sim(tp.v1, tp.r1), k2 = pack_sim(tp.v2, tp.r2);
-      uint32_t k3 = tp.v3 < 0.0f ? 0u : __float_as_uint(tp.v3);
+      auto unpack = [&](uint32_t q) -> uint64_t {
+        if (q == 0u) return 0ull;
+        const int pos = 31 - (int)(q & 31u);
+        const int r = row0 + 32 * (pos >> 4) + acc_row(pos & 15, lane);
+        return ((uint64_t)(q & ~31u) << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)r);
+      };
+      uint64_t k1 = unpack(q1), k2 = unpack(q2);
+      uint32_t k3 = q3 & ~31u;
       merge_top3(k1, k2, k3, __shfl_xor(k1, 32, 64), __shfl_xor(k2, 32, 64), __shfl_xor(k3, 32, 64));
       if (h == 0) {
         const int c = wm * BN + wn * 32 * TN + 32 * j + col;
