@@ -30,11 +30,15 @@
  *    arckv_workspace_size() bytes, 256-byte aligned.  Its contents are
  *    undefined on entry and exit (apart from the counters arckv_assign_stats
  *    reads); it must not be shared by calls that may overlap in time.
- *  - All device work is enqueued on the caller's stream; no entry point
- *    synchronises the host, with one exception: the exact non-negative mass
- *    fit (arckv_fit_params.bias_mode = 1) reads two integers back once per
- *    pivoting iteration, to size the next iteration's system and to stop when
- *    every pair has settled.  Results are valid once the stream reaches them.
+ *  - All device work is enqueued on the caller's stream.  The host is
+ *    synchronised only where the next launches depend on a device result: the
+ *    fits read back the number of pairs to refactor (a failed Cholesky pivot;
+ *    in the mass fit also a cut-off refinement) before each possible
+ *    ridge-escalation round (not with max_escalations = 0), and the
+ *    exact non-negative mass fit (bias_mode = 1) reads two integers back once
+ *    per pivoting iteration, to size the next iteration's system and to stop
+ *    when every pair has settled.  Results are valid once the stream reaches
+ *    them.
  *  - Argument errors are returned synchronously BEFORE any HIP call, so they can
  *    be checked on a machine without a GPU.  A failed kernel launch returns
  *    ARCKV_ERR_HIP.  Numerical failures are reported asynchronously in the
@@ -56,7 +60,7 @@ extern "C" {
 typedef enum {
   ARCKV_OK = 0,
   ARCKV_ERR_INVALID_ARG = 1,   /* null pointer, bad size, t outside [1, T], ... */
-  ARCKV_ERR_UNSUPPORTED = 2,   /* d != 128, unknown dtype, bias_mode != 0, ... */
+  ARCKV_ERR_UNSUPPORTED = 2,   /* d != 128, unknown dtype, bias_mode outside {0, 1}, ... */
   ARCKV_ERR_WORKSPACE = 3,     /* ws too small or misaligned */
   ARCKV_ERR_HIP = 4            /* a HIP launch or runtime call failed */
 } arckv_status;
@@ -101,11 +105,17 @@ typedef struct {
   int32_t bias_mode;     /* 0 = projected least squares (eq. mass_fit, the paper's: w* = max(w~, 0));
                           * 1 = exact non-negative least squares on the same ridged system, by block
                           * principal pivoting; other values unsupported */
-  int32_t max_escalations; /* ridge x10 retries after a failed Cholesky pivot, 0..6; default 3 */
+  int32_t max_escalations; /* ridge x10 retries (from 1e-7 when the ridge is 0) after a failed
+                            * Cholesky pivot or a cut-off mass-fit refinement, 0..6; default 6 */
   int32_t refine_steps;  /* iterative-refinement steps after each Cholesky solve, 0..4; default 2.
                           * Each step recomputes the residual from the data (Phi_C, P_hat),
                           * not from the float32 Gram, so the solves converge to the
-                          * least-squares solutions of the exact normal equations. */
+                          * least-squares solutions of the exact normal equations.  In the
+                          * mass fit a step whose data residual (above 1e-10 |h|) does not
+                          * at least halve is undone and ends the refinement; the pair is
+                          * then refactored with the ridge raised tenfold, as after a failed
+                          * pivot (a ridge small next to the float32 rounding of a
+                          * rank-deficient Gram, t > n, makes the steps diverge). */
   int32_t pair_chunk;    /* pairs processed together by arckv_compact (0 = all B); sizes the workspace */
   int32_t select_chunk;  /* 0 = global top-t (default).  L > 0: when T > 10,000, anchors are the union of
                           * each L-position chunk's local top-t_c (Appendix A.3), so arckv_compact keeps
@@ -229,32 +239,50 @@ arckv_status arckv_merge(const arckv_problem *prob, const void *K, const void *Q
  * w >= 0 (lam the ridge settled by the factorisation above), found by block
  * principal pivoting: each iteration refactors the system restricted to the
  * current free set and solves it with refinement against the data.
+ *   K, V  [B][T][d] the cache; read only when z or m is NULL.
+ *   z, m  [B][n] row maxima and masses from arckv_rowstats, or NULL: both are then
+ *         recomputed from K, V and Q_ref (arckv_rowstats) into the workspace.
  *   beta  [B][t] output.
- *   info  [B] output: 0 = ok, k > 0 = Cholesky pivot k failed after all ridge
- *         escalations, -2 = bias_mode 1 did not settle within nnls_max_iter
- *         iterations (beta is NaN in both cases).
- *   delta_used [B] output (may be NULL): the relative ridge actually used. */
-arckv_status arckv_fit_bias(const arckv_problem *prob, const void *Q_ref, const float *C_k,
-                            int32_t t, const float *z, const float *m,
-                            const arckv_fit_params *p, float *beta, int32_t *info,
-                            float *delta_used, void *ws, size_t ws_bytes, hipStream_t stream);
+ *   info  [B] output: 0 = ok; k > 0 = Cholesky pivot k failed after all ridge
+ *         escalations; -1 = a non-finite value in z, m or C_k (the pair is not
+ *         fitted); -2 = bias_mode 1 did not settle within nnls_max_iter
+ *         iterations.  beta is NaN whenever info != 0.
+ *   delta_used [B] output (may be NULL): the relative ridge actually used.
+ * Ridge escalation: a pair whose factorisation fails, or whose refinement is
+ * cut off (refine_steps), is refactored with the ridge raised tenfold (from
+ * 1e-7 when delta_beta = 0), at most p->max_escalations times in all.  Before
+ * each such round the call reads back one integer (the number of pairs to
+ * refactor) and synchronises the stream; with max_escalations = 0 it never
+ * synchronises. */
+arckv_status arckv_fit_bias(const arckv_problem *prob, const void *K, const void *V, const void *Q_ref,
+                            const float *C_k, int32_t t, const float *z, const float *m,
+                            const arckv_fit_params *p, float *beta, int32_t *info, float *delta_used,
+                            void *ws, size_t ws_bytes, hipStream_t stream);
 
 /* Stage 4: compact values (Appendix A.9, eq. value_lstsq).  With
  * P_hat = softmax(s Q C_k^T + 1 beta^T): C_v solves
  * (A + delta_v tr(A)/t I) C_v = P_hat^T Y, A = P_hat^T P_hat.
- *   Y     [B][n][d] full-attention outputs from arckv_rowstats.
+ *   K, V  [B][T][d] the cache; read only when Y is NULL.
+ *   Y     [B][n][d] full-attention outputs from arckv_rowstats, or NULL:
+ *         recomputed from K, V and Q_ref into the workspace.
  *   C_v   [B][t][d] output.
- *   info / delta_used as for arckv_fit_bias. */
-arckv_status arckv_fit_values(const arckv_problem *prob, const void *Q_ref, const float *C_k,
-                              const float *beta, int32_t t, const float *Y,
-                              const arckv_fit_params *p, float *C_v, int32_t *info,
-                              float *delta_used, void *ws, size_t ws_bytes, hipStream_t stream);
+ *   info  [B] output: 0 = ok; k > 0 = Cholesky pivot k failed after all ridge
+ *         escalations; -1 = a non-finite value in Y, C_k or beta (a failed mass
+ *         fit leaves beta NaN, so its pair reports -1 here).  C_v is NaN
+ *         whenever info != 0.
+ *   delta_used and the escalation rounds as for arckv_fit_bias. */
+arckv_status arckv_fit_values(const arckv_problem *prob, const void *K, const void *V, const void *Q_ref,
+                              const float *C_k, const float *beta, int32_t t, const float *Y,
+                              const arckv_fit_params *p, float *C_v, int32_t *info, float *delta_used,
+                              void *ws, size_t ws_bytes, hipStream_t stream);
 
 /* The whole per-context path for B pairs: score, select, row statistics,
  * merge, mass fit, value fit.  t = arckv_budget(T, rho) (or, with
  * p->select_chunk, arckv_select_count of it) is written to *t_out (host
  * pointer) before any device work.  Outputs: anchors [B][t], C_k [B][t][d],
- * beta [B][t], C_v [B][t][d], info [B][2] (mass-fit, value-fit status as above).
+ * beta [B][t], C_v [B][t][d], info [B][2] (mass-fit, value-fit status as above;
+ * a non-finite value anywhere in K, V or Q_ref reaches the row statistics and
+ * the pair reports -1 in both).
  * Pairs are processed p->pair_chunk at a time (0 = all at once). */
 arckv_status arckv_compact(const arckv_problem *prob, const void *K, const void *V,
                            const void *Q_ref, const arckv_indexer *ix, double rho,
@@ -304,12 +332,15 @@ arckv_status arckv_compact_scored(const arckv_problem *prob, const void *K, cons
  * similarities go to the lowest r).  Copies [B][8] int32 to the device array
  * stats, per pair: [0] keys flagged after the first pass, [1] keys decided in
  * float64, [2] candidate anchors of the flagged keys (a whole anchor tile
- * counts 256), [3] keys left undecided (more candidates than the later passes
- * take; such a key keeps the best similarity of the last pass that saw it, and
- * 0 is expected), [4] and [5] the undecided ones of the first and of the
- * refine pass, [6] keys sent to the refine pass, [7] flagged keys with a whole
- * anchor tile among their candidates.  Those counters are the only workspace
- * contents that outlive a call. */
+ * counts its 256 (bf16) or 128 (float32) anchors), [3] keys left undecided
+ * (no finite similarity reaches the first pass's bound, which takes a
+ * non-finite input; such a key keeps the first pass's best), [4] and [5] the
+ * undecided ones of the first and of the refine pass ([5] stays 0: the refine
+ * pass sends every key's survivors, however many, to the float64 pass, and a
+ * key whose candidates overflow the candidate pool goes there with all t
+ * anchors), [6] keys sent to the refine pass, [7]
+ * flagged keys with a whole anchor tile among their candidates.  Those
+ * counters are the only workspace contents that outlive a call. */
 arckv_status arckv_assign_stats(const arckv_problem *prob, int32_t t, const void *ws, size_t ws_bytes,
                                 int32_t *stats, hipStream_t stream);
 

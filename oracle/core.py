@@ -44,7 +44,8 @@ DELTA_BETA = 1e-6        # relative ridge of the mass fit (paper: unregularised 
 DELTA_V = 1e-3           # lambda_v = DELTA_V * tr(A) / t (paper: lambda_v >= 0, no value)
 EPS_W = 1e-12            # epsilon_w of eq. (mass_fit)
 B_MIN, B_MAX = -30.0, 30.0
-MAX_ESCALATIONS = 3      # ridge x10 retries when a Cholesky pivot fails
+MAX_ESCALATIONS = 6      # ridge x10 retries when a Cholesky pivot fails
+DELTA_FLOOR = 1e-7       # an escalation from a zero ridge starts here
 
 _CHUNK_ELEMS = 1 << 25   # float64 elements per key chunk (256 MiB) in O3/O4/O6
 
@@ -384,10 +385,10 @@ def ridge_cholesky_solve(A: np.ndarray, B: np.ndarray, delta: float,
                          max_escalations: int = MAX_ESCALATIONS):
     """Solve (A + delta * tr(A)/t * I) X = B by Cholesky.
 
-    If a pivot is not positive the relative ridge is multiplied by 10, at
-    most ``max_escalations`` times (reading: the paper states no
-    regulariser for the mass fit and a free lambda_v >= 0 for the values).
-    Returns (X, delta_used, attempts).
+    If a pivot is not positive the relative ridge is multiplied by 10 (a
+    zero ridge is raised to DELTA_FLOOR), at most ``max_escalations`` times
+    (reading: the paper states no regulariser for the mass fit and a free
+    lambda_v >= 0 for the values).  Returns (X, delta_used, attempts).
     """
     import scipy.linalg as sla
     t = A.shape[0]
@@ -398,9 +399,9 @@ def ridge_cholesky_solve(A: np.ndarray, B: np.ndarray, delta: float,
         try:
             c = sla.cho_factor(M, lower=True, check_finite=True)
         except np.linalg.LinAlgError:
-            if attempt == max_escalations or d == 0.0:
+            if attempt == max_escalations:
                 raise CholeskyFailure(f"Cholesky failed at delta={d:g}")
-            d *= 10.0
+            d = max(10.0 * d, DELTA_FLOOR)
             continue
         return sla.cho_solve(c, B), d, attempt + 1
     raise CholeskyFailure("unreachable")

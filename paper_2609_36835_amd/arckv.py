@@ -81,8 +81,9 @@ def lib():
         L.arckv_select.argtypes = [P(Problem), vp, i32, vp, vp, sz, vp]
         L.arckv_rowstats.argtypes = [P(Problem), vp, vp, vp, vp, vp, vp, vp]
         L.arckv_merge.argtypes = [P(Problem), vp, vp, vp, vp, i32, ctypes.c_float, vp, vp, vp, vp, sz, vp]
-        L.arckv_fit_bias.argtypes = [P(Problem), vp, vp, i32, vp, vp, P(FitParams), vp, vp, vp, vp, sz, vp]
-        L.arckv_fit_values.argtypes = [P(Problem), vp, vp, vp, i32, vp, P(FitParams), vp, vp, vp, vp, sz, vp]
+        L.arckv_fit_bias.argtypes = [P(Problem), vp, vp, vp, vp, i32, vp, vp, P(FitParams), vp, vp, vp, vp, sz, vp]
+        L.arckv_fit_values.argtypes = [P(Problem), vp, vp, vp, vp, vp, i32, vp, P(FitParams), vp, vp, vp, vp, sz,
+                                       vp]
         L.arckv_compact.argtypes = [P(Problem), vp, vp, vp, P(Indexer), ctypes.c_double, P(FitParams), P(i32),
                                     vp, vp, vp, vp, vp, vp, sz, vp]
         L.arckv_status_string.argtypes = [ctypes.c_int]
@@ -262,9 +263,12 @@ def merge(K, Q, z, anchors, lambda_m=0.25, scale=None, ws_bytes: Optional[int] =
     return Ck, kappa, phi
 
 
-def fit_bias(Q, C_k, z, m, params: Optional[FitParams] = None, scale=None, T: Optional[int] = None):
+def fit_bias(Q, C_k, z, m, params: Optional[FitParams] = None, scale=None, T: Optional[int] = None, K=None, V=None):
+    """arckv_fit_bias; z and m may be None when K and V are given (recomputed)."""
     B, n, d = Q.shape
     t = C_k.shape[1]
+    if K is not None:
+        T = K.shape[1]
     prob = Problem(B, T or max(t, 1), n, d, _dtype_code(Q.dtype), float(scale) if scale else 0.0)
     params = params or default_params()
     beta = torch.empty(B, t, dtype=torch.float32, device=Q.device)
@@ -272,15 +276,19 @@ def fit_bias(Q, C_k, z, m, params: Optional[FitParams] = None, scale=None, T: Op
     dused = torch.empty(B, dtype=torch.float32, device=Q.device)
     nbytes = workspace_size(prob, t, params)
     ws = _workspace(nbytes, Q.device)
-    _check(lib().arckv_fit_bias(ctypes.byref(prob), _ptr(Q), _ptr(C_k), int(t), _ptr(z), _ptr(m),
+    _check(lib().arckv_fit_bias(ctypes.byref(prob), _ptr(K), _ptr(V), _ptr(Q), _ptr(C_k), int(t), _ptr(z), _ptr(m),
                                 ctypes.byref(params), _ptr(beta), _ptr(info), _ptr(dused), _ptr(ws), nbytes,
                                 _stream()), "arckv_fit_bias")
     return beta, info, dused
 
 
-def fit_values(Q, C_k, beta, Y, params: Optional[FitParams] = None, scale=None, T: Optional[int] = None):
+def fit_values(Q, C_k, beta, Y, params: Optional[FitParams] = None, scale=None, T: Optional[int] = None, K=None,
+               V=None):
+    """arckv_fit_values; Y may be None when K and V are given (recomputed)."""
     B, n, d = Q.shape
     t = C_k.shape[1]
+    if K is not None:
+        T = K.shape[1]
     prob = Problem(B, T or max(t, 1), n, d, _dtype_code(Q.dtype), float(scale) if scale else 0.0)
     params = params or default_params()
     Cv = torch.empty(B, t, d, dtype=torch.float32, device=Q.device)
@@ -288,8 +296,8 @@ def fit_values(Q, C_k, beta, Y, params: Optional[FitParams] = None, scale=None, 
     dused = torch.empty(B, dtype=torch.float32, device=Q.device)
     nbytes = workspace_size(prob, t, params)
     ws = _workspace(nbytes, Q.device)
-    _check(lib().arckv_fit_values(ctypes.byref(prob), _ptr(Q), _ptr(C_k), _ptr(beta), int(t), _ptr(Y),
-                                  ctypes.byref(params), _ptr(Cv), _ptr(info), _ptr(dused), _ptr(ws), nbytes,
+    _check(lib().arckv_fit_values(ctypes.byref(prob), _ptr(K), _ptr(V), _ptr(Q), _ptr(C_k), _ptr(beta), int(t),
+                                  _ptr(Y), ctypes.byref(params), _ptr(Cv), _ptr(info), _ptr(dused), _ptr(ws), nbytes,
                                   _stream()), "arckv_fit_values")
     return Cv, info, dused
 

@@ -10,26 +10,13 @@
 
 #include "arckv.h"
 #include "assign.hpp"
+#include "fit.hpp"
 
 namespace arckv {
 typedef uint16_t bf16_t_;   // bfloat16 storage, opaque on the host
 constexpr int kHeadDimH = 128;
 constexpr int64_t kPadH = 256;
 inline int64_t rup(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
-
-struct FitState {
-  double *trace;
-  float *lam;
-  float *delta;
-  int32_t *info;
-};
-struct NnlsWork {
-  int32_t *F, *idx, *bidx, *pos;
-  int32_t *nf, *nb;
-  int32_t *state;
-  int32_t *red;
-  double *y, *rf, *xf;
-};
 
 hipError_t launch_score(int dtype, const void *K, const void *V, const void *W1, const float *b1, const float *w2,
                         const float *b2, float *scores, int B, int T, hipStream_t s);
@@ -93,8 +80,13 @@ hipError_t launch_mass_residual(const float *LT, const float *z, const float *m,
                                 const int32_t *info, hipStream_t s, const int32_t *row_list = nullptr,
                                 const int32_t *row_count = nullptr, const int32_t *col_list = nullptr,
                                 const int32_t *col_count = nullptr);
+hipError_t launch_mass_solve(float *Gw, const float *Gc, float *dinv, void *lsplit, const MassSolve &ms, int B, int n,
+                             int t, int64_t tp, int64_t np_, int refine_steps, int max_esc, FitState st, int32_t *cnt,
+                             hipStream_t s);
 hipError_t launch_cholesky(float *Gw, const float *Gc, int B, int t, int64_t ld, float delta0, int max_esc,
-                           FitState st, float *dinv, void *lsplit, hipStream_t s);
+                           FitState st, float *dinv, void *lsplit, const int32_t *bad, int32_t *cnt,
+                           hipStream_t s);
+hipError_t launch_nonfinite(const float *a, int B, int64_t per, int32_t *bad, hipStream_t s);
 hipError_t launch_trsv(const float *Gw, const float *dinv, int B, int64_t ld, const double *rhs, double *sw,
                        double *y, double *x, double *acc, const int32_t *info, hipStream_t s);
 hipError_t launch_cholesky_factor(float *Gw, const float *Gc, int B, int t, int64_t ld, float delta0, int max_esc,
@@ -225,14 +217,14 @@ struct Bump {
 // Persistent per-pair arrays ([B]-sized) followed by a chunk region for P pairs.
 struct Plan {
   // persistent
-  int64_t scores, z, m, Y, zmax, kappa, phi, beta_ws, info_g, info_a, st_g, st_a, astats;
+  int64_t scores, z, m, Y, zmax, kappa, phi, beta_ws, info_g, info_a, st_g, st_a, astats, bad, cnt;
   int64_t persistent_bytes;
   // chunk region (offsets relative to chunk base)
   int64_t Ckp;
   int64_t Et, U, Ua, anorm, pn, part1, part2, part3, fcnt, fkey, foff, fn, pcnt, pool, psim, dcnt, dkey, dn,
-      dent;   // merge phase
+      doff;   // merge phase
   int64_t offsets, cursor, perm;
-  int64_t PhiT, LT, Gw, Gc, dinv, lsplit, h, w, y, x, res, sw, u, YT, Bm, X, R, Y2, XT, Pm, UT;  // fit phase
+  int64_t PhiT, LT, Gw, Gc, dinv, lsplit, h, w, y, x, res, sw, rprev, div, u, YT, Bm, X, R, Y2, XT, Pm, UT;  // fit phase
   int64_t nF, nidx, nbidx, npos, nnf, nnb, nstate, nred, ny, nrhs, ndx;   // exact NNLS (bias_mode 1)
   int64_t chunk_bytes;
 };
@@ -251,9 +243,11 @@ static Plan make_plan(const Dims &d, int64_t P) {
   pl.beta_ws = a.take(B * d.tp * 4);
   pl.info_g = a.take(B * 4);
   pl.info_a = a.take(B * 4);
-  pl.st_g = a.take(B * 16);    // trace (8) + lam (4) + delta (4)
-  pl.st_a = a.take(B * 16);
+  pl.st_g = a.take(B * 24);    // trace (8) + lam (4) + delta (4) + nesc (4) + pad (4)
+  pl.st_a = a.take(B * 24);
   pl.astats = a.take(B * kAssignStats * 4);  // assignment statistics [B][kAssignStats]
+  pl.bad = a.take(B * 4);                     // non-finite inputs of the current fit [B]
+  pl.cnt = a.take(16);                        // failed-factorisation count read back by the host
   pl.persistent_bytes = a.off;
 
   Bump c;
@@ -278,7 +272,7 @@ static Plan make_plan(const Dims &d, int64_t P) {
   pl.dcnt = m.take(P * 4);
   pl.dkey = m.take(P * d.Tp * 4);
   pl.dn = m.take(P * d.Tp * 4);
-  pl.dent = m.take(P * d.Tp * 16 * 4);
+  pl.doff = m.take(P * d.Tp * 4);
   pl.offsets = m.take(P * (int64_t)(d.t + 1) * 4);
   pl.cursor = m.take(P * (int64_t)d.t * 4);
   pl.perm = m.take(P * (int64_t)d.T * 4);
@@ -295,6 +289,8 @@ static Plan make_plan(const Dims &d, int64_t P) {
   pl.x = f.take(P * d.tp * 8);
   pl.res = f.take(P * d.tp * 8);
   pl.sw = f.take(P * d.tp * 8);
+  pl.rprev = f.take(P * 8);
+  pl.div = f.take(P * 4);
   pl.u = f.take(P * d.np_ * 8);
   pl.YT = f.take(P * kHeadDimH * d.np_ * 4);
   pl.Bm = f.take(P * d.tp * kHeadDimH * 4);
@@ -414,7 +410,7 @@ static arckv_status run_merge_chunk(const Ctx &c, int b0, int P, const void *K, 
   AssignLists L{c.chunk<int32_t>(c.pl.fcnt), c.chunk<int32_t>(c.pl.fkey),  c.chunk<int32_t>(c.pl.foff),
                 c.chunk<int32_t>(c.pl.fn),   c.chunk<int32_t>(c.pl.pcnt),  c.chunk<int32_t>(c.pl.pool),
                 c.chunk<double>(c.pl.psim),  kPoolPerKey * d.Tp,           c.chunk<int32_t>(c.pl.dcnt),
-                c.chunk<int32_t>(c.pl.dkey), c.chunk<int32_t>(c.pl.dn),    c.chunk<int32_t>(c.pl.dent),
+                c.chunk<int32_t>(c.pl.dkey), c.chunk<int32_t>(c.pl.dn),    c.chunk<int32_t>(c.pl.doff),
                 c.pers<int32_t>(c.pl.astats) + (size_t)b0 * kAssignStats, d.Tp};
   const float *zm = zmax + b0;
   int32_t *kap = kappa + (size_t)b0 * d.T;
@@ -451,13 +447,17 @@ static FitState fit_state(const Ctx &c, int64_t st_off, int64_t info_off, int b0
   st.trace = reinterpret_cast<double *>(base) + b0;
   st.lam = reinterpret_cast<float *>(base + (size_t)B * 8) + b0;
   st.delta = reinterpret_cast<float *>(base + (size_t)B * 12) + b0;
+  st.nesc = reinterpret_cast<int32_t *>(base + (size_t)B * 16) + b0;
   st.info = c.pers<int32_t>(info_off) + b0;
   return st;
 }
 
 // Mass fit for pairs [b0, b0+P): needs Ckp (chunk), z, m.
+// Y (may be null) is only checked for non-finite values, so that arckv_compact
+// reports a non-finite V (which reaches Y alone) in both fits.
 static arckv_status run_fit_bias_chunk(const Ctx &c, int b0, int P, const void *Q, const float *z, const float *m,
-                                       const arckv_fit_params &fp, float *beta, FitState st) {
+                                       const float *Ck, const arckv_fit_params &fp, float *beta, FitState st,
+                                       const float *Y = nullptr) {
   const Dims &d = c.d;
   hipStream_t stream = c.stream;
   const char *Qc = (const char *)Q + (size_t)b0 * d.n * kHeadDimH * c.in_esz();
@@ -467,23 +467,27 @@ static arckv_status run_fit_bias_chunk(const Ctx &c, int b0, int P, const void *
   double *h = c.chunk<double>(c.pl.h), *w = c.chunk<double>(c.pl.w), *y = c.chunk<double>(c.pl.y);
   double *x = c.chunk<double>(c.pl.x), *res = c.chunk<double>(c.pl.res), *sw = c.chunk<double>(c.pl.sw);
   float *dinv = c.chunk<float>(c.pl.dinv);
+  // pairs whose inputs (z, m, C_k, and Y when given) hold a non-finite value report info = -1
+  int32_t *bad = c.pers<int32_t>(c.pl.bad) + b0;
+  if (launch_fill_i32(bad, P, 0, stream) != hipSuccess || launch_nonfinite(zc, P, d.n, bad, stream) != hipSuccess ||
+      (Y && launch_nonfinite(Y + (size_t)b0 * d.n * kHeadDimH, P, (int64_t)d.n * kHeadDimH, bad, stream) !=
+                hipSuccess) ||
+      launch_nonfinite(mc, P, d.n, bad, stream) != hipSuccess ||
+      launch_nonfinite(Ck + (size_t)b0 * d.t * kHeadDimH, P, (int64_t)d.t * kHeadDimH, bad, stream) != hipSuccess)
+    return ARCKV_ERR_HIP;
   // Phi_C^T (split planes), the logits L^T, and h = Phi_C^T m in one pass
   STAGE(ST_PHIC, launch_phic(d.dtype, Qc, c.chunk<char>(c.pl.Ckp), zc, PhiT, LT, mc, h, P, d.t, d.n, d.tp, d.np_,
                              c.scale, stream));
   STAGE(ST_GRAM_G, launch_gram(d.dtype, PhiT, Gw, Gc, P, d.tp, d.np_, stream));
   STAGE(ST_CHOL_G, launch_cholesky(Gw, Gc, P, d.t, d.tp, fp.delta_beta, fp.max_escalations, st, dinv,
-                                   c.chunk<char>(c.pl.lsplit), stream));
+                                   c.chunk<char>(c.pl.lsplit), bad, c.pers<int32_t>(c.pl.cnt), stream));
   {
     StageScope _sc(ST_SOLVE_W, stream);
     double *u = c.chunk<double>(c.pl.u);
-    if (launch_trsv(Gw, dinv, P, d.tp, h, sw, y, w, nullptr, st.info, stream) != hipSuccess) return ARCKV_ERR_HIP;
-    // refinement against the data: res = Phi_C^T (m - Phi_C w) - lam w
-    for (int it = 0; it < fp.refine_steps; ++it) {
-      if (launch_mass_residual(LT, zc, mc, w, st.lam, P, d.n, d.t, d.tp, d.np_, u, res, st.info, stream) !=
-          hipSuccess)
-        return ARCKV_ERR_HIP;
-      if (launch_trsv(Gw, dinv, P, d.tp, res, sw, y, x, w, st.info, stream) != hipSuccess) return ARCKV_ERR_HIP;
-    }
+    const MassSolve ms{LT, zc, mc, h, w, x, y, sw, u, res, c.chunk<double>(c.pl.rprev), c.chunk<int32_t>(c.pl.div)};
+    if (launch_mass_solve(Gw, Gc, dinv, c.chunk<char>(c.pl.lsplit), ms, P, d.n, d.t, d.tp, d.np_, fp.refine_steps,
+                          fp.max_escalations, st, c.pers<int32_t>(c.pl.cnt), stream) != hipSuccess)
+      return ARCKV_ERR_HIP;
     if (fp.bias_mode == 1) {
       // exact NNLS on the ridged system whose ridge the factorisation above
       // settled, pivoting from the unconstrained solution w
@@ -506,8 +510,8 @@ hipError_t launch_pad_beta(const float *beta, int P, int t, int64_t tp, float *b
 
 // Value fit for pairs [b0, b0+P): needs LT (from the mass fit, or recomputed),
 // beta_ws, Y.
-static arckv_status run_fit_values_chunk(const Ctx &c, int b0, int P, const float *Y, const arckv_fit_params &fp,
-                                         float *Cv, FitState st) {
+static arckv_status run_fit_values_chunk(const Ctx &c, int b0, int P, const float *Y, const float *Ck,
+                                         const float *beta, const arckv_fit_params &fp, float *Cv, FitState st) {
   const Dims &d = c.d;
   hipStream_t stream = c.stream;
   void *PT = c.chunk<char>(c.pl.PhiT);
@@ -519,6 +523,14 @@ static arckv_status run_fit_values_chunk(const Ctx &c, int b0, int P, const floa
   const float *Yc = Y + (size_t)b0 * d.n * kHeadDimH;
   const int64_t pl = d.dtype == ARCKV_BF16 ? 2 : 1;
   const int64_t yt_pair = (d.dtype == ARCKV_BF16 ? 2 : 1) * (int64_t)kHeadDimH * d.np_;
+  // pairs whose inputs (Y, C_k, beta) hold a non-finite value report info = -1
+  // (a failed mass fit leaves beta NaN)
+  int32_t *bad = c.pers<int32_t>(c.pl.bad) + b0;
+  if (launch_fill_i32(bad, P, 0, stream) != hipSuccess ||
+      launch_nonfinite(Yc, P, (int64_t)d.n * kHeadDimH, bad, stream) != hipSuccess ||
+      launch_nonfinite(Ck + (size_t)b0 * d.t * kHeadDimH, P, (int64_t)d.t * kHeadDimH, bad, stream) != hipSuccess ||
+      launch_nonfinite(beta + (size_t)b0 * d.t, P, d.t, bad, stream) != hipSuccess)
+    return ARCKV_ERR_HIP;
   // P^T for the Gram and right-hand side, and P (query-major) for the refinement residuals
   STAGE(ST_PHAT, launch_phat(d.dtype, LT, c.pers<float>(c.pl.beta_ws) + (size_t)b0 * d.tp, P, d.n, d.t, d.tp,
                              d.np_, PT, fp.refine_steps > 0 ? Pm : nullptr, stream));
@@ -531,7 +543,7 @@ static arckv_status run_fit_values_chunk(const Ctx &c, int b0, int P, const floa
     if (launch_rhs_gemm(d.dtype, PT, YT, Bm, P, d.tp, d.np_, stream) != hipSuccess) return ARCKV_ERR_HIP;
   }
   STAGE(ST_CHOL_A, launch_cholesky(Gw, Gc, P, d.t, d.tp, fp.delta_v, fp.max_escalations, st, dinv,
-                                   c.chunk<char>(c.pl.lsplit), stream));
+                                   c.chunk<char>(c.pl.lsplit), bad, c.pers<int32_t>(c.pl.cnt), stream));
   {
     StageScope _sc(ST_SOLVE_V, stream);
     if (launch_trsm(true, Gw, dinv, P, d.tp, Bm, Y2, st.info, stream) != hipSuccess) return ARCKV_ERR_HIP;
@@ -569,7 +581,7 @@ arckv_status arckv_default_params(arckv_fit_params *p) {
   p->b_min = -30.0f;
   p->b_max = 30.0f;
   p->bias_mode = 0;
-  p->max_escalations = 3;
+  p->max_escalations = 6;
   p->refine_steps = 2;
   p->pair_chunk = 0;
   p->select_chunk = 0;
@@ -706,24 +718,45 @@ static arckv_status fit_common(const arckv_problem *prob, const float *C_k, int3
   return ARCKV_OK;
 }
 
-arckv_status arckv_fit_bias(const arckv_problem *prob, const void *Q_ref, const float *C_k, int32_t t,
-                            const float *z, const float *m, const arckv_fit_params *p, float *beta, int32_t *info,
-                            float *delta_used, void *ws, size_t ws_bytes, hipStream_t stream) {
+// z, m (mass fit) or Y (value fit) given, or recomputed into the workspace
+// from K, V by the row-statistics kernel.
+static arckv_status fit_rowstats(const Ctx &c, const void *K, const void *V, const void *Q_ref, const float **z,
+                                 const float **m, const float **Y) {
+  if ((z && *z && m && *m) || (Y && *Y)) return ARCKV_OK;
+  if (!K || !V || !aligned(K, 16) || !aligned(V, 16)) return ARCKV_ERR_INVALID_ARG;
+  float *zw = c.pers<float>(c.pl.z), *mw = c.pers<float>(c.pl.m), *Yw = c.pers<float>(c.pl.Y);
+  hipStream_t stream = c.stream;
+  STAGE(ST_ROWSTATS, launch_rowstats(c.d.dtype, K, V, Q_ref, zw, mw, Yw, c.d.B, c.d.T, c.d.n, c.scale, stream));
+  if (z) *z = zw;
+  if (m) *m = mw;
+  if (Y) *Y = Yw;
+  return ARCKV_OK;
+}
+
+arckv_status arckv_fit_bias(const arckv_problem *prob, const void *K, const void *V, const void *Q_ref,
+                            const float *C_k, int32_t t, const float *z, const float *m, const arckv_fit_params *p,
+                            float *beta, int32_t *info, float *delta_used, void *ws, size_t ws_bytes,
+                            hipStream_t stream) {
   arckv_fit_params def;
   arckv_default_params(&def);
   if (!p) p = &def;
-  if (!Q_ref || !z || !m || !beta || !info) return ARCKV_ERR_INVALID_ARG;
-  if (!aligned(Q_ref, 16)) return ARCKV_ERR_INVALID_ARG;
+  if (!Q_ref || !beta || !info) return ARCKV_ERR_INVALID_ARG;
+  if (!aligned(Q_ref, 16) || !aligned(C_k, 16)) return ARCKV_ERR_INVALID_ARG;
+  if ((!z || !m) && (!K || !V)) return ARCKV_ERR_INVALID_ARG;   // z and m are recomputed from K, V
   Ctx c;
   int64_t P = 0;
   CHECK(fit_common(prob, C_k, t, p, ws, ws_bytes, stream, c, P));
+  if (!z || !m) {
+    z = m = nullptr;
+    CHECK(fit_rowstats(c, K, V, Q_ref, &z, &m, nullptr));
+  }
   for (int b0 = 0; b0 < c.d.B; b0 += (int)P) {
     const int Pc = (int)(c.d.B - b0 < P ? c.d.B - b0 : P);
     if (launch_pad_ck(c.d.dtype, C_k + (size_t)b0 * t * kHeadDimH, Pc, t, c.d.tp, c.chunk<char>(c.pl.Ckp), stream) !=
         hipSuccess)
       return ARCKV_ERR_HIP;
     FitState st = fit_state(c, c.pl.st_g, c.pl.info_g, b0);
-    CHECK(run_fit_bias_chunk(c, b0, Pc, Q_ref, z, m, *p, beta, st));
+    CHECK(run_fit_bias_chunk(c, b0, Pc, Q_ref, z, m, C_k, *p, beta, st));
   }
   if (launch_copy_info(c.pers<int32_t>(c.pl.info_g), nullptr, c.d.B, info, stream) != hipSuccess) return ARCKV_ERR_HIP;
   if (delta_used && launch_copy_f32(reinterpret_cast<float *>(c.pers<char>(c.pl.st_g) + (size_t)c.d.B * 12),
@@ -732,17 +765,20 @@ arckv_status arckv_fit_bias(const arckv_problem *prob, const void *Q_ref, const 
   return ARCKV_OK;
 }
 
-arckv_status arckv_fit_values(const arckv_problem *prob, const void *Q_ref, const float *C_k, const float *beta,
-                              int32_t t, const float *Y, const arckv_fit_params *p, float *C_v, int32_t *info,
-                              float *delta_used, void *ws, size_t ws_bytes, hipStream_t stream) {
+arckv_status arckv_fit_values(const arckv_problem *prob, const void *K, const void *V, const void *Q_ref,
+                              const float *C_k, const float *beta, int32_t t, const float *Y,
+                              const arckv_fit_params *p, float *C_v, int32_t *info, float *delta_used, void *ws,
+                              size_t ws_bytes, hipStream_t stream) {
   arckv_fit_params def;
   arckv_default_params(&def);
   if (!p) p = &def;
-  if (!Q_ref || !beta || !Y || !C_v || !info) return ARCKV_ERR_INVALID_ARG;
-  if (!aligned(Q_ref, 16) || !aligned(Y, 16)) return ARCKV_ERR_INVALID_ARG;
+  if (!Q_ref || !beta || !C_v || !info) return ARCKV_ERR_INVALID_ARG;
+  if (!aligned(Q_ref, 16) || !aligned(C_k, 16) || (Y && !aligned(Y, 16))) return ARCKV_ERR_INVALID_ARG;
+  if (!Y && (!K || !V)) return ARCKV_ERR_INVALID_ARG;   // Y is recomputed from K, V
   Ctx c;
   int64_t P = 0;
   CHECK(fit_common(prob, C_k, t, p, ws, ws_bytes, stream, c, P));
+  if (!Y) CHECK(fit_rowstats(c, K, V, Q_ref, nullptr, nullptr, &Y));
   const Dims &d = c.d;
   for (int b0 = 0; b0 < d.B; b0 += (int)P) {
     const int Pc = (int)(d.B - b0 < P ? d.B - b0 : P);
@@ -757,7 +793,7 @@ arckv_status arckv_fit_values(const arckv_problem *prob, const void *Q_ref, cons
     STAGE(ST_PHIC, launch_phic(d.dtype, Qc, c.chunk<char>(c.pl.Ckp), nullptr, c.chunk<char>(c.pl.PhiT),
                                c.chunk<float>(c.pl.LT), nullptr, nullptr, Pc, d.t, d.n, d.tp, d.np_, c.scale, stream));
     FitState st = fit_state(c, c.pl.st_a, c.pl.info_a, b0);
-    CHECK(run_fit_values_chunk(c, b0, Pc, Y, *p, C_v, st));
+    CHECK(run_fit_values_chunk(c, b0, Pc, Y, C_k, beta, *p, C_v, st));
   }
   if (launch_copy_info(c.pers<int32_t>(c.pl.info_a), nullptr, d.B, info, stream) != hipSuccess) return ARCKV_ERR_HIP;
   if (delta_used && launch_copy_f32(reinterpret_cast<float *>(c.pers<char>(c.pl.st_a) + (size_t)d.B * 12),
@@ -812,8 +848,8 @@ static arckv_status compact_impl(const arckv_problem *prob, const void *K, const
   for (int b0 = 0; b0 < d.B; b0 += (int)P) {
     const int Pc = (int)(d.B - b0 < P ? d.B - b0 : P);
     CHECK(run_merge_chunk(c, b0, Pc, K, Q_ref, anchors, p->lambda_m, C_k, kappa, phi, zmax));
-    CHECK(run_fit_bias_chunk(c, b0, Pc, Q_ref, z, m, *p, beta, fit_state(c, c.pl.st_g, c.pl.info_g, b0)));
-    CHECK(run_fit_values_chunk(c, b0, Pc, Y, *p, C_v, fit_state(c, c.pl.st_a, c.pl.info_a, b0)));
+    CHECK(run_fit_bias_chunk(c, b0, Pc, Q_ref, z, m, C_k, *p, beta, fit_state(c, c.pl.st_g, c.pl.info_g, b0), Y));
+    CHECK(run_fit_values_chunk(c, b0, Pc, Y, C_k, beta, *p, C_v, fit_state(c, c.pl.st_a, c.pl.info_a, b0)));
   }
   if (launch_copy_info(c.pers<int32_t>(c.pl.info_g), c.pers<int32_t>(c.pl.info_a), d.B, info, stream) != hipSuccess)
     return ARCKV_ERR_HIP;

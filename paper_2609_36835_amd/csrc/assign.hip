@@ -29,7 +29,6 @@
 
 namespace arckv {
 
-constexpr int kAssignMaxD = 16;   // candidate entries of one key in the float64 pass (assign.hpp)
 constexpr double kU32 = 5.9604644775390625e-08;   // 2^-24, unit roundoff of fp32
 constexpr double kU16 = 4.8828125e-04;            // 2^-11, unit roundoff of fp16
 
@@ -335,11 +334,13 @@ __device__ inline CandA cand_a(const uint64_t *p1, const uint64_t *p2, const uin
   return c;
 }
 
-__device__ inline void push_d(const AssignLists &L, int b, int j, const int32_t *ent, int k) {
+// Queue key j for the float64 pass with its k surviving candidates, which sit
+// at pool offset off (off = -1, k = t: every anchor).
+__device__ inline void push_d(const AssignLists &L, int b, int j, int off, int k) {
   const int slot = atomicAdd(&L.dcnt[b], 1);
   L.dkey[(size_t)b * L.cap + slot] = j;
+  L.doff[(size_t)b * L.cap + slot] = off;
   L.dn[(size_t)b * L.cap + slot] = k;
-  for (int e = 0; e < k; ++e) L.dent[((size_t)b * L.cap + slot) * kAssignMaxD + e] = ent[e];
   atomicAdd(&L.stats[b * kAssignStats + 1], 1);
 }
 
@@ -401,9 +402,8 @@ __global__ void __launch_bounds__(256) k_assign_finalize(
     return;
   }
   const int off = atomicAdd(&L.pcnt[b], nc);
-  if ((int64_t)off + nc > L.pcap) {   // pool full: the key keeps its pass-A best
-    atomicAdd(&st[3], 1);
-    atomicAdd(&st[4], 1);
+  if ((int64_t)off + nc > L.pcap) {   // pool full (near-equal profiles): decided in float64 over all t anchors
+    push_d(L, b, j, -1, t);
     return;
   }
   int32_t *pl = L.pool + (size_t)b * L.pcap + off;
@@ -629,21 +629,13 @@ __global__ void __launch_bounds__(256, 2) k_assign_refine(const E *__restrict__ 
       }
       const double bs = psim[o + best];
       const double thc = bs * (1.0 - eta) / (1.0 + eta) - 1e-300;
-      int32_t surv[kAssignMaxD];
-      int ns = 0;
-      bool over = false;
-      for (int c = 0; c < m; ++c)
-        if (psim[o + c] >= thc) {
-          if (ns == kAssignMaxD) over = true;
-          else surv[ns++] = pool[o + c];
-        }
       kappa[(size_t)b * T + j] = pool[o + best];
-      if (over) {   // (equal similarities of duplicate anchors) the lowest r among the largest stands
-        atomicAdd(&L.stats[b * kAssignStats + 3], 1);
-        atomicAdd(&L.stats[b * kAssignStats + 5], 1);
-      } else if (ns > 1) {
-        push_d(L, b, j, surv, ns);
-      }
+      // the survivors are compacted in place at the front of the key's pool
+      // segment (this thread alone reads and writes it; writes trail reads)
+      int ns = 0;
+      for (int c = 0; c < m; ++c)
+        if (psim[o + c] >= thc) pool[o + ns++] = pool[o + c];
+      if (ns > 1) push_d(L, b, j, o, ns);
     }
   }
 }
@@ -683,7 +675,10 @@ __global__ void __launch_bounds__(256) k_assign_exact(const E *__restrict__ Q, c
   const double zm = (double)zmerge[b];
   const E *Qb = Q + (size_t)b * n * kHeadDim;
   auto n_cand = [&](int di) { return L.dn[(size_t)b * L.cap + di]; };
-  auto cand_at = [&](int di, int ci) { return L.dent[((size_t)b * L.cap + di) * kAssignMaxD + ci]; };
+  auto cand_at = [&](int di, int ci) {   // doff < 0: every anchor is a candidate
+    const int off = L.doff[(size_t)b * L.cap + di];
+    return off < 0 ? ci : L.pool[(size_t)b * L.pcap + off + ci];
+  };
   // register tile of the logit pass: vectors tv, tv + 16 and queries tq + 16 m, m = 0..3
   const int tv = tid >> 4, tq = tid & 15;
   // rows of 128 elements of E as 4 floats per thread-step (bf16: 4 values = 8 bytes)

@@ -20,11 +20,12 @@ struct AssignLists {
   int32_t *dcnt;    // [P] keys queued for the float64 pass
   int32_t *dkey;    // [P][cap]
   int32_t *dn;      // [P][cap] entries per queued key
-  int32_t *dent;    // [P][cap][16] entries: anchor r >= 0, or -(tile + 1) for a whole anchor tile
+  int32_t *doff;    // [P][cap] first surviving candidate of the queued key in the pool (-1: all t anchors)
   int32_t *stats;   // [P][kAssignStats] (assign.hip): flagged after the first pass, sent to the float64
                     // pass, candidates of the flagged keys, undecided (sum of the next two), undecided
-                    // in the first pass, undecided in the refine pass, sent to the refine pass, keys
-                    // whose pass-A candidates include a whole anchor tile
+                    // in the first pass, undecided in the refine pass (kept at 0: survivors of any
+                    // number go to the float64 pass), sent to the refine pass, keys whose pass-A
+                    // candidates include a whole anchor tile
   int64_t cap;      // key capacity per pair
 };
 

@@ -9,44 +9,36 @@
 //                                     registers (one wave) and invert it
 //                      k_chol_panel   L_ik = A_ik L_kk^-T for row blocks i > k
 //                                     (fp32 MFMA with the inverse)
-//                      k_chol_upd     A -= L L^T over a panel's columns
+//                      k_chol_upd     A -= L L^T over a panel's own columns
 //                                     (fp32 MFMA, 128 x 128 tiles), once per
-//                                     64 columns inside a 256-wide outer panel
-//                                     and once per outer panel for the rest
+//                                     64 columns inside a 256-wide outer panel;
+//                                     the rest of the matrix is updated once
+//                                     per outer panel by the big contraction
+//                                     on three bf16 planes of the panel (six
+//                                     products, float32-accurate)
 //                    a failed pivot records info = column + 1 for that pair
-//   k_chol_escalate  for pairs that failed: restore, delta *= 10, refactor in
-//                    one workgroup; at most max_escalations times
+//   escalation       pairs that failed are refactored by the same kernels with
+//                    delta raised tenfold (from 1e-7 when zero), at most
+//                    max_escalations times (launch_cholesky)
 //   solves           TRSV (one rhs, float64 accumulation) / TRSM (128 rhs)
 //   residuals        rhs - (M + lam I) x, float64 (mass fit) or float32 MFMA
 //                    (value fit), for iterative refinement
 #include "common.hpp"
 #include "gemm.hpp"
 #include "gemm_big.hpp"
+#include "fit.hpp"
 
 namespace arckv {
 
 constexpr int kNB = 64;          // Cholesky block
 constexpr int kSD = kNB + 1;     // LDS stride of a 64x64 fp32 tile
 
-struct FitState {
-  double *trace;   // [P]
-  float *lam;      // [P]
-  float *delta;    // [P]
-  int32_t *info;   // [P]
-};
-
-// Work arrays of the exact non-negative fit ([P][tp] unless noted).
-struct NnlsWork {
-  int32_t *F, *idx, *bidx, *pos;   // free flags, free and bound lists, slot of each key
-  int32_t *nf, *nb;                // [P] free- and bound-set sizes
-  int32_t *state;           // [P][4]
-  int32_t *red;             // [2] max free-set size, unsettled pairs
-  double *y, *rf, *xf;      // dual, compressed right-hand side and solution
-};
-
 // --------------------------------------------------------------- ridge
+// info starts at -1 for pairs flagged with non-finite inputs (bad, may be
+// null), which every later kernel then skips, and 0 otherwise.
 __global__ void __launch_bounds__(256) k_ridge_init(float *__restrict__ Gw, const float *__restrict__ Gc, int t,
-                                                    int64_t ld, float delta0, FitState st) {
+                                                    int64_t ld, float delta0, FitState st,
+                                                    const int32_t *__restrict__ bad) {
   __shared__ double red[4];
   const int b = blockIdx.x, tid = threadIdx.x;
   const size_t base = (size_t)b * ld * ld;
@@ -62,80 +54,156 @@ __global__ void __launch_bounds__(256) k_ridge_init(float *__restrict__ Gw, cons
     st.trace[b] = tr;
     st.lam[b] = lam;
     st.delta[b] = delta0;
-    st.info[b] = 0;
+    st.nesc[b] = 0;
+    st.info[b] = bad && bad[b] ? -1 : 0;
   }
+}
+
+// ---------------------------------------------------------------- ridge escalation
+// A pair whose factorisation failed (info > 0) is refactored with the ridge
+// raised tenfold, from kDeltaFloor when it was zero, by the same batched
+// blocked factorisation, while it has escalations left (nesc < max_esc); pairs
+// that are settled carry kEscSkip meanwhile (every factorisation kernel skips
+// info != 0), non-finite ones keep -1.
+constexpr int32_t kEscSkip = -0x30000000;
+constexpr float kDeltaFloor = 1e-7f;
+
+__global__ void k_esc_state(int B, int t, FitState st, int max_esc) {
+  const int b = blockIdx.x * 256 + threadIdx.x;
+  if (b >= B) return;
+  const int32_t f = st.info[b];
+  if (f > 0 && st.nesc[b] < max_esc) {
+    const float delta = fmaxf(10.0f * st.delta[b], kDeltaFloor);
+    st.delta[b] = delta;
+    st.lam[b] = (float)((double)delta * st.trace[b] / (double)t);
+    st.nesc[b] += 1;
+    st.info[b] = 0;
+  } else if (f == 0) {
+    st.info[b] = kEscSkip;
+  }
+}
+
+// Gw = Gc + lam I (lower triangle and diagonal; padding diagonal 1) for the
+// pairs being refactored (info == 0).  One row per thread-block row.
+__global__ void __launch_bounds__(256) k_esc_copy(float *__restrict__ Gw, const float *__restrict__ Gc, int t,
+                                                  int64_t ld, FitState st) {
+  const int b = blockIdx.y;
+  const int64_t r = blockIdx.x;
+  if (st.info[b] != 0) return;
+  const float lam = st.lam[b];
+  const size_t base = (size_t)b * ld * ld + (size_t)r * ld;
+  for (int64_t c = threadIdx.x; c <= r; c += 256)
+    Gw[base + c] = c == r ? (r < t ? Gc[base + c] + lam : 1.0f) : Gc[base + c];
+}
+
+__global__ void k_esc_restore(int B, int32_t *__restrict__ info) {
+  const int b = blockIdx.x * 256 + threadIdx.x;
+  if (b < B && info[b] == kEscSkip) info[b] = 0;
+}
+
+// cnt[0] = number of pairs whose factorisation failed (info > 0) and that
+// have escalations left.
+__global__ void __launch_bounds__(256) k_count_failed(int B, const FitState st, int max_esc, int32_t *cnt) {
+  __shared__ int red[4];
+  int c = 0;
+  for (int b = threadIdx.x; b < B; b += 256) c += st.info[b] > 0 && st.nesc[b] < max_esc;
+  for (int m = 32; m >= 1; m >>= 1) c += __shfl_xor(c, m, 64);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = c;
+  __syncthreads();
+  if (threadIdx.x == 0) cnt[0] = red[0] + red[1] + red[2] + red[3];
+}
+
+// ---------------------------------------------------------------- refinement guard
+// Each refinement step recomputes the residual from the data, so it converges
+// at a rate set by how far the float32 factor is from those normal equations.
+// Where the ridge is small next to the Gram's float32 rounding (a
+// rank-deficient Gram, t > n, with a ridge near 1e-6 of its mean diagonal) a
+// step can instead grow the solution along the Gram's near-null directions.
+// After every step the data residual is checked: one above 1e-10 |h| that did
+// not at least halve undoes that step and ends the pair's refinement
+// (kRefStop); while it has escalations left the pair is then refactored with
+// the ridge raised tenfold and solved again (div).  Pairs not being refactored
+// meanwhile carry kDoneSkip.
+constexpr int32_t kRefStop = -0x20000000;
+constexpr int32_t kDoneSkip = -0x10000000;
+
+// One workgroup per pair; it = 0 records the first residual norm.
+__global__ void __launch_bounds__(256) k_refine_watch(const double *__restrict__ res, const double *__restrict__ h,
+                                                      double *__restrict__ w, const double *__restrict__ x,
+                                                      int64_t tp, int it, double *__restrict__ rprev,
+                                                      int32_t *__restrict__ div, FitState st, int max_esc) {
+  __shared__ double red[2][4];
+  const int b = blockIdx.x, tid = threadIdx.x;
+  if (st.info[b] != 0) return;
+  const double rp = rprev[b];   // read by every thread before thread 0 rewrites it
+  const size_t o = (size_t)b * tp;
+  double r2 = 0.0, h2 = 0.0;
+  for (int64_t r = tid; r < tp; r += 256) {
+    const double a = res[o + r], c = h[o + r];
+    r2 = fma(a, a, r2);
+    h2 = fma(c, c, h2);
+  }
+  r2 = wave_sum(r2);
+  h2 = wave_sum(h2);
+  if ((tid & 63) == 0) {
+    red[0][tid >> 6] = r2;
+    red[1][tid >> 6] = h2;
+  }
+  __syncthreads();
+  const double rn = sqrt(red[0][0] + red[0][1] + red[0][2] + red[0][3]);
+  const double hn = sqrt(red[1][0] + red[1][1] + red[1][2] + red[1][3]);
+  if (it == 0 || !(rn > 0.5 * rp && rn > 1e-10 * hn)) {
+    if (tid == 0) rprev[b] = rn;
+    return;
+  }
+  for (int64_t r = tid; r < tp; r += 256) w[o + r] -= x[o + r];
+  if (tid == 0) {
+    st.info[b] = kRefStop;
+    div[b] = st.nesc[b] < max_esc;
+  }
+}
+
+// cnt[0] = number of nonzero flags.
+__global__ void __launch_bounds__(256) k_count_flags(int B, const int32_t *__restrict__ flag, int32_t *cnt) {
+  __shared__ int red[4];
+  int c = 0;
+  for (int b = threadIdx.x; b < B; b += 256) c += flag[b] != 0;
+  for (int m = 32; m >= 1; m >>= 1) c += __shfl_xor(c, m, 64);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = c;
+  __syncthreads();
+  if (threadIdx.x == 0) cnt[0] = red[0] + red[1] + red[2] + red[3];
+}
+
+// Pairs to refactor get info = 1 (picked up by k_esc_state); the settled rest kDoneSkip.
+__global__ void k_div_mark(int B, int32_t *__restrict__ div, int32_t *__restrict__ info) {
+  const int b = blockIdx.x * 256 + threadIdx.x;
+  if (b >= B) return;
+  const int32_t f = info[b];
+  if (div[b]) {
+    info[b] = 1;
+    div[b] = 0;
+  } else if (f == 0 || f == kRefStop) {
+    info[b] = kDoneSkip;
+  }
+}
+
+__global__ void k_refine_restore(int B, int32_t *__restrict__ info) {
+  const int b = blockIdx.x * 256 + threadIdx.x;
+  if (b < B && (info[b] == kRefStop || info[b] == kDoneSkip)) info[b] = 0;
+}
+
+// ---------------------------------------------------------------- non-finite inputs
+// bad[b] |= 1 when any of the `per` values of pair b in a is not finite (a
+// grid-stride pass over [B][per]; bad is cleared by the caller).
+__global__ void __launch_bounds__(256) k_nonfinite(const float *__restrict__ a, int64_t per, int32_t *__restrict__ bad) {
+  const int b = blockIdx.y;
+  bool any = false;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < per; i += (int64_t)gridDim.x * 256)
+    any |= !isfinite(a[(size_t)b * per + i]);
+  if (__any(any) && (threadIdx.x & 63) == 0) atomicOr(&bad[b], 1);
 }
 
 // --------------------------------------------------------------- 64x64 building blocks
-__device__ inline void load_tile(float *sD, const float *G, int64_t ld) {
-  for (int c = threadIdx.x; c < kNB * kNB / 4; c += 256) {
-    const int r = c / 16, cc = (c % 16) * 4;
-    f32x4 v = *reinterpret_cast<const f32x4 *>(G + (size_t)r * ld + cc);
-    sD[r * kSD + cc] = v[0];
-    sD[r * kSD + cc + 1] = v[1];
-    sD[r * kSD + cc + 2] = v[2];
-    sD[r * kSD + cc + 3] = v[3];
-  }
-}
-__device__ inline void store_tile(const float *sD, float *G, int64_t ld) {
-  for (int c = threadIdx.x; c < kNB * kNB / 4; c += 256) {
-    const int r = c / 16, cc = (c % 16) * 4;
-    f32x4 v = {sD[r * kSD + cc], sD[r * kSD + cc + 1], sD[r * kSD + cc + 2], sD[r * kSD + cc + 3]};
-    *reinterpret_cast<f32x4 *>(G + (size_t)r * ld + cc) = v;
-  }
-}
-
-// In-place Cholesky of the 64x64 tile in LDS (lower triangle).  Returns the
-// first failing column, or -1.  All 256 threads must call it.
-__device__ int factor_tile(float *sD) {
-  for (int c = 0; c < kNB; ++c) {
-    __syncthreads();
-    const float piv = sD[c * kSD + c];
-    if (!(piv > 0.0f) || !isfinite(piv)) return c;
-    const float d = sqrtf(piv);
-    __syncthreads();
-    if (threadIdx.x == 0) sD[c * kSD + c] = d;
-    const float inv = 1.0f / d;
-    for (int r = c + 1 + threadIdx.x; r < kNB; r += 256) sD[r * kSD + c] *= inv;
-    __syncthreads();
-    for (int e = threadIdx.x; e < kNB * kNB; e += 256) {
-      const int r = e / kNB, s = e % kNB;
-      if (s > c && s <= r) sD[r * kSD + s] -= sD[r * kSD + c] * sD[s * kSD + c];
-    }
-  }
-  __syncthreads();
-  return -1;
-}
-
-// X L^T = A for the 64x64 tile sX (in place), L the factored tile sL.
-__device__ void trsm_tile(const float *sL, float *sX) {
-  __syncthreads();
-  if (threadIdx.x < kNB) {
-    const int r = threadIdx.x;
-    for (int c = 0; c < kNB; ++c) {
-      float s = sX[r * kSD + c];
-      for (int q = 0; q < c; ++q) s -= sX[r * kSD + q] * sL[c * kSD + q];
-      sX[r * kSD + c] = s / sL[c * kSD + c];
-    }
-  }
-  __syncthreads();
-}
-
-// C -= A B^T for 64x64 tiles in LDS, fp32 MFMA, result applied to global C.
-__device__ void update_tile(const float *sA, const float *sB, float *C, int64_t ld) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int wi = wave >> 1, wj = wave & 1, h = lane >> 5, col = lane & 31;
-  f32x16 acc = zero16();
-  #pragma unroll
-  for (int ks = 0; ks < kNB / 2; ++ks)
-    acc = Mfma<float>::mma(sA[(32 * wi + col) * kSD + 2 * ks + h], sB[(32 * wj + col) * kSD + 2 * ks + h], acc);
-  #pragma unroll
-  for (int v = 0; v < 16; ++v) {
-    const int r = 32 * wi + acc_row(v, lane), c = 32 * wj + col;
-    C[(size_t)r * ld + c] -= acc[v];
-  }
-}
-
 // Inverse of a factored 64 x 64 lower-triangular block whose row `lane` is
 // held in a[] by lane `lane` of the wave; rdiag[r] = 1 / L[r][r].  Forward
 // substitution column-per-lane, x[r] = (e_r - sum_{q<r} L[r][q] x[q]) L[r][r]^-1
@@ -194,24 +262,6 @@ __global__ void __launch_bounds__(64) k_chol_diag(float *__restrict__ Gw, int64_
 #pragma unroll
   for (int s2 = 0; s2 < kNB; ++s2)
     if (s2 <= lane) D[(size_t)lane * ld + s2] = a[s2];
-  tri_inverse_64(a, rdiag, lane, dinv + ((size_t)b * (ld / kNB) + k) * kNB * kNB);
-}
-
-// Diagonal-block inverses of a finished factor, for pairs whose factorisation
-// went through the escalation path (delta differs from its initial value).
-__global__ void __launch_bounds__(64) k_chol_dinv_escalated(const float *__restrict__ Gw, int64_t ld, float delta0,
-                                                            const float *__restrict__ delta,
-                                                            const int32_t *__restrict__ info,
-                                                            float *__restrict__ dinv) {
-  const int k = blockIdx.x, b = blockIdx.y, lane = threadIdx.x;
-  if (info[b] != 0 || delta[b] == delta0) return;
-  const float *D = Gw + (size_t)b * ld * ld + (size_t)k * kNB * ld + (size_t)k * kNB;
-  float a[kNB], rdiag[kNB];
-#pragma unroll
-  for (int s2 = 0; s2 < kNB; ++s2) a[s2] = s2 <= lane ? D[(size_t)lane * ld + s2] : 0.0f;
-  auto bcast = [](float v, int src) { return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), src)); };
-#pragma unroll
-  for (int r = 0; r < kNB; ++r) rdiag[r] = 1.0f / bcast(a[r], r);
   tri_inverse_64(a, rdiag, lane, dinv + ((size_t)b * (ld / kNB) + k) * kNB * kNB);
 }
 
@@ -446,64 +496,6 @@ struct EpiCholUpd {
     }
   }
 };
-
-// Whole factorisation in one workgroup (escalation path).
-__device__ int factor_matrix_single(float *G, int64_t ld, int nrb, float *sA, float *sB) {
-  for (int k = 0; k < nrb; ++k) {
-    __syncthreads();
-    load_tile(sA, G + (size_t)k * kNB * ld + k * kNB, ld);
-    const int fail = factor_tile(sA);
-    if (fail >= 0) return k * kNB + fail;
-    store_tile(sA, G + (size_t)k * kNB * ld + k * kNB, ld);
-    for (int i = k + 1; i < nrb; ++i) {
-      load_tile(sB, G + (size_t)i * kNB * ld + k * kNB, ld);
-      trsm_tile(sA, sB);
-      store_tile(sB, G + (size_t)i * kNB * ld + k * kNB, ld);
-    }
-    __threadfence_block();
-    __syncthreads();
-    for (int i = k + 1; i < nrb; ++i)
-      for (int j = k + 1; j <= i; ++j) {
-        __syncthreads();
-        load_tile(sA, G + (size_t)i * kNB * ld + k * kNB, ld);
-        load_tile(sB, G + (size_t)j * kNB * ld + k * kNB, ld);
-        __syncthreads();
-        update_tile(sA, sB, G + (size_t)i * kNB * ld + j * kNB, ld);
-        __threadfence_block();
-      }
-    __syncthreads();
-  }
-  return -1;
-}
-
-__global__ void __launch_bounds__(256) k_chol_escalate(float *__restrict__ Gw, const float *__restrict__ Gc, int t,
-                                                       int64_t ld, int max_esc, FitState st) {
-  __shared__ float sA[kNB * kSD], sB[kNB * kSD];
-  const int b = blockIdx.x;
-  if (st.info[b] == 0) return;
-  float *G = Gw + (size_t)b * ld * ld;
-  const float *Gcb = Gc + (size_t)b * ld * ld;
-  const int nrb = (int)(ld / kNB);
-  float delta = st.delta[b];
-  int fail = st.info[b] - 1;
-  for (int e = 0; e < max_esc && fail >= 0; ++e) {
-    delta *= 10.0f;
-    const float lam = (float)((double)delta * st.trace[b] / (double)t);
-    __syncthreads();
-    for (int64_t x = threadIdx.x; x < ld * ld; x += 256) {
-      const int64_t r = x / ld, c = x % ld;
-      G[x] = (r == c) ? (r < t ? Gcb[x] + lam : 1.0f) : Gcb[x];
-    }
-    __threadfence_block();
-    __syncthreads();
-    fail = factor_matrix_single(G, ld, nrb, sA, sB);
-    if (threadIdx.x == 0) {
-      st.delta[b] = delta;
-      st.lam[b] = lam;
-    }
-  }
-  if (threadIdx.x == 0) st.info[b] = fail >= 0 ? fail + 1 : 0;
-}
 
 // --------------------------------------------------------------- one right-hand side
 // One-rhs triangular solves, float64 vectors, right-looking over 64-row
@@ -1253,17 +1245,51 @@ __global__ void k_nnls_finish(const int32_t *__restrict__ state, int B, int32_t 
 }
 
 // ------------------------------------------------------------------ launchers
-// Ridge + factorisation (+ escalation) of the work copy Gw of Gc.
+hipError_t launch_fill_i32(int32_t *p, int64_t count, int32_t v, hipStream_t s);
+hipError_t launch_trsv(const float *Gw, const float *dinv, int B, int64_t ld, const double *rhs, double *sw,
+                       double *y, double *x, double *acc, const int32_t *info, hipStream_t s);
 hipError_t launch_cholesky_factor(float *Gw, const float *Gc, int B, int t, int64_t ld, float delta0, int max_esc,
                                   FitState st, float *dinv, void *lsplit, hipStream_t s);
 
-hipError_t launch_cholesky(float *Gw, const float *Gc, int B, int t, int64_t ld, float delta0, int max_esc,
-                           FitState st, float *dinv, void *lsplit, hipStream_t s) {
-  hipLaunchKernelGGL(k_ridge_init, dim3(B), dim3(256), 0, s, Gw, Gc, t, ld, delta0, st);
-  return launch_cholesky_factor(Gw, Gc, B, t, ld, delta0, max_esc, st, dinv, lsplit, s);
+// Escalation rounds over the pairs whose factorisation failed and that have
+// escalations left.  Before each round the number of such pairs is read back
+// to the host (cnt: one device int32), so rounds run only when a pair needs
+// one; with max_esc = 0 nothing is read back.
+static hipError_t launch_esc_rounds(float *Gw, const float *Gc, int B, int t, int64_t ld, int max_esc, FitState st,
+                                    float *dinv, void *lsplit, int32_t *cnt, hipStream_t s) {
+  hipError_t e = hipSuccess;
+  for (int round = 0; round < max_esc; ++round) {
+    hipLaunchKernelGGL(k_count_failed, dim3(1), dim3(256), 0, s, B, st, max_esc, cnt);
+    int32_t failed = 0;
+    if ((e = hipMemcpyAsync(&failed, cnt, sizeof(failed), hipMemcpyDeviceToHost, s)) != hipSuccess) return e;
+    if ((e = hipStreamSynchronize(s)) != hipSuccess) return e;
+    if (failed == 0) break;
+    hipLaunchKernelGGL(k_esc_state, dim3((B + 255) / 256), dim3(256), 0, s, B, t, st, max_esc);
+    hipLaunchKernelGGL(k_esc_copy, dim3((unsigned)ld, B), dim3(256), 0, s, Gw, Gc, t, ld, st);
+    if ((e = launch_cholesky_factor(Gw, Gc, B, t, ld, 0.0f, 0, st, dinv, lsplit, s)) != hipSuccess) return e;
+    hipLaunchKernelGGL(k_esc_restore, dim3((B + 255) / 256), dim3(256), 0, s, B, st.info);
+  }
+  return hipGetLastError();
 }
 
-// Factor the prepared work copy Gw in place (no ridge set-up); escalation as above.
+// Ridge + factorisation of the work copy Gw of Gc, then the escalation rounds.
+hipError_t launch_cholesky(float *Gw, const float *Gc, int B, int t, int64_t ld, float delta0, int max_esc,
+                           FitState st, float *dinv, void *lsplit, const int32_t *bad, int32_t *cnt,
+                           hipStream_t s) {
+  hipLaunchKernelGGL(k_ridge_init, dim3(B), dim3(256), 0, s, Gw, Gc, t, ld, delta0, st, bad);
+  hipError_t e = launch_cholesky_factor(Gw, Gc, B, t, ld, delta0, 0, st, dinv, lsplit, s);
+  if (e != hipSuccess) return e;
+  return launch_esc_rounds(Gw, Gc, B, t, ld, max_esc, st, dinv, lsplit, cnt, s);
+}
+
+hipError_t launch_nonfinite(const float *a, int B, int64_t per, int32_t *bad, hipStream_t s) {
+  if (per <= 0) return hipSuccess;
+  const int64_t blocks = (per + 255) / 256;
+  hipLaunchKernelGGL(k_nonfinite, dim3((unsigned)(blocks < 64 ? blocks : 64), B), dim3(256), 0, s, a, per, bad);
+  return hipGetLastError();
+}
+
+// Factor the prepared work copy Gw in place (no ridge set-up, no escalation).
 hipError_t launch_cholesky_factor(float *Gw, const float *Gc, int B, int t, int64_t ld, float delta0, int max_esc,
                                   FitState st, float *dinv, void *lsplit, hipStream_t s) {
   // Two-level right-looking blocking: 64-wide diagonal factor + panel solve
@@ -1307,10 +1333,9 @@ hipError_t launch_cholesky_factor(float *Gw, const float *Gc, int B, int t, int6
       if (err != hipSuccess) return err;
     }
   }
-  if (max_esc > 0) {
-    hipLaunchKernelGGL(k_chol_escalate, dim3(B), dim3(256), 0, s, Gw, Gc, t, ld, max_esc, st);
-    hipLaunchKernelGGL(k_chol_dinv_escalated, dim3(nrb, B), dim3(64), 0, s, Gw, ld, delta0, st.delta, st.info, dinv);
-  }
+  (void)Gc;
+  (void)delta0;
+  (void)max_esc;
   return hipGetLastError();
 }
 
@@ -1340,6 +1365,41 @@ hipError_t launch_mass_residual(const float *LT, const float *z, const float *m,
                      u, info, row_list, row_count);
   hipLaunchKernelGGL(k_mass_resid_cols, dim3((unsigned)(tp / (4 * kResKeys)), B), dim3(256), 0, s, LT, z, u, w, lam,
                      n, t, tp, np_, res, info, col_list, col_count);
+  return hipGetLastError();
+}
+
+// Mass-fit solve for the factored pairs (info == 0): w = (G + lam I)^-1 h by
+// the float32 factor, then refine_steps refinement steps against the data
+// under the refinement guard above; pairs the guard cuts off are refactored
+// with the ridge raised tenfold and solved again, while escalations remain.
+// Each such round reads back one integer (the number of pairs to refactor).
+hipError_t launch_mass_solve(float *Gw, const float *Gc, float *dinv, void *lsplit, const MassSolve &ms, int B, int n,
+                             int t, int64_t tp, int64_t np_, int refine_steps, int max_esc, FitState st, int32_t *cnt,
+                             hipStream_t s) {
+  hipError_t e;
+  const dim3 gb((B + 255) / 256);
+  if ((e = launch_fill_i32(ms.div, B, 0, s)) != hipSuccess) return e;
+  for (int round = 0;; ++round) {
+    if ((e = launch_trsv(Gw, dinv, B, tp, ms.h, ms.sw, ms.y, ms.w, nullptr, st.info, s)) != hipSuccess) return e;
+    for (int it = 0; it <= refine_steps && refine_steps > 0; ++it) {
+      if ((e = launch_mass_residual(ms.LT, ms.z, ms.m, ms.w, st.lam, B, n, t, tp, np_, ms.u, ms.res, st.info, s,
+                                      nullptr, nullptr, nullptr, nullptr)) != hipSuccess)
+        return e;
+      hipLaunchKernelGGL(k_refine_watch, dim3(B), dim3(256), 0, s, ms.res, ms.h, ms.w, ms.x, tp, it, ms.rprev,
+                         ms.div, st, max_esc);
+      if (it == refine_steps) break;   // the last residual only checks the last step
+      if ((e = launch_trsv(Gw, dinv, B, tp, ms.res, ms.sw, ms.y, ms.x, ms.w, st.info, s)) != hipSuccess) return e;
+    }
+    if (refine_steps == 0 || round == max_esc) break;
+    hipLaunchKernelGGL(k_count_flags, dim3(1), dim3(256), 0, s, B, (const int32_t *)ms.div, cnt);
+    int32_t flagged = 0;
+    if ((e = hipMemcpyAsync(&flagged, cnt, sizeof(flagged), hipMemcpyDeviceToHost, s)) != hipSuccess) return e;
+    if ((e = hipStreamSynchronize(s)) != hipSuccess) return e;
+    if (flagged == 0) break;
+    hipLaunchKernelGGL(k_div_mark, gb, dim3(256), 0, s, B, ms.div, st.info);
+    if ((e = launch_esc_rounds(Gw, Gc, B, t, tp, max_esc, st, dinv, lsplit, cnt, s)) != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL(k_refine_restore, gb, dim3(256), 0, s, B, st.info);
   return hipGetLastError();
 }
 

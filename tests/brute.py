@@ -131,6 +131,16 @@ def compact_attend(Q, C_k, beta, C_v, scale):
     return out
 
 
+def row_rel_err(O_test, O_ref):
+    """Per-row relative Euclidean error, one row and one element at a time."""
+    out = []
+    for a, b in zip(O_test, O_ref):
+        num = math.sqrt(sum((float(x) - float(y)) ** 2 for x, y in zip(a, b)))
+        den = math.sqrt(sum(float(y) ** 2 for y in b))
+        out.append(num / den)
+    return out
+
+
 def joint_attend(Q, C_k, beta, C_v, K_f, V_f, scale):
     """One softmax over the compact keys (logit + beta_r) followed by the
     uncompressed keys (logit + 0), by explicit loops."""

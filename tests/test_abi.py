@@ -56,7 +56,7 @@ def test_default_params():
     p = A.default_params()
     assert p.lambda_m == pytest.approx(0.25) and p.delta_beta == pytest.approx(1e-6)
     assert p.delta_v == pytest.approx(1e-3) and p.eps_w == pytest.approx(1e-12)
-    assert (p.b_min, p.b_max, p.bias_mode, p.max_escalations, p.refine_steps) == (-30.0, 30.0, 0, 3, 2)
+    assert (p.b_min, p.b_max, p.bias_mode, p.max_escalations, p.refine_steps) == (-30.0, 30.0, 0, 6, 2)
     assert (p.pair_chunk, p.select_chunk, p.nnls_max_iter) == (0, 0, 32)
 
 
@@ -133,12 +133,16 @@ def test_entry_points_reject_bad_arguments_without_gpu():
         (L.arckv_merge(r(prob), fake, fake, fake, fake, 10, 1.5, fake, None, None, fake, 0, None), A.ERR_INVALID_ARG),
         (L.arckv_merge(r(prob), fake, fake, fake, fake, 10, 0.25, odd, None, None, fake, 1 << 40, None),
          A.ERR_INVALID_ARG),                                 # misaligned C_k
-        (L.arckv_fit_bias(r(prob), fake, fake, 10, fake, fake, r(A.default_params(bias_mode=2)), fake, fake, None,
-                          fake, 0, None), A.ERR_UNSUPPORTED),
-        (L.arckv_fit_values(r(prob), fake, fake, fake, 10, None, r(par), fake, fake, None, fake, 0, None),
-         A.ERR_INVALID_ARG),
-        (L.arckv_fit_values(r(prob), fake, fake, fake, 10, odd, r(par), fake, fake, None, ctypes.c_void_p(0x10000),
-                            1 << 40, None), A.ERR_INVALID_ARG),                                  # misaligned Y
+        (L.arckv_fit_bias(r(prob), fake, fake, fake, fake, 10, fake, fake, r(A.default_params(bias_mode=2)), fake,
+                          fake, None, fake, 0, None), A.ERR_UNSUPPORTED),
+        (L.arckv_fit_bias(r(prob), None, fake, fake, fake, 10, None, fake, r(par), fake, fake, None,
+                          ctypes.c_void_p(0x10000), 1 << 40, None), A.ERR_INVALID_ARG),  # z recomputed, no K
+        (L.arckv_fit_values(r(prob), None, None, fake, fake, fake, 10, None, r(par), fake, fake, None, fake, 0, None),
+         A.ERR_INVALID_ARG),                                 # Y recomputed, no K / V
+        (L.arckv_fit_values(r(prob), fake, fake, fake, fake, fake, 10, odd, r(par), fake, fake, None,
+                            ctypes.c_void_p(0x10000), 1 << 40, None), A.ERR_INVALID_ARG),  # misaligned Y
+        (L.arckv_fit_values(r(prob), fake, fake, fake, fake, fake, 10, fake, r(par), None, fake, None,
+                            ctypes.c_void_p(0x10000), 1 << 40, None), A.ERR_INVALID_ARG),  # no C_v
         (L.arckv_compact(r(prob), fake, fake, fake, r(ix), float("nan"), r(par), r(t_out), fake, fake, fake, fake,
                          fake, ctypes.c_void_p(0x10000), 1 << 40, None), A.ERR_INVALID_ARG),
         (L.arckv_compact(r(prob), fake, fake, fake, r(ix), 0.1, r(par), r(t_out), fake, fake, fake, fake, fake,

@@ -330,6 +330,34 @@ def test_ridge_escalation():
         oracle.ridge_cholesky_solve(np.zeros((2, 2)) - np.eye(2), np.ones(2), 0.0)
 
 
+def test_row_rel_err_bruteforce():
+    """The parity metric: per-row ||o - o_ref|| / ||o_ref||, against a loop.
+    Rows differ in scale and the error sits in one row, so a wrong axis or a
+    norm over the whole matrix fails."""
+    g = np.random.default_rng(5)
+    O_ref = g.standard_normal((7, 5)) * np.arange(1, 8)[:, None]
+    O = O_ref.copy()
+    O[3] += 0.01 * g.standard_normal(5)
+    got = oracle.row_rel_err(O, O_ref)
+    want = brute.row_rel_err(O, O_ref)
+    assert got.shape == (7,)
+    np.testing.assert_allclose(got, want, rtol=1e-12, atol=0)
+    assert np.count_nonzero(got) == 1 and got[3] > 0
+    np.testing.assert_allclose(oracle.row_rel_err(2 * O_ref, O_ref), 1.0)
+
+
+def test_ridge_escalation_from_zero():
+    """A zero ridge on a singular Gram (two equal columns) escalates from the
+    floor: delta 0 fails at the second pivot, delta = 1e-7 succeeds."""
+    A = np.array([[1.0, 1.0], [1.0, 1.0]])
+    b = np.array([1.0, 2.0])
+    X, d, attempts = oracle.ridge_cholesky_solve(A, b, 0.0)
+    assert attempts == 2 and d == oracle.DELTA_FLOOR
+    np.testing.assert_allclose((A + d * np.eye(2)) @ X, b, rtol=1e-6)
+    with pytest.raises(oracle.CholeskyFailure):
+        oracle.ridge_cholesky_solve(A, b, 0.0, max_escalations=0)
+
+
 # ----------------------------------------------------------------- O8 value fit
 def test_value_fit_matches_augmented_lstsq():
     K, V, Q, *_ = small_pair(16, T=30, n=50)
