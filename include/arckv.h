@@ -312,6 +312,22 @@ arckv_status arckv_attend(int32_t P, int32_t G, int32_t t, int32_t F, float scal
                           const void *C_k, const float *beta, const void *C_v, const void *K_f,
                           const void *V_f, float *out, void *ws, size_t ws_bytes, hipStream_t stream);
 
+/* arckv_attend for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid allocation): the
+ * same arguments and result, no workspace.  The split-key partials go to a
+ * static device array of 64 MiB that the library holds on each GPU it runs
+ * on until the process ends; the call itself allocates nothing.  Returns
+ * ARCKV_ERR_WORKSPACE when arckv_attend_workspace_size(P, G, t, F) exceeds
+ * 64 MiB (for instance P = 512, G = 4 allows t + F up to 16,128; use
+ * arckv_attend with a workspace beyond that), ARCKV_ERR_HIP if the array's
+ * device address cannot be obtained.  Every call on one GPU shares that GPU's
+ * array, so calls that may overlap in time on one GPU (different streams or
+ * host threads) race; calls ordered on one stream do not.  Nothing in the
+ * array needs to start at zero. */
+arckv_status arckv_attend_noalloc(int32_t P, int32_t G, int32_t t, int32_t F, float scale, const void *Q,
+                                  const void *C_k, const float *beta, const void *C_v, const void *K_f,
+                                  const void *V_f, float *out, hipStream_t stream);
+
 /* arckv_compact with the scoring stage replaced by caller-supplied scores
  * [B][T] float32 (for instance from arckv_score_dsa): select, row statistics,
  * merge and both fits exactly as arckv_compact. */

@@ -27,6 +27,7 @@ ENTRY_POINTS = (
     "arckv_status_string", "arckv_set_timing", "arckv_stage_times", "arckv_reset_timing",
     "arckv_attend_workspace_size", "arckv_attend", "arckv_budgets", "arckv_select_count", "arckv_select_ex",
     "arckv_dsa_workspace_size", "arckv_score_dsa", "arckv_compact_scored", "arckv_assign_stats",
+    "arckv_attend_noalloc",
 )
 
 
@@ -100,6 +101,7 @@ def lib():
         L.arckv_compact_scored.argtypes = [P(Problem), vp, vp, vp, vp, ctypes.c_double, P(FitParams), P(i32),
                                            vp, vp, vp, vp, vp, vp, sz, vp]
         L.arckv_attend.argtypes = [i32, i32, i32, i32, ctypes.c_float, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+        L.arckv_attend_noalloc.argtypes = [i32, i32, i32, i32, ctypes.c_float, vp, vp, vp, vp, vp, vp, vp, vp]
         L.arckv_assign_stats.argtypes = [P(Problem), i32, vp, sz, vp, vp]
         for name in ENTRY_POINTS:
             getattr(L, name).restype = ctypes.c_int if name != "arckv_status_string" else ctypes.c_char_p
@@ -334,6 +336,20 @@ def attend(Q, C_k, beta, C_v, K_f=None, V_f=None, scale=None) -> torch.Tensor:
     t = C_k.shape[1] if C_k is not None else 0
     F = K_f.shape[1] if K_f is not None else 0
     return Attender(P, G, t, F, Q.device, scale)(Q, C_k, beta, C_v, K_f, V_f)
+
+
+def attend_noalloc(Q, C_k, beta, C_v, K_f=None, V_f=None, scale=None, out=None) -> torch.Tensor:
+    """arckv_attend_noalloc: attend() without a workspace (the library's static per-GPU scratch holds the
+    partials).  out [P][G][128] float32 may be given; else it is allocated here, by the caller's side."""
+    P, G, _ = Q.shape
+    t = C_k.shape[1] if C_k is not None else 0
+    F = K_f.shape[1] if K_f is not None else 0
+    if out is None:
+        out = torch.empty(P, G, 128, dtype=torch.float32, device=Q.device)
+    _check(lib().arckv_attend_noalloc(int(P), int(G), int(t), int(F), float(scale) if scale else 0.0, _ptr(Q),
+                                      _ptr(C_k), _ptr(beta), _ptr(C_v), _ptr(K_f), _ptr(V_f), _ptr(out), _stream()),
+           "arckv_attend_noalloc")
+    return out
 
 
 DSA_FIELDS = ("L_q", "L_k", "L_x", "b_x", "U_q", "U_k", "U_v", "L_c", "L_v")

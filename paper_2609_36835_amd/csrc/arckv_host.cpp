@@ -109,6 +109,8 @@ hipError_t launch_values_out(const float *Xp, int B, int64_t tp, int t, const in
 hipError_t launch_copy_info(const int32_t *a, const int32_t *b, int B, int32_t *info, hipStream_t s);
 hipError_t launch_copy_f32(const float *src, float *dst, int B, hipStream_t s);
 int attend_chunks(int t, int F);
+size_t attend_scratch_bytes();
+hipError_t attend_scratch(void **ptr);
 hipError_t launch_dsa_proj(const void *X1, const void *X2, bool x2_f32, const void *W1, const void *W2, int B,
                            int nrows, int n_blocks, bool norm, void *out, hipStream_t s);
 hipError_t launch_dsa_w(const void *X, const void *Lx, const float *bx, int B, int n_pos, int dx, int x_group,
@@ -875,9 +877,9 @@ arckv_status arckv_attend_workspace_size(int32_t P, int32_t G, int32_t t, int32_
   return ARCKV_OK;
 }
 
-arckv_status arckv_attend(int32_t P, int32_t G, int32_t t, int32_t F, float scale, const void *Q, const void *C_k,
-                          const float *beta, const void *C_v, const void *K_f, const void *V_f, float *out, void *ws,
-                          size_t ws_bytes, hipStream_t stream) {
+static arckv_status check_attend_args(int32_t P, int32_t G, int32_t t, int32_t F, float scale, const void *Q,
+                                      const void *C_k, const void *C_v, const void *K_f, const void *V_f,
+                                      const float *out) {
   CHECK(check_attend(P, G, t, F));
   if (!Q || !out) return ARCKV_ERR_INVALID_ARG;
   if (t > 0 && (!C_k || !C_v)) return ARCKV_ERR_INVALID_ARG;
@@ -886,6 +888,13 @@ arckv_status arckv_attend(int32_t P, int32_t G, int32_t t, int32_t F, float scal
   if (!aligned(Q, 16) || (C_k && !aligned(C_k, 16)) || (C_v && !aligned(C_v, 16)) || (K_f && !aligned(K_f, 16)) ||
       (V_f && !aligned(V_f, 16)))
     return ARCKV_ERR_INVALID_ARG;
+  return ARCKV_OK;
+}
+
+arckv_status arckv_attend(int32_t P, int32_t G, int32_t t, int32_t F, float scale, const void *Q, const void *C_k,
+                          const float *beta, const void *C_v, const void *K_f, const void *V_f, float *out, void *ws,
+                          size_t ws_bytes, hipStream_t stream) {
+  CHECK(check_attend_args(P, G, t, F, scale, Q, C_k, C_v, K_f, V_f, out));
   if (!ws || !aligned(ws, 256) || ws_bytes < attend_ws_bytes(P, G, t, F)) return ARCKV_ERR_WORKSPACE;
   const float s = scale > 0.0f ? scale : 1.0f / sqrtf((float)kHeadDimH);
   const size_t nch = (size_t)attend_chunks(t, F);
@@ -894,6 +903,24 @@ arckv_status arckv_attend(int32_t P, int32_t G, int32_t t, int32_t F, float scal
   STAGE(ST_ATTEND, launch_attend(P, G, t, F, s, Q, t > 0 ? C_k : nullptr, t > 0 ? beta : nullptr,
                                  t > 0 ? C_v : nullptr, F > 0 ? K_f : nullptr, F > 0 ? V_f : nullptr, part_o, part_ml,
                                  out, stream));
+  return ARCKV_OK;
+}
+
+arckv_status arckv_attend_noalloc(int32_t P, int32_t G, int32_t t, int32_t F, float scale, const void *Q,
+                                  const void *C_k, const float *beta, const void *C_v, const void *K_f,
+                                  const void *V_f, float *out, hipStream_t stream) {
+  CHECK(check_attend_args(P, G, t, F, scale, Q, C_k, C_v, K_f, V_f, out));
+  if (attend_ws_bytes(P, G, t, F) > attend_scratch_bytes()) return ARCKV_ERR_WORKSPACE;
+  void *base = nullptr;
+  if (attend_scratch(&base) != hipSuccess) return ARCKV_ERR_HIP;
+  const float s = scale > 0.0f ? scale : 1.0f / sqrtf((float)kHeadDimH);
+  const size_t nch = (size_t)attend_chunks(t, F);
+  // every partial is written before the combine reads it: nothing to clear
+  float *part_o = reinterpret_cast<float *>(base);
+  float *part_ml = reinterpret_cast<float *>((char *)base + rup((int64_t)((size_t)P * nch * G * kHeadDimH * 4), 256));
+  if (launch_attend(P, G, t, F, s, Q, t > 0 ? C_k : nullptr, t > 0 ? beta : nullptr, t > 0 ? C_v : nullptr,
+                    F > 0 ? K_f : nullptr, F > 0 ? V_f : nullptr, part_o, part_ml, out, stream) != hipSuccess)
+    return ARCKV_ERR_HIP;
   return ARCKV_OK;
 }
 

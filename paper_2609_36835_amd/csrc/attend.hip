@@ -20,6 +20,8 @@
 //                     the chunk's K and V loads are issued up front.
 //   k_attend_combine  merges the partials of a pair with the usual
 //                     max-rescaling and writes o.
+#include <mutex>
+
 #include "common.hpp"
 
 namespace arckv {
@@ -206,6 +208,40 @@ __global__ void __launch_bounds__(1024) k_attend_combine(int G, const float *__r
 }
 
 int attend_chunks(int t, int F) { return (t + F + kAttChunk - 1) / kAttChunk; }
+
+// ---------------------------------------------------------------- static scratch
+// The split-key partials of arckv_attend_noalloc live in this file-scope
+// device array instead of a caller workspace: one copy per GPU, held until the
+// process ends.  On the host the array's name is only a stand-in, never a
+// device address; the address is taken once per device with
+// hipGetSymbolAddress (with that device current) and kept here.
+constexpr size_t kAttendScratchBytes = size_t(64) << 20;
+static __device__ __align__(256) unsigned char scratch[kAttendScratchBytes];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices] = {};
+}  // namespace
+
+size_t attend_scratch_bytes() { return kAttendScratchBytes; }
+
+// Device address of the current device's scratch array.
+hipError_t attend_scratch(void **ptr) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void *p = nullptr;
+    if ((e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch))) != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    g_scratch_ptr[dev] = p;
+  }
+  *ptr = g_scratch_ptr[dev];
+  return hipSuccess;
+}
 
 hipError_t launch_attend(int P, int G, int t, int F, float scale, const void *Q, const void *Ck, const float *beta,
                          const void *Cv, const void *Kf, const void *Vf, float *part_o, float *part_ml, float *out,

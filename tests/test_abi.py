@@ -188,6 +188,15 @@ def test_attend_workspace_and_validation():
         A.ERR_WORKSPACE
     assert L.arckv_attend(2, 4, 10, 0, 0.0, fake, fake, None, fake, None, None, fake, ctypes.c_void_p(0x1010), nws,
                           None) == A.ERR_WORKSPACE
+    # the no-allocation variant: the same argument checks, and partials beyond its 64 MiB static scratch are
+    # rejected before any HIP call
+    assert L.arckv_attend_noalloc(2, 4, 10, 0, 0.0, None, fake, None, fake, None, None, fake, None) == \
+        A.ERR_INVALID_ARG
+    assert L.arckv_attend_noalloc(2, 4, 10, 3, 0.0, fake, fake, None, fake, None, None, fake, None) == \
+        A.ERR_INVALID_ARG
+    assert A.attend_workspace_size(512, 4, 16128, 0) <= 64 << 20 < A.attend_workspace_size(512, 4, 16129, 0)
+    assert L.arckv_attend_noalloc(512, 4, 16129, 0, 0.0, fake, fake, None, fake, None, None, fake, None) == \
+        A.ERR_WORKSPACE
 
 
 def test_budgets_and_select_count_match_oracle():
