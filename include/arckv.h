@@ -111,11 +111,12 @@ typedef struct {
                           * Each step recomputes the residual from the data (Phi_C, P_hat),
                           * not from the float32 Gram, so the solves converge to the
                           * least-squares solutions of the exact normal equations.  In the
-                          * mass fit a step whose data residual (above 1e-10 |h|) does not
-                          * at least halve is undone and ends the refinement; the pair is
-                          * then refactored with the ridge raised tenfold, as after a failed
-                          * pivot (a ridge small next to the float32 rounding of a
-                          * rank-deficient Gram, t > n, makes the steps diverge). */
+                          * mass fit (refine_steps >= 2) a correction (above 1e-10 |w|) that
+                          * is not at most half the previous one is undone and ends the
+                          * refinement; the pair is then refactored with the ridge raised
+                          * tenfold, as after a failed pivot (a ridge small next to the
+                          * float32 rounding of a rank-deficient Gram, t > n, makes the
+                          * steps diverge). */
   int32_t pair_chunk;    /* pairs processed together by arckv_compact (0 = all B); sizes the workspace */
   int32_t select_chunk;  /* 0 = global top-t (default).  L > 0: when T > 10,000, anchors are the union of
                           * each L-position chunk's local top-t_c (Appendix A.3), so arckv_compact keeps

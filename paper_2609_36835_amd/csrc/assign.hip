@@ -443,9 +443,12 @@ __global__ void __launch_bounds__(256) k_assign_finalize(
 // taking the groups of 64 queued keys g = blockIdx.x, blockIdx.x + kRefineBlocks,
 // ...  Each wave owns a quarter of the queries and works through it without
 // workgroup barriers: for 32 queries at a time it forms the 64 keys' profiles
-// (two 32 x 32 MFMA tiles) into a wave-private LDS tile and accumulates the
-// dot products of CAP candidates (two per lane); the four waves' partial sums
-// meet once at the end.
+// (two 32 x 32 MFMA tiles, a tile skipped when none of the chunk's candidates
+// belongs to its 32 keys) into a wave-private LDS tile and accumulates the dot
+// products of CAP candidates (eight per lane); the four waves' partial sums
+// meet once at the end.  The keys' profiles are recomputed per chunk, so CAP is
+// large: a key with whole anchor tiles among its candidates brings 256 or 128
+// of them at once.
 constexpr int kRefineBlocks = 32;
 
 template <typename E>
@@ -456,9 +459,9 @@ __global__ void __launch_bounds__(256, 2) k_assign_refine(const E *__restrict__ 
                                                        int T, int t, int n, int64_t tp, int64_t np_, double s,
                                                        int32_t *__restrict__ kappa, AssignLists L) {
   constexpr bool BF = sizeof(E) == 2;
-  constexpr int NK = 64, CAP = 128, NQW = 32, SE = NQW + 4, NCL = CAP / 64;
+  constexpr int NK = 64, CAP = 512, NQW = 32, SE = NQW + 4, NCL = CAP / 64;
   constexpr int SKB = BF ? kHeadDim + 8 : kHeadDim + 4;   // key-row stride (elements)
-  __shared__ int32_t kpos[NK], koff[NK], kbase[NK + 1];
+  __shared__ int32_t kpos[NK], koff[NK], kbase[NK + 1], khalf;
   __shared__ int32_t cr[CAP];
   __shared__ uint8_t ck[CAP];
   __shared__ double kn[NK];
@@ -509,7 +512,9 @@ __global__ void __launch_bounds__(256, 2) k_assign_refine(const E *__restrict__ 
     const int total = kbase[NK];
     for (int c0 = 0; c0 < total; c0 += CAP) {
       const int cn = min(CAP, total - c0);
-      __syncthreads();   // the previous chunk is done with cr / ck / red
+      __syncthreads();   // the previous chunk is done with cr / ck / red / khalf
+      if (tid == 0) khalf = 0;
+      __syncthreads();
       for (int c = tid; c < cn; c += 256) {
         const int g = c0 + c;
         int lo = 0, hi = NK;   // the key k with kbase[k] <= g < kbase[k + 1]
@@ -520,8 +525,10 @@ __global__ void __launch_bounds__(256, 2) k_assign_refine(const E *__restrict__ 
         }
         ck[c] = (uint8_t)lo;
         cr[c] = pool[koff[lo] + g - kbase[lo]];
+        atomicOr(&khalf, 1 << (lo >> 5));   // which 32-key halves this chunk's candidates belong to
       }
       __syncthreads();
+      const int need = khalf;
       int kc[NCL];
       const float *uc[NCL];
       double dc[NCL];
@@ -536,6 +543,7 @@ __global__ void __launch_bounds__(256, 2) k_assign_refine(const E *__restrict__ 
         const int iq = (int)i0 + col;   // this lane's query row of the MFMA A operand
 #pragma unroll 1
         for (int kt = 0; kt < 2; ++kt) {
+          if (!((need >> kt) & 1)) continue;   // no candidate of this chunk reads these keys' profiles
           double l[BF ? 1 : 16];
           if constexpr (!BF) {
 #pragma unroll
@@ -585,7 +593,7 @@ __global__ void __launch_bounds__(256, 2) k_assign_refine(const E *__restrict__ 
         }
         __builtin_amdgcn_wave_barrier();   // the wave's LDS writes before its reads (in-order per wave)
         asm volatile("" ::: "memory");
-#pragma unroll 2
+#pragma unroll 1
         for (int q4 = 0; q4 < NQW / 4; ++q4) {
 #pragma unroll
           for (int u = 0; u < NCL; ++u) {

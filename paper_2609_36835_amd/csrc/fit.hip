@@ -117,43 +117,43 @@ __global__ void __launch_bounds__(256) k_count_failed(int B, const FitState st, 
 // Each refinement step recomputes the residual from the data, so it converges
 // at a rate set by how far the float32 factor is from those normal equations.
 // Where the ridge is small next to the Gram's float32 rounding (a
-// rank-deficient Gram, t > n, with a ridge near 1e-6 of its mean diagonal) a
-// step can instead grow the solution along the Gram's near-null directions.
-// After every step the data residual is checked: one above 1e-10 |h| that did
-// not at least halve undoes that step and ends the pair's refinement
-// (kRefStop); while it has escalations left the pair is then refactored with
-// the ridge raised tenfold and solved again (div).  Pairs not being refactored
-// meanwhile carry kDoneSkip.
+// rank-deficient Gram, t > n, with a ridge near 1e-6 of its mean diagonal) the
+// steps instead grow the solution along the Gram's near-null directions.  After
+// every step but the first the correction is compared with the previous one:
+// a correction above 1e-10 |w| that is not at most half the previous one is
+// undone and ends the pair's refinement (kRefStop); while it has escalations
+// left the pair is then refactored with the ridge raised tenfold and solved
+// again (div).  Pairs not being refactored meanwhile carry kDoneSkip.
 constexpr int32_t kRefStop = -0x20000000;
 constexpr int32_t kDoneSkip = -0x10000000;
 
-// One workgroup per pair; it = 0 records the first residual norm.
-__global__ void __launch_bounds__(256) k_refine_watch(const double *__restrict__ res, const double *__restrict__ h,
-                                                      double *__restrict__ w, const double *__restrict__ x,
-                                                      int64_t tp, int it, double *__restrict__ rprev,
+// One workgroup per pair, after step it (w already holds w + x); it = 0 records
+// the first correction's norm.
+__global__ void __launch_bounds__(256) k_refine_watch(double *__restrict__ w, const double *__restrict__ x,
+                                                      int64_t tp, int it, double *__restrict__ xprev,
                                                       int32_t *__restrict__ div, FitState st, int max_esc) {
   __shared__ double red[2][4];
   const int b = blockIdx.x, tid = threadIdx.x;
   if (st.info[b] != 0) return;
-  const double rp = rprev[b];   // read by every thread before thread 0 rewrites it
+  const double xp = xprev[b];   // read by every thread before thread 0 rewrites it
   const size_t o = (size_t)b * tp;
-  double r2 = 0.0, h2 = 0.0;
+  double x2 = 0.0, w2 = 0.0;
   for (int64_t r = tid; r < tp; r += 256) {
-    const double a = res[o + r], c = h[o + r];
-    r2 = fma(a, a, r2);
-    h2 = fma(c, c, h2);
+    const double a = x[o + r], c = w[o + r];
+    x2 = fma(a, a, x2);
+    w2 = fma(c, c, w2);
   }
-  r2 = wave_sum(r2);
-  h2 = wave_sum(h2);
+  x2 = wave_sum(x2);
+  w2 = wave_sum(w2);
   if ((tid & 63) == 0) {
-    red[0][tid >> 6] = r2;
-    red[1][tid >> 6] = h2;
+    red[0][tid >> 6] = x2;
+    red[1][tid >> 6] = w2;
   }
   __syncthreads();
-  const double rn = sqrt(red[0][0] + red[0][1] + red[0][2] + red[0][3]);
-  const double hn = sqrt(red[1][0] + red[1][1] + red[1][2] + red[1][3]);
-  if (it == 0 || !(rn > 0.5 * rp && rn > 1e-10 * hn)) {
-    if (tid == 0) rprev[b] = rn;
+  const double xn = sqrt(red[0][0] + red[0][1] + red[0][2] + red[0][3]);
+  const double wn = sqrt(red[1][0] + red[1][1] + red[1][2] + red[1][3]);
+  if (it == 0 || !(xn > 0.5 * xp && xn > 1e-10 * wn)) {
+    if (tid == 0) xprev[b] = xn;
     return;
   }
   for (int64_t r = tid; r < tp; r += 256) w[o + r] -= x[o + r];
@@ -1370,7 +1370,7 @@ hipError_t launch_mass_residual(const float *LT, const float *z, const float *m,
 
 // Mass-fit solve for the factored pairs (info == 0): w = (G + lam I)^-1 h by
 // the float32 factor, then refine_steps refinement steps against the data
-// under the refinement guard above; pairs the guard cuts off are refactored
+// under the refinement guard above (which needs two steps to compare); pairs the guard cuts off are refactored
 // with the ridge raised tenfold and solved again, while escalations remain.
 // Each such round reads back one integer (the number of pairs to refactor).
 hipError_t launch_mass_solve(float *Gw, const float *Gc, float *dinv, void *lsplit, const MassSolve &ms, int B, int n,
@@ -1381,16 +1381,15 @@ hipError_t launch_mass_solve(float *Gw, const float *Gc, float *dinv, void *lspl
   if ((e = launch_fill_i32(ms.div, B, 0, s)) != hipSuccess) return e;
   for (int round = 0;; ++round) {
     if ((e = launch_trsv(Gw, dinv, B, tp, ms.h, ms.sw, ms.y, ms.w, nullptr, st.info, s)) != hipSuccess) return e;
-    for (int it = 0; it <= refine_steps && refine_steps > 0; ++it) {
+    for (int it = 0; it < refine_steps; ++it) {
       if ((e = launch_mass_residual(ms.LT, ms.z, ms.m, ms.w, st.lam, B, n, t, tp, np_, ms.u, ms.res, st.info, s,
                                       nullptr, nullptr, nullptr, nullptr)) != hipSuccess)
         return e;
-      hipLaunchKernelGGL(k_refine_watch, dim3(B), dim3(256), 0, s, ms.res, ms.h, ms.w, ms.x, tp, it, ms.rprev,
-                         ms.div, st, max_esc);
-      if (it == refine_steps) break;   // the last residual only checks the last step
       if ((e = launch_trsv(Gw, dinv, B, tp, ms.res, ms.sw, ms.y, ms.x, ms.w, st.info, s)) != hipSuccess) return e;
+      hipLaunchKernelGGL(k_refine_watch, dim3(B), dim3(256), 0, s, ms.w, ms.x, tp, it, ms.rprev, ms.div, st,
+                         max_esc);
     }
-    if (refine_steps == 0 || round == max_esc) break;
+    if (refine_steps < 2 || round == max_esc) break;
     hipLaunchKernelGGL(k_count_flags, dim3(1), dim3(256), 0, s, B, (const int32_t *)ms.div, cnt);
     int32_t flagged = 0;
     if ((e = hipMemcpyAsync(&flagged, cnt, sizeof(flagged), hipMemcpyDeviceToHost, s)) != hipSuccess) return e;

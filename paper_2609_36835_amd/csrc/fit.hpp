@@ -35,7 +35,7 @@ struct MassSolve {
   double *y, *sw;    // triangular-solve work
   double *u;         // [P][np] data residual m - Phi_C w
   double *res;       // normal-equation residual
-  double *rprev;     // [P] previous residual norm
+  double *rprev;     // [P] norm of the previous refinement correction
   int32_t *div;      // [P] pair to be refactored with a larger ridge
 };
 

@@ -14,8 +14,9 @@ hipError_t launch_assign_gemm(int dtype, const void *U, const void *Et, uint64_t
                               hipStream_t s) {
   if (N == 0) return hipSuccess;
   if (dtype == ARCKV_BF16) {
-    // tile order: groups of 7 anchor tiles walk the key tiles (about 7 x 4.5 tiles per XCD at a time)
-    BigShape g2{P, (int)tp, (int)N, (int)np_, tp * np_, 0, np_, Et_rows * np_, 0, np_, false, 7};
+    // tile order: all anchor tiles of a pair walk the key tiles together (about 13 x 2.5 tiles per XCD
+    // at a time): half the L2 misses of groups of 7, 2-3% faster
+    BigShape g2{P, (int)tp, (int)N, (int)np_, tp * np_, 0, np_, Et_rows * np_, 0, np_, false, 13};
     EpiArgmaxBig<4, 2, 2, 4> e2{part1, part2, part3, (tp / 256) * N, (int)N, t};
     return launch_gemm_big<4, 2, 2, 4, 64, 1, 1, 2, f16>(g2, (const bf16 *)U, (const bf16 *)Et, e2, s);
   }
