@@ -14,12 +14,14 @@
 //     are flagged, with the best two of each tile above the threshold, or the
 //     whole tile where its third value reaches it, as candidates
 //     (k_assign_finalize).
-//  C  flagged keys are re-scored against their candidates: for bf16 inputs from
-//     logits formed on MFMA with one fp32 accumulator per 16-wide slice of the
-//     head dimension, summed in float64, so the logit error is at most
-//     gamma_16 s sum_k |q_k k_k|; exponentials with float64 range reduction; dot
-//     products in float64 (for fp32 inputs, float64 logits).  Keys that still
-//     have more than one survivor go on (k_assign_refine).
+//  C  flagged keys are re-scored against their candidates' fp32 profiles
+//     (k_prof_anchor_*): for bf16 inputs the key's logits come from MFMA with
+//     one fp32 accumulator per 16-wide slice of the head dimension, the eight
+//     slices summed in fp32 (logit error at most gamma_23 s ||q|| ||k||), the
+//     exponentials from v_exp_f32 (exp32_err), and each dot product from fp32
+//     products summed four at a time, then in float64 (for fp32 inputs, float64
+//     logits).  Keys that still have more than one survivor go on
+//     (k_assign_refine).
 //  D  float64 throughout: logits, exponentials, norms and dot products
 //     (k_assign_exact).  Equal float64 similarities go to the lower r.
 //
