@@ -443,35 +443,36 @@ __global__ void __launch_bounds__(256) k_assign_finalize(
 // bound on both is decided; the survivors of the others go to pass D.
 // Work distribution: a fixed grid of kRefineBlocks workgroups per pair, each
 // taking the groups of 64 queued keys g = blockIdx.x, blockIdx.x + kRefineBlocks,
-// ...  Each wave owns a quarter of the queries and works through it without
-// workgroup barriers: for 32 queries at a time it forms the 64 keys' profiles
-// (two 32 x 32 MFMA tiles, a tile skipped when none of the chunk's candidates
-// belongs to its 32 keys) into a wave-private LDS tile and accumulates the dot
-// products of CAP candidates (eight per lane); the four waves' partial sums
-// meet once at the end.  The keys' profiles are recomputed per chunk, so CAP is
-// large: a key with whole anchor tiles among its candidates brings 256 or 128
-// of them at once.
+// ...  The queries are swept in tiles of 128.  Per tile the eight waves form the
+// 64 keys' profiles (one 32 x 32 MFMA tile each: a key half by a quarter of the
+// queries, skipped when none of the chunk's candidates belongs to that half)
+// into a shared LDS tile; each wave takes 32 candidates, two per load
+// instruction: a half-wave covers one candidate's 128 queries, four per lane,
+// so every load reads two contiguous 512-byte runs of anchor profile rows.  A
+// tile's anchor-profile loads are issued before its profile phase.  The
+// candidates' partial sums stay in registers (float64) across the tiles and are
+// reduced over the half-waves once per chunk.
 constexpr int kRefineBlocks = 32;
 
 template <typename E>
-__global__ void __launch_bounds__(256, 2) k_assign_refine(const E *__restrict__ Q, const E *__restrict__ K,
+__global__ void __launch_bounds__(512, 2) k_assign_refine(const E *__restrict__ Q, const E *__restrict__ K,
                                                        const float *__restrict__ zmerge,
                                                        const AssignPair *__restrict__ pn,
                                                        const float *__restrict__ Ua, const double *__restrict__ anorm,
                                                        int T, int t, int n, int64_t tp, int64_t np_, double s,
                                                        int32_t *__restrict__ kappa, AssignLists L) {
   constexpr bool BF = sizeof(E) == 2;
-  constexpr int NK = 64, CAP = 512, NQW = 32, SE = NQW + 4, NCL = CAP / 64;
+  constexpr int NK = 64, NW = 8, CPW = 32, CAP = NW * CPW, QT = 128, SE = QT + 4;
   constexpr int SKB = BF ? kHeadDim + 8 : kHeadDim + 4;   // key-row stride (elements)
   __shared__ int32_t kpos[NK], koff[NK], kbase[NK + 1], khalf;
   __shared__ int32_t cr[CAP];
-  __shared__ uint8_t ck[CAP];
+  __shared__ int32_t ck[CAP];
   __shared__ double kn[NK];
   __shared__ __attribute__((aligned(16))) E sK[NK * SKB];
-  __shared__ __attribute__((aligned(16))) float eW[4][NK * SE];   // wave-private profile tiles
-  __shared__ double red[4][CAP];
-  int bx, b;
-  pair_block(kRefineBlocks, gridDim.y, bx, b);
+  __shared__ __attribute__((aligned(16))) float eS[NK * SE];   // the keys' profiles on one query tile
+  // pair-major over the whole grid (no XCD remap): the anchor profiles do not
+  // fit an L2 anyway, and a pair with many candidates spreads over every XCD
+  const int bx = blockIdx.x, b = blockIdx.y;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int h = lane >> 5, col = lane & 31;
   const int F = L.fcnt[b];
@@ -482,8 +483,7 @@ __global__ void __launch_bounds__(256, 2) k_assign_refine(const E *__restrict__ 
   const float *Uab = Ua + (size_t)b * tp * np_;
   int32_t *pool = L.pool + (size_t)b * L.pcap;
   double *psim = L.psim + (size_t)b * L.pcap;
-  float *ew = eW[wave];
-  const int64_t qw = np_ / 4, qlo = wave * qw;   // this wave's queries
+  const int kt = wave >> 2, qsub = wave & 3;   // this wave's key half and query quarter in the profile phase
   for (int f0 = bx * NK; f0 < F; f0 += kRefineBlocks * NK) {   // uniform over the workgroup
     const int nk = min(NK, F - f0);
     __syncthreads();   // the previous group is done with the shared arrays
@@ -506,7 +506,7 @@ __global__ void __launch_bounds__(256, 2) k_assign_refine(const E *__restrict__ 
       }
       kbase[NK] = acc;
     }
-    for (int x = tid; x < NK * kHeadDim; x += 256) {   // the keys' rows (zero for empty slots)
+    for (int x = tid; x < NK * kHeadDim; x += NW * 64) {   // the keys' rows (zero for empty slots)
       const int k = x / kHeadDim, c = x % kHeadDim;
       sK[k * SKB + c] = kpos[k] >= 0 ? K[((size_t)b * T + kpos[k]) * kHeadDim + c] : (E)0.0f;
     }
@@ -514,48 +514,52 @@ __global__ void __launch_bounds__(256, 2) k_assign_refine(const E *__restrict__ 
     const int total = kbase[NK];
     for (int c0 = 0; c0 < total; c0 += CAP) {
       const int cn = min(CAP, total - c0);
-      __syncthreads();   // the previous chunk is done with cr / ck / red / khalf
+      __syncthreads();   // the previous chunk is done with cr / ck / khalf
       if (tid == 0) khalf = 0;
       __syncthreads();
-      for (int c = tid; c < cn; c += 256) {
-        const int g = c0 + c;
-        int lo = 0, hi = NK;   // the key k with kbase[k] <= g < kbase[k + 1]
-        while (hi - lo > 1) {
-          const int mid = (lo + hi) >> 1;
-          if (kbase[mid] <= g) lo = mid;
-          else hi = mid;
+      for (int c = tid; c < CAP; c += NW * 64) {
+        int lo = -1, r = 0;
+        if (c < cn) {
+          const int g = c0 + c;
+          int lo2 = 0, hi = NK;   // the key k with kbase[k] <= g < kbase[k + 1]
+          while (hi - lo2 > 1) {
+            const int mid = (lo2 + hi) >> 1;
+            if (kbase[mid] <= g) lo2 = mid;
+            else hi = mid;
+          }
+          lo = lo2;
+          r = pool[koff[lo] + g - kbase[lo]];
+          atomicOr(&khalf, 1 << (lo >> 5));   // which 32-key halves this chunk's candidates belong to
         }
-        ck[c] = (uint8_t)lo;
-        cr[c] = pool[koff[lo] + g - kbase[lo]];
-        atomicOr(&khalf, 1 << (lo >> 5));   // which 32-key halves this chunk's candidates belong to
+        ck[c] = lo;
+        cr[c] = r;
       }
       __syncthreads();
       const int need = khalf;
-      int kc[NCL];
-      const float *uc[NCL];
-      double dc[NCL];
+      double acc[CPW / 2];
 #pragma unroll
-      for (int u = 0; u < NCL; ++u) {
-        const int c = lane + 64 * u;
-        kc[u] = c < cn ? ck[c] : -1;
-        uc[u] = Uab + (size_t)(c < cn ? cr[c] : 0) * np_;
-        dc[u] = 0.0;
-      }
-      for (int64_t i0 = qlo; i0 < qlo + qw; i0 += NQW) {
-        const int iq = (int)i0 + col;   // this lane's query row of the MFMA A operand
-#pragma unroll 1
-        for (int kt = 0; kt < 2; ++kt) {
-          if (!((need >> kt) & 1)) continue;   // no candidate of this chunk reads these keys' profiles
+      for (int u = 0; u < CPW / 2; ++u) acc[u] = 0.0;
+      const int cw0 = wave * CPW;   // this wave's candidates cw0 + 2u + h
+      const int qo = 4 * col;        // half-wave lane col covers queries i0 + 4 col .. + 3
+      for (int i0 = 0; i0 < n; i0 += QT) {
+        // ---- this tile's anchor-profile values, loaded first so that their
+        // latency overlaps the profile phase (they do not depend on it)
+        f32x4 w[CPW / 2];
+#pragma unroll
+        for (int u = 0; u < CPW / 2; ++u) {
+          const int c = cw0 + 2 * u + h;
+          w[u] = ck[c] >= 0 ? *reinterpret_cast<const f32x4 *>(Uab + (size_t)cr[c] * np_ + i0 + qo)
+                            : f32x4{0.f, 0.f, 0.f, 0.f};
+        }
+        // ---- the 64 keys' profiles on queries [i0, i0 + 128)
+        if ((need >> kt) & 1) {
+          const int iq = i0 + 32 * qsub + col;   // this lane's query row of the MFMA A operand
           double l[BF ? 1 : 16];
-          if constexpr (!BF) {
-#pragma unroll
-            for (int v = 0; v < 16; ++v) l[v] = 0.0;
-          }
           f32x16 lsum;
           if constexpr (BF) {
             const bf16 *qrow = reinterpret_cast<const bf16 *>(Qb) + (size_t)(iq < n ? iq : 0) * kHeadDim + 8 * h;
             const bf16 *krow = reinterpret_cast<const bf16 *>(sK) + (kt * 32 + col) * SKB + 8 * h;
-#pragma unroll
+#pragma unroll 2
             for (int ks = 0; ks < 8; ++ks) {
               const bf16x8 a = iq < n ? *reinterpret_cast<const bf16x8 *>(qrow + ks * 16) : Mfma<bf16>::zero();
               const bf16x8 bk = *reinterpret_cast<const bf16x8 *>(krow + ks * 16);
@@ -567,12 +571,14 @@ __global__ void __launch_bounds__(256, 2) k_assign_refine(const E *__restrict__ 
               }
             }
           } else {
+#pragma unroll
+            for (int v = 0; v < 16; ++v) l[v] = 0.0;
             const float *krow = reinterpret_cast<const float *>(sK) + (kt * 32 + col) * SKB;
             for (int k = 0; k < kHeadDim; k += 4) {
               const f32x4 kv = *reinterpret_cast<const f32x4 *>(krow + k);
 #pragma unroll
               for (int v = 0; v < 16; ++v) {
-                const int qi = (int)i0 + acc_row(v, lane);
+                const int qi = i0 + 32 * qsub + acc_row(v, lane);
                 if (qi < n) {
                   const f32x4 qv = *reinterpret_cast<const f32x4 *>(reinterpret_cast<const float *>(Qb) +
                                                                    (size_t)qi * kHeadDim + k);
@@ -584,41 +590,41 @@ __global__ void __launch_bounds__(256, 2) k_assign_refine(const E *__restrict__ 
           }
 #pragma unroll
           for (int v = 0; v < 16; ++v) {
-            const int qi = acc_row(v, lane);
+            const int qi = 32 * qsub + acc_row(v, lane);
             float ev = 0.0f;
             if (i0 + qi < n) {
               if constexpr (BF) ev = __builtin_amdgcn_exp2f(fmaf(lsum[v], c2, -zs2));
               else ev = (float)exp(s * l[v] - zm);
             }
-            ew[(kt * 32 + col) * SE + qi] = ev;
+            eS[(kt * 32 + col) * SE + qi] = ev;
           }
         }
-        __builtin_amdgcn_wave_barrier();   // the wave's LDS writes before its reads (in-order per wave)
-        asm volatile("" ::: "memory");
-#pragma unroll 1
-        for (int q4 = 0; q4 < NQW / 4; ++q4) {
+        __syncthreads();   // the tile's profiles are complete
+        // ---- 32 candidates per wave: half-wave h takes candidate cw0 + 2u + h
 #pragma unroll
-          for (int u = 0; u < NCL; ++u) {
-            if (kc[u] >= 0) {
-              const f32x4 e4 = *reinterpret_cast<const f32x4 *>(&ew[kc[u] * SE + 4 * q4]);
-              const f32x4 w = *reinterpret_cast<const f32x4 *>(uc[u] + i0 + 4 * q4);
-              float p4 = e4[0] * w[0];   // four non-negative products in fp32 (within gamma_4), then float64
+        for (int u = 0; u < CPW / 2; ++u) {
+          const int k = ck[cw0 + 2 * u + h];
+          if (k >= 0) {
+            const f32x4 e4 = *reinterpret_cast<const f32x4 *>(&eS[k * SE + qo]);
+            float p4 = e4[0] * w[u][0];   // four non-negative products in fp32 (within gamma_4), then float64
 #pragma unroll
-              for (int e = 1; e < 4; ++e) p4 = fmaf(e4[e], w[e], p4);
-              dc[u] += (double)p4;
-            }
+            for (int e = 1; e < 4; ++e) p4 = fmaf(e4[e], w[u][e], p4);
+            acc[u] += (double)p4;
           }
         }
-        __builtin_amdgcn_wave_barrier();   // reads done before the next tile overwrites the wave's tile
-        asm volatile("" ::: "memory");
+        __syncthreads();   // reads of the tile done before the next one overwrites it
       }
+      // ---- reduce each candidate's partial sums over its half-wave
 #pragma unroll
-      for (int u = 0; u < NCL; ++u) red[wave][lane + 64 * u] = dc[u];
-      __syncthreads();
-      for (int c = tid; c < cn; c += 256) {
-        const double d = red[0][c] + red[1][c] + red[2][c] + red[3][c];
-        const int k = ck[c];
-        psim[koff[k] + c0 + c - kbase[k]] = d / anorm[(size_t)b * tp + cr[c]];
+      for (int u = 0; u < CPW / 2; ++u) {
+        double d = acc[u];
+#pragma unroll
+        for (int m = 16; m >= 1; m >>= 1) d += __shfl_xor(d, m, 64);
+        const int c = cw0 + 2 * u + h;
+        if (col == 0 && c < cn) {
+          const int k = ck[c];
+          psim[koff[k] + c0 + c - kbase[k]] = d / anorm[(size_t)b * tp + cr[c]];
+        }
       }
     }
     __syncthreads();   // every similarity of the group's keys is in the pool
@@ -892,10 +898,10 @@ hipError_t launch_assign_refine(int dtype, const void *Q, const void *K, const f
   if (T - t <= 0) return hipSuccess;
   const dim3 g(kRefineBlocks, P);
   if (dtype == ARCKV_BF16)
-    hipLaunchKernelGGL(k_assign_refine<bf16>, g, dim3(256), 0, s, (const bf16 *)Q, (const bf16 *)K, zmerge,
+    hipLaunchKernelGGL(k_assign_refine<bf16>, g, dim3(512), 0, s, (const bf16 *)Q, (const bf16 *)K, zmerge,
                        (const AssignPair *)pn, Ua, anorm, T, t, n, tp, np_, (double)scale, kappa, L);
   else
-    hipLaunchKernelGGL(k_assign_refine<float>, g, dim3(256), 0, s, (const float *)Q, (const float *)K, zmerge,
+    hipLaunchKernelGGL(k_assign_refine<float>, g, dim3(512), 0, s, (const float *)Q, (const float *)K, zmerge,
                        (const AssignPair *)pn, Ua, anorm, T, t, n, tp, np_, (double)scale, kappa, L);
   return hipGetLastError();
 }
