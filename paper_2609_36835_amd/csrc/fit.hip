@@ -14,8 +14,9 @@
 //                                     64 columns inside a 256-wide outer panel;
 //                                     the rest of the matrix is updated once
 //                                     per outer panel by the big contraction
-//                                     on three bf16 planes of the panel (six
-//                                     products, float32-accurate)
+//                                     on fp16 MFMA, the panel scaled per row
+//                                     by a power of two and split into hi + lo
+//                                     (three products, about 2^-22 relative)
 //                    a failed pivot records info = column + 1 for that pair
 //   escalation       pairs that failed are refactored by the same kernels with
 //                    delta raised tenfold (from 1e-7 when zero), at most
@@ -434,48 +435,62 @@ __global__ void __launch_bounds__(256) k_chol_upd(float *__restrict__ Gw, int64_
     }
 }
 
-// Outer trailing update as a bf16 MFMA contraction: the finished 256-column
-// panel L[K1:ld, K0:K1] is split exactly into three bf16 planes (x = hi + mid
-// + lo, 8 significant bits each), and G -= L L^T takes the six products whose
-// plane indices sum to at most 2 (the dropped terms are below 2^-23 of |x y|),
-// so it reproduces the fp32 update at fp32 accuracy on the bf16 MFMA rate.
-// Planes: Ls [P][3][ld][256], row r holding L[r][K0:K0+256].
-__global__ void __launch_bounds__(256) k_chol_split3(const float *__restrict__ Gw, int64_t ld, int K0, int K1,
-                                                     bf16 *__restrict__ Ls, const int32_t *__restrict__ info) {
+// Rows K1.. of the panel columns K0 .. K0 + 255 for the trailing update on
+// fp16 MFMA: each row is scaled by a power of two that brings its largest
+// magnitude into [2^13, 2^14) and split exactly into fp16 hi + lo (22
+// significant bits), so hi.hi + hi.lo + lo.hi is the row product to about
+// 2^-22 relative.  One wave per row (four columns per lane); the inverse scale
+// of each row goes after the two planes for the update's epilogue.
+// Layout per pair: hi [ld][256], lo [ld][256] (fp16), inverse scales [ld] (fp32).
+__global__ void __launch_bounds__(256) k_chol_split2(const float *__restrict__ Gw, int64_t ld, int K0, int K1,
+                                                     f16 *__restrict__ Ls, const int32_t *__restrict__ info) {
   const int b = blockIdx.y;
   if (info[b] != 0) return;
-  const int64_t e = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 4;   // 4 consecutive columns
-  const int64_t r = K1 + e / 256, q = e % 256;
-  if (r >= ld) return;
-  const f32x4 v = *reinterpret_cast<const f32x4 *>(Gw + (size_t)b * ld * ld + (size_t)r * ld + K0 + q);
-  bf16 *base = Ls + (size_t)b * 3 * ld * 256 + (size_t)r * 256 + q;
+  const int lane = threadIdx.x & 63;
+  const int64_t r = K1 + (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (r >= ld) return;   // uniform over the wave
+  const f32x4 v = *reinterpret_cast<const f32x4 *>(Gw + (size_t)b * ld * ld + (size_t)r * ld + K0 + 4 * lane);
+  float m = fmaxf(fmaxf(fabsf(v[0]), fabsf(v[1])), fmaxf(fabsf(v[2]), fabsf(v[3])));
+  m = wave_max(m);
+  int ex = 0;
+  if (m > 0.0f) frexpf(m, &ex);          // m = f 2^ex, f in [0.5, 1)
+  const int sh = min(14 - ex, 126);      // m 2^sh < 2^14
+  f16 *base = Ls + (size_t)b * 3 * ld * 256 + (size_t)r * 256 + 4 * lane;
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
-    const bf16 hi = (bf16)v[k];
-    const float r1 = v[k] - (float)hi;
-    const bf16 mid = (bf16)r1;
-    const bf16 lo = (bf16)(r1 - (float)mid);
+    const float x = ldexpf(v[k], sh);
+    const f16 hi = (f16)x;
     base[k] = hi;
-    base[(size_t)ld * 256 + k] = mid;
-    base[(size_t)2 * ld * 256 + k] = lo;
+    base[(size_t)ld * 256 + k] = (f16)(x - (float)hi);
   }
+  if (lane == 0) reinterpret_cast<float *>(Ls + (size_t)b * 3 * ld * 256 + (size_t)2 * ld * 256)[r] = ldexpf(1.0f, -sh);
 }
 
-// G[K1 + r][K1 + c] -= acc for the tile's entries with c <= r + 63 (the lower
-// triangle, up to whole diagonal 64-blocks); per row block of the wave, every
-// old value is loaded before any store so the loads pipeline.
+// G[K1 + r][K1 + c] -= acc s_r s_c for the tile's entries with c <= r + 63
+// (the lower triangle, up to whole diagonal 64-blocks), s the rows' inverse
+// scales of k_chol_split2 (256 x 256 tiles, 512 threads); per row block of the
+// wave, every old value is loaded before any store so the loads pipeline.
 template <int TM, int TN>
 struct EpiCholUpd {
   float *G;
   int64_t ld;
   int K1;
   const int32_t *info;
+  const float *rs;        // inverse scales of pair 0, rows from K1
+  int64_t rs_pair;        // floats between pairs
   __device__ __forceinline__ bool skip(int p) const { return info[p] != 0; }
-  __device__ __forceinline__ void operator()(f32x16 (&acc)[TM][TN], int p, int row0, int col0, int, int, int lane,
-                                             int, int) const {
-    if (info[p] != 0) return;
+  __device__ __forceinline__ void operator()(f32x16 (&acc)[TM][TN], int p, int row0, int col0, int mt, int nt,
+                                             int lane, int, int) const {
+    if (info[p] != 0) return;   // uniform over the workgroup
+    // the tile's 256 row and 256 column scales, staged in LDS (the operand
+    // stages are free: the caller synchronised the workgroup before the epilogue)
+    extern __shared__ __attribute__((aligned(1024))) char big_smem[];
+    float *ssc = reinterpret_cast<float *>(big_smem);
+    const float *sp = rs + (size_t)p * rs_pair;
+    for (int x = threadIdx.x; x < 512; x += blockDim.x) ssc[x] = sp[(x < 256 ? mt : nt) * 256 + (x & 255)];
+    __syncthreads();
     float *Gp = G + (size_t)p * ld * ld + (size_t)K1 * ld + K1;
-    const int col = lane & 31;
+    const int col = lane & 31, rl = row0 - mt * 256, cl = col0 - nt * 256;
 #pragma unroll
     for (int i = 0; i < TM; ++i) {
       float old[TN][16];
@@ -487,12 +502,15 @@ struct EpiCholUpd {
           old[j][v] = __builtin_nontemporal_load(&Gp[(size_t)r * ld + c]);
         }
 #pragma unroll
-      for (int j = 0; j < TN; ++j)
+      for (int j = 0; j < TN; ++j) {
+        const float scj = ssc[256 + cl + 32 * j + col];
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
           const int r = row0 + 32 * i + acc_row(v, lane), c = col0 + 32 * j + col;
-          if (c <= r + 63) Gp[(size_t)r * ld + c] = old[j][v] - acc[i][j][v];
+          const float sr = ssc[rl + 32 * i + acc_row(v, lane)];
+          if (c <= r + 63) Gp[(size_t)r * ld + c] = old[j][v] - acc[i][j][v] * (sr * scj);
         }
+      }
     }
   }
 };
@@ -1314,22 +1332,23 @@ hipError_t launch_cholesky_factor(float *Gw, const float *Gc, int B, int t, int6
       }
     }
     if (K1 < ld) {
-      // rank-256 trailing update on bf16 MFMA with the split panel (see k_chol_split3)
-      bf16 *Ls = reinterpret_cast<bf16 *>(lsplit);
+      // rank-256 trailing update on fp16 MFMA with the scaled split panel (see k_chol_split2)
+      f16 *Ls = reinterpret_cast<f16 *>(lsplit);
       const int64_t rows = ld - K1;
-      hipLaunchKernelGGL(k_chol_split3, dim3((unsigned)(rows * 256 / 4 / 256), B), dim3(256), 0, s, Gw, ld, K0, K1,
-                         Ls, st.info);
-      // The six products with plane indices summing to at most 2 as one
-      // contraction over K = 6 x 256: segments (hi,hi) (hi,mid) (mid,hi)
-      // (hi,lo) (lo,hi) (mid,mid), so 256 x 256 tiles fit the LDS.
-      BigShape g{B, (int)rows, (int)rows, 6 * kOuter, 3 * ld * 256, ld * 256, 256, 3 * ld * 256, ld * 256, 256, true,
+      hipLaunchKernelGGL(k_chol_split2, dim3((unsigned)(rows / 4), B), dim3(256), 0, s, Gw, ld, K0, K1, Ls, st.info);
+      // The three products hi.hi, hi.lo, lo.hi as one contraction over
+      // K = 3 x 256 (each 256-column segment reads one plane pair), so 256 x 256
+      // tiles fit the LDS.
+      BigShape g{B, (int)rows, (int)rows, 3 * kOuter, 3 * ld * 256, ld * 256, 256, 3 * ld * 256, ld * 256, 256, true,
                  4};
       g.kseg = kOuter;
-      g.sega = 0u | (0u << 2) | (1u << 4) | (0u << 6) | (2u << 8) | (1u << 10);
-      g.segb = 0u | (1u << 2) | (0u << 4) | (2u << 6) | (0u << 8) | (1u << 10);
-      EpiCholUpd<2, 4> e{Gw, ld, K1, st.info};
-      const hipError_t err =
-          launch_gemm_big<4, 2, 2, 4, 64, 1, 1, 2>(g, Ls + (size_t)K1 * 256, Ls + (size_t)K1 * 256, e, s);
+      g.sega = 0u | (0u << 2) | (1u << 4);
+      g.segb = 0u | (1u << 2) | (0u << 4);
+      EpiCholUpd<2, 4> e{Gw, ld, K1, st.info,
+                         reinterpret_cast<const float *>(Ls + (size_t)2 * ld * 256) + K1, 3 * ld * 256 / 2};
+      const hipError_t err = launch_gemm_big<4, 2, 2, 4, 64, 1, 1, 2, f16>(
+          g, reinterpret_cast<const bf16 *>(Ls + (size_t)K1 * 256), reinterpret_cast<const bf16 *>(Ls + (size_t)K1 * 256),
+          e, s);
       if (err != hipSuccess) return err;
     }
   }
