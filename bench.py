@@ -178,14 +178,14 @@ def measured_traffic(which, wl):
     return rec.get("traffic_bytes_per_launch")
 
 
-def stage_rooflines(wl, t, stages, steps, refine_steps=2, bias_mode=0):
+def stage_rooflines(wl, t, stages, steps, refine_steps=2, bias_mode=0, value_refine_steps=1):
     """Per-stage roofline.  `algorithmic_*` is the method's own work for all pairs (the flops of a contraction,
     or the HBM bytes a stage must move), and `frac` prices it at the arithmetic's peak over the stage's
     event-timed duration per step.  Where the implementation issues more than that, `issued_*` / `issued_frac`
     report what it runs:
       - the Grams and the value right-hand side on split bf16 operands issue three bf16 products per term;
-      - the two solves include `refine_steps` refinement steps against the data (each a residual and another
-        solve), which the method itself does not need: its solve is one forward and one backward triangular
+      - the two solves include `refine_steps` (mass fit) and `value_refine_steps` refinement steps against the
+        data (each a residual and another solve), which the method itself does not need: its solve is one forward and one backward triangular
         sweep (mass fit: L read twice, 4 t^2 bytes per pair; value fit: 2 t^2 d flops per pair);
       - the profile pass materialises E^T (2 bytes per entry) for the assignment contraction: its algorithmic work
         is the logit contraction (2 n T d flops), the store is the implementation's.
@@ -194,7 +194,7 @@ def stage_rooflines(wl, t, stages, steps, refine_steps=2, bias_mode=0):
     the beta solve is a data-dependent number of pivoting iterations and is not priced."""
     B, T, n, d = wl.pairs, wl.T, wl.n, wl.d
     esz = 2 if wl.dtype == "bf16" else 4
-    r = refine_steps
+    r, rv = refine_steps, value_refine_steps
     split = 3.0 if wl.dtype == "bf16" else 1.0
     work = {   # stage: (unit, algorithmic amount for all pairs, peak, issued amount or None)
         "rowstats": ("flop", 4.0 * n * T * d * B, PEAK_BF16_TFLOPS, None),
@@ -212,7 +212,7 @@ def stage_rooflines(wl, t, stages, steps, refine_steps=2, bias_mode=0):
         "rhs_B": ("flop", 2.0 * n * t * d * B, PEAK_BF16_TFLOPS, split * 2.0 * n * t * d * B),
         "chol_A": ("flop", t ** 3 / 3.0 * B, PEAK_FP32_TFLOPS, None),
         "solve_values": ("flop", 2.0 * t * t * d * B, PEAK_FP32_TFLOPS,
-                         ((r + 1) * 2.0 * t * t * d + r * 2 * 2.0 * n * t * d) * B),
+                         ((rv + 1) * 2.0 * t * t * d + rv * 2 * 2.0 * n * t * d) * B),
     }
     out = {}
     if bias_mode == 1:
@@ -534,7 +534,8 @@ def main():
         "roofline_score_select": roofline_ss,
         "cpu_baseline": cpu,
         "stage_ms_per_step": {k: round(v[0] / args.steps, 3) for k, v in stages.items() if v[1]},
-        "stage_roofline": stage_rooflines(wl, t, stages, args.steps, params.refine_steps, args.bias_mode),
+        "stage_roofline": stage_rooflines(wl, t, stages, args.steps, params.refine_steps, args.bias_mode,
+                                          params.value_refine_steps),
         "assignment": assign_stats,
         "quality": qual,
     }

@@ -107,11 +107,11 @@ typedef struct {
                           * principal pivoting; other values unsupported */
   int32_t max_escalations; /* ridge x10 retries (from 1e-7 when the ridge is 0) after a failed
                             * Cholesky pivot or a cut-off mass-fit refinement, 0..6; default 6 */
-  int32_t refine_steps;  /* iterative-refinement steps after each Cholesky solve, 0..4; default 2.
-                          * Each step recomputes the residual from the data (Phi_C, P_hat),
-                          * not from the float32 Gram, so the solves converge to the
-                          * least-squares solutions of the exact normal equations.  In the
-                          * mass fit (refine_steps >= 2) a correction (above 1e-10 |w|) that
+  int32_t refine_steps;  /* iterative-refinement steps after each mass-fit Cholesky solve, 0..4;
+                          * default 2.  Each step recomputes the residual from the data
+                          * (Phi_C; P_hat for the value fit), not from the float32 Gram, so
+                          * the solves converge to the least-squares solutions of the exact
+                          * normal equations.  With refine_steps >= 2 a correction (above 1e-10 |w|) that
                           * is not at most half the previous one is undone and ends the
                           * refinement; the pair is then refactored with the ridge raised
                           * tenfold, as after a failed pivot (a ridge small next to the
@@ -123,6 +123,9 @@ typedef struct {
                           * arckv_select_count(T, t, L) anchors; merge and fits stay global. */
   int32_t nnls_max_iter; /* bias_mode 1: pivoting iterations (one masked Cholesky solve each), 1..256;
                           * default 32.  A pair not settled by then reports info = -2. */
+  int32_t value_refine_steps; /* refinement steps after the value-fit solve, 0..4; default 1 (its ridge
+                               * keeps the system well conditioned: one step reaches the float32
+                               * floor of its residual) */
 } arckv_fit_params;
 
 /* Fill *p with the defaults listed above.  Returns ARCKV_ERR_INVALID_ARG on NULL. */

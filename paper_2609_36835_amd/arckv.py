@@ -52,7 +52,8 @@ class FitParams(ctypes.Structure):
                 ("eps_w", ctypes.c_float), ("b_min", ctypes.c_float), ("b_max", ctypes.c_float),
                 ("bias_mode", ctypes.c_int32), ("max_escalations", ctypes.c_int32),
                 ("refine_steps", ctypes.c_int32), ("pair_chunk", ctypes.c_int32),
-                ("select_chunk", ctypes.c_int32), ("nnls_max_iter", ctypes.c_int32)]
+                ("select_chunk", ctypes.c_int32), ("nnls_max_iter", ctypes.c_int32),
+                ("value_refine_steps", ctypes.c_int32)]
 
 
 class DSAIndexer(ctypes.Structure):

@@ -360,6 +360,7 @@ static arckv_status check_params(const arckv_fit_params *p) {
   if (p->nnls_max_iter < 1 || p->nnls_max_iter > 256) return ARCKV_ERR_INVALID_ARG;
   if (p->max_escalations < 0 || p->max_escalations > 6) return ARCKV_ERR_INVALID_ARG;
   if (p->refine_steps < 0 || p->refine_steps > 4) return ARCKV_ERR_INVALID_ARG;
+  if (p->value_refine_steps < 0 || p->value_refine_steps > 4) return ARCKV_ERR_INVALID_ARG;
   if (p->pair_chunk < 0) return ARCKV_ERR_INVALID_ARG;
   if (p->select_chunk < 0) return ARCKV_ERR_INVALID_ARG;
   return ARCKV_OK;
@@ -535,7 +536,7 @@ static arckv_status run_fit_values_chunk(const Ctx &c, int b0, int P, const floa
     return ARCKV_ERR_HIP;
   // P^T for the Gram and right-hand side, and P (query-major) for the refinement residuals
   STAGE(ST_PHAT, launch_phat(d.dtype, LT, c.pers<float>(c.pl.beta_ws) + (size_t)b0 * d.tp, P, d.n, d.t, d.tp,
-                             d.np_, PT, fp.refine_steps > 0 ? Pm : nullptr, stream));
+                             d.np_, PT, fp.value_refine_steps > 0 ? Pm : nullptr, stream));
   STAGE(ST_GRAM_A, launch_gram(d.dtype, PT, Gw, Gc, P, d.tp, d.np_, stream));
   {
     StageScope _sc(ST_RHS, stream);
@@ -551,7 +552,7 @@ static arckv_status run_fit_values_chunk(const Ctx &c, int b0, int P, const floa
     if (launch_trsm(true, Gw, dinv, P, d.tp, Bm, Y2, st.info, stream) != hipSuccess) return ARCKV_ERR_HIP;
     if (launch_trsm(false, Gw, dinv, P, d.tp, Y2, X, st.info, stream) != hipSuccess) return ARCKV_ERR_HIP;
     // refinement against the data: R = P^T (Y - P X) - lam X
-    for (int it = 0; it < fp.refine_steps; ++it) {
+    for (int it = 0; it < fp.value_refine_steps; ++it) {
       if (launch_transpose128(d.dtype, X, P, (int)d.tp, d.tp * kHeadDimH, d.tp, XT, pl * d.tp * kHeadDimH, stream) !=
           hipSuccess)
         return ARCKV_ERR_HIP;
@@ -585,6 +586,7 @@ arckv_status arckv_default_params(arckv_fit_params *p) {
   p->bias_mode = 0;
   p->max_escalations = 6;
   p->refine_steps = 2;
+  p->value_refine_steps = 1;
   p->pair_chunk = 0;
   p->select_chunk = 0;
   p->nnls_max_iter = 32;

@@ -81,6 +81,8 @@ int main() {
   EXPECT(arckv_workspace_size(&prob, 102, &p2, &b1), ARCKV_ERR_INVALID_ARG);
   p2 = par; p2.refine_steps = 5;
   EXPECT(arckv_workspace_size(&prob, 102, &p2, &b1), ARCKV_ERR_INVALID_ARG);
+  p2 = par; p2.value_refine_steps = -1;
+  EXPECT(arckv_workspace_size(&prob, 102, &p2, &b1), ARCKV_ERR_INVALID_ARG);
   p2 = par; p2.delta_v = NAN;
   EXPECT(arckv_workspace_size(&prob, 102, &p2, &b1), ARCKV_ERR_INVALID_ARG);
 

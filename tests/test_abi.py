@@ -56,7 +56,8 @@ def test_default_params():
     p = A.default_params()
     assert p.lambda_m == pytest.approx(0.25) and p.delta_beta == pytest.approx(1e-6)
     assert p.delta_v == pytest.approx(1e-3) and p.eps_w == pytest.approx(1e-12)
-    assert (p.b_min, p.b_max, p.bias_mode, p.max_escalations, p.refine_steps) == (-30.0, 30.0, 0, 6, 2)
+    assert (p.b_min, p.b_max, p.bias_mode, p.max_escalations, p.refine_steps, p.value_refine_steps) == \
+        (-30.0, 30.0, 0, 6, 2, 1)
     assert (p.pair_chunk, p.select_chunk, p.nnls_max_iter) == (0, 0, 32)
 
 
@@ -93,7 +94,8 @@ def test_workspace_validation_and_monotonicity():
     ("bias_mode", 2, A.ERR_UNSUPPORTED), ("bias_mode", -1, A.ERR_UNSUPPORTED),
     ("nnls_max_iter", 0, A.ERR_INVALID_ARG), ("nnls_max_iter", 257, A.ERR_INVALID_ARG),
     ("max_escalations", 7, A.ERR_INVALID_ARG),
-    ("refine_steps", -1, A.ERR_INVALID_ARG), ("pair_chunk", -2, A.ERR_INVALID_ARG),
+    ("refine_steps", -1, A.ERR_INVALID_ARG), ("value_refine_steps", 5, A.ERR_INVALID_ARG),
+    ("pair_chunk", -2, A.ERR_INVALID_ARG),
 ])
 def test_param_validation(field, value, code):
     p = A.problem_from_dims(2, 1024, 256)
