@@ -204,66 +204,101 @@ __global__ void __launch_bounds__(256) k_nonfinite(const float *__restrict__ a, 
   if (__any(any) && (threadIdx.x & 63) == 0) atomicOr(&bad[b], 1);
 }
 
-// --------------------------------------------------------------- 64x64 building blocks
-// Inverse of a factored 64 x 64 lower-triangular block whose row `lane` is
-// held in a[] by lane `lane` of the wave; rdiag[r] = 1 / L[r][r].  Forward
-// substitution column-per-lane, x[r] = (e_r - sum_{q<r} L[r][q] x[q]) L[r][r]^-1
-// with L[r][q] broadcast from lane r; the upper triangle comes out zero.  Row
-// r of the inverse is written to Xi[r][0..63].
-__device__ __forceinline__ void tri_inverse_64(const float (&a)[kNB], const float (&rdiag)[kNB], int lane,
-                                               float *__restrict__ Xi) {
-  auto bcast = [](float v, int src) { return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), src)); };
-  float x[kNB];
-#pragma unroll
-  for (int r = 0; r < kNB; ++r) {
-    float acc = r == lane ? 1.0f : 0.0f;
-#pragma unroll
-    for (int q = 0; q < r; ++q) acc = fmaf(-bcast(a[q], r), x[q], acc);
-    x[r] = acc * rdiag[r];
-  }
-#pragma unroll
-  for (int r = 0; r < kNB; ++r) Xi[r * kNB + lane] = x[r];
-}
-
 // Factor the 64 x 64 diagonal block k in place and write L_kk^-1 to
-// dinv[b][k] (one wave per pair).  Lane r keeps row r of the block in
-// registers; the pivot and the finished column entries are broadcast with
-// readlane, so the 64 column steps need no LDS traffic or barriers.
-// Right-looking: after column c is scaled, a[s] -= L[r][c] L[s][c] for s > c
-// (entries above the diagonal are updated too and ignored).
-__global__ void __launch_bounds__(64) k_chol_diag(float *__restrict__ Gw, int64_t ld, int k,
-                                                  int32_t *__restrict__ info, float *__restrict__ dinv) {
-  const int b = blockIdx.x, lane = threadIdx.x;
-  if (info[b] != 0) return;
+// dinv[b][k] (one workgroup of 256 threads per pair).  Thread (r, cls) with
+// r = tid / 4, cls = tid % 4 keeps A[r][4j + cls] (j < 16) in registers.
+// Right-looking over the 64 columns c with one barrier per column: column c,
+// updated through column c - 1 but not yet scaled, sits in LDS (its owners
+// publish it right after their own update of step c - 1), so every thread
+// reads the pivot, takes d = sqrt and 1 / d itself, scales the entries it
+// needs, L[x][c] = A'[x][c] / d, and subtracts L[r][c] L[q][c] from its
+// entries.  The inverse X = L^-1 is an elimination on the identity in the
+// same loop: row c of X is row c of the updated identity times 1 / d,
+// published at step c, and rows below subtract L[r][c] X[c][q] one step
+// later, when that row is visible.  Both recurrences accumulate in column
+// order with the same products and fused multiply-adds as a plain
+// column-by-column factorisation and row-by-row substitution.  A failed pivot
+// records info = column + 1 and leaves the block and dinv unwritten.
+__global__ void __launch_bounds__(256) k_chol_diag(float *__restrict__ Gw, int64_t ld, int k,
+                                                   int32_t *__restrict__ info, float *__restrict__ dinv) {
+  __shared__ float sA[kNB * kSD];   // column c: A updated through column c - 1, unscaled
+  __shared__ float sX[kNB * kSD];   // L^-1, one row per column step
+  __shared__ float sd[kNB], sdg[kNB];   // 1 / L[c][c] and L[c][c]
+  const int b = blockIdx.x, tid = threadIdx.x;
+  if (info[b] != 0) return;   // uniform over the workgroup
+  const int r = tid >> 2, cls = tid & 3;
   float *D = Gw + (size_t)b * ld * ld + (size_t)k * kNB * ld + (size_t)k * kNB;
-  float a[kNB];
+  for (int e = tid; e < kNB * kNB / 4; e += 256) {
+    const int rr = e >> 4, c4 = (e & 15) * 4;
+    const f32x4 v = *reinterpret_cast<const f32x4 *>(D + (size_t)rr * ld + c4);
 #pragma unroll
-  for (int s4 = 0; s4 < kNB / 4; ++s4) {
-    const f32x4 v = *reinterpret_cast<const f32x4 *>(D + (size_t)lane * ld + 4 * s4);
-    a[4 * s4] = v[0];
-    a[4 * s4 + 1] = v[1];
-    a[4 * s4 + 2] = v[2];
-    a[4 * s4 + 3] = v[3];
+    for (int q = 0; q < 4; ++q) sA[rr * kSD + c4 + q] = v[q];
   }
-  auto bcast = [](float v, int src) { return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), src)); };
-  float rdiag[kNB];
+  __syncthreads();
+  // Each thread reads only its own entries, and column 0 needs no update.
+  float a[16], y[16];
 #pragma unroll
+  for (int j = 0; j < 16; ++j) {
+    const int q = 4 * j + cls;
+    a[j] = sA[r * kSD + q];
+    y[j] = q == r ? 1.0f : 0.0f;
+  }
+  int fail = 0;
+  float plrc = 0.0f;   // L[r][c - 1]
+#pragma unroll 1
   for (int c = 0; c < kNB; ++c) {
-    const float piv = bcast(a[c], c);
-    if (!(piv > 0.0f) || !isfinite(piv)) {
-      if (lane == 0) info[b] = k * kNB + c + 1;
-      return;
+    const float piv = sA[c * kSD + c];
+    const float arc = sA[r * kSD + c];
+    float col[16], xp[16];
+#pragma unroll
+    for (int j = 0; j < 16; ++j) col[j] = sA[(4 * j + cls) * kSD + c];
+    if (c > 0) {
+#pragma unroll
+      for (int j = 0; j < 16; ++j) xp[j] = sX[(c - 1) * kSD + 4 * j + cls];
+    }
+    if (!(piv > 0.0f) || !isfinite(piv)) {   // uniform: every thread read the same pivot
+      fail = c + 1;
+      break;
     }
     const float d = sqrtf(piv), inv = 1.0f / d;
-    rdiag[c] = inv;
-    a[c] = lane == c ? d : (lane > c ? a[c] * inv : a[c]);
+    if (c > 0 && r >= c) {
 #pragma unroll
-    for (int s2 = c + 1; s2 < kNB; ++s2) a[s2] = fmaf(-a[c], bcast(a[c], s2), a[s2]);
+      for (int j = 0; j < 16; ++j) y[j] = fmaf(-plrc, xp[j], y[j]);
+    }
+    if (r == c) {
+#pragma unroll
+      for (int j = 0; j < 16; ++j) sX[c * kSD + 4 * j + cls] = y[j] * inv;
+    }
+    const float lrc = arc * inv;
+    if (r > c) {
+#pragma unroll
+      for (int j = 0; j < 16; ++j) a[j] = fmaf(-lrc, col[j] * inv, a[j]);
+    }
+    plrc = lrc;
+    if (c + 1 < kNB && cls == ((c + 1) & 3)) {
+      const int jn = (c + 1) >> 2;
+      float v = a[0];
+#pragma unroll
+      for (int j = 1; j < 16; ++j) v = j == jn ? a[j] : v;
+      sA[r * kSD + c + 1] = v;
+    }
+    if (tid == 0) {
+      sd[c] = inv;
+      sdg[c] = d;
+    }
+    __syncthreads();
   }
-#pragma unroll
-  for (int s2 = 0; s2 < kNB; ++s2)
-    if (s2 <= lane) D[(size_t)lane * ld + s2] = a[s2];
-  tri_inverse_64(a, rdiag, lane, dinv + ((size_t)b * (ld / kNB) + k) * kNB * kNB);
+  if (fail) {
+    if (tid == 0) info[b] = k * kNB + fail;
+    return;
+  }
+  float *Xi = dinv + ((size_t)b * (ld / kNB) + k) * kNB * kNB;
+  for (int e = tid; e < kNB * kNB; e += 256) {
+    const int rr = e >> 6, q = e & 63;
+    if (q < rr) D[(size_t)rr * ld + q] = sA[rr * kSD + q] * sd[q];
+    else if (q == rr) D[(size_t)rr * ld + q] = sdg[q];
+    Xi[e] = sX[rr * kSD + q];
+  }
 }
 
 // Panel: L_ik = A_ik L_kk^-T for the rows below diagonal block k, as an fp32
@@ -1321,7 +1356,7 @@ hipError_t launch_cholesky_factor(float *Gw, const float *Gc, int B, int t, int6
     const int K1 = (int)(K0 + kOuter < ld ? K0 + kOuter : ld);
     for (int c = K0; c < K1; c += kNB) {
       const int k = c / kNB;
-      hipLaunchKernelGGL(k_chol_diag, dim3(B), dim3(64), 0, s, Gw, ld, k, st.info, dinv);
+      hipLaunchKernelGGL(k_chol_diag, dim3(B), dim3(256), 0, s, Gw, ld, k, st.info, dinv);
       const int rem = nrb - k - 1;
       if (rem > 0)
         hipLaunchKernelGGL(k_chol_panel, dim3((rem + 1) / 2, B), dim3(256), 0, s, Gw, ld, k, dinv, st.info);
