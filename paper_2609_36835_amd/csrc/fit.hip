@@ -888,77 +888,6 @@ __global__ void __launch_bounds__(256) k_transpose128(const float *__restrict__ 
 }
 
 // --------------------------------------------------------------- 128 right-hand sides
-// Forward (L X = R) or backward (L^T X = R) substitution for 64 of the 128
-// columns per workgroup, float32, 32-row blocks.  X may alias nothing.
-template <bool FWD>
-__global__ void __launch_bounds__(256) k_trsm(const float *__restrict__ Gw, int64_t ld,
-                                              const float *__restrict__ R, float *__restrict__ X,
-                                              const int32_t *__restrict__ info) {
-  constexpr int RB = 32;
-  __shared__ float sL[RB][RB + 1];
-  __shared__ float sY[RB][64 + 1];
-  const int b = blockIdx.y, tid = threadIdx.x;
-  if (info[b] != 0) return;
-  const int c = tid & 63, g = tid >> 6, c0 = blockIdx.x * 64;
-  const float *L = Gw + (size_t)b * ld * ld;
-  const float *Rb = R + (size_t)b * ld * kHeadDim;
-  float *Xb = X + (size_t)b * ld * kHeadDim;
-  const int nb = (int)(ld / RB);
-  for (int step = 0; step < nb; ++step) {
-    const int kb = FWD ? step : nb - 1 - step;
-    const int r0 = kb * RB;
-    float acc[8];
-    #pragma unroll
-    for (int e = 0; e < 8; ++e) acc[e] = Rb[(size_t)(r0 + 8 * g + e) * kHeadDim + c0 + c];
-    const int p_beg = FWD ? 0 : r0 + RB, p_end = FWD ? r0 : (int)ld;
-    for (int p0 = p_beg; p0 < p_end; p0 += RB) {
-      __syncthreads();
-      for (int e = tid; e < RB * RB; e += 256) {
-        const int rr = e / RB, pp = e % RB;
-        // FWD: sL[rr][pp] = L[r0+rr][p0+pp];  BWD: sL[rr][pp] = L[p0+pp][r0+rr]
-        sL[rr][pp] = FWD ? L[(size_t)(r0 + rr) * ld + p0 + pp] : L[(size_t)(p0 + pp) * ld + r0 + rr];
-      }
-      for (int e = tid; e < RB * 64; e += 256) {
-        const int pp = e / 64, cc = e % 64;
-        sY[pp][cc] = Xb[(size_t)(p0 + pp) * kHeadDim + c0 + cc];
-      }
-      __syncthreads();
-      for (int pp = 0; pp < RB; ++pp) {
-        const float yv = sY[pp][c];
-        #pragma unroll
-        for (int e = 0; e < 8; ++e) acc[e] -= sL[8 * g + e][pp] * yv;
-      }
-    }
-    __syncthreads();
-    for (int e = tid; e < RB * RB; e += 256) {
-      const int rr = e / RB, pp = e % RB;
-      sL[rr][pp] = L[(size_t)(r0 + rr) * ld + r0 + pp];
-    }
-    #pragma unroll
-    for (int e = 0; e < 8; ++e) sY[8 * g + e][c] = acc[e];
-    __syncthreads();
-    if (g == 0) {
-      if (FWD) {
-        for (int rr = 0; rr < RB; ++rr) {
-          float v = sY[rr][c];
-          for (int q = 0; q < rr; ++q) v -= sL[rr][q] * sY[q][c];
-          sY[rr][c] = v / sL[rr][rr];
-        }
-      } else {
-        for (int rr = RB - 1; rr >= 0; --rr) {
-          float v = sY[rr][c];
-          for (int q = rr + 1; q < RB; ++q) v -= sL[q][rr] * sY[q][c];
-          sY[rr][c] = v / sL[rr][rr];
-        }
-      }
-    }
-    __syncthreads();
-    #pragma unroll
-    for (int e = 0; e < 8; ++e) Xb[(size_t)(r0 + 8 * g + e) * kHeadDim + c0 + c] = sY[8 * g + e][c];
-    __threadfence_block();
-  }
-}
-
 // 128-rhs triangular solve on fp32 MFMA: L X = R (forward) or L^T X = R
 // (backward), two workgroups per pair with 64 columns each, 64-row blocks.
 // For block kb the update  acc = sum_p L_kb,p X_p  (forward) or
