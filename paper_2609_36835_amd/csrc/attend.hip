@@ -193,11 +193,15 @@ __global__ void __launch_bounds__(1024) k_attend_combine(int G, const float *__r
   if (idx >= G * kHeadDim) return;
   const int q = idx / kHeadDim, dim = idx % kHeadDim;
   const float *ml = part_ml + (size_t)p * nch * G * 2;
+  // Both sweeps are unrolled so that eight chunks' loads are in flight at once
+  // (one dependent load per chunk left the long contexts latency-bound).
   float M = -INFINITY;
+#pragma unroll 8
   for (int c = 0; c < nch; ++c) M = fmaxf(M, ml[((size_t)c * G + q) * 2]);
   const float Mref = M == -INFINITY ? 0.0f : M;
   float acc = 0.0f, lsum = 0.0f;
   const float *po = part_o + (size_t)p * nch * G * kHeadDim;
+#pragma unroll 8
   for (int c = 0; c < nch; ++c) {
     const float mc = ml[((size_t)c * G + q) * 2];
     const float f = mc == -INFINITY ? 0.0f : __expf(mc - Mref);
