@@ -426,13 +426,23 @@ __global__ void __launch_bounds__(256) k_assign_finalize(
   atomicAdd(&st[6], 1);
 }
 
+// Workgroup barrier that waits for this wave's LDS operations only: global
+// loads issued before it stay in flight across it.
+__device__ __forceinline__ void lds_only_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0); vmcnt and expcnt unconstrained
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
 // ---------------------------------------------------------------- pass C
-// Refine the keys queued by pass A.  A workgroup takes 64 queued keys of one
-// pair and their candidates from the pool, in chunks of CAP.  The keys'
-// profiles are formed in fp32 and each candidate pair accumulates
-// sum_i e_ij e_ir (fp32 products summed four at a time, then in float64)
-// against the anchor's stored profile; the similarity e_j . e_r / ||e_r|| goes
-// back to the pool.
+// Refine the keys queued by pass A.  The queued keys of a pair form groups of
+// 64 (in queue order) and a group's candidates in the pool form chunks of CAP;
+// each (group, chunk) is one work item.  The keys' profiles are formed in
+// fp32 and each candidate pair accumulates sum_i e_ij e_ir (fp32 products
+// summed four at a time, then in float64) against the anchor's stored
+// profile; the similarity e_j . e_r / ||e_r|| goes back to the pool, and
+// k_assign_decide takes the decisions once every item is done.
 //  bf16 inputs: logits from eight MFMA slices as in k_prof_anchor_bf16
 //   (kSliceTerms), exponentials within exp32_err.  Bound of one similarity:
 //   (1 + eps_k)(1 + eps_a)/(1 - eps_a)(1 + gamma_4) - 1 with eps_k = gamma_23 s
@@ -441,33 +451,33 @@ __global__ void __launch_bounds__(256) k_assign_finalize(
 //   rounding of the two profiles and of the partial products.
 // A key whose best similarity exceeds every other candidate's by more than the
 // bound on both is decided; the survivors of the others go to pass D.
-// Work distribution: a fixed grid of kRefineBlocks workgroups per pair, each
-// taking the groups of 64 queued keys g = blockIdx.x, blockIdx.x + kRefineBlocks,
-// ...  The queries are swept in tiles of 128.  Per tile the eight waves form the
-// 64 keys' profiles (one 32 x 32 MFMA tile each: a key half by a quarter of the
-// queries, skipped when none of the chunk's candidates belongs to that half)
-// into a shared LDS tile; each wave takes 32 candidates, two per load
-// instruction: a half-wave covers one candidate's 128 queries, four per lane,
-// so every load reads two contiguous 512-byte runs of anchor profile rows.  A
-// tile's anchor-profile loads are issued before its profile phase.  The
-// candidates' partial sums stay in registers (float64) across the tiles and are
-// reduced over the half-waves once per chunk.
-constexpr int kRefineBlocks = 32;
+// Work distribution: k_refine_plan lays out each pair's items (goff); a fixed
+// grid of kRefineBlocks workgroups per pair takes items it = blockIdx.x,
+// blockIdx.x + kRefineBlocks, ..., so the chunks of one group with many
+// candidates (keys whose candidates include whole anchor tiles) spread over
+// workgroups instead of running in sequence on one.  The queries are swept in
+// tiles of 128.  Per tile the eight waves form the 64 keys' profiles (one
+// 32 x 32 MFMA tile each: a key half by a quarter of the queries) into a
+// shared LDS tile; each wave takes 32 candidates, two per load instruction: a
+// half-wave covers one candidate's 128 queries, four per lane, so every load
+// reads two contiguous 512-byte runs of anchor profile rows.  The candidates'
+// partial sums stay in registers (float64) across the tiles and are reduced
+// over the half-waves once per item.
+constexpr int kRefineBlocks = 128;
+constexpr int kRefineCpw = 32;   // candidates per wave
 
 template <typename E>
 __global__ void __launch_bounds__(512, 2) k_assign_refine(const E *__restrict__ Q, const E *__restrict__ K,
                                                        const float *__restrict__ zmerge,
-                                                       const AssignPair *__restrict__ pn,
                                                        const float *__restrict__ Ua, const double *__restrict__ anorm,
-                                                       int T, int t, int n, int64_t tp, int64_t np_, double s,
-                                                       int32_t *__restrict__ kappa, AssignLists L) {
+                                                       int T, int n, int64_t tp, int64_t np_, double s,
+                                                       AssignLists L) {
   constexpr bool BF = sizeof(E) == 2;
-  constexpr int NK = 64, NW = 8, CPW = 32, CAP = NW * CPW, QT = 128, SE = QT + 4;
+  constexpr int NK = 64, NW = 8, CPW = kRefineCpw, CAP = NW * CPW, QT = 128, SE = QT + 4;
   constexpr int SKB = BF ? kHeadDim + 8 : kHeadDim + 4;   // key-row stride (elements)
-  __shared__ int32_t kpos[NK], koff[NK], kbase[NK + 1], khalf;
+  __shared__ int32_t kpos[NK], koff[NK], kbase[NK + 1], khalf, item_g, item_c0;
   __shared__ int32_t cr[CAP];
   __shared__ int32_t ck[CAP];
-  __shared__ double kn[NK];
   __shared__ __attribute__((aligned(16))) E sK[NK * SKB];
   __shared__ __attribute__((aligned(16))) float eS[NK * SE];   // the keys' profiles on one query tile
   // pair-major over the whole grid (no XCD remap): the anchor profiles do not
@@ -476,7 +486,6 @@ __global__ void __launch_bounds__(512, 2) k_assign_refine(const E *__restrict__ 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int h = lane >> 5, col = lane & 31;
   const int F = L.fcnt[b];
-  const AssignPair pp = pn[b];
   const double zm = (double)zmerge[b];
   const float c2 = (float)(s * 1.4426950408889634), zs2 = zmerge[b] * 1.4426950408889634f;
   const E *Qb = Q + (size_t)b * n * kHeadDim;
@@ -484,35 +493,53 @@ __global__ void __launch_bounds__(512, 2) k_assign_refine(const E *__restrict__ 
   int32_t *pool = L.pool + (size_t)b * L.pcap;
   double *psim = L.psim + (size_t)b * L.pcap;
   const int kt = wave >> 2, qsub = wave & 3;   // this wave's key half and query quarter in the profile phase
-  for (int f0 = bx * NK; f0 < F; f0 += kRefineBlocks * NK) {   // uniform over the workgroup
-    const int nk = min(NK, F - f0);
-    __syncthreads();   // the previous group is done with the shared arrays
-    if (tid < NK) {
-      kpos[tid] = -1;
-      koff[tid] = 0;
-      if (tid < nk) {
-        const size_t q = (size_t)b * L.cap + f0 + tid;
-        kpos[tid] = L.fkey[q];
-        koff[tid] = L.foff[q];
-        kn[tid] = row_norm(K + ((size_t)b * T + kpos[tid]) * kHeadDim);
+  const int G = (F + NK - 1) / NK;
+  const int32_t *goff = L.goff + (size_t)b * L.gcap;
+  const int items = F > 0 ? goff[G] : 0;
+  int cur = -1;   // the group whose keys are in the shared arrays
+  for (int it = bx; it < items; it += kRefineBlocks) {   // uniform over the workgroup
+    __syncthreads();   // the previous item is done with the shared arrays
+    if (tid == 0) {   // the group g with goff[g] <= it < goff[g + 1]
+      int lo = 0, hi = G;
+      while (hi - lo > 1) {
+        const int mid = (lo + hi) >> 1;
+        if (goff[mid] <= it) lo = mid;
+        else hi = mid;
       }
+      item_g = lo;
+      item_c0 = (it - goff[lo]) * CAP;
     }
     __syncthreads();
-    if (tid == 0) {
-      int acc = 0;
-      for (int k = 0; k < NK; ++k) {
-        kbase[k] = acc;
-        acc += k < nk ? L.fn[(size_t)b * L.cap + f0 + k] : 0;
+    const int g = item_g, c0 = item_c0;
+    if (g != cur) {   // load the group's keys (uniform)
+      cur = g;
+      const int f0 = g * NK, nk = min(NK, F - f0);
+      if (tid < NK) {
+        kpos[tid] = -1;
+        koff[tid] = 0;
+        if (tid < nk) {
+          const size_t q = (size_t)b * L.cap + f0 + tid;
+          kpos[tid] = L.fkey[q];
+          koff[tid] = L.foff[q];
+        }
       }
-      kbase[NK] = acc;
+      __syncthreads();
+      if (tid == 0) {
+        int acc = 0;
+        for (int k = 0; k < NK; ++k) {
+          kbase[k] = acc;
+          acc += k < nk ? L.fn[(size_t)b * L.cap + f0 + k] : 0;
+        }
+        kbase[NK] = acc;
+      }
+      for (int x = tid; x < NK * kHeadDim; x += NW * 64) {   // the keys' rows (zero for empty slots)
+        const int k = x / kHeadDim, c = x % kHeadDim;
+        sK[k * SKB + c] = kpos[k] >= 0 ? K[((size_t)b * T + kpos[k]) * kHeadDim + c] : (E)0.0f;
+      }
+      __syncthreads();
     }
-    for (int x = tid; x < NK * kHeadDim; x += NW * 64) {   // the keys' rows (zero for empty slots)
-      const int k = x / kHeadDim, c = x % kHeadDim;
-      sK[k * SKB + c] = kpos[k] >= 0 ? K[((size_t)b * T + kpos[k]) * kHeadDim + c] : (E)0.0f;
-    }
-    __syncthreads();
     const int total = kbase[NK];
-    for (int c0 = 0; c0 < total; c0 += CAP) {
+    {
       const int cn = min(CAP, total - c0);
       __syncthreads();   // the previous chunk is done with cr / ck / khalf
       if (tid == 0) khalf = 0;
@@ -520,15 +547,15 @@ __global__ void __launch_bounds__(512, 2) k_assign_refine(const E *__restrict__ 
       for (int c = tid; c < CAP; c += NW * 64) {
         int lo = -1, r = 0;
         if (c < cn) {
-          const int g = c0 + c;
-          int lo2 = 0, hi = NK;   // the key k with kbase[k] <= g < kbase[k + 1]
+          const int gi = c0 + c;
+          int lo2 = 0, hi = NK;   // the key k with kbase[k] <= gi < kbase[k + 1]
           while (hi - lo2 > 1) {
             const int mid = (lo2 + hi) >> 1;
-            if (kbase[mid] <= g) lo2 = mid;
+            if (kbase[mid] <= gi) lo2 = mid;
             else hi = mid;
           }
           lo = lo2;
-          r = pool[koff[lo] + g - kbase[lo]];
+          r = pool[koff[lo] + gi - kbase[lo]];
           atomicOr(&khalf, 1 << (lo >> 5));   // which 32-key halves this chunk's candidates belong to
         }
         ck[c] = lo;
@@ -541,29 +568,62 @@ __global__ void __launch_bounds__(512, 2) k_assign_refine(const E *__restrict__ 
       for (int u = 0; u < CPW / 2; ++u) acc[u] = 0.0;
       const int cw0 = wave * CPW;   // this wave's candidates cw0 + 2u + h
       const int qo = 4 * col;        // half-wave lane col covers queries i0 + 4 col .. + 3
-      for (int i0 = 0; i0 < n; i0 += QT) {
-        // ---- this tile's anchor-profile values, loaded first so that their
-        // latency overlaps the profile phase (they do not depend on it)
-        f32x4 w[CPW / 2];
-#pragma unroll
-        for (int u = 0; u < CPW / 2; ++u) {
-          const int c = cw0 + 2 * u + h;
-          w[u] = ck[c] >= 0 ? *reinterpret_cast<const f32x4 *>(Uab + (size_t)cr[c] * np_ + i0 + qo)
-                            : f32x4{0.f, 0.f, 0.f, 0.f};
-        }
-        // ---- the 64 keys' profiles on queries [i0, i0 + 128)
-        if ((need >> kt) & 1) {
+      const bool prof = (need >> kt) & 1;   // this wave forms profiles in this chunk
+      // Loads are unconditional so that the compiler can count them exactly
+      // across the tile loop (a load under a branch may not have been issued,
+      // which forces a full drain at the next use): an empty candidate slot
+      // holds anchor 0 and is skipped when used; query rows past n are
+      // clamped, and their profiles are zeroed below.
+      auto load_w = [&](int i0, int u) -> f32x4 {
+        const int c = cw0 + 2 * u + h;
+        return *reinterpret_cast<const f32x4 *>(Uab + (size_t)cr[c] * np_ + i0 + qo);
+      };
+      // bf16 inputs: the loads run one query tile ahead.  The query fragments
+      // of tile i0 + 128 are issued as soon as the MFMAs of tile i0 have read
+      // theirs, and each anchor-profile value of tile i0 + 128 as soon as its
+      // tile-i0 value is used; the tile barriers wait for LDS only.  Vector
+      // loads complete in issue order, so the profile phase waits for its
+      // query fragments alone while the anchor values stay in flight.
+      // fp32 inputs: one tile at a time.
+      bf16x8 qa[BF ? 8 : 1];
+      auto load_q = [&](int i0) {
+        if constexpr (BF) {
           const int iq = i0 + 32 * qsub + col;   // this lane's query row of the MFMA A operand
+          const bf16 *qrow = reinterpret_cast<const bf16 *>(Qb) + (size_t)(iq < n ? iq : n - 1) * kHeadDim + 8 * h;
+#pragma unroll
+          for (int ks = 0; ks < 8; ++ks) qa[ks] = *reinterpret_cast<const bf16x8 *>(qrow + ks * 16);
+        }
+      };
+      auto tile_barrier = [&]() {
+        if constexpr (BF) lds_only_barrier();
+        else __syncthreads();
+      };
+      f32x4 w[CPW / 2];
+      if constexpr (BF) {
+        load_q(0);
+        // the same issue order as at the end of each tile (query fragments,
+        // then anchor values), so that the counts agree at the loop head
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int u = 0; u < CPW / 2; ++u) w[u] = load_w(0, u);
+      }
+      for (int i0 = 0; i0 < n; i0 += QT) {
+        const int nxt = i0 + QT < n ? i0 + QT : i0;   // the last tile reloads itself
+        if constexpr (!BF) {
+#pragma unroll
+          for (int u = 0; u < CPW / 2; ++u) w[u] = load_w(i0, u);
+        }
+        // ---- the 64 keys' profiles on queries [i0, i0 + 128) (bf16: always, so
+        // that no load or MFMA of the tile loop sits under a branch)
+        if (BF || prof) {
           double l[BF ? 1 : 16];
           f32x16 lsum;
           if constexpr (BF) {
-            const bf16 *qrow = reinterpret_cast<const bf16 *>(Qb) + (size_t)(iq < n ? iq : 0) * kHeadDim + 8 * h;
             const bf16 *krow = reinterpret_cast<const bf16 *>(sK) + (kt * 32 + col) * SKB + 8 * h;
-#pragma unroll 2
+#pragma unroll
             for (int ks = 0; ks < 8; ++ks) {
-              const bf16x8 a = iq < n ? *reinterpret_cast<const bf16x8 *>(qrow + ks * 16) : Mfma<bf16>::zero();
               const bf16x8 bk = *reinterpret_cast<const bf16x8 *>(krow + ks * 16);
-              const f32x16 part = Mfma<bf16>::mma(a, bk, zero16());
+              const f32x16 part = Mfma<bf16>::mma(qa[ks], bk, zero16());
               if (ks == 0) lsum = part;
               else {
 #pragma unroll
@@ -599,20 +659,21 @@ __global__ void __launch_bounds__(512, 2) k_assign_refine(const E *__restrict__ 
             eS[(kt * 32 + col) * SE + qi] = ev;
           }
         }
-        __syncthreads();   // the tile's profiles are complete
-        // ---- 32 candidates per wave: half-wave h takes candidate cw0 + 2u + h
+        if constexpr (BF) load_q(nxt);   // the MFMAs above have read qa
+        tile_barrier();   // the tile's profiles are complete
+        // ---- CPW candidates per wave: half-wave h takes candidate cw0 + 2u + h
+        // Branch-free: an empty slot reads key 0's profile and adds an exact zero.
 #pragma unroll
         for (int u = 0; u < CPW / 2; ++u) {
           const int k = ck[cw0 + 2 * u + h];
-          if (k >= 0) {
-            const f32x4 e4 = *reinterpret_cast<const f32x4 *>(&eS[k * SE + qo]);
-            float p4 = e4[0] * w[u][0];   // four non-negative products in fp32 (within gamma_4), then float64
+          const f32x4 e4 = *reinterpret_cast<const f32x4 *>(&eS[(k >= 0 ? k : 0) * SE + qo]);
+          float p4 = e4[0] * w[u][0];   // four non-negative products in fp32 (within gamma_4), then float64
 #pragma unroll
-            for (int e = 1; e < 4; ++e) p4 = fmaf(e4[e], w[u][e], p4);
-            acc[u] += (double)p4;
-          }
+          for (int e = 1; e < 4; ++e) p4 = fmaf(e4[e], w[u][e], p4);
+          acc[u] += k >= 0 ? (double)p4 : 0.0;
+          if constexpr (BF) w[u] = load_w(nxt, u);
         }
-        __syncthreads();   // reads of the tile done before the next one overwrites it
+        tile_barrier();   // reads of the tile done before the next one overwrites it
       }
       // ---- reduce each candidate's partial sums over its half-wave
 #pragma unroll
@@ -627,32 +688,88 @@ __global__ void __launch_bounds__(512, 2) k_assign_refine(const E *__restrict__ 
         }
       }
     }
-    __syncthreads();   // every similarity of the group's keys is in the pool
-    if (tid < nk && kbase[tid + 1] > kbase[tid]) {
-      const int j = kpos[tid], o = koff[tid], m = kbase[tid + 1] - kbase[tid];
-      int best = 0;
-      for (int c = 1; c < m; ++c)
-        if (psim[o + c] > psim[o + best] || (psim[o + c] == psim[o + best] && pool[o + c] < pool[o + best]))
-          best = c;
-      double eta;
-      if constexpr (BF) {
-        const double g = gamma_m(kSliceTerms) * s * pp.qmax, Z = fabs(zm) * 1.4426950408889634;
-        const double ek = g * kn[tid] + exp32_err(s * pp.qmax * kn[tid] * 1.4426950408889634 * 1.001, Z);
-        const double ea = g * pp.amax + exp32_err(s * pp.qmax * pp.amax * 1.4426950408889634 * 1.001, Z);
-        eta = (1.0 + ek) * (1.0 + ea) / (1.0 - ea) * (1.0 + gamma_m(4)) * (1.0 + 1e-12) - 1.0;
-      } else {
-        eta = 3.0 * kU32 + gamma_m(4) + 1e-12;
-      }
-      const double bs = psim[o + best];
-      const double thc = bs * (1.0 - eta) / (1.0 + eta) - 1e-300;
-      kappa[(size_t)b * T + j] = pool[o + best];
-      // the survivors are compacted in place at the front of the key's pool
-      // segment (this thread alone reads and writes it; writes trail reads)
-      int ns = 0;
-      for (int c = 0; c < m; ++c)
-        if (psim[o + c] >= thc) pool[o + ns++] = pool[o + c];
-      if (ns > 1) push_d(L, b, j, o, ns);
+  }
+}
+
+// Pass C work items: each group of 64 queued keys (in queue order) has
+// ceil(candidates / cap_c) chunks; goff[g] is the first item of group g (an
+// exclusive prefix) and goff[G] the pair's item count.  One workgroup per
+// pair, 256 groups per scan step.
+__global__ void __launch_bounds__(256) k_refine_plan(AssignLists L, int cap_c) {
+  __shared__ int32_t sc[256];
+  __shared__ int32_t carry;
+  const int b = blockIdx.x, tid = threadIdx.x;
+  const int F = L.fcnt[b], G = (F + 63) / 64;
+  int32_t *goff = L.goff + (size_t)b * L.gcap;
+  const int32_t *fn = L.fn + (size_t)b * L.cap;
+  if (tid == 0) carry = 0;
+  for (int g0 = 0; g0 < G; g0 += 256) {   // uniform over the workgroup
+    const int g = g0 + tid;
+    int nit = 0;
+    if (g < G) {
+      int tot = 0;
+      for (int k = g * 64; k < min(F, g * 64 + 64); ++k) tot += fn[k];
+      nit = (tot + cap_c - 1) / cap_c;
     }
+    __syncthreads();   // carry holds the previous steps' total
+    sc[tid] = nit;
+    __syncthreads();
+    for (int d = 1; d < 256; d <<= 1) {   // inclusive scan
+      const int v = tid >= d ? sc[tid - d] : 0;
+      __syncthreads();
+      sc[tid] += v;
+      __syncthreads();
+    }
+    if (g < G) goff[g] = carry + sc[tid] - nit;
+    __syncthreads();
+    if (tid == 0) carry += sc[255];
+  }
+  __syncthreads();
+  if (tid == 0) goff[G] = carry;
+}
+
+// Pass C decision, one thread per queued key, once every chunk of its
+// candidates has its similarity: the best one (equal ones to the lower r)
+// becomes the key's anchor for now, the candidates within the bound of it
+// survive, compacted in place at the front of the key's pool segment, and a
+// key with more than one survivor goes to pass D.
+template <typename E>
+__global__ void __launch_bounds__(256) k_assign_decide(const E *__restrict__ K, const float *__restrict__ zmerge,
+                                                       const AssignPair *__restrict__ pn, int T, double s,
+                                                       int32_t *__restrict__ kappa, AssignLists L) {
+  constexpr bool BF = sizeof(E) == 2;
+  const int b = blockIdx.y;
+  const int F = L.fcnt[b];
+  const AssignPair pp = pn[b];
+  const double zm = (double)zmerge[b];
+  int32_t *pool = L.pool + (size_t)b * L.pcap;
+  const double *psim = L.psim + (size_t)b * L.pcap;
+  for (int f = blockIdx.x * 256 + threadIdx.x; f < F; f += gridDim.x * 256) {
+    const size_t q = (size_t)b * L.cap + f;
+    const int j = L.fkey[q], o = L.foff[q], m = L.fn[q];
+    if (m <= 0) continue;
+    int best = 0;
+    for (int c = 1; c < m; ++c)
+      if (psim[o + c] > psim[o + best] || (psim[o + c] == psim[o + best] && pool[o + c] < pool[o + best]))
+        best = c;
+    double eta;
+    if constexpr (BF) {
+      const double kn = row_norm(K + ((size_t)b * T + j) * kHeadDim);
+      const double g = gamma_m(kSliceTerms) * s * pp.qmax, Z = fabs(zm) * 1.4426950408889634;
+      const double ek = g * kn + exp32_err(s * pp.qmax * kn * 1.4426950408889634 * 1.001, Z);
+      const double ea = g * pp.amax + exp32_err(s * pp.qmax * pp.amax * 1.4426950408889634 * 1.001, Z);
+      eta = (1.0 + ek) * (1.0 + ea) / (1.0 - ea) * (1.0 + gamma_m(4)) * (1.0 + 1e-12) - 1.0;
+    } else {
+      eta = 3.0 * kU32 + gamma_m(4) + 1e-12;
+    }
+    const double bs = psim[o + best];
+    const double thc = bs * (1.0 - eta) / (1.0 + eta) - 1e-300;
+    kappa[(size_t)b * T + j] = pool[o + best];
+    // writes trail reads: this thread alone owns the key's pool segment
+    int ns = 0;
+    for (int c = 0; c < m; ++c)
+      if (psim[o + c] >= thc) pool[o + ns++] = pool[o + c];
+    if (ns > 1) push_d(L, b, j, o, ns);
   }
 }
 
@@ -896,13 +1013,20 @@ hipError_t launch_assign_refine(int dtype, const void *Q, const void *K, const f
                                 const float *Ua, const double *anorm, int P, int T, int t, int n, int64_t tp,
                                 int64_t np_, float scale, int32_t *kappa, const AssignLists &L, hipStream_t s) {
   if (T - t <= 0) return hipSuccess;
-  const dim3 g(kRefineBlocks, P);
-  if (dtype == ARCKV_BF16)
-    hipLaunchKernelGGL(k_assign_refine<bf16>, g, dim3(512), 0, s, (const bf16 *)Q, (const bf16 *)K, zmerge,
-                       (const AssignPair *)pn, Ua, anorm, T, t, n, tp, np_, (double)scale, kappa, L);
-  else
-    hipLaunchKernelGGL(k_assign_refine<float>, g, dim3(512), 0, s, (const float *)Q, (const float *)K, zmerge,
-                       (const AssignPair *)pn, Ua, anorm, T, t, n, tp, np_, (double)scale, kappa, L);
+  const bool bf = dtype == ARCKV_BF16;
+  hipLaunchKernelGGL(k_refine_plan, dim3(P), dim3(256), 0, s, L, 8 * kRefineCpw);
+  const dim3 g(kRefineBlocks, P), gd(8, P);
+  if (bf) {
+    hipLaunchKernelGGL(k_assign_refine<bf16>, g, dim3(512), 0, s, (const bf16 *)Q, (const bf16 *)K, zmerge, Ua,
+                       anorm, T, n, tp, np_, (double)scale, L);
+    hipLaunchKernelGGL(k_assign_decide<bf16>, gd, dim3(256), 0, s, (const bf16 *)K, zmerge, (const AssignPair *)pn,
+                       T, (double)scale, kappa, L);
+  } else {
+    hipLaunchKernelGGL(k_assign_refine<float>, g, dim3(512), 0, s, (const float *)Q, (const float *)K, zmerge, Ua,
+                       anorm, T, n, tp, np_, (double)scale, L);
+    hipLaunchKernelGGL(k_assign_decide<float>, gd, dim3(256), 0, s, (const float *)K, zmerge,
+                       (const AssignPair *)pn, T, (double)scale, kappa, L);
+  }
   return hipGetLastError();
 }
 

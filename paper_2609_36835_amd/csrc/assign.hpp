@@ -27,6 +27,9 @@ struct AssignLists {
                     // number go to the float64 pass), sent to the refine pass, keys whose pass-A
                     // candidates include a whole anchor tile
   int64_t cap;      // key capacity per pair
+  int32_t *goff;    // [P][gcap] pass C work items: first (group of 64 queued keys, candidate chunk) item of each
+                    // group, then the pair's item count
+  int64_t gcap;     // >= cap / 64 + 1
 };
 
 }  // namespace arckv
