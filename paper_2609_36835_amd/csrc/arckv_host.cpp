@@ -224,7 +224,7 @@ struct Plan {
   // chunk region (offsets relative to chunk base)
   int64_t Ckp;
   int64_t Et, U, Ua, anorm, pn, part1, part2, part3, fcnt, fkey, foff, fn, pcnt, pool, psim, dcnt, dkey, dn,
-      doff, goff;   // merge phase
+      doff, goff, dgrp, dgn, dsim, dr, ditem;   // merge phase
   int64_t offsets, cursor, perm;
   int64_t PhiT, LT, Gw, Gc, dinv, lsplit, h, w, y, x, res, sw, rprev, div, u, YT, Bm, X, R, Y2, XT, Pm, UT;  // fit phase
   int64_t nF, nidx, nbidx, npos, nnf, nnb, nstate, nred, ny, nrhs, ndx;   // exact NNLS (bias_mode 1)
@@ -272,10 +272,16 @@ static Plan make_plan(const Dims &d, int64_t P) {
   pl.pool = m.take(P * kPoolPerKey * d.Tp * 4);   // candidate pool: kPoolPerKey entries per key on average
   pl.psim = m.take(P * kPoolPerKey * d.Tp * 8);
   pl.dcnt = m.take(P * 4);
-  pl.dkey = m.take(P * d.Tp * 4);
-  pl.dn = m.take(P * d.Tp * 4);
-  pl.doff = m.take(P * d.Tp * 4);
+  const int64_t dcap = pass_d_capacity(d.Tp, kPoolPerKey);
+  pl.dkey = m.take(P * dcap * 4);
+  pl.dn = m.take(P * dcap * 4);
+  pl.doff = m.take(P * dcap * 4);
   pl.goff = m.take(P * (d.Tp / 64 + 2) * 4);   // pass C work items per group of 64 queued keys
+  pl.dgrp = m.take(P * dcap * 4);
+  pl.dgn = m.take(P * dcap * 4);
+  pl.dsim = m.take(P * dcap * 8);
+  pl.dr = m.take(P * dcap * 4);
+  pl.ditem = m.take(P * (dcap + 2) * 4);
   pl.offsets = m.take(P * (int64_t)(d.t + 1) * 4);
   pl.cursor = m.take(P * (int64_t)d.t * 4);
   pl.perm = m.take(P * (int64_t)d.T * 4);
@@ -416,7 +422,9 @@ static arckv_status run_merge_chunk(const Ctx &c, int b0, int P, const void *K, 
                 c.chunk<double>(c.pl.psim),  kPoolPerKey * d.Tp,           c.chunk<int32_t>(c.pl.dcnt),
                 c.chunk<int32_t>(c.pl.dkey), c.chunk<int32_t>(c.pl.dn),    c.chunk<int32_t>(c.pl.doff),
                 c.pers<int32_t>(c.pl.astats) + (size_t)b0 * kAssignStats, d.Tp,
-                c.chunk<int32_t>(c.pl.goff), d.Tp / 64 + 2};
+                c.chunk<int32_t>(c.pl.goff), d.Tp / 64 + 2,
+                c.chunk<int32_t>(c.pl.dgrp), c.chunk<int32_t>(c.pl.dgn), c.chunk<double>(c.pl.dsim),
+                c.chunk<int32_t>(c.pl.dr),   c.chunk<int32_t>(c.pl.ditem), pass_d_capacity(d.Tp, kPoolPerKey)};
   const float *zm = zmax + b0;
   int32_t *kap = kappa + (size_t)b0 * d.T;
   const float *phib = phi + (size_t)b0 * d.T;

@@ -338,11 +338,22 @@ __device__ inline CandA cand_a(const uint64_t *p1, const uint64_t *p2, const uin
 
 // Queue key j for the float64 pass with its k surviving candidates, which sit
 // at pool offset off (off = -1, k = t: every anchor).
+// Queue key j for the float64 pass with k candidates starting at pool offset
+// off (off < 0: all t anchors).  More than kPassDSplit pool candidates are
+// split over consecutive entries; the capacity dcap covers the largest split
+// the pool allows.
 __device__ inline void push_d(const AssignLists &L, int b, int j, int off, int k) {
-  const int slot = atomicAdd(&L.dcnt[b], 1);
-  L.dkey[(size_t)b * L.cap + slot] = j;
-  L.doff[(size_t)b * L.cap + slot] = off;
-  L.dn[(size_t)b * L.cap + slot] = k;
+  const bool split = off >= 0 && k > kPassDSplit;
+  const int ne = split ? (k + kPassDSplit - 1) / kPassDSplit : 1;
+  const int slot = atomicAdd(&L.dcnt[b], ne);
+  for (int e = 0; e < ne; ++e) {
+    const size_t q = (size_t)b * L.dcap + slot + e;
+    L.dkey[q] = j;
+    L.doff[q] = split ? off + e * kPassDSplit : off;
+    L.dn[q] = split ? min(kPassDSplit, k - e * kPassDSplit) : k;
+    L.dgrp[q] = split ? slot : -1;
+    L.dgn[q] = ne;
+  }
   atomicAdd(&L.stats[b * kAssignStats + 1], 1);
 }
 
@@ -777,12 +788,73 @@ __global__ void __launch_bounds__(256) k_assign_decide(const E *__restrict__ K, 
 // Float64 decision for the remaining keys: logits as float64 sums of exact
 // products, exp in float64, norms and dot products in float64; the largest
 // similarity wins and equal ones go to the lower r.  A key's entries are the
-// anchors that survived pass C.  A fixed grid of kExactBlocks workgroups per
-// pair takes groups of kExactGroup queued keys (group g = blockIdx.x,
-// blockIdx.x + kExactBlocks, ...); a group's keys and candidate anchors (up to
-// 32 vectors) share one sweep over the queries in tiles of 32, and a key with
-// more candidates than fit continues in the next sweep.
-constexpr int kExactBlocks = 64, kExactGroup = 8;
+// anchors that survived pass C.  k_exact_plan packs consecutive queued
+// entries into items of up to 32 vectors (an entry is its key and its
+// candidates); a fixed grid of kExactBlocks workgroups per pair takes items
+// it = blockIdx.x, blockIdx.x + kExactBlocks, ...  An item's keys and
+// candidate anchors share one sweep over the queries in tiles of 64, and an
+// entry with more candidates than fit (all t anchors) continues in the next
+// sweep.  An entry of a split key leaves its best (similarity, anchor) for
+// k_exact_merge instead of deciding the key.
+constexpr int kExactBlocks = 128;
+
+// Pass D work items: greedy packing of consecutive entries into items of at
+// most 32 vectors (an entry needs 1 + its candidates; a larger one forms an
+// item of its own).  ditem = {count, first entry of each item, dcnt}.  One
+// workgroup per pair; entry sizes staged in LDS, packed by one thread.
+__global__ void __launch_bounds__(256) k_exact_plan(AssignLists L) {
+  constexpr int W = 2048;
+  __shared__ int32_t sdn[W];
+  const int b = blockIdx.x, tid = threadIdx.x;
+  const int D = L.dcnt[b];
+  const int32_t *dn = L.dn + (size_t)b * L.dcap;
+  int32_t *items = L.ditem + (size_t)b * (L.dcap + 2);
+  int nit = 0, nv = 0;   // thread 0 only
+  for (int w0 = 0; w0 < D; w0 += W) {   // uniform over the workgroup
+    const int nw = min(W, D - w0);
+    __syncthreads();   // thread 0 is done with the previous window
+    for (int x = tid; x < nw; x += 256) sdn[x] = dn[w0 + x];
+    __syncthreads();
+    if (tid == 0) {
+      for (int x = 0; x < nw; ++x) {
+        const int need = 1 + sdn[x];
+        if (w0 + x == 0 || nv + need > 32) {
+          items[1 + nit++] = w0 + x;
+          nv = 0;
+        }
+        nv += need;
+      }
+    }
+  }
+  if (tid == 0) {
+    items[0] = nit;
+    items[1 + nit] = D;
+  }
+}
+
+// A split key's decision from its entries' bests: the largest similarity,
+// equal ones to the lower r (the same order as within an entry).  One thread
+// per first entry of a split key.
+__global__ void __launch_bounds__(256) k_exact_merge(int T, int32_t *__restrict__ kappa, AssignLists L) {
+  const int b = blockIdx.y;
+  const int D = L.dcnt[b];
+  for (int di = blockIdx.x * 256 + threadIdx.x; di < D; di += gridDim.x * 256) {
+    const size_t q = (size_t)b * L.dcap + di;
+    if (L.dgrp[q] != di) continue;
+    const int ne = L.dgn[q];
+    double bs = L.dsim[q];
+    int br = L.dr[q];
+    for (int e = 1; e < ne; ++e) {
+      const double sim = L.dsim[q + e];
+      const int r = L.dr[q + e];
+      if (sim > bs || (sim == bs && r < br)) {
+        bs = sim;
+        br = r;
+      }
+    }
+    kappa[(size_t)b * T + L.dkey[q]] = br;
+  }
+}
 
 template <typename E>
 __global__ void __launch_bounds__(256) k_assign_exact(const E *__restrict__ Q, const E *__restrict__ K,
@@ -796,7 +868,7 @@ __global__ void __launch_bounds__(256) k_assign_exact(const E *__restrict__ Q, c
   __shared__ int32_t vpos[NV], vown[NV], vr[NV];
   __shared__ double vdot[NV], vnn[NV];
   // batch segments: first and one-past-last vector, continues, final
-  __shared__ int32_t sg_v0[NV], sg_v1[NV], sg_cont[NV], sg_final[NV];
+  __shared__ int32_t sg_v0[NV], sg_v1[NV], sg_cont[NV], sg_final[NV], sg_di[NV];
   __shared__ int32_t nv_s, nseg_s, di_s, ci_s, done_s;
   __shared__ double run_sim;
   __shared__ int32_t run_r;
@@ -807,9 +879,9 @@ __global__ void __launch_bounds__(256) k_assign_exact(const E *__restrict__ Q, c
   const int32_t *S = anchors + (size_t)b * t;
   const double zm = (double)zmerge[b];
   const E *Qb = Q + (size_t)b * n * kHeadDim;
-  auto n_cand = [&](int di) { return L.dn[(size_t)b * L.cap + di]; };
+  auto n_cand = [&](int di) { return L.dn[(size_t)b * L.dcap + di]; };
   auto cand_at = [&](int di, int ci) {   // doff < 0: every anchor is a candidate
-    const int off = L.doff[(size_t)b * L.cap + di];
+    const int off = L.doff[(size_t)b * L.dcap + di];
     return off < 0 ? ci : L.pool[(size_t)b * L.pcap + off + ci];
   };
   // register tile of the logit pass: vectors tv, tv + 16 and queries tq + 16 m, m = 0..3
@@ -823,9 +895,11 @@ __global__ void __launch_bounds__(256) k_assign_exact(const E *__restrict__ Q, c
       return *reinterpret_cast<const f32x4 *>(p);
     }
   };
-  for (int g0 = bx * kExactGroup; g0 < D; g0 += kExactBlocks * kExactGroup) {
-    const int g1 = min(D, g0 + kExactGroup);
-    __syncthreads();   // every thread has left the previous group's loop
+  const int32_t *items = L.ditem + (size_t)b * (L.dcap + 2);
+  const int nitems = D > 0 ? items[0] : 0;
+  for (int it = bx; it < nitems; it += kExactBlocks) {   // uniform over the workgroup
+    const int g0 = items[1 + it], g1 = items[2 + it];
+    __syncthreads();   // every thread has left the previous item's loop
     if (tid == 0) {
       di_s = g0;
       ci_s = 0;
@@ -838,8 +912,9 @@ __global__ void __launch_bounds__(256) k_assign_exact(const E *__restrict__ Q, c
         while (di < g1 && nv + 2 <= NV) {
           const int nck = n_cand(di);
           sg_cont[ns] = ci > 0;
+          sg_di[ns] = di;
           sg_v0[ns] = nv;
-          vpos[nv] = L.dkey[(size_t)b * L.cap + di];
+          vpos[nv] = L.dkey[(size_t)b * L.dcap + di];
           vown[nv] = -1;
           vr[nv] = -1;
           const int kv = nv++;
@@ -932,8 +1007,15 @@ __global__ void __launch_bounds__(256) k_assign_exact(const E *__restrict__ Q, c
               br = vr[v];
             }
           }
-          if (sg_final[g] && br != 0x7FFFFFFF) kappa[(size_t)b * T + vpos[sg_v0[g]]] = br;
-          else {
+          if (sg_final[g]) {
+            const size_t q = (size_t)b * L.dcap + sg_di[g];
+            if (L.dgrp[q] >= 0) {   // part of a split key: k_exact_merge decides
+              L.dsim[q] = bs;
+              L.dr[q] = br;
+            } else if (br != 0x7FFFFFFF) {
+              kappa[(size_t)b * T + vpos[sg_v0[g]]] = br;
+            }
+          } else {
             run_sim = bs;
             run_r = br;
           }
@@ -1034,12 +1116,14 @@ hipError_t launch_assign_refine(int dtype, const void *Q, const void *K, const f
 hipError_t launch_assign_exact(int dtype, const void *Q, const void *K, const int32_t *anchors, const float *zmerge,
                                int P, int T, int t, int n, float scale, int32_t *kappa, const AssignLists &L,
                                hipStream_t s) {
+  hipLaunchKernelGGL(k_exact_plan, dim3(P), dim3(256), 0, s, L);
   if (dtype == ARCKV_BF16)
-    hipLaunchKernelGGL(k_assign_exact<bf16>, dim3(kExactBlocks, P), dim3(256), 0, s, (const bf16 *)Q, (const bf16 *)K, anchors,
-                       zmerge, T, t, n, (double)scale, kappa, L);
+    hipLaunchKernelGGL(k_assign_exact<bf16>, dim3(kExactBlocks, P), dim3(256), 0, s, (const bf16 *)Q,
+                       (const bf16 *)K, anchors, zmerge, T, t, n, (double)scale, kappa, L);
   else
-    hipLaunchKernelGGL(k_assign_exact<float>, dim3(kExactBlocks, P), dim3(256), 0, s, (const float *)Q, (const float *)K, anchors,
-                       zmerge, T, t, n, (double)scale, kappa, L);
+    hipLaunchKernelGGL(k_assign_exact<float>, dim3(kExactBlocks, P), dim3(256), 0, s, (const float *)Q,
+                       (const float *)K, anchors, zmerge, T, t, n, (double)scale, kappa, L);
+  hipLaunchKernelGGL(k_exact_merge, dim3(8, P), dim3(256), 0, s, T, kappa, L);
   return hipGetLastError();
 }
 
