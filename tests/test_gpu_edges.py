@@ -1,7 +1,7 @@
 """GPU edge cases: full retention, a single anchor, tiny and ragged caches against
 the oracle, lambda_m = 0, Cholesky failure and ridge escalation (also at the
-32K-context shape), non-finite inputs, recomputed row statistics, and the exact
-fit where it cannot bind."""
+32K-context shape), non-finite inputs, recomputed row statistics, the exact
+fit where it cannot bind, and keys tied with many anchors."""
 import math
 
 import numpy as np
@@ -288,3 +288,34 @@ def test_exact_fit_degenerate_cases():
     _, _, _, out1 = run(wl, 0.001, bias_mode=1)
     assert np.all(out1[4].numpy() == 0)
     np.testing.assert_allclose(np64(out1[2]), np64(out0[2]), rtol=0, atol=1e-5)
+
+
+@pytest.mark.parametrize("n_dup_anchors", [40, 70])
+def test_key_tied_with_many_anchors(n_dup_anchors):
+    """Keys whose row repeats in more than 31 anchors (eq. anchor_assignment):
+    every tied anchor survives the refine pass, the float64 pass splits the key
+    over several entries, and the merged decision is the lowest tied r (ties to
+    the lowest r).  The other keys match the float64 oracle up to certified
+    near-ties."""
+    rng = np.random.default_rng(11 + n_dup_anchors)
+    T, n, t = 640, 256, 160
+    s = 1.0 / math.sqrt(128)
+    K = rng.standard_normal((T, 128)).astype(np.float32)
+    V = rng.standard_normal((T, 128)).astype(np.float32)
+    Q = rng.standard_normal((n, 128)).astype(np.float32)
+    dup = np.sort(rng.choice(T, n_dup_anchors + 24, replace=False))
+    K[dup] = K[dup[0]]
+    others = np.setdiff1d(np.arange(T), dup)
+    S = np.sort(np.concatenate([dup[:n_dup_anchors], rng.choice(others, t - n_dup_anchors, replace=False)]))
+    Kb, Vb, Qb = (torch.from_numpy(x).to(torch.bfloat16) for x in (K, V, Q))
+    kap, st = gpu_assignment(Kb[None].cuda().contiguous(), Vb[None].cuda().contiguous(),
+                             Qb[None].cuda().contiguous(), torch.from_numpy(S.astype(np.int32))[None].cuda(), s)
+    r_dup = np.searchsorted(S, dup[:n_dup_anchors])      # the tied anchors' indices r
+    for j in dup[n_dup_anchors:]:                          # the tied keys that are not anchors
+        assert kap[j] == r_dup.min(), (j, kap[j], r_dup.min())
+    assert st[1] >= len(dup) - n_dup_anchors               # they went to the float64 pass
+    assert np.all(kap[S] == np.arange(t))
+    K64, Q64 = np64(Kb), np64(Qb)
+    ref, _, _ = oracle.profiles_assign_phi(Q64, K64, S, s)
+    ref[dup] = kap[dup]   # checked above against the exact tie rule
+    certify_flips(kap, ref, Q64, K64, S, s)
