@@ -165,11 +165,11 @@ struct StageScope {
     std::lock_guard<std::mutex> lk(g_timing.mu);
     a = take_event();
     b = take_event();
-    if (a) hipEventRecord(a, s);
+    if (a) (void)hipEventRecord(a, s);
   }
   ~StageScope() {
     if (!a || !b) return;
-    hipEventRecord(b, s);
+    (void)hipEventRecord(b, s);
     std::lock_guard<std::mutex> lk(g_timing.mu);
     g_timing.pending.push_back({stage, a, b});
   }

@@ -100,18 +100,6 @@ __global__ void __launch_bounds__(256) k_pair_norms(const E *__restrict__ Q, con
   }
 }
 
-// exp(x) for x <= ~0 in float64 range reduction around the hardware base-2
-// exponential: x log2(e) = k + f, f in [0, 1), exp(x) = 2^f 2^k.  Relative error
-// at most 2^-22 (v_exp_f32 within 1 ulp on [1, 2), f rounded to fp32 within
-// 2^-25 absolute, and the products in float64).
-__device__ inline double exp_reduced(double x) {
-  const double y = x * 1.4426950408889634074;
-  const double k = floor(y);
-  const float f = (float)(y - k);
-  return ldexp((double)__builtin_amdgcn_exp2f(f), (int)k);
-}
-constexpr double kExpReducedErr = 2.384185791015625e-07;   // 2^-22
-
 // Logit of one (query, key) element from the eight 16-wide slices of the head
 // dimension: each slice is one MFMA into a zero accumulator (products of bf16
 // values are exact in fp32, so a slice sum is within gamma_16 of the sum of its
