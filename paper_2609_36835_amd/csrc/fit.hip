@@ -301,10 +301,10 @@ __global__ void __launch_bounds__(256) k_chol_diag(float *__restrict__ Gw, int64
   }
 }
 
-// Panel: L_ik = A_ik L_kk^-T for the rows below diagonal block k, as an fp32
-// MFMA product with the inverse from k_chol_diag.  A workgroup takes 128 rows
-// (4 waves x 32 rows x 64 columns).
-__global__ void __launch_bounds__(256) k_chol_panel(float *__restrict__ Gw, int64_t ld, int k,
+// Panel: L_ik = A_ik L_kk^-T for the rows below diagonal block k up to row
+// r_end, as an fp32 MFMA product with the inverse from k_chol_diag.  A
+// workgroup takes 128 rows (4 waves x 32 rows x 64 columns).
+__global__ void __launch_bounds__(256) k_chol_panel(float *__restrict__ Gw, int64_t ld, int k, int64_t r_end,
                                                     const float *__restrict__ dinv,
                                                     const int32_t *__restrict__ info) {
   __shared__ float sLi[kNB * kSD], sA[128 * kSD];
@@ -323,7 +323,7 @@ __global__ void __launch_bounds__(256) k_chol_panel(float *__restrict__ Gw, int6
   for (int e = tid; e < 128 * kNB / 4; e += 256) {
     const int r = e / 16, c4 = (e % 16) * 4;
     f32x4 v = {0.f, 0.f, 0.f, 0.f};
-    if (rb + r < ld) v = *reinterpret_cast<const f32x4 *>(G + (size_t)(rb + r) * ld + (size_t)k * kNB + c4);
+    if (rb + r < r_end) v = *reinterpret_cast<const f32x4 *>(G + (size_t)(rb + r) * ld + (size_t)k * kNB + c4);
 #pragma unroll
     for (int q = 0; q < 4; ++q) sA[r * kSD + c4 + q] = v[q];
   }
@@ -338,7 +338,7 @@ __global__ void __launch_bounds__(256) k_chol_panel(float *__restrict__ Gw, int6
 #pragma unroll
   for (int v = 0; v < 16; ++v) {
     const int64_t r = rb + 32 * wave + acc_row(v, lane);
-    if (r < ld) {
+    if (r < r_end) {
       G[(size_t)r * ld + (size_t)k * kNB + col] = acc0[v];
       G[(size_t)r * ld + (size_t)k * kNB + 32 + col] = acc1[v];
     }
@@ -347,7 +347,7 @@ __global__ void __launch_bounds__(256) k_chol_panel(float *__restrict__ Gw, int6
 
 // Trailing update of the blocked factorisation on fp32 MFMA:
 //   G[r][c] -= sum_{q in [q0, q0+kw)} L[r][q] L[c][q]
-// for r in [r_lo, ld), c in [r_lo, c_hi), c <= r (up to the 64-wide diagonal
+// for r in [r_lo, r_hi), c in [r_lo, c_hi), c <= r (up to the 64-wide diagonal
 // block), with 128 x 128 output tiles (4 waves of 64 x 64).  Only tiles on or
 // below the diagonal are launched: row tile ti holds column tiles
 // tj < min(ti + 1, n_ct); workgroups are remapped so each XCD owns a
@@ -372,8 +372,9 @@ __host__ __device__ inline int64_t chol_upd_tiles(int n_rt, int n_ct) {
   return (int64_t)n_ct * (n_ct + 1) / 2 + (int64_t)(n_rt - n_ct) * n_ct;
 }
 
-__global__ void __launch_bounds__(256) k_chol_upd(float *__restrict__ Gw, int64_t ld, int r_lo, int c_hi, int q0,
-                                                  int kw, int n_rt, int n_ct, const int32_t *__restrict__ info) {
+__global__ void __launch_bounds__(256) k_chol_upd(float *__restrict__ Gw, int64_t ld, int r_lo, int r_hi, int c_hi,
+                                                  int q0, int kw, int n_rt, int n_ct,
+                                                  const int32_t *__restrict__ info) {
   // LDS rows of 33 floats: the 4-byte fragment reads of 32 consecutive rows
   // then fall in 32 distinct banks.  Two buffers; the next slab is fetched into
   // registers while the current one is consumed.
@@ -397,7 +398,7 @@ __global__ void __launch_bounds__(256) k_chol_upd(float *__restrict__ Gw, int64_
       const int row_a = rb + r, row_b = cb + r;
       ra[c] = f32x4{0.f, 0.f, 0.f, 0.f};
       rbv[c] = ra[c];
-      if (row_a < ld) ra[c] = *reinterpret_cast<const f32x4 *>(G + (size_t)row_a * ld + q0 + kq + c4);
+      if (row_a < r_hi) ra[c] = *reinterpret_cast<const f32x4 *>(G + (size_t)row_a * ld + q0 + kq + c4);
       if (row_b < c_hi) rbv[c] = *reinterpret_cast<const f32x4 *>(G + (size_t)row_b * ld + q0 + kq + c4);
     }
   };
@@ -465,7 +466,7 @@ __global__ void __launch_bounds__(256) k_chol_upd(float *__restrict__ Gw, int64_
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
         const int r = rb + wm * 64 + 32 * i + acc_row(v, lane);
-        if (r < ld && c < c_hi && c <= r + 63) G[(size_t)r * ld + c] = old[i][j][v] - acc[i][j][v];
+        if (r < r_hi && c < c_hi && c <= r + 63) G[(size_t)r * ld + c] = old[i][j][v] - acc[i][j][v];
       }
     }
 }
@@ -549,6 +550,152 @@ struct EpiCholUpd {
     }
   }
 };
+
+// Rows K1 .. ld of the outer panel (columns K0 .. K1 = K0 + 256), once its
+// 256 x 256 diagonal block is factored: for each 64-column block k in order,
+// the panel step L_rk = A_rk L_kk^-T (as k_chol_panel), then the update of
+// the panel's later blocks j, A_rj -= L_rk L_jk^T (as k_chol_upd), with the
+// same MFMA products summed in the same order, so the values equal those of
+// the separate launches; then the rows' L is written back and split into the
+// scaled fp16 hi / lo planes of the rank-256 trailing update (as
+// k_chol_split2).  A workgroup of 8 waves keeps 128 rows x 256 columns in LDS,
+// so the strip is read and written once instead of once per step; each
+// 128 x 64 product is 4 x 2 waves of 32 x 32.
+constexpr int kStripRows = 128, kStripLd = 256 + 1;   // LDS row stride (floats)
+constexpr size_t kStripLds = ((size_t)kStripRows * kStripLd + (size_t)kNB * kSD) * sizeof(float);
+
+__global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) k_chol_strip(float *__restrict__ Gw, int64_t ld, int K0,
+                                                    const float *__restrict__ dinv, f16 *__restrict__ Ls,
+                                                    const int32_t *__restrict__ info) {
+  extern __shared__ float strip_smem[];
+  float *sT = strip_smem;                                  // [128][257]: the rows' 256 panel columns
+  float *sB = strip_smem + (size_t)kStripRows * kStripLd;  // [64][65]: D_k or L_jk
+  const int b = blockIdx.y;
+  if (info[b] != 0) return;   // uniform over the workgroup
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1, h = lane >> 5, col = lane & 31;
+  const int K1 = K0 + 256;
+  const int64_t R = K1 + (int64_t)blockIdx.x * kStripRows;
+  float *G = Gw + (size_t)b * ld * ld;
+  const int nb = (int)(ld / kNB);
+  // The ten B operands in order: step (k, k) is the panel step with D_k, step
+  // (k, j > k) the update of block j with L_jk of the diagonal block.  The next
+  // step's tile is loaded into registers while the current step's products
+  // run (two 16-byte loads per thread) and stored to sB after the barrier.
+  constexpr int kSteps = 10;
+  constexpr int8_t step_k[kSteps] = {0, 0, 0, 0, 1, 1, 1, 2, 2, 3};
+  constexpr int8_t step_j[kSteps] = {0, 1, 2, 3, 1, 2, 3, 2, 3, 3};
+  f32x4 pre[2];
+  auto load_b = [&](int st) {
+    const int k = step_k[st], j = step_j[st];
+    const float *src = j == k ? dinv + ((size_t)b * nb + K0 / kNB + k) * kNB * kNB
+                              : G + (size_t)(K0 + kNB * j) * ld + K0 + kNB * k;
+    const int64_t lds = j == k ? kNB : ld;
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+      const int e = tid + 512 * c, i = e >> 4, c4 = (e & 15) * 4;
+      pre[c] = *reinterpret_cast<const f32x4 *>(src + (size_t)i * lds + c4);
+    }
+  };
+  auto stash_b = [&]() {
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+      const int e = tid + 512 * c, i = e >> 4, c4 = (e & 15) * 4;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) sB[i * kSD + c4 + q] = pre[c][q];
+    }
+  };
+  // this wave's 32 x 32 block of T[:, 64 ka ..] x sB^T: rows 32 wm, columns 32 wn
+  // (operands read from LDS up front, then the 32 products in order of ks)
+  auto product = [&](int ka) {
+    float av[kNB / 2], bv[kNB / 2];
+#pragma unroll
+    for (int ks = 0; ks < kNB / 2; ++ks) {
+      av[ks] = sT[(32 * wm + col) * kStripLd + 64 * ka + 2 * ks + h];
+      bv[ks] = sB[(32 * wn + col) * kSD + 2 * ks + h];
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    f32x16 acc = zero16();
+#pragma unroll
+    for (int ks = 0; ks < kNB / 2; ++ks) acc = Mfma<float>::mma(av[ks], bv[ks], acc);
+    return acc;
+  };
+  {  // the strip, 128 rows x 64 chunks of 4: every load in flight before the first LDS store
+    f32x4 v[kStripRows * 64 / 512];
+#pragma unroll
+    for (int i = 0; i < kStripRows * 64 / 512; ++i) {
+      const int e = tid + 512 * i, r = e >> 6, c4 = (e & 63) * 4;
+      v[i] = *reinterpret_cast<const f32x4 *>(G + (size_t)(R + r) * ld + K0 + c4);
+    }
+    load_b(0);
+#pragma unroll
+    for (int i = 0; i < kStripRows * 64 / 512; ++i) {
+      const int e = tid + 512 * i, r = e >> 6, c4 = (e & 63) * 4;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) sT[r * kStripLd + c4 + q] = v[i][q];
+    }
+  }
+#pragma unroll
+  for (int st = 0; st < kSteps; ++st) {
+    const int k = step_k[st], j = step_j[st];
+    __syncthreads();   // sT is up to date and every wave is done with sB
+    stash_b();
+    if (st + 1 < kSteps) load_b(st + 1);
+    __syncthreads();
+    const f32x16 acc = product(k);
+    if (j == k) {      // panel step: L_k replaces block k once every wave has read it
+      __syncthreads();
+#pragma unroll
+      for (int v = 0; v < 16; ++v)
+        sT[(32 * wm + acc_row(v, lane)) * kStripLd + 64 * k + 32 * wn + col] = acc[v];
+    } else {           // update of block j (this wave's own entries; block k is not written)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        float &x = sT[(32 * wm + acc_row(v, lane)) * kStripLd + 64 * j + 32 * wn + col];
+        x = x - acc[v];
+      }
+    }
+  }
+  __syncthreads();
+  // write the rows' L and their scaled fp16 split: each wave takes 16 rows
+  // (wave, wave + 8, ...), four columns per lane, and reduces the 16 row
+  // maxima together.  Row r of the split: s = 2^sh with m 2^sh < 2^14 for the
+  // row's largest magnitude m, hi = fp16(x s), lo = fp16(x s - hi), and 1 / s.
+  constexpr int kRowsPerWave = kStripRows / 8;
+  f32x4 v[kRowsPerWave];
+  float m[kRowsPerWave];
+#pragma unroll
+  for (int i = 0; i < kRowsPerWave; ++i) {
+    const int rr = wave + 8 * i;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) v[i][q] = sT[rr * kStripLd + 4 * lane + q];
+    m[i] = fmaxf(fmaxf(fabsf(v[i][0]), fabsf(v[i][1])), fmaxf(fabsf(v[i][2]), fabsf(v[i][3])));
+  }
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1)
+#pragma unroll
+    for (int i = 0; i < kRowsPerWave; ++i) m[i] = fmaxf(m[i], __shfl_xor(m[i], off, 64));
+  f16 *Lb = Ls + (size_t)b * 3 * ld * 256;
+#pragma unroll
+  for (int i = 0; i < kRowsPerWave; ++i) {
+    const int64_t r = R + wave + 8 * i;
+    *reinterpret_cast<f32x4 *>(G + (size_t)r * ld + K0 + 4 * lane) = v[i];
+    int ex = 0;
+    if (m[i] > 0.0f) frexpf(m[i], &ex);   // m = f 2^ex, f in [0.5, 1)
+    const int sh = min(14 - ex, 126);
+    f16x4 hi, lo;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const float x = ldexpf(v[i][q], sh);
+      hi[q] = (f16)x;
+      lo[q] = (f16)(x - (float)hi[q]);
+    }
+    f16 *base = Lb + (size_t)r * 256 + 4 * lane;
+    *reinterpret_cast<f16x4 *>(base) = hi;
+    *reinterpret_cast<f16x4 *>(base + (size_t)ld * 256) = lo;
+    if (lane == 0) reinterpret_cast<float *>(Lb + (size_t)2 * ld * 256)[r] = ldexpf(1.0f, -sh);
+  }
+}
 
 // --------------------------------------------------------------- one right-hand side
 // One-rhs triangular solves, float64 vectors, right-looking over 64-row
@@ -1280,26 +1427,32 @@ hipError_t launch_cholesky_factor(float *Gw, const float *Gc, int B, int t, int6
   // panel with k = 256 (a quarter of the trailing-matrix traffic of 64-wide
   // steps).
   constexpr int kOuter = 256;
-  const int nrb = (int)(ld / kNB);
   for (int K0 = 0; K0 < ld; K0 += kOuter) {
     const int K1 = (int)(K0 + kOuter < ld ? K0 + kOuter : ld);
+    // the 256 x 256 diagonal block: 64-wide steps restricted to its rows
     for (int c = K0; c < K1; c += kNB) {
       const int k = c / kNB;
       hipLaunchKernelGGL(k_chol_diag, dim3(B), dim3(256), 0, s, Gw, ld, k, st.info, dinv);
-      const int rem = nrb - k - 1;
+      const int rem = (K1 - c) / kNB - 1;   // row blocks of the diagonal block below block k
       if (rem > 0)
-        hipLaunchKernelGGL(k_chol_panel, dim3((rem + 1) / 2, B), dim3(256), 0, s, Gw, ld, k, dinv, st.info);
+        hipLaunchKernelGGL(k_chol_panel, dim3((rem + 1) / 2, B), dim3(256), 0, s, Gw, ld, k, (int64_t)K1, dinv,
+                           st.info);
       if (c + kNB < K1) {
-        const int r_lo = c + kNB, n_rt = (int)((ld - r_lo + 127) / 128), n_ct = (K1 - r_lo + 127) / 128;
+        const int r_lo = c + kNB, n_rt = (K1 - r_lo + 127) / 128, n_ct = (K1 - r_lo + 127) / 128;
         hipLaunchKernelGGL(k_chol_upd, dim3((unsigned)(chol_upd_tiles(n_rt, n_ct) * B)), dim3(256), 0, s, Gw, ld,
-                           r_lo, K1, c, kNB, n_rt, n_ct, st.info);
+                           r_lo, K1, K1, c, kNB, n_rt, n_ct, st.info);
       }
     }
     if (K1 < ld) {
-      // rank-256 trailing update on fp16 MFMA with the scaled split panel (see k_chol_split2)
       f16 *Ls = reinterpret_cast<f16 *>(lsplit);
       const int64_t rows = ld - K1;
-      hipLaunchKernelGGL(k_chol_split2, dim3((unsigned)(rows / 4), B), dim3(256), 0, s, Gw, ld, K0, K1, Ls, st.info);
+      // the rows below: all four steps, written back once, with the split planes
+      const hipError_t ea = hipFuncSetAttribute((const void *)k_chol_strip,
+                                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)kStripLds);
+      if (ea != hipSuccess) return ea;
+      hipLaunchKernelGGL(k_chol_strip, dim3((unsigned)(rows / kStripRows), B), dim3(512), kStripLds, s, Gw, ld, K0,
+                         dinv, Ls, st.info);
+      // rank-256 trailing update on fp16 MFMA with the scaled split panel
       // The three products hi.hi, hi.lo, lo.hi as one contraction over
       // K = 3 x 256 (each 256-column segment reads one plane pair), so 256 x 256
       // tiles fit the LDS.
