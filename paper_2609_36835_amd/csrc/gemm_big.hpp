@@ -1,9 +1,8 @@
 // Large-tile batched TN contraction on bf16 or fp16 MFMA (32x32x16) for the
 // big contractions of the path: the anchor assignment (one fp16 plane), the
 // split-bf16 Gram matrices (hi/lo planes, three products) and the Cholesky
-// trailing updates (hi/mid/lo planes of an fp32 panel, the six products whose
-// plane indices sum to at most 2, which reproduce the fp32 product to within
-// about 2^-23 relative).
+// trailing updates (row-scaled fp16 hi/lo planes of an fp32 panel, three
+// products as one contraction over three K segments, about 2^-22 relative).
 //
 // C[M][N] = sum_k A[m][k] B[n][k], both operands K-contiguous.  A workgroup of
 // WM x WN waves owns a (32 WM TM) x (32 WN TN) tile; each wave a 32TM x 32TN
@@ -15,8 +14,9 @@
 // one chunk per half-wave) free of bank conflicts.  NS LDS stages: slabs
 // i+1 .. i+NS-1 are in flight while slab i feeds the MFMAs (a counted vmcnt
 // wait lets the younger slabs stay outstanding); fragments for k-step ks+1 are
-// read while the MFMAs of ks run.  One workgroup barrier per slab, without the
-// full memory fence of __syncthreads(), so the prefetch stays in flight.
+// read while the MFMAs of ks run, and a slab's last k-step of MFMAs runs after
+// the next slab's barrier.  One workgroup barrier per slab, without the full
+// memory fence of __syncthreads(), so the prefetch stays in flight.
 // Dimensions must be multiples of the tile; workgroups are remapped so that
 // each XCD owns a contiguous, M-grouped (or lower-triangular) range of tiles.
 #pragma once
@@ -104,6 +104,9 @@ __device__ __forceinline__ void wait_vmcnt() {
   static_assert(N >= 0 && N < 64, "vmcnt range");
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
+
+// s_waitcnt lgkmcnt(0) (vmcnt and expcnt left unconstrained).
+__device__ __forceinline__ void wait_lgkmcnt0() { __builtin_amdgcn_s_waitcnt((15) | (3 << 14) | (7 << 4)); }
 
 // Workgroup barrier without a memory fence; the empty asm statements keep the
 // compiler from moving LDS accesses across it.
@@ -204,10 +207,33 @@ __global__ void __launch_bounds__(64 * WM * WN, 1) k_gemm_big(BigShape g, const 
 #pragma unroll
     for (int j = 0; j < TN; ++j) acc[i][j] = zero16();
 
+  // one k-step of products from fragments in registers
+  auto step = [&](bf16x8 (&fa)[NA][TM], bf16x8 (&fb)[NB][TN]) {
+#pragma unroll
+    for (int ii = 0; ii < TM; ++ii)
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        acc[ii][j] = mma16<E>(fa[0][ii], fb[0][j], acc[ii][j]);
+        if constexpr (NB > 1) acc[ii][j] = mma16<E>(fa[0][ii], fb[1][j], acc[ii][j]);
+        if constexpr (NA > 1) acc[ii][j] = mma16<E>(fa[1][ii], fb[0][j], acc[ii][j]);
+        if constexpr (NA > 2 && NB > 2) {
+          acc[ii][j] = mma16<E>(fa[0][ii], fb[2][j], acc[ii][j]);
+          acc[ii][j] = mma16<E>(fa[2][ii], fb[0][j], acc[ii][j]);
+          acc[ii][j] = mma16<E>(fa[1][ii], fb[1][j], acc[ii][j]);
+        }
+      }
+  };
+
+  // Fragments of k-step ks go to buffer ks & 1.  The products of a slab's last
+  // k-step (buffer 1) run after the next slab's barrier, under the LDS reads
+  // of that slab's first k-step, so the matrix cores are not idle while every
+  // wave fetches its first fragments; the sums keep their order.
+  static_assert(C::KS % 2 == 0, "the last k-step of a slab sits in buffer 1");
   const int nk = g.K / BK;
 #pragma unroll
   for (int st = 0; st < NS - 1; ++st)
     if (st < nk) issue(st, st);
+  bf16x8 fa[2][NA][TM], fb[2][NB][TN];
   for (int i = 0; i < nk; ++i) {
     // this wave's runs of slab i have landed (the younger slabs i+1 ..
     // i+NS-2 may still be in flight); after the barrier every wave's have, and
@@ -217,31 +243,21 @@ __global__ void __launch_bounds__(64 * WM * WN, 1) k_gemm_big(BigShape g, const 
       if (i + 1 < nk) wait_vmcnt<C::SLAB_INST>();
       else wait_vmcnt<0>();
     }
+    wait_lgkmcnt0();   // the deferred fragments are in registers
     lds_barrier();
     if (i + NS - 1 < nk) issue(i + NS - 1, (i + NS - 1) % NS);
     const char *s = big_smem + (i % NS) * C::STAGE;
-    bf16x8 fa[2][NA][TM], fb[2][NB][TN];
     rd(s, 0, fa[0], fb[0]);
+    __builtin_amdgcn_sched_barrier(0);
+    if (i > 0) step(fa[1], fb[1]);
 #pragma unroll
-    for (int ks = 0; ks < C::KS; ++ks) {
-      if (ks + 1 < C::KS) rd(s, ks + 1, fa[(ks + 1) & 1], fb[(ks + 1) & 1]);
-      const int cur = ks & 1;
-#pragma unroll
-      for (int ii = 0; ii < TM; ++ii)
-#pragma unroll
-        for (int j = 0; j < TN; ++j) {
-          acc[ii][j] = mma16<E>(fa[cur][0][ii], fb[cur][0][j], acc[ii][j]);
-          if constexpr (NB > 1) acc[ii][j] = mma16<E>(fa[cur][0][ii], fb[cur][1][j], acc[ii][j]);
-          if constexpr (NA > 1) acc[ii][j] = mma16<E>(fa[cur][1][ii], fb[cur][0][j], acc[ii][j]);
-          if constexpr (NA > 2 && NB > 2) {
-            acc[ii][j] = mma16<E>(fa[cur][0][ii], fb[cur][2][j], acc[ii][j]);
-            acc[ii][j] = mma16<E>(fa[cur][2][ii], fb[cur][0][j], acc[ii][j]);
-            acc[ii][j] = mma16<E>(fa[cur][1][ii], fb[cur][1][j], acc[ii][j]);
-          }
-        }
+    for (int ks = 0; ks + 1 < C::KS; ++ks) {
+      rd(s, ks + 1, fa[(ks + 1) & 1], fb[(ks + 1) & 1]);
+      step(fa[ks & 1], fb[ks & 1]);
     }
     asm volatile("" ::: "memory");
   }
+  if (nk > 0) step(fa[1], fb[1]);
   __syncthreads();
   epi(acc, p, mt * C::BM + wm * 32 * TM, nt * C::BN + wn * 32 * TN, mt, nt, lane, wm, wn);
 }
