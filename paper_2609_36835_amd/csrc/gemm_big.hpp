@@ -245,11 +245,14 @@ __global__ void __launch_bounds__(64 * WM * WN, 1) k_gemm_big(BigShape g, const 
     }
     wait_lgkmcnt0();   // the deferred fragments are in registers
     lds_barrier();
-    if (i + NS - 1 < nk) issue(i + NS - 1, (i + NS - 1) % NS);
     const char *s = big_smem + (i % NS) * C::STAGE;
     rd(s, 0, fa[0], fb[0]);
     __builtin_amdgcn_sched_barrier(0);
     if (i > 0) step(fa[1], fb[1]);
+    // the next slab's loads go out once the deferred MFMAs are issued (before
+    // them they hold up the first fragment reads, later they land late)
+    __builtin_amdgcn_sched_barrier(0);
+    if (i + NS - 1 < nk) issue(i + NS - 1, (i + NS - 1) % NS);
 #pragma unroll
     for (int ks = 0; ks + 1 < C::KS; ++ks) {
       rd(s, ks + 1, fa[(ks + 1) & 1], fb[(ks + 1) & 1]);
