@@ -4,19 +4,22 @@
 // M a float32 Gram matrix of size tp (padded; the padding is an identity
 // block with zero right-hand side, so padded unknowns solve to 0):
 //   k_ridge_init     lam = delta * tr(M)/t, write M + lam I into the work copy
-//   Cholesky         right-looking, float32, two-level blocking:
-//                      k_chol_diag    factor a 64 x 64 diagonal block in
-//                                     registers (one wave) and invert it
-//                      k_chol_panel   L_ik = A_ik L_kk^-T for row blocks i > k
-//                                     (fp32 MFMA with the inverse)
-//                      k_chol_upd     A -= L L^T over a panel's own columns
-//                                     (fp32 MFMA, 128 x 128 tiles), once per
-//                                     64 columns inside a 256-wide outer panel;
-//                                     the rest of the matrix is updated once
-//                                     per outer panel by the big contraction
-//                                     on fp16 MFMA, the panel scaled per row
-//                                     by a power of two and split into hi + lo
-//                                     (three products, about 2^-22 relative)
+//   Cholesky         right-looking, float32, two-level blocking over
+//                    256-wide outer panels:
+//                      k_chol_diag    factor a 64 x 64 diagonal block and
+//                                     invert it (256 threads, a quarter row
+//                                     each, one barrier per column)
+//                      k_chol_panel   L_ik = A_ik L_kk^-T inside the panel's
+//                                     256 x 256 diagonal block (fp32 MFMA
+//                                     with the inverse)
+//                      k_chol_upd     A -= L L^T inside that block (fp32 MFMA)
+//                      k_chol_strip   the rows below it: the same panel steps
+//                                     and updates on a 128 x 256 strip held in
+//                                     LDS, then the split planes
+//                    the rest of the matrix is updated once per outer panel by
+//                    the big contraction on fp16 MFMA, the panel scaled per row
+//                    by a power of two and split into hi + lo (three products,
+//                    about 2^-22 relative)
 //                    a failed pivot records info = column + 1 for that pair
 //   escalation       pairs that failed are refactored by the same kernels with
 //                    delta raised tenfold (from 1e-7 when zero), at most
@@ -471,41 +474,11 @@ __global__ void __launch_bounds__(256) k_chol_upd(float *__restrict__ Gw, int64_
     }
 }
 
-// Rows K1.. of the panel columns K0 .. K0 + 255 for the trailing update on
-// fp16 MFMA: each row is scaled by a power of two that brings its largest
-// magnitude into [2^13, 2^14) and split exactly into fp16 hi + lo (22
-// significant bits), so hi.hi + hi.lo + lo.hi is the row product to about
-// 2^-22 relative.  One wave per row (four columns per lane); the inverse scale
-// of each row goes after the two planes for the update's epilogue.
-// Layout per pair: hi [ld][256], lo [ld][256] (fp16), inverse scales [ld] (fp32).
-__global__ void __launch_bounds__(256) k_chol_split2(const float *__restrict__ Gw, int64_t ld, int K0, int K1,
-                                                     f16 *__restrict__ Ls, const int32_t *__restrict__ info) {
-  const int b = blockIdx.y;
-  if (info[b] != 0) return;
-  const int lane = threadIdx.x & 63;
-  const int64_t r = K1 + (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (r >= ld) return;   // uniform over the wave
-  const f32x4 v = *reinterpret_cast<const f32x4 *>(Gw + (size_t)b * ld * ld + (size_t)r * ld + K0 + 4 * lane);
-  float m = fmaxf(fmaxf(fabsf(v[0]), fabsf(v[1])), fmaxf(fabsf(v[2]), fabsf(v[3])));
-  m = wave_max(m);
-  int ex = 0;
-  if (m > 0.0f) frexpf(m, &ex);          // m = f 2^ex, f in [0.5, 1)
-  const int sh = min(14 - ex, 126);      // m 2^sh < 2^14
-  f16 *base = Ls + (size_t)b * 3 * ld * 256 + (size_t)r * 256 + 4 * lane;
-#pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    const float x = ldexpf(v[k], sh);
-    const f16 hi = (f16)x;
-    base[k] = hi;
-    base[(size_t)ld * 256 + k] = (f16)(x - (float)hi);
-  }
-  if (lane == 0) reinterpret_cast<float *>(Ls + (size_t)b * 3 * ld * 256 + (size_t)2 * ld * 256)[r] = ldexpf(1.0f, -sh);
-}
-
 // G[K1 + r][K1 + c] -= acc s_r s_c for the tile's entries with c <= r + 63
 // (the lower triangle, up to whole diagonal 64-blocks), s the rows' inverse
-// scales of k_chol_split2 (256 x 256 tiles, 512 threads); per row block of the
-// wave, every old value is loaded before any store so the loads pipeline.
+// scales stored with the split planes by k_chol_strip (256 x 256 tiles, 512
+// threads); per row block of the wave, every old value is loaded before any
+// store so the loads pipeline.
 template <int TM, int TN>
 struct EpiCholUpd {
   float *G;
@@ -556,9 +529,13 @@ struct EpiCholUpd {
 // the panel step L_rk = A_rk L_kk^-T (as k_chol_panel), then the update of
 // the panel's later blocks j, A_rj -= L_rk L_jk^T (as k_chol_upd), with the
 // same MFMA products summed in the same order, so the values equal those of
-// the separate launches; then the rows' L is written back and split into the
-// scaled fp16 hi / lo planes of the rank-256 trailing update (as
-// k_chol_split2).  A workgroup of 8 waves keeps 128 rows x 256 columns in LDS,
+// the separate launches; then the rows' L is written back and split for the
+// rank-256 trailing update on fp16 MFMA: each row is scaled by a power of two
+// that brings its largest magnitude into [2^13, 2^14) and split exactly into
+// fp16 hi + lo (22 significant bits), so hi.hi + hi.lo + lo.hi is the row
+// product to about 2^-22 relative.  Split layout per pair: hi [ld][256], lo
+// [ld][256] (fp16), inverse scales [ld] (fp32; rows below K1 only).
+// A workgroup of 8 waves keeps 128 rows x 256 columns in LDS,
 // so the strip is read and written once instead of once per step; each
 // 128 x 64 product is 4 x 2 waves of 32 x 32.
 constexpr int kStripRows = 128, kStripLd = 256 + 1;   // LDS row stride (floats)
