@@ -291,7 +291,7 @@ static Plan make_plan(const Dims &d, int64_t P) {
   pl.Gw = f.take(P * d.tp * d.tp * 4);
   pl.Gc = f.take(P * d.tp * d.tp * 4);
   pl.dinv = f.take(P * d.tp * 64 * 4);   // one 64 x 64 inverse per diagonal block
-  pl.lsplit = f.take(P * 3 * d.tp * 256 * 2);   // fp16 hi / lo planes and row scales of one 256-column panel
+  pl.lsplit = f.take(P * (4 * d.tp * d.tp + 8 * d.tp));   // L's fp16 hi / lo planes, row shifts and scales
   pl.h = f.take(P * d.tp * 8);
   pl.w = f.take(P * d.tp * 8);
   pl.y = f.take(P * d.tp * 8);

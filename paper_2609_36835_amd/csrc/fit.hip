@@ -474,18 +474,19 @@ __global__ void __launch_bounds__(256) k_chol_upd(float *__restrict__ Gw, int64_
     }
 }
 
-// G[K1 + r][K1 + c] -= acc s_r s_c for the tile's entries with c <= r + 63
+// Left-looking update of the column panel K0 .. K0 + 255:
+// G[K0 + r][K0 + c] -= acc s_r s_c for the tile's entries with c <= r + 63
 // (the lower triangle, up to whole diagonal 64-blocks), s the rows' inverse
-// scales stored with the split planes by k_chol_strip (256 x 256 tiles, 512
-// threads); per row block of the wave, every old value is loaded before any
-// store so the loads pipeline.
+// scales 2^-shift (k_chol_scales; 256 x 256 tiles, 512 threads); per row
+// block of the wave, every old value is loaded before any store so the loads
+// pipeline.
 template <int TM, int TN>
 struct EpiCholUpd {
   float *G;
   int64_t ld;
-  int K1;
+  int K0;
   const int32_t *info;
-  const float *rs;        // inverse scales of pair 0, rows from K1
+  const float *rs;        // inverse scales of pair 0, rows from K0
   int64_t rs_pair;        // floats between pairs
   __device__ __forceinline__ bool skip(int p) const { return info[p] != 0; }
   __device__ __forceinline__ void operator()(f32x16 (&acc)[TM][TN], int p, int row0, int col0, int mt, int nt,
@@ -498,7 +499,7 @@ struct EpiCholUpd {
     const float *sp = rs + (size_t)p * rs_pair;
     for (int x = threadIdx.x; x < 512; x += blockDim.x) ssc[x] = sp[(x < 256 ? mt : nt) * 256 + (x & 255)];
     __syncthreads();
-    float *Gp = G + (size_t)p * ld * ld + (size_t)K1 * ld + K1;
+    float *Gp = G + (size_t)p * ld * ld + (size_t)K0 * ld + K0;
     const int col = lane & 31, rl = row0 - mt * 256, cl = col0 - nt * 256;
 #pragma unroll
     for (int i = 0; i < TM; ++i) {
@@ -529,21 +530,19 @@ struct EpiCholUpd {
 // the panel step L_rk = A_rk L_kk^-T (as k_chol_panel), then the update of
 // the panel's later blocks j, A_rj -= L_rk L_jk^T (as k_chol_upd), with the
 // same MFMA products summed in the same order, so the values equal those of
-// the separate launches; then the rows' L is written back and split for the
-// rank-256 trailing update on fp16 MFMA: each row is scaled by a power of two
-// that brings its largest magnitude into [2^13, 2^14) and split exactly into
-// fp16 hi + lo (22 significant bits), so hi.hi + hi.lo + lo.hi is the row
-// product to about 2^-22 relative.  Split layout per pair: hi [ld][256], lo
-// [ld][256] (fp16), inverse scales [ld] (fp32; rows below K1 only).
-// A workgroup of 8 waves keeps 128 rows x 256 columns in LDS,
+// the separate launches; then the rows' L is written back and, scaled by the
+// row's power of two 2^shift[r] (k_chol_scales), split exactly into fp16
+// hi + lo planes (22 significant bits) at the panel's columns of the
+// left-looking updates' operand.  A workgroup of 8 waves keeps 128 rows x 256
+// columns in LDS,
 // so the strip is read and written once instead of once per step; each
 // 128 x 64 product is 4 x 2 waves of 32 x 32.
 constexpr int kStripRows = 128, kStripLd = 256 + 1;   // LDS row stride (floats)
 constexpr size_t kStripLds = ((size_t)kStripRows * kStripLd + (size_t)kNB * kSD) * sizeof(float);
 
-__global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))) k_chol_strip(float *__restrict__ Gw, int64_t ld, int K0,
-                                                    const float *__restrict__ dinv, f16 *__restrict__ Ls,
-                                                    const int32_t *__restrict__ info) {
+__global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2)))
+k_chol_strip(float *__restrict__ Gw, int64_t ld, int K0, const float *__restrict__ dinv, f16 *__restrict__ Lp,
+             const int32_t *__restrict__ shift, const int32_t *__restrict__ info) {
   extern __shared__ float strip_smem[];
   float *sT = strip_smem;                                  // [128][257]: the rows' 256 panel columns
   float *sB = strip_smem + (size_t)kStripRows * kStripLd;  // [64][65]: D_k or L_jk
@@ -634,44 +633,56 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2))
     }
   }
   __syncthreads();
-  // write the rows' L and their scaled fp16 split: each wave takes 16 rows
-  // (wave, wave + 8, ...), four columns per lane, and reduces the 16 row
-  // maxima together.  Row r of the split: s = 2^sh with m 2^sh < 2^14 for the
-  // row's largest magnitude m, hi = fp16(x s), lo = fp16(x s - hi), and 1 / s.
+  // write the rows' L and their split: each wave takes 16 rows (wave,
+  // wave + 8, ...), four columns per lane; x 2^sh = hi + lo with hi = fp16(x 2^sh)
+  // and lo = fp16(x 2^sh - hi)
   constexpr int kRowsPerWave = kStripRows / 8;
-  f32x4 v[kRowsPerWave];
-  float m[kRowsPerWave];
-#pragma unroll
+  const int32_t *shb = shift + (size_t)b * ld;
+  f16 *hib = Lp + (size_t)b * 2 * ld * ld, *lob = hib + (size_t)ld * ld;
+#pragma unroll 4
   for (int i = 0; i < kRowsPerWave; ++i) {
     const int rr = wave + 8 * i;
+    const int64_t r = R + rr;
+    f32x4 v;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) v[i][q] = sT[rr * kStripLd + 4 * lane + q];
-    m[i] = fmaxf(fmaxf(fabsf(v[i][0]), fabsf(v[i][1])), fmaxf(fabsf(v[i][2]), fabsf(v[i][3])));
-  }
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1)
-#pragma unroll
-    for (int i = 0; i < kRowsPerWave; ++i) m[i] = fmaxf(m[i], __shfl_xor(m[i], off, 64));
-  f16 *Lb = Ls + (size_t)b * 3 * ld * 256;
-#pragma unroll
-  for (int i = 0; i < kRowsPerWave; ++i) {
-    const int64_t r = R + wave + 8 * i;
-    *reinterpret_cast<f32x4 *>(G + (size_t)r * ld + K0 + 4 * lane) = v[i];
-    int ex = 0;
-    if (m[i] > 0.0f) frexpf(m[i], &ex);   // m = f 2^ex, f in [0.5, 1)
-    const int sh = min(14 - ex, 126);
+    for (int q = 0; q < 4; ++q) v[q] = sT[rr * kStripLd + 4 * lane + q];
+    *reinterpret_cast<f32x4 *>(G + (size_t)r * ld + K0 + 4 * lane) = v;
+    const int sh = shb[r];
     f16x4 hi, lo;
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      const float x = ldexpf(v[i][q], sh);
+      const float x = ldexpf(v[q], sh);
       hi[q] = (f16)x;
       lo[q] = (f16)(x - (float)hi[q]);
     }
-    f16 *base = Lb + (size_t)r * 256 + 4 * lane;
-    *reinterpret_cast<f16x4 *>(base) = hi;
-    *reinterpret_cast<f16x4 *>(base + (size_t)ld * 256) = lo;
-    if (lane == 0) reinterpret_cast<float *>(Lb + (size_t)2 * ld * 256)[r] = ldexpf(1.0f, -sh);
+    *reinterpret_cast<f16x4 *>(hib + (size_t)r * ld + K0 + 4 * lane) = hi;
+    *reinterpret_cast<f16x4 *>(lob + (size_t)r * ld + K0 + 4 * lane) = lo;
   }
+}
+
+// Per-row shifts of the left-looking updates' operand.  |L_rk| <= sqrt(A_rr)
+// for every k (row r of L L^T = A), so 2^sh with sqrt(A_rr) 2^sh in
+// [2^13, 2^14) keeps every scaled entry of the row below 2^14, inside fp16's
+// range with the lo part carrying the next 11 bits; one shift per row for the
+// whole factorisation lets a contraction run over all earlier panels at once.
+// shift[r] = sh, inv[r] = 2^-sh (rows of a non-positive diagonal get 0: their
+// factorisation fails at that pivot).
+__global__ void __launch_bounds__(256) k_chol_scales(const float *__restrict__ Gw, int64_t ld,
+                                                     int32_t *__restrict__ shift, float *__restrict__ inv,
+                                                     const int32_t *__restrict__ info) {
+  const int b = blockIdx.y;
+  if (info[b] != 0) return;
+  const int64_t r = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (r >= ld) return;
+  const float d = Gw[(size_t)b * ld * ld + (size_t)r * ld + r];
+  int sh = 0;
+  if (d > 0.0f && isfinite(d)) {
+    int ex = 0;
+    frexpf(sqrtf(d), &ex);   // sqrt(d) = f 2^ex, f in [0.5, 1)
+    sh = max(min(14 - ex, 126), -126);
+  }
+  shift[(size_t)b * ld + r] = sh;
+  inv[(size_t)b * ld + r] = ldexpf(1.0f, -sh);
 }
 
 // --------------------------------------------------------------- one right-hand side
@@ -1398,14 +1409,40 @@ hipError_t launch_nonfinite(const float *a, int B, int64_t per, int32_t *bad, hi
 // Factor the prepared work copy Gw in place (no ridge set-up, no escalation).
 hipError_t launch_cholesky_factor(float *Gw, const float *Gc, int B, int t, int64_t ld, float delta0, int max_esc,
                                   FitState st, float *dinv, void *lsplit, hipStream_t s) {
-  // Two-level right-looking blocking: 64-wide diagonal factor + panel solve
-  // steps inside 256-wide outer panels; inside an outer panel only its own
-  // columns are updated, and the trailing matrix is updated once per outer
-  // panel with k = 256 (a quarter of the trailing-matrix traffic of 64-wide
-  // steps).
+  // 256-wide outer panels, left-looking: before a panel is factored, one
+  // contraction applies every earlier panel to it (rows K0 .. ld, K = 3 K0 over
+  // the fp16 hi / lo planes of L), so each trailing entry is read and written
+  // once per factorisation instead of once per outer panel.  Inside the panel,
+  // 64-wide diagonal factor + panel-solve steps on its 256 x 256 diagonal block,
+  // then the fused strip kernel on the rows below, which also writes their
+  // planes for the later panels' contractions.
+  // lsplit layout (B (4 ld^2 + 8 ld) bytes): planes [B][2][ld][ld] fp16 (hi,
+  // lo), then shifts [B][ld] int32, then inverse scales [B][ld] fp32.
   constexpr int kOuter = 256;
+  f16 *Lp = reinterpret_cast<f16 *>(lsplit);
+  int32_t *shift = reinterpret_cast<int32_t *>(Lp + (size_t)B * 2 * ld * ld);
+  float *sinv = reinterpret_cast<float *>(shift + (size_t)B * ld);
+  hipLaunchKernelGGL(k_chol_scales, dim3((unsigned)((ld + 255) / 256), B), dim3(256), 0, s, Gw, ld, shift, sinv,
+                     st.info);
+  const hipError_t ea = hipFuncSetAttribute((const void *)k_chol_strip, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                            (int)kStripLds);
+  if (ea != hipSuccess) return ea;
   for (int K0 = 0; K0 < ld; K0 += kOuter) {
     const int K1 = (int)(K0 + kOuter < ld ? K0 + kOuter : ld);
+    if (K0 > 0) {
+      // A[K0.., K0..K1) -= L[K0.., 0..K0) L[K0..K1, 0..K0)^T: the three products
+      // hi.hi, hi.lo, lo.hi as one contraction over K = 3 x K0 (segments of K0
+      // columns, each reading one plane pair), 256 x 256 tiles down the panel
+      const f16 *Ar = Lp + (size_t)K0 * ld;
+      BigShape g{B, (int)(ld - K0), kOuter, 3 * K0, 2 * ld * ld, ld * ld, ld, 2 * ld * ld, ld * ld, ld, false, 4};
+      g.kseg = K0;
+      g.sega = 0u | (0u << 2) | (1u << 4);
+      g.segb = 0u | (1u << 2) | (0u << 4);
+      EpiCholUpd<2, 4> e{Gw, ld, K0, st.info, sinv + K0, ld};
+      const hipError_t err = launch_gemm_big<4, 2, 2, 4, 64, 1, 1, 2, f16>(
+          g, reinterpret_cast<const bf16 *>(Ar), reinterpret_cast<const bf16 *>(Ar), e, s);
+      if (err != hipSuccess) return err;
+    }
     // the 256 x 256 diagonal block: 64-wide steps restricted to its rows
     for (int c = K0; c < K1; c += kNB) {
       const int k = c / kNB;
@@ -1420,31 +1457,10 @@ hipError_t launch_cholesky_factor(float *Gw, const float *Gc, int B, int t, int6
                            r_lo, K1, K1, c, kNB, n_rt, n_ct, st.info);
       }
     }
-    if (K1 < ld) {
-      f16 *Ls = reinterpret_cast<f16 *>(lsplit);
-      const int64_t rows = ld - K1;
-      // the rows below: all four steps, written back once, with the split planes
-      const hipError_t ea = hipFuncSetAttribute((const void *)k_chol_strip,
-                                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)kStripLds);
-      if (ea != hipSuccess) return ea;
-      hipLaunchKernelGGL(k_chol_strip, dim3((unsigned)(rows / kStripRows), B), dim3(512), kStripLds, s, Gw, ld, K0,
-                         dinv, Ls, st.info);
-      // rank-256 trailing update on fp16 MFMA with the scaled split panel
-      // The three products hi.hi, hi.lo, lo.hi as one contraction over
-      // K = 3 x 256 (each 256-column segment reads one plane pair), so 256 x 256
-      // tiles fit the LDS.
-      BigShape g{B, (int)rows, (int)rows, 3 * kOuter, 3 * ld * 256, ld * 256, 256, 3 * ld * 256, ld * 256, 256, true,
-                 4};
-      g.kseg = kOuter;
-      g.sega = 0u | (0u << 2) | (1u << 4);
-      g.segb = 0u | (1u << 2) | (0u << 4);
-      EpiCholUpd<2, 4> e{Gw, ld, K1, st.info,
-                         reinterpret_cast<const float *>(Ls + (size_t)2 * ld * 256) + K1, 3 * ld * 256 / 2};
-      const hipError_t err = launch_gemm_big<4, 2, 2, 4, 64, 1, 1, 2, f16>(
-          g, reinterpret_cast<const bf16 *>(Ls + (size_t)K1 * 256), reinterpret_cast<const bf16 *>(Ls + (size_t)K1 * 256),
-          e, s);
-      if (err != hipSuccess) return err;
-    }
+    // the rows below: all four steps, written back once, with their planes
+    if (K1 < ld)
+      hipLaunchKernelGGL(k_chol_strip, dim3((unsigned)((ld - K1) / kStripRows), B), dim3(512), kStripLds, s, Gw, ld,
+                         K0, dinv, Lp, shift, st.info);
   }
   (void)Gc;
   (void)delta0;
