@@ -712,11 +712,40 @@ __global__ void __launch_bounds__(256) k_trsv_step(const float *__restrict__ Gw,
   const double *src = (FWD && j == 0) ? rhs + (size_t)b * ld : work + (size_t)b * ld;
   if (tid < kNB) sv[tid] = src[(size_t)j * kNB + tid];
   __syncthreads();
+  if constexpr (FWD) {
+    // row-major tiles: four lanes per row, each over 16 contiguous columns
+    // (16-byte loads); a lane's partial is the sum the column-quarter took in
+    // the transposed form, and the quarters meet in the same order
+    const int rr = tid >> 2, qs = tid & 3;
+    auto rowdot = [&](const float *row, const double *vec) {
+      double pr = 0.0;
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        const f32x4 v = *reinterpret_cast<const f32x4 *>(row + 16 * qs + 4 * c);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) pr += (double)v[q] * vec[16 * qs + 4 * c + q];
+      }
+      const double p1 = __shfl_down(pr, 1, 4), p2 = __shfl_down(pr, 2, 4), p3 = __shfl_down(pr, 3, 4);
+      return ((pr + p1) + p2) + p3;   // valid in the row's first lane
+    };
+    const double sr = rowdot(D + rr * kNB, sv);
+    if (qs == 0) sol[rr] = sr;
+    __syncthreads();
+    if (g == 0 && tid < kNB) out[(size_t)b * ld + (size_t)j * kNB + tid] = sol[tid];
+    if (!has_target) return;
+    const double ur = rowdot(L + ((size_t)i * kNB + rr) * ld + (size_t)j * kNB, sol);
+    if (qs == 0) {
+      const size_t e = (size_t)b * ld + (size_t)i * kNB + rr;
+      const double base = j == 0 ? rhs[e] : work[e];
+      work[e] = base - ur;
+    }
+    return;
+  }
   double part = 0.0;
 #pragma unroll
   for (int e = 0; e < 16; ++e) {
     const int q = 16 * wave + e;
-    part += (double)(FWD ? D[lane * kNB + q] : D[q * kNB + lane]) * sv[q];
+    part += (double)D[q * kNB + lane] * sv[q];
   }
   red[wave][lane] = part;
   __syncthreads();
@@ -731,16 +760,13 @@ __global__ void __launch_bounds__(256) k_trsv_step(const float *__restrict__ Gw,
 #pragma unroll
   for (int e = 0; e < 16; ++e) {
     const int q = 16 * wave + e;
-    const float l = FWD ? L[((size_t)i * kNB + lane) * ld + (size_t)j * kNB + q]
-                        : L[((size_t)j * kNB + q) * ld + (size_t)i * kNB + lane];
-    part += (double)l * sol[q];
+    part += (double)L[((size_t)j * kNB + q) * ld + (size_t)i * kNB + lane] * sol[q];
   }
   red[wave][lane] = part;     // red is free: every thread read it before the last barrier
   __syncthreads();
   if (tid < kNB) {
     const size_t e = (size_t)b * ld + (size_t)i * kNB + tid;
-    const double base = (FWD && j == 0) ? rhs[e] : work[e];
-    work[e] = base - (red[0][tid] + red[1][tid] + red[2][tid] + red[3][tid]);
+    work[e] = work[e] - (red[0][tid] + red[1][tid] + red[2][tid] + red[3][tid]);
   }
 }
 
