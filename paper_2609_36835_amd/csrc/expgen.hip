@@ -21,6 +21,7 @@
 #include "common.hpp"
 
 namespace arckv {
+typedef __attribute__((__vector_size__(4 * sizeof(uint32_t)))) uint32_t u32x4;
 
 enum { MODE_PROFILE = 0, MODE_PHIC = 1 };
 
@@ -393,7 +394,9 @@ __global__ void __launch_bounds__(256, 2) k_expgen_bf16(const bf16 *__restrict__
 #pragma unroll
       for (int pass = 0; pass < 4; ++pass) {             // 32 rows x 8 chunks of 16 B
         const int chunk = pass * 64 + lane, r = chunk / 8, c8 = (chunk % 8) * 8;
-        *reinterpret_cast<bf16x8 *>(prow[pass] + i0 + c8) = *reinterpret_cast<const bf16x8 *>(&sb[r * SO_H + c8]);
+        // E^T is written once and read back much later: streaming stores
+        __builtin_nontemporal_store(*reinterpret_cast<const u32x4 *>(&sb[r * SO_H + c8]),
+                                    reinterpret_cast<u32x4 *>(prow[pass] + i0 + c8));
       }
       wave_fence();
     } else {
