@@ -103,6 +103,9 @@ hipError_t launch_transpose128(int dtype, const float *in, int B, int rows, int6
                                void *out, int64_t out_pair, hipStream_t s);
 hipError_t launch_trsm(bool fwd, const float *Gw, const float *dinv, int B, int64_t ld, const float *R, float *X,
                        const int32_t *info, hipStream_t s);
+hipError_t launch_trsm_fwd_blocked(const float *Gw, const float *dinv, const void *lsplit, int B, int64_t ld,
+                                   const float *R, float *Y, const float *lam, const int32_t *info, void *tw,
+                                   hipStream_t s);
 hipError_t launch_add(float *x, const float *dx, int B, int64_t n_per, const int32_t *info, hipStream_t s);
 hipError_t launch_values_out(const float *Xp, int B, int64_t tp, int t, const int32_t *info, float *Cv,
                              hipStream_t s);
@@ -226,7 +229,7 @@ struct Plan {
   int64_t Et, U, Ua, anorm, pn, part1, part2, part3, fcnt, fkey, foff, fn, pcnt, pool, psim, dcnt, dkey, dn,
       doff, goff, dgrp, dgn, dsim, dr, ditem;   // merge phase
   int64_t offsets, cursor, perm;
-  int64_t PhiT, LT, Gw, Gc, dinv, lsplit, h, w, y, x, res, sw, rprev, div, u, YT, Bm, X, R, Y2, XT, Pm, UT;  // fit phase
+  int64_t PhiT, LT, Gw, Gc, dinv, lsplit, tw, h, w, y, x, res, sw, rprev, div, u, YT, Bm, X, R, Y2, XT, Pm, UT;  // fit phase
   int64_t nF, nidx, nbidx, npos, nnf, nnb, nstate, nred, ny, nrhs, ndx;   // exact NNLS (bias_mode 1)
   int64_t chunk_bytes;
 };
@@ -292,6 +295,7 @@ static Plan make_plan(const Dims &d, int64_t P) {
   pl.Gc = f.take(P * d.tp * d.tp * 4);
   pl.dinv = f.take(P * d.tp * 64 * 4);   // one 64 x 64 inverse per diagonal block
   pl.lsplit = f.take(P * (4 * d.tp * d.tp + 8 * d.tp));   // L's fp16 hi / lo planes, row shifts and scales
+  pl.tw = f.take(P * (4 * kHeadDimH * d.tp + 4 * kHeadDimH + 8));   // forward solve: Y^T planes, column scales, flags
   pl.h = f.take(P * d.tp * 8);
   pl.w = f.take(P * d.tp * 8);
   pl.y = f.take(P * d.tp * 8);
@@ -559,7 +563,9 @@ static arckv_status run_fit_values_chunk(const Ctx &c, int b0, int P, const floa
                                    c.chunk<char>(c.pl.lsplit), bad, c.pers<int32_t>(c.pl.cnt), stream));
   {
     StageScope _sc(ST_SOLVE_V, stream);
-    if (launch_trsm(true, Gw, dinv, P, d.tp, Bm, Y2, st.info, stream) != hipSuccess) return ARCKV_ERR_HIP;
+    void *lsp = c.chunk<char>(c.pl.lsplit), *tw = c.chunk<char>(c.pl.tw);
+    if (launch_trsm_fwd_blocked(Gw, dinv, lsp, P, d.tp, Bm, Y2, st.lam, st.info, tw, stream) != hipSuccess)
+      return ARCKV_ERR_HIP;
     if (launch_trsm(false, Gw, dinv, P, d.tp, Y2, X, st.info, stream) != hipSuccess) return ARCKV_ERR_HIP;
     // refinement against the data: R = P^T (Y - P X) - lam X
     for (int it = 0; it < fp.value_refine_steps; ++it) {
@@ -568,7 +574,8 @@ static arckv_status run_fit_values_chunk(const Ctx &c, int b0, int P, const floa
         return ARCKV_ERR_HIP;
       if (launch_value_residual(d.dtype, XT, Pm, PT, Yc, UT, X, st.lam, R, P, d.n, d.tp, d.np_, stream) != hipSuccess)
         return ARCKV_ERR_HIP;
-      if (launch_trsm(true, Gw, dinv, P, d.tp, R, Y2, st.info, stream) != hipSuccess) return ARCKV_ERR_HIP;
+      if (launch_trsm_fwd_blocked(Gw, dinv, lsp, P, d.tp, R, Y2, st.lam, st.info, tw, stream) != hipSuccess)
+        return ARCKV_ERR_HIP;
       if (launch_trsm(false, Gw, dinv, P, d.tp, Y2, R, st.info, stream) != hipSuccess) return ARCKV_ERR_HIP;
       if (launch_add(X, R, P, d.tp * kHeadDimH, st.info, stream) != hipSuccess) return ARCKV_ERR_HIP;
     }

@@ -1150,6 +1150,202 @@ __global__ void __launch_bounds__(256) k_trsm_mfma(const float *__restrict__ Gw,
   }
 }
 
+// ---------------------------------------------------------------- blocked forward solve
+// L Y = R for 128 right-hand sides in 256-row blocks kb: the contribution of the
+// earlier blocks, L[kb, 0:kb] Y[0:kb], is one contraction on fp16 MFMA over the
+// factorisation's hi / lo planes of L (row r scaled by 2^shift[r]) and hi / lo
+// planes of Y^T (column c scaled by 2^e_c), the three products hi.hi, hi.lo,
+// lo.hi as in the left-looking update (about 2^-22 relative); the 256 x 256
+// diagonal block is then solved by one workgroup per pair with the stored
+// 64 x 64 inverses on fp32 MFMA.  Pairs flagged here are solved again by the
+// fp32 kernel (k_trsm_mfma).
+
+// e_c with 2 ||R_c|| / sqrt(lam) 2^e_c < 2^10: |Y_rc| <= ||R_c|| / sigma_min(L)
+// and sigma_min(L)^2 is about the smallest eigenvalue of the ridged Gram, at
+// least lam, so the scaled values keep 2^6 of headroom under fp16's largest.
+// A pair without a ridge, or with a non-finite right-hand side, is flagged.
+__global__ void __launch_bounds__(1024) k_trsm_colexp(const float *__restrict__ R, int64_t ld,
+                                                      const float *__restrict__ lam, const int32_t *__restrict__ info,
+                                                      int32_t *__restrict__ ex, int32_t *__restrict__ flag) {
+  __shared__ double part[8][kHeadDim];
+  const int b = blockIdx.x, tid = threadIdx.x, c = tid & (kHeadDim - 1), g = tid >> 7;
+  if (info[b] != 0) return;
+  // eight row groups per column, eight loads in flight per thread
+  const float *Rb = R + (size_t)b * ld * kHeadDim + c;
+  double ss = 0.0;
+#pragma unroll 8
+  for (int64_t r = g; r < ld; r += 8) {
+    const double v = Rb[r * kHeadDim];
+    ss = fma(v, v, ss);
+  }
+  part[g][c] = ss;
+  if (tid == 0) flag[b] = 0;
+  __syncthreads();
+  if (g != 0) return;
+  ss = 0.0;
+#pragma unroll
+  for (int q = 0; q < 8; ++q) ss += part[q][c];
+  const float lb = lam[b];
+  const double bound = lb > 0.0f ? 2.0 * sqrt(ss) / sqrt((double)lb) : INFINITY;
+  int e = 0;
+  const bool ok = isfinite(bound);
+  if (ok && bound > 0.0) {
+    int x = 0;
+    frexp(bound, &x);   // bound < 2^x
+    e = max(min(10 - x, 126), -126);
+  }
+  ex[(size_t)b * kHeadDim + c] = e;
+  if (!ok) flag[b] = 1;
+}
+
+// Y[r0 + m][c] = R[r0 + m][c] - acc 2^-shift[r0 + m] 2^-e_c for one 256-row block
+// (tile rows m, columns c < 128).
+template <int TM, int TN>
+struct EpiTrsmFwd {
+  const float *R;
+  float *Y;
+  int64_t ld;
+  int r0;
+  const float *sinv;     // L's inverse row scales [P][ld]
+  const int32_t *ex;     // [P][128]
+  const int32_t *info, *flag;
+  __device__ __forceinline__ bool skip(int p) const { return info[p] != 0 || flag[p] != 0; }
+  __device__ __forceinline__ void operator()(f32x16 (&acc)[TM][TN], int p, int row0, int col0, int, int, int lane,
+                                             int, int) const {
+    const int col = lane & 31;
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+      const int c = col0 + 32 * j + col;
+      const float sc = ldexpf(1.0f, -ex[(size_t)p * kHeadDim + c]);
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int64_t r = r0 + row0 + 32 * i + acc_row(v, lane);
+          const size_t o = ((size_t)p * ld + r) * kHeadDim + c;
+          Y[o] = R[o] - acc[i][j][v] * (sinv[(size_t)p * ld + r] * sc);
+        }
+    }
+  }
+};
+
+// One 256-row block per pair: right-hand sides rows r0 .. r0 + 255 (src), four
+// 64-row steps y_s = D_s r_s with r_s' -= L_s's y_s for the later steps s'
+// (right-looking inside the block, the right-hand sides held in registers:
+// wave (wm, wn) owns rows 32 wm and columns 32 wn of every 64-row step).  Writes
+// Y (fp32) and the planes of Y^T for the later blocks' contractions; a scaled
+// value at or above 2^15 flags the pair.
+__global__ void __launch_bounds__(512) k_trsm_fwd_blk(const float *__restrict__ Gw, const float *__restrict__ dinv,
+                                                      int64_t ld, int kb, const float *__restrict__ src,
+                                                      float *__restrict__ Y, f16 *__restrict__ Yt,
+                                                      const int32_t *__restrict__ ex,
+                                                      const int32_t *__restrict__ info, int32_t *__restrict__ flag) {
+  constexpr int SY = 160;             // row stride of the [64][128] operand: the two half-waves on opposite banks
+  __shared__ float sD[kNB * kSD];      // D_s, then L_s's
+  __shared__ float sY[kNB * SY];       // r_s, then y_s, [k][c]
+  const int b = blockIdx.x;
+  if (info[b] != 0 || flag[b] != 0) return;   // uniform over the workgroup
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 2, wn = wave & 3, h = lane >> 5, col = lane & 31;
+  const int nb = (int)(ld / kNB);
+  const int64_t r0 = (int64_t)kb * 256;
+  const float *L = Gw + (size_t)b * ld * ld;
+  const int c = 32 * wn + col;
+  const int e = ex[(size_t)b * kHeadDim + c];
+  f32x16 rt[4];
+#pragma unroll
+  for (int s = 0; s < 4; ++s)
+#pragma unroll
+    for (int v = 0; v < 16; ++v)
+      rt[s][v] = src[((size_t)b * ld + r0 + 64 * s + 32 * wm + acc_row(v, lane)) * kHeadDim + c];
+  auto stage = [&](const float *A, int64_t lda) {   // a 64 x 64 operand into sD, row-major
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const int g = tid + 512 * q, i = g >> 4, c4 = (g & 15) * 4;
+      const f32x4 v = *reinterpret_cast<const f32x4 *>(A + (size_t)i * lda + c4);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) sD[i * kSD + c4 + u] = v[u];
+    }
+  };
+  auto product = [&]() {   // this wave's 32 x 32 block of sD x sY
+    f32x16 acc = zero16();
+#pragma unroll 8
+    for (int ks = 0; ks < kNB / 2; ++ks)
+      acc = Mfma<float>::mma(sD[(32 * wm + col) * kSD + 2 * ks + h], sY[(2 * ks + h) * SY + c], acc);
+    return acc;
+  };
+  bool over = false;
+#pragma unroll
+  for (int s = 0; s < 4; ++s) {
+    __syncthreads();
+#pragma unroll
+    for (int v = 0; v < 16; ++v) sY[(32 * wm + acc_row(v, lane)) * SY + c] = rt[s][v];
+    stage(dinv + ((size_t)b * nb + 4 * kb + s) * kNB * kNB, kNB);
+    __syncthreads();
+    const f32x16 y = product();
+    __syncthreads();
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int64_t r = r0 + 64 * s + 32 * wm + acc_row(v, lane);
+      sY[(32 * wm + acc_row(v, lane)) * SY + c] = y[v];
+      Y[((size_t)b * ld + r) * kHeadDim + c] = y[v];
+    }
+    // planes of Y^T: rows 8 g + 4 h .. + 3 of this lane are four consecutive r
+    f16 *hi = Yt + ((size_t)b * 2 * kHeadDim + c) * ld + r0 + 64 * s + 32 * wm + 4 * h;
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      f16x4 xh, xl;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const float x = ldexpf(y[4 * g + u], e);
+        over |= !(fabsf(x) < 32768.0f);
+        xh[u] = (f16)x;
+        xl[u] = (f16)(x - (float)xh[u]);
+      }
+      *reinterpret_cast<f16x4 *>(hi + 8 * g) = xh;
+      *reinterpret_cast<f16x4 *>(hi + (size_t)kHeadDim * ld + 8 * g) = xl;
+    }
+#pragma unroll
+    for (int s2 = s + 1; s2 < 4; ++s2) {
+      __syncthreads();   // every wave is done with sD; sY holds y_s
+      stage(L + (size_t)(r0 + 64 * s2) * ld + r0 + 64 * s, ld);
+      __syncthreads();
+      const f32x16 u = product();
+#pragma unroll
+      for (int v = 0; v < 16; ++v) rt[s2][v] -= u[v];
+    }
+  }
+  if (over) flag[b] = 1;
+}
+
+// After the blocked solve: a column whose largest scaled value |Y_rc| 2^e_c is
+// below 2^-6 (a bound far above the solution) kept fewer than about 18
+// significant bits in its planes; its pair is flagged for the fp32 solve.
+__global__ void __launch_bounds__(1024) k_trsm_colcheck(const float *__restrict__ Y, int64_t ld,
+                                                        const int32_t *__restrict__ ex,
+                                                        const int32_t *__restrict__ info, int32_t *__restrict__ flag) {
+  __shared__ float part[8][kHeadDim];
+  const int b = blockIdx.x, tid = threadIdx.x, c = tid & (kHeadDim - 1), g = tid >> 7;
+  if (info[b] != 0 || flag[b] != 0) return;   // uniform over the workgroup
+  const float *Yb = Y + (size_t)b * ld * kHeadDim + c;
+  float m = 0.0f;
+#pragma unroll 8
+  for (int64_t r = g; r < ld; r += 8) m = fmaxf(m, fabsf(Yb[r * kHeadDim]));
+  part[g][c] = m;
+  __syncthreads();
+  if (g != 0) return;
+#pragma unroll
+  for (int q = 1; q < 8; ++q) m = fmaxf(m, part[q][c]);
+  if (m > 0.0f && ldexpf(m, ex[(size_t)b * kHeadDim + c]) < 0.015625f) flag[b] = 1;
+}
+
+// out[b] = 1 where the fp32 solve must skip pair b (failed, or solved above)
+__global__ void k_trsm_fallback_mask(const int32_t *__restrict__ info, const int32_t *__restrict__ flag, int B,
+                                     int32_t *__restrict__ out) {
+  const int b = blockIdx.x * 256 + threadIdx.x;
+  if (b < B) out[b] = (info[b] != 0 || flag[b] == 0) ? 1 : 0;
+}
+
 __global__ void __launch_bounds__(256) k_add_copy(float *__restrict__ x, const float *__restrict__ dx, int64_t n_per,
                                                   const int32_t *__restrict__ info) {
   const int b = blockIdx.y;
@@ -1640,6 +1836,42 @@ hipError_t launch_trsm(bool fwd, const float *Gw, const float *dinv, int B, int6
   else
     hipLaunchKernelGGL(k_trsm_mfma<false>, grid, dim3(256), 0, s, Gw, ld, dinv, R, X, info);
   return hipGetLastError();
+}
+
+// Blocked forward solve L Y = R (see k_trsm_fwd_blk) with the fp32 solve for the
+// pairs it flags.  lsplit holds the factorisation's planes, shifts and inverse
+// scales (launch_cholesky_factor); tw: Y^T planes [B][2][128][ld] fp16, then
+// e [B][128], flags [B] and the fallback mask [B] (int32).
+hipError_t launch_trsm_fwd_blocked(const float *Gw, const float *dinv, const void *lsplit, int B, int64_t ld,
+                                   const float *R, float *Y, const float *lam, const int32_t *info, void *tw,
+                                   hipStream_t s) {
+  const f16 *Lp = reinterpret_cast<const f16 *>(lsplit);
+  const float *sinv = reinterpret_cast<const float *>(reinterpret_cast<const int32_t *>(Lp + (size_t)B * 2 * ld * ld) +
+                                                      (size_t)B * ld);
+  f16 *Yt = reinterpret_cast<f16 *>(tw);
+  int32_t *ex = reinterpret_cast<int32_t *>(Yt + (size_t)B * 2 * kHeadDim * ld);
+  int32_t *flag = ex + (size_t)B * kHeadDim;
+  int32_t *mask = flag + B;
+  hipLaunchKernelGGL(k_trsm_colexp, dim3(B), dim3(1024), 0, s, R, ld, lam, info, ex, flag);
+  const int nblk = (int)(ld / 256);
+  for (int kb = 0; kb < nblk; ++kb) {
+    if (kb > 0) {
+      const int K0 = 256 * kb;
+      BigShape g{B, 256, kHeadDim, 3 * K0, 2 * ld * ld, ld * ld, ld, 2 * kHeadDim * ld, kHeadDim * ld, ld, false, 1};
+      g.kseg = K0;
+      g.sega = 0u | (0u << 2) | (1u << 4);
+      g.segb = 0u | (1u << 2) | (0u << 4);
+      EpiTrsmFwd<2, 2> e{R, Y, ld, K0, sinv, ex, info, flag};
+      const hipError_t err = launch_gemm_big<4, 2, 2, 2, 64, 1, 1, 2, f16>(
+          g, reinterpret_cast<const bf16 *>(Lp + (size_t)K0 * ld), reinterpret_cast<const bf16 *>(Yt), e, s);
+      if (err != hipSuccess) return err;
+    }
+    hipLaunchKernelGGL(k_trsm_fwd_blk, dim3(B), dim3(512), 0, s, Gw, dinv, ld, kb, kb == 0 ? R : Y, Y, Yt, ex, info,
+                       flag);
+  }
+  hipLaunchKernelGGL(k_trsm_colcheck, dim3(B), dim3(1024), 0, s, Y, ld, ex, info, flag);
+  hipLaunchKernelGGL(k_trsm_fallback_mask, dim3((B + 255) / 256), dim3(256), 0, s, info, flag, B, mask);
+  return launch_trsm(true, Gw, dinv, B, ld, R, Y, mask, s);
 }
 
 hipError_t launch_add(float *x, const float *dx, int B, int64_t n_per, const int32_t *info, hipStream_t s) {
