@@ -30,6 +30,7 @@
 #include "common.hpp"
 
 namespace arckv {
+typedef __attribute__((__vector_size__(4 * sizeof(double)))) double f64x4;
 
 constexpr double kU32 = 5.9604644775390625e-08;   // 2^-24, unit roundoff of fp32
 constexpr double kU16 = 4.8828125e-04;            // 2^-11, unit roundoff of fp16
@@ -933,10 +934,13 @@ __global__ void __launch_bounds__(256) k_assign_exact(const E *__restrict__ Q, c
         const f32x4 w = v < nv ? load4(K + ((size_t)b * T + vpos[v]) * kHeadDim + k) : f32x4{0.f, 0.f, 0.f, 0.f};
         *reinterpret_cast<f32x4 *>(&sK[v * SK + k]) = w;
       }
-      if (tid < NV) {
-        vdot[tid] = 0.0;
-        vnn[tid] = 0.0;
-      }
+      __syncthreads();   // sK and the batch's vectors are published
+      // Running sums of vector rv: eight lanes per vector (queries 8 rq .. 8 rq + 7
+      // of each tile), combined in a fixed tree and kept by the first lane.
+      const int rv = tid >> 3, rq = tid & 7;
+      const int vo = rv < nv ? vown[rv] : -1;
+      double acc_d = 0.0, acc_n = 0.0;
+      const int lane = tid & 63, wave = tid >> 6, lr = lane & 15, lk = lane >> 4;
       for (int i0 = 0; i0 < n; i0 += NQ) {
         __syncthreads();
         for (int x = tid; x < NQ * kHeadDim / 4; x += 256) {
@@ -945,43 +949,52 @@ __global__ void __launch_bounds__(256) k_assign_exact(const E *__restrict__ Q, c
           *reinterpret_cast<f32x4 *>(&sQ[q * SK + k]) = w;
         }
         __syncthreads();
-        double l[2][4];
+        // logits on fp64 MFMA (16 x 16 x 4): wave w owns queries 16 w .. 16 w + 15
+        // of the tile and both 16-vector halves; each lane supplies k = 16 g + 4 lk + u
+        // to the four products of group g (bf16 / fp32 values are exact in fp64)
+        f64x4 c0 = {0.0, 0.0, 0.0, 0.0}, c1 = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll 2
+        for (int g = 0; g < kHeadDim / 16; ++g) {
+          const f32x4 a0 = *reinterpret_cast<const f32x4 *>(&sK[lr * SK + 16 * g + 4 * lk]);
+          const f32x4 a1 = *reinterpret_cast<const f32x4 *>(&sK[(16 + lr) * SK + 16 * g + 4 * lk]);
+          const f32x4 bq = *reinterpret_cast<const f32x4 *>(&sQ[(16 * wave + lr) * SK + 16 * g + 4 * lk]);
 #pragma unroll
-        for (int a = 0; a < 2; ++a)
-#pragma unroll
-          for (int m = 0; m < 4; ++m) l[a][m] = 0.0;
-        for (int k = 0; k < kHeadDim; k += 4) {
-          const f32x4 k0 = *reinterpret_cast<const f32x4 *>(&sK[tv * SK + k]);
-          const f32x4 k1 = *reinterpret_cast<const f32x4 *>(&sK[(tv + 16) * SK + k]);
-#pragma unroll
-          for (int m = 0; m < 4; ++m) {
-            const f32x4 qv = *reinterpret_cast<const f32x4 *>(&sQ[(tq + 16 * m) * SK + k]);
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              l[0][m] = fma((double)k0[e], (double)qv[e], l[0][m]);
-              l[1][m] = fma((double)k1[e], (double)qv[e], l[1][m]);
-            }
+          for (int u = 0; u < 4; ++u) {
+            c0 = __builtin_amdgcn_mfma_f64_16x16x4f64((double)a0[u], (double)bq[u], c0, 0, 0, 0);
+            c1 = __builtin_amdgcn_mfma_f64_16x16x4f64((double)a1[u], (double)bq[u], c1, 0, 0, 0);
           }
         }
+        // lane holds vectors 4 r + lk (and + 16) for query 16 w + lr
 #pragma unroll
-        for (int a = 0; a < 2; ++a)
-#pragma unroll
-          for (int m = 0; m < 4; ++m) {
-            const int v = tv + 16 * a, q = tq + 16 * m;
-            sE[v * (NQ + 1) + q] = v < nv && i0 + q < n ? exp(s * l[a][m] - zm) : 0.0;
-          }
+        for (int r = 0; r < 4; ++r) {
+          const int v = 4 * r + lk, q = 16 * wave + lr;
+          const bool qv = i0 + q < n;
+          sE[v * (NQ + 1) + q] = v < nv && qv ? exp(s * c0[r] - zm) : 0.0;
+          sE[(v + 16) * (NQ + 1) + q] = v + 16 < nv && qv ? exp(s * c1[r] - zm) : 0.0;
+        }
         __syncthreads();
-        if (tid < nv && vown[tid] >= 0) {
-          const int o = vown[tid];
-          double d = vdot[tid], nn = vnn[tid];
-          for (int q = 0; q < NQ; ++q) {
-            const double ev = sE[tid * (NQ + 1) + q];
-            d = fma(sE[o * (NQ + 1) + q], ev, d);
+        double d = 0.0, nn = 0.0;
+        if (vo >= 0) {
+#pragma unroll
+          for (int x = 0; x < 8; ++x) {
+            const int q = 8 * rq + x;
+            const double ev = sE[rv * (NQ + 1) + q];
+            d = fma(sE[vo * (NQ + 1) + q], ev, d);
             nn = fma(ev, ev, nn);
           }
-          vdot[tid] = d;
-          vnn[tid] = nn;
         }
+        d += __shfl_xor(d, 1, 64);
+        nn += __shfl_xor(nn, 1, 64);
+        d += __shfl_xor(d, 2, 64);
+        nn += __shfl_xor(nn, 2, 64);
+        d += __shfl_xor(d, 4, 64);
+        nn += __shfl_xor(nn, 4, 64);
+        acc_d += d;
+        acc_n += nn;
+      }
+      if (rq == 0) {
+        vdot[rv] = acc_d;
+        vnn[rv] = acc_n;
       }
       __syncthreads();
       if (tid == 0) {
