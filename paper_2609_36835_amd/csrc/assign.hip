@@ -26,6 +26,8 @@
 //     (k_assign_exact).  Equal float64 similarities go to the lower r.
 //
 // The bounds are stated on the functions that use them.
+#include <type_traits>
+
 #include "assign.hpp"
 #include "common.hpp"
 
@@ -941,13 +943,29 @@ __global__ void __launch_bounds__(256) k_assign_exact(const E *__restrict__ Q, c
       const int vo = rv < nv ? vown[rv] : -1;
       double acc_d = 0.0, acc_n = 0.0;
       const int lane = tid & 63, wave = tid >> 6, lr = lane & 15, lk = lane >> 4;
+      // the next query tile is loaded into registers while this one's products run
+      constexpr int QCH = NQ * kHeadDim / 4 / 256;   // groups of 4 values per thread
+      using Raw = std::conditional_t<sizeof(E) == 2, bf16x4, f32x4>;
+      Raw qn[QCH];
+      auto fetch_q = [&](int j0) {
+#pragma unroll
+        for (int c = 0; c < QCH; ++c) {
+          const int x = tid + 256 * c, q = x / (kHeadDim / 4), k = 4 * (x % (kHeadDim / 4));
+          qn[c] = j0 + q < n ? *reinterpret_cast<const Raw *>(Qb + (size_t)(j0 + q) * kHeadDim + k) : Raw{};
+        }
+      };
+      fetch_q(0);
       for (int i0 = 0; i0 < n; i0 += NQ) {
-        __syncthreads();
-        for (int x = tid; x < NQ * kHeadDim / 4; x += 256) {
-          const int q = x / (kHeadDim / 4), k = 4 * (x % (kHeadDim / 4));
-          const f32x4 w = i0 + q < n ? load4(Qb + (size_t)(i0 + q) * kHeadDim + k) : f32x4{0.f, 0.f, 0.f, 0.f};
+        __syncthreads();   // every wave is done with the previous tile
+#pragma unroll
+        for (int c = 0; c < QCH; ++c) {
+          const int x = tid + 256 * c, q = x / (kHeadDim / 4), k = 4 * (x % (kHeadDim / 4));
+          f32x4 w;
+#pragma unroll
+          for (int u = 0; u < 4; ++u) w[u] = (float)qn[c][u];
           *reinterpret_cast<f32x4 *>(&sQ[q * SK + k]) = w;
         }
+        if (i0 + NQ < n) fetch_q(i0 + NQ);
         __syncthreads();
         // logits on fp64 MFMA (16 x 16 x 4): wave w owns queries 16 w .. 16 w + 15
         // of the tile and both 16-vector halves; each lane supplies k = 16 g + 4 lk + u
