@@ -145,14 +145,25 @@ __global__ void __launch_bounds__(256) k_prof_anchor_bf16(const bf16 *__restrict
   const bf16 *Qb = Q + (size_t)b * n * kHeadDim;
   float *urow = Ua + ((size_t)b * tp + (rvalid ? r : 0)) * np_;
   double ss = 0.0;
+  // the next 64-query tile is loaded into registers while this one is processed
+  f32x4 qn[4];
+  auto fetch_q = [&](int j0) {
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int c = tid + 256 * u, rr = c / 16, cc = (c % 16) * 8;
+      qn[u] = j0 + rr < n ? *reinterpret_cast<const f32x4 *>(Qb + (size_t)(j0 + rr) * kHeadDim + cc)
+                          : f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+  };
+  fetch_q(0);
   for (int i0 = 0; i0 < np_; i0 += 64) {
     __syncthreads();
-    for (int c = tid; c < 64 * 16; c += 256) {
-      const int rr = c / 16, cc = (c % 16) * 8;
-      f32x4 v = {0.f, 0.f, 0.f, 0.f};
-      if (i0 + rr < n) v = *reinterpret_cast<const f32x4 *>(Qb + (size_t)(i0 + rr) * kHeadDim + cc);
-      *reinterpret_cast<f32x4 *>(&sQ[rr * SQ + cc]) = v;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int c = tid + 256 * u, rr = c / 16, cc = (c % 16) * 8;
+      *reinterpret_cast<f32x4 *>(&sQ[rr * SQ + cc]) = qn[u];
     }
+    if (i0 + 64 < np_) fetch_q(i0 + 64);
     __syncthreads();
 #pragma unroll
     for (int ms = 0; ms < 2; ++ms) {
