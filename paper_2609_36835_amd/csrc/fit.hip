@@ -976,17 +976,35 @@ __global__ void __launch_bounds__(256) k_phat(const float *__restrict__ LT, cons
   T *Pm = reinterpret_cast<T *>(outm) + (size_t)b * PL * tp * np_;
   constexpr int EPV = 16 / sizeof(T);                     // elements per 16-byte store
   typedef __attribute__((ext_vector_type(4))) uint32_t u32x4;
+  // this wave's 16 keys of the next tile: logits and biases loaded while the
+  // current tile is stored
+  float ln[16], bn[16];
+  auto fetch_l = [&](int64_t q0) {
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      const int64_t r = q0 + 16 * wave + e;
+      const bool ok = i < n && r < t;
+      ln[e] = ok ? L[(size_t)r * np_] : 0.0f;
+      bn[e] = ok ? bb[r] : 0.0f;
+    }
+  };
+  fetch_l(0);
   for (int64_t r0 = 0; r0 < tp; r0 += 64) {
     __syncthreads();   // the previous tile's stores have read sp
+    float lc[16], bc[16];
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      lc[e] = ln[e];
+      bc[e] = bn[e];
+    }
+    if (r0 + 64 < tp) fetch_l(r0 + 64);
 #pragma unroll
     for (int e4 = 0; e4 < 16; e4 += 4) {   // four consecutive keys per LDS write
       float pv[4];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const int64_t r = r0 + 16 * wave + e4 + e;
-        pv[e] = (i < n && r < t)
-                    ? __builtin_amdgcn_exp2f((L[(size_t)r * np_] + bb[r] - M) * kLog2e) * inv
-                    : 0.0f;
+        pv[e] = (i < n && r < t) ? __builtin_amdgcn_exp2f((lc[e4 + e] + bc[e4 + e] - M) * kLog2e) * inv : 0.0f;
       }
       const int rr = 16 * wave + e4;
       if constexpr (PL == 2) {
