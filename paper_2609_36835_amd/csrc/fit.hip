@@ -7,8 +7,8 @@
 //   Cholesky         right-looking, float32, two-level blocking over
 //                    256-wide outer panels:
 //                      k_chol_diag    factor a 64 x 64 diagonal block and
-//                                     invert it (256 threads, a quarter row
-//                                     each, one barrier per column)
+//                                     invert it (1024 threads, four entries
+//                                     of a row each, one barrier per column)
 //                      k_chol_panel   L_ik = A_ik L_kk^-T inside the panel's
 //                                     256 x 256 diagonal block (fp32 MFMA
 //                                     with the inverse)
@@ -210,6 +210,11 @@ __global__ void __launch_bounds__(256) k_nonfinite(const float *__restrict__ a, 
 // Factor the 64 x 64 diagonal block k in place and write L_kk^-1 to
 // dinv[b][k] (one workgroup of 256 threads per pair).  Thread (r, cls) with
 // r = tid / 4, cls = tid % 4 keeps A[r][4j + cls] (j < 16) in registers.
+// Threads of k_chol_diag: 64 rows x kDiagCls column classes, each thread
+// holding kDiagPer entries of its row (four waves per SIMD hide each other's
+// latency along the per-column dependence chain).
+constexpr int kDiagCls = 16, kDiagPer = kNB / kDiagCls, kDiagThreads = kNB * kDiagCls;
+
 // Right-looking over the 64 columns c with one barrier per column: column c,
 // updated through column c - 1 but not yet scaled, sits in LDS (its owners
 // publish it right after their own update of step c - 1), so every thread
@@ -222,16 +227,16 @@ __global__ void __launch_bounds__(256) k_nonfinite(const float *__restrict__ a, 
 // order with the same products and fused multiply-adds as a plain
 // column-by-column factorisation and row-by-row substitution.  A failed pivot
 // records info = column + 1 and leaves the block and dinv unwritten.
-__global__ void __launch_bounds__(256) k_chol_diag(float *__restrict__ Gw, int64_t ld, int k,
+__global__ void __launch_bounds__(kDiagThreads) k_chol_diag(float *__restrict__ Gw, int64_t ld, int k,
                                                    int32_t *__restrict__ info, float *__restrict__ dinv) {
   __shared__ float sA[kNB * kSD];   // column c: A updated through column c - 1, unscaled
   __shared__ float sX[kNB * kSD];   // L^-1, one row per column step
   __shared__ float sd[kNB], sdg[kNB];   // 1 / L[c][c] and L[c][c]
   const int b = blockIdx.x, tid = threadIdx.x;
   if (info[b] != 0) return;   // uniform over the workgroup
-  const int r = tid >> 2, cls = tid & 3;
+  const int r = tid / kDiagCls, cls = tid % kDiagCls;
   float *D = Gw + (size_t)b * ld * ld + (size_t)k * kNB * ld + (size_t)k * kNB;
-  for (int e = tid; e < kNB * kNB / 4; e += 256) {
+  for (int e = tid; e < kNB * kNB / 4; e += kDiagThreads) {
     const int rr = e >> 4, c4 = (e & 15) * 4;
     const f32x4 v = *reinterpret_cast<const f32x4 *>(D + (size_t)rr * ld + c4);
 #pragma unroll
@@ -239,10 +244,10 @@ __global__ void __launch_bounds__(256) k_chol_diag(float *__restrict__ Gw, int64
   }
   __syncthreads();
   // Each thread reads only its own entries, and column 0 needs no update.
-  float a[16], y[16];
+  float a[kDiagPer], y[kDiagPer];
 #pragma unroll
-  for (int j = 0; j < 16; ++j) {
-    const int q = 4 * j + cls;
+  for (int j = 0; j < kDiagPer; ++j) {
+    const int q = kDiagCls * j + cls;
     a[j] = sA[r * kSD + q];
     y[j] = q == r ? 1.0f : 0.0f;
   }
@@ -252,12 +257,12 @@ __global__ void __launch_bounds__(256) k_chol_diag(float *__restrict__ Gw, int64
   for (int c = 0; c < kNB; ++c) {
     const float piv = sA[c * kSD + c];
     const float arc = sA[r * kSD + c];
-    float col[16], xp[16];
+    float col[kDiagPer], xp[kDiagPer];
 #pragma unroll
-    for (int j = 0; j < 16; ++j) col[j] = sA[(4 * j + cls) * kSD + c];
+    for (int j = 0; j < kDiagPer; ++j) col[j] = sA[(kDiagCls * j + cls) * kSD + c];
     if (c > 0) {
 #pragma unroll
-      for (int j = 0; j < 16; ++j) xp[j] = sX[(c - 1) * kSD + 4 * j + cls];
+      for (int j = 0; j < kDiagPer; ++j) xp[j] = sX[(c - 1) * kSD + kDiagCls * j + cls];
     }
     if (!(piv > 0.0f) || !isfinite(piv)) {   // uniform: every thread read the same pivot
       fail = c + 1;
@@ -266,23 +271,23 @@ __global__ void __launch_bounds__(256) k_chol_diag(float *__restrict__ Gw, int64
     const float d = sqrtf(piv), inv = 1.0f / d;
     if (c > 0 && r >= c) {
 #pragma unroll
-      for (int j = 0; j < 16; ++j) y[j] = fmaf(-plrc, xp[j], y[j]);
+      for (int j = 0; j < kDiagPer; ++j) y[j] = fmaf(-plrc, xp[j], y[j]);
     }
     if (r == c) {
 #pragma unroll
-      for (int j = 0; j < 16; ++j) sX[c * kSD + 4 * j + cls] = y[j] * inv;
+      for (int j = 0; j < kDiagPer; ++j) sX[c * kSD + kDiagCls * j + cls] = y[j] * inv;
     }
     const float lrc = arc * inv;
     if (r > c) {
 #pragma unroll
-      for (int j = 0; j < 16; ++j) a[j] = fmaf(-lrc, col[j] * inv, a[j]);
+      for (int j = 0; j < kDiagPer; ++j) a[j] = fmaf(-lrc, col[j] * inv, a[j]);
     }
     plrc = lrc;
-    if (c + 1 < kNB && cls == ((c + 1) & 3)) {
-      const int jn = (c + 1) >> 2;
+    if (c + 1 < kNB && cls == (c + 1) % kDiagCls) {
+      const int jn = (c + 1) / kDiagCls;
       float v = a[0];
 #pragma unroll
-      for (int j = 1; j < 16; ++j) v = j == jn ? a[j] : v;
+      for (int j = 1; j < kDiagPer; ++j) v = j == jn ? a[j] : v;
       sA[r * kSD + c + 1] = v;
     }
     if (tid == 0) {
@@ -296,7 +301,7 @@ __global__ void __launch_bounds__(256) k_chol_diag(float *__restrict__ Gw, int64
     return;
   }
   float *Xi = dinv + ((size_t)b * (ld / kNB) + k) * kNB * kNB;
-  for (int e = tid; e < kNB * kNB; e += 256) {
+  for (int e = tid; e < kNB * kNB; e += kDiagThreads) {
     const int rr = e >> 6, q = e & 63;
     if (q < rr) D[(size_t)rr * ld + q] = sA[rr * kSD + q] * sd[q];
     else if (q == rr) D[(size_t)rr * ld + q] = sdg[q];
@@ -1686,7 +1691,7 @@ hipError_t launch_cholesky_factor(float *Gw, const float *Gc, int B, int t, int6
     // the 256 x 256 diagonal block: 64-wide steps restricted to its rows
     for (int c = K0; c < K1; c += kNB) {
       const int k = c / kNB;
-      hipLaunchKernelGGL(k_chol_diag, dim3(B), dim3(256), 0, s, Gw, ld, k, st.info, dinv);
+      hipLaunchKernelGGL(k_chol_diag, dim3(B), dim3(kDiagThreads), 0, s, Gw, ld, k, st.info, dinv);
       const int rem = (K1 - c) / kNB - 1;   // row blocks of the diagonal block below block k
       if (rem > 0)
         hipLaunchKernelGGL(k_chol_panel, dim3((rem + 1) / 2, B), dim3(256), 0, s, Gw, ld, k, (int64_t)K1, dinv,
