@@ -1885,7 +1885,7 @@ hipError_t launch_trsm_fwd_blocked(const float *Gw, const float *dinv, const voi
       g.sega = 0u | (0u << 2) | (1u << 4);
       g.segb = 0u | (1u << 2) | (0u << 4);
       EpiTrsmFwd<2, 2> e{R, Y, ld, K0, sinv, ex, info, flag};
-      const hipError_t err = launch_gemm_big<4, 2, 2, 2, 64, 1, 1, 2, f16>(
+      const hipError_t err = launch_gemm_big<4, 2, 2, 2, 64, 1, 1, 3, f16>(
           g, reinterpret_cast<const bf16 *>(Lp + (size_t)K0 * ld), reinterpret_cast<const bf16 *>(Yt), e, s);
       if (err != hipSuccess) return err;
     }
