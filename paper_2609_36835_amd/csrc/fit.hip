@@ -4,8 +4,14 @@
 // M a float32 Gram matrix of size tp (padded; the padding is an identity
 // block with zero right-hand side, so padded unknowns solve to 0):
 //   k_ridge_init     lam = delta * tr(M)/t, write M + lam I into the work copy
-//   Cholesky         right-looking, float32, two-level blocking over
-//                    256-wide outer panels:
+//   Cholesky         float32, left-looking over 256-wide outer panels:
+//                      k_chol_scales  per-row power-of-two shifts s_r from the
+//                                     diagonal (sqrt(A_rr) s_r in [2^13, 2^14))
+//                      (contraction)  before a panel is factored, the big
+//                                     contraction on fp16 MFMA applies every
+//                                     earlier panel to it (hi / lo planes of
+//                                     L s_r, three products, about 2^-22
+//                                     relative)
 //                      k_chol_diag    factor a 64 x 64 diagonal block and
 //                                     invert it (1024 threads, four entries
 //                                     of a row each, one barrier per column)
@@ -13,18 +19,16 @@
 //                                     256 x 256 diagonal block (fp32 MFMA
 //                                     with the inverse)
 //                      k_chol_upd     A -= L L^T inside that block (fp32 MFMA)
-//                      k_chol_strip   the rows below it: the same panel steps
+//                      k_chol_strip16 the rows below it: the same panel steps
 //                                     and updates on a 128 x 256 strip held in
-//                                     LDS, then the split planes
-//                    the rest of the matrix is updated once per outer panel by
-//                    the big contraction on fp16 MFMA, the panel scaled per row
-//                    by a power of two and split into hi + lo (three products,
-//                    about 2^-22 relative)
+//                                     LDS as hi / lo planes (fp16 MFMA), then
+//                                     L and its planes written back
 //                    a failed pivot records info = column + 1 for that pair
 //   escalation       pairs that failed are refactored by the same kernels with
 //                    delta raised tenfold (from 1e-7 when zero), at most
 //                    max_escalations times (launch_cholesky)
-//   solves           TRSV (one rhs, float64 accumulation) / TRSM (128 rhs)
+//   solves           TRSV (one rhs, float64 accumulation) / TRSM (128 rhs; the
+//                    forward one in 256-row blocks on the planes of L)
 //   residuals        rhs - (M + lam I) x, float64 (mass fit) or float32 MFMA
 //                    (value fit), for iterative refinement
 #include "common.hpp"
@@ -532,25 +536,41 @@ struct EpiCholUpd {
 
 // Rows K1 .. ld of the outer panel (columns K0 .. K1 = K0 + 256), once its
 // 256 x 256 diagonal block is factored: for each 64-column block k in order,
-// the panel step L_rk = A_rk L_kk^-T (as k_chol_panel), then the update of
-// the panel's later blocks j, A_rj -= L_rk L_jk^T (as k_chol_upd), with the
-// same MFMA products summed in the same order, so the values equal those of
-// the separate launches; then the rows' L is written back and, scaled by the
-// row's power of two 2^shift[r] (k_chol_scales), split exactly into fp16
-// hi + lo planes (22 significant bits) at the panel's columns of the
-// left-looking updates' operand.  A workgroup of 8 waves keeps 128 rows x 256
-// columns in LDS,
-// so the strip is read and written once instead of once per step; each
+// the panel step L_rk = A_rk L_kk^-T (with the stored inverse), then the
+// update of the panel's later blocks j, A_rj -= L_rk L_jk^T; then the rows' L
+// is written back with the fp16 hi / lo planes of the left-looking updates'
+// operand.  A workgroup of 8 waves keeps 128 rows x 256 columns in LDS, so
+// the strip is read and written once instead of once per step; each
 // 128 x 64 product is 4 x 2 waves of 32 x 32.
-constexpr int kStripRows = 128, kStripLd = 256 + 1;   // LDS row stride (floats)
-constexpr size_t kStripLds = ((size_t)kStripRows * kStripLd + (size_t)kNB * kSD) * sizeof(float);
+constexpr int kStripRows = 128;
+
+// k_chol_strip16: the strip on fp16 MFMA (32x32x16), every product as hi.hi + hi.lo +
+// lo.hi of fp16 planes (about 2^-22 relative, as in the trailing
+// contraction).  With s_x = 2^shift[x] (sqrt(A_xx) s_x in [2^13, 2^14)):
+//  - an entry of a block not yet factored, |A'_rc| <= sqrt(A_rr A_cc), is held
+//    as A'_rc s_r s_c 2^-14, a factored one, |L_rc| <= sqrt(A_rr), as L_rc s_r,
+//    both below 2^14, as hi / lo planes in LDS;
+//  - the B operand rows (D_k with its columns m scaled by 2^14 / s_m, or L_jk)
+//    are split after scaling each row by the power of two that brings its
+//    largest magnitude into [2^13, 2^14);
+//  - an update recombines hi + lo in fp32, subtracts and splits again.
+// The planes left in LDS are the split the left-looking contractions read,
+// and G gets (hi + lo) / s_r.  LDS rows are unpadded with their 16-byte chunks XOR-swizzled by
+// row, so each quarter-wave's fragment reads touch 16 distinct bank groups.
+constexpr size_t kStrip16Lds = ((size_t)2 * kStripRows * 256 + (size_t)2 * kNB * kNB) * sizeof(f16) +
+                               (size_t)(kNB + kStripRows + 256) * sizeof(int32_t);
 
 __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2, 2)))
-k_chol_strip(float *__restrict__ Gw, int64_t ld, int K0, const float *__restrict__ dinv, f16 *__restrict__ Lp,
-             const int32_t *__restrict__ shift, const int32_t *__restrict__ info) {
-  extern __shared__ float strip_smem[];
-  float *sT = strip_smem;                                  // [128][257]: the rows' 256 panel columns
-  float *sB = strip_smem + (size_t)kStripRows * kStripLd;  // [64][65]: D_k or L_jk
+k_chol_strip16(float *__restrict__ Gw, int64_t ld, int K0, const float *__restrict__ dinv, f16 *__restrict__ Lp,
+               const int32_t *__restrict__ shift, const int32_t *__restrict__ info) {
+  extern __shared__ __attribute__((aligned(16))) char strip16_smem[];
+  f16 *sTh = reinterpret_cast<f16 *>(strip16_smem);        // [128][256] hi
+  f16 *sTl = sTh + kStripRows * 256;                         // [128][256] lo
+  f16 *sBh = sTl + kStripRows * 256;                         // [64][64] hi
+  f16 *sBl = sBh + kNB * kNB;                                // [64][64] lo
+  int32_t *sBe = reinterpret_cast<int32_t *>(sBl + kNB * kNB);   // [64] row exponents of B
+  int32_t *sSh = sBe + kNB;                                  // [128] row shifts of the strip
+  int32_t *sShC = sSh + kStripRows;                          // [256] shifts of the panel's columns
   const int b = blockIdx.y;
   if (info[b] != 0) return;   // uniform over the workgroup
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -559,10 +579,18 @@ k_chol_strip(float *__restrict__ Gw, int64_t ld, int K0, const float *__restrict
   const int64_t R = K1 + (int64_t)blockIdx.x * kStripRows;
   float *G = Gw + (size_t)b * ld * ld;
   const int nb = (int)(ld / kNB);
-  // The ten B operands in order: step (k, k) is the panel step with D_k, step
-  // (k, j > k) the update of block j with L_jk of the diagonal block.  The next
-  // step's tile is loaded into registers while the current step's products
-  // run (two 16-byte loads per thread) and stored to sB after the barrier.
+  // element (r, c) of a plane: T rows of 32 chunks, B rows of 8 chunks
+  auto tix = [](int r, int c) { return r * 256 + 8 * ((c >> 3) ^ (r & 15)) + (c & 7); };
+  auto bix = [](int i, int m) { return i * kNB + 8 * ((m >> 3) ^ ((i >> 1) & 7)) + (m & 7); };
+  auto split4 = [](f32x4 x, f16x4 &hi, f16x4 &lo) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      hi[q] = (f16)x[q];
+      lo[q] = (f16)(x[q] - (float)hi[q]);
+    }
+  };
+  if (tid < kStripRows) sSh[tid] = shift[(size_t)b * ld + R + tid];
+  if (tid < 256) sShC[tid] = shift[(size_t)b * ld + K0 + tid];
   constexpr int kSteps = 10;
   constexpr int8_t step_k[kSteps] = {0, 0, 0, 0, 1, 1, 1, 2, 2, 3};
   constexpr int8_t step_j[kSteps] = {0, 1, 2, 3, 1, 2, 3, 2, 3, 3};
@@ -578,30 +606,50 @@ k_chol_strip(float *__restrict__ Gw, int64_t ld, int K0, const float *__restrict
       pre[c] = *reinterpret_cast<const f32x4 *>(src + (size_t)i * lds + c4);
     }
   };
-  auto stash_b = [&]() {
+  // B rows scaled by their own power of two (16 consecutive lanes hold a row);
+  // for D_k its columns first take 2^14 / s_m
+  auto stash_b = [&](int k, bool panel) {
 #pragma unroll
     for (int c = 0; c < 2; ++c) {
       const int e = tid + 512 * c, i = e >> 4, c4 = (e & 15) * 4;
+      if (panel) {
 #pragma unroll
-      for (int q = 0; q < 4; ++q) sB[i * kSD + c4 + q] = pre[c][q];
+        for (int q = 0; q < 4; ++q) pre[c][q] = ldexpf(pre[c][q], 14 - sShC[64 * k + c4 + q]);
+      }
+      float m = fmaxf(fmaxf(fabsf(pre[c][0]), fabsf(pre[c][1])), fmaxf(fabsf(pre[c][2]), fabsf(pre[c][3])));
+#pragma unroll
+      for (int o = 1; o < 16; o <<= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
+      int ex = 0;
+      if (m > 0.0f) frexpf(m, &ex);
+      const int sc = max(min(14 - ex, 126), -126);
+      f32x4 x;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) x[q] = ldexpf(pre[c][q], sc);
+      f16x4 hi, lo;
+      split4(x, hi, lo);
+      *reinterpret_cast<f16x4 *>(&sBh[bix(i, c4)]) = hi;
+      *reinterpret_cast<f16x4 *>(&sBl[bix(i, c4)]) = lo;
+      if ((e & 15) == 0) sBe[i] = sc;
     }
   };
-  // this wave's 32 x 32 block of T[:, 64 ka ..] x sB^T: rows 32 wm, columns 32 wn
-  // (operands read from LDS up front, then the 32 products in order of ks)
+  // this wave's 32 x 32 block of T[:, 64 ka ..] x B^T, in the scaled units
+  const int arow = 32 * wm + col, brow = 32 * wn + col;
   auto product = [&](int ka) {
-    float av[kNB / 2], bv[kNB / 2];
-#pragma unroll
-    for (int ks = 0; ks < kNB / 2; ++ks) {
-      av[ks] = sT[(32 * wm + col) * kStripLd + 64 * ka + 2 * ks + h];
-      bv[ks] = sB[(32 * wn + col) * kSD + 2 * ks + h];
-    }
-    __builtin_amdgcn_sched_barrier(0);
     f32x16 acc = zero16();
 #pragma unroll
-    for (int ks = 0; ks < kNB / 2; ++ks) acc = Mfma<float>::mma(av[ks], bv[ks], acc);
+    for (int ks = 0; ks < kNB / 16; ++ks) {
+      const int ca = 64 * ka + 16 * ks + 8 * h, cb = 16 * ks + 8 * h;
+      const bf16x8 ah = *reinterpret_cast<const bf16x8 *>(&sTh[tix(arow, ca)]);
+      const bf16x8 al = *reinterpret_cast<const bf16x8 *>(&sTl[tix(arow, ca)]);
+      const bf16x8 bh = *reinterpret_cast<const bf16x8 *>(&sBh[bix(brow, cb)]);
+      const bf16x8 bl = *reinterpret_cast<const bf16x8 *>(&sBl[bix(brow, cb)]);
+      acc = mma16<f16>(ah, bh, acc);
+      acc = mma16<f16>(ah, bl, acc);
+      acc = mma16<f16>(al, bh, acc);
+    }
     return acc;
   };
-  {  // the strip, 128 rows x 64 chunks of 4: every load in flight before the first LDS store
+  {  // the strip, 128 rows x 64 groups of 4, scaled by s_r s_c 2^-14 and split
     f32x4 v[kStripRows * 64 / 512];
 #pragma unroll
     for (int i = 0; i < kStripRows * 64 / 512; ++i) {
@@ -609,57 +657,67 @@ k_chol_strip(float *__restrict__ Gw, int64_t ld, int K0, const float *__restrict
       v[i] = *reinterpret_cast<const f32x4 *>(G + (size_t)(R + r) * ld + K0 + c4);
     }
     load_b(0);
+    __syncthreads();   // sSh, sShC
 #pragma unroll
     for (int i = 0; i < kStripRows * 64 / 512; ++i) {
       const int e = tid + 512 * i, r = e >> 6, c4 = (e & 63) * 4;
+      const int sh = sSh[r] - 14;
+      f32x4 x;
 #pragma unroll
-      for (int q = 0; q < 4; ++q) sT[r * kStripLd + c4 + q] = v[i][q];
+      for (int q = 0; q < 4; ++q) x[q] = ldexpf(v[i][q], sh + sShC[c4 + q]);
+      f16x4 hi, lo;
+      split4(x, hi, lo);
+      *reinterpret_cast<f16x4 *>(&sTh[tix(r, c4)]) = hi;
+      *reinterpret_cast<f16x4 *>(&sTl[tix(r, c4)]) = lo;
     }
   }
 #pragma unroll
   for (int st = 0; st < kSteps; ++st) {
     const int k = step_k[st], j = step_j[st];
-    __syncthreads();   // sT is up to date and every wave is done with sB
-    stash_b();
+    __syncthreads();   // the strip is up to date and every wave is done with sB
+    stash_b(k, j == k);
     if (st + 1 < kSteps) load_b(st + 1);
     __syncthreads();
     const f32x16 acc = product(k);
-    if (j == k) {      // panel step: L_k replaces block k once every wave has read it
+    if (j == k) {      // panel step: L_k s_r replaces block k
+      const float inv_b = ldexpf(1.0f, -sBe[brow]);
       __syncthreads();
 #pragma unroll
-      for (int v = 0; v < 16; ++v)
-        sT[(32 * wm + acc_row(v, lane)) * kStripLd + 64 * k + 32 * wn + col] = acc[v];
-    } else {           // update of block j (this wave's own entries; block k is not written)
+      for (int v = 0; v < 16; ++v) {
+        const int r = 32 * wm + acc_row(v, lane), c = 64 * k + 32 * wn + col;
+        const float x = acc[v] * inv_b;
+        const f16 hi = (f16)x;
+        sTh[tix(r, c)] = hi;
+        sTl[tix(r, c)] = (f16)(x - (float)hi);
+      }
+    } else {           // update of block j (this wave's own entries), in its units s_r s_c 2^-14
+      const float inv_b = ldexpf(1.0f, sShC[64 * j + brow] - 14 - sBe[brow]);
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
-        float &x = sT[(32 * wm + acc_row(v, lane)) * kStripLd + 64 * j + 32 * wn + col];
-        x = x - acc[v];
+        const int r = 32 * wm + acc_row(v, lane), c = 64 * j + 32 * wn + col;
+        const float x = ((float)sTh[tix(r, c)] + (float)sTl[tix(r, c)]) - acc[v] * inv_b;
+        const f16 hi = (f16)x;
+        sTh[tix(r, c)] = hi;
+        sTl[tix(r, c)] = (f16)(x - (float)hi);
       }
     }
   }
   __syncthreads();
-  // write the rows' L and their split: each wave takes 16 rows (wave,
-  // wave + 8, ...), four columns per lane; x 2^sh = hi + lo with hi = fp16(x 2^sh)
-  // and lo = fp16(x 2^sh - hi)
+  // write the rows' planes and L = (hi + lo) 2^-shift: each wave takes 16 rows,
+  // four columns per lane
   constexpr int kRowsPerWave = kStripRows / 8;
-  const int32_t *shb = shift + (size_t)b * ld;
   f16 *hib = Lp + (size_t)b * 2 * ld * ld, *lob = hib + (size_t)ld * ld;
 #pragma unroll 4
   for (int i = 0; i < kRowsPerWave; ++i) {
     const int rr = wave + 8 * i;
     const int64_t r = R + rr;
-    f32x4 v;
+    const f16x4 hi = *reinterpret_cast<const f16x4 *>(&sTh[tix(rr, 4 * lane)]);
+    const f16x4 lo = *reinterpret_cast<const f16x4 *>(&sTl[tix(rr, 4 * lane)]);
+    const float us = ldexpf(1.0f, -sSh[rr]);
+    f32x4 x;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) v[q] = sT[rr * kStripLd + 4 * lane + q];
-    *reinterpret_cast<f32x4 *>(G + (size_t)r * ld + K0 + 4 * lane) = v;
-    const int sh = shb[r];
-    f16x4 hi, lo;
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const float x = ldexpf(v[q], sh);
-      hi[q] = (f16)x;
-      lo[q] = (f16)(x - (float)hi[q]);
-    }
+    for (int q = 0; q < 4; ++q) x[q] = ((float)hi[q] + (float)lo[q]) * us;
+    *reinterpret_cast<f32x4 *>(G + (size_t)r * ld + K0 + 4 * lane) = x;
     *reinterpret_cast<f16x4 *>(hib + (size_t)r * ld + K0 + 4 * lane) = hi;
     *reinterpret_cast<f16x4 *>(lob + (size_t)r * ld + K0 + 4 * lane) = lo;
   }
@@ -1669,8 +1727,8 @@ hipError_t launch_cholesky_factor(float *Gw, const float *Gc, int B, int t, int6
   float *sinv = reinterpret_cast<float *>(shift + (size_t)B * ld);
   hipLaunchKernelGGL(k_chol_scales, dim3((unsigned)((ld + 255) / 256), B), dim3(256), 0, s, Gw, ld, shift, sinv,
                      st.info);
-  const hipError_t ea = hipFuncSetAttribute((const void *)k_chol_strip, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                            (int)kStripLds);
+  const hipError_t ea = hipFuncSetAttribute((const void *)k_chol_strip16, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                            (int)kStrip16Lds);
   if (ea != hipSuccess) return ea;
   for (int K0 = 0; K0 < ld; K0 += kOuter) {
     const int K1 = (int)(K0 + kOuter < ld ? K0 + kOuter : ld);
@@ -1704,8 +1762,8 @@ hipError_t launch_cholesky_factor(float *Gw, const float *Gc, int B, int t, int6
     }
     // the rows below: all four steps, written back once, with their planes
     if (K1 < ld)
-      hipLaunchKernelGGL(k_chol_strip, dim3((unsigned)((ld - K1) / kStripRows), B), dim3(512), kStripLds, s, Gw, ld,
-                         K0, dinv, Lp, shift, st.info);
+      hipLaunchKernelGGL(k_chol_strip16, dim3((unsigned)((ld - K1) / kStripRows), B), dim3(512), kStrip16Lds, s, Gw,
+                         ld, K0, dinv, Lp, shift, st.info);
   }
   (void)Gc;
   (void)delta0;
