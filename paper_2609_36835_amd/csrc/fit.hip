@@ -671,10 +671,30 @@ k_chol_strip16(float *__restrict__ Gw, int64_t ld, int K0, const float *__restri
       *reinterpret_cast<f16x4 *>(&sTl[tix(r, c4)]) = lo;
     }
   }
+  // block kb (final after its panel step): planes and L = (hi + lo) / s_r of
+  // all 128 rows, four columns per thread-group, issued while later steps run
+  f16 *hib = Lp + (size_t)b * 2 * ld * ld, *lob = hib + (size_t)ld * ld;
+  auto write_block = [&](int kb) {
+#pragma unroll
+    for (int q = 0; q < kStripRows * 16 / 512; ++q) {
+      const int g = tid + 512 * q, rr = g >> 4, c = 64 * kb + (g & 15) * 4;
+      const int64_t r = R + rr;
+      const f16x4 hi = *reinterpret_cast<const f16x4 *>(&sTh[tix(rr, c)]);
+      const f16x4 lo = *reinterpret_cast<const f16x4 *>(&sTl[tix(rr, c)]);
+      const float us = ldexpf(1.0f, -sSh[rr]);
+      f32x4 x;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) x[u] = ((float)hi[u] + (float)lo[u]) * us;
+      *reinterpret_cast<f32x4 *>(G + (size_t)r * ld + K0 + c) = x;
+      *reinterpret_cast<f16x4 *>(hib + (size_t)r * ld + K0 + c) = hi;
+      *reinterpret_cast<f16x4 *>(lob + (size_t)r * ld + K0 + c) = lo;
+    }
+  };
 #pragma unroll
   for (int st = 0; st < kSteps; ++st) {
     const int k = step_k[st], j = step_j[st];
     __syncthreads();   // the strip is up to date and every wave is done with sB
+    if (st > 0 && step_j[st - 1] == step_k[st - 1]) write_block(step_k[st - 1]);
     stash_b(k, j == k);
     if (st + 1 < kSteps) load_b(st + 1);
     __syncthreads();
@@ -703,24 +723,7 @@ k_chol_strip16(float *__restrict__ Gw, int64_t ld, int K0, const float *__restri
     }
   }
   __syncthreads();
-  // write the rows' planes and L = (hi + lo) 2^-shift: each wave takes 16 rows,
-  // four columns per lane
-  constexpr int kRowsPerWave = kStripRows / 8;
-  f16 *hib = Lp + (size_t)b * 2 * ld * ld, *lob = hib + (size_t)ld * ld;
-#pragma unroll 4
-  for (int i = 0; i < kRowsPerWave; ++i) {
-    const int rr = wave + 8 * i;
-    const int64_t r = R + rr;
-    const f16x4 hi = *reinterpret_cast<const f16x4 *>(&sTh[tix(rr, 4 * lane)]);
-    const f16x4 lo = *reinterpret_cast<const f16x4 *>(&sTl[tix(rr, 4 * lane)]);
-    const float us = ldexpf(1.0f, -sSh[rr]);
-    f32x4 x;
-#pragma unroll
-    for (int q = 0; q < 4; ++q) x[q] = ((float)hi[q] + (float)lo[q]) * us;
-    *reinterpret_cast<f32x4 *>(G + (size_t)r * ld + K0 + 4 * lane) = x;
-    *reinterpret_cast<f16x4 *>(hib + (size_t)r * ld + K0 + 4 * lane) = hi;
-    *reinterpret_cast<f16x4 *>(lob + (size_t)r * ld + K0 + 4 * lane) = lo;
-  }
+  write_block(step_k[kSteps - 1]);   // the last panel step's block
 }
 
 // Per-row shifts of the left-looking updates' operand.  |L_rk| <= sqrt(A_rr)
