@@ -269,6 +269,38 @@ def test_escalated_value_fit_matches_oracle_at_used_ridge():
         assert err <= 1e-3, (b, err)
 
 
+def test_value_fit_tiny_ridge_well_posed():
+    """A full-rank value-fit Gram (t = 600 < n = 1024, three 256-row blocks)
+    with a 1e-12 relative ridge: no escalation, but the a-priori bound
+    ||R_c|| / sqrt(lam) that scales the forward solve's fp16 operand is far
+    above the solution, so the solve must fall back to its fp32 form (or keep
+    enough bits) and still match the float64 fit at that ridge (eq.
+    value_lstsq) to the fp32 bar of 1e-4."""
+    wl = synth.custom("vtiny", kv_heads=2, T=3000, q_heads_per_kv=4, n_pos=256, rho=0.2, dtype="f32", rope=True)
+    dev, host = make_inputs(wl)
+    s = 1.0 / math.sqrt(128)
+    t = oracle.budget(wl.T, wl.rho)
+    assert 512 < t < wl.n
+    refs = [oracle.compact_pair(host["K"][b], host["V"][b], host["Q"][b], host["W1"][b], host["b1"][b],
+                                host["w2"][b], host["b2"][b], t=t, scale=s) for b in range(wl.pairs)]
+    Ck = np.stack([r.C_k for r in refs]).astype(np.float32)
+    beta = np.stack([r.beta for r in refs]).astype(np.float32)
+    Y = np.stack([r.Y for r in refs]).astype(np.float32)
+    params = A().default_params(delta_v=1e-12, max_escalations=0)
+    Cv, info, dused = A().fit_values(dev["Q"], torch.from_numpy(Ck).cuda(), torch.from_numpy(beta).cuda(),
+                                     torch.from_numpy(Y).cuda(), params=params, scale=s, T=wl.T)
+    Cv, info, dused = np64(Cv), info.cpu().numpy(), dused.cpu().numpy()
+    assert np.all(info == 0), info
+    for b in range(wl.pairs):
+        Q = host["Q"][b]
+        vf = oracle.fit_values(Q, Ck[b].astype(np.float64), beta[b].astype(np.float64), Y[b].astype(np.float64), s,
+                               delta=float(dused[b]))
+        err = oracle.row_rel_err(oracle.attend_compact(Q, Ck[b], beta[b], Cv[b], s),
+                                 oracle.attend_compact(Q, Ck[b], beta[b], vf.C_v, s)).max()
+        print(f"  pair {b}: ridge {dused[b]:.1e}; output max row rel err {err:.3e}", flush=True)
+        assert err <= 1e-4, (b, err)
+
+
 def test_exact_fit_degenerate_cases():
     """The exact non-negative fit where the constraints cannot bind: full
     retention (C_k = K, so w = 1 fits the mass exactly: beta = 0) and a single
