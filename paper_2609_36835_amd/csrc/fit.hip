@@ -1737,15 +1737,12 @@ hipError_t launch_cholesky_factor(float *Gw, const float *Gc, int B, int t, int6
     const int K1 = (int)(K0 + kOuter < ld ? K0 + kOuter : ld);
     if (K0 > 0) {
       // A[K0.., K0..K1) -= L[K0.., 0..K0) L[K0..K1, 0..K0)^T: the three products
-      // hi.hi, hi.lo, lo.hi as one contraction over K = 3 x K0 (segments of K0
-      // columns, each reading one plane pair), 256 x 256 tiles down the panel
+      // hi.hi, hi.lo, lo.hi per k-step from both planes of each operand (each
+      // plane is read once), 256 x 256 tiles down the panel
       const f16 *Ar = Lp + (size_t)K0 * ld;
-      BigShape g{B, (int)(ld - K0), kOuter, 3 * K0, 2 * ld * ld, ld * ld, ld, 2 * ld * ld, ld * ld, ld, false, 4};
-      g.kseg = K0;
-      g.sega = 0u | (0u << 2) | (1u << 4);
-      g.segb = 0u | (1u << 2) | (0u << 4);
+      BigShape g{B, (int)(ld - K0), kOuter, K0, 2 * ld * ld, ld * ld, ld, 2 * ld * ld, ld * ld, ld, false, 4};
       EpiCholUpd<2, 4> e{Gw, ld, K0, st.info, sinv + K0, ld};
-      const hipError_t err = launch_gemm_big<4, 2, 2, 4, 64, 1, 1, 2, f16>(
+      const hipError_t err = launch_gemm_big<4, 2, 2, 4, 32, 2, 2, 2, f16>(
           g, reinterpret_cast<const bf16 *>(Ar), reinterpret_cast<const bf16 *>(Ar), e, s);
       if (err != hipSuccess) return err;
     }
@@ -1941,12 +1938,9 @@ hipError_t launch_trsm_fwd_blocked(const float *Gw, const float *dinv, const voi
   for (int kb = 0; kb < nblk; ++kb) {
     if (kb > 0) {
       const int K0 = 256 * kb;
-      BigShape g{B, 256, kHeadDim, 3 * K0, 2 * ld * ld, ld * ld, ld, 2 * kHeadDim * ld, kHeadDim * ld, ld, false, 1};
-      g.kseg = K0;
-      g.sega = 0u | (0u << 2) | (1u << 4);
-      g.segb = 0u | (1u << 2) | (0u << 4);
+      BigShape g{B, 256, kHeadDim, K0, 2 * ld * ld, ld * ld, ld, 2 * kHeadDim * ld, kHeadDim * ld, ld, false, 1};
       EpiTrsmFwd<2, 2> e{R, Y, ld, K0, sinv, ex, info, flag};
-      const hipError_t err = launch_gemm_big<4, 2, 2, 2, 64, 1, 1, 3, f16>(
+      const hipError_t err = launch_gemm_big<4, 2, 2, 2, 32, 2, 2, 3, f16>(
           g, reinterpret_cast<const bf16 *>(Lp + (size_t)K0 * ld), reinterpret_cast<const bf16 *>(Yt), e, s);
       if (err != hipSuccess) return err;
     }
