@@ -229,11 +229,13 @@ __global__ void __launch_bounds__(256) k_prof_anchor_f32(const float *__restrict
 
 // The contraction's anchor operand U [P][tp][np]: Ua / anorm, stored in fp16
 // scaled by 2^15 for bf16 inputs (one rounding of the fp32 product) or in
-// fp32; rows r >= t and columns i >= n are zero.  One wave per row.
+// fp32; rows r >= t and columns i >= n are zero.  One wave per row, four
+// consecutive columns per lane (np_ is a multiple of 256).
 template <typename T>
 __global__ void __launch_bounds__(256) k_anchor_u(const float *__restrict__ Ua, const double *__restrict__ anorm,
                                                   int n, int t, int64_t tp, int64_t np_, float uscale,
                                                   T *__restrict__ U) {
+  typedef __attribute__((__vector_size__(4 * sizeof(T)))) T T4;
   const int b = blockIdx.y, lane = threadIdx.x & 63;
   const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (r >= tp) return;
@@ -241,7 +243,14 @@ __global__ void __launch_bounds__(256) k_anchor_u(const float *__restrict__ Ua, 
   const float *arow = Ua + ((size_t)b * tp + r) * np_;
   const double nr = r < t ? anorm[(size_t)b * tp + r] : 0.0;
   const float inv = nr > 0.0 ? (float)((double)uscale / nr) : 0.0f;
-  for (int64_t i = lane; i < np_; i += 64) urow[i] = (T)(r < t && i < n ? arow[i] * inv : 0.0f);
+  for (int64_t i = 4 * lane; i < np_; i += 256) {
+    f32x4 a = {0.0f, 0.0f, 0.0f, 0.0f};
+    if (r < t && i < n) a = *reinterpret_cast<const f32x4 *>(arow + i);
+    T4 o;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) o[e] = (T)(i + e < n ? a[e] * inv : 0.0f);
+    *reinterpret_cast<T4 *>(urow + i) = o;
+  }
 }
 
 // ---------------------------------------------------------------- pass A bounds

@@ -234,42 +234,46 @@ __global__ void __launch_bounds__(512, 1) k_rowstats_bf16(const bf16 *__restrict
   for (int cs = 0; cs < 4; ++cs) accY[cs] = zero16();
 
   const int nt = (Tn + kRsK - 1) / kRsK;
-  issue_k(0, 0);
-  load_v(0);
-  store_vt(0);
-  __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
-  for (int i = 0; i < nt; ++i) {
-    const int k0 = i * kRsK, st = i & 1;
-    const bool more = i + 1 < nt;
-    if (more) {
-      issue_k(k0 + kRsK, st ^ 1);
-      load_v(k0 + kRsK);
-    }
-    const char *sk = sbuf + st * kRsStage, *svt = sk + kRsKBytes;
-    f32x16 accS[2];
+  // S = K Q^T for the 64 keys in the K part of LDS stage st
+  auto scores = [&](int st, f32x16 (&S)[2]) {
+    const char *sk = sbuf + st * kRsStage;
 #pragma unroll
     for (int ms = 0; ms < 2; ++ms) {
-      accS[ms] = zero16();
+      S[ms] = zero16();
       const int row = 32 * ms + col;
 #pragma unroll
       for (int ks = 0; ks < kHeadDim / 16; ++ks) {
         const bf16x8 a = *reinterpret_cast<const bf16x8 *>(sk + row * 256 + 16 * ((2 * ks + h) ^ (row & 15)));
-        accS[ms] = Mfma<bf16>::mma(a, qf[ks], accS[ms]);
+        S[ms] = Mfma<bf16>::mma(a, qf[ks], S[ms]);
       }
+    }
+  };
+  // Tile i: the online softmax of its scores S and Y^T += V^T P^T from the V
+  // part of stage i & 1.  The scores of tile i + 1 (K part of stage (i + 1) & 1)
+  // go to Sn in the same basic block as the exponentials, so the matrix cores
+  // work on them while the VALUs run the softmax (in the last tile they read a
+  // stale stage and are discarded).  Keys therefore run one tile ahead of
+  // values: on entry stage (i + 1) & 1 holds K tile i + 1 and stage i & 1
+  // holds V^T tile i; V tile i + 1 is in registers.
+  auto body = [&](int i, f32x16 (&S)[2], f32x16 (&Sn)[2]) {
+    const int k0 = i * kRsK, st = i & 1;
+    if (i + 1 < nt) store_vt(st ^ 1);
+    if (i + 2 < nt) {   // stage st: its K tile was read in tile i - 1, before the last barrier
+      issue_k(k0 + 2 * kRsK, st);
+      load_v(k0 + 2 * kRsK);
     }
     if (k0 + kRsK > Tn) {   // last tile: keys past Tn get no weight
 #pragma unroll
       for (int ms = 0; ms < 2; ++ms)
 #pragma unroll
         for (int v = 0; v < 16; ++v)
-          if (k0 + 32 * ms + acc_row(v, lane) >= Tn) accS[ms][v] = -INFINITY;
+          if (k0 + 32 * ms + acc_row(v, lane) >= Tn) S[ms][v] = -INFINITY;
     }
     float bmax = -INFINITY;
 #pragma unroll
     for (int ms = 0; ms < 2; ++ms)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) bmax = fmaxf(bmax, accS[ms][v]);
+      for (int v = 0; v < 16; ++v) bmax = fmaxf(bmax, S[ms][v]);
     bmax = fmaxf(bmax, __shfl_xor(bmax, 32, 64));
     const float new_max = fmaxf(run_max, bmax);
     // The accumulators are rescaled only when some row's maximum grew (rare
@@ -285,24 +289,26 @@ __global__ void __launch_bounds__(512, 1) k_rowstats_bf16(const bf16 *__restrict
         for (int v = 0; v < 16; ++v) accY[cs][v] *= alpha;
     }
     run_max = new_max;
+    scores(st ^ 1, Sn);
     const float mc2 = new_max * c2;
     float psum = 0.0f;
 #pragma unroll
     for (int ms = 0; ms < 2; ++ms)
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
-        const float p = __builtin_amdgcn_exp2f(fmaf(accS[ms][v], c2, -mc2));
-        accS[ms][v] = p;
+        const float p = __builtin_amdgcn_exp2f(fmaf(S[ms][v], c2, -mc2));
+        S[ms][v] = p;
         psum += p;
       }
     run_sum += psum;
+    const char *svt = sbuf + st * kRsStage + kRsKBytes;
 #pragma unroll
     for (int kk = 0; kk < kRsK / 16; ++kk) {
       const int ms = kk >> 1, base = 8 * (kk & 1);
       uint32_t pk[4];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const bf16x2 x = {(bf16)accS[ms][base + 2 * e], (bf16)accS[ms][base + 2 * e + 1]};
+        const bf16x2 x = {(bf16)S[ms][base + 2 * e], (bf16)S[ms][base + 2 * e + 1]};
         pk[e] = __builtin_bit_cast(uint32_t, x);
       }
       // pk[0..1]: own keys 4h + 0..3, pk[2..3]: own keys 8 + 4h + 0..3 (of this
@@ -325,10 +331,26 @@ __global__ void __launch_bounds__(512, 1) k_rowstats_bf16(const bf16 *__restrict
         accY[cs] = Mfma<bf16>::mma(vf, pf, accY[cs]);
       }
     }
-    if (more) store_vt(st ^ 1);
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
+  };
+
+  issue_k(0, 0);
+  if (nt > 1) issue_k(kRsK, 1);
+  load_v(0);
+  __builtin_amdgcn_s_waitcnt(0);
+  store_vt(0);
+  if (nt > 1) load_v(kRsK);
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  f32x16 Sa[2], Sb[2];
+  scores(0, Sa);
+  int i = 0;
+  for (; i + 1 < nt; i += 2) {
+    body(i, Sa, Sb);
+    body(i + 1, Sb, Sa);
   }
+  if (i < nt) body(i, Sa, Sb);
   run_sum += __shfl_xor(run_sum, 32, 64);
   if (!qvalid) return;
   const float inv = 1.0f / run_sum;
