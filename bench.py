@@ -23,7 +23,7 @@ sys.path.insert(0, ROOT)
 import synth  # noqa: E402
 
 HEADLINE = "llama8b_bf16_T32768"
-PEAK_BF16_TFLOPS = 2500.0        # MI355X dense bf16 MFMA
+PEAK_BF16_TFLOPS = 2500.0        # MI355X dense bf16 / fp16 MFMA
 PEAK_FP32_TFLOPS = 157.3
 
 
@@ -184,6 +184,8 @@ def stage_rooflines(wl, t, stages, steps, refine_steps=2, bias_mode=0, value_ref
     event-timed duration per step.  Where the implementation issues more than that, `issued_*` / `issued_frac`
     report what it runs:
       - the Grams and the value right-hand side on split bf16 operands issue three bf16 products per term;
+      - the Cholesky factorisations run their bulk (the left-looking updates and the strip below each diagonal
+        block) on split fp16 planes of L, three fp16 products per term, so they are priced at the fp16 peak;
       - the two solves include `refine_steps` (mass fit) and `value_refine_steps` refinement steps against the
         data (each a residual and another solve), which the method itself does not need: its solve is one forward and one backward triangular
         sweep (mass fit: L read twice, 4 t^2 bytes per pair; value fit: 2 t^2 d flops per pair);
@@ -204,13 +206,13 @@ def stage_rooflines(wl, t, stages, steps, refine_steps=2, bias_mode=0, value_ref
         "merge": ("byte", (T * d * esz + 8 * T + 2 * t * d * 4) * B, PEAK_HBM_GBS, None),
         "phic": ("flop", 2.0 * n * t * d * B, PEAK_BF16_TFLOPS, None),
         "gram_G": ("flop", 1.0 * n * t * (t + 1) * B, PEAK_BF16_TFLOPS, split * n * t * (t + 1) * B),
-        "chol_G": ("flop", t ** 3 / 3.0 * B, PEAK_FP32_TFLOPS, None),
+        "chol_G": ("flop", t ** 3 / 3.0 * B, PEAK_BF16_TFLOPS, 3.0 * t ** 3 / 3.0 * B),
         "solve_beta": ("byte", 4.0 * t * t * B, PEAK_HBM_GBS,
                        ((r + 1) * 4.0 * t * t + r * 2 * 4.0 * t * n) * B),
         "phat": ("byte", (2 * 4.0 * t * n + 4 * 2.0 * t * n) * B, PEAK_HBM_GBS, None),
         "gram_A": ("flop", 1.0 * n * t * (t + 1) * B, PEAK_BF16_TFLOPS, split * n * t * (t + 1) * B),
         "rhs_B": ("flop", 2.0 * n * t * d * B, PEAK_BF16_TFLOPS, split * 2.0 * n * t * d * B),
-        "chol_A": ("flop", t ** 3 / 3.0 * B, PEAK_FP32_TFLOPS, None),
+        "chol_A": ("flop", t ** 3 / 3.0 * B, PEAK_BF16_TFLOPS, 3.0 * t ** 3 / 3.0 * B),
         "solve_values": ("flop", 2.0 * t * t * d * B, PEAK_FP32_TFLOPS,
                          ((rv + 1) * 2.0 * t * t * d + rv * 2 * 2.0 * n * t * d) * B),
     }
