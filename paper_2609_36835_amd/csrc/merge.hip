@@ -22,28 +22,39 @@ __global__ void __launch_bounds__(256) k_zmax(const float *__restrict__ z, int n
   if (tid == 0) zmax[b] = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
 }
 
-// One wave per pair.  Produces offsets [t+1] and perm [T] (positions grouped by
-// kappa, ascending position within each group).  cursor [t] is scratch.
-__global__ void __launch_bounds__(64) k_group_sort(const int32_t *__restrict__ kappa, int T, int t,
-                                                   int32_t *__restrict__ offsets, int32_t *__restrict__ cursor,
-                                                   int32_t *__restrict__ perm) {
-  const int b = blockIdx.x, lane = threadIdx.x;
+// Groups whose cursors fit in LDS (64 KB) take the LDS variant.
+constexpr int kSortLdsGroups = 16384;
+
+// One workgroup per pair.  Produces offsets [t+1] and perm [T] (positions
+// grouped by kappa, ascending position within each group).  The cursors live
+// in LDS (kLds, t <= kSortLdsGroups) or in cursor [B][t] (global scratch).
+// Four waves clear and count; wave 0 alone scans and places, one 64-position
+// chunk at a time in order, which keeps every group in ascending position.
+template <bool kLds>
+__global__ void __launch_bounds__(256) k_group_sort(const int32_t *__restrict__ kappa, int T, int t,
+                                                    int32_t *__restrict__ offsets, int32_t *__restrict__ cursor,
+                                                    int32_t *__restrict__ perm) {
+  __shared__ int32_t lcur[kLds ? kSortLdsGroups : 1];
+  const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63;
   const int32_t *kp = kappa + (size_t)b * T;
   int32_t *off = offsets + (size_t)b * (t + 1);
-  int32_t *cur = cursor + (size_t)b * t;
+  int32_t *cur = kLds ? lcur : cursor + (size_t)b * t;
   int32_t *pm = perm + (size_t)b * T;
   // every access to cur[] is an atomic, fenced between phases
-  for (int r = lane; r < t; r += 64) atomicExch(&cur[r], 0);
-  __threadfence();
-  for (int j = lane; j < T; j += 64) atomicAdd(&cur[kp[j]], 1);
-  __threadfence();
+  for (int r = tid; r < t; r += 256) atomicExch(&cur[r], 0);
+  if (!kLds) __threadfence();
+  __syncthreads();
+  for (int j = tid; j < T; j += 256) atomicAdd(&cur[kp[j]], 1);
+  if (!kLds) __threadfence();
+  __syncthreads();
+  if (tid >= 64) return;
   // exclusive scan of the counts
   int32_t carry = 0;
   for (int r0 = 0; r0 < t; r0 += 64) {
     const int r = r0 + lane;
     int32_t c = r < t ? atomicAdd(&cur[r], 0) : 0;
     int32_t x = c;
-    #pragma unroll
+#pragma unroll
     for (int d = 1; d < 64; d <<= 1) {
       int32_t y = __shfl_up(x, d, 64);
       if (lane >= d) x += y;
@@ -55,7 +66,7 @@ __global__ void __launch_bounds__(64) k_group_sort(const int32_t *__restrict__ k
     carry += __shfl(x, 63, 64);
   }
   if (lane == 0) off[t] = carry;
-  __threadfence();
+  if (!kLds) __threadfence();
   int nbits = 1;
   while ((1 << nbits) < t) ++nbits;
   const uint64_t lanemask = lane == 0 ? 0ull : (~0ull >> (64 - lane));
@@ -179,7 +190,10 @@ hipError_t launch_group_merge(int dtype, const void *K, const float *phi, const 
                               const int32_t *anchors, int B, int T, int t, int64_t tp, float lambda,
                               int32_t *offsets, int32_t *cursor, int32_t *perm, float *Ck, void *Ckp,
                               hipStream_t s) {
-  hipLaunchKernelGGL(k_group_sort, dim3(B), dim3(64), 0, s, kappa, T, t, offsets, cursor, perm);
+  if (t <= kSortLdsGroups)
+    hipLaunchKernelGGL(k_group_sort<true>, dim3(B), dim3(256), 0, s, kappa, T, t, offsets, cursor, perm);
+  else
+    hipLaunchKernelGGL(k_group_sort<false>, dim3(B), dim3(256), 0, s, kappa, T, t, offsets, cursor, perm);
   dim3 grid((unsigned)(tp / 4), B);
   if (dtype == ARCKV_BF16)
     hipLaunchKernelGGL(k_group_merge<bf16>, grid, dim3(256), 0, s, (const bf16 *)K, phi, offsets, perm, anchors, T,

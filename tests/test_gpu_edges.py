@@ -351,3 +351,30 @@ def test_key_tied_with_many_anchors(n_dup_anchors):
     ref, _, _ = oracle.profiles_assign_phi(Q64, K64, S, s)
     ref[dup] = kap[dup]   # checked above against the exact tie rule
     certify_flips(kap, ref, Q64, K64, S, s)
+
+
+@pytest.mark.parametrize("t", [16384, 17000])
+def test_merge_many_groups(t):
+    """The grouping of keys by anchor (a stable counting sort inside arckv_merge)
+    with as many groups as its LDS cursors hold (t = 16384) and more (t = 17000,
+    cursors in global scratch): every anchor keeps itself and the merged keys
+    equal eq. key_merge on the GPU's assignment and mass weights."""
+    rng = np.random.default_rng(t)
+    T, n = 20000, 64
+    s = 1.0 / math.sqrt(128)
+    K = rng.standard_normal((T, 128)).astype(np.float32)
+    V = rng.standard_normal((T, 128)).astype(np.float32)
+    Q = rng.standard_normal((n, 128)).astype(np.float32)
+    S = np.sort(rng.choice(T, t, replace=False))
+    Kb, Vb, Qb = (torch.from_numpy(x).to(torch.bfloat16)[None].cuda().contiguous() for x in (K, V, Q))
+    from paper_2609_36835_amd import arckv
+    z, _, _ = arckv.rowstats(Kb, Vb, Qb, scale=s)
+    Ck, kappa, phi, st = arckv.merge(Kb, Qb, z, torch.from_numpy(S.astype(np.int32))[None].cuda(),
+                                     lambda_m=oracle.LAMBDA_M, scale=s, return_stats=True)
+    kap = kappa[0].cpu().numpy().astype(np.int64)
+    assert np.all(kap[S] == np.arange(t))
+    assert kap.min() >= 0 and kap.max() < t
+    assert st[0].cpu().numpy()[3] == 0
+    K64 = np64(Kb)[0]
+    ref = oracle.merge_keys(K64, np64(phi)[0], kap, S, oracle.LAMBDA_M)
+    np.testing.assert_allclose(np64(Ck)[0], ref, rtol=0, atol=2e-5 * np.abs(K64).max())
