@@ -1134,49 +1134,62 @@ __global__ void __launch_bounds__(256) k_transpose128(const float *__restrict__ 
 
 // --------------------------------------------------------------- 128 right-hand sides
 // 128-rhs triangular solve on fp32 MFMA: L X = R (forward) or L^T X = R
-// (backward), two workgroups per pair with 64 columns each, 64-row blocks.
-// For block kb the update  acc = sum_p L_kb,p X_p  (forward) or
-// sum_p L_p,kb^T X_p  (backward) is an MFMA product with the L tile and the X
-// tile staged in LDS (4 waves = 2 row tiles x 2 column tiles); the block is then
-// X_kb = D (R_kb - acc) with D = L_kb,kb^-1 (forward) or its transpose
-// (backward), the diagonal-block inverses written by the factorisation.
+// (backward), one workgroup per pair (8 waves = 2 row tiles x 4 column tiles
+// of 32), 64-row blocks, so L is read once per solve.  For block kb the
+// update  acc = sum_p L_kb,p X_p  (forward) or  sum_p L_p,kb^T X_p  (backward)
+// is an MFMA product with the L tile and the X tile staged in LDS; the block
+// is then X_kb = D (R_kb - acc) with D = L_kb,kb^-1 (forward) or its
+// transpose (backward), the diagonal-block inverses written by the
+// factorisation.
+constexpr int kTrsmRB = 64, kTrsmSLD = kTrsmRB + 1, kTrsmSXD = kHeadDim + 1;
+constexpr size_t kTrsmLds = (size_t)2 * (kTrsmRB * kTrsmSLD + kTrsmRB * kTrsmSXD) * sizeof(float);
+
 template <bool FWD>
-__global__ void __launch_bounds__(256) k_trsm_mfma(const float *__restrict__ Gw, int64_t ld,
+__global__ void __launch_bounds__(512) k_trsm_mfma(const float *__restrict__ Gw, int64_t ld,
                                                    const float *__restrict__ dinv, const float *__restrict__ R,
                                                    float *__restrict__ X, const int32_t *__restrict__ info) {
-  constexpr int RB = 64, NC = 64, SLD = RB + 1, SXD = NC + 1;
-  __shared__ float sL[2][RB * SLD];
-  __shared__ float sX[2][RB * SXD];
+  constexpr int RB = kTrsmRB, SLD = kTrsmSLD, SXD = kTrsmSXD;
+  extern __shared__ float trsm_smem[];
+  auto sL = [&](int bf) { return trsm_smem + bf * RB * SLD; };
+  auto sX = [&](int bf) { return trsm_smem + 2 * RB * SLD + bf * RB * SXD; };
   const int b = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   if (info[b] != 0) return;
-  const int wr = wave >> 1, wc = wave & 1, h = lane >> 5, col = lane & 31;
-  const int c0 = blockIdx.x * NC;
+  const int wr = wave >> 2, wc = wave & 3, h = lane >> 5, col = lane & 31;
   const float *L = Gw + (size_t)b * ld * ld;
   const float *Rb = R + (size_t)b * ld * kHeadDim;
   float *Xb = X + (size_t)b * ld * kHeadDim;
   const int nb = (int)(ld / RB);
   const float *Db = dinv + (size_t)b * nb * RB * RB;
-  f32x4 rl[4], rx[4];
+  f32x4 rl[2], rx[4];
   // tile (i, k) of the operand: forward L[r0+i][p0+k], backward L[p0+k][r0+i]
   auto fetch = [&](int r0, int p0) {
 #pragma unroll
-    for (int c = 0; c < 4; ++c) {
-      const int e = tid + 256 * c, i = e / 16, k4 = (e % 16) * 4;
+    for (int c = 0; c < 2; ++c) {
+      const int e = tid + 512 * c, i = e / 16, k4 = (e % 16) * 4;
       rl[c] = FWD ? *reinterpret_cast<const f32x4 *>(L + (size_t)(r0 + i) * ld + p0 + k4)
                   : *reinterpret_cast<const f32x4 *>(L + (size_t)(p0 + i) * ld + r0 + k4);
-      rx[c] = *reinterpret_cast<const f32x4 *>(Xb + (size_t)(p0 + i) * kHeadDim + c0 + k4);
+    }
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const int e = tid + 512 * c, i = e / 32, k4 = (e % 32) * 4;
+      rx[c] = *reinterpret_cast<const f32x4 *>(Xb + (size_t)(p0 + i) * kHeadDim + k4);
     }
   };
   auto stash = [&](int bf) {
 #pragma unroll
-    for (int c = 0; c < 4; ++c) {
-      const int e = tid + 256 * c, i = e / 16, k4 = (e % 16) * 4;
+    for (int c = 0; c < 2; ++c) {
+      const int e = tid + 512 * c, i = e / 16, k4 = (e % 16) * 4;
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        if (FWD) sL[bf][i * SLD + k4 + q] = rl[c][q];
-        else sL[bf][(k4 + q) * SLD + i] = rl[c][q];
-        sX[bf][i * SXD + k4 + q] = rx[c][q];
+        if (FWD) sL(bf)[i * SLD + k4 + q] = rl[c][q];
+        else sL(bf)[(k4 + q) * SLD + i] = rl[c][q];
       }
+    }
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const int e = tid + 512 * c, i = e / 32, k4 = (e % 32) * 4;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) sX(bf)[i * SXD + k4 + q] = rx[c][q];
     }
   };
   for (int step = 0; step < nb; ++step) {
@@ -1196,39 +1209,39 @@ __global__ void __launch_bounds__(256) k_trsm_mfma(const float *__restrict__ Gw,
       if (more) fetch(r0, (pb + 1) * RB);
 #pragma unroll 8
       for (int ks = 0; ks < RB / 2; ++ks)
-        acc = Mfma<float>::mma(sL[bf][(32 * wr + col) * SLD + 2 * ks + h],
-                               sX[bf][(2 * ks + h) * SXD + 32 * wc + col], acc);
+        acc = Mfma<float>::mma(sL(bf)[(32 * wr + col) * SLD + 2 * ks + h],
+                               sX(bf)[(2 * ks + h) * SXD + 32 * wc + col], acc);
       if (more) stash(bf ^ 1);
       __syncthreads();
       bf ^= 1;
     }
     __syncthreads();
-    // right-hand side minus update into sX[0]; D into sL[0] (row r = output row)
+    // right-hand side minus update into sX(0); D into sL(0) (row r = output row)
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
       const int r = 32 * wr + acc_row(v, lane), c = 32 * wc + col;
-      sX[0][r * SXD + c] = Rb[(size_t)(r0 + r) * kHeadDim + c0 + c] - acc[v];
+      sX(0)[r * SXD + c] = Rb[(size_t)(r0 + r) * kHeadDim + c] - acc[v];
     }
     const float *Dk = Db + (size_t)kb * RB * RB;
-    for (int e = tid; e < RB * RB / 4; e += 256) {
+    for (int e = tid; e < RB * RB / 4; e += 512) {
       const int i = e / 16, k4 = (e % 16) * 4;
       const f32x4 v = *reinterpret_cast<const f32x4 *>(Dk + i * RB + k4);
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        if (FWD) sL[0][i * SLD + k4 + q] = v[q];
-        else sL[0][(k4 + q) * SLD + i] = v[q];
+        if (FWD) sL(0)[i * SLD + k4 + q] = v[q];
+        else sL(0)[(k4 + q) * SLD + i] = v[q];
       }
     }
     __syncthreads();
     f32x16 out = zero16();
 #pragma unroll 8
     for (int ks = 0; ks < RB / 2; ++ks)
-      out = Mfma<float>::mma(sL[0][(32 * wr + col) * SLD + 2 * ks + h], sX[0][(2 * ks + h) * SXD + 32 * wc + col],
+      out = Mfma<float>::mma(sL(0)[(32 * wr + col) * SLD + 2 * ks + h], sX(0)[(2 * ks + h) * SXD + 32 * wc + col],
                              out);
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
       const int r = 32 * wr + acc_row(v, lane), c = 32 * wc + col;
-      Xb[(size_t)(r0 + r) * kHeadDim + c0 + c] = out[v];
+      Xb[(size_t)(r0 + r) * kHeadDim + c] = out[v];
     }
     __threadfence_block();
   }
@@ -1911,11 +1924,14 @@ hipError_t launch_transpose128(int dtype, const float *in, int B, int rows, int6
 
 hipError_t launch_trsm(bool fwd, const float *Gw, const float *dinv, int B, int64_t ld, const float *R, float *X,
                        const int32_t *info, hipStream_t s) {
-  dim3 grid(kHeadDim / 64, B);
+  const void *kern = fwd ? (const void *)k_trsm_mfma<true> : (const void *)k_trsm_mfma<false>;
+  const hipError_t e = hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kTrsmLds);
+  if (e != hipSuccess) return e;
+  dim3 grid(1, B);
   if (fwd)
-    hipLaunchKernelGGL(k_trsm_mfma<true>, grid, dim3(256), 0, s, Gw, ld, dinv, R, X, info);
+    hipLaunchKernelGGL(k_trsm_mfma<true>, grid, dim3(512), kTrsmLds, s, Gw, ld, dinv, R, X, info);
   else
-    hipLaunchKernelGGL(k_trsm_mfma<false>, grid, dim3(256), 0, s, Gw, ld, dinv, R, X, info);
+    hipLaunchKernelGGL(k_trsm_mfma<false>, grid, dim3(512), kTrsmLds, s, Gw, ld, dinv, R, X, info);
   return hipGetLastError();
 }
 
